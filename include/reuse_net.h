@@ -1,0 +1,198 @@
+/*
+ * reuse_net — frame-to-frame convolutional activation reuse on MI355X (gfx950).
+ *
+ * The method (Abstract; Sec. 1): keep each conv layer's activations from the
+ * previous frame, find which input pixels changed, and recompute only the
+ * outputs those changes can reach, reusing the cached activations everywhere
+ * else.  A k x k convolution spreads a change by (k-1)/2 pixels on each side
+ * per layer (Fig. 1 caption).  Instead of the paper's single rectangle per
+ * frame, changes are tracked as small dirty tiles (the local-area variant of
+ * Sec. 3), and many independent streams (environments, cameras, occlusion
+ * variants) are processed per launch.
+ *
+ * Network: n_conv 3x3 stride-1 pad-1 conv layers, each followed by bias and
+ * ReLU, then a dense layer to n_out logits (Sec. 2: two conv layers and a
+ * dense layer).  The dense input is the last conv output flattened in
+ * (channel, row, column) order, as torch's NCHW .flatten(1).
+ *
+ * Conventions
+ *   - Every function returns an rn_status (0 = RN_OK, negative = error) unless
+ *     stated otherwise; on an argument error nothing is changed and
+ *     reuse_net_last_error() describes the failure.  No function aborts.
+ *   - "dev_" pointers are device memory owned by the caller.  The library
+ *     never allocates or frees device memory: all of its device state lives in
+ *     the caller's workspace, which must outlive the net.
+ *   - hip_stream is a hipStream_t passed as void* (NULL = the null stream).
+ *     reuse_net_step and reuse_net_full only enqueue kernels on it and return;
+ *     launch failures return RN_EHIP, device faults surface at the caller's
+ *     next synchronisation.  No host synchronisation happens inside them.
+ *   - Introspection calls (get_*, read_activation) synchronise the stream of
+ *     the last step and copy into caller host buffers.
+ *   - A net is not thread-safe; calls on one net must not overlap.
+ */
+#ifndef REUSE_NET_H
+#define REUSE_NET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RN_MAX_CONV 8
+
+typedef enum {
+    RN_OK = 0,
+    RN_EINVAL = -1,        /* bad argument or null pointer */
+    RN_EUNSUPPORTED = -2,  /* valid request this build does not implement */
+    RN_ENOSPACE = -3,      /* workspace or caller buffer too small */
+    RN_EHIP = -4,          /* a HIP runtime call failed */
+    RN_ESTATE = -5         /* call not valid in the net's current state */
+} rn_status;
+
+typedef enum { RN_F32 = 0, RN_BF16 = 1, RN_U8 = 2 } rn_dtype;
+
+/* One conv layer (OIHW weights).  Supported: k = 3, stride = 1, pad = 1. */
+typedef struct {
+    int32_t cin, cout, k, stride, pad;
+} rn_conv_spec;
+
+typedef struct {
+    int32_t in_c, in_h, in_w;     /* channels, rows, columns of one frame */
+    int32_t stack;                /* 1, or 4: the last 4 frames are conv1's input channels,
+                                     oldest first (Sec. 1 and Sec. 3: multiple input frames);
+                                     conv[0].cin must equal in_c * stack */
+    int32_t n_conv;               /* 1..RN_MAX_CONV */
+    const rn_conv_spec *conv;     /* host array [n_conv], read during create only */
+    int32_t n_out;                /* logits per stream, 1..64 */
+    int32_t tile_h, tile_w;       /* dirty-tile grid cell on every layer; supported: 4 x 4 */
+    int32_t max_streams;          /* cache slots, 1..65535 */
+    rn_dtype act_dtype;           /* RN_F32, or RN_BF16 (bf16 weights and activations,
+                                     fp32 accumulation, fp32 logits) */
+} rn_config;
+
+typedef struct {                  /* HOST pointers, float32, read during create only */
+    const float *const *conv_w;   /* [n_conv], each [cout][cin][k][k] (OIHW) */
+    const float *const *conv_b;   /* [n_conv], each [cout] */
+    const float *dense_w;         /* [n_out][C_L * H * W], (c, y, x) flatten order */
+    const float *dense_b;         /* [n_out] */
+} rn_weights;
+
+typedef struct reuse_net reuse_net;   /* opaque host object owned by the library */
+
+/* Bytes of device workspace a net with this config needs (0 if the config is
+ * invalid or unsupported). */
+size_t reuse_net_workspace_bytes(const rn_config *cfg);
+
+/* Validate cfg, lay out the caller's workspace (dev_workspace, >= the size
+ * above, 256-byte aligned), pack the weights into the kernels' layouts and
+ * upload them on hip_stream, clear every cache and mark every slot unprimed.
+ * Synchronises hip_stream before returning.  *out receives the net. */
+rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_workspace,
+                           size_t workspace_bytes, void *hip_stream, reuse_net **out);
+
+/* One reuse step (Abstract; Sec. 1) for n streams.
+ *   dev_stream_ids: [n] distinct cache slots in [0, max_streams), or NULL for 0..n-1.
+ *   dev_frames:     [n][in_c][in_h][in_w], RN_F32 values, or RN_U8 levels k read as
+ *                   k / 255 (correctly rounded float32).  With stack = 4 this is the
+ *                   newest frame only; the library keeps the older three.
+ *   dev_boxes, dev_box_off: NULL for change detection by diff.  Otherwise the
+ *                   caller states the change (Sec. 1, known-change use such as
+ *                   occlusion): boxes [nb][4] int32 (y0, x0, y1, x1), half-open, clipped
+ *                   to the frame; stream i owns boxes [box_off[i], box_off[i+1]);
+ *                   box_off has n+1 entries and box_off[0] = 0.  Only pixels inside
+ *                   the boxes are read from dev_frames.
+ *   dev_logits:     [n][n_out] float32 output.
+ * Change rule: a pixel changed iff the float32 bits of some channel differ from
+ * the cached input (so -0 vs +0 is a change and an identical NaN is not).  A
+ * slot that was never primed, or was reset, is treated as all-changed.
+ * Enqueues diff (or boxes) -> dilation and tile masks -> work-list compaction ->
+ * dirty-tile conv per layer (bias, ReLU and scatter into the caches fused) ->
+ * dense head. */
+rn_status reuse_net_step(reuse_net *net, int32_t n, const int32_t *dev_stream_ids,
+                         const void *dev_frames, rn_dtype frame_dtype,
+                         const int32_t *dev_boxes, const int32_t *dev_box_off,
+                         float *dev_logits, void *hip_stream);
+
+/* Dense recompute of every layer for n streams (the comparison path): as a
+ * step on which every pixel changed.  Leaves the slots primed. */
+rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *dev_stream_ids,
+                         const void *dev_frames, rn_dtype frame_dtype, float *dev_logits,
+                         void *hip_stream);
+
+/* Mark one slot (or all, stream_id = -1) unprimed: its next step recomputes
+ * everything.  Synchronises the last step's stream. */
+rn_status reuse_net_reset(reuse_net *net, int32_t stream_id);
+
+/* ---- introspection (synchronous; for parity checks and statistics) ---- */
+
+/* Pixel change mask of a slot after its last step, layer 0 (input) .. n_conv.
+ * Row-major bit rows: word (y * words_per_row + x / 64), bit x % 64, with
+ * words_per_row = ceil(in_w / 64).  words >= in_h * words_per_row. */
+rn_status reuse_net_get_pixel_mask(reuse_net *net, int32_t layer, int32_t stream_id,
+                                   uint64_t *out, size_t words);
+
+/* Dirty-tile mask of a slot after its last step: bit t = ty * TW + tx of word
+ * t / 64, TW = ceil(in_w / tile_w).  words >= ceil(TH * TW / 64). */
+rn_status reuse_net_get_tile_mask(reuse_net *net, int32_t layer, int32_t stream_id,
+                                  uint64_t *out, size_t words);
+
+/* Work list of layer 1..n_conv from the last step or full: the dirty tiles in
+ * ascending (batch index i, ty, tx) order, encoded i << 16 | ty << 8 | tx, where
+ * i indexes that call's stream batch.  *count receives the length; at most
+ * cap entries are copied (RN_ENOSPACE if cap < count, with *count still set). */
+rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, size_t cap,
+                                 int32_t *count);
+
+/* Cached activations of a slot, layer 0 (the float32 input cache, newest frame
+ * for stack = 4) .. n_conv, as float32 [C][H][W] in host memory. */
+rn_status reuse_net_read_activation(reuse_net *net, int32_t stream_id, int32_t layer,
+                                    float *host_out);
+
+typedef struct {
+    int64_t streams;              /* n of the last step */
+    int64_t changed_px;           /* changed input pixels, summed over the streams */
+    int64_t dirty_tiles[RN_MAX_CONV + 1];   /* per layer 0..n_conv */
+    int64_t useful_mac;           /* MACs of in-image pixels of dirty tiles + dense head */
+    int64_t issued_mac;           /* MACs the kernels issued (whole tiles) + dense head */
+    int64_t dense_mac;            /* MACs of a dense recompute of the same streams */
+} rn_stats;
+
+/* Statistics of the last step or full call. */
+rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out);
+
+/* ---- kernel timing with HIP events (measurement support) ---- */
+
+#define RN_PHASES 5
+typedef enum {
+    RN_PHASE_MASKS = 0,   /* diff or boxes, dilation, tile masks */
+    RN_PHASE_COMPACT = 1, /* work-list compaction */
+    RN_PHASE_CONV1 = 2,   /* first conv layer on dirty tiles */
+    RN_PHASE_CONVN = 3,   /* conv layers 2..n_conv on dirty tiles (MFMA) */
+    RN_PHASE_HEAD = 4     /* dense head */
+} rn_phase;
+
+typedef struct {
+    double ms[RN_PHASES];         /* summed event time per phase */
+    int64_t launches[RN_PHASES];  /* kernel launches per phase */
+} rn_profile;
+
+/* enable != 0: bracket every later kernel launch with HIP events on the
+ * launch stream and accumulate; 0 stops.  Either way the totals restart. */
+rn_status reuse_net_set_profiling(reuse_net *net, int32_t enable);
+
+/* Synchronise and return the totals since profiling was enabled. */
+rn_status reuse_net_get_profile(reuse_net *net, rn_profile *out);
+
+/* Text of the last error on this net (never NULL; "" if none).  net may be
+ * NULL for errors of reuse_net_create. */
+const char *reuse_net_last_error(const reuse_net *net);
+
+/* Release the host object.  The caller then owns (and may free) the workspace. */
+void reuse_net_destroy(reuse_net *net);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

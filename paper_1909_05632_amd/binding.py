@@ -1,0 +1,340 @@
+"""ctypes binding of libreuse_net.so (include/reuse_net.h).
+
+The module-level functions carry the C names and only marshal arguments:
+every step of the reuse path runs in the library's HIP kernels.  ``ReuseNet``
+is a convenience wrapper that uses torch for device memory and streams.
+There is no fallback: if the library is not built, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libreuse_net.so")
+
+RN_MAX_CONV = 8
+RN_PHASES = 5
+RN_OK, RN_EINVAL, RN_EUNSUPPORTED, RN_ENOSPACE, RN_EHIP, RN_ESTATE = 0, -1, -2, -3, -4, -5
+RN_F32, RN_BF16, RN_U8 = 0, 1, 2
+PHASES = ("masks", "compact", "conv1", "convN", "head")
+STATUS_NAMES = {0: "RN_OK", -1: "RN_EINVAL", -2: "RN_EUNSUPPORTED", -3: "RN_ENOSPACE",
+                -4: "RN_EHIP", -5: "RN_ESTATE"}
+
+# Every entry point include/reuse_net.h declares.
+EXPORTS = (
+    "reuse_net_workspace_bytes", "reuse_net_create", "reuse_net_step", "reuse_net_full",
+    "reuse_net_reset", "reuse_net_get_pixel_mask", "reuse_net_get_tile_mask",
+    "reuse_net_get_worklist", "reuse_net_read_activation", "reuse_net_get_stats",
+    "reuse_net_set_profiling", "reuse_net_get_profile", "reuse_net_last_error",
+    "reuse_net_destroy",
+)
+
+
+class rn_conv_spec(ctypes.Structure):
+    _fields_ = [("cin", ctypes.c_int32), ("cout", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32)]
+
+
+class rn_config(ctypes.Structure):
+    _fields_ = [("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32), ("in_w", ctypes.c_int32),
+                ("stack", ctypes.c_int32), ("n_conv", ctypes.c_int32),
+                ("conv", ctypes.POINTER(rn_conv_spec)), ("n_out", ctypes.c_int32),
+                ("tile_h", ctypes.c_int32), ("tile_w", ctypes.c_int32),
+                ("max_streams", ctypes.c_int32), ("act_dtype", ctypes.c_int)]
+
+
+class rn_weights(ctypes.Structure):
+    _fields_ = [("conv_w", ctypes.POINTER(ctypes.c_void_p)),
+                ("conv_b", ctypes.POINTER(ctypes.c_void_p)),
+                ("dense_w", ctypes.c_void_p), ("dense_b", ctypes.c_void_p)]
+
+
+class rn_stats(ctypes.Structure):
+    _fields_ = [("streams", ctypes.c_int64), ("changed_px", ctypes.c_int64),
+                ("dirty_tiles", ctypes.c_int64 * (RN_MAX_CONV + 1)),
+                ("useful_mac", ctypes.c_int64), ("issued_mac", ctypes.c_int64),
+                ("dense_mac", ctypes.c_int64)]
+
+
+class rn_profile(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * RN_PHASES), ("launches", ctypes.c_int64 * RN_PHASES)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the HIP library and declare the C signatures.  Raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_1909_05632_amd.build`")
+    L = ctypes.CDLL(path)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    st = ctypes.c_int
+    L.reuse_net_workspace_bytes.restype = SZ
+    L.reuse_net_workspace_bytes.argtypes = [ctypes.POINTER(rn_config)]
+    L.reuse_net_create.restype = st
+    L.reuse_net_create.argtypes = [ctypes.POINTER(rn_config), ctypes.POINTER(rn_weights), P, SZ, P,
+                                   ctypes.POINTER(P)]
+    L.reuse_net_step.restype = st
+    L.reuse_net_step.argtypes = [P, I32, P, P, ctypes.c_int, P, P, P, P]
+    L.reuse_net_full.restype = st
+    L.reuse_net_full.argtypes = [P, I32, P, P, ctypes.c_int, P, P]
+    L.reuse_net_reset.restype = st
+    L.reuse_net_reset.argtypes = [P, I32]
+    for name in ("reuse_net_get_pixel_mask", "reuse_net_get_tile_mask"):
+        getattr(L, name).restype = st
+        getattr(L, name).argtypes = [P, I32, I32, P, SZ]
+    L.reuse_net_get_worklist.restype = st
+    L.reuse_net_get_worklist.argtypes = [P, I32, P, SZ, ctypes.POINTER(I32)]
+    L.reuse_net_read_activation.restype = st
+    L.reuse_net_read_activation.argtypes = [P, I32, I32, P]
+    L.reuse_net_get_stats.restype = st
+    L.reuse_net_get_stats.argtypes = [P, ctypes.POINTER(rn_stats)]
+    L.reuse_net_set_profiling.restype = st
+    L.reuse_net_set_profiling.argtypes = [P, I32]
+    L.reuse_net_get_profile.restype = st
+    L.reuse_net_get_profile.argtypes = [P, ctypes.POINTER(rn_profile)]
+    L.reuse_net_last_error.restype = ctypes.c_char_p
+    L.reuse_net_last_error.argtypes = [P]
+    L.reuse_net_destroy.restype = None
+    L.reuse_net_destroy.argtypes = [P]
+    _lib = L
+    return L
+
+
+class ReuseNetError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _check(status: int, net_handle=None):
+    if status != RN_OK:
+        msg = load_library().reuse_net_last_error(net_handle).decode()
+        raise ReuseNetError(status, msg)
+
+
+# ------------------------------------------------------- C-named wrappers
+
+def reuse_net_workspace_bytes(cfg: rn_config) -> int:
+    return load_library().reuse_net_workspace_bytes(ctypes.byref(cfg))
+
+
+def reuse_net_create(cfg: rn_config, weights: rn_weights, dev_workspace: int, nbytes: int,
+                     hip_stream: int) -> int:
+    h = ctypes.c_void_p()
+    _check(load_library().reuse_net_create(ctypes.byref(cfg), ctypes.byref(weights), dev_workspace,
+                                           nbytes, hip_stream, ctypes.byref(h)))
+    return h.value
+
+
+def reuse_net_step(net: int, n: int, dev_stream_ids: int, dev_frames: int, frame_dtype: int,
+                   dev_boxes: int, dev_box_off: int, dev_logits: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_step(net, n, dev_stream_ids, dev_frames, frame_dtype, dev_boxes,
+                                         dev_box_off, dev_logits, hip_stream), net)
+
+
+def reuse_net_full(net: int, n: int, dev_stream_ids: int, dev_frames: int, frame_dtype: int,
+                   dev_logits: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_full(net, n, dev_stream_ids, dev_frames, frame_dtype,
+                                         dev_logits, hip_stream), net)
+
+
+def reuse_net_reset(net: int, stream_id: int) -> None:
+    _check(load_library().reuse_net_reset(net, stream_id), net)
+
+
+def reuse_net_get_pixel_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
+    out = np.zeros(words, np.uint64)
+    _check(load_library().reuse_net_get_pixel_mask(net, layer, stream_id, out.ctypes.data, words), net)
+    return out
+
+
+def reuse_net_get_tile_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
+    out = np.zeros(words, np.uint64)
+    _check(load_library().reuse_net_get_tile_mask(net, layer, stream_id, out.ctypes.data, words), net)
+    return out
+
+
+def reuse_net_get_worklist(net: int, layer: int, cap: int) -> np.ndarray:
+    out = np.zeros(max(cap, 1), np.uint32)
+    cnt = ctypes.c_int32()
+    _check(load_library().reuse_net_get_worklist(net, layer, out.ctypes.data, cap, ctypes.byref(cnt)), net)
+    return out[:cnt.value].copy()
+
+
+def reuse_net_read_activation(net: int, stream_id: int, layer: int, shape) -> np.ndarray:
+    out = np.zeros(shape, np.float32)
+    _check(load_library().reuse_net_read_activation(net, stream_id, layer, out.ctypes.data), net)
+    return out
+
+
+def reuse_net_get_stats(net: int) -> dict:
+    s = rn_stats()
+    _check(load_library().reuse_net_get_stats(net, ctypes.byref(s)), net)
+    return {"streams": s.streams, "changed_px": s.changed_px, "dirty_tiles": list(s.dirty_tiles),
+            "useful_mac": s.useful_mac, "issued_mac": s.issued_mac, "dense_mac": s.dense_mac}
+
+
+def reuse_net_set_profiling(net: int, enable: bool) -> None:
+    _check(load_library().reuse_net_set_profiling(net, int(enable)), net)
+
+
+def reuse_net_get_profile(net: int) -> dict:
+    p = rn_profile()
+    _check(load_library().reuse_net_get_profile(net, ctypes.byref(p)), net)
+    return {name: {"ms": p.ms[i], "launches": p.launches[i]} for i, name in enumerate(PHASES)}
+
+
+def reuse_net_last_error(net: Optional[int]) -> str:
+    return load_library().reuse_net_last_error(net).decode()
+
+
+def reuse_net_destroy(net: int) -> None:
+    load_library().reuse_net_destroy(net)
+
+
+# ------------------------------------------------------- torch convenience
+
+def _dtype_code(name: str) -> int:
+    return {"f32": RN_F32, "fp32": RN_F32, "float32": RN_F32, "bf16": RN_BF16,
+            "bfloat16": RN_BF16}[name]
+
+
+class ReuseNet:
+    """One reuse net on a CUDA (HIP) device, workspace held in a torch tensor.
+
+    convs: sequence of output channels (3x3, stride 1, pad 1 each).
+    weights: (conv_w list of OIHW float32, conv_b list, dense_w [n_out][C_L*H*W], dense_b).
+    """
+
+    def __init__(self, in_c: int, h: int, w: int, convs: Sequence[int], n_out: int,
+                 max_streams: int, weights, act_dtype: str = "f32", stack: int = 1,
+                 device="cuda", tile: int = 4):
+        import torch
+        self.torch = torch
+        self.device = torch.device(device)
+        self.in_c, self.h, self.w, self.stack = in_c, h, w, stack
+        self.convs = list(convs)
+        self.n_out, self.max_streams = n_out, max_streams
+        specs = []
+        c = in_c * stack
+        for co in self.convs:
+            specs.append((c, co, 3, 1, 1))
+            c = co
+        self.specs = specs
+        self._spec_arr = (rn_conv_spec * len(specs))(*[rn_conv_spec(*s) for s in specs])
+        self.cfg = rn_config(in_c, h, w, stack, len(specs), self._spec_arr, n_out, tile, tile,
+                             max_streams, _dtype_code(act_dtype))
+        nbytes = reuse_net_workspace_bytes(self.cfg)
+        if nbytes == 0:
+            # Re-run create's validation to report why.
+            _check(load_library().reuse_net_create(ctypes.byref(self.cfg), None, None, 0, None,
+                                                   ctypes.byref(ctypes.c_void_p())))
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        conv_w, conv_b, dense_w, dense_b = weights
+        self._host = [np.ascontiguousarray(a, dtype=np.float32) for a in (*conv_w, *conv_b, dense_w, dense_b)]
+        L = len(specs)
+        cw = (ctypes.c_void_p * L)(*[a.ctypes.data for a in self._host[:L]])
+        cb = (ctypes.c_void_p * L)(*[a.ctypes.data for a in self._host[L:2 * L]])
+        wts = rn_weights(cw, cb, self._host[2 * L].ctypes.data, self._host[2 * L + 1].ctypes.data)
+        stream = torch.cuda.current_stream(self.device).cuda_stream
+        self.handle = reuse_net_create(self.cfg, wts, self.workspace.data_ptr(), nbytes, stream)
+        self._host = None
+        self.words_per_row = -(-w // 64)
+        self.tiles = (-(-h // tile), -(-w // tile))
+        self.tile_words = -(-(self.tiles[0] * self.tiles[1]) // 64)
+
+    # -- hot path
+    def _frames(self, frames):
+        t = self.torch
+        if frames.dtype == t.uint8:
+            code = RN_U8
+        elif frames.dtype == t.float32:
+            code = RN_F32
+        else:
+            raise TypeError("frames must be uint8 or float32")
+        if not frames.is_cuda or not frames.is_contiguous():
+            raise ValueError("frames must be a contiguous device tensor")
+        return frames, code
+
+    def step(self, frames, stream_ids=None, boxes=None, box_off=None, out=None, stream=None):
+        t = self.torch
+        frames, code = self._frames(frames)
+        n = frames.shape[0]
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        ids = stream_ids.data_ptr() if stream_ids is not None else None
+        bx = boxes.data_ptr() if boxes is not None else None
+        bo = box_off.data_ptr() if box_off is not None else None
+        reuse_net_step(self.handle, n, ids, frames.data_ptr(), code, bx, bo, out.data_ptr(), s)
+        return out
+
+    def full(self, frames, stream_ids=None, out=None, stream=None):
+        t = self.torch
+        frames, code = self._frames(frames)
+        n = frames.shape[0]
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        ids = stream_ids.data_ptr() if stream_ids is not None else None
+        reuse_net_full(self.handle, n, ids, frames.data_ptr(), code, out.data_ptr(), s)
+        return out
+
+    def reset(self, stream_id: int = -1):
+        reuse_net_reset(self.handle, stream_id)
+
+    # -- introspection
+    def pixel_mask(self, layer: int, stream_id: int) -> np.ndarray:
+        """uint64 [H][words_per_row] bit rows."""
+        words = self.h * self.words_per_row
+        return reuse_net_get_pixel_mask(self.handle, layer, stream_id, words).reshape(
+            self.h, self.words_per_row)
+
+    def pixel_mask_u8(self, layer: int, stream_id: int) -> np.ndarray:
+        """uint8 [H][W], 1 = dirty (unpacked from the bit rows)."""
+        m = self.pixel_mask(layer, stream_id)
+        bits = np.unpackbits(m.view(np.uint8).reshape(self.h, -1), axis=1, bitorder="little")
+        return bits[:, :self.w]
+
+    def tile_mask_u8(self, layer: int, stream_id: int) -> np.ndarray:
+        m = reuse_net_get_tile_mask(self.handle, layer, stream_id, self.tile_words)
+        bits = np.unpackbits(m.view(np.uint8), bitorder="little")
+        th, tw = self.tiles
+        return bits[:th * tw].reshape(th, tw)
+
+    def worklist(self, layer: int, cap: Optional[int] = None) -> np.ndarray:
+        cap = cap if cap is not None else self.max_streams * self.tiles[0] * self.tiles[1]
+        return reuse_net_get_worklist(self.handle, layer, cap)
+
+    def activation(self, stream_id: int, layer: int) -> np.ndarray:
+        c = self.in_c if layer == 0 else self.convs[layer - 1]
+        return reuse_net_read_activation(self.handle, stream_id, layer, (c, self.h, self.w))
+
+    def stats(self) -> dict:
+        return reuse_net_get_stats(self.handle)
+
+    def set_profiling(self, on: bool):
+        reuse_net_set_profiling(self.handle, on)
+
+    def profile(self) -> dict:
+        return reuse_net_get_profile(self.handle)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            reuse_net_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,598 @@
+// Host side of reuse_net: config validation, workspace layout, weight packing,
+// and the per-step launch sequence
+//   masks (diff or boxes, growth, tile masks) -> work lists -> conv layer 1 ->
+//   conv layers 2..L -> dense head,
+// all enqueued on the caller's stream with no host synchronisation.
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "rn_internal.hpp"
+
+using namespace rn;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+struct Plan {
+    int L = 0, H = 0, W = 0, WW = 0, TH = 0, TW = 0, TMW = 0, ntiles = 0;
+    int in_c = 0, stack = 1, S = 0, N = 0;
+    rn_dtype dt = RN_F32;
+    size_t esz = 4;
+    int C[RN_MAX_CONV + 1] = {0};          // channels per layer (0 = conv1 input)
+    int radius[RN_MAX_CONV] = {0};         // change growth per layer, (k - 1) / 2
+    size_t K = 0;                          // head input elements per slot (tiled)
+    int head_sg = 8;
+    size_t part_elems = 0;
+    // byte offsets into the workspace
+    size_t o_lut, o_xin, o_ring, o_dring, o_primed, o_ids, o_act[RN_MAX_CONV + 1], o_w[RN_MAX_CONV],
+        o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile,
+        o_wl[RN_MAX_CONV + 1], o_cnt, o_part;
+    size_t w_elems[RN_MAX_CONV] = {0};
+    size_t act_stride[RN_MAX_CONV + 1] = {0};   // elements per slot
+    size_t total = 0;
+};
+
+void head_split(const Plan &p, int n, int *nsplit, size_t *chunk) {
+    const int groups = ceil_div(n, p.head_sg);
+    const size_t max_split = std::max<size_t>(1, (p.K + 1023) / 1024);
+    size_t ns = std::min<size_t>(max_split, std::max<size_t>(1, (size_t)ceil_div(2048, groups)));
+    size_t ch = (p.K + ns - 1) / ns;
+    ch = (ch + 1023) / 1024 * 1024;
+    *chunk = ch;
+    *nsplit = (int)((p.K + ch - 1) / ch);
+}
+
+rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
+    auto fail = [&](rn_status st, const std::string &m) {
+        *err = m;
+        return st;
+    };
+    if (!cfg) return fail(RN_EINVAL, "config is NULL");
+    if (cfg->n_conv < 1 || cfg->n_conv > RN_MAX_CONV) return fail(RN_EINVAL, "n_conv must be 1..8");
+    if (!cfg->conv) return fail(RN_EINVAL, "conv specs are NULL");
+    if (cfg->in_c < 1 || cfg->in_h < 1 || cfg->in_w < 1) return fail(RN_EINVAL, "bad frame shape");
+    if (cfg->stack != 1 && cfg->stack != 4) return fail(RN_EINVAL, "stack must be 1 or 4");
+    if (cfg->n_out < 1 || cfg->n_out > kHeadMaxOut) return fail(RN_EINVAL, "n_out must be 1..64");
+    if (cfg->max_streams < 1 || cfg->max_streams > 65535) return fail(RN_EINVAL, "max_streams must be 1..65535");
+    if (cfg->act_dtype != RN_F32 && cfg->act_dtype != RN_BF16) return fail(RN_EINVAL, "act_dtype must be F32 or BF16");
+    if (cfg->tile_h < 1 || cfg->tile_w < 1) return fail(RN_EINVAL, "bad tile");
+    int c = cfg->in_c * cfg->stack;
+    for (int l = 0; l < cfg->n_conv; ++l) {
+        const rn_conv_spec &s = cfg->conv[l];
+        if (s.cin != c) return fail(RN_EINVAL, "conv channel chain is inconsistent at layer " + std::to_string(l + 1));
+        if (s.cout < 1 || s.k < 1 || s.stride < 1 || s.pad < 0) return fail(RN_EINVAL, "bad conv spec");
+        if (s.k % 2 == 0 || s.pad != (s.k - 1) / 2) return fail(RN_EINVAL, "conv needs odd k and pad = (k-1)/2");
+        if (s.k != 3 || s.stride != 1) return fail(RN_EUNSUPPORTED, "only 3x3 stride-1 conv layers are implemented");
+        c = s.cout;
+    }
+    if (cfg->tile_h != kTile || cfg->tile_w != kTile) return fail(RN_EUNSUPPORTED, "only 4x4 tiles are implemented");
+    if (cfg->in_w % 4 != 0) return fail(RN_EUNSUPPORTED, "in_w must be a multiple of 4");
+    if (cfg->stack == 4 && cfg->in_c != 1) return fail(RN_EUNSUPPORTED, "stack = 4 needs in_c = 1");
+    if (cfg->act_dtype != RN_F32) return fail(RN_EUNSUPPORTED, "bf16 activations are not implemented yet");
+    p->L = cfg->n_conv;
+    p->H = cfg->in_h;
+    p->W = cfg->in_w;
+    p->WW = ceil_div(p->W, 64);
+    p->TH = ceil_div(p->H, kTile);
+    p->TW = ceil_div(p->W, kTile);
+    if (p->TH > 256 || p->TW > 256) return fail(RN_EUNSUPPORTED, "frames above 1024 x 1024 are not implemented");
+    p->ntiles = p->TH * p->TW;
+    p->TMW = ceil_div(p->ntiles, 64);
+    p->in_c = cfg->in_c;
+    p->stack = cfg->stack;
+    p->S = cfg->max_streams;
+    p->N = cfg->n_out;
+    p->dt = cfg->act_dtype;
+    p->esz = p->dt == RN_F32 ? 4 : 2;
+    p->C[0] = cfg->in_c * cfg->stack;
+    for (int l = 0; l < p->L; ++l) {
+        p->C[l + 1] = cfg->conv[l].cout;
+        p->radius[l] = (cfg->conv[l].k - 1) / 2;
+    }
+    if (!conv_first_supported(p->C[0], p->C[1], p->dt))
+        return fail(RN_EUNSUPPORTED, "no first-layer kernel for " + std::to_string(p->C[0]) + "->" + std::to_string(p->C[1]));
+    for (int l = 2; l <= p->L; ++l)
+        if (!conv_mfma_supported(p->C[l - 1], p->C[l], p->dt))
+            return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" + std::to_string(p->C[l]));
+    p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
+    p->head_sg = head_streams_per_block(p->N);
+    size_t part = 0;
+    for (int n = 1; n <= p->S; ++n) {
+        int ns;
+        size_t ch;
+        head_split(*p, n, &ns, &ch);
+        part = std::max(part, (size_t)ns * n);
+    }
+    p->part_elems = part * p->N;
+
+    const size_t S = p->S, HW = (size_t)p->H * p->W, HWW = (size_t)p->H * p->WW;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + std::max<size_t>(bytes, 1));
+        return o;
+    };
+    p->o_lut = take(256 * 4);
+    p->o_xin = take(S * p->stack * p->in_c * HW * 4);
+    p->o_ring = take(S * 4);
+    p->o_dring = take(p->stack == 4 ? S * 4 * HWW * 8 : 0);
+    p->o_primed = take(S * 4);
+    p->o_ids = take(S * 4);
+    p->act_stride[0] = (size_t)p->stack * p->in_c * HW;
+    for (int l = 1; l <= p->L; ++l) {
+        p->act_stride[l] = (size_t)p->ntiles * kTilePx * p->C[l];
+        p->o_act[l] = take(S * p->act_stride[l] * p->esz);
+    }
+    for (int l = 0; l < p->L; ++l) {
+        p->w_elems[l] = l == 0 ? conv_first_packed_elems(p->C[0], p->C[1])
+                               : conv_mfma_packed_elems(p->C[l], p->C[l + 1], p->dt);
+        p->o_w[l] = take(p->w_elems[l] * 4);
+        p->o_b[l] = take((size_t)p->C[l + 1] * 4);
+    }
+    p->o_wd = take((size_t)p->N * p->K * p->esz);
+    p->o_bd = take((size_t)p->N * 4);
+    for (int l = 0; l <= p->L; ++l) {
+        p->o_pm[l] = take(S * HWW * 8);
+        p->o_tm[l] = take(S * p->TMW * 8);
+    }
+    p->o_nchg = take(S * 4);
+    p->o_ntile = take(S * (p->L + 1) * 4);
+    for (int l = 1; l <= p->L; ++l) p->o_wl[l] = take(S * p->ntiles * 4);
+    p->o_cnt = take((RN_MAX_CONV + 1) * 4);
+    p->o_part = take(p->part_elems * 4);
+    p->total = off;
+    return RN_OK;
+}
+
+struct ProfRec {
+    int phase;
+    hipEvent_t e0, e1;
+};
+
+}  // namespace
+
+struct reuse_net {
+    Plan p;
+    rn_config cfg;
+    char *ws = nullptr;
+    int cus = 256;
+    hipStream_t last_stream = nullptr;
+    int last_n = 0;
+    bool has_step = false;
+    bool prof = false;
+    std::vector<hipEvent_t> pool;
+    size_t pool_used = 0;
+    std::vector<ProfRec> recs;
+    std::string err;
+
+    template <typename T>
+    T *at(size_t off) const { return reinterpret_cast<T *>(ws + off); }
+
+    rn_status fail(rn_status st, const std::string &m) {
+        err = m;
+        return st;
+    }
+    hipEvent_t next_event() {
+        if (pool_used == pool.size()) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            pool.push_back(e);
+        }
+        return pool[pool_used++];
+    }
+};
+
+namespace {
+
+template <typename F>
+hipError_t timed(reuse_net *net, int phase, hipStream_t s, F &&fn) {
+    if (!net->prof) return fn();
+    hipEvent_t e0 = net->next_event(), e1 = net->next_event();
+    if (!e0 || !e1) return hipErrorOutOfMemory;
+    (void)hipEventRecord(e0, s);
+    hipError_t e = fn();
+    (void)hipEventRecord(e1, s);
+    net->recs.push_back({phase, e0, e1});
+    return e;
+}
+
+rn_status sync_last(reuse_net *net) {
+    if (!net->has_step) return RN_OK;
+    hipError_t e = hipStreamSynchronize(net->last_stream);
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("stream sync: ") + hipGetErrorString(e));
+    return RN_OK;
+}
+
+MaskGeom make_geom(reuse_net *net) {
+    const Plan &p = net->p;
+    MaskGeom g{};
+    g.L = p.L;
+    g.H = p.H;
+    g.W = p.W;
+    g.WW = p.WW;
+    g.TH = p.TH;
+    g.TW = p.TW;
+    g.TMW = p.TMW;
+    g.cin = p.in_c;
+    g.stack = p.stack;
+    for (int l = 0; l < p.L; ++l) g.radius[l] = p.radius[l];
+    for (int l = 0; l <= p.L; ++l) {
+        g.pmask[l] = net->at<uint64_t>(p.o_pm[l]);
+        g.tmask[l] = net->at<uint64_t>(p.o_tm[l]);
+    }
+    return g;
+}
+
+rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void *frames, rn_dtype fdt,
+                   const int32_t *boxes, const int32_t *box_off, float *logits, void *stream, int force_all) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (n < 1 || n > p.S) return net->fail(RN_EINVAL, "n must be 1..max_streams");
+    if (!frames) return net->fail(RN_EINVAL, "frames are NULL");
+    if (!logits) return net->fail(RN_EINVAL, "logits are NULL");
+    if (fdt != RN_F32 && fdt != RN_U8) return net->fail(RN_EINVAL, "frame dtype must be F32 or U8");
+    if (boxes && !box_off) return net->fail(RN_EINVAL, "boxes given without box offsets");
+    if (boxes && p.stack != 1) return net->fail(RN_EUNSUPPORTED, "change boxes with stacked frames are not implemented");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int32_t *ids = ids_in ? ids_in : net->at<int32_t>(p.o_ids);
+
+    MaskGeom g = make_geom(net);
+    MaskArgs ma{};
+    ma.n = n;
+    ma.ids = ids;
+    ma.frames = frames;
+    ma.frame_u8 = fdt == RN_U8;
+    ma.boxes = force_all ? nullptr : boxes;
+    ma.box_off = box_off;
+    ma.force_all = force_all;
+    ma.lut = net->at<float>(p.o_lut);
+    ma.xin = net->at<float>(p.o_xin);
+    ma.ring_head = net->at<int32_t>(p.o_ring);
+    ma.dring = net->at<uint64_t>(p.o_dring);
+    ma.primed = net->at<int32_t>(p.o_primed);
+    ma.nchg = net->at<int32_t>(p.o_nchg);
+    ma.ntile = net->at<int32_t>(p.o_ntile);
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("mask kernel: ") + hipGetErrorString(e));
+
+    CompactArgs ca{};
+    ca.n = n;
+    ca.L = p.L;
+    ca.TW = p.TW;
+    ca.TMW = p.TMW;
+    ca.ntiles = p.ntiles;
+    ca.ids = ids;
+    ca.ntile = ma.ntile;
+    for (int l = 0; l <= p.L; ++l) {
+        ca.tmask[l] = g.tmask[l];
+        ca.wl[l] = l ? net->at<uint32_t>(p.o_wl[l]) : nullptr;
+    }
+    ca.cnt = net->at<int32_t>(p.o_cnt);
+    e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
+
+    const int max_tiles = n * p.ntiles;
+    for (int l = 1; l <= p.L; ++l) {
+        ConvArgs cv{};
+        cv.wl = ca.wl[l];
+        cv.cnt = ca.cnt + l;
+        cv.ids = ids;
+        cv.in = l == 1 ? static_cast<const void *>(ma.xin) : net->at<void>(p.o_act[l - 1]);
+        cv.out = net->at<void>(p.o_act[l]);
+        cv.w = net->at<void>(p.o_w[l - 1]);
+        cv.bias = net->at<float>(p.o_b[l - 1]);
+        cv.ring_head = ma.ring_head;
+        cv.H = p.H;
+        cv.W = p.W;
+        cv.TH = p.TH;
+        cv.TW = p.TW;
+        cv.cin = p.C[l - 1];
+        cv.cout = p.C[l];
+        cv.stack = p.stack;
+        cv.in_stride = p.act_stride[l - 1];
+        cv.out_stride = p.act_stride[l];
+        if (l == 1) {
+            const int grid = std::max(1, std::min(net->cus * 8, ceil_div(max_tiles, 4)));
+            e = timed(net, RN_PHASE_CONV1, s, [&] { return launch_conv_first(cv, p.dt, grid, s); });
+        } else {
+            const int grid = std::max(1, std::min(net->cus, ceil_div(max_tiles, 4)));
+            e = timed(net, RN_PHASE_CONVN, s, [&] { return launch_conv_mfma(cv, p.dt, grid, s); });
+        }
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv kernel: ") + hipGetErrorString(e));
+    }
+
+    HeadArgs ha{};
+    ha.n = n;
+    ha.n_out = p.N;
+    ha.ids = ids;
+    ha.act = net->at<void>(p.o_act[p.L]);
+    ha.w = net->at<void>(p.o_wd);
+    ha.bias = net->at<float>(p.o_bd);
+    ha.part = net->at<float>(p.o_part);
+    ha.logits = logits;
+    ha.K = p.K;
+    head_split(p, n, &ha.nsplit, &ha.chunk);
+    e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_head(ha, p.dt, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head kernel: ") + hipGetErrorString(e));
+
+    net->last_stream = s;
+    net->last_n = n;
+    net->has_step = true;
+    net->err.clear();
+    return RN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t reuse_net_workspace_bytes(const rn_config *cfg) {
+    Plan p;
+    std::string err;
+    if (plan_config(cfg, &p, &err) != RN_OK) return 0;
+    return p.total;
+}
+
+rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_workspace, size_t bytes,
+                           void *hip_stream, reuse_net **out) {
+    g_create_error.clear();
+    if (!out) {
+        g_create_error = "out is NULL";
+        return RN_EINVAL;
+    }
+    *out = nullptr;
+    Plan p;
+    rn_status st = plan_config(cfg, &p, &g_create_error);
+    if (st != RN_OK) return st;
+    if (!w || !w->conv_w || !w->conv_b || !w->dense_w || !w->dense_b) {
+        g_create_error = "weights are NULL";
+        return RN_EINVAL;
+    }
+    for (int l = 0; l < p.L; ++l)
+        if (!w->conv_w[l] || !w->conv_b[l]) {
+            g_create_error = "conv weights of layer " + std::to_string(l + 1) + " are NULL";
+            return RN_EINVAL;
+        }
+    if (!dev_workspace) {
+        g_create_error = "workspace is NULL";
+        return RN_EINVAL;
+    }
+    if (reinterpret_cast<uintptr_t>(dev_workspace) % kAlign) {
+        g_create_error = "workspace must be 256-byte aligned";
+        return RN_EINVAL;
+    }
+    if (bytes < p.total) {
+        g_create_error = "workspace too small: need " + std::to_string(p.total) + " bytes";
+        return RN_ENOSPACE;
+    }
+    reuse_net *net = new reuse_net();
+    net->p = p;
+    net->cfg = *cfg;
+    net->cfg.conv = nullptr;
+    net->ws = static_cast<char *>(dev_workspace);
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
+        net->cus = std::max(1, prop.multiProcessorCount);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+    // Host-side images of the constant parts.
+    std::vector<float> lut(256);
+    for (int k = 0; k < 256; ++k) lut[k] = (float)k / 255.0f;   // IEEE division: correctly rounded
+    std::vector<int32_t> ids(p.S);
+    for (int i = 0; i < p.S; ++i) ids[i] = i;
+    std::vector<std::vector<float>> wpack(p.L);
+    for (int l = 0; l < p.L; ++l) {
+        wpack[l].assign(p.w_elems[l], 0.f);
+        if (l == 0) pack_conv_first(w->conv_w[0], p.C[0], p.C[1], p.dt, wpack[l].data());
+        else pack_conv_mfma(w->conv_w[l], p.C[l], p.C[l + 1], p.dt, wpack[l].data());
+    }
+    // Dense weights from (c, y, x) order to the tiled cache order, 0 at padded pixels.
+    const int CL = p.C[p.L];
+    std::vector<float> wd((size_t)p.N * p.K, 0.f);
+    for (int o = 0; o < p.N; ++o)
+        for (int ty = 0; ty < p.TH; ++ty)
+            for (int tx = 0; tx < p.TW; ++tx)
+                for (int m = 0; m < kTilePx; ++m) {
+                    const int y = ty * kTile + m / kTile, x = tx * kTile + m % kTile;
+                    if (y >= p.H || x >= p.W) continue;
+                    const size_t dst = (size_t)o * p.K + ((size_t)(ty * p.TW + tx) * kTilePx + m) * CL;
+                    for (int c = 0; c < CL; ++c)
+                        wd[dst + c] = w->dense_w[(size_t)o * CL * p.H * p.W + ((size_t)c * p.H + y) * p.W + x];
+                }
+
+    hipError_t e = hipMemsetAsync(dev_workspace, 0, p.total, s);
+    auto up = [&](size_t off, const void *src, size_t n) {
+        if (e == hipSuccess) e = hipMemcpyAsync(net->ws + off, src, n, hipMemcpyHostToDevice, s);
+    };
+    up(p.o_lut, lut.data(), 256 * 4);
+    up(p.o_ids, ids.data(), (size_t)p.S * 4);
+    for (int l = 0; l < p.L; ++l) {
+        up(p.o_w[l], wpack[l].data(), p.w_elems[l] * 4);
+        up(p.o_b[l], w->conv_b[l], (size_t)p.C[l + 1] * 4);
+    }
+    up(p.o_wd, wd.data(), wd.size() * 4);
+    up(p.o_bd, w->dense_b, (size_t)p.N * 4);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        g_create_error = std::string("upload: ") + hipGetErrorString(e);
+        delete net;
+        return RN_EHIP;
+    }
+    *out = net;
+    return RN_OK;
+}
+
+rn_status reuse_net_step(reuse_net *net, int32_t n, const int32_t *ids, const void *frames, rn_dtype fdt,
+                         const int32_t *boxes, const int32_t *box_off, float *logits, void *stream) {
+    return run_step(net, n, ids, frames, fdt, boxes, box_off, logits, stream, 0);
+}
+
+rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *ids, const void *frames, rn_dtype fdt,
+                         float *logits, void *stream) {
+    return run_step(net, n, ids, frames, fdt, nullptr, nullptr, logits, stream, 1);
+}
+
+rn_status reuse_net_reset(reuse_net *net, int32_t sid) {
+    if (!net) return RN_EINVAL;
+    if (sid < -1 || sid >= net->p.S) return net->fail(RN_EINVAL, "stream_id out of range");
+    rn_status st = sync_last(net);
+    if (st != RN_OK) return st;
+    int32_t *pr = net->at<int32_t>(net->p.o_primed);
+    hipError_t e = sid < 0 ? hipMemset(pr, 0, (size_t)net->p.S * 4) : hipMemset(pr + sid, 0, 4);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("reset: ") + hipGetErrorString(e));
+    return RN_OK;
+}
+
+static rn_status copy_out(reuse_net *net, void *dst, const void *src, size_t bytes) {
+    rn_status st = sync_last(net);
+    if (st != RN_OK) return st;
+    hipError_t e = hipMemcpy(dst, src, bytes, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("copy: ") + hipGetErrorString(e));
+    return RN_OK;
+}
+
+rn_status reuse_net_get_pixel_mask(reuse_net *net, int32_t layer, int32_t sid, uint64_t *out, size_t words) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (layer < 0 || layer > p.L || sid < 0 || sid >= p.S || !out) return net->fail(RN_EINVAL, "bad layer, stream or buffer");
+    const size_t need = (size_t)p.H * p.WW;
+    if (words < need) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(need) + " words");
+    return copy_out(net, out, net->at<uint64_t>(p.o_pm[layer]) + (size_t)sid * need, need * 8);
+}
+
+rn_status reuse_net_get_tile_mask(reuse_net *net, int32_t layer, int32_t sid, uint64_t *out, size_t words) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (layer < 0 || layer > p.L || sid < 0 || sid >= p.S || !out) return net->fail(RN_EINVAL, "bad layer, stream or buffer");
+    if (words < (size_t)p.TMW) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(p.TMW) + " words");
+    return copy_out(net, out, net->at<uint64_t>(p.o_tm[layer]) + (size_t)sid * p.TMW, (size_t)p.TMW * 8);
+}
+
+rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, size_t cap, int32_t *count) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (layer < 1 || layer > p.L || !count) return net->fail(RN_EINVAL, "bad layer or count pointer");
+    int32_t c = 0;
+    rn_status st = copy_out(net, &c, net->at<int32_t>(p.o_cnt) + layer, 4);
+    if (st != RN_OK) return st;
+    *count = c;
+    if ((size_t)c > cap) return net->fail(RN_ENOSPACE, "work list has " + std::to_string(c) + " entries");
+    if (c == 0) return RN_OK;
+    if (!out) return net->fail(RN_EINVAL, "out is NULL");
+    return copy_out(net, out, net->at<uint32_t>(p.o_wl[layer]), (size_t)c * 4);
+}
+
+rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, float *host_out) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (layer < 0 || layer > p.L || sid < 0 || sid >= p.S || !host_out) return net->fail(RN_EINVAL, "bad layer, stream or buffer");
+    const size_t HW = (size_t)p.H * p.W;
+    if (layer == 0) {
+        int head = 0;
+        if (p.stack != 1) {
+            rn_status st = copy_out(net, &head, net->at<int32_t>(p.o_ring) + sid, 4);
+            if (st != RN_OK) return st;
+        }
+        const float *src = net->at<float>(p.o_xin) + ((size_t)sid * p.stack + head) * p.in_c * HW;
+        return copy_out(net, host_out, src, (size_t)p.in_c * HW * 4);
+    }
+    const int C = p.C[layer];
+    std::vector<float> buf(p.act_stride[layer]);
+    rn_status st = copy_out(net, buf.data(), net->at<float>(p.o_act[layer]) + (size_t)sid * p.act_stride[layer],
+                            p.act_stride[layer] * 4);
+    if (st != RN_OK) return st;
+    for (int y = 0; y < p.H; ++y)
+        for (int x = 0; x < p.W; ++x) {
+            const size_t src = ((size_t)((y / kTile) * p.TW + x / kTile) * kTilePx + (y % kTile) * kTile + x % kTile) * C;
+            for (int c = 0; c < C; ++c) host_out[(size_t)c * HW + (size_t)y * p.W + x] = buf[src + c];
+        }
+    return RN_OK;
+}
+
+rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out) {
+    if (!net) return RN_EINVAL;
+    if (!out) return net->fail(RN_EINVAL, "out is NULL");
+    memset(out, 0, sizeof *out);
+    if (!net->has_step) return RN_OK;
+    const Plan &p = net->p;
+    const int n = net->last_n;
+    std::vector<int32_t> nchg(n), ntile((size_t)n * (p.L + 1));
+    rn_status st = copy_out(net, nchg.data(), net->at<int32_t>(p.o_nchg), (size_t)n * 4);
+    if (st == RN_OK) st = copy_out(net, ntile.data(), net->at<int32_t>(p.o_ntile), ntile.size() * 4);
+    if (st != RN_OK) return st;
+    out->streams = n;
+    for (int i = 0; i < n; ++i) {
+        out->changed_px += nchg[i];
+        for (int l = 0; l <= p.L; ++l) out->dirty_tiles[l] += ntile[(size_t)i * (p.L + 1) + l];
+    }
+    const int64_t head_mac = (int64_t)n * p.N * p.C[p.L] * p.H * p.W;
+    int64_t useful = head_mac, issued = (int64_t)n * p.N * (int64_t)p.K, dense = head_mac;
+    for (int l = 1; l <= p.L; ++l) {
+        const int64_t per_px = (int64_t)9 * p.C[l - 1] * p.C[l];
+        dense += (int64_t)n * p.H * p.W * per_px;
+        issued += out->dirty_tiles[l] * kTilePx * per_px;
+        int32_t c = 0;
+        std::vector<uint32_t> wl((size_t)n * p.ntiles);
+        st = reuse_net_get_worklist(net, l, wl.data(), wl.size(), &c);
+        if (st != RN_OK) return st;
+        for (int j = 0; j < c; ++j) {
+            const int ty = (wl[j] >> 8) & 255, tx = wl[j] & 255;
+            const int hy = std::min(kTile, p.H - ty * kTile), wx = std::min(kTile, p.W - tx * kTile);
+            useful += (int64_t)hy * wx * per_px;
+        }
+    }
+    out->useful_mac = useful;
+    out->issued_mac = issued;
+    out->dense_mac = dense;
+    return RN_OK;
+}
+
+rn_status reuse_net_set_profiling(reuse_net *net, int32_t enable) {
+    if (!net) return RN_EINVAL;
+    rn_status st = sync_last(net);
+    if (st != RN_OK) return st;
+    net->recs.clear();
+    net->pool_used = 0;
+    net->prof = enable != 0;
+    return RN_OK;
+}
+
+rn_status reuse_net_get_profile(reuse_net *net, rn_profile *out) {
+    if (!net) return RN_EINVAL;
+    if (!out) return net->fail(RN_EINVAL, "out is NULL");
+    memset(out, 0, sizeof *out);
+    rn_status st = sync_last(net);
+    if (st != RN_OK) return st;
+    for (const ProfRec &r : net->recs) {
+        float ms = 0.f;
+        hipError_t e = hipEventElapsedTime(&ms, r.e0, r.e1);
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("event time: ") + hipGetErrorString(e));
+        out->ms[r.phase] += ms;
+        out->launches[r.phase] += 1;
+    }
+    return RN_OK;
+}
+
+const char *reuse_net_last_error(const reuse_net *net) {
+    return net ? net->err.c_str() : g_create_error.c_str();
+}
+
+void reuse_net_destroy(reuse_net *net) {
+    if (!net) return;
+    for (hipEvent_t e : net->pool) (void)hipEventDestroy(e);
+    delete net;
+}
+
+}  // extern "C"

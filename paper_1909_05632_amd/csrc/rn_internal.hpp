@@ -1,0 +1,103 @@
+// Internal declarations shared by the reuse_net host planner and its kernels.
+// Not part of the public ABI (that is include/reuse_net.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "reuse_net.h"
+
+namespace rn {
+
+constexpr int kTile = 4;          // dirty-tile edge on every layer
+constexpr int kTilePx = kTile * kTile;
+constexpr int kHeadMaxOut = 64;
+
+// Geometry shared by the mask kernels.  Every supported layer is 3x3, stride 1,
+// pad 1, so every layer's output grid equals the input grid.
+struct MaskGeom {
+    int L;                        // conv layers
+    int H, W, WW;                 // rows, columns, 64-bit words per mask row
+    int TH, TW, TMW;              // tile rows, tile columns, 64-bit words per tile mask
+    int cin;                      // channels per frame
+    int stack;                    // 1, or 4 (ring of the last 4 frames)
+    int radius[RN_MAX_CONV];      // (k - 1) / 2 per layer
+    uint64_t *pmask[RN_MAX_CONV + 1];   // [S][H][WW] per layer
+    uint64_t *tmask[RN_MAX_CONV + 1];   // [S][TMW] per layer
+};
+
+// Per-step inputs of the mask kernel.
+struct MaskArgs {
+    int n;
+    const int32_t *ids;           // [n] slots (never NULL: identity table otherwise)
+    const void *frames;           // [n][cin][H][W]
+    int frame_u8;                 // 1: uint8 levels, 0: float32
+    const int32_t *boxes;         // NULL: diff
+    const int32_t *box_off;       // [n+1]
+    int force_all;                // 1: every pixel changed (dense path)
+    const float *lut;             // [256] level -> float32
+    float *xin;                   // [S][stack][cin][H][W] input cache (ring for stack=4)
+    int32_t *ring_head;           // [S] newest ring position (stack=4)
+    uint64_t *dring;              // [S][stack][H][WW] last single-frame change masks (stack=4)
+    int32_t *primed;              // [S]
+    int32_t *nchg;                // [n] changed pixels
+    int32_t *ntile;               // [n][L+1] dirty tiles per layer
+};
+
+struct CompactArgs {
+    int n, L, TW, TMW, ntiles;
+    const int32_t *ids;
+    const int32_t *ntile;         // [n][L+1]
+    uint64_t *tmask[RN_MAX_CONV + 1];
+    uint32_t *wl[RN_MAX_CONV + 1];
+    int32_t *cnt;                 // [L+1]
+};
+
+struct ConvArgs {
+    const uint32_t *wl;           // work list of this layer
+    const int32_t *cnt;           // device count of this layer
+    const int32_t *ids;
+    const void *in;               // previous layer cache (layer 1: float32 input ring)
+    void *out;                    // this layer's cache [S][TH][TW][16][cout]
+    const void *w;                // packed weights
+    const float *bias;            // [cout]
+    const int32_t *ring_head;     // stack=4 only
+    int H, W, TH, TW;
+    int cin, cout;
+    int stack;
+    size_t in_stride, out_stride; // elements per slot
+};
+
+struct HeadArgs {
+    int n, n_out;
+    const int32_t *ids;
+    const void *act;              // last cache [S][K]
+    const void *w;                // [n_out][K] tiled order, zero at padded pixels
+    const float *bias;            // [n_out]
+    float *part;                  // [nsplit][n][n_out]
+    float *logits;                // [n][n_out]
+    size_t K;                     // elements per slot
+    int nsplit;
+    size_t chunk;                 // elements per split (multiple of 4)
+};
+
+// Launchers (each returns the hipGetLastError of its launch).
+hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s);
+hipError_t launch_compact(const CompactArgs &a, hipStream_t s);
+hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
+hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
+bool conv_mfma_supported(int cin, int cout, rn_dtype dt);
+bool conv_first_supported(int cin, int cout, rn_dtype dt);
+hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
+int head_streams_per_block(int n_out);
+
+// Packed weight sizes (elements of the act dtype) for the kernels' layouts.
+size_t conv_first_packed_elems(int cin, int cout);
+size_t conv_mfma_packed_elems(int cin, int cout, rn_dtype dt);
+void pack_conv_first(const float *oihw, int cin, int cout, rn_dtype dt, void *dst);
+void pack_conv_mfma(const float *oihw, int cin, int cout, rn_dtype dt, void *dst);
+
+}  // namespace rn

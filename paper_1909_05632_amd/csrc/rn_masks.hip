@@ -1,0 +1,299 @@
+// Change detection, change growth, dirty-tile masks and work-list compaction.
+//
+// Change detection (Abstract; Sec. 1): a pixel changed iff the float32 bits of
+// one of its channels differ from the cached input.  Growth (Fig. 1 caption):
+// a 3x3 stride-1 layer spreads a change by one pixel on each side.  Dirty
+// tiles (Sec. 3, local areas instead of one rectangle): a 4x4 cell of a
+// layer's grid is dirty iff it holds a dirty pixel.  The work list of a layer
+// is its dirty tiles in (batch index, tile row, tile column) order.
+//
+// Masks are bit rows: word (y * WW + x / 64), bit x % 64.  One workgroup owns
+// one stream: it diffs the frame against the cache with 16-byte loads, ORs the
+// change bits into a mask held in LDS, grows it layer by layer in LDS with
+// shifts and ORs, and reduces 4x4 cells to tile bits with one ballot per 64
+// tiles.  No global atomics; every output word has exactly one writer.
+#include "rn_internal.hpp"
+
+namespace rn {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ inline uint32_t f32_bits(float v) { return __float_as_uint(v); }
+
+__device__ inline uint64_t row_valid_bits(int W, int wx) {
+    int nb = W - 64 * wx;
+    return nb >= 64 ? ~0ull : ((1ull << nb) - 1ull);
+}
+
+__device__ inline int block_sum(int v, int *red) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    int s = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) s += red[w];
+    return s;
+}
+
+// Load 4 consecutive pixels of one channel plane as float32.
+template <bool U8>
+__device__ inline float4 load4(const void *frames, size_t off, const float *lut) {
+    if constexpr (U8) {
+        uint32_t q = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(frames) + off);
+        return make_float4(lut[q & 255u], lut[(q >> 8) & 255u], lut[(q >> 16) & 255u], lut[q >> 24]);
+    } else {
+        return *reinterpret_cast<const float4 *>(static_cast<const float *>(frames) + off);
+    }
+}
+
+template <bool U8>
+__device__ inline float load1(const void *frames, size_t off, const float *lut) {
+    if constexpr (U8) return lut[static_cast<const uint8_t *>(frames)[off]];
+    else return static_cast<const float *>(frames)[off];
+}
+
+// Write layer l's pixel mask and tile mask of one slot; returns the dirty tiles.
+__device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red) {
+    const int HWW = g.H * g.WW;
+    uint64_t *pm = g.pmask[l] + (size_t)slot * HWW;
+    for (int w = threadIdx.x; w < HWW; w += blockDim.x) pm[w] = A[w];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int ntiles = g.TH * g.TW;
+    uint64_t *tm = g.tmask[l] + (size_t)slot * g.TMW;
+    int cnt = 0;
+    for (int base = wave * 64; base < ntiles; base += (int)blockDim.x) {
+        const int t = base + lane;
+        bool dirty = false;
+        if (t < ntiles) {
+            const int ty = t / g.TW, tx = t - ty * g.TW;
+            const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
+            const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+            uint64_t bits = 0;
+            for (int y = y0; y < y1; ++y) bits |= A[y * g.WW + wx] >> sh;
+            dirty = (bits & ((1ull << kTile) - 1ull)) != 0;
+        }
+        const uint64_t m = __ballot(dirty);
+        if (lane == 0) {
+            tm[base >> 6] = m;
+            cnt += __popcll(m);
+        }
+    }
+    return block_sum(lane == 0 ? cnt : 0, red);
+}
+
+// Grow a change set by one pixel on every side (3x3 window), clipped to the grid.
+__device__ void grow1(const MaskGeom &g, const uint64_t *src, uint64_t *dst) {
+    const int HWW = g.H * g.WW;
+    for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
+        const int y = w / g.WW, wx = w - y * g.WW;
+        uint64_t acc = 0;
+        for (int dy = -1; dy <= 1; ++dy) {
+            const int yy = y + dy;
+            if (yy < 0 || yy >= g.H) continue;
+            const uint64_t *row = src + yy * g.WW;
+            const uint64_t c = row[wx];
+            const uint64_t lft = wx > 0 ? row[wx - 1] : 0ull;
+            const uint64_t rgt = wx + 1 < g.WW ? row[wx + 1] : 0ull;
+            acc |= c | (c << 1) | (lft >> 63) | (c >> 1) | (rgt << 63);
+        }
+        dst[w] = acc & row_valid_bits(g.W, wx);
+    }
+}
+
+template <bool U8>
+__global__ __launch_bounds__(kThreads) void k_masks(MaskGeom g, MaskArgs a) {
+    extern __shared__ uint64_t smem[];
+    __shared__ int red[kThreads / 64];
+    __shared__ int s_tiles[RN_MAX_CONV + 1];
+    const int HWW = g.H * g.WW;
+    uint64_t *A = smem;
+    uint64_t *B = smem + HWW;
+    float *lut = reinterpret_cast<float *>(smem + 2 * HWW);
+
+    const int i = blockIdx.x;
+    const int slot = a.ids[i];
+    const int primed = a.force_all ? 0 : a.primed[slot];
+    const size_t HW = (size_t)g.H * g.W;
+    const int C = g.cin;
+
+    for (int w = threadIdx.x; w < HWW; w += blockDim.x) A[w] = 0ull;
+    if (U8)
+        for (int j = threadIdx.x; j < 256; j += blockDim.x) lut[j] = a.lut[j];
+    __syncthreads();
+
+    // Cache planes: the previous newest frame, and where the new frame goes.
+    float *prev, *next;
+    int head = 0, nhead = 0;
+    if (g.stack == 1) {
+        prev = next = a.xin + (size_t)slot * C * HW;
+    } else {
+        head = a.ring_head[slot];
+        nhead = (head + 1) & 3;
+        prev = a.xin + ((size_t)slot * 4 + head) * C * HW;
+        next = a.xin + ((size_t)slot * 4 + nhead) * C * HW;
+    }
+    const size_t fbase = (size_t)i * C * HW;
+
+    if (a.boxes != nullptr && primed) {
+        // Known change (Sec. 1): the boxes are the change set; only box pixels
+        // are read from the frame and copied into the cache.
+        const int b0 = a.box_off[i], b1 = a.box_off[i + 1];
+        for (int b = b0; b < b1; ++b) {
+            const int y0 = max(a.boxes[4 * b + 0], 0), x0 = max(a.boxes[4 * b + 1], 0);
+            const int y1 = min(a.boxes[4 * b + 2], g.H), x1 = min(a.boxes[4 * b + 3], g.W);
+            const int bh = y1 - y0, bw = x1 - x0;
+            if (bh <= 0 || bw <= 0) continue;
+            for (int e = threadIdx.x; e < bh * bw; e += blockDim.x) {
+                const int y = y0 + e / bw, x = x0 + e % bw;
+                const size_t px = (size_t)y * g.W + x;
+                for (int c = 0; c < C; ++c)
+                    next[c * HW + px] = load1<U8>(a.frames, fbase + c * HW + px, lut);
+                atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
+                         1ull << (x & 63));
+            }
+        }
+    } else {
+        // Diff, 4 pixels (one 16-byte load per plane) per thread per iteration.
+        const int n4 = (int)(HW / 4);
+        for (int q = threadIdx.x; q < n4; q += blockDim.x) {
+            uint32_t ch = primed ? 0u : 0xFu;
+            for (int c = 0; c < C; ++c) {
+                const float4 nv = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, lut);
+                const float4 ov = *reinterpret_cast<const float4 *>(prev + c * HW + 4 * (size_t)q);
+                const uint32_t d = (f32_bits(nv.x) != f32_bits(ov.x) ? 1u : 0u) |
+                                   (f32_bits(nv.y) != f32_bits(ov.y) ? 2u : 0u) |
+                                   (f32_bits(nv.z) != f32_bits(ov.z) ? 4u : 0u) |
+                                   (f32_bits(nv.w) != f32_bits(ov.w) ? 8u : 0u);
+                ch |= d;
+                if (g.stack != 1 || d != 0u || !primed)
+                    *reinterpret_cast<float4 *>(next + c * HW + 4 * (size_t)q) = nv;
+                if (g.stack != 1 && !primed) {
+                    // Priming a stacked input: every older frame is this frame.
+                    for (int r = 0; r < 4; ++r)
+                        *reinterpret_cast<float4 *>(a.xin + ((size_t)slot * 4 + r) * C * HW +
+                                                    c * HW + 4 * (size_t)q) = nv;
+                }
+            }
+            if (ch) {
+                const int p = 4 * q, y = p / g.W, x = p - y * g.W;
+                atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
+                         (unsigned long long)ch << (x & 63));
+            }
+        }
+    }
+    __syncthreads();
+
+    if (g.stack != 1) {
+        // Stacked input: channel j of step t is frame t-3+j, so the stack
+        // changed where any of the last 4 single-frame diffs did.  Keep this
+        // step's single-frame diff in the ring and OR the ring together.
+        uint64_t *ring = a.dring + (size_t)slot * 4 * HWW;
+        for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
+            const uint64_t d = A[w];
+            if (!primed) {
+                for (int r = 0; r < 4; ++r) ring[r * HWW + w] = 0ull;
+            } else {
+                ring[nhead * HWW + w] = d;
+                A[w] = d | ring[((nhead + 1) & 3) * HWW + w] | ring[((nhead + 2) & 3) * HWW + w] |
+                       ring[((nhead + 3) & 3) * HWW + w];
+            }
+        }
+        __syncthreads();
+    }
+
+    int nchg = 0;
+    for (int w = threadIdx.x; w < HWW; w += blockDim.x) nchg += __popcll(A[w]);
+    nchg = block_sum(nchg, red);
+
+    int t0 = emit_layer(g, A, 0, slot, red);
+    if (threadIdx.x == 0) s_tiles[0] = t0;
+    for (int l = 1; l <= g.L; ++l) {
+        for (int r = 0; r < g.radius[l - 1]; ++r) {
+            __syncthreads();
+            grow1(g, A, B);
+            __syncthreads();
+            uint64_t *t = A;
+            A = B;
+            B = t;
+        }
+        const int tl = emit_layer(g, A, l, slot, red);
+        if (threadIdx.x == 0) s_tiles[l] = tl;
+    }
+    if (threadIdx.x == 0) {
+        a.nchg[i] = nchg;
+        for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_tiles[l];
+        a.primed[slot] = 1;
+        if (g.stack != 1) a.ring_head[slot] = nhead;
+    }
+}
+
+// Work lists: block (bx, l-1) writes the entries of streams [16 bx, 16 bx + 16)
+// of layer l at their exclusive-prefix offsets.  Counts come from the mask
+// kernel, so the order is fixed and no atomics are needed.
+constexpr int kStreamsPerBlock = 16;
+
+__global__ __launch_bounds__(kThreads) void k_compact(CompactArgs a) {
+    __shared__ int red[kThreads / 64];
+    __shared__ int s_off[kStreamsPerBlock];
+    const int l = blockIdx.y + 1;
+    const int L1 = a.L + 1;
+    const int i0 = blockIdx.x * kStreamsPerBlock;
+    int pre = 0;
+    for (int j = threadIdx.x; j < i0; j += blockDim.x) pre += a.ntile[(size_t)j * L1 + l];
+    pre = block_sum(pre, red);
+    if (blockIdx.x == 0) {
+        int tot = 0;
+        for (int j = threadIdx.x; j < a.n; j += blockDim.x) tot += a.ntile[(size_t)j * L1 + l];
+        tot = block_sum(tot, red);
+        if (threadIdx.x == 0) a.cnt[l] = tot;
+    }
+    if (threadIdx.x == 0) {
+        int o = pre;
+        for (int s = 0; s < kStreamsPerBlock; ++s) {
+            s_off[s] = o;
+            if (i0 + s < a.n) o += a.ntile[(size_t)(i0 + s) * L1 + l];
+        }
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    for (int s = wave; s < kStreamsPerBlock; s += (int)(blockDim.x >> 6)) {
+        const int i = i0 + s;
+        if (i >= a.n) break;
+        const int slot = a.ids[i];
+        const uint64_t *tm = a.tmask[l] + (size_t)slot * a.TMW;
+        uint32_t *wl = a.wl[l];
+        int base = s_off[s];
+        for (int wd = 0; wd < a.TMW; ++wd) {
+            const uint64_t word = tm[wd];
+            if ((word >> lane) & 1ull) {
+                const int t = wd * 64 + lane;
+                const int ty = t / a.TW, tx = t - ty * a.TW;
+                wl[base + __popcll(word & below)] =
+                    ((uint32_t)i << 16) | ((uint32_t)ty << 8) | (uint32_t)tx;
+            }
+            base += __popcll(word);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s) {
+    const size_t shm = (size_t)2 * g.H * g.WW * sizeof(uint64_t) + 256 * sizeof(float);
+    if (a.frame_u8)
+        hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kThreads), shm, s, g, a);
+    else
+        hipLaunchKernelGGL(k_masks<false>, dim3(a.n), dim3(kThreads), shm, s, g, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact(const CompactArgs &a, hipStream_t s) {
+    dim3 grid((a.n + kStreamsPerBlock - 1) / kStreamsPerBlock, a.L);
+    hipLaunchKernelGGL(k_compact, grid, dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace rn

@@ -1,0 +1,113 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects bad
+arguments with status codes (host-side validation only: no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_1909_05632_amd as pkg
+from paper_1909_05632_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "reuse_net.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(reuse_net_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pkg.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _cfg(convs=((1, 40), (40, 80)), h=105, w=80, stack=1, n_out=6, tile=4, streams=8,
+         k=3, s=1, p=1, dtype=B.RN_F32, in_c=1):
+    specs = (B.rn_conv_spec * len(convs))(*[B.rn_conv_spec(ci, co, k, s, p) for ci, co in convs])
+    cfg = B.rn_config(in_c, h, w, stack, len(convs), specs, n_out, tile, tile, streams, dtype)
+    cfg._keep = specs
+    return cfg
+
+
+def test_workspace_bytes_valid_configs():
+    n1 = B.reuse_net_workspace_bytes(_cfg(streams=1))
+    n8 = B.reuse_net_workspace_bytes(_cfg(streams=8))
+    assert n1 > 0 and n8 > n1
+    # The caches dominate: 8 streams of 105x80 fp32 caches at 40 + 80 channels.
+    assert n8 > 8 * (27 * 20 * 16) * 120 * 4
+    assert B.reuse_net_workspace_bytes(_cfg(((4, 40), (40, 80)), stack=4)) > 0
+    assert B.reuse_net_workspace_bytes(
+        _cfg(((1, 64), (64, 128), (128, 128)), h=210, w=160, n_out=18)) > 0
+
+
+@pytest.mark.parametrize("bad", [
+    dict(k=2, p=0),                   # even kernel
+    dict(p=0),                        # pad != (k-1)/2
+    dict(s=0),                        # stride 0
+    dict(convs=((1, 40), (32, 80))),  # broken channel chain
+    dict(convs=()),                   # no layers
+    dict(stack=3),
+    dict(streams=0),
+    dict(n_out=0),
+    dict(tile=8),                     # valid but unsupported tile
+    dict(w=78),                       # width not a multiple of 4
+    dict(k=5, p=2),                   # valid but unsupported kernel size
+    dict(convs=((1, 40), (40, 72))),  # no MFMA kernel for this shape
+])
+def test_workspace_bytes_rejects_bad_configs(bad):
+    assert B.reuse_net_workspace_bytes(_cfg(**bad)) == 0
+
+
+def _create(cfg, weights=True, ptr=256, nbytes=None):
+    lib = pkg.load_library()
+    h = ctypes.c_void_p()
+    keep = []
+    w = None
+    if weights:
+        L = cfg.n_conv
+        arrs = [np.zeros(1 << 16, np.float32) for _ in range(2 * L + 2)]
+        keep.append(arrs)
+        cw = (ctypes.c_void_p * max(L, 1))(*[a.ctypes.data for a in arrs[:L]])
+        cb = (ctypes.c_void_p * max(L, 1))(*[a.ctypes.data for a in arrs[L:2 * L]])
+        w = B.rn_weights(cw, cb, arrs[-2].ctypes.data, arrs[-1].ctypes.data)
+        keep += [cw, cb]
+    need = B.reuse_net_workspace_bytes(cfg)
+    st = lib.reuse_net_create(ctypes.byref(cfg), ctypes.byref(w) if w else None, ptr,
+                              need if nbytes is None else nbytes, None, ctypes.byref(h))
+    return st, h.value, B.reuse_net_last_error(None)
+
+
+def test_create_reports_argument_errors_without_touching_the_gpu():
+    st, h, msg = _create(_cfg(k=2, p=0))
+    assert st == B.RN_EINVAL and h is None and "odd" in msg
+    st, h, msg = _create(_cfg(tile=8))
+    assert st == B.RN_EUNSUPPORTED and "tile" in msg
+    st, h, msg = _create(_cfg(), weights=False)
+    assert st == B.RN_EINVAL and "weights" in msg
+    st, h, msg = _create(_cfg(), nbytes=1024)
+    assert st == B.RN_ENOSPACE and "too small" in msg
+    st, h, msg = _create(_cfg(), ptr=256 + 4)
+    assert st == B.RN_EINVAL and "aligned" in msg
+    st, h, msg = _create(_cfg(), ptr=None)
+    assert st == B.RN_EINVAL
+    lib = pkg.load_library()
+    assert lib.reuse_net_create(None, None, None, 0, None, None) == B.RN_EINVAL
+
+
+def test_null_net_calls_return_einval():
+    lib = pkg.load_library()
+    assert lib.reuse_net_step(None, 1, None, None, 0, None, None, None, None) == B.RN_EINVAL
+    assert lib.reuse_net_full(None, 1, None, None, 0, None, None) == B.RN_EINVAL
+    assert lib.reuse_net_reset(None, -1) == B.RN_EINVAL
+    assert lib.reuse_net_get_stats(None, None) == B.RN_EINVAL
+    assert lib.reuse_net_get_profile(None, None) == B.RN_EINVAL
+    lib.reuse_net_destroy(None)

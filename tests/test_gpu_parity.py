@@ -1,0 +1,192 @@
+"""GPU parity of the reuse path (through the C ABI) against the CPU oracle.
+
+Masks and work lists: bit-exact.  Activations and logits: max abs error 1e-4
+(float32 path).  Every input is seeded and synthetic (sprite frames standing in
+for the Atari frames)."""
+import numpy as np
+import pytest
+
+import oracle
+from synth import frames as synth
+from tests.conftest import gpu_available
+from tests.gpu_util import (ATOL_F32, check_masks, check_values, make_net, oracle_d0, oracle_net,
+                            sprite_inputs)
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X GPU")]
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+def _run_sequence(torch, wl, streams, frames, weights, slots=None, max_streams=None, u8=False,
+                  sample=None, mask_every=1, value_every=1, label=""):
+    u8x, x = sprite_inputs(wl, range(streams), frames)
+    S = max_streams or streams
+    net = make_net(wl, S, weights)
+    onet = oracle_net(wl)
+    ids = None
+    slots = np.arange(streams) if slots is None else np.asarray(slots)
+    if not np.array_equal(slots, np.arange(streams)):
+        ids = torch.from_numpy(slots.astype(np.int32)).cuda()
+    dev = torch.from_numpy(u8x if u8 else x).cuda()
+    sample = list(range(streams)) if sample is None else sample
+    for t in range(frames):
+        logits = net.step(dev[t][:, None].contiguous(), stream_ids=ids).cpu().numpy()
+        if t % mask_every == 0 or t == frames - 1:
+            d0 = oracle_d0(x[t - 1][:, None] if t else None, x[t][:, None], primed=t > 0)
+            check_masks(net, onet, d0, slots, label=f"{label} t={t}")
+        if t % value_every == 0 or t == frames - 1:
+            check_values(net, onet, weights, x[t][:, None], slots, sample, logits,
+                         label=f"{label} t={t}")
+    return net
+
+
+def test_single_stream_53x40_all_frames(torch):
+    # 1 stream x 16 frames of 53x40 (ragged last tile row: 53 = 13 * 4 + 1).
+    wl = synth.WORKLOADS["atari-ds4-1x16"]
+    for bias in (0.0, 0.1):
+        weights = synth.net_weights(wl, bias_std=bias)
+        _run_sequence(torch, wl, 1, wl.frames, weights, label=f"bias={bias}").close()
+
+
+def test_batch_105x80_permuted_slots_u8(torch):
+    # 12 streams on permuted cache slots out of 20; uint8 frames read as k/255.
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    slots = np.random.default_rng(7).permutation(20)[:12]
+    _run_sequence(torch, wl, 12, 6, weights, slots=slots, max_streams=20, u8=True,
+                  sample=[0, 5, 11], label="u8").close()
+
+
+def test_small_ragged_shapes(torch):
+    # Frame sizes that are not multiples of the tile in either direction, and
+    # widths above 64 (two mask words per row) and at most 64.
+    for (h, w) in [(9, 12), (17, 68), (30, 132)]:
+        wl = synth.Workload(cid=50 + h, streams=3, frames=5, h=h, w=w, convs=(40, 80), n_out=6,
+                            n_sprites=2, smin=2, smax=5, vmin=1, vmax=3)
+        weights = synth.net_weights(wl, bias_std=0.1)
+        _run_sequence(torch, wl, 3, 5, weights, label=f"{h}x{w}").close()
+
+
+def test_unchanged_frame_gives_no_work_and_same_logits(torch):
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _, x = sprite_inputs(wl, range(4), 2)
+    net = make_net(wl, 4, weights)
+    dev = torch.from_numpy(x).cuda()
+    net.step(dev[0][:, None].contiguous())
+    a = net.step(dev[1][:, None].contiguous()).cpu().numpy()
+    b = net.step(dev[1][:, None].contiguous()).cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    for l in range(3):
+        for i in range(4):
+            assert net.tile_mask_u8(l, i).sum() == 0
+    for l in (1, 2):
+        assert net.worklist(l).size == 0
+    st = net.stats()
+    assert st["changed_px"] == 0 and sum(st["dirty_tiles"]) == 0
+    net.close()
+
+
+def test_all_changed_step_equals_full_bitwise(torch):
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    u8 = synth.sprite_batch(wl, streams=range(3), frames=2, full_change=True)
+    x = synth.to_f32(u8)
+    dev = torch.from_numpy(x).cuda()
+    a, b = make_net(wl, 3, weights), make_net(wl, 3, weights)
+    a.step(dev[0][:, None].contiguous())
+    la = a.step(dev[1][:, None].contiguous()).cpu().numpy()
+    lb = b.full(dev[1][:, None].contiguous()).cpu().numpy()
+    assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
+    th, tw = 27, 20
+    for l in (1, 2):
+        assert a.worklist(l).size == 3 * th * tw
+        for i in range(3):
+            ga, gb = a.activation(i, l), b.activation(i, l)
+            assert np.array_equal(ga.view(np.uint32), gb.view(np.uint32))
+    ref, _ = oracle.forward(oracle_net(wl), *weights, x[1][:, None])
+    assert np.abs(la - ref).max() <= ATOL_F32
+    a.close()
+    b.close()
+
+
+def test_reset_recomputes_everything(torch):
+    wl = synth.WORKLOADS["atari-ds4-1x16"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _, x = sprite_inputs(wl, range(2), 3)
+    net = make_net(wl, 2, weights)
+    dev = torch.from_numpy(x).cuda()
+    net.step(dev[0][:, None].contiguous())
+    net.step(dev[1][:, None].contiguous())
+    net.reset(1)
+    logits = net.step(dev[1][:, None].contiguous()).cpu().numpy()
+    assert net.tile_mask_u8(2, 0).sum() == 0          # stream 0 unchanged
+    assert net.tile_mask_u8(2, 1).all()               # stream 1 reset: all dirty
+    ref, _ = oracle.forward(oracle_net(wl), *weights, x[1][:, None])
+    assert np.abs(logits - ref).max() <= ATOL_F32
+    net.close()
+
+
+def test_change_boxes_occlusion(torch):
+    # Known-change mode: prime every stream on the base image with the dense
+    # path, then move an 8x8 zero patch along a row with explicit boxes: each
+    # step's boxes are the previous patch (restored from the base) and the new one.
+    wl = synth.WORKLOADS["occlusion-105x80-4096"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    base = synth.to_f32(synth.occlusion_base(wl))
+    rows = [0, 30, 97]                                  # 97 + 8 = 105: touches the bottom edge
+    n = len(rows)
+    net = make_net(wl, n, weights)
+    onet = oracle_net(wl)
+    net.full(torch.from_numpy(np.stack([base[None]] * n)).cuda())
+    prev = None
+    for x0 in [0, 1, 2, 40, 72]:
+        frames = np.stack([synth.occlusion_variant_frame(base, y, x0, 8)[None] for y in rows])
+        boxes, off = [], [0]
+        for y in rows:
+            if prev is not None:
+                boxes.append((y, prev, y + 8, prev + 8))
+            boxes.append((y, x0, y + 8, x0 + 8))
+            off.append(len(boxes))
+        prev = x0
+        tb = torch.tensor(np.asarray(boxes, np.int32).reshape(-1, 4)).cuda()
+        to = torch.tensor(np.asarray(off, np.int32)).cuda()
+        logits = net.step(torch.from_numpy(frames).cuda(), boxes=tb, box_off=to).cpu().numpy()
+        d0 = np.stack([oracle.box_mask(wl.h, wl.w, boxes[off[i]:off[i + 1]]) for i in range(n)])
+        check_masks(net, onet, d0, np.arange(n), label=f"x0={x0}")
+        check_values(net, onet, weights, frames, np.arange(n), [0, 2], logits, label=f"x0={x0}")
+    net.close()
+
+
+def test_double_run_is_deterministic(torch):
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl)
+    _, x = sprite_inputs(wl, range(8), 4)
+    dev = torch.from_numpy(x).cuda()
+    outs = []
+    for _ in range(2):
+        net = make_net(wl, 8, weights)
+        seq = [net.step(dev[t][:, None].contiguous()).cpu().numpy() for t in range(4)]
+        outs.append((np.stack(seq), net.activation(3, 2)))
+        net.close()
+    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
+    assert np.array_equal(outs[0][1].view(np.uint32), outs[1][1].view(np.uint32))
+
+
+def test_full_size_256x64_atari_ds2(torch):
+    # The benchmark workload at full size: 256 streams x 64 frames of 105x80.
+    # Masks and work lists of every stream and frame bit-exact; logits of every
+    # stream and activations of streams {0, 1, 128, 255} on every 8th frame.
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl)
+    net = _run_sequence(torch, wl, 256, 64, weights, sample=[0, 1, 128, 255], value_every=8,
+                        label="256x64")
+    st = net.stats()
+    frac = st["changed_px"] / (256 * 105 * 80)
+    assert 0.001 < frac < 0.06, frac                       # ~1-3% changed pixels
+    net.close()
