@@ -81,6 +81,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=None)
+    ap.add_argument("--head", default="tiles", choices=["tiles", "full"])
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -98,7 +99,7 @@ def main():
     u8 = synth.sprite_batch(wl)                                 # [F][S][H][W]
     frames = torch.from_numpy(synth.to_f32(u8)).cuda().unsqueeze(2).contiguous()  # [F][S][1][H][W]
     net = ReuseNet(wl.in_c, wl.h, wl.w, wl.convs, wl.n_out, S, weights, act_dtype=args.dtype,
-                   stack=wl.stack)
+                   stack=wl.stack, head=args.head)
     out = torch.empty((S, wl.n_out), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     seq = schedule(F, args.warmup + args.steps)
@@ -164,9 +165,20 @@ def main():
     flops_convn = sum(dirty[:, l].sum() * 16 * chans[l] * 9 * chans[l - 1] * 2 for l in range(2, L + 1))
     if prof["convN"]["ms"] > 0:
         kern["convN"]["tflops"] = flops_convn / (prof["convN"]["ms"] / 1e3) / 1e12
-    # dense head: reads every stream's a_L cache (tiled, padded) and the weights once per launch
-    head_bytes = (S * tiles * 16 * chans[L] * 4 + wl.n_out * tiles * 16 * chans[L] * 4) * K
+    K_el = tiles * 16 * chans[L]
+    if args.head == "full":
+        # full-read head: every stream's whole last-layer cache plus the weights, per launch
+        head_bytes = (S * K_el * 4 + wl.n_out * K_el * 4) * K
+    else:
+        # tile-partial head: the per-tile partials of every stream
+        head_bytes = S * tiles * wl.n_out * 4 * K
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
+    # MFMA conv bytes per tile: halo in, tile out (+ head weights of the tile on the last layer)
+    bytes_convn = sum(dirty[:, l].sum() * (36 * chans[l - 1] + 16 * chans[l] +
+                                           (16 * chans[l] * wl.n_out if (l == L and args.head == "tiles") else 0)) * 4
+                      for l in range(2, L + 1))
+    if prof["convN"]["ms"] > 0:
+        kern["convN"]["gbs"] = bytes_convn / (prof["convN"]["ms"] / 1e3) / 1e9
     # masks: frames + cached input read, changed pixels written (~0), masks written
     mask_bytes = (2 * S * wl.h * wl.w * 4 * wl.in_c) * K
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
@@ -202,7 +214,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "streams": S, "frames": F, "h": wl.h, "w": wl.w,
-                   "convs": list(wl.convs), "n_out": wl.n_out, "tile": "4x4",
+                   "convs": list(wl.convs), "n_out": wl.n_out, "tile": "4x4", "head": args.head,
                    "description": wl.description},
         "dense_path": {"value": fps_dense, "unit": "frames/s", "ms_per_step": ms_dense},
         "speedup_vs_dense": fps / fps_dense,

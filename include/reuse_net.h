@@ -53,6 +53,17 @@ typedef enum {
 
 typedef enum { RN_F32 = 0, RN_BF16 = 1, RN_U8 = 2 } rn_dtype;
 
+/* How the dense head is evaluated.  Both give the same logits up to float32
+ * rounding order; each is deterministic.
+ *   RN_HEAD_TILES: the head is linear, so the logits are a sum over tiles of
+ *     each tile's contribution (the reuse idea of Sec. 1 applied to the dense
+ *     layer).  The last conv layer's epilogue recomputes the contribution of
+ *     every tile it recomputes, and the head adds the cached contributions in
+ *     a fixed tile order.  Needs n_conv >= 2.
+ *   RN_HEAD_FULL: the head reads the whole last-layer cache of every stream
+ *     every step (split-K GEMV over C_L*H*W). */
+typedef enum { RN_HEAD_TILES = 0, RN_HEAD_FULL = 1 } rn_head_mode;
+
 /* One conv layer (OIHW weights).  Supported: k = 3, stride = 1, pad = 1. */
 typedef struct {
     int32_t cin, cout, k, stride, pad;
@@ -70,6 +81,7 @@ typedef struct {
     int32_t max_streams;          /* cache slots, 1..65535 */
     rn_dtype act_dtype;           /* RN_F32, or RN_BF16 (bf16 weights and activations,
                                      fp32 accumulation, fp32 logits) */
+    rn_head_mode head_mode;       /* RN_HEAD_TILES (default, zero) or RN_HEAD_FULL */
 } rn_config;
 
 typedef struct {                  /* HOST pointers, float32, read during create only */
@@ -115,8 +127,12 @@ rn_status reuse_net_step(reuse_net *net, int32_t n, const int32_t *dev_stream_id
                          const int32_t *dev_boxes, const int32_t *dev_box_off,
                          float *dev_logits, void *hip_stream);
 
-/* Dense recompute of every layer for n streams (the comparison path): as a
- * step on which every pixel changed.  Leaves the slots primed. */
+/* Dense recompute of every layer for n streams (the comparison path): the
+ * frames are copied into the input caches and every tile of every layer is
+ * recomputed, without change detection or work lists.  Gives the same bits as
+ * a step on which every pixel changed, and leaves the slots primed.  The
+ * change masks of the slots are left as they were; reuse_net_get_worklist
+ * reports RN_ESTATE until the next step. */
 rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *dev_stream_ids,
                          const void *dev_frames, rn_dtype frame_dtype, float *dev_logits,
                          void *hip_stream);

@@ -9,6 +9,8 @@ from .binding import (  # noqa: F401
     LIB_PATH,
     RN_BF16,
     RN_F32,
+    RN_HEAD_FULL,
+    RN_HEAD_TILES,
     RN_U8,
     ReuseNet,
     ReuseNetError,

@@ -20,6 +20,7 @@ RN_MAX_CONV = 8
 RN_PHASES = 5
 RN_OK, RN_EINVAL, RN_EUNSUPPORTED, RN_ENOSPACE, RN_EHIP, RN_ESTATE = 0, -1, -2, -3, -4, -5
 RN_F32, RN_BF16, RN_U8 = 0, 1, 2
+RN_HEAD_TILES, RN_HEAD_FULL = 0, 1
 PHASES = ("masks", "compact", "conv1", "convN", "head")
 STATUS_NAMES = {0: "RN_OK", -1: "RN_EINVAL", -2: "RN_EUNSUPPORTED", -3: "RN_ENOSPACE",
                 -4: "RN_EHIP", -5: "RN_ESTATE"}
@@ -44,7 +45,8 @@ class rn_config(ctypes.Structure):
                 ("stack", ctypes.c_int32), ("n_conv", ctypes.c_int32),
                 ("conv", ctypes.POINTER(rn_conv_spec)), ("n_out", ctypes.c_int32),
                 ("tile_h", ctypes.c_int32), ("tile_w", ctypes.c_int32),
-                ("max_streams", ctypes.c_int32), ("act_dtype", ctypes.c_int)]
+                ("max_streams", ctypes.c_int32), ("act_dtype", ctypes.c_int),
+                ("head_mode", ctypes.c_int)]
 
 
 class rn_weights(ctypes.Structure):
@@ -217,7 +219,7 @@ class ReuseNet:
 
     def __init__(self, in_c: int, h: int, w: int, convs: Sequence[int], n_out: int,
                  max_streams: int, weights, act_dtype: str = "f32", stack: int = 1,
-                 device="cuda", tile: int = 4):
+                 device="cuda", tile: int = 4, head: str = "tiles"):
         import torch
         self.torch = torch
         self.device = torch.device(device)
@@ -232,7 +234,8 @@ class ReuseNet:
         self.specs = specs
         self._spec_arr = (rn_conv_spec * len(specs))(*[rn_conv_spec(*s) for s in specs])
         self.cfg = rn_config(in_c, h, w, stack, len(specs), self._spec_arr, n_out, tile, tile,
-                             max_streams, _dtype_code(act_dtype))
+                             max_streams, _dtype_code(act_dtype),
+                             {"tiles": RN_HEAD_TILES, "full": RN_HEAD_FULL}[head])
         nbytes = reuse_net_workspace_bytes(self.cfg)
         if nbytes == 0:
             # Re-run create's validation to report why.

@@ -12,9 +12,17 @@
 // Cache layout ("tiled NHWC"): per slot [TH][TW][16][C], a tile's 16 pixels in
 // row-major order, channels innermost; one tile is 16 * C contiguous elements.
 //
-// Both kernels are persistent: the grid is sized to the chip and each block
-// walks the device-side work list until the device-side count is exhausted,
-// so no host synchronisation is needed to size a launch.
+// The kernels are persistent: the grid is sized to the chip and the blocks walk
+// the device-side work list until the device-side count is exhausted, so no
+// host synchronisation is needed to size a launch.  In dense mode (the
+// comparison path) they walk every tile of every stream instead of a list;
+// the arithmetic per tile is the same code, so a dense pass and a reuse pass
+// give the same bits.
+//
+// Tile-partial head (last layer only): the dense head is linear, so the logits
+// are a sum over tiles of each tile's own contribution.  The epilogue computes
+// that contribution for the tiles it recomputes and stores it per (stream,
+// tile); clean tiles keep theirs.  The head then only adds partials.
 #include "rn_internal.hpp"
 
 namespace rn {
@@ -22,12 +30,47 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-[[maybe_unused]] __device__ inline float bf16_round(float v) {
-    // Round to nearest even on the upper 16 bits (finite values; NaN kept NaN).
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7F800000u) == 0x7F800000u) return __uint_as_float((u | ((u & 0xFFFF) ? 0x00400000u : 0u)) & 0xFFFF0000u);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return __uint_as_float(u & 0xFFFF0000u);
+// Order this wave's LDS writes before its later LDS reads (and keep the
+// compiler from moving memory operations across).
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ inline float wave_sum(float v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+struct TileRef {
+    int slot, tile, ty, tx;
+};
+
+template <bool DENSE>
+__device__ inline TileRef decode(const ConvArgs &a, int t) {
+    TileRef r;
+    if constexpr (DENSE) {
+        const int ntiles = a.TH * a.TW;
+        const int i = t / ntiles;
+        r.tile = t - i * ntiles;
+        r.ty = r.tile / a.TW;
+        r.tx = r.tile - r.ty * a.TW;
+        r.slot = a.ids[i];
+    } else {
+        const uint32_t e = a.wl[t];
+        r.slot = a.ids[e >> 16];
+        r.ty = (e >> 8) & 255;
+        r.tx = e & 255;
+        r.tile = r.ty * a.TW + r.tx;
+    }
+    return r;
+}
+
+template <bool DENSE>
+__device__ inline int work_count(const ConvArgs &a) {
+    if constexpr (DENSE) return a.dense_n * a.TH * a.TW;
+    else return *a.cnt;
 }
 
 // ------------------------------------------------------------------ first layer
@@ -35,7 +78,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Direct conv for a few input channels (1, or 4 stacked frames): 9 * CIN FMAs
 // per output, too few for a matrix core to pay off; the layer is HBM-bound on
 // its output writes.  One wave per tile; weights and bias in LDS.
-template <int CIN, int COUT>
+template <int CIN, int COUT, bool DENSE>
 __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     __shared__ float s_w[CIN * 9 * COUT];
     __shared__ float s_b[COUT];
@@ -46,66 +89,56 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     __syncthreads();
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int cnt = *a.cnt;
+    const int cnt = work_count<DENSE>(a);
     const size_t HW = (size_t)a.H * a.W;
     const int cin1 = CIN / a.stack;               // channels per frame
     float *halo = s_halo[wave];
     const float *xin = static_cast<const float *>(a.in);
     float *outp = static_cast<float *>(a.out);
 
-    for (int base = blockIdx.x * 4; base < cnt; base += gridDim.x * 4) {
-        const int t = base + wave;
-        const bool valid = t < cnt;
-        int slot = 0, ty = 0, tx = 0;
-        if (valid) {
-            const uint32_t e = a.wl[t];
-            slot = a.ids[e >> 16];
-            ty = (e >> 8) & 255;
-            tx = e & 255;
-            int head = 0;
-            if (a.stack != 1) head = a.ring_head[slot];
-            for (int h = lane; h < CIN * 36; h += 64) {
-                const int c = h / 36, pos = h - c * 36;
-                const int hy = pos / 6, hx = pos - hy * 6;
-                const int y = ty * kTile - 1 + hy, x = tx * kTile - 1 + hx;
-                float v = 0.0f;
-                if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
-                    const float *plane;
-                    if (a.stack == 1) {
-                        plane = xin + ((size_t)slot * CIN + c) * HW;
-                    } else {
-                        // Channel c = frame j (oldest first) of the ring, channel c1 of it.
-                        const int j = c / cin1, c1 = c - j * cin1;
-                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
-                        plane = xin + (((size_t)slot * 4 + rp) * cin1 + c1) * HW;
-                    }
-                    v = plane[(size_t)y * a.W + x];
+    for (int t = blockIdx.x * 4 + wave; t < cnt; t += gridDim.x * 4) {
+        const TileRef r = decode<DENSE>(a, t);
+        int head = 0;
+        if (a.stack != 1) head = a.ring_head[r.slot];
+        for (int h = lane; h < CIN * 36; h += 64) {
+            const int c = h / 36, pos = h - c * 36;
+            const int hy = pos / 6, hx = pos - hy * 6;
+            const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+            float v = 0.0f;
+            if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
+                const float *plane;
+                if (a.stack == 1) {
+                    plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                } else {
+                    // Channel c = frame j (oldest first) of the ring, channel c1 of it.
+                    const int j = c / cin1, c1 = c - j * cin1;
+                    const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                    plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
                 }
-                halo[h] = v;
+                v = plane[(size_t)y * a.W + x];
             }
+            halo[h] = v;
         }
-        __syncthreads();
-        if (valid) {
-            float *dst = outp + (size_t)slot * a.out_stride + (size_t)(ty * a.TW + tx) * kTilePx * COUT;
-            for (int o = lane; o < kTilePx * COUT; o += 64) {
-                const int m = o / COUT, co = o - m * COUT;
-                const int py = m >> 2, px = m & 3;
-                float acc = 0.0f;
+        wave_sync();
+        float *dst = outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
+        for (int o = lane; o < kTilePx * COUT; o += 64) {
+            const int m = o / COUT, co = o - m * COUT;
+            const int py = m >> 2, px = m & 3;
+            float acc = 0.0f;
 #pragma unroll
-                for (int c = 0; c < CIN; ++c)
+            for (int c = 0; c < CIN; ++c)
 #pragma unroll
-                    for (int ky = 0; ky < 3; ++ky)
+                for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
-                        for (int kx = 0; kx < 3; ++kx)
-                            acc = fmaf(s_w[(c * 9 + ky * 3 + kx) * COUT + co],
-                                       halo[c * 36 + (py + ky) * 6 + px + kx], acc);
-                float v = acc + s_b[co];
-                v = v > 0.0f ? v : 0.0f;
-                if (ty * kTile + py >= a.H || tx * kTile + px >= a.W) v = 0.0f;
-                dst[o] = v;
-            }
+                    for (int kx = 0; kx < 3; ++kx)
+                        acc = fmaf(s_w[(c * 9 + ky * 3 + kx) * COUT + co],
+                                   halo[c * 36 + (py + ky) * 6 + px + kx], acc);
+            float v = acc + s_b[co];
+            v = v > 0.0f ? v : 0.0f;
+            if (r.ty * kTile + py >= a.H || r.tx * kTile + px >= a.W) v = 0.0f;
+            dst[o] = v;
         }
-        __syncthreads();
+        wave_sync();
     }
 }
 
@@ -119,157 +152,283 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
 // from the 6x6 x CIN halo in LDS (im2col is an address computation), and lane l
 // ends up holding tile row l / 16, columns i = 0..3, of channel l % 16 + 16 nb.
 // The weights are pre-packed in fragment order [kstep][nb][lane] so each B
-// read is one conflict-free 256-byte LDS row.  When all of them fit in LDS
-// (KPS = 9) they are loaded once per persistent block; otherwise they are
-// streamed in stages of KPS kernel positions per tile group.
-template <int CIN, int COUT, int KPS, int WAVES>
-struct MfmaCfg {
+// read is one conflict-free 256-byte LDS row.
+template <int CIN, int COUT>
+struct Mfma {
     static constexpr int NB = COUT / 16;
-    static constexpr int CS = CIN + 1;       // halo channel stride in LDS (odd: spreads banks)
-    static constexpr int KSP = CIN / 4;      // k-steps per kernel position
-    static constexpr int NST = (9 + KPS - 1) / KPS;
-    static constexpr int WST = KPS * CIN * COUT;
-    static constexpr size_t lds_bytes = (size_t)(WST + WAVES * 36 * CS) * sizeof(float);
+    static constexpr int CS = CIN + 1;        // halo channel stride in LDS (odd: spreads banks)
+    static constexpr int KSP = CIN / 4;       // k-steps per kernel position
+    static constexpr int HALO = 36 * CS;      // floats of one halo in LDS
+    static constexpr int SR = COUT + 4;       // row stride of the output staging area
+    static constexpr int HV = (36 * KSP + 63) / 64;   // 16-byte halo loads per lane
+    static constexpr int WTOT = 9 * CIN * COUT;
+    static_assert(16 * SR <= HALO, "output staging must fit in the halo area");
+    static_assert(COUT % 16 == 0 && CIN % 4 == 0, "MFMA tiling");
 };
 
-template <int CIN, int COUT, int KPS, int WAVES>
-__global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_f32(ConvArgs a) {
-    using C = MfmaCfg<CIN, COUT, KPS, WAVES>;
-    constexpr int NB = C::NB, CS = C::CS, KSP = C::KSP, NST = C::NST, WST = C::WST;
-    constexpr int WTOT = 9 * CIN * COUT;
-    extern __shared__ float smem[];
-    __shared__ float s_bias[COUT];
-    float *s_w = smem;
-    float *s_halo = smem + WST;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int cnt = *a.cnt;
-    const int ngroups = (cnt + WAVES - 1) / WAVES;
-    if ((int)blockIdx.x >= ngroups) return;       // uniform per block
-    const float *wg = static_cast<const float *>(a.w);
-    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
-    if constexpr (NST == 1) {
-        for (int j = tid; j < WTOT / 4; j += blockDim.x)
-            reinterpret_cast<float4 *>(s_w)[j] = reinterpret_cast<const float4 *>(wg)[j];
+// Global -> registers: the halo of one tile, 16 bytes per lane per load.
+template <int CIN, int COUT>
+__device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *regs, int lane) {
+    using M = Mfma<CIN, COUT>;
+    const float *src = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
+#pragma unroll
+    for (int j = 0; j < M::HV; ++j) {
+        const int h = lane + 64 * j;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (h < 36 * M::KSP) {
+            const int pos = h / M::KSP, c4 = h - pos * M::KSP;
+            const int hy = pos / 6, hx = pos - hy * 6;
+            const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+            if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+                v = *reinterpret_cast<const float4 *>(
+                    src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
+                    c4 * 4);
+        }
+        regs[j] = v;
     }
+}
+
+template <int CIN, int COUT>
+__device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
+    using M = Mfma<CIN, COUT>;
+#pragma unroll
+    for (int j = 0; j < M::HV; ++j) {
+        const int h = lane + 64 * j;
+        if (h < 36 * M::KSP) {
+            const int pos = h / M::KSP, c4 = h - pos * M::KSP;
+            float *d = halo + pos * M::CS + c4 * 4;
+            d[0] = regs[j].x;
+            d[1] = regs[j].y;
+            d[2] = regs[j].z;
+            d[3] = regs[j].w;
+        }
+    }
+}
+
+// acc += A(halo, kernel positions [k0, k0 + nk)) x B(weights in LDS from kernel position k0).
+template <int CIN, int COUT, int NK>
+__device__ inline void mfma_positions(floatx4 *acc, const float *halo, const float *s_w, int k0, int lane) {
+    using M = Mfma<CIN, COUT>;
     const int mrow = lane & 15, kq = lane >> 4;
     const int py = mrow >> 2, px = mrow & 3;
-    float *my_halo = s_halo + wave * 36 * CS;
-    const float *inp = static_cast<const float *>(a.in);
-    float *outp = static_cast<float *>(a.out);
-
-    for (int grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
-        const int t = grp * WAVES + wave;
-        const bool valid = t < cnt;
-        int slot = 0, ty = 0, tx = 0;
-        if (valid) {
-            const uint32_t e = a.wl[t];
-            slot = a.ids[e >> 16];
-            ty = (e >> 8) & 255;
-            tx = e & 255;
-            const float *src = inp + (size_t)slot * a.in_stride;
-            for (int h = lane; h < 36 * KSP; h += 64) {
-                const int pos = h / KSP, c4 = h - pos * KSP;
-                const int hy = pos / 6, hx = pos - hy * 6;
-                const int y = ty * kTile - 1 + hy, x = tx * kTile - 1 + hx;
-                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (y >= 0 && y < a.H && x >= 0 && x < a.W)
-                    v = *reinterpret_cast<const float4 *>(
-                        src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
-                        c4 * 4);
-                float *d = my_halo + pos * CS + c4 * 4;
-                d[0] = v.x;
-                d[1] = v.y;
-                d[2] = v.z;
-                d[3] = v.w;
-            }
-        }
-        floatx4 acc[NB];
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int kp = 0; kp < NK; ++kp) {
+        const int kpos = k0 + kp;
+        const int ky = kpos / 3, kx = kpos - ky * 3;
+        const float *arow = halo + ((py + ky) * 6 + px + kx) * M::CS + kq;
+        const float *brow = s_w + kp * M::KSP * M::NB * 64 + lane;
+#pragma unroll
+        for (int cs = 0; cs < M::KSP; ++cs) {
+            const float av = arow[cs * 4];
+#pragma unroll
+            for (int nb = 0; nb < M::NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, brow[(cs * M::NB + nb) * 64], acc[nb], 0, 0, 0);
+        }
+    }
+}
 
-        for (int st = 0; st < NST; ++st) {
-            if constexpr (NST > 1) {
-                __syncthreads();
-                const int n0 = st * WST;
-                const int nf = min(WST, WTOT - n0);
-                for (int j = tid; j < nf / 4; j += blockDim.x)
-                    reinterpret_cast<float4 *>(s_w)[j] = reinterpret_cast<const float4 *>(wg + n0)[j];
+// Bias, ReLU, zero outside the image, coalesced store of the 16 x COUT tile
+// through LDS (the halo area is free by now), and the tile's head partials.
+template <int CIN, int COUT>
+__device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *acc, const float *s_bias,
+                                float *stage, int lane) {
+    using M = Mfma<CIN, COUT>;
+    const int mrow = lane & 15, kq = lane >> 4;
+    const bool row_in = r.ty * kTile + kq < a.H;
+#pragma unroll
+    for (int nb = 0; nb < M::NB; ++nb) {
+        const float b = s_bias[nb * 16 + mrow];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v = acc[nb][i] + b;
+            v = v > 0.0f ? v : 0.0f;
+            if (!row_in || r.tx * kTile + i >= a.W) v = 0.0f;
+            acc[nb][i] = v;
+            stage[(kq * 4 + i) * M::SR + nb * 16 + mrow] = v;
+        }
+    }
+    wave_sync();
+    float4 *d4 = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
+                                            (size_t)r.tile * kTilePx * COUT);
+#pragma unroll
+    for (int j = 0; j < M::NB; ++j) {              // 16 * COUT / 4 float4 = 64 * NB
+        const int o4 = lane + 64 * j;
+        const int e = 4 * o4, m = e / COUT, n = e - m * COUT;
+        d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
+    }
+    if (a.n_out > 0) {
+        const int ntiles = a.TH * a.TW;
+        for (int o = 0; o < a.n_out; ++o) {
+            const float4 *w4 =
+                reinterpret_cast<const float4 *>(a.hw + ((size_t)o * ntiles + r.tile) * kTilePx * COUT) + lane;
+            float p = 0.f;
+#pragma unroll
+            for (int nb = 0; nb < M::NB; ++nb) {
+                const float4 w = w4[nb * 64];
+                p = fmaf(acc[nb][0], w.x, p);
+                p = fmaf(acc[nb][1], w.y, p);
+                p = fmaf(acc[nb][2], w.z, p);
+                p = fmaf(acc[nb][3], w.w, p);
             }
+            p = wave_sum(p);
+            if (lane == 0) a.hpart[((size_t)r.slot * ntiles + r.tile) * a.n_out + o] = p;
+        }
+    }
+    wave_sync();
+}
+
+// Weights resident in LDS for the whole persistent kernel; every wave walks its
+// own tiles independently and prefetches the next tile's halo into registers
+// while the matrix cores work on the current one.
+template <int CIN, int COUT, int WAVES>
+struct Resident {
+    static constexpr size_t lds_bytes =
+        (size_t)(Mfma<CIN, COUT>::WTOT + WAVES * Mfma<CIN, COUT>::HALO) * sizeof(float);
+};
+
+template <int CIN, int COUT, int WAVES, bool DENSE>
+__global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
+    using M = Mfma<CIN, COUT>;
+    extern __shared__ float smem[];
+    __shared__ float s_bias[COUT];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int cnt = work_count<DENSE>(a);
+    if ((int)blockIdx.x * WAVES >= cnt) return;          // uniform per block
+    float *s_w = smem;
+    float *halo = smem + M::WTOT + wave * M::HALO;
+    const float4 *wg = static_cast<const float4 *>(a.w);
+    for (int j = tid; j < M::WTOT / 4; j += blockDim.x) reinterpret_cast<float4 *>(s_w)[j] = wg[j];
+    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+    __syncthreads();
+
+    const int stride = gridDim.x * WAVES;
+    int t = blockIdx.x * WAVES + wave;
+    if (t >= cnt) return;                                 // no block barrier after this point
+    float4 pre[M::HV];
+    TileRef nxt = decode<DENSE>(a, t);
+    fetch_halo<CIN, COUT>(a, nxt, pre, lane);
+    for (; t < cnt; t += stride) {
+        const TileRef cur = nxt;
+        store_halo<CIN, COUT>(halo, pre, lane);
+        wave_sync();
+        if (t + stride < cnt) {
+            nxt = decode<DENSE>(a, t + stride);
+            fetch_halo<CIN, COUT>(a, nxt, pre, lane);
+        }
+        floatx4 acc[M::NB];
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
+        wave_sync();
+        epilogue<CIN, COUT>(a, cur, acc, s_bias, halo, lane);
+    }
+}
+
+// Weights too large for LDS: a block works on a group of 4 tiles (one per
+// wave) and streams the weights through LDS in stages of KPS kernel positions.
+template <int CIN, int COUT, int KPS>
+struct Staged {
+    static constexpr int NST = (9 + KPS - 1) / KPS;
+    static constexpr int WST = KPS * CIN * COUT;
+    static constexpr size_t lds_bytes = (size_t)(WST + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
+};
+
+template <int CIN, int COUT, int KPS, bool DENSE>
+__global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
+    using M = Mfma<CIN, COUT>;
+    using S = Staged<CIN, COUT, KPS>;
+    extern __shared__ float smem[];
+    __shared__ float s_bias[COUT];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int cnt = work_count<DENSE>(a);
+    const int ngroups = (cnt + 3) / 4;
+    if ((int)blockIdx.x >= ngroups) return;               // uniform per block
+    float *s_w = smem;
+    float *halo = smem + S::WST + wave * M::HALO;
+    const float *wg = static_cast<const float *>(a.w);
+    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+
+    for (int g = blockIdx.x; g < ngroups; g += gridDim.x) {
+        const int t = g * 4 + wave;
+        const bool valid = t < cnt;
+        TileRef r{0, 0, 0, 0};
+        if (valid) {
+            r = decode<DENSE>(a, t);
+            float4 regs[M::HV];
+            fetch_halo<CIN, COUT>(a, r, regs, lane);
+            store_halo<CIN, COUT>(halo, regs, lane);
+        }
+        floatx4 acc[M::NB];
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int st = 0; st < S::NST; ++st) {
+            __syncthreads();                               // previous stage fully consumed
+            const int n0 = st * S::WST;
+            const int nf = min(S::WST, M::WTOT - n0);
+            for (int j = tid; j < nf / 4; j += blockDim.x)
+                reinterpret_cast<float4 *>(s_w)[j] = reinterpret_cast<const float4 *>(wg + n0)[j];
             __syncthreads();
             if (valid) {
-#pragma unroll
-                for (int kp = 0; kp < KPS; ++kp) {
-                    const int kpos = st * KPS + kp;
-                    if (NST > 1 && kpos >= 9) break;
-                    const int ky = kpos / 3, kx = kpos - ky * 3;
-                    const float *arow = my_halo + ((py + ky) * 6 + px + kx) * CS + kq;
-                    const float *brow = s_w + kp * KSP * NB * 64 + lane;
-#pragma unroll
-                    for (int cs = 0; cs < KSP; ++cs) {
-                        const float av = arow[cs * 4];
-#pragma unroll
-                        for (int nb = 0; nb < NB; ++nb)
-                            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, brow[(cs * NB + nb) * 64],
-                                                                           acc[nb], 0, 0, 0);
-                    }
-                }
+                if (st * KPS + KPS <= 9) mfma_positions<CIN, COUT, KPS>(acc, halo, s_w, st * KPS, lane);
+                else mfma_positions<CIN, COUT, 9 % KPS>(acc, halo, s_w, st * KPS, lane);
             }
         }
         if (valid) {
-            float *dst = outp + (size_t)slot * a.out_stride + (size_t)(ty * a.TW + tx) * kTilePx * COUT;
-            const bool row_in = ty * kTile + kq < a.H;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                const int n = nb * 16 + mrow;
-                const float b = s_bias[n];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float v = acc[nb][i] + b;
-                    v = v > 0.0f ? v : 0.0f;
-                    if (!row_in || tx * kTile + i >= a.W) v = 0.0f;
-                    dst[(kq * 4 + i) * COUT + n] = v;
-                }
-            }
+            wave_sync();
+            epilogue<CIN, COUT>(a, r, acc, s_bias, halo, lane);
         }
-        __syncthreads();
     }
 }
 
 // ------------------------------------------------------------------ dispatch
 
+constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // 160 KiB per CU, less the static arrays
+
+template <int CIN, int COUT>
+constexpr bool use_resident() { return Resident<CIN, COUT, 8>::lds_bytes <= kLdsBudget; }
+
 template <int CIN, int COUT>
 constexpr int pick_kps() {
-    // Largest stage (9, 3 or 1 kernel positions) that fits 160 KiB of LDS
-    // next to the halos of 4 waves.
-    return MfmaCfg<CIN, COUT, 9, 4>::lds_bytes <= 160 * 1024 - 2048   ? 9
-           : MfmaCfg<CIN, COUT, 3, 4>::lds_bytes <= 160 * 1024 - 2048 ? 3
-                                                                      : 1;
+    return Staged<CIN, COUT, 3>::lds_bytes <= kLdsBudget ? 3 : 1;
 }
 
-template <int CIN, int COUT>
-hipError_t run_mfma(const ConvArgs &a, int grid, hipStream_t s) {
-    constexpr int KPS = pick_kps<CIN, COUT>();
-    constexpr size_t lds = MfmaCfg<CIN, COUT, KPS, 4>::lds_bytes;
-    auto kern = k_conv_mfma_f32<CIN, COUT, KPS, 4>;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        attr_set = true;
+template <typename K>
+hipError_t set_lds(K kern, size_t lds) {
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)lds);
+}
+
+template <int CIN, int COUT, bool DENSE>
+hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
+    const int total_max = a.max_tiles;
+    if constexpr (use_resident<CIN, COUT>()) {
+        constexpr size_t lds = Resident<CIN, COUT, 8>::lds_bytes;
+        auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE>;
+        static hipError_t attr = set_lds(kern, lds);
+        if (attr != hipSuccess) return attr;
+        const int grid = std::max(1, std::min(cus, (total_max + 7) / 8));
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, a);
+    } else {
+        constexpr int KPS = pick_kps<CIN, COUT>();
+        constexpr size_t lds = Staged<CIN, COUT, KPS>::lds_bytes;
+        auto kern = k_conv_mfma_staged<CIN, COUT, KPS, DENSE>;
+        static hipError_t attr = set_lds(kern, lds);
+        if (attr != hipSuccess) return attr;
+        const int grid = std::max(1, std::min(cus, (total_max + 3) / 4));
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
     }
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
     return hipGetLastError();
 }
 
-template <int CIN, int COUT>
-hipError_t run_first(const ConvArgs &a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT>), dim3(grid), dim3(256), 0, s, a);
+template <int CIN, int COUT, bool DENSE>
+hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
+    const int total_max = a.max_tiles;
+    const int grid = std::max(1, std::min(cus * 8, (total_max + 3) / 4));
+    hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-#define RN_MFMA_SHAPES(X) X(20, 40) X(40, 80) X(80, 160) X(64, 128) X(128, 128)
+#define RN_MFMA_SHAPES(X) X(40, 80) X(80, 160) X(64, 128) X(128, 128)
 #define RN_FIRST_SHAPES(X) X(1, 20) X(1, 40) X(1, 64) X(1, 80) X(4, 20) X(4, 40) X(4, 64) X(4, 80)
 
 }  // namespace
@@ -290,17 +449,25 @@ bool conv_first_supported(int cin, int cout, rn_dtype dt) {
     return false;
 }
 
-hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s) {
+// cus: compute units of the device; the persistent grid is at most one block
+// (resident or staged MFMA kernel) or eight blocks (first layer) per CU.
+hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s) {
     (void)dt;
-#define X(ci, co) if (a.cin == ci && a.cout == co) return run_mfma<ci, co>(a, grid, s);
+    const bool dense = a.wl == nullptr;
+#define X(ci, co)                                                                          \
+    if (a.cin == ci && a.cout == co)                                                       \
+        return dense ? run_mfma<ci, co, true>(a, cus, s) : run_mfma<ci, co, false>(a, cus, s);
     RN_MFMA_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s) {
+hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s) {
     (void)dt;
-#define X(ci, co) if (a.cin == ci && a.cout == co) return run_first<ci, co>(a, grid, s);
+    const bool dense = a.wl == nullptr;
+#define X(ci, co)                                                                          \
+    if (a.cin == ci && a.cout == co)                                                       \
+        return dense ? run_first<ci, co, true>(a, cus, s) : run_first<ci, co, false>(a, cus, s);
     RN_FIRST_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
@@ -335,6 +502,27 @@ void pack_conv_mfma(const float *oihw, int cin, int cout, rn_dtype dt, void *dst
                 const int kpos = k / cin, ci = k - kpos * cin;
                 d[((size_t)ks * nb_n + nb) * 64 + l] = oihw[((size_t)n * cin + ci) * 9 + kpos];
             }
+}
+
+size_t tile_head_w_elems(int ntiles, int cout, int n_out) { return (size_t)n_out * ntiles * kTilePx * cout; }
+
+void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst) {
+    // [o][tile][nb][lane][i]: the weight of the output the MFMA epilogue holds
+    // in lane `lane`, register i of block nb: channel nb * 16 + lane % 16, tile
+    // row lane / 16, tile column i.  Zero outside the image.
+    const int NB = C / 16, ntiles = TH * TW;
+    for (int o = 0; o < n_out; ++o)
+        for (int t = 0; t < ntiles; ++t) {
+            const int ty = t / TW, tx = t % TW;
+            for (int nb = 0; nb < NB; ++nb)
+                for (int l = 0; l < 64; ++l)
+                    for (int i = 0; i < 4; ++i) {
+                        const int c = nb * 16 + l % 16, y = ty * kTile + l / 16, x = tx * kTile + i;
+                        const size_t di = ((((size_t)o * ntiles + t) * NB + nb) * 64 + l) * 4 + i;
+                        dst[di] = (y < H && x < W) ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x]
+                                                   : 0.f;
+                    }
+        }
 }
 
 }  // namespace rn

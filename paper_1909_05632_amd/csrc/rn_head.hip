@@ -83,13 +83,32 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_f32(HeadArgs a) {
     }
 }
 
-__global__ void k_head_reduce(HeadArgs a) {
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+// One wave per (stream, logit): lanes add the split partials, then a fixed
+// butterfly adds the lanes.
+__global__ __launch_bounds__(kThreads) void k_head_reduce(HeadArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int j = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     if (j >= a.n * a.n_out) return;
     const int o = j % a.n_out;
     float v = 0.f;
-    for (int s = 0; s < a.nsplit; ++s) v += a.part[(size_t)s * a.n * a.n_out + j];
-    a.logits[j] = v + a.bias[o];
+    for (int s = lane; s < a.nsplit; s += 64) v += a.part[(size_t)s * a.n * a.n_out + j];
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) a.logits[j] = v + a.bias[o];
+}
+
+// Tile-partial head: logits[i][o] = bd[o] + sum over tiles of the cached
+// per-tile partials of stream i, added in a fixed order (lane-strided tiles,
+// then a fixed butterfly).  Wave w of the block handles logits o = w, w+4, ...
+__global__ __launch_bounds__(kThreads) void k_tile_head(TileHeadArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = blockIdx.x;
+    const float *P = a.hpart + (size_t)a.ids[i] * a.ntiles * a.n_out;
+    for (int o = wave; o < a.n_out; o += kThreads / 64) {
+        float v = 0.f;
+        for (int t = lane; t < a.ntiles; t += 64) v += P[(size_t)t * a.n_out + o];
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0) a.logits[(size_t)i * a.n_out + o] = v + a.bias[o];
+    }
 }
 
 // Generic head for any n_out (<= kHeadMaxOut): 8 outputs per pass over a_L.
@@ -159,7 +178,12 @@ hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int tot = a.n * a.n_out;
-    hipLaunchKernelGGL(k_head_reduce, dim3((tot + 255) / 256), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_head_reduce, dim3((tot + 3) / 4), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(k_tile_head, dim3(a.n), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -31,12 +31,13 @@ struct Plan {
     int C[RN_MAX_CONV + 1] = {0};          // channels per layer (0 = conv1 input)
     int radius[RN_MAX_CONV] = {0};         // change growth per layer, (k - 1) / 2
     size_t K = 0;                          // head input elements per slot (tiled)
+    int head_mode = RN_HEAD_TILES;
     int head_sg = 8;
     size_t part_elems = 0;
     // byte offsets into the workspace
     size_t o_lut, o_xin, o_ring, o_dring, o_primed, o_ids, o_act[RN_MAX_CONV + 1], o_w[RN_MAX_CONV],
         o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile,
-        o_wl[RN_MAX_CONV + 1], o_cnt, o_part;
+        o_wl[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
     size_t act_stride[RN_MAX_CONV + 1] = {0};   // elements per slot
     size_t total = 0;
@@ -79,6 +80,7 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     if (cfg->in_w % 4 != 0) return fail(RN_EUNSUPPORTED, "in_w must be a multiple of 4");
     if (cfg->stack == 4 && cfg->in_c != 1) return fail(RN_EUNSUPPORTED, "stack = 4 needs in_c = 1");
     if (cfg->act_dtype != RN_F32) return fail(RN_EUNSUPPORTED, "bf16 activations are not implemented yet");
+    if (cfg->head_mode != RN_HEAD_TILES && cfg->head_mode != RN_HEAD_FULL) return fail(RN_EINVAL, "bad head_mode");
     p->L = cfg->n_conv;
     p->H = cfg->in_h;
     p->W = cfg->in_w;
@@ -105,6 +107,8 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
         if (!conv_mfma_supported(p->C[l - 1], p->C[l], p->dt))
             return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" + std::to_string(p->C[l]));
     p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
+    // The tile-partial head lives in the epilogue of an MFMA layer.
+    p->head_mode = (cfg->head_mode == RN_HEAD_TILES && p->L >= 2) ? RN_HEAD_TILES : RN_HEAD_FULL;
     p->head_sg = head_streams_per_block(p->N);
     size_t part = 0;
     for (int n = 1; n <= p->S; ++n) {
@@ -149,7 +153,10 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_ntile = take(S * (p->L + 1) * 4);
     for (int l = 1; l <= p->L; ++l) p->o_wl[l] = take(S * p->ntiles * 4);
     p->o_cnt = take((RN_MAX_CONV + 1) * 4);
-    p->o_part = take(p->part_elems * 4);
+    const bool tiles_head = p->head_mode == RN_HEAD_TILES;
+    p->o_part = take(tiles_head ? 0 : p->part_elems * 4);
+    p->o_hw = take(tiles_head ? tile_head_w_elems(p->ntiles, p->C[p->L], p->N) * 4 : 0);
+    p->o_hp = take(tiles_head ? S * p->ntiles * p->N * 4 : 0);
     p->total = off;
     return RN_OK;
 }
@@ -169,6 +176,7 @@ struct reuse_net {
     hipStream_t last_stream = nullptr;
     int last_n = 0;
     bool has_step = false;
+    bool last_was_full = false;
     bool prof = false;
     std::vector<hipEvent_t> pool;
     size_t pool_used = 0;
@@ -233,8 +241,69 @@ MaskGeom make_geom(reuse_net *net) {
     return g;
 }
 
+// Conv layers 1..L (list mode: the work lists; dense mode: every tile), then the head.
+hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const *wl, const int32_t *cnt,
+                      float *logits, hipStream_t s, bool dense) {
+    const Plan &p = net->p;
+    const bool tiles_head = p.head_mode == RN_HEAD_TILES;
+    hipError_t e = hipSuccess;
+    for (int l = 1; l <= p.L; ++l) {
+        ConvArgs cv{};
+        cv.wl = dense ? nullptr : wl[l];
+        cv.cnt = dense ? nullptr : cnt + l;
+        cv.ids = ids;
+        cv.in = l == 1 ? static_cast<const void *>(net->at<float>(p.o_xin)) : net->at<void>(p.o_act[l - 1]);
+        cv.out = net->at<void>(p.o_act[l]);
+        cv.w = net->at<void>(p.o_w[l - 1]);
+        cv.bias = net->at<float>(p.o_b[l - 1]);
+        cv.ring_head = net->at<int32_t>(p.o_ring);
+        cv.H = p.H;
+        cv.W = p.W;
+        cv.TH = p.TH;
+        cv.TW = p.TW;
+        cv.cin = p.C[l - 1];
+        cv.cout = p.C[l];
+        cv.stack = p.stack;
+        cv.in_stride = p.act_stride[l - 1];
+        cv.out_stride = p.act_stride[l];
+        cv.dense_n = dense ? n : 0;
+        cv.max_tiles = n * p.ntiles;
+        if (l == p.L && tiles_head) {
+            cv.n_out = p.N;
+            cv.hw = net->at<float>(p.o_hw);
+            cv.hpart = net->at<float>(p.o_hp);
+        }
+        if (l == 1) e = timed(net, RN_PHASE_CONV1, s, [&] { return launch_conv_first(cv, p.dt, net->cus, s); });
+        else e = timed(net, RN_PHASE_CONVN, s, [&] { return launch_conv_mfma(cv, p.dt, net->cus, s); });
+        if (e != hipSuccess) return e;
+    }
+    if (tiles_head) {
+        TileHeadArgs ta{};
+        ta.n = n;
+        ta.n_out = p.N;
+        ta.ntiles = p.ntiles;
+        ta.ids = ids;
+        ta.hpart = net->at<float>(p.o_hp);
+        ta.bias = net->at<float>(p.o_bd);
+        ta.logits = logits;
+        return timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_head(ta, s); });
+    }
+    HeadArgs ha{};
+    ha.n = n;
+    ha.n_out = p.N;
+    ha.ids = ids;
+    ha.act = net->at<void>(p.o_act[p.L]);
+    ha.w = net->at<void>(p.o_wd);
+    ha.bias = net->at<float>(p.o_bd);
+    ha.part = net->at<float>(p.o_part);
+    ha.logits = logits;
+    ha.K = p.K;
+    head_split(p, n, &ha.nsplit, &ha.chunk);
+    return timed(net, RN_PHASE_HEAD, s, [&] { return launch_head(ha, p.dt, s); });
+}
+
 rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void *frames, rn_dtype fdt,
-                   const int32_t *boxes, const int32_t *box_off, float *logits, void *stream, int force_all) {
+                   const int32_t *boxes, const int32_t *box_off, float *logits, void *stream) {
     if (!net) return RN_EINVAL;
     const Plan &p = net->p;
     if (n < 1 || n > p.S) return net->fail(RN_EINVAL, "n must be 1..max_streams");
@@ -252,9 +321,9 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     ma.ids = ids;
     ma.frames = frames;
     ma.frame_u8 = fdt == RN_U8;
-    ma.boxes = force_all ? nullptr : boxes;
+    ma.boxes = boxes;
     ma.box_off = box_off;
-    ma.force_all = force_all;
+    ma.force_all = 0;
     ma.lut = net->at<float>(p.o_lut);
     ma.xin = net->at<float>(p.o_xin);
     ma.ring_head = net->at<int32_t>(p.o_ring);
@@ -281,53 +350,53 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
 
-    const int max_tiles = n * p.ntiles;
-    for (int l = 1; l <= p.L; ++l) {
-        ConvArgs cv{};
-        cv.wl = ca.wl[l];
-        cv.cnt = ca.cnt + l;
-        cv.ids = ids;
-        cv.in = l == 1 ? static_cast<const void *>(ma.xin) : net->at<void>(p.o_act[l - 1]);
-        cv.out = net->at<void>(p.o_act[l]);
-        cv.w = net->at<void>(p.o_w[l - 1]);
-        cv.bias = net->at<float>(p.o_b[l - 1]);
-        cv.ring_head = ma.ring_head;
-        cv.H = p.H;
-        cv.W = p.W;
-        cv.TH = p.TH;
-        cv.TW = p.TW;
-        cv.cin = p.C[l - 1];
-        cv.cout = p.C[l];
-        cv.stack = p.stack;
-        cv.in_stride = p.act_stride[l - 1];
-        cv.out_stride = p.act_stride[l];
-        if (l == 1) {
-            const int grid = std::max(1, std::min(net->cus * 8, ceil_div(max_tiles, 4)));
-            e = timed(net, RN_PHASE_CONV1, s, [&] { return launch_conv_first(cv, p.dt, grid, s); });
-        } else {
-            const int grid = std::max(1, std::min(net->cus, ceil_div(max_tiles, 4)));
-            e = timed(net, RN_PHASE_CONVN, s, [&] { return launch_conv_mfma(cv, p.dt, grid, s); });
-        }
-        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv kernel: ") + hipGetErrorString(e));
-    }
-
-    HeadArgs ha{};
-    ha.n = n;
-    ha.n_out = p.N;
-    ha.ids = ids;
-    ha.act = net->at<void>(p.o_act[p.L]);
-    ha.w = net->at<void>(p.o_wd);
-    ha.bias = net->at<float>(p.o_bd);
-    ha.part = net->at<float>(p.o_part);
-    ha.logits = logits;
-    ha.K = p.K;
-    head_split(p, n, &ha.nsplit, &ha.chunk);
-    e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_head(ha, p.dt, s); });
-    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head kernel: ") + hipGetErrorString(e));
-
+    e = run_layers(net, n, ids, ca.wl, ca.cnt, logits, s, false);
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));
     net->last_stream = s;
     net->last_n = n;
     net->has_step = true;
+    net->last_was_full = false;
+    net->err.clear();
+    return RN_OK;
+}
+
+rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void *frames, rn_dtype fdt,
+                   float *logits, void *stream) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (n < 1 || n > p.S) return net->fail(RN_EINVAL, "n must be 1..max_streams");
+    if (!frames) return net->fail(RN_EINVAL, "frames are NULL");
+    if (!logits) return net->fail(RN_EINVAL, "logits are NULL");
+    if (fdt != RN_F32 && fdt != RN_U8) return net->fail(RN_EINVAL, "frame dtype must be F32 or U8");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int32_t *ids = ids_in ? ids_in : net->at<int32_t>(p.o_ids);
+    PrimeArgs pa{};
+    pa.n = n;
+    pa.L = p.L;
+    pa.cin = p.in_c;
+    pa.stack = p.stack;
+    pa.H = p.H;
+    pa.W = p.W;
+    pa.ntiles = p.ntiles;
+    pa.ids = ids;
+    pa.frames = frames;
+    pa.frame_u8 = fdt == RN_U8;
+    pa.lut = net->at<float>(p.o_lut);
+    pa.xin = net->at<float>(p.o_xin);
+    pa.ring_head = net->at<int32_t>(p.o_ring);
+    pa.dring = net->at<uint64_t>(p.o_dring);
+    pa.primed = net->at<int32_t>(p.o_primed);
+    pa.nchg = net->at<int32_t>(p.o_nchg);
+    pa.ntile = net->at<int32_t>(p.o_ntile);
+    pa.dring_words = p.stack == 4 ? (size_t)4 * p.H * p.WW : 0;
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_prime(pa, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("prime kernel: ") + hipGetErrorString(e));
+    e = run_layers(net, n, ids, nullptr, nullptr, logits, s, true);
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));
+    net->last_stream = s;
+    net->last_n = n;
+    net->has_step = true;
+    net->last_was_full = true;
     net->err.clear();
     return RN_OK;
 }
@@ -422,6 +491,12 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
         up(p.o_b[l], w->conv_b[l], (size_t)p.C[l + 1] * 4);
     }
     up(p.o_wd, wd.data(), wd.size() * 4);
+    std::vector<float> hw;
+    if (p.head_mode == RN_HEAD_TILES) {
+        hw.assign(tile_head_w_elems(p.ntiles, CL, p.N), 0.f);
+        pack_tile_head(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hw.data());
+        up(p.o_hw, hw.data(), hw.size() * 4);
+    }
     up(p.o_bd, w->dense_b, (size_t)p.N * 4);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
@@ -435,12 +510,12 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
 
 rn_status reuse_net_step(reuse_net *net, int32_t n, const int32_t *ids, const void *frames, rn_dtype fdt,
                          const int32_t *boxes, const int32_t *box_off, float *logits, void *stream) {
-    return run_step(net, n, ids, frames, fdt, boxes, box_off, logits, stream, 0);
+    return run_step(net, n, ids, frames, fdt, boxes, box_off, logits, stream);
 }
 
 rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *ids, const void *frames, rn_dtype fdt,
                          float *logits, void *stream) {
-    return run_step(net, n, ids, frames, fdt, nullptr, nullptr, logits, stream, 1);
+    return run_full(net, n, ids, frames, fdt, logits, stream);
 }
 
 rn_status reuse_net_reset(reuse_net *net, int32_t sid) {
@@ -484,6 +559,7 @@ rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, s
     if (!net) return RN_EINVAL;
     const Plan &p = net->p;
     if (layer < 1 || layer > p.L || !count) return net->fail(RN_EINVAL, "bad layer or count pointer");
+    if (net->last_was_full) return net->fail(RN_ESTATE, "the last call was reuse_net_full: no work list");
     int32_t c = 0;
     rn_status st = copy_out(net, &c, net->at<int32_t>(p.o_cnt) + layer, 4);
     if (st != RN_OK) return st;
@@ -543,6 +619,10 @@ rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out) {
         const int64_t per_px = (int64_t)9 * p.C[l - 1] * p.C[l];
         dense += (int64_t)n * p.H * p.W * per_px;
         issued += out->dirty_tiles[l] * kTilePx * per_px;
+        if (net->last_was_full) {
+            useful += (int64_t)n * p.H * p.W * per_px;
+            continue;
+        }
         int32_t c = 0;
         std::vector<uint32_t> wl((size_t)n * p.ntiles);
         st = reuse_net_get_worklist(net, l, wl.data(), wl.size(), &c);

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include <string>
 #include <vector>
 
@@ -69,6 +71,38 @@ struct ConvArgs {
     int cin, cout;
     int stack;
     size_t in_stride, out_stride; // elements per slot
+    int dense_n;                  // dense mode (wl == NULL): every tile of streams 0..dense_n-1
+    int max_tiles;                // host bound on the tiles of this launch (sizes the grid)
+    // Tile-partial dense head fused into the last layer's epilogue (n_out > 0):
+    // hpart[slot][tile][o] = sum over the tile's outputs of hw * activation.
+    int n_out;
+    const float *hw;              // [n_out][TH*TW][16*cout] in the epilogue's fragment order
+    float *hpart;                 // [S][TH*TW][n_out]
+};
+
+// Dense path: copy the frames into the input cache and mark the slots primed.
+struct PrimeArgs {
+    int n, L, cin, stack, H, W, ntiles;
+    const int32_t *ids;
+    const void *frames;
+    int frame_u8;
+    const float *lut;
+    float *xin;
+    int32_t *ring_head;
+    uint64_t *dring;
+    int32_t *primed;
+    int32_t *nchg;
+    int32_t *ntile;
+    size_t dring_words;           // per slot (stack = 4)
+};
+
+// Sum of the per-tile head partials: logits[i][o] = bd[o] + sum_t hpart[ids[i]][t][o].
+struct TileHeadArgs {
+    int n, n_out, ntiles;
+    const int32_t *ids;
+    const float *hpart;
+    const float *bias;
+    float *logits;
 };
 
 struct HeadArgs {
@@ -86,6 +120,10 @@ struct HeadArgs {
 
 // Launchers (each returns the hipGetLastError of its launch).
 hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s);
+hipError_t launch_prime(const PrimeArgs &a, hipStream_t s);
+hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s);
+size_t tile_head_w_elems(int ntiles, int cout, int n_out);
+void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s);
 hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
 hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);

@@ -229,6 +229,42 @@ __global__ __launch_bounds__(kThreads) void k_masks(MaskGeom g, MaskArgs a) {
     }
 }
 
+// Dense path: copy every pixel of the frames into the input cache (all four
+// ring positions when stacking: before 4 frames exist, frame 0 repeats), mark
+// the slots primed and report every pixel and tile as recomputed.
+template <bool U8>
+__global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
+    const int i = blockIdx.x;
+    const int slot = a.ids[i];
+    const size_t HW = (size_t)a.H * a.W;
+    const int C = a.cin;
+    const size_t fbase = (size_t)i * C * HW;
+    const int n4 = (int)(HW / 4);
+    for (int q = blockIdx.y * blockDim.x + threadIdx.x; q < n4; q += gridDim.y * blockDim.x) {
+        for (int c = 0; c < C; ++c) {
+            const float4 v = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, a.lut);
+            if (a.stack == 1) {
+                *reinterpret_cast<float4 *>(a.xin + (size_t)slot * C * HW + c * HW + 4 * (size_t)q) = v;
+            } else {
+                for (int r = 0; r < 4; ++r)
+                    *reinterpret_cast<float4 *>(a.xin + ((size_t)slot * 4 + r) * C * HW + c * HW +
+                                                4 * (size_t)q) = v;
+            }
+        }
+    }
+    if (a.stack != 1) {
+        uint64_t *ring = a.dring + (size_t)slot * a.dring_words;
+        for (size_t w = blockIdx.y * blockDim.x + threadIdx.x; w < a.dring_words; w += gridDim.y * blockDim.x)
+            ring[w] = 0ull;
+    }
+    if (blockIdx.y == 0 && threadIdx.x == 0) {
+        a.primed[slot] = 1;
+        if (a.stack != 1) a.ring_head[slot] = 0;
+        a.nchg[i] = (int)HW;
+        for (int l = 0; l <= a.L; ++l) a.ntile[(size_t)i * (a.L + 1) + l] = a.ntiles;
+    }
+}
+
 // Work lists: block (bx, l-1) writes the entries of streams [16 bx, 16 bx + 16)
 // of layer l at their exclusive-prefix offsets.  Counts come from the mask
 // kernel, so the order is fixed and no atomics are needed.
@@ -287,6 +323,15 @@ hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s) {
         hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kThreads), shm, s, g, a);
     else
         hipLaunchKernelGGL(k_masks<false>, dim3(a.n), dim3(kThreads), shm, s, g, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {
+    dim3 grid(a.n, 4);
+    if (a.frame_u8)
+        hipLaunchKernelGGL(k_prime<true>, grid, dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_prime<false>, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

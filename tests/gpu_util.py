@@ -14,10 +14,10 @@ def oracle_net(wl, bf16=False):
     return oracle.Net(wl.in_c, wl.h, wl.w, wl.conv_specs(), wl.n_out, 4, 4, bf16)
 
 
-def make_net(wl, streams, weights, act_dtype="f32"):
+def make_net(wl, streams, weights, act_dtype="f32", head="tiles"):
     from paper_1909_05632_amd import ReuseNet
     return ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, streams, weights, act_dtype=act_dtype,
-                    stack=wl.stack)
+                    stack=wl.stack, head=head)
 
 
 def oracle_d0(prev_x, cur_x, primed):

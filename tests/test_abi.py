@@ -31,11 +31,18 @@ def test_library_exports_every_declared_symbol():
 
 
 def _cfg(convs=((1, 40), (40, 80)), h=105, w=80, stack=1, n_out=6, tile=4, streams=8,
-         k=3, s=1, p=1, dtype=B.RN_F32, in_c=1):
+         k=3, s=1, p=1, dtype=B.RN_F32, in_c=1, head=B.RN_HEAD_TILES):
     specs = (B.rn_conv_spec * len(convs))(*[B.rn_conv_spec(ci, co, k, s, p) for ci, co in convs])
-    cfg = B.rn_config(in_c, h, w, stack, len(convs), specs, n_out, tile, tile, streams, dtype)
+    cfg = B.rn_config(in_c, h, w, stack, len(convs), specs, n_out, tile, tile, streams, dtype, head)
     cfg._keep = specs
     return cfg
+
+
+def test_head_modes_size_the_workspace():
+    tiles = B.reuse_net_workspace_bytes(_cfg(head=B.RN_HEAD_TILES))
+    full = B.reuse_net_workspace_bytes(_cfg(head=B.RN_HEAD_FULL))
+    assert tiles > 0 and full > 0 and tiles != full
+    assert B.reuse_net_workspace_bytes(_cfg(head=7)) == 0
 
 
 def test_workspace_bytes_valid_configs():
@@ -62,6 +69,7 @@ def test_workspace_bytes_valid_configs():
     dict(w=78),                       # width not a multiple of 4
     dict(k=5, p=2),                   # valid but unsupported kernel size
     dict(convs=((1, 40), (40, 72))),  # no MFMA kernel for this shape
+    dict(convs=((1, 20), (20, 40))),  # 40 output channels: not a multiple of 16
 ])
 def test_workspace_bytes_rejects_bad_configs(bad):
     assert B.reuse_net_workspace_bytes(_cfg(**bad)) == 0

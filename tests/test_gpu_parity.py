@@ -23,10 +23,10 @@ def torch():
 
 
 def _run_sequence(torch, wl, streams, frames, weights, slots=None, max_streams=None, u8=False,
-                  sample=None, mask_every=1, value_every=1, label=""):
+                  sample=None, mask_every=1, value_every=1, label="", head="tiles"):
     u8x, x = sprite_inputs(wl, range(streams), frames)
     S = max_streams or streams
-    net = make_net(wl, S, weights)
+    net = make_net(wl, S, weights, head=head)
     onet = oracle_net(wl)
     ids = None
     slots = np.arange(streams) if slots is None else np.asarray(slots)
@@ -70,6 +70,33 @@ def test_small_ragged_shapes(torch):
                             n_sprites=2, smin=2, smax=5, vmin=1, vmax=3)
         weights = synth.net_weights(wl, bias_std=0.1)
         _run_sequence(torch, wl, 3, 5, weights, label=f"{h}x{w}").close()
+
+
+def test_full_read_head_mode(torch):
+    # The split-K head that reads every stream's whole last-layer cache.
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _run_sequence(torch, wl, 10, 5, weights, sample=[0, 9], label="head=full", head="full").close()
+
+
+def test_head_modes_agree_and_dense_path_has_no_worklist(torch):
+    from paper_1909_05632_amd import ReuseNetError
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _, x = sprite_inputs(wl, range(6), 4)
+    dev = torch.from_numpy(x).cuda()
+    a, b = make_net(wl, 6, weights, head="tiles"), make_net(wl, 6, weights, head="full")
+    for t in range(4):
+        la = a.step(dev[t][:, None].contiguous()).cpu().numpy()
+        lb = b.step(dev[t][:, None].contiguous()).cpu().numpy()
+        assert np.abs(la - lb).max() <= 2 * ATOL_F32
+    a.full(dev[3][:, None].contiguous())
+    with pytest.raises(ReuseNetError, match="RN_ESTATE"):
+        a.worklist(1)
+    st = a.stats()
+    assert st["useful_mac"] == st["dense_mac"] and st["changed_px"] == 6 * wl.h * wl.w
+    a.close()
+    b.close()
 
 
 def test_unchanged_frame_gives_no_work_and_same_logits(torch):
