@@ -150,7 +150,7 @@ def tile_mask(d: np.ndarray, tile_h: int, tile_w: int) -> np.ndarray:
 
 
 def worklist(masks: np.ndarray) -> np.ndarray:
-    """uint8 [n][th][tw] -> uint32 entries s<<16 | ty<<8 | tx in (s, ty, tx) order."""
+    """uint8 [n][th][tw] -> uint32 entries s<<16 | ty<<8 | tx in (ty, tx, s) order."""
     masks = _u8(masks)
     n, th, tw = masks.shape
     out = np.empty(max(1, masks.size), np.uint32)

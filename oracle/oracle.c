@@ -154,12 +154,12 @@ void orc_tile_mask(int h, int w, const uint8_t *d, int tile_h, int tile_w, uint8
 }
 
 int orc_worklist(int n, int th, int tw, const uint8_t *masks, uint32_t *out) {
-    /* Every dirty tile of one layer, ordered by stream, then tile row, then
-     * tile column. */
+    /* Every dirty tile of one layer, ordered by tile row, then tile column,
+     * then stream: tiles at the same position are adjacent. */
     int cnt = 0;
-    for (int s = 0; s < n; ++s)
-        for (int ty = 0; ty < th; ++ty)
-            for (int tx = 0; tx < tw; ++tx)
+    for (int ty = 0; ty < th; ++ty)
+        for (int tx = 0; tx < tw; ++tx)
+            for (int s = 0; s < n; ++s)
                 if (masks[((size_t)s * th + ty) * tw + tx])
                     out[cnt++] = ((uint32_t)s << 16) | ((uint32_t)ty << 8) | (uint32_t)tx;
     return cnt;

@@ -77,8 +77,9 @@ void orc_dilate(int h, int w, const uint8_t *din, int k, int s, int p, uint8_t *
  * (local-area recompute, Sec. 3). */
 void orc_tile_mask(int h, int w, const uint8_t *d, int tile_h, int tile_w, uint8_t *m);
 
-/* Work list of one layer: every (stream, ty, tx) with m = 1, ascending, encoded
- * stream << 16 | ty << 8 | tx.  masks: [n][th][tw].  Returns the count. */
+/* Work list of one layer: every (stream, ty, tx) with m = 1, ordered by
+ * (ty, tx, stream) ascending, encoded stream << 16 | ty << 8 | tx.
+ * masks: [n][th][tw].  Returns the count. */
 int orc_worklist(int n, int th, int tw, const uint8_t *masks, uint32_t *out);
 
 /* One conv layer, full recompute: y = ReLU(fl32(b + sum w * x)).  bf16 != 0

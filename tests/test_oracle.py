@@ -210,12 +210,14 @@ def test_worklist_order_and_encoding(orc):
     rng = np.random.default_rng(6)
     masks = (rng.random((5, 27, 20)) < 0.1).astype(np.uint8)
     wl = orc.worklist(masks)
-    ref = [(s << 16) | (ty << 8) | tx for (s, ty, tx) in np.argwhere(masks)]
+    # Position-major: argwhere over the [ty][tx][s] transpose lists (ty, tx, s) ascending.
+    ref = [(s << 16) | (ty << 8) | tx for (ty, tx, s) in np.argwhere(masks.transpose(1, 2, 0))]
     assert wl.tolist() == ref
+    assert sorted(wl.tolist(), key=lambda e: ((e >> 8) & 255, e & 255, e >> 16)) == wl.tolist()
     assert orc.worklist(np.zeros((3, 4, 4), np.uint8)).size == 0
     full = orc.worklist(np.ones((2, 3, 2), np.uint8))
-    assert full.tolist() == [(s << 16) | (y << 8) | x for s in range(2) for y in range(3)
-                             for x in range(2)]
+    assert full.tolist() == [(s << 16) | (y << 8) | x for y in range(3) for x in range(2)
+                             for s in range(2)]
 
 
 # ------------------------------------------------------------------ conv / dense
