@@ -51,9 +51,9 @@ template <bool DENSE>
 __device__ inline TileRef decode(const ConvArgs &a, int t) {
     TileRef r;
     if constexpr (DENSE) {
-        const int ntiles = a.TH * a.TW;
-        const int i = t / ntiles;
-        r.tile = t - i * ntiles;
+        // Every tile of every stream, position-major like the work lists.
+        r.tile = t / a.dense_n;
+        const int i = t - r.tile * a.dense_n;
         r.ty = r.tile / a.TW;
         r.tx = r.tile - r.ty * a.TW;
         r.slot = a.ids[i];
@@ -71,6 +71,26 @@ template <bool DENSE>
 __device__ inline int work_count(const ConvArgs &a) {
     if constexpr (DENSE) return a.dense_n * a.TH * a.TW;
     else return *a.cnt;
+}
+
+// XCD-aware split of the work items [0, cnt): workgroups are dispatched round
+// robin over the chip's 8 XCDs (block b runs on XCD b % 8), each with its own
+// L2.  Item range [cnt x / 8, cnt (x + 1) / 8) goes to the blocks of XCD x, so
+// the tiles of neighbouring positions (same head weights, overlapping halos)
+// are served from one L2.  `units` work items per block per round.
+struct XcdRange {
+    int first, end, stride;
+};
+
+__device__ inline XcdRange xcd_range(int cnt, int units) {
+    constexpr int kXcd = 8;
+    const int x = blockIdx.x % kXcd, k = blockIdx.x / kXcd;
+    const int blocks_x = ((int)gridDim.x - x + kXcd - 1) / kXcd;
+    XcdRange r;
+    r.first = (int)((long long)cnt * x / kXcd) + k * units;
+    r.end = (int)((long long)cnt * (x + 1) / kXcd);
+    r.stride = blocks_x * units;
+    return r;
 }
 
 // ------------------------------------------------------------------ first layer
@@ -96,7 +116,8 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     const float *xin = static_cast<const float *>(a.in);
     float *outp = static_cast<float *>(a.out);
 
-    for (int t = blockIdx.x * 4 + wave; t < cnt; t += gridDim.x * 4) {
+    const XcdRange xr = xcd_range(cnt, 4);
+    for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
         const TileRef r = decode<DENSE>(a, t);
         int head = 0;
         if (a.stack != 1) head = a.ring_head[r.slot];
@@ -293,7 +314,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     __shared__ float s_bias[COUT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cnt = work_count<DENSE>(a);
-    if ((int)blockIdx.x * WAVES >= cnt) return;          // uniform per block
+    const XcdRange xr = xcd_range(cnt, WAVES);
+    if (xr.first >= xr.end) return;                       // uniform per block
     float *s_w = smem;
     float *halo = smem + M::WTOT + wave * M::HALO;
     const float4 *wg = static_cast<const float4 *>(a.w);
@@ -301,17 +323,17 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
     __syncthreads();
 
-    const int stride = gridDim.x * WAVES;
-    int t = blockIdx.x * WAVES + wave;
-    if (t >= cnt) return;                                 // no block barrier after this point
+    const int stride = xr.stride;
+    int t = xr.first + wave;
+    if (t >= xr.end) return;                              // no block barrier after this point
     float4 pre[M::HV];
     TileRef nxt = decode<DENSE>(a, t);
     fetch_halo<CIN, COUT>(a, nxt, pre, lane);
-    for (; t < cnt; t += stride) {
+    for (; t < xr.end; t += stride) {
         const TileRef cur = nxt;
         store_halo<CIN, COUT>(halo, pre, lane);
         wave_sync();
-        if (t + stride < cnt) {
+        if (t + stride < xr.end) {
             nxt = decode<DENSE>(a, t + stride);
             fetch_halo<CIN, COUT>(a, nxt, pre, lane);
         }
@@ -341,16 +363,16 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     __shared__ float s_bias[COUT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cnt = work_count<DENSE>(a);
-    const int ngroups = (cnt + 3) / 4;
-    if ((int)blockIdx.x >= ngroups) return;               // uniform per block
+    const XcdRange xr = xcd_range(cnt, 4);
+    if (xr.first >= xr.end) return;                       // uniform per block
     float *s_w = smem;
     float *halo = smem + S::WST + wave * M::HALO;
     const float *wg = static_cast<const float *>(a.w);
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
 
-    for (int g = blockIdx.x; g < ngroups; g += gridDim.x) {
-        const int t = g * 4 + wave;
-        const bool valid = t < cnt;
+    for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
+        const int t = g + wave;
+        const bool valid = t < xr.end;
         TileRef r{0, 0, 0, 0};
         if (valid) {
             r = decode<DENSE>(a, t);
@@ -392,6 +414,13 @@ constexpr int pick_kps() {
     return Staged<CIN, COUT, 3>::lds_bytes <= kLdsBudget ? 3 : 1;
 }
 
+// Persistent grid: at most `cap` blocks, no more than the work needs, and a
+// multiple of 8 so that every XCD segment of xcd_range has blocks.
+inline int persistent_grid(int cap, int need) {
+    int g = std::max(1, std::min(cap, need));
+    return (g + 7) / 8 * 8;
+}
+
 template <typename K>
 hipError_t set_lds(K kern, size_t lds) {
     return hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -406,7 +435,7 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
-        const int grid = std::max(1, std::min(cus, (total_max + 7) / 8));
+        const int grid = persistent_grid(cus, (total_max + 7) / 8);
         hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, a);
     } else {
         constexpr int KPS = pick_kps<CIN, COUT>();
@@ -414,7 +443,7 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         auto kern = k_conv_mfma_staged<CIN, COUT, KPS, DENSE>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
-        const int grid = std::max(1, std::min(cus, (total_max + 3) / 4));
+        const int grid = persistent_grid(cus, (total_max + 3) / 4);
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
     }
     return hipGetLastError();
@@ -423,7 +452,7 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
 template <int CIN, int COUT, bool DENSE>
 hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
     const int total_max = a.max_tiles;
-    const int grid = std::max(1, std::min(cus * 8, (total_max + 3) / 4));
+    const int grid = persistent_grid(cus * 8, (total_max + 3) / 4);
     hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }

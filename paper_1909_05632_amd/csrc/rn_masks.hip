@@ -5,13 +5,16 @@
 // a 3x3 stride-1 layer spreads a change by one pixel on each side.  Dirty
 // tiles (Sec. 3, local areas instead of one rectangle): a 4x4 cell of a
 // layer's grid is dirty iff it holds a dirty pixel.  The work list of a layer
-// is its dirty tiles in (batch index, tile row, tile column) order.
+// is its dirty tiles in (tile row, tile column, batch index) order.
+//
+// The work list of a layer is ordered by tile position first (see k_poswrite).
 //
 // Masks are bit rows: word (y * WW + x / 64), bit x % 64.  One workgroup owns
 // one stream: it diffs the frame against the cache with 16-byte loads, ORs the
 // change bits into a mask held in LDS, grows it layer by layer in LDS with
 // shifts and ORs, and reduces 4x4 cells to tile bits with one ballot per 64
 // tiles.  No global atomics; every output word has exactly one writer.
+// The lists are then built position-major from the tile masks.
 #include "rn_internal.hpp"
 
 namespace rn {
@@ -155,31 +158,52 @@ __global__ __launch_bounds__(kThreads) void k_masks(MaskGeom g, MaskArgs a) {
             }
         }
     } else {
-        // Diff, 4 pixels (one 16-byte load per plane) per thread per iteration.
+        // Diff, 4 pixels (one 16-byte load per plane) per thread per item; the
+        // loads of U items are issued before any compare so that many are in
+        // flight per thread.
+        constexpr int U = 8;
         const int n4 = (int)(HW / 4);
-        for (int q = threadIdx.x; q < n4; q += blockDim.x) {
-            uint32_t ch = primed ? 0u : 0xFu;
+        for (int q0 = threadIdx.x; q0 < n4; q0 += U * (int)blockDim.x) {
+            uint32_t ch[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) ch[u] = primed ? 0u : 0xFu;
             for (int c = 0; c < C; ++c) {
-                const float4 nv = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, lut);
-                const float4 ov = *reinterpret_cast<const float4 *>(prev + c * HW + 4 * (size_t)q);
-                const uint32_t d = (f32_bits(nv.x) != f32_bits(ov.x) ? 1u : 0u) |
-                                   (f32_bits(nv.y) != f32_bits(ov.y) ? 2u : 0u) |
-                                   (f32_bits(nv.z) != f32_bits(ov.z) ? 4u : 0u) |
-                                   (f32_bits(nv.w) != f32_bits(ov.w) ? 8u : 0u);
-                ch |= d;
-                if (g.stack != 1 || d != 0u || !primed)
-                    *reinterpret_cast<float4 *>(next + c * HW + 4 * (size_t)q) = nv;
-                if (g.stack != 1 && !primed) {
-                    // Priming a stacked input: every older frame is this frame.
-                    for (int r = 0; r < 4; ++r)
-                        *reinterpret_cast<float4 *>(a.xin + ((size_t)slot * 4 + r) * C * HW +
-                                                    c * HW + 4 * (size_t)q) = nv;
+                float4 nv[U], ov[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int q = q0 + u * (int)blockDim.x;
+                    if (q < n4) {
+                        nv[u] = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, lut);
+                        ov[u] = *reinterpret_cast<const float4 *>(prev + c * HW + 4 * (size_t)q);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int q = q0 + u * (int)blockDim.x;
+                    if (q >= n4) continue;
+                    const uint32_t d = (f32_bits(nv[u].x) != f32_bits(ov[u].x) ? 1u : 0u) |
+                                       (f32_bits(nv[u].y) != f32_bits(ov[u].y) ? 2u : 0u) |
+                                       (f32_bits(nv[u].z) != f32_bits(ov[u].z) ? 4u : 0u) |
+                                       (f32_bits(nv[u].w) != f32_bits(ov[u].w) ? 8u : 0u);
+                    ch[u] |= d;
+                    if (g.stack != 1 || d != 0u || !primed)
+                        *reinterpret_cast<float4 *>(next + c * HW + 4 * (size_t)q) = nv[u];
+                    if (g.stack != 1 && !primed) {
+                        // Priming a stacked input: every older frame is this frame.
+                        for (int r = 0; r < 4; ++r)
+                            *reinterpret_cast<float4 *>(a.xin + ((size_t)slot * 4 + r) * C * HW + c * HW +
+                                                        4 * (size_t)q) = nv[u];
+                    }
                 }
             }
-            if (ch) {
-                const int p = 4 * q, y = p / g.W, x = p - y * g.W;
-                atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
-                         (unsigned long long)ch << (x & 63));
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int q = q0 + u * (int)blockDim.x;
+                if (q < n4 && ch[u]) {
+                    const int p = 4 * q, y = p / g.W, x = p - y * g.W;
+                    atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
+                             (unsigned long long)ch[u] << (x & 63));
+                }
             }
         }
     }
@@ -265,53 +289,103 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
     }
 }
 
-// Work lists: block (bx, l-1) writes the entries of streams [16 bx, 16 bx + 16)
-// of layer l at their exclusive-prefix offsets.  Counts come from the mask
-// kernel, so the order is fixed and no atomics are needed.
-constexpr int kStreamsPerBlock = 16;
+// Work lists, position-major: the entries of layer l are its dirty tiles in
+// (ty, tx, batch index) order.  Two passes over the tile masks, each with one
+// block per (64-position word, layer):
+//   k_poscount: per position, the number of streams whose tile is dirty
+//               (64 ballots per chunk of 64 streams give the column counts);
+//   k_poswrite: each position's offset (prefix over all earlier positions),
+//               then every dirty (position, stream) at offset + rank.
+// Every count and entry has exactly one writer; no atomics on global memory.
+constexpr int kChunksPerPass = 16;          // 1024 streams per pass
 
-__global__ __launch_bounds__(kThreads) void k_compact(CompactArgs a) {
+__device__ inline uint64_t tile_word(const CompactArgs &a, int l, int i, int wd) {
+    return i < a.n ? a.tmask[l][(size_t)a.ids[i] * a.TMW + wd] : 0ull;
+}
+
+__global__ __launch_bounds__(kThreads) void k_poscount(CompactArgs a) {
+    __shared__ int s_cnt[64];
+    const int wd = blockIdx.x, l = blockIdx.y + 1;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (threadIdx.x < 64) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int nch = (a.n + 63) / 64;
+    for (int c = wave; c < nch; c += (int)(blockDim.x >> 6)) {
+        const uint64_t word = tile_word(a, l, 64 * c + lane, wd);
+        int mine = 0;
+        for (int j = 0; j < 64; ++j) {
+            const uint64_t b = __ballot((word >> j) & 1ull);
+            if (lane == j) mine = __popcll(b);
+        }
+        atomicAdd(&s_cnt[lane], mine);           // LDS, 4 waves
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int t = 64 * wd + threadIdx.x;
+        if (t < a.ntiles) a.poscnt[(size_t)l * a.ntiles + t] = s_cnt[threadIdx.x];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_poswrite(CompactArgs a) {
     __shared__ int red[kThreads / 64];
-    __shared__ int s_off[kStreamsPerBlock];
-    const int l = blockIdx.y + 1;
-    const int L1 = a.L + 1;
-    const int i0 = blockIdx.x * kStreamsPerBlock;
+    __shared__ int s_run[64];
+    __shared__ int s_base[kChunksPerPass][64];
+    __shared__ uint64_t s_bal[kChunksPerPass][64];
+    const int wd = blockIdx.x, l = blockIdx.y + 1;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int32_t *pc = a.poscnt + (size_t)l * a.ntiles;
     int pre = 0;
-    for (int j = threadIdx.x; j < i0; j += blockDim.x) pre += a.ntile[(size_t)j * L1 + l];
+    for (int t = threadIdx.x; t < 64 * wd; t += blockDim.x) pre += pc[t];
     pre = block_sum(pre, red);
-    if (blockIdx.x == 0) {
+    if (wd == 0) {
         int tot = 0;
-        for (int j = threadIdx.x; j < a.n; j += blockDim.x) tot += a.ntile[(size_t)j * L1 + l];
+        for (int t = threadIdx.x; t < a.ntiles; t += blockDim.x) tot += pc[t];
         tot = block_sum(tot, red);
         if (threadIdx.x == 0) a.cnt[l] = tot;
     }
     if (threadIdx.x == 0) {
-        int o = pre;
-        for (int s = 0; s < kStreamsPerBlock; ++s) {
-            s_off[s] = o;
-            if (i0 + s < a.n) o += a.ntile[(size_t)(i0 + s) * L1 + l];
+        int r = pre;
+        for (int j = 0; j < 64; ++j) {
+            s_run[j] = r;
+            const int t = 64 * wd + j;
+            if (t < a.ntiles) r += pc[t];
         }
     }
     __syncthreads();
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    for (int s = wave; s < kStreamsPerBlock; s += (int)(blockDim.x >> 6)) {
-        const int i = i0 + s;
-        if (i >= a.n) break;
-        const int slot = a.ids[i];
-        const uint64_t *tm = a.tmask[l] + (size_t)slot * a.TMW;
-        uint32_t *wl = a.wl[l];
-        int base = s_off[s];
-        for (int wd = 0; wd < a.TMW; ++wd) {
-            const uint64_t word = tm[wd];
-            if ((word >> lane) & 1ull) {
-                const int t = wd * 64 + lane;
-                const int ty = t / a.TW, tx = t - ty * a.TW;
-                wl[base + __popcll(word & below)] =
-                    ((uint32_t)i << 16) | ((uint32_t)ty << 8) | (uint32_t)tx;
+    const int cap = a.n * a.ntiles;
+    const int nch = (a.n + 63) / 64;
+    for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
+        const int nc = min(kChunksPerPass, nch - c0);
+        for (int cc = wave; cc < nc; cc += (int)(blockDim.x >> 6)) {
+            const uint64_t word = tile_word(a, l, 64 * (c0 + cc) + lane, wd);
+            for (int j = 0; j < 64; ++j) {
+                const uint64_t b = __ballot((word >> j) & 1ull);
+                if (lane == j) s_bal[cc][j] = b;
             }
-            base += __popcll(word);
         }
+        __syncthreads();
+        if (threadIdx.x < 64) {
+            int r = s_run[threadIdx.x];
+            for (int cc = 0; cc < nc; ++cc) {
+                s_base[cc][threadIdx.x] = r;
+                r += __popcll(s_bal[cc][threadIdx.x]);
+            }
+            s_run[threadIdx.x] = r;
+        }
+        __syncthreads();
+        for (int pi = wave; pi < nc * 64; pi += (int)(blockDim.x >> 6)) {
+            const int cc = pi >> 6, j = pi & 63;
+            const int t = 64 * wd + j;
+            const uint64_t b = s_bal[cc][j];
+            if (t < a.ntiles && ((b >> lane) & 1ull)) {
+                const int idx = s_base[cc][j] + __popcll(b & below);
+                const int i = 64 * (c0 + cc) + lane;
+                const int ty = t / a.TW, tx = t - ty * a.TW;
+                if (idx < cap) a.wl[l][idx] = ((uint32_t)i << 16) | ((uint32_t)ty << 8) | (uint32_t)tx;
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -336,8 +410,11 @@ hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s) {
-    dim3 grid((a.n + kStreamsPerBlock - 1) / kStreamsPerBlock, a.L);
-    hipLaunchKernelGGL(k_compact, grid, dim3(kThreads), 0, s, a);
+    dim3 grid(a.TMW, a.L);
+    hipLaunchKernelGGL(k_poscount, grid, dim3(kThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_poswrite, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -217,3 +217,43 @@ def test_full_size_256x64_atari_ds2(torch):
     frac = st["changed_px"] / (256 * 105 * 80)
     assert 0.001 < frac < 0.06, frac                       # ~1-3% changed pixels
     net.close()
+
+
+def test_stacked_frames_ring(torch):
+    # The last 4 frames are conv1's input channels (oldest first); each step
+    # passes only the newest frame and the library keeps the older three.  The
+    # oracle sees the plain 4-channel input, with frame 0 repeated at start-up.
+    wl = synth.WORKLOADS["stack4-512x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    n, F = 6, 10
+    u8 = synth.sprite_batch(wl, streams=range(n), frames=F)
+    x = synth.to_f32(u8)                                          # [F][n][H][W]
+    xs = np.stack([np.stack([synth.stacked_view(x[:, i], t) for i in range(n)]) for t in range(F)])
+    net = make_net(wl, n, weights)
+    onet = oracle_net(wl)
+    dev = torch.from_numpy(x).cuda()
+    for t in range(F):
+        logits = net.step(dev[t][:, None].contiguous()).cpu().numpy()
+        d0 = oracle_d0(xs[t - 1] if t else None, xs[t], primed=t > 0)
+        check_masks(net, onet, d0, np.arange(n), label=f"stack t={t}")
+        check_values(net, onet, weights, xs[t], np.arange(n), [0, n - 1], logits, label=f"stack t={t}")
+        assert np.array_equal(net.activation(2, 0)[0], x[t][2])   # newest frame in the ring
+    net.close()
+
+
+def test_three_layer_64_128_128_small_frames(torch):
+    # The full-resolution net's channels (1->64->128->128, 18 logits) on small
+    # ragged frames: weight-staged MFMA kernels for 64->128 and 128->128.
+    wl = synth.Workload(cid=77, streams=5, frames=6, h=42, w=32, convs=(64, 128, 128), n_out=18,
+                        n_sprites=3, smin=3, smax=6, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    for head in ("tiles", "full"):
+        _run_sequence(torch, wl, 5, 6, weights, label=f"3-layer head={head}", head=head).close()
+
+
+def test_fullres_210x160_three_layers(torch):
+    # Full-resolution frames with the 3-layer net: masks and lists every frame,
+    # logits of every stream and activations of stream 0 on the last frame.
+    wl = synth.WORKLOADS["fullres-1024x32"]
+    weights = synth.net_weights(wl)
+    _run_sequence(torch, wl, 3, 3, weights, sample=[0], value_every=10, label="210x160").close()
