@@ -38,11 +38,6 @@ __device__ inline void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ inline float wave_sum(float v) {
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
 struct TileRef {
     int slot, tile, ty, tx;
 };
@@ -51,9 +46,16 @@ template <bool DENSE>
 __device__ inline TileRef decode(const ConvArgs &a, int t) {
     TileRef r;
     if constexpr (DENSE) {
-        // Every tile of every stream, position-major like the work lists.
-        r.tile = t / a.dense_n;
-        const int i = t - r.tile * a.dense_n;
+        // Every tile of every stream, in chunks of 32 streams, position-major
+        // within a chunk: 32 consecutive tiles share a head-weight slice, and
+        // a chunk's neighbouring halos are still in L2 when they are reused.
+        constexpr int CH = 32;
+        const int per_chunk = CH * a.TH * a.TW;
+        const int c = t / per_chunk;
+        const int rr = t - c * per_chunk;
+        const int nc = min(CH, a.dense_n - c * CH);
+        r.tile = rr / nc;
+        const int i = c * CH + (rr - r.tile * nc);
         r.ty = r.tile / a.TW;
         r.tx = r.tile - r.ty * a.TW;
         r.slot = a.ids[i];
@@ -226,25 +228,39 @@ __device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
     }
 }
 
-// acc += A(halo, kernel positions [k0, k0 + nk)) x B(weights in LDS from kernel position k0).
+// acc += A(halo, kernel positions [k0, k0 + NK)) x B(weights in LDS from kernel position k0).
 template <int CIN, int COUT, int NK>
 __device__ inline void mfma_positions(floatx4 *acc, const float *halo, const float *s_w, int k0, int lane) {
     using M = Mfma<CIN, COUT>;
     const int mrow = lane & 15, kq = lane >> 4;
     const int py = mrow >> 2, px = mrow & 3;
+    const float *abase = halo + (py * 6 + px) * M::CS + kq;
+    const float *bbase = s_w + lane;
+    // Software pipeline: the A value and the NB B values of k-step s+1 are
+    // read from LDS while the NB matrix ops of k-step s run.
+    constexpr int NS = NK * M::KSP;
+    float a_cur = abase[((k0 / 3) * 6 + (k0 % 3)) * M::CS];
+    float b_cur[M::NB];
 #pragma unroll
-    for (int kp = 0; kp < NK; ++kp) {
-        const int kpos = k0 + kp;
-        const int ky = kpos / 3, kx = kpos - ky * 3;
-        const float *arow = halo + ((py + ky) * 6 + px + kx) * M::CS + kq;
-        const float *brow = s_w + kp * M::KSP * M::NB * 64 + lane;
+    for (int nb = 0; nb < M::NB; ++nb) b_cur[nb] = bbase[nb * 64];
+#pragma unroll 2
+    for (int s = 0; s < NS; ++s) {
+        float a_nxt = 0.f;
+        float b_nxt[M::NB];
+        if (s + 1 < NS) {
+            const int s1 = s + 1;
+            const int kp = s1 / M::KSP, cs = s1 - kp * M::KSP;
+            const int kpos = k0 + kp, ky = kpos / 3, kx = kpos - ky * 3;
+            a_nxt = abase[(ky * 6 + kx) * M::CS + cs * 4];
 #pragma unroll
-        for (int cs = 0; cs < M::KSP; ++cs) {
-            const float av = arow[cs * 4];
-#pragma unroll
-            for (int nb = 0; nb < M::NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, brow[(cs * M::NB + nb) * 64], acc[nb], 0, 0, 0);
+            for (int nb = 0; nb < M::NB; ++nb) b_nxt[nb] = bbase[(s1 * M::NB + nb) * 64];
         }
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_cur, b_cur[nb], acc[nb], 0, 0, 0);
+        a_cur = a_nxt;
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) b_cur[nb] = b_nxt[nb];
     }
 }
 
@@ -278,21 +294,39 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
         d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
     }
     if (a.n_out > 0) {
+        // Tile contribution to each logit: per-lane partial dot products, then
+        // the lane sums, 8 logits at a time so the butterfly steps of
+        // different logits overlap.
         const int ntiles = a.TH * a.TW;
-        for (int o = 0; o < a.n_out; ++o) {
-            const float4 *w4 =
-                reinterpret_cast<const float4 *>(a.hw + ((size_t)o * ntiles + r.tile) * kTilePx * COUT) + lane;
-            float p = 0.f;
+        for (int o0 = 0; o0 < a.n_out; o0 += 8) {
+            float p[8];
 #pragma unroll
-            for (int nb = 0; nb < M::NB; ++nb) {
-                const float4 w = w4[nb * 64];
-                p = fmaf(acc[nb][0], w.x, p);
-                p = fmaf(acc[nb][1], w.y, p);
-                p = fmaf(acc[nb][2], w.z, p);
-                p = fmaf(acc[nb][3], w.w, p);
+            for (int q = 0; q < 8; ++q) {
+                p[q] = 0.f;
+                const int o = o0 + q;
+                if (o < a.n_out) {
+                    const float4 *w4 = reinterpret_cast<const float4 *>(
+                                           a.hw + ((size_t)o * ntiles + r.tile) * kTilePx * COUT) + lane;
+#pragma unroll
+                    for (int nb = 0; nb < M::NB; ++nb) {
+                        const float4 w = w4[nb * 64];
+                        p[q] = fmaf(acc[nb][0], w.x, p[q]);
+                        p[q] = fmaf(acc[nb][1], w.y, p[q]);
+                        p[q] = fmaf(acc[nb][2], w.z, p[q]);
+                        p[q] = fmaf(acc[nb][3], w.w, p[q]);
+                    }
+                }
             }
-            p = wave_sum(p);
-            if (lane == 0) a.hpart[((size_t)r.slot * ntiles + r.tile) * a.n_out + o] = p;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) p[q] += __shfl_xor(p[q], off, 64);
+            if (lane < 8 && o0 + lane < a.n_out) {
+                float v = p[0];
+#pragma unroll
+                for (int q = 1; q < 8; ++q) v = lane == q ? p[q] : v;
+                a.hpart[((size_t)r.slot * ntiles + r.tile) * a.n_out + o0 + lane] = v;
+            }
         }
     }
     wave_sync();

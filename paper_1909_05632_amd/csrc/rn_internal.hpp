@@ -56,7 +56,6 @@ struct CompactArgs {
     uint64_t *tmask[RN_MAX_CONV + 1];
     uint32_t *wl[RN_MAX_CONV + 1];
     int32_t *cnt;                 // [L+1]
-    int32_t *poscnt;              // [L+1][ntiles] dirty streams per tile position
 };
 
 struct ConvArgs {

@@ -290,81 +290,78 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 }
 
 // Work lists, position-major: the entries of layer l are its dirty tiles in
-// (ty, tx, batch index) order.  Two passes over the tile masks, each with one
-// block per (64-position word, layer):
-//   k_poscount: per position, the number of streams whose tile is dirty
-//               (64 ballots per chunk of 64 streams give the column counts);
-//   k_poswrite: each position's offset (prefix over all earlier positions),
-//               then every dirty (position, stream) at offset + rank.
-// Every count and entry has exactly one writer; no atomics on global memory.
+// (ty, tx, batch index) order.  One block per (64-position word wd, layer):
+//   - its offset is the number of dirty tiles at earlier positions, i.e. the
+//     popcount of tile-mask words 0..wd-1 of every stream;
+//   - 64 ballots per chunk of 64 streams transpose the chunk's words into one
+//     stream bitmap per position, giving per-position counts and, by
+//     popcount below the lane, each stream's rank within its position.
+// Every entry has exactly one writer; no global atomics.
 constexpr int kChunksPerPass = 16;          // 1024 streams per pass
 
 __device__ inline uint64_t tile_word(const CompactArgs &a, int l, int i, int wd) {
     return i < a.n ? a.tmask[l][(size_t)a.ids[i] * a.TMW + wd] : 0ull;
 }
 
-__global__ __launch_bounds__(kThreads) void k_poscount(CompactArgs a) {
-    __shared__ int s_cnt[64];
-    const int wd = blockIdx.x, l = blockIdx.y + 1;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (threadIdx.x < 64) s_cnt[threadIdx.x] = 0;
-    __syncthreads();
-    const int nch = (a.n + 63) / 64;
-    for (int c = wave; c < nch; c += (int)(blockDim.x >> 6)) {
-        const uint64_t word = tile_word(a, l, 64 * c + lane, wd);
-        int mine = 0;
-        for (int j = 0; j < 64; ++j) {
-            const uint64_t b = __ballot((word >> j) & 1ull);
-            if (lane == j) mine = __popcll(b);
-        }
-        atomicAdd(&s_cnt[lane], mine);           // LDS, 4 waves
-    }
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        const int t = 64 * wd + threadIdx.x;
-        if (t < a.ntiles) a.poscnt[(size_t)l * a.ntiles + t] = s_cnt[threadIdx.x];
-    }
-}
-
-__global__ __launch_bounds__(kThreads) void k_poswrite(CompactArgs a) {
+__global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     __shared__ int red[kThreads / 64];
+    __shared__ int s_cnt[64];
     __shared__ int s_run[64];
     __shared__ int s_base[kChunksPerPass][64];
     __shared__ uint64_t s_bal[kChunksPerPass][64];
     const int wd = blockIdx.x, l = blockIdx.y + 1;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int32_t *pc = a.poscnt + (size_t)l * a.ntiles;
+    const int nwaves = (int)(blockDim.x >> 6);
+    const int nch = (a.n + 63) / 64;
+
+    // Dirty tiles at positions before this word, over all streams.
     int pre = 0;
-    for (int t = threadIdx.x; t < 64 * wd; t += blockDim.x) pre += pc[t];
-    pre = block_sum(pre, red);
-    if (wd == 0) {
-        int tot = 0;
-        for (int t = threadIdx.x; t < a.ntiles; t += blockDim.x) tot += pc[t];
-        tot = block_sum(tot, red);
-        if (threadIdx.x == 0) a.cnt[l] = tot;
+    for (int e = threadIdx.x; e < a.n * wd; e += blockDim.x) {
+        const int i = e / wd, w = e - i * wd;
+        pre += __popcll(a.tmask[l][(size_t)a.ids[i] * a.TMW + w]);
     }
+    pre = block_sum(pre, red);
+
+    // Per-position counts of this word; the ballots of the first pass stay in LDS.
+    if (threadIdx.x < 64) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    for (int c = wave; c < nch; c += nwaves) {
+        const uint64_t word = tile_word(a, l, 64 * c + lane, wd);
+        int mine = 0;
+        for (int j = 0; j < 64; ++j) {
+            const uint64_t b = __ballot((word >> j) & 1ull);
+            if (lane == j) {
+                mine = __popcll(b);
+                if (c < kChunksPerPass) s_bal[c][j] = b;
+            }
+        }
+        atomicAdd(&s_cnt[lane], mine);           // LDS
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
         int r = pre;
         for (int j = 0; j < 64; ++j) {
             s_run[j] = r;
-            const int t = 64 * wd + j;
-            if (t < a.ntiles) r += pc[t];
+            r += s_cnt[j];
         }
+        if (wd == a.TMW - 1) a.cnt[l] = r;       // the last word closes the list
     }
     __syncthreads();
+
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     const int cap = a.n * a.ntiles;
-    const int nch = (a.n + 63) / 64;
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
-        for (int cc = wave; cc < nc; cc += (int)(blockDim.x >> 6)) {
-            const uint64_t word = tile_word(a, l, 64 * (c0 + cc) + lane, wd);
-            for (int j = 0; j < 64; ++j) {
-                const uint64_t b = __ballot((word >> j) & 1ull);
-                if (lane == j) s_bal[cc][j] = b;
+        if (c0 > 0) {
+            for (int cc = wave; cc < nc; cc += nwaves) {
+                const uint64_t word = tile_word(a, l, 64 * (c0 + cc) + lane, wd);
+                for (int j = 0; j < 64; ++j) {
+                    const uint64_t b = __ballot((word >> j) & 1ull);
+                    if (lane == j) s_bal[cc][j] = b;
+                }
             }
+            __syncthreads();
         }
-        __syncthreads();
         if (threadIdx.x < 64) {
             int r = s_run[threadIdx.x];
             for (int cc = 0; cc < nc; ++cc) {
@@ -374,7 +371,7 @@ __global__ __launch_bounds__(kThreads) void k_poswrite(CompactArgs a) {
             s_run[threadIdx.x] = r;
         }
         __syncthreads();
-        for (int pi = wave; pi < nc * 64; pi += (int)(blockDim.x >> 6)) {
+        for (int pi = wave; pi < nc * 64; pi += nwaves) {
             const int cc = pi >> 6, j = pi & 63;
             const int t = 64 * wd + j;
             const uint64_t b = s_bal[cc][j];
@@ -411,10 +408,7 @@ hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {
 
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s) {
     dim3 grid(a.TMW, a.L);
-    hipLaunchKernelGGL(k_poscount, grid, dim3(kThreads), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_poswrite, grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_compact_pos, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
