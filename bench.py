@@ -82,6 +82,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=None)
     ap.add_argument("--head", default="tiles", choices=["tiles", "full"])
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy, 3 times (scales the "
+                         "FETCH_SIZE / WRITE_SIZE counters to bytes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -89,6 +92,17 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        n = 1 << 28                                             # 1 GiB of float32
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"bytes_read": 4 * n, "bytes_written": 4 * n,
+                                               "launches": 3}}))
+        return
 
     from paper_1909_05632_amd import ReuseNet
     from synth import frames as synth
