@@ -42,9 +42,12 @@ struct TileRef {
     int slot, tile, ty, tx;
 };
 
+// A work item is named by one 32-bit word: list mode, the slot-encoded entry
+// slot << 16 | ty << 8 | tx (one load); dense mode, the same word built from
+// the stream id (one load) and the position.  item_word issues the load;
+// item_ref only decodes, so the load can be issued iterations ahead.
 template <bool DENSE>
-__device__ inline TileRef decode(const ConvArgs &a, int t) {
-    TileRef r;
+__device__ inline uint32_t item_word(const ConvArgs &a, int t) {
     if constexpr (DENSE) {
         // Every tile of every stream, in chunks of 32 streams, position-major
         // within a chunk: 32 consecutive tiles share a head-weight slice, and
@@ -54,19 +57,27 @@ __device__ inline TileRef decode(const ConvArgs &a, int t) {
         const int c = t / per_chunk;
         const int rr = t - c * per_chunk;
         const int nc = min(CH, a.dense_n - c * CH);
-        r.tile = rr / nc;
-        const int i = c * CH + (rr - r.tile * nc);
-        r.ty = r.tile / a.TW;
-        r.tx = r.tile - r.ty * a.TW;
-        r.slot = a.ids[i];
+        const int tile = rr / nc;
+        const int i = c * CH + (rr - tile * nc);
+        const int ty = tile / a.TW;
+        return ((uint32_t)a.ids[i] << 16) | ((uint32_t)ty << 8) | (uint32_t)(tile - ty * a.TW);
     } else {
-        const uint32_t e = a.wl[t];
-        r.slot = a.ids[e >> 16];
-        r.ty = (e >> 8) & 255;
-        r.tx = e & 255;
-        r.tile = r.ty * a.TW + r.tx;
+        return a.wl[t];
     }
+}
+
+__device__ inline TileRef item_ref(const ConvArgs &a, uint32_t e) {
+    TileRef r;
+    r.slot = (int)(e >> 16);
+    r.ty = (e >> 8) & 255;
+    r.tx = e & 255;
+    r.tile = r.ty * a.TW + r.tx;
     return r;
+}
+
+template <bool DENSE>
+__device__ inline TileRef decode(const ConvArgs &a, int t) {
+    return item_ref(a, item_word<DENSE>(a, t));
 }
 
 template <bool DENSE>
@@ -301,20 +312,37 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
         for (int o0 = 0; o0 < a.n_out; o0 += 8) {
             float p[8];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                p[q] = 0.f;
-                const int o = o0 + q;
-                if (o < a.n_out) {
-                    const float4 *w4 = reinterpret_cast<const float4 *>(
-                                           a.hw + ((size_t)o * ntiles + r.tile) * kTilePx * COUT) + lane;
+            for (int q = 0; q < 8; q += 2) {
+                // Two logits per batch: their 2 x NB weight loads are issued
+                // together (indices clamped, results of absent logits dropped).
+                const int oa = min(o0 + q, a.n_out - 1), ob = min(o0 + q + 1, a.n_out - 1);
+                const float4 *wa = reinterpret_cast<const float4 *>(
+                                       a.hw + ((size_t)oa * ntiles + r.tile) * kTilePx * COUT) + lane;
+                const float4 *wb = reinterpret_cast<const float4 *>(
+                                       a.hw + ((size_t)ob * ntiles + r.tile) * kTilePx * COUT) + lane;
+                float4 va[M::NB], vb[M::NB];
 #pragma unroll
-                    for (int nb = 0; nb < M::NB; ++nb) {
-                        const float4 w = w4[nb * 64];
-                        p[q] = fmaf(acc[nb][0], w.x, p[q]);
-                        p[q] = fmaf(acc[nb][1], w.y, p[q]);
-                        p[q] = fmaf(acc[nb][2], w.z, p[q]);
-                        p[q] = fmaf(acc[nb][3], w.w, p[q]);
-                    }
+                for (int nb = 0; nb < M::NB; ++nb) {
+                    va[nb] = wa[nb * 64];
+                    vb[nb] = wb[nb * 64];
+                }
+                float pa = 0.f, pb = 0.f;
+#pragma unroll
+                for (int nb = 0; nb < M::NB; ++nb) {
+                    pa = fmaf(acc[nb][0], va[nb].x, pa);
+                    pa = fmaf(acc[nb][1], va[nb].y, pa);
+                    pa = fmaf(acc[nb][2], va[nb].z, pa);
+                    pa = fmaf(acc[nb][3], va[nb].w, pa);
+                    pb = fmaf(acc[nb][0], vb[nb].x, pb);
+                    pb = fmaf(acc[nb][1], vb[nb].y, pb);
+                    pb = fmaf(acc[nb][2], vb[nb].z, pb);
+                    pb = fmaf(acc[nb][3], vb[nb].w, pb);
+                }
+                p[q] = pa;
+                p[q + 1] = pb;
+                if (o0 + q + 2 >= a.n_out) {
+                    for (int z = q + 2; z < 8; ++z) p[z] = 0.f;
+                    break;
                 }
             }
 #pragma unroll
@@ -360,23 +388,27 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     const int stride = xr.stride;
     int t = xr.first + wave;
     if (t >= xr.end) return;                              // no block barrier after this point
+    // Pipeline: the halo of the next tile is fetched into registers during this
+    // tile's matrix work, and the work item after that is read one more
+    // iteration ahead, so neither load is waited for before the matrix ops.
     float4 pre[M::HV];
-    TileRef nxt = decode<DENSE>(a, t);
-    fetch_halo<CIN, COUT>(a, nxt, pre, lane);
+    uint32_t e_cur = item_word<DENSE>(a, t);
+    uint32_t e_nxt = t + stride < xr.end ? item_word<DENSE>(a, t + stride) : 0u;
+    fetch_halo<CIN, COUT>(a, item_ref(a, e_cur), pre, lane);
     for (; t < xr.end; t += stride) {
-        const TileRef cur = nxt;
+        const TileRef cur = item_ref(a, e_cur);
         store_halo<CIN, COUT>(halo, pre, lane);
         wave_sync();
-        if (t + stride < xr.end) {
-            nxt = decode<DENSE>(a, t + stride);
-            fetch_halo<CIN, COUT>(a, nxt, pre, lane);
-        }
+        const uint32_t e_nn = t + 2 * stride < xr.end ? item_word<DENSE>(a, t + 2 * stride) : 0u;
+        if (t + stride < xr.end) fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
         wave_sync();
         epilogue<CIN, COUT>(a, cur, acc, s_bias, halo, lane);
+        e_cur = e_nxt;
+        e_nxt = e_nn;
     }
 }
 

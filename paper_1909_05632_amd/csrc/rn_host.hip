@@ -37,7 +37,7 @@ struct Plan {
     // byte offsets into the workspace
     size_t o_lut, o_xin, o_ring, o_dring, o_primed, o_ids, o_act[RN_MAX_CONV + 1], o_w[RN_MAX_CONV],
         o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile,
-        o_wl[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
+        o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
     size_t act_stride[RN_MAX_CONV + 1] = {0};   // elements per slot
     size_t total = 0;
@@ -151,7 +151,10 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     }
     p->o_nchg = take(S * 4);
     p->o_ntile = take(S * (p->L + 1) * 4);
-    for (int l = 1; l <= p->L; ++l) p->o_wl[l] = take(S * p->ntiles * 4);
+    for (int l = 1; l <= p->L; ++l) {
+        p->o_wl[l] = take(S * p->ntiles * 4);
+        p->o_wls[l] = take(S * p->ntiles * 4);
+    }
     p->o_cnt = take((RN_MAX_CONV + 1) * 4);
     const bool tiles_head = p->head_mode == RN_HEAD_TILES;
     p->o_part = take(tiles_head ? 0 : p->part_elems * 4);
@@ -345,12 +348,13 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     for (int l = 0; l <= p.L; ++l) {
         ca.tmask[l] = g.tmask[l];
         ca.wl[l] = l ? net->at<uint32_t>(p.o_wl[l]) : nullptr;
+        ca.wls[l] = l ? net->at<uint32_t>(p.o_wls[l]) : nullptr;
     }
     ca.cnt = net->at<int32_t>(p.o_cnt);
     e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
 
-    e = run_layers(net, n, ids, ca.wl, ca.cnt, logits, s, false);
+    e = run_layers(net, n, ids, ca.wls, ca.cnt, logits, s, false);
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));
     net->last_stream = s;
     net->last_n = n;

@@ -54,12 +54,13 @@ struct CompactArgs {
     const int32_t *ids;
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
-    uint32_t *wl[RN_MAX_CONV + 1];
+    uint32_t *wl[RN_MAX_CONV + 1];  // entries i << 16 | ty << 8 | tx (batch index i)
+    uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels
     int32_t *cnt;                 // [L+1]
 };
 
 struct ConvArgs {
-    const uint32_t *wl;           // work list of this layer
+    const uint32_t *wl;           // work list of this layer, slot-encoded (NULL: dense mode)
     const int32_t *cnt;           // device count of this layer
     const int32_t *ids;
     const void *in;               // previous layer cache (layer 1: float32 input ring)

@@ -378,8 +378,11 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             if (t < a.ntiles && ((b >> lane) & 1ull)) {
                 const int idx = s_base[cc][j] + __popcll(b & below);
                 const int i = 64 * (c0 + cc) + lane;
-                const int ty = t / a.TW, tx = t - ty * a.TW;
-                if (idx < cap) a.wl[l][idx] = ((uint32_t)i << 16) | ((uint32_t)ty << 8) | (uint32_t)tx;
+                const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
+                if (idx < cap) {
+                    a.wl[l][idx] = ((uint32_t)i << 16) | pos;
+                    a.wls[l][idx] = ((uint32_t)a.ids[i] << 16) | pos;
+                }
             }
         }
         __syncthreads();
