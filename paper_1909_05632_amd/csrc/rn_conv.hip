@@ -178,26 +178,42 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
 
 // ------------------------------------------------------------------ MFMA layers
 
-// Implicit GEMM per tile: M = 16 pixels, N = COUT, K = 9 * CIN ordered
-// (ky, kx, ci).  v_mfma_f32_16x16x4_f32 operand layout (lane l):
-//   A: row l % 16, k l / 16;  B: k l / 16, column l % 16;
-//   D: rows 4 (l / 16) + i, column l % 16, i = 0..3.
-// So row m = pixel (m / 4, m % 4) of the tile; the A operand is read straight
-// from the 6x6 x CIN halo in LDS (im2col is an address computation), and lane l
-// ends up holding tile row l / 16, columns i = 0..3, of channel l % 16 + 16 nb.
-// The weights are pre-packed in fragment order [kstep][nb][lane] so each B
-// read is one conflict-free 256-byte LDS row.
+// Implicit GEMM per tile: M = 16 pixels, N = COUT, K = 9 * CIN.
+// v_mfma_f32_16x16x4_f32 operand layout (lane l, kq = l / 16):
+//   A: row l % 16, k-row kq;  B: k-row kq, column l % 16;
+//   D: rows 4 kq + i, column l % 16, i = 0..3.
+// Rows are tile pixels in column-major order, row m = pixel (m % 4, m / 4), so
+// lane l of D holds pixels (i, kq), i = 0..3, of channel l % 16 + 16 nb.
+// K is walked per kernel position in channel blocks of 16 (plus one block of
+// 8 when CIN % 16 = 8).  Inside a block, k-step j gives lane group kq the
+// channel c0 + 4 kq + j (c0 + 2 kq + j in a block of 8), so each lane's A
+// values for the block's 4 (2) k-steps are contiguous channels of one halo
+// pixel: one 16-byte (8-byte) LDS read.  The weights are packed to match,
+// [kpos][block][nb][lane][j], so the B values are one 16-byte read per nb.
+// Bank layout of the halo: the 16-byte A reads of one 8-lane phase touch 8
+// pixels.  With a pixel stride of CIN + 4 floats they fall in distinct banks.
+// When CIN = 8 (mod 32) the halo is stored unpadded (pixel stride CIN, which
+// lets 8 waves' halos fit in LDS next to the 40->80 weights) and the 16-byte
+// chunk index of pixel p is XOR-ed with (p / 12) & 1, which again puts every
+// phase in distinct banks for all 9 kernel positions (checked exhaustively on
+// the host for CIN = 40, 72, 104, 136).  Blocks are double-buffered: the
+// operands of the next block are read while the matrix cores work on the
+// current one.
 template <int CIN, int COUT>
 struct Mfma {
     static constexpr int NB = COUT / 16;
-    static constexpr int CS = CIN + 1;        // halo channel stride in LDS (odd: spreads banks)
-    static constexpr int KSP = CIN / 4;       // k-steps per kernel position
+    static constexpr bool SWZ = (CIN % 32) == 8;
+    static constexpr int CS = SWZ ? CIN : CIN + 4;   // halo pixel stride in LDS (floats)
+    static constexpr int NF = CIN / 16;       // full channel blocks per kernel position
+    static constexpr int TAIL = (CIN % 16) ? 1 : 0;
+    static constexpr int NBLK = NF + TAIL;
+    static constexpr int C4 = CIN / 4;        // float4 per halo pixel
     static constexpr int HALO = 36 * CS;      // floats of one halo in LDS
     static constexpr int SR = COUT + 4;       // row stride of the output staging area
-    static constexpr int HV = (36 * KSP + 63) / 64;   // 16-byte halo loads per lane
+    static constexpr int HV = (36 * C4 + 63) / 64;   // 16-byte halo loads per lane
     static constexpr int WTOT = 9 * CIN * COUT;
     static_assert(16 * SR <= HALO, "output staging must fit in the halo area");
-    static_assert(COUT % 16 == 0 && CIN % 4 == 0, "MFMA tiling");
+    static_assert(COUT % 16 == 0 && CIN % 8 == 0, "MFMA tiling");
 };
 
 // Global -> registers: the halo of one tile, 16 bytes per lane per load.
@@ -209,8 +225,8 @@ __device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *r
     for (int j = 0; j < M::HV; ++j) {
         const int h = lane + 64 * j;
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (h < 36 * M::KSP) {
-            const int pos = h / M::KSP, c4 = h - pos * M::KSP;
+        if (h < 36 * M::C4) {
+            const int pos = h / M::C4, c4 = h - pos * M::C4;
             const int hy = pos / 6, hx = pos - hy * 6;
             const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
             if (y >= 0 && y < a.H && x >= 0 && x < a.W)
@@ -222,19 +238,72 @@ __device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *r
     }
 }
 
+// Offset (floats) of 16-byte channel chunk c of halo pixel p.
+template <int CIN, int COUT>
+__device__ inline int chunk_off(int p, int c) {
+    using M = Mfma<CIN, COUT>;
+    if constexpr (M::SWZ) return p * M::CS + 4 * (c ^ ((p / 12) & 1));
+    else return p * M::CS + 4 * c;
+}
+
 template <int CIN, int COUT>
 __device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
     using M = Mfma<CIN, COUT>;
 #pragma unroll
     for (int j = 0; j < M::HV; ++j) {
         const int h = lane + 64 * j;
-        if (h < 36 * M::KSP) {
-            const int pos = h / M::KSP, c4 = h - pos * M::KSP;
-            float *d = halo + pos * M::CS + c4 * 4;
-            d[0] = regs[j].x;
-            d[1] = regs[j].y;
-            d[2] = regs[j].z;
-            d[3] = regs[j].w;
+        if (h < 36 * M::C4) {
+            const int pos = h / M::C4, c4 = h - pos * M::C4;
+            *reinterpret_cast<float4 *>(halo + chunk_off<CIN, COUT>(pos, c4)) = regs[j];
+        }
+    }
+}
+
+template <int NB>
+struct BlockOps {
+    float4 a;
+    float4 b[NB];
+};
+
+// Operands of channel block `blk` at kernel position `kpos` (s_w holds the
+// weights from kernel position k0 on).
+template <int CIN, int COUT>
+__device__ inline void load_block(BlockOps<Mfma<CIN, COUT>::NB> &o, const float *halo, int pix, const float *s_w,
+                                  int kpos, int k0, int blk, int lane) {
+    using M = Mfma<CIN, COUT>;
+    const int kq = lane >> 4;
+    const int ky = kpos / 3, kx = kpos - ky * 3;
+    const int p = pix + ky * 6 + kx;
+    const float *wb = s_w + (size_t)(kpos - k0) * CIN * COUT + blk * 16 * COUT;
+    if (blk < M::NF) {
+        o.a = *reinterpret_cast<const float4 *>(halo + chunk_off<CIN, COUT>(p, 4 * blk + kq));
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb)
+            o.b[nb] = *reinterpret_cast<const float4 *>(wb + (nb * 64 + lane) * 4);
+    } else {
+        const float2 a2 = *reinterpret_cast<const float2 *>(
+            halo + chunk_off<CIN, COUT>(p, 4 * blk + (kq >> 1)) + 2 * (kq & 1));
+        o.a = make_float4(a2.x, a2.y, 0.f, 0.f);
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) {
+            const float2 b2 = *reinterpret_cast<const float2 *>(wb + (nb * 64 + lane) * 2);
+            o.b[nb] = make_float4(b2.x, b2.y, 0.f, 0.f);
+        }
+    }
+}
+
+template <int CIN, int COUT>
+__device__ inline void mma_block(floatx4 *acc, const BlockOps<Mfma<CIN, COUT>::NB> &o, int blk) {
+    using M = Mfma<CIN, COUT>;
+    const int steps = blk < M::NF ? 4 : 2;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (j >= steps) break;
+        const float av = j == 0 ? o.a.x : j == 1 ? o.a.y : j == 2 ? o.a.z : o.a.w;
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) {
+            const float bv = j == 0 ? o.b[nb].x : j == 1 ? o.b[nb].y : j == 2 ? o.b[nb].z : o.b[nb].w;
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[nb], 0, 0, 0);
         }
     }
 }
@@ -243,35 +312,23 @@ __device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
 template <int CIN, int COUT, int NK>
 __device__ inline void mfma_positions(floatx4 *acc, const float *halo, const float *s_w, int k0, int lane) {
     using M = Mfma<CIN, COUT>;
-    const int mrow = lane & 15, kq = lane >> 4;
-    const int py = mrow >> 2, px = mrow & 3;
-    const float *abase = halo + (py * 6 + px) * M::CS + kq;
-    const float *bbase = s_w + lane;
-    // Software pipeline: the A value and the NB B values of k-step s+1 are
-    // read from LDS while the NB matrix ops of k-step s run.
-    constexpr int NS = NK * M::KSP;
-    float a_cur = abase[((k0 / 3) * 6 + (k0 % 3)) * M::CS];
-    float b_cur[M::NB];
+    const int mrow = lane & 15;
+    const int pix = (mrow & 3) * 6 + (mrow >> 2);   // column-major pixel rows
+    BlockOps<M::NB> cur, nxt;
+    load_block<CIN, COUT>(cur, halo, pix, s_w, k0, k0, 0, lane);
+    for (int kp = 0; kp < NK; ++kp) {
+        const int kpos = k0 + kp;
 #pragma unroll
-    for (int nb = 0; nb < M::NB; ++nb) b_cur[nb] = bbase[nb * 64];
-#pragma unroll 2
-    for (int s = 0; s < NS; ++s) {
-        float a_nxt = 0.f;
-        float b_nxt[M::NB];
-        if (s + 1 < NS) {
-            const int s1 = s + 1;
-            const int kp = s1 / M::KSP, cs = s1 - kp * M::KSP;
-            const int kpos = k0 + kp, ky = kpos / 3, kx = kpos - ky * 3;
-            a_nxt = abase[(ky * 6 + kx) * M::CS + cs * 4];
-#pragma unroll
-            for (int nb = 0; nb < M::NB; ++nb) b_nxt[nb] = bbase[(s1 * M::NB + nb) * 64];
+        for (int blk = 0; blk < M::NBLK; ++blk) {
+            if (blk + 1 < M::NBLK) load_block<CIN, COUT>(nxt, halo, pix, s_w, kpos, k0, blk + 1, lane);
+            else if (kp + 1 < NK) load_block<CIN, COUT>(nxt, halo, pix, s_w, kpos + 1, k0, 0, lane);
+            // Keep the next block's LDS reads ahead of this block's matrix ops
+            // (the scheduler would otherwise sink them to their first use).
+            __builtin_amdgcn_sched_barrier(0);
+            mma_block<CIN, COUT>(acc, cur, blk);
+            __builtin_amdgcn_sched_barrier(0);
+            cur = nxt;
         }
-#pragma unroll
-        for (int nb = 0; nb < M::NB; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_cur, b_cur[nb], acc[nb], 0, 0, 0);
-        a_cur = a_nxt;
-#pragma unroll
-        for (int nb = 0; nb < M::NB; ++nb) b_cur[nb] = b_nxt[nb];
     }
 }
 
@@ -281,8 +338,8 @@ template <int CIN, int COUT>
 __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *acc, const float *s_bias,
                                 float *stage, int lane) {
     using M = Mfma<CIN, COUT>;
-    const int mrow = lane & 15, kq = lane >> 4;
-    const bool row_in = r.ty * kTile + kq < a.H;
+    const int mrow = lane & 15, kq = lane >> 4;       // D holds pixels (py = i, px = kq)
+    const bool col_in = r.tx * kTile + kq < a.W;
 #pragma unroll
     for (int nb = 0; nb < M::NB; ++nb) {
         const float b = s_bias[nb * 16 + mrow];
@@ -290,9 +347,9 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
         for (int i = 0; i < 4; ++i) {
             float v = acc[nb][i] + b;
             v = v > 0.0f ? v : 0.0f;
-            if (!row_in || r.tx * kTile + i >= a.W) v = 0.0f;
+            if (!col_in || r.ty * kTile + i >= a.H) v = 0.0f;
             acc[nb][i] = v;
-            stage[(kq * 4 + i) * M::SR + nb * 16 + mrow] = v;
+            stage[(i * 4 + kq) * M::SR + nb * 16 + mrow] = v;
         }
     }
     wave_sync();
@@ -585,26 +642,35 @@ void pack_conv_first(const float *oihw, int cin, int cout, rn_dtype dt, void *ds
 }
 
 void pack_conv_mfma(const float *oihw, int cin, int cout, rn_dtype dt, void *dst) {
-    // Fragment order [kstep][nb][lane]: element B[k][n] with
-    // k = kstep * 4 + lane / 16 = (ky * 3 + kx) * cin + ci, n = nb * 16 + lane % 16.
+    // [kpos][block][nb][lane][j]: block b of a kernel position covers channels
+    // [16 b, 16 b + 16) (the last block [16 nf, 16 nf + 8) when cin % 16 = 8);
+    // element j of lane l is B[channel][n] with n = nb * 16 + l % 16 and
+    // channel = 16 b + 4 (l / 16) + j (block of 8: 16 nf + 2 (l / 16) + j).
     (void)dt;
     float *d = static_cast<float *>(dst);
-    const int nb_n = cout / 16, ksteps = 9 * cin / 4;
-    for (int ks = 0; ks < ksteps; ++ks)
-        for (int nb = 0; nb < nb_n; ++nb)
-            for (int l = 0; l < 64; ++l) {
-                const int k = ks * 4 + l / 16, n = nb * 16 + l % 16;
-                const int kpos = k / cin, ci = k - kpos * cin;
-                d[((size_t)ks * nb_n + nb) * 64 + l] = oihw[((size_t)n * cin + ci) * 9 + kpos];
-            }
+    const int nb_n = cout / 16, nf = cin / 16;
+    size_t o = 0;
+    for (int kpos = 0; kpos < 9; ++kpos) {
+        for (int b = 0; b < nf + (cin % 16 ? 1 : 0); ++b) {
+            const bool full = b < nf;
+            const int steps = full ? 4 : 2;
+            for (int nb = 0; nb < nb_n; ++nb)
+                for (int l = 0; l < 64; ++l)
+                    for (int j = 0; j < steps; ++j) {
+                        const int ci = 16 * b + (full ? 4 : 2) * (l / 16) + j;
+                        const int n = nb * 16 + l % 16;
+                        d[o++] = oihw[((size_t)n * cin + ci) * 9 + kpos];
+                    }
+        }
+    }
 }
 
 size_t tile_head_w_elems(int ntiles, int cout, int n_out) { return (size_t)n_out * ntiles * kTilePx * cout; }
 
 void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst) {
     // [o][tile][nb][lane][i]: the weight of the output the MFMA epilogue holds
-    // in lane `lane`, register i of block nb: channel nb * 16 + lane % 16, tile
-    // row lane / 16, tile column i.  Zero outside the image.
+    // in lane `lane`, register i of block nb: channel nb * 16 + lane % 16,
+    // tile pixel (row i, column lane / 16).  Zero outside the image.
     const int NB = C / 16, ntiles = TH * TW;
     for (int o = 0; o < n_out; ++o)
         for (int t = 0; t < ntiles; ++t) {
@@ -612,7 +678,7 @@ void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH
             for (int nb = 0; nb < NB; ++nb)
                 for (int l = 0; l < 64; ++l)
                     for (int i = 0; i < 4; ++i) {
-                        const int c = nb * 16 + l % 16, y = ty * kTile + l / 16, x = tx * kTile + i;
+                        const int c = nb * 16 + l % 16, y = ty * kTile + i, x = tx * kTile + l / 16;
                         const size_t di = ((((size_t)o * ntiles + t) * NB + nb) * 64 + l) * 4 + i;
                         dst[di] = (y < H && x < W) ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x]
                                                    : 0.f;
