@@ -82,7 +82,19 @@ typedef struct {
     rn_dtype act_dtype;           /* RN_F32, or RN_BF16 (bf16 weights and activations,
                                      fp32 accumulation, fp32 logits) */
     rn_head_mode head_mode;       /* RN_HEAD_TILES (default, zero) or RN_HEAD_FULL */
+    int32_t options;              /* bit set of RN_OPT_*, 0 = defaults */
 } rn_config;
+
+/* Options.
+ *   RN_OPT_SEPARATE_FIRST: keep layer 1 as its own kernel writing its cache.
+ *     By default, when the frame has one channel and layer 2 runs on the
+ *     resident-weight MFMA kernel, layer 1 is folded into layer 2: each dirty
+ *     layer-2 tile computes the layer-1 activations of its halo from the input
+ *     patch around it (the same arithmetic, so the same bits) instead of
+ *     reading a layer-1 cache.  Layer-1 masks and work lists are produced
+ *     either way; reuse_net_read_activation(layer 1) then computes the layer
+ *     on demand. */
+#define RN_OPT_SEPARATE_FIRST 1
 
 typedef struct {                  /* HOST pointers, float32, read during create only */
     const float *const *conv_w;   /* [n_conv], each [cout][cin][k][k] (OIHW) */

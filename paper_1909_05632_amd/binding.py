@@ -21,6 +21,7 @@ RN_PHASES = 5
 RN_OK, RN_EINVAL, RN_EUNSUPPORTED, RN_ENOSPACE, RN_EHIP, RN_ESTATE = 0, -1, -2, -3, -4, -5
 RN_F32, RN_BF16, RN_U8 = 0, 1, 2
 RN_HEAD_TILES, RN_HEAD_FULL = 0, 1
+RN_OPT_SEPARATE_FIRST = 1
 PHASES = ("masks", "compact", "conv1", "convN", "head")
 STATUS_NAMES = {0: "RN_OK", -1: "RN_EINVAL", -2: "RN_EUNSUPPORTED", -3: "RN_ENOSPACE",
                 -4: "RN_EHIP", -5: "RN_ESTATE"}
@@ -46,7 +47,7 @@ class rn_config(ctypes.Structure):
                 ("conv", ctypes.POINTER(rn_conv_spec)), ("n_out", ctypes.c_int32),
                 ("tile_h", ctypes.c_int32), ("tile_w", ctypes.c_int32),
                 ("max_streams", ctypes.c_int32), ("act_dtype", ctypes.c_int),
-                ("head_mode", ctypes.c_int)]
+                ("head_mode", ctypes.c_int), ("options", ctypes.c_int32)]
 
 
 class rn_weights(ctypes.Structure):
@@ -219,7 +220,7 @@ class ReuseNet:
 
     def __init__(self, in_c: int, h: int, w: int, convs: Sequence[int], n_out: int,
                  max_streams: int, weights, act_dtype: str = "f32", stack: int = 1,
-                 device="cuda", tile: int = 4, head: str = "tiles"):
+                 device="cuda", tile: int = 4, head: str = "tiles", fuse_first: bool = True):
         import torch
         self.torch = torch
         self.device = torch.device(device)
@@ -235,7 +236,8 @@ class ReuseNet:
         self._spec_arr = (rn_conv_spec * len(specs))(*[rn_conv_spec(*s) for s in specs])
         self.cfg = rn_config(in_c, h, w, stack, len(specs), self._spec_arr, n_out, tile, tile,
                              max_streams, _dtype_code(act_dtype),
-                             {"tiles": RN_HEAD_TILES, "full": RN_HEAD_FULL}[head])
+                             {"tiles": RN_HEAD_TILES, "full": RN_HEAD_FULL}[head],
+                             0 if fuse_first else RN_OPT_SEPARATE_FIRST)
         nbytes = reuse_net_workspace_bytes(self.cfg)
         if nbytes == 0:
             # Re-run create's validation to report why.

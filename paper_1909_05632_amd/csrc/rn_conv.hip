@@ -259,6 +259,64 @@ __device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
     }
 }
 
+// Layer 1 folded into the halo staging (one input channel): the 6x6 x CIN
+// layer-1 activations around the tile are computed from the 8x8 input patch
+// around it, in the same FMA order as k_conv_first_f32 (so the values are the
+// bits that kernel would have cached).  Halo pixels outside the image are the
+// layer-2 zero padding.
+__device__ inline float fetch_patch(const ConvArgs &a, const TileRef &r, int lane) {
+    const int y = r.ty * kTile - 2 + (lane >> 3), x = r.tx * kTile - 2 + (lane & 7);
+    const float *plane = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
+    return (y >= 0 && y < a.H && x >= 0 && x < a.W) ? plane[(size_t)y * a.W + x] : 0.f;
+}
+
+template <int CIN, int COUT>
+__device__ inline void build_halo_fused(float *halo, float pin, const ConvArgs &a, const TileRef &r,
+                                        const float *s_w1, const float *s_b1, int lane) {
+    using M = Mfma<CIN, COUT>;
+    constexpr int NU = 36 * M::C4;            // 4-channel units of the halo
+    constexpr int UV = (NU + 63) / 64;
+    float *patch = halo + M::HALO - 64;       // scratch: tail of this wave's halo area
+    patch[lane] = pin;
+    wave_sync();
+    float4 v[UV];
+#pragma unroll
+    for (int k = 0; k < UV; ++k) {
+        const int u = lane + 64 * k;
+        v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (u < NU) {
+            const int pos = u / M::C4, c4 = u - pos * M::C4;
+            const int hy = pos / 6, hx = pos - hy * 6;
+            const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+            if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
+                float o[4];
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    const int c = 4 * c4 + cc;
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+                        for (int kx = 0; kx < 3; ++kx)
+                            acc = fmaf(s_w1[(ky * 3 + kx) * CIN + c], patch[(hy + ky) * 8 + hx + kx], acc);
+                    const float t = acc + s_b1[c];
+                    o[cc] = t > 0.0f ? t : 0.0f;
+                }
+                v[k] = make_float4(o[0], o[1], o[2], o[3]);
+            }
+        }
+    }
+    wave_sync();                              // patch reads done before the halo overwrites it
+#pragma unroll
+    for (int k = 0; k < UV; ++k) {
+        const int u = lane + 64 * k;
+        if (u < NU) {
+            const int pos = u / M::C4, c4 = u - pos * M::C4;
+            *reinterpret_cast<float4 *>(halo + chunk_off<CIN, COUT>(pos, c4)) = v[k];
+        }
+    }
+}
+
 template <int NB>
 struct BlockOps {
     float4 a;
@@ -426,11 +484,13 @@ struct Resident {
         (size_t)(Mfma<CIN, COUT>::WTOT + WAVES * Mfma<CIN, COUT>::HALO) * sizeof(float);
 };
 
-template <int CIN, int COUT, int WAVES, bool DENSE>
+template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE>
 __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
+    __shared__ float s_w1[FUSE ? 9 * CIN : 1];
+    __shared__ float s_b1[FUSE ? CIN : 1];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cnt = work_count<DENSE>(a);
     const XcdRange xr = xcd_range(cnt, WAVES);
@@ -440,24 +500,36 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     const float4 *wg = static_cast<const float4 *>(a.w);
     for (int j = tid; j < M::WTOT / 4; j += blockDim.x) reinterpret_cast<float4 *>(s_w)[j] = wg[j];
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+    if constexpr (FUSE) {
+        for (int j = tid; j < 9 * CIN; j += blockDim.x) s_w1[j] = a.w1[j];
+        for (int j = tid; j < CIN; j += blockDim.x) s_b1[j] = a.b1[j];
+    }
     __syncthreads();
 
     const int stride = xr.stride;
     int t = xr.first + wave;
     if (t >= xr.end) return;                              // no block barrier after this point
-    // Pipeline: the halo of the next tile is fetched into registers during this
-    // tile's matrix work, and the work item after that is read one more
-    // iteration ahead, so neither load is waited for before the matrix ops.
-    float4 pre[M::HV];
+    // Pipeline: the halo (or, fused, the input patch) of the next tile is
+    // fetched into registers during this tile's matrix work, and the work item
+    // after that is read one more iteration ahead, so neither load is waited
+    // for before the matrix ops.
+    constexpr int HVR = FUSE ? 1 : M::HV;
+    float4 pre[HVR];
+    float pin = 0.f;
     uint32_t e_cur = item_word<DENSE>(a, t);
     uint32_t e_nxt = t + stride < xr.end ? item_word<DENSE>(a, t + stride) : 0u;
-    fetch_halo<CIN, COUT>(a, item_ref(a, e_cur), pre, lane);
+    if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_cur), lane);
+    else fetch_halo<CIN, COUT>(a, item_ref(a, e_cur), pre, lane);
     for (; t < xr.end; t += stride) {
         const TileRef cur = item_ref(a, e_cur);
-        store_halo<CIN, COUT>(halo, pre, lane);
+        if constexpr (FUSE) build_halo_fused<CIN, COUT>(halo, pin, a, cur, s_w1, s_b1, lane);
+        else store_halo<CIN, COUT>(halo, pre, lane);
         wave_sync();
         const uint32_t e_nn = t + 2 * stride < xr.end ? item_word<DENSE>(a, t + 2 * stride) : 0u;
-        if (t + stride < xr.end) fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
+        if (t + stride < xr.end) {
+            if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_nxt), lane);
+            else fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
+        }
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -532,6 +604,12 @@ constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // 160 KiB per CU, less the s
 template <int CIN, int COUT>
 constexpr bool use_resident() { return Resident<CIN, COUT, 8>::lds_bytes <= kLdsBudget; }
 
+// Static LDS of the fused variant: bias, layer-1 weights and bias.
+template <int CIN, int COUT>
+constexpr bool fused_fits() {
+    return Resident<CIN, COUT, 8>::lds_bytes + (COUT + 10 * CIN) * sizeof(float) <= 160 * 1024;
+}
+
 template <int CIN, int COUT>
 constexpr int pick_kps() {
     return Staged<CIN, COUT, 3>::lds_bytes <= kLdsBudget ? 3 : 1;
@@ -550,23 +628,30 @@ hipError_t set_lds(K kern, size_t lds) {
                                (int)lds);
 }
 
+template <int CIN, int COUT, bool DENSE, bool FUSE>
+hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {
+    constexpr size_t lds = Resident<CIN, COUT, 8>::lds_bytes;
+    auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE, FUSE>;
+    static hipError_t attr = set_lds(kern, lds);
+    if (attr != hipSuccess) return attr;
+    const int grid = persistent_grid(cus, (a.max_tiles + 7) / 8);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, a);
+    return hipGetLastError();
+}
+
 template <int CIN, int COUT, bool DENSE>
 hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
-    const int total_max = a.max_tiles;
     if constexpr (use_resident<CIN, COUT>()) {
-        constexpr size_t lds = Resident<CIN, COUT, 8>::lds_bytes;
-        auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE>;
-        static hipError_t attr = set_lds(kern, lds);
-        if (attr != hipSuccess) return attr;
-        const int grid = persistent_grid(cus, (total_max + 7) / 8);
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, a);
+        if (a.fuse_first) return run_resident<CIN, COUT, DENSE, true>(a, cus, s);
+        return run_resident<CIN, COUT, DENSE, false>(a, cus, s);
     } else {
+        if (a.fuse_first) return hipErrorInvalidValue;
         constexpr int KPS = pick_kps<CIN, COUT>();
         constexpr size_t lds = Staged<CIN, COUT, KPS>::lds_bytes;
         auto kern = k_conv_mfma_staged<CIN, COUT, KPS, DENSE>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
-        const int grid = persistent_grid(cus, (total_max + 3) / 4);
+        const int grid = persistent_grid(cus, (a.max_tiles + 3) / 4);
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
     }
     return hipGetLastError();
@@ -588,6 +673,14 @@ hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt) {
     if (dt != RN_F32) return false;
 #define X(ci, co) if (cin == ci && cout == co) return true;
+    RN_MFMA_SHAPES(X)
+#undef X
+    return false;
+}
+
+bool conv_fused_first_supported(int c1, int c2, rn_dtype dt) {
+    if (dt != RN_F32) return false;
+#define X(ci, co) if (c1 == ci && c2 == co) return use_resident<ci, co>() && fused_fits<ci, co>();
     RN_MFMA_SHAPES(X)
 #undef X
     return false;

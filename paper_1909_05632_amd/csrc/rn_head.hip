@@ -97,9 +97,38 @@ __global__ __launch_bounds__(kThreads) void k_head_reduce(HeadArgs a) {
 }
 
 // Tile-partial head: logits[i][o] = bd[o] + sum over tiles of the cached
-// per-tile partials of stream i, added in a fixed order (lane-strided tiles,
-// then a fixed butterfly).  Wave w of the block handles logits o = w, w+4, ...
+// per-tile partials of stream i, added in a fixed order: thread j adds tiles
+// j, j + 256, ... (each tile's NO partials are one contiguous read), then a
+// fixed butterfly per wave and the 4 waves in order.
+template <int NO>
 __global__ __launch_bounds__(kThreads) void k_tile_head(TileHeadArgs a) {
+    __shared__ float red[kThreads / 64][NO];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = blockIdx.x;
+    const float *P = a.hpart + (size_t)a.ids[i] * a.ntiles * NO;
+    float acc[NO];
+#pragma unroll
+    for (int o = 0; o < NO; ++o) acc[o] = 0.f;
+    for (int t = threadIdx.x; t < a.ntiles; t += kThreads) {
+#pragma unroll
+        for (int o = 0; o < NO; ++o) acc[o] += P[(size_t)t * NO + o];
+    }
+#pragma unroll
+    for (int o = 0; o < NO; ++o) {
+        float v = acc[o];
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0) red[wave][o] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < NO) {
+        float v = red[0][threadIdx.x];
+        for (int w = 1; w < kThreads / 64; ++w) v += red[w][threadIdx.x];
+        a.logits[(size_t)i * NO + threadIdx.x] = v + a.bias[threadIdx.x];
+    }
+}
+
+// Any n_out: wave w of the block handles logits o = w, w + 4, ...
+__global__ __launch_bounds__(kThreads) void k_tile_head_generic(TileHeadArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int i = blockIdx.x;
     const float *P = a.hpart + (size_t)a.ids[i] * a.ntiles * a.n_out;
@@ -183,7 +212,12 @@ hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
 }
 
 hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s) {
-    hipLaunchKernelGGL(k_tile_head, dim3(a.n), dim3(kThreads), 0, s, a);
+    if (a.n_out == 6)
+        hipLaunchKernelGGL(k_tile_head<6>, dim3(a.n), dim3(kThreads), 0, s, a);
+    else if (a.n_out == 18)
+        hipLaunchKernelGGL(k_tile_head<18>, dim3(a.n), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_tile_head_generic, dim3(a.n), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -32,6 +32,7 @@ struct Plan {
     int radius[RN_MAX_CONV] = {0};         // change growth per layer, (k - 1) / 2
     size_t K = 0;                          // head input elements per slot (tiled)
     int head_mode = RN_HEAD_TILES;
+    bool fuse_first = false;               // layer 1 folded into layer 2's halo staging
     int head_sg = 8;
     size_t part_elems = 0;
     // byte offsets into the workspace
@@ -81,6 +82,7 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     if (cfg->stack == 4 && cfg->in_c != 1) return fail(RN_EUNSUPPORTED, "stack = 4 needs in_c = 1");
     if (cfg->act_dtype != RN_F32) return fail(RN_EUNSUPPORTED, "bf16 activations are not implemented yet");
     if (cfg->head_mode != RN_HEAD_TILES && cfg->head_mode != RN_HEAD_FULL) return fail(RN_EINVAL, "bad head_mode");
+    if (cfg->options & ~RN_OPT_SEPARATE_FIRST) return fail(RN_EINVAL, "unknown option bits");
     p->L = cfg->n_conv;
     p->H = cfg->in_h;
     p->W = cfg->in_w;
@@ -107,6 +109,8 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
         if (!conv_mfma_supported(p->C[l - 1], p->C[l], p->dt))
             return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" + std::to_string(p->C[l]));
     p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
+    p->fuse_first = !(cfg->options & RN_OPT_SEPARATE_FIRST) && p->L >= 2 && p->C[0] == 1 && p->stack == 1 &&
+                    conv_fused_first_supported(p->C[1], p->C[2], p->dt);
     // The tile-partial head lives in the epilogue of an MFMA layer.
     p->head_mode = (cfg->head_mode == RN_HEAD_TILES && p->L >= 2) ? RN_HEAD_TILES : RN_HEAD_FULL;
     p->head_sg = head_streams_per_block(p->N);
@@ -251,6 +255,7 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
     const bool tiles_head = p.head_mode == RN_HEAD_TILES;
     hipError_t e = hipSuccess;
     for (int l = 1; l <= p.L; ++l) {
+        if (l == 1 && p.fuse_first) continue;            // computed inside layer 2
         ConvArgs cv{};
         cv.wl = dense ? nullptr : wl[l];
         cv.cnt = dense ? nullptr : cnt + l;
@@ -271,6 +276,13 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
         cv.out_stride = p.act_stride[l];
         cv.dense_n = dense ? n : 0;
         cv.max_tiles = n * p.ntiles;
+        if (l == 2 && p.fuse_first) {
+            cv.fuse_first = 1;
+            cv.in = net->at<float>(p.o_xin);
+            cv.in_stride = p.act_stride[0];
+            cv.w1 = net->at<float>(p.o_w[0]);
+            cv.b1 = net->at<float>(p.o_b[0]);
+        }
         if (l == p.L && tiles_head) {
             cv.n_out = p.N;
             cv.hw = net->at<float>(p.o_hw);
@@ -587,6 +599,33 @@ rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, 
         }
         const float *src = net->at<float>(p.o_xin) + ((size_t)sid * p.stack + head) * p.in_c * HW;
         return copy_out(net, host_out, src, (size_t)p.in_c * HW * 4);
+    }
+    if (layer == 1 && p.fuse_first) {
+        // Layer 1 has no cache of its own in this mode: recompute it for this
+        // slot from the input cache with the first-layer kernel.
+        rn_status st = sync_last(net);
+        if (st != RN_OK) return st;
+        ConvArgs cv{};
+        cv.ids = net->at<int32_t>(p.o_ids) + sid;   // identity table: points at the value sid
+        cv.in = net->at<float>(p.o_xin);
+        cv.out = net->at<void>(p.o_act[1]);
+        cv.w = net->at<void>(p.o_w[0]);
+        cv.bias = net->at<float>(p.o_b[0]);
+        cv.ring_head = net->at<int32_t>(p.o_ring);
+        cv.H = p.H;
+        cv.W = p.W;
+        cv.TH = p.TH;
+        cv.TW = p.TW;
+        cv.cin = p.C[0];
+        cv.cout = p.C[1];
+        cv.stack = p.stack;
+        cv.in_stride = p.act_stride[0];
+        cv.out_stride = p.act_stride[1];
+        cv.dense_n = 1;
+        cv.max_tiles = p.ntiles;
+        hipError_t e = launch_conv_first(cv, p.dt, net->cus, net->last_stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(net->last_stream);
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("layer-1 recompute: ") + hipGetErrorString(e));
     }
     const int C = p.C[layer];
     std::vector<float> buf(p.act_stride[layer]);

@@ -79,6 +79,12 @@ struct ConvArgs {
     int n_out;
     const float *hw;              // [n_out][TH*TW][16*cout] in the epilogue's fragment order
     float *hpart;                 // [S][TH*TW][n_out]
+    // Layer 1 folded into this layer's halo staging (this is layer 2 and the
+    // input has one channel): `in` is the float32 input cache and the halo's
+    // layer-1 activations are computed from the input patch with w1/b1.
+    int fuse_first;
+    const float *w1;              // layer-1 weights, [k][c1] (first-layer packing, one input channel)
+    const float *b1;              // [c1]
 };
 
 // Dense path: copy the frames into the input cache and mark the slots primed.
@@ -130,6 +136,7 @@ hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream
 hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt);
 bool conv_first_supported(int cin, int cout, rn_dtype dt);
+bool conv_fused_first_supported(int c1, int c2, rn_dtype dt);
 hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
 int head_streams_per_block(int n_out);
 

@@ -21,6 +21,7 @@ namespace rn {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kMaskThreads = 1024;         // one block per stream
 
 __device__ inline uint32_t f32_bits(float v) { return __float_as_uint(v); }
 
@@ -106,9 +107,9 @@ __device__ void grow1(const MaskGeom &g, const uint64_t *src, uint64_t *dst) {
 }
 
 template <bool U8>
-__global__ __launch_bounds__(kThreads) void k_masks(MaskGeom g, MaskArgs a) {
+__global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) {
     extern __shared__ uint64_t smem[];
-    __shared__ int red[kThreads / 64];
+    __shared__ int red[kMaskThreads / 64];
     __shared__ int s_tiles[RN_MAX_CONV + 1];
     const int HWW = g.H * g.WW;
     uint64_t *A = smem;
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(kThreads) void k_masks(MaskGeom g, MaskArgs a) {
         // Diff, 4 pixels (one 16-byte load per plane) per thread per item; the
         // loads of U items are issued before any compare so that many are in
         // flight per thread.
-        constexpr int U = 8;
+        constexpr int U = 4;
         const int n4 = (int)(HW / 4);
         for (int q0 = threadIdx.x; q0 < n4; q0 += U * (int)blockDim.x) {
             uint32_t ch[U];
@@ -314,11 +315,12 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     const int nwaves = (int)(blockDim.x >> 6);
     const int nch = (a.n + 63) / 64;
 
-    // Dirty tiles at positions before this word, over all streams.
+    // Dirty tiles at positions before this word, over all streams (one thread
+    // per stream; the words of a stream are independent loads).
     int pre = 0;
-    for (int e = threadIdx.x; e < a.n * wd; e += blockDim.x) {
-        const int i = e / wd, w = e - i * wd;
-        pre += __popcll(a.tmask[l][(size_t)a.ids[i] * a.TMW + w]);
+    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
+        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * a.TMW;
+        for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
     }
     pre = block_sum(pre, red);
 
@@ -394,9 +396,9 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
 hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s) {
     const size_t shm = (size_t)2 * g.H * g.WW * sizeof(uint64_t) + 256 * sizeof(float);
     if (a.frame_u8)
-        hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kThreads), shm, s, g, a);
+        hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kMaskThreads), shm, s, g, a);
     else
-        hipLaunchKernelGGL(k_masks<false>, dim3(a.n), dim3(kThreads), shm, s, g, a);
+        hipLaunchKernelGGL(k_masks<false>, dim3(a.n), dim3(kMaskThreads), shm, s, g, a);
     return hipGetLastError();
 }
 

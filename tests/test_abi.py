@@ -31,9 +31,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def _cfg(convs=((1, 40), (40, 80)), h=105, w=80, stack=1, n_out=6, tile=4, streams=8,
-         k=3, s=1, p=1, dtype=B.RN_F32, in_c=1, head=B.RN_HEAD_TILES):
+         k=3, s=1, p=1, dtype=B.RN_F32, in_c=1, head=B.RN_HEAD_TILES, options=0):
     specs = (B.rn_conv_spec * len(convs))(*[B.rn_conv_spec(ci, co, k, s, p) for ci, co in convs])
-    cfg = B.rn_config(in_c, h, w, stack, len(convs), specs, n_out, tile, tile, streams, dtype, head)
+    cfg = B.rn_config(in_c, h, w, stack, len(convs), specs, n_out, tile, tile, streams, dtype, head,
+                      options)
     cfg._keep = specs
     return cfg
 
@@ -43,6 +44,10 @@ def test_head_modes_size_the_workspace():
     full = B.reuse_net_workspace_bytes(_cfg(head=B.RN_HEAD_FULL))
     assert tiles > 0 and full > 0 and tiles != full
     assert B.reuse_net_workspace_bytes(_cfg(head=7)) == 0
+
+
+def test_separate_first_layer_option_is_accepted():
+    assert B.reuse_net_workspace_bytes(_cfg(options=B.RN_OPT_SEPARATE_FIRST)) > 0
 
 
 def test_workspace_bytes_valid_configs():
@@ -70,6 +75,7 @@ def test_workspace_bytes_valid_configs():
     dict(k=5, p=2),                   # valid but unsupported kernel size
     dict(convs=((1, 40), (40, 72))),  # no MFMA kernel for this shape
     dict(convs=((1, 20), (20, 40))),  # 40 output channels: not a multiple of 16
+    dict(options=6),                  # unknown option bits
 ])
 def test_workspace_bytes_rejects_bad_configs(bad):
     assert B.reuse_net_workspace_bytes(_cfg(**bad)) == 0

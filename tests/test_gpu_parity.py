@@ -99,6 +99,30 @@ def test_head_modes_agree_and_dense_path_has_no_worklist(torch):
     b.close()
 
 
+def test_folded_first_layer_matches_separate_first_layer_bitwise(torch):
+    # Layer 1 computed inside layer 2's halo staging vs its own kernel and
+    # cache: the same arithmetic, so the same bits (logits, both layers).
+    wl = synth.WORKLOADS["atari-ds2-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _, x = sprite_inputs(wl, range(5), 4)
+    dev = torch.from_numpy(x).cuda()
+    from paper_1909_05632_amd import ReuseNet
+    nets = [ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, 5, weights, fuse_first=f) for f in (True, False)]
+    for t in range(4):
+        outs = [n.step(dev[t][:, None].contiguous()).cpu().numpy() for n in nets]
+        assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32)), t
+        for l in (1, 2):
+            assert np.array_equal(nets[0].worklist(l), nets[1].worklist(l))
+    for i in (0, 4):
+        for l in (1, 2):
+            a, b = nets[0].activation(i, l), nets[1].activation(i, l)
+            assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), (i, l)
+    full = [n.full(dev[2][:, None].contiguous()).cpu().numpy() for n in nets]
+    assert np.array_equal(full[0].view(np.uint32), full[1].view(np.uint32))
+    for n in nets:
+        n.close()
+
+
 def test_unchanged_frame_gives_no_work_and_same_logits(torch):
     wl = synth.WORKLOADS["atari-ds2-256x64"]
     weights = synth.net_weights(wl, bias_std=0.05)
