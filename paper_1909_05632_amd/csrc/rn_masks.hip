@@ -300,8 +300,15 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 // Every entry has exactly one writer; no global atomics.
 constexpr int kChunksPerPass = 16;          // 1024 streams per pass
 
-__device__ inline uint64_t tile_word(const CompactArgs &a, int l, int i, int wd) {
-    return i < a.n ? a.tmask[l][(size_t)a.ids[i] * a.TMW + wd] : 0ull;
+// Stage the slots and this word's tile bits of streams [64 c0, 64 (c0 + nc)) in LDS.
+__device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, int nc, int32_t *s_slot,
+                                  uint64_t *s_word) {
+    for (int j = threadIdx.x; j < nc * 64; j += blockDim.x) {
+        const int i = 64 * c0 + j;
+        const int slot = i < a.n ? a.ids[i] : -1;
+        s_slot[j] = slot;
+        s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMW + wd] : 0ull;
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
@@ -310,6 +317,8 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     __shared__ int s_run[64];
     __shared__ int s_base[kChunksPerPass][64];
     __shared__ uint64_t s_bal[kChunksPerPass][64];
+    __shared__ int32_t s_slot[kChunksPerPass * 64];
+    __shared__ uint64_t s_word[kChunksPerPass * 64];
     const int wd = blockIdx.x, l = blockIdx.y + 1;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int nwaves = (int)(blockDim.x >> 6);
@@ -323,21 +332,26 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
         for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
     }
     pre = block_sum(pre, red);
-
-    // Per-position counts of this word; the ballots of the first pass stay in LDS.
     if (threadIdx.x < 64) s_cnt[threadIdx.x] = 0;
-    __syncthreads();
-    for (int c = wave; c < nch; c += nwaves) {
-        const uint64_t word = tile_word(a, l, 64 * c + lane, wd);
-        int mine = 0;
-        for (int j = 0; j < 64; ++j) {
-            const uint64_t b = __ballot((word >> j) & 1ull);
-            if (lane == j) {
-                mine = __popcll(b);
-                if (c < kChunksPerPass) s_bal[c][j] = b;
+
+    // Per-position counts of this word over all streams.
+    for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
+        const int nc = min(kChunksPerPass, nch - c0);
+        __syncthreads();
+        stage_pass(a, l, wd, c0, nc, s_slot, s_word);
+        __syncthreads();
+        for (int cc = wave; cc < nc; cc += nwaves) {
+            const uint64_t word = s_word[cc * 64 + lane];
+            int mine = 0;
+            for (int j = 0; j < 64; ++j) {
+                const uint64_t b = __ballot((word >> j) & 1ull);
+                if (lane == j) {
+                    mine = __popcll(b);
+                    s_bal[cc][j] = b;
+                }
             }
+            atomicAdd(&s_cnt[lane], mine);       // LDS
         }
-        atomicAdd(&s_cnt[lane], mine);           // LDS
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -354,9 +368,14 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     const int cap = a.n * a.ntiles;
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
-        if (c0 > 0) {
+        if (nch > kChunksPerPass) {
+            // More than one pass: stage and transpose this pass again (with a
+            // single pass, LDS still holds it from the counting loop).
+            __syncthreads();
+            stage_pass(a, l, wd, c0, nc, s_slot, s_word);
+            __syncthreads();
             for (int cc = wave; cc < nc; cc += nwaves) {
-                const uint64_t word = tile_word(a, l, 64 * (c0 + cc) + lane, wd);
+                const uint64_t word = s_word[cc * 64 + lane];
                 for (int j = 0; j < 64; ++j) {
                     const uint64_t b = __ballot((word >> j) & 1ull);
                     if (lane == j) s_bal[cc][j] = b;
@@ -383,11 +402,10 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
                 const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
                 if (idx < cap) {
                     a.wl[l][idx] = ((uint32_t)i << 16) | pos;
-                    a.wls[l][idx] = ((uint32_t)a.ids[i] << 16) | pos;
+                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + lane] << 16) | pos;
                 }
             }
         }
-        __syncthreads();
     }
 }
 
