@@ -533,7 +533,12 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // A wave in its matrix phase issues ahead of the other wave of its SIMD
+        // (which is then staging or storing), so the two drift out of phase
+        // and the matrix pipe is not left idle while both do memory work.
+        __builtin_amdgcn_s_setprio(2);
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
+        __builtin_amdgcn_s_setprio(0);
         wave_sync();
         epilogue<CIN, COUT>(a, cur, acc, s_bias, halo, lane);
         e_cur = e_nxt;

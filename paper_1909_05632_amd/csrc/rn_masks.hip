@@ -364,7 +364,6 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     }
     __syncthreads();
 
-    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     const int cap = a.n * a.ntiles;
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
@@ -392,18 +391,24 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             s_run[threadIdx.x] = r;
         }
         __syncthreads();
-        for (int pi = wave; pi < nc * 64; pi += nwaves) {
+        // One thread per (chunk, position): walk the set bits of the position's
+        // stream bitmap; its entries are [base, base + popcount) in stream order.
+        for (int pi = threadIdx.x; pi < nc * 64; pi += blockDim.x) {
             const int cc = pi >> 6, j = pi & 63;
             const int t = 64 * wd + j;
-            const uint64_t b = s_bal[cc][j];
-            if (t < a.ntiles && ((b >> lane) & 1ull)) {
-                const int idx = s_base[cc][j] + __popcll(b & below);
-                const int i = 64 * (c0 + cc) + lane;
-                const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
+            uint64_t b = s_bal[cc][j];
+            if (t >= a.ntiles) continue;
+            const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
+            int idx = s_base[cc][j];
+            while (b) {
+                const int k = __ffsll((long long)b) - 1;  // next stream of this position
+                b &= b - 1;
+                const int i = 64 * (c0 + cc) + k;
                 if (idx < cap) {
                     a.wl[l][idx] = ((uint32_t)i << 16) | pos;
-                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + lane] << 16) | pos;
+                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
                 }
+                ++idx;
             }
         }
     }
