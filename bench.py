@@ -1,12 +1,21 @@
 """Benchmark of frame-to-frame convolutional activation reuse on one MI355X.
 
 A step is one pass of the whole hot path over one frame of every stream:
-diff -> change growth and dirty-tile masks -> work lists -> dirty-tile conv
-layers (bias, ReLU, scatter into the caches) -> dense head.  Frames are
-synthetic sprite sequences resident in HBM before timing starts; the frame
-order runs 1..F-1 and then back and forth (every transition is an ordinary
-sprite move).  The dense recompute path of the same library and the CPU
+diff (or explicit change boxes) -> change growth and dirty-tile masks -> work
+lists -> dirty-tile conv layers (bias, ReLU, scatter into the caches) -> dense
+head.  Inputs are synthetic and resident in HBM before timing starts.  The
+dense recompute path of the same library (`reuse_net_full`) and the CPU
 oracle are timed in the same run.
+
+Workloads (synth.WORKLOADS):
+  atari-ds2-256x64 (default)  256 streams x 64 frames, 105x80, 1->40->80, dense->6
+  atari-ds4-1x16              1 stream x 16 frames, 53x40
+  stack4-512x64               512 streams, the last 4 frames stacked as input channels
+  occlusion-105x80-4096       4096 occlusion variants as 64 streams x 64 boxed steps
+  fullres-1024x32             1024 streams x 32 frames, 210x160, 1->64->128->128, dense->18
+                              (--change-frac picks the sprite preset of the sweep)
+The frame order runs 1..F-1 and then back and forth, so every transition is
+an ordinary sprite move.
 
 Prints one JSON line.
 """
@@ -25,6 +34,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_F32_TFLOPS = 157.3
+PEAK_MFMA_BF16_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_conv_mfma_atari-ds2-256x64.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_1909_05632_amd", "csrc", "rn_conv.hip")
 
@@ -44,8 +55,6 @@ def measured_traffic(kernel: str):
     if rec.get("source_sha256_16") != kernel_source_hash() or rec.get("kernel") != kernel:
         return None
     return rec.get("bytes_per_launch")
-PEAK_MFMA_F32_TFLOPS = 157.3
-PEAK_MFMA_BF16_TFLOPS = 2500.0
 
 
 def schedule(frames: int, length: int):
@@ -60,34 +69,118 @@ def schedule(frames: int, length: int):
     return seq
 
 
-def cpu_baseline(wl, weights, frames_u8, budget_s: float):
-    """Time the CPU oracle (full recompute + masks + work lists) on a bounded sample."""
-    import oracle
-    from synth import frames as synth
-    onet = oracle.Net(wl.in_c, wl.h, wl.w, wl.conv_specs(), wl.n_out)
-    cores = len(os.sched_getaffinity(0))
-    n_streams = min(16, frames_u8.shape[1])
-    x = synth.to_f32(frames_u8[:, :n_streams])
-    done, t0 = 0, time.perf_counter()
-    t = 0
-    frames_done = 0
-    while True:
-        t += 1
-        if t >= x.shape[0]:
-            t = 1
-        d0 = np.stack([oracle.diff(x[t - 1][i][None], x[t][i][None]) for i in range(n_streams)])
-        d, m = oracle.masks(onet, d0, want_pixels=False)
-        oracle.worklists(m)
-        oracle.forward(onet, *weights, x[t][:, None])
-        done += n_streams
-        frames_done += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
-    return {"value": done / el, "unit": "frames/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n_streams} streams x {frames_done} frames of {wl.h}x{wl.w} "
-                      f"(full recompute in double + diff, masks and work lists), {el:.1f} s, "
-                      f"OpenMP over streams"}
+# ------------------------------------------------------------------ drivers
+
+class SpriteDriver:
+    """Independent streams of sprite frames (optionally stacked 4 deep)."""
+
+    unit = "frames/s"
+    metric = "frames/sec (all streams)"
+
+    def __init__(self, torch, wl, length, preset=None):
+        from synth import frames as synth
+        self.wl = wl
+        self.S = wl.streams
+        self.preset = preset or {}
+        self.u8 = synth.sprite_batch(wl, **self.preset)            # [F][S][H][W]
+        self.frames = torch.from_numpy(synth.to_f32(self.u8)).cuda().unsqueeze(2).contiguous()
+        self.seq = schedule(wl.frames, length)
+
+    def prime_frames(self):
+        return self.frames[0]
+
+    def step(self, k):
+        return self.frames[self.seq[k]], None, None
+
+    def dense_frames(self, k):
+        return self.frames[self.seq[k]]
+
+    def cpu_sample(self, oracle, weights, budget_s):
+        from synth import frames as synth
+        wl = self.wl
+        onet = oracle.Net(wl.in_c, wl.h, wl.w, wl.conv_specs(), wl.n_out)
+        n = min(16 if wl.h * wl.w < 20000 else 4, self.S)
+        x = synth.to_f32(self.u8[:, :n])
+        done, t0, t, frames = 0, time.perf_counter(), 0, 0
+        while True:
+            t = t % (x.shape[0] - 1) + 1
+            if wl.stack > 1:
+                cur = np.stack([synth.stacked_view(x[:, i], t) for i in range(n)])
+                prev = np.stack([synth.stacked_view(x[:, i], t - 1) for i in range(n)])
+            else:
+                cur, prev = x[t][:, None], x[t - 1][:, None]
+            d0 = np.stack([oracle.diff(prev[i], cur[i]) for i in range(n)])
+            _, m = oracle.masks(onet, d0, want_pixels=False)
+            oracle.worklists(m)
+            oracle.forward(onet, *weights, cur)
+            done += n
+            frames += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                break
+        return done / el, f"{n} streams x {frames} frames of {wl.h}x{wl.w}" + \
+            (" (4 stacked)" if wl.stack > 1 else "")
+
+
+class OcclusionDriver:
+    """4096 occlusion variants of one base image: stream y moves an 8x8 zero
+    patch along row y, one column per step, with explicit change boxes."""
+
+    unit = "variants/s"
+    metric = "occlusion variants/sec"
+
+    def __init__(self, torch, wl, length):
+        from synth import frames as synth
+        self.wl = wl
+        P, G = wl.extra["patch"], wl.extra["grid"]
+        self.S = G
+        self.base = synth.to_f32(synth.occlusion_base(wl))
+        var = np.stack([np.stack([synth.occlusion_variant_frame(self.base, y, x, P)[None]
+                                  for y in range(G)]) for x in range(G)])  # [x][y][1][H][W]
+        self.frames = torch.from_numpy(var).cuda().contiguous()
+        boxes = np.zeros((G, 2 * G, 4), np.int32)
+        for x in range(G):
+            px = (x - 1) % G
+            for y in range(G):
+                boxes[x, 2 * y] = (y, px, y + P, px + P)          # previous patch: restore
+                boxes[x, 2 * y + 1] = (y, x, y + P, x + P)        # new patch
+        self.boxes = torch.from_numpy(boxes).cuda()
+        self.box_off = torch.arange(0, 2 * G + 1, 2, dtype=torch.int32).cuda()
+        self.base_dev = torch.from_numpy(np.stack([self.base[None]] * G)).cuda().contiguous()
+        self.G = G
+
+    def prime_frames(self):
+        return self.base_dev
+
+    def step(self, k):
+        # Step k places the patch at column k % G (the first step after priming
+        # also "restores" column G-1, which is unchanged: a harmless extra box).
+        x = k % self.G
+        return self.frames[x], self.boxes[x], self.box_off
+
+    def dense_frames(self, k):
+        return self.frames[k % self.G]
+
+    def cpu_sample(self, oracle, weights, budget_s):
+        from synth import frames as synth
+        wl = self.wl
+        onet = oracle.Net(1, wl.h, wl.w, wl.conv_specs(), wl.n_out)
+        P, n = wl.extra["patch"], 16
+        done, t0, x = 0, time.perf_counter(), 0
+        while True:
+            var = np.stack([synth.occlusion_variant_frame(self.base, y, x, P)[None] for y in range(n)])
+            px = (x - 1) % self.G
+            d0 = np.stack([oracle.box_mask(wl.h, wl.w, [(y, px, y + P, px + P), (y, x, y + P, x + P)])
+                           for y in range(n)])
+            _, m = oracle.masks(onet, d0, want_pixels=False)
+            oracle.worklists(m)
+            oracle.forward(onet, *weights, var)
+            done += n
+            x = (x + 1) % self.G
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                break
+        return done / el, f"{done} variants (16 per batch) of {wl.h}x{wl.w}"
 
 
 def main():
@@ -96,11 +189,15 @@ def main():
     ap.add_argument("--steps", type=int, default=120)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="atari-ds2-256x64")
+    ap.add_argument("--change-frac", type=float, default=None,
+                    help="full-resolution sweep preset: 0.001, 0.01, 0.05, 0.2 or 1.0")
     ap.add_argument("--dtype", default="f32", choices=["f32"])
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=None)
     ap.add_argument("--head", default="tiles", choices=["tiles", "full"])
+    ap.add_argument("--separate-first", action="store_true",
+                    help="run layer 1 as its own kernel instead of inside layer 2")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy, 3 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -127,34 +224,44 @@ def main():
     from synth import frames as synth
 
     wl = synth.WORKLOADS[args.workload]
-    S, F = wl.streams, wl.frames
+    length = args.warmup + args.steps
+    if args.workload.startswith("occlusion"):
+        drv = OcclusionDriver(torch, wl, length)
+    else:
+        preset = None
+        if args.change_frac is not None:
+            preset = ({"full_change": True} if args.change_frac >= 1.0
+                      else dict(synth.FRACTION_PRESETS[args.change_frac]))
+        drv = SpriteDriver(torch, wl, length, preset)
+    S = drv.S
     weights = synth.net_weights(wl)
-    u8 = synth.sprite_batch(wl)                                 # [F][S][H][W]
-    frames = torch.from_numpy(synth.to_f32(u8)).cuda().unsqueeze(2).contiguous()  # [F][S][1][H][W]
-    net = ReuseNet(wl.in_c, wl.h, wl.w, wl.convs, wl.n_out, S, weights, act_dtype=args.dtype,
-                   stack=wl.stack, head=args.head)
+    net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, S, weights, act_dtype=args.dtype,
+                   stack=wl.stack, head=args.head, fuse_first=not args.separate_first)
     out = torch.empty((S, wl.n_out), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    seq = schedule(F, args.warmup + args.steps)
+
+    def do_step(k):
+        f, b, bo = drv.step(k)
+        net.step(f, boxes=b, box_off=bo, out=out)
 
     # Stats pass: dirty tiles of exactly the steps the timed pass will run.
-    net.full(frames[0], out=out)
+    net.full(drv.prime_frames(), out=out)
     stats = []
-    for t in seq:
-        net.step(frames[t], out=out)
+    for k in range(length):
+        do_step(k)
         stats.append(net.stats())
     timed_stats = stats[args.warmup:]
 
     def run_reuse(profile: bool):
-        net.full(frames[0], out=out)
-        for t in seq[:args.warmup]:
-            net.step(frames[t], out=out)
+        net.full(drv.prime_frames(), out=out)
+        for k in range(args.warmup):
+            do_step(k)
         torch.cuda.synchronize()
         net.set_profiling(profile)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for t in seq[args.warmup:]:
-            net.step(frames[t], out=out)
+        for k in range(args.warmup, length):
+            do_step(k)
         e1.record(stream)
         torch.cuda.synchronize()
         prof = net.profile() if profile else None
@@ -167,13 +274,13 @@ def main():
 
     # Dense recompute path of the same library on the same frames.
     dsteps = args.dense_steps or max(10, args.steps // 2)
-    for t in seq[:args.warmup]:
-        net.full(frames[t], out=out)
+    for k in range(args.warmup):
+        net.full(drv.dense_frames(k), out=out)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for t in seq[args.warmup:args.warmup + dsteps]:
-        net.full(frames[t], out=out)
+    for k in range(args.warmup, args.warmup + dsteps):
+        net.full(drv.dense_frames(k), out=out)
     e1.record(stream)
     torch.cuda.synchronize()
     ms_dense = e0.elapsed_time(e1) / dsteps
@@ -190,55 +297,59 @@ def main():
     useful = np.mean([s["useful_mac"] for s in timed_stats])
     dense_mac = wl.dense_macs_per_frame()
 
-    # Per-kernel roofline figures from the HIP events of the profiled pass.
+    # Per-kernel figures from the HIP events of the profiled pass.
     kern = {}
     for name, rec in prof.items():
         kern[name] = {"ms_per_step": rec["ms"] / K, "launches": rec["launches"]}
-    # conv layers 2..L on MFMA: algorithmic flops = dirty tiles x 16 px x cout x 9 cin x 2
+    # MFMA conv layers 2..L: algorithmic flops = dirty tiles x 16 px x cout x 9 cin x 2
     flops_convn = sum(dirty[:, l].sum() * 16 * chans[l] * 9 * chans[l - 1] * 2 for l in range(2, L + 1))
     if prof["convN"]["ms"] > 0:
         kern["convN"]["tflops"] = flops_convn / (prof["convN"]["ms"] / 1e3) / 1e12
     K_el = tiles * 16 * chans[L]
     if args.head == "full":
-        # full-read head: every stream's whole last-layer cache plus the weights, per launch
-        head_bytes = (S * K_el * 4 + wl.n_out * K_el * 4) * K
+        head_bytes = (S * K_el * 4 + wl.n_out * K_el * 4) * K  # whole last-layer caches + weights
     else:
-        # tile-partial head: the per-tile partials of every stream
-        head_bytes = S * tiles * wl.n_out * 4 * K
+        head_bytes = S * tiles * wl.n_out * 4 * K               # per-tile partials
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
-    # MFMA conv bytes per tile: halo in, tile out (+ head weights of the tile on the last layer)
-    bytes_convn = sum(dirty[:, l].sum() * (36 * chans[l - 1] + 16 * chans[l] +
-                                           (16 * chans[l] * wl.n_out if (l == L and args.head == "tiles") else 0)) * 4
-                      for l in range(2, L + 1))
-    if prof["convN"]["ms"] > 0:
-        kern["convN"]["gbs"] = bytes_convn / (prof["convN"]["ms"] / 1e3) / 1e9
-    # masks: frames + cached input read, changed pixels written (~0), masks written
-    mask_bytes = (2 * S * wl.h * wl.w * 4 * wl.in_c) * K
+    mask_bytes = 2 * S * wl.h * wl.w * 4 * wl.in_c * K         # frame + cached input
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
-    conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * 4 + 36 * chans[0] * 4)
-    kern["conv1"]["gbs"] = conv1_bytes / (prof["conv1"]["ms"] / 1e3) / 1e9 if prof["conv1"]["ms"] else 0
+    if prof["conv1"]["ms"] > 0:
+        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * 4 + 36 * chans[0] * 4)
+        kern["conv1"]["gbs"] = conv1_bytes / (prof["conv1"]["ms"] / 1e3) / 1e9
 
-    dominant = max(("convN", "head", "masks", "conv1"), key=lambda k: prof[k]["ms"])
+    folded = (not args.separate_first) and chans[0] == 1 and L >= 2 and chans[1] == 40
+    dominant = max(("convN", "head", "masks", "conv1", "compact"), key=lambda k: prof[k]["ms"])
     if dominant == "convN":
         ach = kern["convN"]["tflops"]
-        roof = {"bound": "mfma", "kernel": "k_conv_mfma_res (layer 2 on dirty tiles; layer 1 folded "
-                                           "into its halo staging, tile head in its epilogue)",
+        roof = {"bound": "mfma",
+                "kernel": "MFMA dirty-tile conv, layers 2..L" + (" (layer 1 folded into layer 2)"
+                                                                  if folded else ""),
                 "achieved": ach, "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
                 "frac": ach / PEAK_MFMA_F32_TFLOPS,
-                "traffic": measured_traffic("conv_mfma_res_40_80_reuse")}
+                "traffic": measured_traffic("conv_mfma_res_40_80_reuse")
+                if args.workload == "atari-ds2-256x64" and folded and args.head == "tiles" else None}
     else:
-        ach = kern[dominant]["gbs"]
+        ach = kern[dominant].get("gbs", 0.0)
         roof = {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None}
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(wl, weights, u8, args.cpu_budget)
+        import oracle
+        v, sample = drv.cpu_sample(oracle, weights, args.cpu_budget)
+        cpu = {"value": v, "unit": drv.unit, "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+               "sample": sample + " (full recompute in double + change masks and work lists, "
+                                  "OpenMP over streams)"}
 
+    cfg = {"workload": args.workload, "streams": S, "frames": wl.frames, "h": wl.h, "w": wl.w,
+           "convs": list(wl.convs), "n_out": wl.n_out, "tile": "4x4", "head": args.head,
+           "stack": wl.stack, "description": wl.description}
+    if args.change_frac is not None:
+        cfg["change_preset"] = args.change_frac
     line = {
-        "metric": "frames/sec (all streams)",
+        "metric": drv.metric,
         "value": fps,
-        "unit": "frames/s",
+        "unit": drv.unit,
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
@@ -246,12 +357,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": args.dtype,
         "data": "synthetic",
-        "config": {"workload": args.workload, "streams": S, "frames": F, "h": wl.h, "w": wl.w,
-                   "convs": list(wl.convs), "n_out": wl.n_out, "tile": "4x4", "head": args.head,
-                   "description": wl.description},
-        "dense_path": {"value": fps_dense, "unit": "frames/s", "ms_per_step": ms_dense},
+        "config": cfg,
+        "dense_path": {"value": fps_dense, "unit": drv.unit, "ms_per_step": ms_dense},
         "speedup_vs_dense": fps / fps_dense,
         "changed_px_frac": changed,
         "dirty_tile_frac": [float(dirty[:, l].mean() / (S * tiles)) for l in range(L + 1)],
