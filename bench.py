@@ -191,7 +191,7 @@ def main():
     ap.add_argument("--workload", default="atari-ds2-256x64")
     ap.add_argument("--change-frac", type=float, default=None,
                     help="full-resolution sweep preset: 0.001, 0.01, 0.05, 0.2 or 1.0")
-    ap.add_argument("--dtype", default="f32", choices=["f32"])
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=None)
@@ -306,26 +306,28 @@ def main():
     if prof["convN"]["ms"] > 0:
         kern["convN"]["tflops"] = flops_convn / (prof["convN"]["ms"] / 1e3) / 1e12
     K_el = tiles * 16 * chans[L]
+    esz = 2 if args.dtype == "bf16" else 4
     if args.head == "full":
-        head_bytes = (S * K_el * 4 + wl.n_out * K_el * 4) * K  # whole last-layer caches + weights
+        head_bytes = (S * K_el * esz + wl.n_out * K_el * 4) * K  # whole last-layer caches + weights
     else:
         head_bytes = S * tiles * wl.n_out * 4 * K               # per-tile partials
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
     mask_bytes = 2 * S * wl.h * wl.w * 4 * wl.in_c * K         # frame + cached input
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
     if prof["conv1"]["ms"] > 0:
-        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * 4 + 36 * chans[0] * 4)
+        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + 36 * chans[0] * 4)
         kern["conv1"]["gbs"] = conv1_bytes / (prof["conv1"]["ms"] / 1e3) / 1e9
 
     folded = (not args.separate_first) and chans[0] == 1 and L >= 2 and chans[1] == 40
     dominant = max(("convN", "head", "masks", "conv1", "compact"), key=lambda k: prof[k]["ms"])
     if dominant == "convN":
         ach = kern["convN"]["tflops"]
+        peak = PEAK_MFMA_BF16_TFLOPS if args.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
         roof = {"bound": "mfma",
                 "kernel": "MFMA dirty-tile conv, layers 2..L" + (" (layer 1 folded into layer 2)"
                                                                   if folded else ""),
-                "achieved": ach, "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
-                "frac": ach / PEAK_MFMA_F32_TFLOPS,
+                "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                "frac": ach / peak,
                 "traffic": measured_traffic("conv_mfma_res_40_80_reuse")
                 if args.workload == "atari-ds2-256x64" and folded and args.head == "tiles" else None}
     else:

@@ -23,88 +23,12 @@
 // are a sum over tiles of each tile's own contribution.  The epilogue computes
 // that contribution for the tiles it recomputes and stores it per (stream,
 // tile); clean tiles keep theirs.  The head then only adds partials.
-#include "rn_internal.hpp"
+#include "rn_device.hpp"
 
 namespace rn {
 namespace {
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-// Order this wave's LDS writes before its later LDS reads (and keep the
-// compiler from moving memory operations across).
-__device__ inline void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-struct TileRef {
-    int slot, tile, ty, tx;
-};
-
-// A work item is named by one 32-bit word: list mode, the slot-encoded entry
-// slot << 16 | ty << 8 | tx (one load); dense mode, the same word built from
-// the stream id (one load) and the position.  item_word issues the load;
-// item_ref only decodes, so the load can be issued iterations ahead.
-template <bool DENSE>
-__device__ inline uint32_t item_word(const ConvArgs &a, int t) {
-    if constexpr (DENSE) {
-        // Every tile of every stream, in chunks of 32 streams, position-major
-        // within a chunk: 32 consecutive tiles share a head-weight slice, and
-        // a chunk's neighbouring halos are still in L2 when they are reused.
-        constexpr int CH = 32;
-        const int per_chunk = CH * a.TH * a.TW;
-        const int c = t / per_chunk;
-        const int rr = t - c * per_chunk;
-        const int nc = min(CH, a.dense_n - c * CH);
-        const int tile = rr / nc;
-        const int i = c * CH + (rr - tile * nc);
-        const int ty = tile / a.TW;
-        return ((uint32_t)a.ids[i] << 16) | ((uint32_t)ty << 8) | (uint32_t)(tile - ty * a.TW);
-    } else {
-        return a.wl[t];
-    }
-}
-
-__device__ inline TileRef item_ref(const ConvArgs &a, uint32_t e) {
-    TileRef r;
-    r.slot = (int)(e >> 16);
-    r.ty = (e >> 8) & 255;
-    r.tx = e & 255;
-    r.tile = r.ty * a.TW + r.tx;
-    return r;
-}
-
-template <bool DENSE>
-__device__ inline TileRef decode(const ConvArgs &a, int t) {
-    return item_ref(a, item_word<DENSE>(a, t));
-}
-
-template <bool DENSE>
-__device__ inline int work_count(const ConvArgs &a) {
-    if constexpr (DENSE) return a.dense_n * a.TH * a.TW;
-    else return *a.cnt;
-}
-
-// XCD-aware split of the work items [0, cnt): workgroups are dispatched round
-// robin over the chip's 8 XCDs (block b runs on XCD b % 8), each with its own
-// L2.  Item range [cnt x / 8, cnt (x + 1) / 8) goes to the blocks of XCD x, so
-// the tiles of neighbouring positions (same head weights, overlapping halos)
-// are served from one L2.  `units` work items per block per round.
-struct XcdRange {
-    int first, end, stride;
-};
-
-__device__ inline XcdRange xcd_range(int cnt, int units) {
-    constexpr int kXcd = 8;
-    const int x = blockIdx.x % kXcd, k = blockIdx.x / kXcd;
-    const int blocks_x = ((int)gridDim.x - x + kXcd - 1) / kXcd;
-    XcdRange r;
-    r.first = (int)((long long)cnt * x / kXcd) + k * units;
-    r.end = (int)((long long)cnt * (x + 1) / kXcd);
-    r.stride = blocks_x * units;
-    return r;
-}
+using namespace dev;
 
 // ------------------------------------------------------------------ first layer
 
@@ -620,18 +544,6 @@ constexpr int pick_kps() {
     return Staged<CIN, COUT, 3>::lds_bytes <= kLdsBudget ? 3 : 1;
 }
 
-// Persistent grid: at most `cap` blocks, no more than the work needs, and a
-// multiple of 8 so that every XCD segment of xcd_range has blocks.
-inline int persistent_grid(int cap, int need) {
-    int g = std::max(1, std::min(cap, need));
-    return (g + 7) / 8 * 8;
-}
-
-template <typename K>
-hipError_t set_lds(K kern, size_t lds) {
-    return hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)lds);
-}
 
 template <int CIN, int COUT, bool DENSE, bool FUSE>
 hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {

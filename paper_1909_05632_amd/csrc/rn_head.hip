@@ -17,15 +17,27 @@ namespace {
 
 constexpr int kThreads = 256;
 
-template <int NO, int SG>
+// Four consecutive activations as float32 (float32 or bf16 caches).
+template <typename AT>
+__device__ inline float4 load_act4(const AT *p);
+template <>
+__device__ inline float4 load_act4<float>(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+template <>
+__device__ inline float4 load_act4<uint16_t>(const uint16_t *p) {
+    const uint2 q = *reinterpret_cast<const uint2 *>(p);
+    return make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xFFFF0000u),
+                       __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xFFFF0000u));
+}
+
+template <int NO, int SG, typename AT>
 __global__ __launch_bounds__(kThreads) void k_head_partial_f32(HeadArgs a) {
     __shared__ float red[kThreads / 64][SG * NO];
     const int split = blockIdx.x, g = blockIdx.y;
     const size_t k0 = (size_t)split * a.chunk;
     const size_t k1 = min(k0 + a.chunk, a.K);
     const float *W = static_cast<const float *>(a.w);
-    const float *act = static_cast<const float *>(a.act);
-    const float *rows[SG];
+    const AT *act = static_cast<const AT *>(a.act);
+    const AT *rows[SG];
     int ns = 0;
 #pragma unroll
     for (int s = 0; s < SG; ++s) {
@@ -49,7 +61,7 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_f32(HeadArgs a) {
 #pragma unroll
         for (int s = 0; s < SG; ++s) {
             if (s < ns) {
-                const float4 av = *reinterpret_cast<const float4 *>(rows[s] + k);
+                const float4 av = load_act4<AT>(rows[s] + k);
 #pragma unroll
                 for (int o = 0; o < NO; ++o) {
                     float t = acc[s][o];
@@ -141,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void k_tile_head_generic(TileHeadArgs a) 
 }
 
 // Generic head for any n_out (<= kHeadMaxOut): 8 outputs per pass over a_L.
-template <int SG>
+template <int SG, typename AT>
 __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, int o0) {
     constexpr int NO = 8;
     __shared__ float red[kThreads / 64][SG * NO];
@@ -149,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
     const size_t k0 = (size_t)split * a.chunk;
     const size_t k1 = min(k0 + a.chunk, a.K);
     const float *W = static_cast<const float *>(a.w);
-    const float *act = static_cast<const float *>(a.act);
+    const AT *act = static_cast<const AT *>(a.act);
     float acc[SG][NO];
     for (int s = 0; s < SG; ++s)
         for (int o = 0; o < NO; ++o) acc[s][o] = 0.f;
@@ -158,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
         for (int s = 0; s < SG; ++s) {
             const int i = g * SG + s;
             if (i >= a.n) break;
-            const float4 av = *reinterpret_cast<const float4 *>(act + (size_t)a.ids[i] * a.K + k);
+            const float4 av = load_act4<AT>(act + (size_t)a.ids[i] * a.K + k);
             for (int o = 0; o < no; ++o) {
                 const float4 wv = *reinterpret_cast<const float4 *>(W + (size_t)(o0 + o) * a.K + k);
                 float t = acc[s][o];
@@ -193,17 +205,22 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
 
 int head_streams_per_block(int n_out) { return n_out == 18 ? 4 : 8; }
 
-hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
-    (void)dt;
+template <typename AT>
+void launch_head_partials(const HeadArgs &a, hipStream_t s) {
     const int sg = head_streams_per_block(a.n_out);
     dim3 grid(a.nsplit, (a.n + sg - 1) / sg);
     if (a.n_out == 6)
-        hipLaunchKernelGGL((k_head_partial_f32<6, 8>), grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((k_head_partial_f32<6, 8, AT>), grid, dim3(kThreads), 0, s, a);
     else if (a.n_out == 18)
-        hipLaunchKernelGGL((k_head_partial_f32<18, 4>), grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((k_head_partial_f32<18, 4, AT>), grid, dim3(kThreads), 0, s, a);
     else
         for (int o0 = 0; o0 < a.n_out; o0 += 8)
-            hipLaunchKernelGGL((k_head_partial_generic<8>), grid, dim3(kThreads), 0, s, a, o0);
+            hipLaunchKernelGGL((k_head_partial_generic<8, AT>), grid, dim3(kThreads), 0, s, a, o0);
+}
+
+hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
+    if (dt == RN_BF16) launch_head_partials<uint16_t>(a, s);
+    else launch_head_partials<float>(a, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int tot = a.n * a.n_out;

@@ -40,6 +40,7 @@ struct Plan {
         o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile,
         o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
+    size_t w_bytes[RN_MAX_CONV] = {0};
     size_t act_stride[RN_MAX_CONV + 1] = {0};   // elements per slot
     size_t total = 0;
 };
@@ -80,7 +81,6 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     if (cfg->tile_h != kTile || cfg->tile_w != kTile) return fail(RN_EUNSUPPORTED, "only 4x4 tiles are implemented");
     if (cfg->in_w % 4 != 0) return fail(RN_EUNSUPPORTED, "in_w must be a multiple of 4");
     if (cfg->stack == 4 && cfg->in_c != 1) return fail(RN_EUNSUPPORTED, "stack = 4 needs in_c = 1");
-    if (cfg->act_dtype != RN_F32) return fail(RN_EUNSUPPORTED, "bf16 activations are not implemented yet");
     if (cfg->head_mode != RN_HEAD_TILES && cfg->head_mode != RN_HEAD_FULL) return fail(RN_EINVAL, "bad head_mode");
     if (cfg->options & ~RN_OPT_SEPARATE_FIRST) return fail(RN_EINVAL, "unknown option bits");
     p->L = cfg->n_conv;
@@ -103,11 +103,15 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
         p->C[l + 1] = cfg->conv[l].cout;
         p->radius[l] = (cfg->conv[l].k - 1) / 2;
     }
-    if (!conv_first_supported(p->C[0], p->C[1], p->dt))
-        return fail(RN_EUNSUPPORTED, "no first-layer kernel for " + std::to_string(p->C[0]) + "->" + std::to_string(p->C[1]));
+    const bool bf = p->dt == RN_BF16;
+    const char *dts = bf ? " (bf16)" : " (float32)";
+    if (!(bf ? conv_first_bf16_supported(p->C[0], p->C[1]) : conv_first_supported(p->C[0], p->C[1], p->dt)))
+        return fail(RN_EUNSUPPORTED, "no first-layer kernel for " + std::to_string(p->C[0]) + "->" +
+                                         std::to_string(p->C[1]) + dts);
     for (int l = 2; l <= p->L; ++l)
-        if (!conv_mfma_supported(p->C[l - 1], p->C[l], p->dt))
-            return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" + std::to_string(p->C[l]));
+        if (!(bf ? conv_mfma_bf16_supported(p->C[l - 1], p->C[l]) : conv_mfma_supported(p->C[l - 1], p->C[l], p->dt)))
+            return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" +
+                                             std::to_string(p->C[l]) + dts);
     p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
     p->fuse_first = !(cfg->options & RN_OPT_SEPARATE_FIRST) && p->L >= 2 && p->C[0] == 1 && p->stack == 1 &&
                     conv_fused_first_supported(p->C[1], p->C[2], p->dt);
@@ -144,10 +148,12 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     for (int l = 0; l < p->L; ++l) {
         p->w_elems[l] = l == 0 ? conv_first_packed_elems(p->C[0], p->C[1])
                                : conv_mfma_packed_elems(p->C[l], p->C[l + 1], p->dt);
-        p->o_w[l] = take(p->w_elems[l] * 4);
+        // layer 1 keeps float32 weights (bf16-rounded values in bf16 mode); MFMA layers store bf16.
+        p->w_bytes[l] = p->w_elems[l] * ((l > 0 && p->dt == RN_BF16) ? 2 : 4);
+        p->o_w[l] = take(p->w_bytes[l]);
         p->o_b[l] = take((size_t)p->C[l + 1] * 4);
     }
-    p->o_wd = take((size_t)p->N * p->K * p->esz);
+    p->o_wd = take((size_t)p->N * p->K * 4);
     p->o_bd = take((size_t)p->N * 4);
     for (int l = 0; l <= p->L; ++l) {
         p->o_pm[l] = take(S * HWW * 8);
@@ -288,8 +294,15 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
             cv.hw = net->at<float>(p.o_hw);
             cv.hpart = net->at<float>(p.o_hp);
         }
-        if (l == 1) e = timed(net, RN_PHASE_CONV1, s, [&] { return launch_conv_first(cv, p.dt, net->cus, s); });
-        else e = timed(net, RN_PHASE_CONVN, s, [&] { return launch_conv_mfma(cv, p.dt, net->cus, s); });
+        const bool bf = p.dt == RN_BF16;
+        if (l == 1)
+            e = timed(net, RN_PHASE_CONV1, s, [&] {
+                return bf ? launch_conv_first_bf16(cv, net->cus, s) : launch_conv_first(cv, p.dt, net->cus, s);
+            });
+        else
+            e = timed(net, RN_PHASE_CONVN, s, [&] {
+                return bf ? launch_conv_mfma_bf16(cv, net->cus, s) : launch_conv_mfma(cv, p.dt, net->cus, s);
+            });
         if (e != hipSuccess) return e;
     }
     if (tiles_head) {
@@ -476,11 +489,20 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     for (int k = 0; k < 256; ++k) lut[k] = (float)k / 255.0f;   // IEEE division: correctly rounded
     std::vector<int32_t> ids(p.S);
     for (int i = 0; i < p.S; ++i) ids[i] = i;
-    std::vector<std::vector<float>> wpack(p.L);
+    const bool bf = p.dt == RN_BF16;
+    auto rnd = [&](float v) { return bf ? round_bf16_host(v) : v; };
+    std::vector<std::vector<unsigned char>> wpack(p.L);
     for (int l = 0; l < p.L; ++l) {
-        wpack[l].assign(p.w_elems[l], 0.f);
-        if (l == 0) pack_conv_first(w->conv_w[0], p.C[0], p.C[1], p.dt, wpack[l].data());
-        else pack_conv_mfma(w->conv_w[l], p.C[l], p.C[l + 1], p.dt, wpack[l].data());
+        wpack[l].assign(p.w_bytes[l], 0);
+        if (l == 0) {
+            float *d = reinterpret_cast<float *>(wpack[l].data());
+            pack_conv_first(w->conv_w[0], p.C[0], p.C[1], p.dt, d);
+            for (size_t j = 0; j < p.w_elems[0]; ++j) d[j] = rnd(d[j]);
+        } else if (bf) {
+            pack_conv_mfma_bf16(w->conv_w[l], p.C[l], p.C[l + 1], wpack[l].data());
+        } else {
+            pack_conv_mfma(w->conv_w[l], p.C[l], p.C[l + 1], p.dt, wpack[l].data());
+        }
     }
     // Dense weights from (c, y, x) order to the tiled cache order, 0 at padded pixels.
     const int CL = p.C[p.L];
@@ -493,7 +515,7 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
                     if (y >= p.H || x >= p.W) continue;
                     const size_t dst = (size_t)o * p.K + ((size_t)(ty * p.TW + tx) * kTilePx + m) * CL;
                     for (int c = 0; c < CL; ++c)
-                        wd[dst + c] = w->dense_w[(size_t)o * CL * p.H * p.W + ((size_t)c * p.H + y) * p.W + x];
+                        wd[dst + c] = rnd(w->dense_w[(size_t)o * CL * p.H * p.W + ((size_t)c * p.H + y) * p.W + x]);
                 }
 
     hipError_t e = hipMemsetAsync(dev_workspace, 0, p.total, s);
@@ -503,7 +525,7 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     up(p.o_lut, lut.data(), 256 * 4);
     up(p.o_ids, ids.data(), (size_t)p.S * 4);
     for (int l = 0; l < p.L; ++l) {
-        up(p.o_w[l], wpack[l].data(), p.w_elems[l] * 4);
+        up(p.o_w[l], wpack[l].data(), p.w_bytes[l]);
         up(p.o_b[l], w->conv_b[l], (size_t)p.C[l + 1] * 4);
     }
     up(p.o_wd, wd.data(), wd.size() * 4);
@@ -511,6 +533,7 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     if (p.head_mode == RN_HEAD_TILES) {
         hw.assign(tile_head_w_elems(p.ntiles, CL, p.N), 0.f);
         pack_tile_head(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hw.data());
+        for (float &v : hw) v = rnd(v);
         up(p.o_hw, hw.data(), hw.size() * 4);
     }
     up(p.o_bd, w->dense_b, (size_t)p.N * 4);
@@ -629,8 +652,19 @@ rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, 
     }
     const int C = p.C[layer];
     std::vector<float> buf(p.act_stride[layer]);
-    rn_status st = copy_out(net, buf.data(), net->at<float>(p.o_act[layer]) + (size_t)sid * p.act_stride[layer],
-                            p.act_stride[layer] * 4);
+    rn_status st;
+    if (p.dt == RN_BF16) {
+        std::vector<uint16_t> hb(p.act_stride[layer]);
+        st = copy_out(net, hb.data(), net->at<uint16_t>(p.o_act[layer]) + (size_t)sid * p.act_stride[layer],
+                      p.act_stride[layer] * 2);
+        for (size_t j = 0; j < hb.size(); ++j) {
+            const uint32_t u = (uint32_t)hb[j] << 16;
+            memcpy(&buf[j], &u, 4);
+        }
+    } else {
+        st = copy_out(net, buf.data(), net->at<float>(p.o_act[layer]) + (size_t)sid * p.act_stride[layer],
+                      p.act_stride[layer] * 4);
+    }
     if (st != RN_OK) return st;
     for (int y = 0; y < p.H; ++y)
         for (int x = 0; x < p.W; ++x) {

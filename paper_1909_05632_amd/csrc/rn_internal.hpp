@@ -137,6 +137,12 @@ hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt);
 bool conv_first_supported(int cin, int cout, rn_dtype dt);
 bool conv_fused_first_supported(int c1, int c2, rn_dtype dt);
+bool conv_mfma_bf16_supported(int cin, int cout);
+bool conv_first_bf16_supported(int cin, int cout);
+hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s);
+hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s);
+void pack_conv_mfma_bf16(const float *oihw, int cin, int cout, void *dst);
+float round_bf16_host(float v);
 hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
 int head_streams_per_block(int n_out);
 

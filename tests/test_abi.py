@@ -46,6 +46,19 @@ def test_head_modes_size_the_workspace():
     assert B.reuse_net_workspace_bytes(_cfg(head=7)) == 0
 
 
+def test_bf16_configs():
+    full = ((1, 64), (64, 128), (128, 128))
+    assert B.reuse_net_workspace_bytes(_cfg(full, h=210, w=160, n_out=18, dtype=B.RN_BF16)) > 0
+    # bf16 caches are half the size of float32 ones.
+    f32 = B.reuse_net_workspace_bytes(_cfg(full, h=210, w=160, n_out=18, streams=64))
+    b16 = B.reuse_net_workspace_bytes(_cfg(full, h=210, w=160, n_out=18, streams=64, dtype=B.RN_BF16))
+    assert b16 < 0.6 * f32
+    # 40 input channels have no bf16 MFMA kernel (K blocks of 32 channels).
+    assert B.reuse_net_workspace_bytes(_cfg(dtype=B.RN_BF16)) == 0
+    st, h, msg = _create(_cfg(dtype=B.RN_BF16))
+    assert st == B.RN_EUNSUPPORTED and "bf16" in msg
+
+
 def test_separate_first_layer_option_is_accepted():
     assert B.reuse_net_workspace_bytes(_cfg(options=B.RN_OPT_SEPARATE_FIRST)) > 0
 

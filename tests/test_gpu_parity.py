@@ -22,12 +22,16 @@ def torch():
     return torch
 
 
+BF16_REL = 1e-2          # bf16: max |gpu - oracle| <= 1e-2 * max |oracle| per tensor
+
+
 def _run_sequence(torch, wl, streams, frames, weights, slots=None, max_streams=None, u8=False,
-                  sample=None, mask_every=1, value_every=1, label="", head="tiles"):
+                  sample=None, mask_every=1, value_every=1, label="", head="tiles", act_dtype="f32"):
     u8x, x = sprite_inputs(wl, range(streams), frames)
     S = max_streams or streams
-    net = make_net(wl, S, weights, head=head)
-    onet = oracle_net(wl)
+    net = make_net(wl, S, weights, head=head, act_dtype=act_dtype)
+    bf = act_dtype == "bf16"
+    onet = oracle_net(wl, bf16=bf)
     ids = None
     slots = np.arange(streams) if slots is None else np.asarray(slots)
     if not np.array_equal(slots, np.arange(streams)):
@@ -41,7 +45,7 @@ def _run_sequence(torch, wl, streams, frames, weights, slots=None, max_streams=N
             check_masks(net, onet, d0, slots, label=f"{label} t={t}")
         if t % value_every == 0 or t == frames - 1:
             check_values(net, onet, weights, x[t][:, None], slots, sample, logits,
-                         label=f"{label} t={t}")
+                         label=f"{label} t={t}", rel=BF16_REL if bf else None)
     return net
 
 
@@ -281,3 +285,41 @@ def test_fullres_210x160_three_layers(torch):
     wl = synth.WORKLOADS["fullres-1024x32"]
     weights = synth.net_weights(wl)
     _run_sequence(torch, wl, 3, 3, weights, sample=[0], value_every=10, label="210x160").close()
+
+
+def test_bf16_three_layer_small_frames(torch):
+    # bf16 weights and activations, float32 accumulation, on the full-resolution
+    # net's channels; masks and lists bit-exact, values norm-relative 1e-2
+    # against the oracle's bf16 mode.
+    wl = synth.Workload(cid=78, streams=5, frames=6, h=42, w=32, convs=(64, 128, 128), n_out=18,
+                        n_sprites=3, smin=3, smax=6, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    for head in ("tiles", "full"):
+        _run_sequence(torch, wl, 5, 6, weights, label=f"bf16 head={head}", head=head,
+                      act_dtype="bf16").close()
+
+
+def test_bf16_step_equals_full_bitwise(torch):
+    wl = synth.Workload(cid=79, streams=3, frames=2, h=20, w=24, convs=(64, 128, 128), n_out=18)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    u8 = synth.sprite_batch(wl, streams=range(3), frames=2, full_change=True)
+    x = synth.to_f32(u8)
+    dev = torch.from_numpy(x).cuda()
+    a, b = make_net(wl, 3, weights, act_dtype="bf16"), make_net(wl, 3, weights, act_dtype="bf16")
+    a.step(dev[0][:, None].contiguous())
+    la = a.step(dev[1][:, None].contiguous()).cpu().numpy()
+    lb = b.full(dev[1][:, None].contiguous()).cpu().numpy()
+    assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
+    for l in (1, 2, 3):
+        ga = a.activation(1, l)
+        assert np.array_equal(ga.view(np.uint32), b.activation(1, l).view(np.uint32))
+        assert not (ga.view(np.uint32) & 0xFFFF).any()           # every activation is a bf16 value
+    a.close()
+    b.close()
+
+
+def test_bf16_fullres_210x160(torch):
+    wl = synth.WORKLOADS["fullres-1024x32"]
+    weights = synth.net_weights(wl)
+    _run_sequence(torch, wl, 2, 3, weights, sample=[0], value_every=10, label="bf16 210x160",
+                  act_dtype="bf16").close()
