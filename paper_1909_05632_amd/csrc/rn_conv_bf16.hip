@@ -95,179 +95,290 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
 
 // ------------------------------------------------------------------ MFMA layers
 
+// Implicit GEMM over a group of T tiles: M = 16 T pixels, N = COUT, K = 9 CIN.
 // v_mfma_f32_16x16x32_bf16 operand layout (lane l, kq = l / 16):
 //   A: row l % 16, k = 8 kq + j (j = 0..7);  B: k = 8 kq + j, column l % 16;
-//   D: rows 4 kq + i, column l % 16 (as the float32 16x16x4 instruction).
-// Rows are tile pixels in column-major order (row m = pixel (m % 4, m / 4)).
-// K per kernel position is walked in blocks of 32 channels; lane group kq of
-// block b takes channels 32 b + 8 kq .. + 7, one 16-byte LDS read for A; the
-// weights are packed [kpos][block][nb][lane][8] so B is one 16-byte read per
-// nb.  Halo pixel stride CIN + 8 bf16 (a 16-byte pad) puts the 16-byte A reads
-// of each 8-lane phase in distinct banks.  Weights are streamed through LDS
-// in stages of KPS kernel positions for a group of 4 tiles (one per wave).
+//   D: rows 4 kq + i, column l % 16.
+// Rows are tile pixels in column-major order (row m = pixel (m % 4, m / 4)), so
+// lane l of D holds pixels (i, kq), i = 0..3.  K is walked per kernel position
+// in steps of 32 channels; lane group kq of step b takes channels 32 b + 8 kq
+// .. + 7, one 16-byte LDS read for A.  The weights are packed
+// [kpos][step][nb][lane][8] so that B is one 16-byte read per 16 outputs.
+//
+// Register blocking: four waves (one per SIMD) form a 2 x 2 grid; a wave owns
+// MT tiles (16 MT rows) x COUT / 2 outputs, so every A fragment it reads feeds
+// COUT / 32 matrix ops and every B fragment MT.  At the bf16 matrix rate this
+// keeps the LDS traffic at or below half of its 256 bytes per clock.
+//
+// Weights stream through LDS one kernel position per stage, double-buffered:
+// the next stage is fetched into registers while the matrix cores work on the
+// current one, then written to the other buffer, one block barrier per stage.
+// Every group walks the nine positions in the same order, so the stage after
+// position 8 is the next group's position 0 and the pipeline never drains.
+// The halos of the next group are fetched into registers during the second
+// half of the current group.
+//
+// Halo layout in LDS: pixel p = 6 hy + hx at p * PS 16-byte chunks, chunk c of
+// the pixel stored at slot c ^ g(hy, hx) with g taking hy % 4 (and hx % 4 for
+// 16 chunks per pixel).  For every kernel position the 16 rows of a read then
+// fall in 16 distinct bank groups, and so do the 8 rows of each half (checked
+// exhaustively on the host for 32, 64 and 128 channels; 64 channels need the
+// 12-chunk pixel stride).
 template <int CIN, int COUT>
-struct MfmaBf {
+struct GrpBf {
+    static constexpr int WM = 2;                     // waves along M
+    static constexpr int WAVES = 2 * WM;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int MT = CIN >= 128 ? 4 : 8;    // tiles per wave
+    static constexpr int T = WM * MT;                // tiles per group
     static constexpr int NB = COUT / 16;
-    static constexpr int CS = CIN + 8;          // halo pixel stride (bf16 elements)
-    static constexpr int NBLK = CIN / 32;       // k-steps per kernel position
-    static constexpr int C8 = CIN / 8;          // 16-byte chunks per pixel
-    static constexpr int HALO = 36 * CS;        // bf16 elements of one halo in LDS
-    static constexpr int SR = COUT + 8;         // output staging row stride (bf16)
-    static constexpr int HV = (36 * C8 + 63) / 64;
-    static constexpr int WTOT = 9 * CIN * COUT; // bf16 elements
-    static_assert(CIN % 32 == 0 && COUT % 16 == 0, "bf16 MFMA tiling");
+    static constexpr int NBW = NB / 2;               // 16-output blocks per wave
+    static constexpr int C8 = CIN / 8;               // 16-byte chunks per pixel
+    static constexpr int PS = C8 == 8 ? 12 : C8;     // pixel stride in chunks
+    static constexpr int HALO = 36 * PS * 8;         // bf16 elements per tile halo
+    static constexpr int KB = CIN / 32;              // k-steps per kernel position
+    static constexpr int WST = CIN * COUT;           // bf16 elements per weight stage
+    static constexpr int WPT = (WST / 8 + THREADS - 1) / THREADS;      // 16-byte weight loads per thread
+    static constexpr int HCH = T * 36 * C8;                            // 16-byte halo chunks per group
+    static constexpr int HPT = (HCH + THREADS - 1) / THREADS;          // per thread
+    static constexpr int SR = COUT + 8;              // output staging row stride (bf16)
+    static constexpr size_t lds_bytes = (size_t)(T * HALO + 2 * WST) * 2;
+    static_assert(CIN % 32 == 0 && COUT % 32 == 0, "bf16 MFMA tiling");
+    static_assert(C8 == 4 || C8 == 8 || C8 == 16, "halo swizzle is defined for 32, 64, 128 channels");
     static_assert(16 * SR <= HALO, "output staging must fit in the halo area");
 };
 
-template <int CIN, int COUT, int KPS>
-struct StagedBf {
-    static constexpr int NST = (9 + KPS - 1) / KPS;
-    static constexpr int WST = KPS * CIN * COUT;                       // bf16 elements per stage
-    static constexpr size_t lds_bytes = (size_t)(WST + 4 * MfmaBf<CIN, COUT>::HALO) * 2;
-};
+template <int C8>
+__device__ inline int halo_swz(int hy, int hx) {
+    return C8 == 16 ? (hy & 3) | ((hx & 3) << 2) : (hy & 3);
+}
 
-template <int CIN, int COUT, int KPS, bool DENSE>
-__global__ __launch_bounds__(256) void k_conv_mfma_bf16(ConvArgs a) {
-    using M = MfmaBf<CIN, COUT>;
-    using S = StagedBf<CIN, COUT, KPS>;
-    extern __shared__ uint16_t smem16[];
-    __shared__ float s_bias[COUT];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, 4);
-    if (xr.first >= xr.end) return;                       // uniform per block
-    uint16_t *s_w = smem16;
-    uint16_t *halo = smem16 + S::WST + wave * M::HALO;
-    const uint16_t *wg = static_cast<const uint16_t *>(a.w);
+// Element offset (bf16) of chunk c of halo pixel (hy, hx).
+template <int CIN, int COUT>
+__device__ inline int halo_chunk(int hy, int hx, int c) {
+    using G = GrpBf<CIN, COUT>;
+    return ((hy * 6 + hx) * G::PS + (c ^ halo_swz<G::C8>(hy, hx))) * 8;
+}
+
+// Fetch this thread's share of a group's halos: chunk h = tid + THREADS j of
+// T x 36 pixels x C8 chunks; zero outside the image and for absent tiles.
+template <int CIN, int COUT>
+__device__ inline void fetch_group_halos(const ConvArgs &a, const uint32_t *items, int nvalid, u32x4 *regs,
+                                         int tid) {
+    using G = GrpBf<CIN, COUT>;
     const uint16_t *inp = static_cast<const uint16_t *>(a.in);
-    uint16_t *outp = static_cast<uint16_t *>(a.out);
-    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
-    const int mrow = lane & 15, kq = lane >> 4;
-    const int pix = (mrow & 3) * 6 + (mrow >> 2);
+#pragma unroll
+    for (int j = 0; j < G::HPT; ++j) {
+        const int h = tid + G::THREADS * j;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (h < G::HCH) {
+            const int t = h / (36 * G::C8), rem = h - t * (36 * G::C8);
+            const int pos = rem / G::C8, c = rem - pos * G::C8;
+            if (t < nvalid) {
+                const TileRef r = item_ref(a, items[t]);
+                const int hy = pos / 6, hx = pos - hy * 6;
+                const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+                if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+                    v = *reinterpret_cast<const u32x4 *>(
+                        inp + (size_t)r.slot * a.in_stride +
+                        ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN + c * 8);
+            }
+        }
+        regs[j] = v;
+    }
+}
 
-    for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        const int t = g + wave;
-        const bool valid = t < xr.end;
-        TileRef r{0, 0, 0, 0};
-        if (valid) {
-            r = decode<DENSE>(a, t);
-            const uint16_t *src = inp + (size_t)r.slot * a.in_stride;
+template <int CIN, int COUT>
+__device__ inline void store_group_halos(uint16_t *halos, const u32x4 *regs, int tid) {
+    using G = GrpBf<CIN, COUT>;
 #pragma unroll
-            for (int j = 0; j < M::HV; ++j) {
-                const int h = lane + 64 * j;
-                if (h < 36 * M::C8) {
-                    const int pos = h / M::C8, c8 = h - pos * M::C8;
-                    const int hy = pos / 6, hx = pos - hy * 6;
-                    const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
-                    u32x4 v = {0u, 0u, 0u, 0u};
-                    if (y >= 0 && y < a.H && x >= 0 && x < a.W)
-                        v = *reinterpret_cast<const u32x4 *>(
-                            src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
-                            c8 * 8);
-                    *reinterpret_cast<u32x4 *>(halo + pos * M::CS + c8 * 8) = v;
-                }
-            }
-        }
-        floatx4 acc[M::NB];
-#pragma unroll
-        for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int st = 0; st < S::NST; ++st) {
-            __syncthreads();                               // previous stage fully consumed
-            const int n0 = st * S::WST;
-            const int nf = min(S::WST, M::WTOT - n0);
-            for (int j = tid; j < nf / 8; j += blockDim.x)
-                reinterpret_cast<u32x4 *>(s_w)[j] = reinterpret_cast<const u32x4 *>(wg + n0)[j];
-            __syncthreads();
-            if (valid) {
-#pragma unroll
-                for (int kp = 0; kp < KPS; ++kp) {
-                    const int kpos = st * KPS + kp;
-                    if (kpos >= 9) break;
-                    const int ky = kpos / 3, kx = kpos - ky * 3;
-                    const uint16_t *ap = halo + (pix + ky * 6 + kx) * M::CS + 8 * kq;
-#pragma unroll
-                    for (int blk = 0; blk < M::NBLK; ++blk) {
-                        const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ap + 32 * blk));
-                        const uint16_t *wb = s_w + (size_t)((kp * M::NBLK + blk) * M::NB) * 64 * 8 + lane * 8;
-#pragma unroll
-                        for (int nb = 0; nb < M::NB; ++nb) {
-                            const bf16x8 bv = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wb + nb * 64 * 8));
-                            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[nb], 0, 0, 0);
-                        }
-                    }
-                }
-            }
-        }
-        if (valid) {
-            wave_sync();
-            // Epilogue: bias, ReLU, zero outside the image, round to bf16.
-            uint16_t *stage = halo;
-            const bool col_in = r.tx * kTile + kq < a.W;
-#pragma unroll
-            for (int nb = 0; nb < M::NB; ++nb) {
-                const float b = s_bias[nb * 16 + mrow];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float v = acc[nb][i] + b;
-                    v = v > 0.0f ? v : 0.0f;
-                    if (!col_in || r.ty * kTile + i >= a.H) v = 0.0f;
-                    const uint16_t h = f2bf(v);
-                    acc[nb][i] = bf2f(h);                  // the stored value feeds the head
-                    stage[(i * 4 + kq) * M::SR + nb * 16 + mrow] = h;
-                }
-            }
-            wave_sync();
-            u32x4 *d = reinterpret_cast<u32x4 *>(outp + (size_t)r.slot * a.out_stride +
-                                                 (size_t)r.tile * kTilePx * COUT);
-#pragma unroll
-            for (int j = 0; j < (16 * COUT / 8 + 63) / 64; ++j) {
-                const int o8 = lane + 64 * j;
-                if (o8 < 16 * COUT / 8) {
-                    const int e = 8 * o8, m = e / COUT, n = e - m * COUT;
-                    d[o8] = *reinterpret_cast<const u32x4 *>(stage + m * M::SR + n);
-                }
-            }
-            if (a.n_out > 0) {
-                const int ntiles = a.TH * a.TW;
-                for (int o = 0; o < a.n_out; ++o) {
-                    const float4 *w4 = reinterpret_cast<const float4 *>(
-                                           a.hw + ((size_t)o * ntiles + r.tile) * kTilePx * COUT) + lane;
-                    float p = 0.f;
-#pragma unroll
-                    for (int nb = 0; nb < M::NB; ++nb) {
-                        const float4 w = w4[nb * 64];
-                        p = fmaf(acc[nb][0], w.x, p);
-                        p = fmaf(acc[nb][1], w.y, p);
-                        p = fmaf(acc[nb][2], w.z, p);
-                        p = fmaf(acc[nb][3], w.w, p);
-                    }
-                    for (int off = 32; off > 0; off >>= 1) p += __shfl_xor(p, off, 64);
-                    if (lane == 0) a.hpart[((size_t)r.slot * ntiles + r.tile) * a.n_out + o] = p;
-                }
-            }
-            wave_sync();
+    for (int j = 0; j < G::HPT; ++j) {
+        const int h = tid + G::THREADS * j;
+        if (h < G::HCH) {
+            const int t = h / (36 * G::C8), rem = h - t * (36 * G::C8);
+            const int pos = rem / G::C8, c = rem - pos * G::C8;
+            const int hy = pos / 6, hx = pos - hy * 6;
+            *reinterpret_cast<u32x4 *>(halos + t * G::HALO + halo_chunk<CIN, COUT>(hy, hx, c)) = regs[j];
         }
     }
 }
 
-constexpr size_t kLdsBudgetBf = 160 * 1024 - 1024;
+template <int CIN, int COUT>
+__device__ inline void fetch_stage(const uint16_t *wg, int kpos, u32x4 *regs, int tid) {
+    using G = GrpBf<CIN, COUT>;
+    const u32x4 *src = reinterpret_cast<const u32x4 *>(wg + (size_t)kpos * G::WST);
+#pragma unroll
+    for (int j = 0; j < G::WPT; ++j) {
+        const int e = tid + G::THREADS * j;
+        if (e < G::WST / 8) regs[j] = src[e];
+    }
+}
 
 template <int CIN, int COUT>
-constexpr int pick_kps_bf() {
-    return StagedBf<CIN, COUT, 9>::lds_bytes <= kLdsBudgetBf   ? 9
-           : StagedBf<CIN, COUT, 3>::lds_bytes <= kLdsBudgetBf ? 3
-                                                               : 1;
+__device__ inline void store_stage(uint16_t *dst, const u32x4 *regs, int tid) {
+    using G = GrpBf<CIN, COUT>;
+#pragma unroll
+    for (int j = 0; j < G::WPT; ++j) {
+        const int e = tid + G::THREADS * j;
+        if (e < G::WST / 8) reinterpret_cast<u32x4 *>(dst)[e] = regs[j];
+    }
+}
+
+template <int MT, int NBW>
+struct FragsBf {
+    bf16x8 a[MT];
+    bf16x8 b[NBW];
+};
+
+// A and B fragments of k-step kb at kernel position (ky, kx).
+template <int CIN, int COUT>
+__device__ inline void load_frags(FragsBf<GrpBf<CIN, COUT>::MT, GrpBf<CIN, COUT>::NBW> &f, const uint16_t *halos, const uint16_t *wst,
+                                  int ky, int kx, int kb, int wm, int half, int lane) {
+    using G = GrpBf<CIN, COUT>;
+    const int m = lane & 15, kq = lane >> 4;
+    const int hy = (m & 3) + ky, hx = (m >> 2) + kx;
+    const int off = halo_chunk<CIN, COUT>(hy, hx, 4 * kb + kq);
+#pragma unroll
+    for (int mt = 0; mt < G::MT; ++mt)
+        f.a[mt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
+                                                 halos + (wm * G::MT + mt) * G::HALO + off));
+    const uint16_t *wb = wst + ((size_t)(kb * G::NB + half * G::NBW) * 64 + lane) * 8;
+#pragma unroll
+    for (int nb = 0; nb < G::NBW; ++nb)
+        f.b[nb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wb + nb * 64 * 8));
+}
+
+template <int MT, int NBW>
+__device__ inline void mma_frags(floatx4 (&acc)[MT][NBW], const FragsBf<MT, NBW> &f) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+            acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[mt], f.b[nb], acc[mt][nb], 0, 0, 0);
+}
+
+template <int CIN, int COUT, bool DENSE>
+__global__ __launch_bounds__((GrpBf<CIN, COUT>::THREADS)) void k_conv_bf16_grp(ConvArgs a) {
+    using G = GrpBf<CIN, COUT>;
+    extern __shared__ uint16_t smem16[];
+    __shared__ float s_bias[COUT];
+    __shared__ uint32_t s_items[2][G::T];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % G::WM, half = wave / G::WM;
+    const int cnt = work_count<DENSE>(a);
+    const XcdRange xr = xcd_range(cnt, G::T);
+    if (xr.first >= xr.end) return;                       // uniform per block
+    uint16_t *halos = smem16;
+    uint16_t *wbuf = smem16 + G::T * G::HALO;             // two stages
+    const uint16_t *wg = static_cast<const uint16_t *>(a.w);
+    uint16_t *outp = static_cast<uint16_t *>(a.out);
+    for (int j = tid; j < COUT; j += G::THREADS) s_bias[j] = a.bias[j];
+
+    // Prologue: items, halos and weight stage 0 of the first group.
+    int g = xr.first;
+    if (tid < G::T) s_items[0][tid] = g + tid < xr.end ? item_word<DENSE>(a, g + tid) : 0u;
+    u32x4 wreg[G::WPT];
+    fetch_stage<CIN, COUT>(wg, 0, wreg, tid);
+    __syncthreads();
+    {
+        u32x4 hreg[G::HPT];
+        fetch_group_halos<CIN, COUT>(a, s_items[0], min(G::T, xr.end - g), hreg, tid);
+        store_group_halos<CIN, COUT>(halos, hreg, tid);
+    }
+    store_stage<CIN, COUT>(wbuf, wreg, tid);
+    __syncthreads();
+
+    int buf = 0;                                          // weight buffer of the current stage
+    for (int it = 0; g < xr.end; g += xr.stride, ++it) {  // uniform per block
+        const int cur = it & 1;
+        const int nvalid = min(G::T, xr.end - g);
+        const int gn = g + xr.stride;
+        const bool has_next = gn < xr.end;
+        if (tid < G::T) s_items[cur ^ 1][tid] = has_next && gn + tid < xr.end ? item_word<DENSE>(a, gn + tid) : 0u;
+        u32x4 hreg[G::HPT];
+        floatx4 acc[G::MT][G::NBW];
+#pragma unroll
+        for (int mt = 0; mt < G::MT; ++mt)
+#pragma unroll
+            for (int nb = 0; nb < G::NBW; ++nb) acc[mt][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+        for (int kpos = 0; kpos < 9; ++kpos) {
+            // Weights of the next stage (next group's position 0 after position 8).
+            fetch_stage<CIN, COUT>(wg, kpos == 8 ? 0 : kpos + 1, wreg, tid);
+            // Next group's halos: its items were published by the barrier of stage 0.
+            if (kpos == 4 && has_next)
+                fetch_group_halos<CIN, COUT>(a, s_items[cur ^ 1], min(G::T, xr.end - gn), hreg, tid);
+            const uint16_t *wst = wbuf + buf * G::WST;
+            const int ky = kpos / 3, kx = kpos - ky * 3;
+            FragsBf<G::MT, G::NBW> f0, f1;
+            load_frags<CIN, COUT>(f0, halos, wst, ky, kx, 0, wm, half, lane);
+#pragma unroll
+            for (int kb = 0; kb < G::KB; ++kb) {
+                if (kb + 1 < G::KB) {
+                    if (kb & 1) load_frags<CIN, COUT>(f0, halos, wst, ky, kx, kb + 1, wm, half, lane);
+                    else load_frags<CIN, COUT>(f1, halos, wst, ky, kx, kb + 1, wm, half, lane);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (kb & 1) mma_frags<G::MT, G::NBW>(acc, f1);
+                else mma_frags<G::MT, G::NBW>(acc, f0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            store_stage<CIN, COUT>(wbuf + (buf ^ 1) * G::WST, wreg, tid);
+            buf ^= 1;
+            __syncthreads();
+        }
+
+        // Epilogue: bias, ReLU, zero outside the image, round to bf16, stage the
+        // group's outputs in the (now free) halo area, then coalesced stores.
+        uint16_t *stage = halos;
+        const int m = lane & 15, kq = lane >> 4;
+#pragma unroll
+        for (int mt = 0; mt < G::MT; ++mt) {
+            const int t = wm * G::MT + mt;
+            const TileRef r = item_ref(a, s_items[cur][t]);
+            const bool col_in = r.tx * kTile + kq < a.W;
+#pragma unroll
+            for (int nb = 0; nb < G::NBW; ++nb) {
+                const int n = (half * G::NBW + nb) * 16 + m;
+                const float b = s_bias[n];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float v = acc[mt][nb][i] + b;
+                    v = v > 0.0f ? v : 0.0f;
+                    const bool inside = col_in & (r.ty * kTile + i < a.H);
+                    v = inside ? v : 0.0f;
+                    stage[(t * 16 + i * 4 + kq) * G::SR + n] = f2bf(v);
+                }
+            }
+        }
+        __syncthreads();
+        constexpr int V8 = 16 * COUT / 8;                  // 16-byte vectors per tile
+        for (int e = tid; e < G::T * V8; e += G::THREADS) {
+            const int t = e / V8, o8 = e - t * V8;
+            if (t < nvalid) {
+                const TileRef r = item_ref(a, s_items[cur][t]);
+                const int px = (8 * o8) / COUT, n = 8 * o8 - px * COUT;
+                reinterpret_cast<u32x4 *>(outp + (size_t)r.slot * a.out_stride +
+                                          (size_t)r.tile * kTilePx * COUT)[o8] =
+                    *reinterpret_cast<const u32x4 *>(stage + (t * 16 + px) * G::SR + n);
+            }
+        }
+        __syncthreads();
+        if (has_next) store_group_halos<CIN, COUT>(halos, hreg, tid);
+        __syncthreads();
+    }
 }
 
 template <int CIN, int COUT, bool DENSE>
 hipError_t run_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s) {
-    constexpr int KPS = pick_kps_bf<CIN, COUT>();
-    constexpr size_t lds = StagedBf<CIN, COUT, KPS>::lds_bytes;
-    auto kern = k_conv_mfma_bf16<CIN, COUT, KPS, DENSE>;
+    using G = GrpBf<CIN, COUT>;
+    if (a.n_out > 0) return hipErrorInvalidValue;          // head partials come from their own kernel
+    constexpr size_t lds = G::lds_bytes;
+    auto kern = k_conv_bf16_grp<CIN, COUT, DENSE>;
     static hipError_t attr = set_lds(kern, lds);
     if (attr != hipSuccess) return attr;
-    const int grid = persistent_grid(cus, (a.max_tiles + 3) / 4);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
+    const int grid = persistent_grid(cus, (a.max_tiles + G::T - 1) / G::T);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(G::THREADS), lds, s, a);
     return hipGetLastError();
 }
 
@@ -324,6 +435,8 @@ hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s) {
 #undef X
     return hipErrorInvalidValue;
 }
+
+uint16_t bf16_bits_host(float v) { return host_bf16(v); }
 
 float round_bf16_host(float v) {
     const uint32_t u = (uint32_t)host_bf16(v) << 16;

@@ -10,12 +10,22 @@
 // Partials go to [split][stream][o]; a second kernel adds them in split order.
 // Both orders are fixed, so the result is deterministic and a step on an
 // unchanged cache reproduces the previous logits bit for bit.
-#include "rn_internal.hpp"
+#include "rn_device.hpp"
 
 namespace rn {
 namespace {
 
 constexpr int kThreads = 256;
+
+using dev::floatx4;
+using dev::XcdRange;
+using dev::TileRef;
+using dev::xcd_range;
+using dev::item_ref;
+using dev::item_word;
+using dev::work_count;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Four consecutive activations as float32 (float32 or bf16 caches).
 template <typename AT>
@@ -201,6 +211,96 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
     }
 }
 
+// ------------------------------------------------------------------ bf16 tile partials
+
+// Tile contributions to the logits for a bf16 last layer, as a matrix product
+// per tile position: for the tiles of one position P (rows), with the head
+// weights of P (bf16, packed [P][k-step][n-block][lane][8]),
+//   hpart[tile][o] = sum_k act_tile[k] * hw[P][k][o],  k = pixel * C + channel,
+// on v_mfma_f32_16x16x32_bf16 (A: the tile's cache slice read straight from
+// memory, 16 bytes per lane per k-step; products of two bf16 values are exact
+// in float32).  The work list is position-major, so a block of 16 consecutive
+// items mostly shares one position and the position's weights are read once
+// for all of them; a block with several positions makes one pass per
+// position, each row kept only in its own pass.  The four waves split K into
+// fixed quarters and add them in wave order, so a row's result does not
+// depend on which rows share its block: list and dense passes agree bit for
+// bit.
+template <int C, int NBO, bool DENSE>
+__global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
+    constexpr int KS = 16 * C / 32;           // k-steps
+    constexpr int KW = KS / 4;                // per wave
+    __shared__ floatx4 red[4][NBO][64];
+    __shared__ uint32_t s_item[16];
+    __shared__ int s_pos[16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int cnt = work_count<DENSE>(a);
+    const XcdRange xr = xcd_range(cnt, 16);
+    const uint16_t *act = static_cast<const uint16_t *>(a.in);
+    const uint16_t *hw = reinterpret_cast<const uint16_t *>(a.hw);
+    const int ntiles = a.TH * a.TW;
+    const int row = lane & 15, kq = lane >> 4;
+    for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
+        if (tid < 16) {
+            const bool valid = g + tid < xr.end;
+            const uint32_t e = valid ? item_word<DENSE>(a, g + tid) : 0u;
+            s_item[tid] = e;
+            s_pos[tid] = valid ? item_ref(a, e).tile : -1;
+        }
+        __syncthreads();
+        const TileRef r = item_ref(a, s_item[row]);
+        const int my_pos = s_pos[row];
+        const uint16_t *arow = act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C + 8 * kq;
+        uint32_t done = 0;                     // rows handled (same value in every thread)
+        for (;;) {
+            int P = -1;
+            for (int q = 0; q < 16; ++q)
+                if (P < 0 && !((done >> q) & 1) && s_pos[q] >= 0) P = s_pos[q];
+            if (P < 0) break;
+            const bool mine = my_pos == P;
+            floatx4 acc[NBO];
+#pragma unroll
+            for (int nb = 0; nb < NBO; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            const uint16_t *wp = hw + (((size_t)P * KS + wave * KW) * NBO * 64 + lane) * 8;
+#pragma unroll 4
+            for (int s = 0; s < KW; ++s) {
+                u32x4 av = {0u, 0u, 0u, 0u};
+                if (mine) av = *reinterpret_cast<const u32x4 *>(arow + 32 * (wave * KW + s));
+                const bf16x8 a8 = __builtin_bit_cast(bf16x8, av);
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) {
+                    const bf16x8 b8 = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u32x4 *>(wp + ((size_t)s * NBO + nb) * 64 * 8));
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b8, acc[nb], 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int nb = 0; nb < NBO; ++nb) red[wave][nb][lane] = acc[nb];
+            __syncthreads();
+            if (wave == 0) {
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) {
+                    floatx4 v = red[0][nb][lane];
+#pragma unroll
+                    for (int w = 1; w < 4; ++w) v += red[w][nb][lane];
+                    const int o = nb * 16 + row;      // D: rows 4 kq + i, column lane % 16
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = 4 * kq + i;
+                        if (o < a.n_out && s_pos[q] == P) {
+                            const TileRef rq = item_ref(a, s_item[q]);
+                            a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = v[i];
+                        }
+                    }
+                }
+            }
+            for (int q = 0; q < 16; ++q)
+                if (s_pos[q] == P) done |= 1u << q;
+            __syncthreads();                   // red is reused by the next pass
+        }
+    }
+}
+
 }  // namespace
 
 int head_streams_per_block(int n_out) { return n_out == 18 ? 4 : 8; }
@@ -226,6 +326,53 @@ hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
     const int tot = a.n * a.n_out;
     hipLaunchKernelGGL(k_head_reduce, dim3((tot + 3) / 4), dim3(kThreads), 0, s, a);
     return hipGetLastError();
+}
+
+size_t tile_part_bf16_elems(int ntiles, int C, int n_out) {
+    const int nbo = n_out <= 16 ? 1 : n_out <= 32 ? 2 : 4;
+    return (size_t)ntiles * kTilePx * C * 16 * nbo;
+}
+
+void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, uint16_t *dst) {
+    // [tile][k-step][n-block][lane][j]: k = 32 step + 8 (lane / 16) + j is
+    // pixel k / C (row-major in the tile) and channel k % C; column
+    // o = 16 n-block + lane % 16.  Zero for o >= n_out and outside the image.
+    const int nbo = n_out <= 16 ? 1 : n_out <= 32 ? 2 : 4;
+    const int ntiles = TH * TW, KS = kTilePx * C / 32;
+    size_t d = 0;
+    for (int t = 0; t < ntiles; ++t) {
+        const int ty = t / TW, tx = t % TW;
+        for (int s = 0; s < KS; ++s)
+            for (int nb = 0; nb < nbo; ++nb)
+                for (int l = 0; l < 64; ++l)
+                    for (int j = 0; j < 8; ++j) {
+                        const int k = 32 * s + 8 * (l / 16) + j, m = k / C, c = k % C;
+                        const int o = nb * 16 + l % 16, y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
+                        const float v = (o < n_out && y < H && x < W)
+                                            ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x]
+                                            : 0.f;
+                        dst[d++] = bf16_bits_host(v);
+                    }
+    }
+}
+
+template <int C, bool DENSE>
+hipError_t run_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
+    const int grid = dev::persistent_grid(cus * 4, (a.max_tiles + 15) / 16);
+    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_bf16<C, 1, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_bf16<C, 2, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_tile_part_bf16<C, 4, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+bool tile_part_bf16_supported(int C) { return C == 64 || C == 128; }
+
+hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
+    const bool dense = a.wl == nullptr;
+    if (a.cout == 64) return dense ? run_tile_part_bf16<64, true>(a, cus, s) : run_tile_part_bf16<64, false>(a, cus, s);
+    if (a.cout == 128)
+        return dense ? run_tile_part_bf16<128, true>(a, cus, s) : run_tile_part_bf16<128, false>(a, cus, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s) {

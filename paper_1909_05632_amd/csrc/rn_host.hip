@@ -115,8 +115,11 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
     p->fuse_first = !(cfg->options & RN_OPT_SEPARATE_FIRST) && p->L >= 2 && p->C[0] == 1 && p->stack == 1 &&
                     conv_fused_first_supported(p->C[1], p->C[2], p->dt);
-    // The tile-partial head lives in the epilogue of an MFMA layer.
-    p->head_mode = (cfg->head_mode == RN_HEAD_TILES && p->L >= 2) ? RN_HEAD_TILES : RN_HEAD_FULL;
+    // The tile-partial head lives in the epilogue of an MFMA layer (float32) or
+    // in its own matrix kernel after the last layer (bf16).
+    p->head_mode = (cfg->head_mode == RN_HEAD_TILES && p->L >= 2 && (!bf || tile_part_bf16_supported(p->C[p->L])))
+                       ? RN_HEAD_TILES
+                       : RN_HEAD_FULL;
     p->head_sg = head_streams_per_block(p->N);
     size_t part = 0;
     for (int n = 1; n <= p->S; ++n) {
@@ -168,7 +171,9 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_cnt = take((RN_MAX_CONV + 1) * 4);
     const bool tiles_head = p->head_mode == RN_HEAD_TILES;
     p->o_part = take(tiles_head ? 0 : p->part_elems * 4);
-    p->o_hw = take(tiles_head ? tile_head_w_elems(p->ntiles, p->C[p->L], p->N) * 4 : 0);
+    p->o_hw = take(!tiles_head ? 0
+                   : p->dt == RN_BF16 ? tile_part_bf16_elems(p->ntiles, p->C[p->L], p->N) * 2
+                                      : tile_head_w_elems(p->ntiles, p->C[p->L], p->N) * 4);
     p->o_hp = take(tiles_head ? S * p->ntiles * p->N * 4 : 0);
     p->total = off;
     return RN_OK;
@@ -260,6 +265,7 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
     const Plan &p = net->p;
     const bool tiles_head = p.head_mode == RN_HEAD_TILES;
     hipError_t e = hipSuccess;
+    ConvArgs last{};
     for (int l = 1; l <= p.L; ++l) {
         if (l == 1 && p.fuse_first) continue;            // computed inside layer 2
         ConvArgs cv{};
@@ -289,12 +295,14 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
             cv.w1 = net->at<float>(p.o_w[0]);
             cv.b1 = net->at<float>(p.o_b[0]);
         }
+        const bool bf = p.dt == RN_BF16;
         if (l == p.L && tiles_head) {
             cv.n_out = p.N;
             cv.hw = net->at<float>(p.o_hw);
             cv.hpart = net->at<float>(p.o_hp);
+            last = cv;
+            if (bf) cv.n_out = 0;                         // partials from their own kernel below
         }
-        const bool bf = p.dt == RN_BF16;
         if (l == 1)
             e = timed(net, RN_PHASE_CONV1, s, [&] {
                 return bf ? launch_conv_first_bf16(cv, net->cus, s) : launch_conv_first(cv, p.dt, net->cus, s);
@@ -303,6 +311,14 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
             e = timed(net, RN_PHASE_CONVN, s, [&] {
                 return bf ? launch_conv_mfma_bf16(cv, net->cus, s) : launch_conv_mfma(cv, p.dt, net->cus, s);
             });
+        if (e != hipSuccess) return e;
+    }
+    if (tiles_head && p.dt == RN_BF16) {
+        // bf16: the tiles of the last work list (every tile in dense mode) get
+        // their partials from the matrix kernel, reading the updated cache.
+        last.in = net->at<void>(p.o_act[p.L]);
+        last.in_stride = p.act_stride[p.L];
+        e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_part_bf16(last, net->cus, s); });
         if (e != hipSuccess) return e;
     }
     if (tiles_head) {
@@ -530,7 +546,12 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     }
     up(p.o_wd, wd.data(), wd.size() * 4);
     std::vector<float> hw;
-    if (p.head_mode == RN_HEAD_TILES) {
+    std::vector<uint16_t> hwb;
+    if (p.head_mode == RN_HEAD_TILES && bf) {
+        hwb.assign(tile_part_bf16_elems(p.ntiles, CL, p.N), 0);
+        pack_tile_part_bf16(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hwb.data());
+        up(p.o_hw, hwb.data(), hwb.size() * 2);
+    } else if (p.head_mode == RN_HEAD_TILES) {
         hw.assign(tile_head_w_elems(p.ntiles, CL, p.N), 0.f);
         pack_tile_head(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hw.data());
         for (float &v : hw) v = rnd(v);

@@ -143,6 +143,13 @@ hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s);
 hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s);
 void pack_conv_mfma_bf16(const float *oihw, int cin, int cout, void *dst);
 float round_bf16_host(float v);
+uint16_t bf16_bits_host(float v);
+// bf16 tile head partials (last layer bf16, tile head): hw is the packed bf16
+// weights of pack_tile_part_bf16, `in` the last cache, cout its channels.
+bool tile_part_bf16_supported(int C);
+size_t tile_part_bf16_elems(int ntiles, int C, int n_out);
+void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, uint16_t *dst);
+hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
 int head_streams_per_block(int n_out);
 

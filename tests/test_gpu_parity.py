@@ -299,6 +299,17 @@ def test_bf16_three_layer_small_frames(torch):
                       act_dtype="bf16").close()
 
 
+def test_bf16_narrow_channels(torch):
+    # The 32->64 and 64->64 bf16 matrix kernels and the 64-channel bf16 tile
+    # head, on ragged frames (tile groups and head blocks with partial fills).
+    wl = synth.Workload(cid=80, streams=6, frames=4, h=30, w=28, convs=(32, 64, 64), n_out=6,
+                        n_sprites=3, smin=3, smax=6, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    for head in ("tiles", "full"):
+        _run_sequence(torch, wl, 6, 4, weights, label=f"bf16 narrow head={head}", head=head,
+                      act_dtype="bf16").close()
+
+
 def test_bf16_step_equals_full_bitwise(torch):
     wl = synth.Workload(cid=79, streams=3, frames=2, h=20, w=24, convs=(64, 128, 128), n_out=18)
     weights = synth.net_weights(wl, bias_std=0.05)
