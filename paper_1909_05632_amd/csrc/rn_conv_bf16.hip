@@ -4,6 +4,7 @@
 // duties as the float32 kernels in rn_conv.hip (bias, ReLU, zero outside the
 // image, scatter into the tiled cache, tile head partials).
 #include <cstring>
+#include <utility>
 
 #include "rn_device.hpp"
 
@@ -13,6 +14,8 @@ namespace {
 using namespace dev;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // float -> bf16 bits, round to nearest even (NaN stays a quiet NaN).
@@ -95,122 +98,137 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
 
 // ------------------------------------------------------------------ MFMA layers
 
-// Implicit GEMM over a group of T tiles: M = 16 T pixels, N = COUT, K = 9 CIN.
-// v_mfma_f32_16x16x32_bf16 operand layout (lane l, kq = l / 16):
-//   A: row l % 16, k = 8 kq + j (j = 0..7);  B: k = 8 kq + j, column l % 16;
-//   D: rows 4 kq + i, column l % 16.
-// Rows are tile pixels in column-major order (row m = pixel (m % 4, m / 4)), so
-// lane l of D holds pixels (i, kq), i = 0..3.  K is walked per kernel position
-// in steps of 32 channels; lane group kq of step b takes channels 32 b + 8 kq
-// .. + 7, one 16-byte LDS read for A.  The weights are packed
-// [kpos][step][nb][lane][8] so that B is one 16-byte read per 16 outputs.
+// Implicit GEMM over a group of T = 16 tiles: M = 256 pixels, N = COUT,
+// K = 9 CIN, on v_mfma_f32_32x32x16_bf16 (one wave per SIMD issues this
+// instruction at close to the full matrix rate; the 16x16x32 one needs two).
+// Operand layout (lane l, h = l / 32):
+//   A: row l % 32, k = 8 h + j (j = 0..7);  B: k = 8 h + j, column l % 32;
+//   D: element i of lane l is row 8 (i / 4) + 4 h + i % 4, column l % 32.
+// The product is formed transposed, D = W^T X: A holds 32 output channels,
+// B the 32 pixels of a pair of tiles (column c = tile 2 p + c / 16, pixel c %
+// 16 in column-major order: pixel (c % 4, (c % 16) / 4)).  Lane l of D then
+// holds, for each g = 0..3, the four neighbouring channels 8 g + 4 h .. + 3 of
+// one pixel, which the epilogue rounds and stores as one 8-byte word.  K is
+// walked in steps of 16 channels of one kernel position; lane half h reads
+// channels 8 h .. + 7 of the step, one 16-byte LDS read per operand.  The
+// weights are packed [kpos][step][n-block][lane][8] (lane l: output 32 n-block
+// + l % 32).
 //
 // Register blocking: four waves (one per SIMD) form a 2 x 2 grid; a wave owns
-// MT tiles (16 MT rows) x COUT / 2 outputs, so every A fragment it reads feeds
-// COUT / 32 matrix ops and every B fragment MT.  At the bf16 matrix rate this
-// keeps the LDS traffic at or below half of its 256 bytes per clock.
+// 8 tiles (256 rows of the transposed product... 4 tile pairs) x COUT / 2
+// outputs, so every weight fragment it reads feeds four matrix ops and every
+// halo fragment COUT / 64.  At the matrix rate this keeps the LDS traffic near
+// 100 of its 256 bytes per clock.
 //
-// Weights stream through LDS one kernel position per stage, double-buffered:
-// the next stage is fetched into registers while the matrix cores work on the
-// current one, then written to the other buffer, one block barrier per stage.
-// Every group walks the nine positions in the same order, so the stage after
-// position 8 is the next group's position 0 and the pipeline never drains.
-// The halos of the next group are fetched into registers during the second
-// half of the current group.
+// Loop nest per group: for each chunk of HC = min(CIN, 64) input channels (a
+// "pass"), the chunk's halos of the 16 tiles sit in LDS and the nine kernel
+// positions stream their weights for that chunk through LDS, one position per
+// stage, double-buffered.  Each weight byte brought to the CU serves 16 tiles
+// and each halo byte is brought once.  The weights two stages ahead are
+// fetched into registers at the start of a stage and written to the free
+// buffer at the start of the next stage; the next pass's halo chunk (the next
+// group's first chunk after the last pass) is fetched in two halves, after the
+// matrix ops of stages 1 and 3, and written to LDS once the pass is done.  The
+// nine stages are unrolled and every load is issued on every path (a halo
+// chunk outside the image reads a fixed valid address and is dropped when
+// stored), so each wait names exactly the loads it needs, all issued at least
+// a stage earlier.  Each stage ends with one block barrier.
 //
-// Halo layout in LDS: pixel p = 6 hy + hx at p * PS 16-byte chunks, chunk c of
-// the pixel stored at slot c ^ g(hy, hx) with g taking hy % 4 (and hx % 4 for
-// 16 chunks per pixel).  For every kernel position the 16 rows of a read then
-// fall in 16 distinct bank groups, and so do the 8 rows of each half (checked
-// exhaustively on the host for 32, 64 and 128 channels; 64 channels need the
-// 12-chunk pixel stride).
+// Halo layout in LDS: pixel p = 6 hy + hx at p * C8 16-byte chunks, chunk c of
+// the pixel stored at slot c ^ g(hy, hx), g = 2 (hy % 4) + (hx / 2) % 2 for 8
+// chunks per pixel and hy % 4 for 4.  The LDS serves 16 lanes of a 16-byte
+// read per clock (256 bytes); the 16 pixels such a group reads (one tile, one
+// chunk) then fall in 16 distinct bank groups for every kernel position
+// (checked exhaustively on the host).
 template <int CIN, int COUT>
 struct GrpBf {
-    static constexpr int WM = 2;                     // waves along M
-    static constexpr int WAVES = 2 * WM;
-    static constexpr int THREADS = 64 * WAVES;
-    static constexpr int MT = CIN >= 128 ? 4 : 8;    // tiles per wave
-    static constexpr int T = WM * MT;                // tiles per group
-    static constexpr int NB = COUT / 16;
-    static constexpr int NBW = NB / 2;               // 16-output blocks per wave
-    static constexpr int C8 = CIN / 8;               // 16-byte chunks per pixel
-    static constexpr int PS = C8 == 8 ? 12 : C8;     // pixel stride in chunks
-    static constexpr int HALO = 36 * PS * 8;         // bf16 elements per tile halo
-    static constexpr int KB = CIN / 32;              // k-steps per kernel position
-    static constexpr int WST = CIN * COUT;           // bf16 elements per weight stage
-    static constexpr int WPT = (WST / 8 + THREADS - 1) / THREADS;      // 16-byte weight loads per thread
-    static constexpr int HCH = T * 36 * C8;                            // 16-byte halo chunks per group
-    static constexpr int HPT = (HCH + THREADS - 1) / THREADS;          // per thread
-    static constexpr int SR = COUT + 8;              // output staging row stride (bf16)
-    static constexpr size_t lds_bytes = (size_t)(T * HALO + 2 * WST) * 2;
-    static_assert(CIN % 32 == 0 && COUT % 32 == 0, "bf16 MFMA tiling");
-    static_assert(C8 == 4 || C8 == 8 || C8 == 16, "halo swizzle is defined for 32, 64, 128 channels");
-    static_assert(16 * SR <= HALO, "output staging must fit in the halo area");
+    static constexpr int THREADS = 512;              // eight waves, 4 (M) x 2 (N)
+    static constexpr int WM = 4;
+    static constexpr int MP = 2;                     // tile pairs per wave
+    static constexpr int T = WM * 2 * MP;            // tiles per group
+    static constexpr int NB = COUT / 32;             // 32-output blocks
+    static constexpr int NBW = NB / 2;               // per wave
+    static constexpr int HC = CIN < 64 ? CIN : 64;   // channels per pass
+    static constexpr int NPASS = CIN / HC;
+    static constexpr int C8 = HC / 8;                // 16-byte chunks per pixel and pass
+    static constexpr int HALO = 36 * C8 * 8;         // bf16 elements per tile halo chunk
+    static constexpr int KS = HC / 16;               // k-steps per stage
+    static constexpr int WST = HC * COUT;            // bf16 elements per weight stage
+    static constexpr int WPT = (WST / 8 + THREADS - 1) / THREADS;   // 16-byte weight loads per thread and stage
+    static constexpr int PSTEP = THREADS / T / C8;   // pixel step of a thread's halo chunks
+    static constexpr int HPT = (36 + PSTEP - 1) / PSTEP;            // halo chunks per thread and pass
+    static constexpr size_t lds_bytes = (size_t)(T * HALO + 3 * WST) * 2;
+    static_assert(CIN % HC == 0 && HC % 32 == 0 && COUT % 64 == 0, "bf16 MFMA tiling");
+    static_assert(C8 == 4 || C8 == 8, "halo swizzle is defined for 32- and 64-channel chunks");
+    static_assert(THREADS % (T * C8) == 0, "whole halo pixels per thread group");
 };
-
-template <int C8>
-__device__ inline int halo_swz(int hy, int hx) {
-    return C8 == 16 ? (hy & 3) | ((hx & 3) << 2) : (hy & 3);
-}
 
 // Element offset (bf16) of chunk c of halo pixel (hy, hx).
 template <int CIN, int COUT>
 __device__ inline int halo_chunk(int hy, int hx, int c) {
     using G = GrpBf<CIN, COUT>;
-    return ((hy * 6 + hx) * G::PS + (c ^ halo_swz<G::C8>(hy, hx))) * 8;
+    const int g = G::C8 == 8 ? 2 * (hy & 3) + ((hx >> 1) & 1) : (hy & 3);
+    return ((hy * 6 + hx) * G::C8 + (c ^ g)) * 8;
 }
 
-// Fetch this thread's share of a group's halos: chunk h = tid + THREADS j of
-// T x 36 pixels x C8 chunks; zero outside the image and for absent tiles.
-template <int CIN, int COUT>
-__device__ inline void fetch_group_halos(const ConvArgs &a, const uint32_t *items, int nvalid, u32x4 *regs,
-                                         int tid) {
+// Halo chunk j of pass `pass` of a group: the THREADS / T threads tid / (THREADS
+// / T) = t serve tile t; thread tid takes chunk c = tid % C8 of pixel p0 +
+// PSTEP j, p0 = (tid % (THREADS / T)) / C8.  The load is always issued (from
+// the cache's first element when the pixel is outside the image, past 36 or
+// of an absent tile) and bit j of `ok` says whether it counts.
+template <int CIN, int COUT, int J>
+__device__ inline void fetch_halo_chunk(const ConvArgs &a, const uint32_t *items, int nvalid, int pass, u32x4 *regs,
+                                        uint32_t &ok, int tid) {
     using G = GrpBf<CIN, COUT>;
+    constexpr int TPT = G::THREADS / G::T;           // threads per tile
     const uint16_t *inp = static_cast<const uint16_t *>(a.in);
-#pragma unroll
-    for (int j = 0; j < G::HPT; ++j) {
-        const int h = tid + G::THREADS * j;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (h < G::HCH) {
-            const int t = h / (36 * G::C8), rem = h - t * (36 * G::C8);
-            const int pos = rem / G::C8, c = rem - pos * G::C8;
-            if (t < nvalid) {
-                const TileRef r = item_ref(a, items[t]);
-                const int hy = pos / 6, hx = pos - hy * 6;
-                const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
-                if (y >= 0 && y < a.H && x >= 0 && x < a.W)
-                    v = *reinterpret_cast<const u32x4 *>(
-                        inp + (size_t)r.slot * a.in_stride +
-                        ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN + c * 8);
-            }
-        }
-        regs[j] = v;
-    }
+    const int t = tid / TPT, c = tid % G::C8, p0 = (tid % TPT) / G::C8;
+    const TileRef r = item_ref(a, items[t]);
+    const int pos = p0 + G::PSTEP * J;
+    const int hy = pos / 6, hx = pos - hy * 6;
+    const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+    const bool in = t < nvalid && pos < 36 && y >= 0 && y < a.H && x >= 0 && x < a.W;
+    const size_t e = in ? (size_t)r.slot * a.in_stride + pass * G::HC + c * 8 +
+                              ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN
+                        : 0;
+    regs[J] = *reinterpret_cast<const u32x4 *>(inp + e);
+    ok = in ? ok | (1u << J) : ok & ~(1u << J);
+}
+
+template <int CIN, int COUT, int J0, int J1>
+__device__ inline void fetch_halos(const ConvArgs &a, const uint32_t *items, int nvalid, int pass, u32x4 *regs,
+                                   uint32_t &ok, int tid) {
+    [&]<int... J>(std::integer_sequence<int, J...>) {
+        (fetch_halo_chunk<CIN, COUT, J0 + J>(a, items, nvalid, pass, regs, ok, tid), ...);
+    }(std::make_integer_sequence<int, J1 - J0>{});
 }
 
 template <int CIN, int COUT>
-__device__ inline void store_group_halos(uint16_t *halos, const u32x4 *regs, int tid) {
+__device__ inline void store_halos(uint16_t *halos, const u32x4 *regs, uint32_t ok, int tid) {
     using G = GrpBf<CIN, COUT>;
+    constexpr int TPT = G::THREADS / G::T;
+    const int t = tid / TPT, c = tid % G::C8, p0 = (tid % TPT) / G::C8;
 #pragma unroll
     for (int j = 0; j < G::HPT; ++j) {
-        const int h = tid + G::THREADS * j;
-        if (h < G::HCH) {
-            const int t = h / (36 * G::C8), rem = h - t * (36 * G::C8);
-            const int pos = rem / G::C8, c = rem - pos * G::C8;
-            const int hy = pos / 6, hx = pos - hy * 6;
-            *reinterpret_cast<u32x4 *>(halos + t * G::HALO + halo_chunk<CIN, COUT>(hy, hx, c)) = regs[j];
-        }
+        const int pos = p0 + G::PSTEP * j;
+        if (36 % G::PSTEP != 0 && pos >= 36) break;
+        const int hy = pos / 6, hx = pos - hy * 6;
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4 *>(halos + t * G::HALO + halo_chunk<CIN, COUT>(hy, hx, c)) =
+            (ok >> j) & 1 ? regs[j] : z;
     }
 }
 
+// Weight stage q = pass * 9 + kpos: kernel position kpos, channels of the pass.
 template <int CIN, int COUT>
-__device__ inline void fetch_stage(const uint16_t *wg, int kpos, u32x4 *regs, int tid) {
+__device__ inline void fetch_stage(const uint16_t *wg, int q, u32x4 *regs, int tid) {
     using G = GrpBf<CIN, COUT>;
-    const u32x4 *src = reinterpret_cast<const u32x4 *>(wg + (size_t)kpos * G::WST);
+    const int pass = q / 9, kpos = q - pass * 9;
+    const u32x4 *src = reinterpret_cast<const u32x4 *>(wg + (size_t)kpos * CIN * COUT + (size_t)pass * G::WST);
 #pragma unroll
     for (int j = 0; j < G::WPT; ++j) {
         const int e = tid + G::THREADS * j;
-        if (e < G::WST / 8) regs[j] = src[e];
+        if ((G::WST / 8) % G::THREADS == 0 || e < G::WST / 8) regs[j] = src[e];
     }
 }
 
@@ -220,152 +238,217 @@ __device__ inline void store_stage(uint16_t *dst, const u32x4 *regs, int tid) {
 #pragma unroll
     for (int j = 0; j < G::WPT; ++j) {
         const int e = tid + G::THREADS * j;
-        if (e < G::WST / 8) reinterpret_cast<u32x4 *>(dst)[e] = regs[j];
+        if ((G::WST / 8) % G::THREADS == 0 || e < G::WST / 8) reinterpret_cast<u32x4 *>(dst)[e] = regs[j];
     }
 }
 
-template <int MT, int NBW>
+// Fragments of one 16-channel k-step: the halo columns of the wave's MP tile
+// pairs and the weight rows of its NBW 32-output blocks.
+template <int MP, int NBW>
 struct FragsBf {
-    bf16x8 a[MT];
-    bf16x8 b[NBW];
+    bf16x8 xb[MP];
+    bf16x8 wa[NBW];
 };
 
-// A and B fragments of k-step kb at kernel position (ky, kx).
 template <int CIN, int COUT>
-__device__ inline void load_frags(FragsBf<GrpBf<CIN, COUT>::MT, GrpBf<CIN, COUT>::NBW> &f, const uint16_t *halos, const uint16_t *wst,
-                                  int ky, int kx, int kb, int wm, int half, int lane) {
+__device__ inline void load_kstep(FragsBf<GrpBf<CIN, COUT>::MP, GrpBf<CIN, COUT>::NBW> &f, const uint16_t *halos,
+                                  const uint16_t *wst, int kpos, int s, int wm, int half, int lane) {
     using G = GrpBf<CIN, COUT>;
-    const int m = lane & 15, kq = lane >> 4;
-    const int hy = (m & 3) + ky, hx = (m >> 2) + kx;
-    const int off = halo_chunk<CIN, COUT>(hy, hx, 4 * kb + kq);
+    const int ky = kpos / 3, kx = kpos - ky * 3;
+    const int col = lane & 31, h = lane >> 5, m = col & 15;
+    const int off = halo_chunk<CIN, COUT>((m & 3) + ky, (m >> 2) + kx, 2 * s + h);
+    const uint16_t *hb = halos + (wm * 2 * G::MP + (col >> 4)) * G::HALO + off;
+    const uint16_t *wb = wst + (((size_t)s * G::NB + half * G::NBW) * 64 + lane) * 8;
 #pragma unroll
-    for (int mt = 0; mt < G::MT; ++mt)
-        f.a[mt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
-                                                 halos + (wm * G::MT + mt) * G::HALO + off));
-    const uint16_t *wb = wst + ((size_t)(kb * G::NB + half * G::NBW) * 64 + lane) * 8;
+    for (int p = 0; p < G::MP; ++p)
+        f.xb[p] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(hb + 2 * p * G::HALO));
 #pragma unroll
     for (int nb = 0; nb < G::NBW; ++nb)
-        f.b[nb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wb + nb * 64 * 8));
+        f.wa[nb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wb + nb * 512));
 }
 
-template <int MT, int NBW>
-__device__ inline void mma_frags(floatx4 (&acc)[MT][NBW], const FragsBf<MT, NBW> &f) {
+// The matrix work of one stage (kernel position kpos) on the wave's MP tile
+// pairs x NBW 32-output blocks.  The first k-step's fragments arrive in f0
+// (read before the previous stage's barrier); each later k-step is read just
+// before its matrix ops (the other wave of the SIMD runs meanwhile).
+template <int CIN, int COUT, int MP, int NBW, typename Mid>
+__device__ inline void stage_mma(floatx16 (&acc)[MP][NBW], const FragsBf<MP, NBW> &f0, const uint16_t *halos,
+                                 const uint16_t *wst, int kpos, int wm, int half, int lane, Mid &&mid) {
+    using G = GrpBf<CIN, COUT>;
+    static_assert(MP == G::MP && NBW == G::NBW, "accumulator shape");
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int s = 0; s < G::KS; ++s) {
+        FragsBf<MP, NBW> f;
+        if (s == 0) f = f0;
+        else load_kstep<CIN, COUT>(f, halos, wst, kpos, s, wm, half, lane);
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-            acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[mt], f.b[nb], acc[mt][nb], 0, 0, 0);
+        for (int p = 0; p < MP; ++p)
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                acc[p][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.wa[nb], f.xb[p], acc[p][nb], 0, 0, 0);
+        // The stage's memory work goes out while the first k-step's matrix
+        // ops run (pinned there: the scheduler would sink the loads to the
+        // end of the stage, leaving them a barrier's distance to arrive).
+        __builtin_amdgcn_sched_barrier(0);
+        if (s == 0) {
+            mid();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
 }
 
 template <int CIN, int COUT, bool DENSE>
-__global__ __launch_bounds__((GrpBf<CIN, COUT>::THREADS)) void k_conv_bf16_grp(ConvArgs a) {
+__global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     using G = GrpBf<CIN, COUT>;
+    constexpr int NQ = 9 * G::NPASS;                      // stages per group
     extern __shared__ uint16_t smem16[];
-    __shared__ float s_bias[COUT];
-    __shared__ uint32_t s_items[2][G::T];
+    __shared__ __align__(16) float s_bias[COUT];
+    __shared__ uint32_t s_items[3][G::T];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % G::WM, half = wave / G::WM;
     const int cnt = work_count<DENSE>(a);
     const XcdRange xr = xcd_range(cnt, G::T);
     if (xr.first >= xr.end) return;                       // uniform per block
     uint16_t *halos = smem16;
-    uint16_t *wbuf = smem16 + G::T * G::HALO;             // two stages
+    uint16_t *wbuf = smem16 + G::T * G::HALO;             // three stages; stage q of a group in q % 3
     const uint16_t *wg = static_cast<const uint16_t *>(a.w);
     uint16_t *outp = static_cast<uint16_t *>(a.out);
     for (int j = tid; j < COUT; j += G::THREADS) s_bias[j] = a.bias[j];
+    // Work items of group k (k strides after the first), 0 past the end.
+    auto items_of = [&](int k) -> uint32_t {
+        const int t = xr.first + k * xr.stride + tid;
+        return t < xr.end && tid < G::T ? item_word<DENSE>(a, t) : 0u;
+    };
+    auto nvalid_of = [&](int k) { return max(0, min(G::T, xr.end - (xr.first + k * xr.stride))); };
 
-    // Prologue: items, halos and weight stage 0 of the first group.
-    int g = xr.first;
-    if (tid < G::T) s_items[0][tid] = g + tid < xr.end ? item_word<DENSE>(a, g + tid) : 0u;
+    // Prologue: items of groups 0 and 1 in LDS, of group 2 in flight (items are
+    // written to LDS a group before the halo fetch that reads them and loaded
+    // a group before that); pass 0 halos and weight stages 0 and 1 in LDS,
+    // stage 2 in flight to registers.
+    if (tid < G::T) {
+        s_items[0][tid] = items_of(0);
+        s_items[1][tid] = items_of(1);
+    }
+    uint32_t ireg = items_of(2);
     u32x4 wreg[G::WPT];
     fetch_stage<CIN, COUT>(wg, 0, wreg, tid);
-    __syncthreads();
-    {
-        u32x4 hreg[G::HPT];
-        fetch_group_halos<CIN, COUT>(a, s_items[0], min(G::T, xr.end - g), hreg, tid);
-        store_group_halos<CIN, COUT>(halos, hreg, tid);
-    }
+    lds_barrier();
+    u32x4 hreg[G::HPT];
+    uint32_t hok = 0;
+    fetch_halos<CIN, COUT, 0, G::HPT>(a, s_items[0], nvalid_of(0), 0, hreg, hok, tid);
+    store_halos<CIN, COUT>(halos, hreg, hok, tid);
     store_stage<CIN, COUT>(wbuf, wreg, tid);
-    __syncthreads();
+    fetch_stage<CIN, COUT>(wg, 1, wreg, tid);
+    store_stage<CIN, COUT>(wbuf + G::WST, wreg, tid);
+    fetch_stage<CIN, COUT>(wg, 2, wreg, tid);
+    lds_barrier();
+    FragsBf<G::MP, G::NBW> f0;                            // first k-step of the next stage
+    load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
+    for (int it = 0;; ++it) {                             // groups, uniform per block
+        const int g = xr.first + it * xr.stride;
+        if (g >= xr.end) break;
+        const int cur = it % 3;
+        const int nvalid = nvalid_of(it);
+        __builtin_amdgcn_sched_barrier(0);
+        floatx16 acc[G::MP][G::NBW];
+#pragma unroll
+        for (int p = 0; p < G::MP; ++p)
+#pragma unroll
+            for (int nb = 0; nb < G::NBW; ++nb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[p][nb][e] = 0.f;
 
-    int buf = 0;                                          // weight buffer of the current stage
-    for (int it = 0; g < xr.end; g += xr.stride, ++it) {  // uniform per block
-        const int cur = it & 1;
-        const int nvalid = min(G::T, xr.end - g);
-        const int gn = g + xr.stride;
-        const bool has_next = gn < xr.end;
-        if (tid < G::T) s_items[cur ^ 1][tid] = has_next && gn + tid < xr.end ? item_word<DENSE>(a, gn + tid) : 0u;
-        u32x4 hreg[G::HPT];
-        floatx4 acc[G::MT][G::NBW];
-#pragma unroll
-        for (int mt = 0; mt < G::MT; ++mt)
-#pragma unroll
-            for (int nb = 0; nb < G::NBW; ++nb) acc[mt][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-        for (int kpos = 0; kpos < 9; ++kpos) {
-            // Weights of the next stage (next group's position 0 after position 8).
-            fetch_stage<CIN, COUT>(wg, kpos == 8 ? 0 : kpos + 1, wreg, tid);
-            // Next group's halos: its items were published by the barrier of stage 0.
-            if (kpos == 4 && has_next)
-                fetch_group_halos<CIN, COUT>(a, s_items[cur ^ 1], min(G::T, xr.end - gn), hreg, tid);
-            const uint16_t *wst = wbuf + buf * G::WST;
-            const int ky = kpos / 3, kx = kpos - ky * 3;
-            FragsBf<G::MT, G::NBW> f0, f1;
-            load_frags<CIN, COUT>(f0, halos, wst, ky, kx, 0, wm, half, lane);
-#pragma unroll
-            for (int kb = 0; kb < G::KB; ++kb) {
-                if (kb + 1 < G::KB) {
-                    if (kb & 1) load_frags<CIN, COUT>(f0, halos, wst, ky, kx, kb + 1, wm, half, lane);
-                    else load_frags<CIN, COUT>(f1, halos, wst, ky, kx, kb + 1, wm, half, lane);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-                if (kb & 1) mma_frags<G::MT, G::NBW>(acc, f1);
-                else mma_frags<G::MT, G::NBW>(acc, f0);
-                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll 1
+        for (int pass = 0; pass < G::NPASS; ++pass) {
+            // What the halo prefetch of this pass loads: the group's next
+            // chunk, or the next group's first chunk.
+            const bool last_pass = pass + 1 == G::NPASS;
+            const uint32_t *hitems = last_pass ? s_items[(it + 1) % 3] : s_items[cur];
+            const int hvalid = last_pass ? nvalid_of(it + 1) : nvalid;
+            const int hpass = last_pass ? 0 : pass + 1;
+            auto stage = [&](auto kc) __attribute__((always_inline)) {
+                constexpr int kpos = decltype(kc)::value;
+                const int q = pass * 9 + kpos;
+                __builtin_amdgcn_sched_barrier(0);            // keep each stage's work in its stage
+                // The matrix work on stage q (buffer q % 3 = kpos % 3, as 9
+                // divides the stages of a group); during it, stage q + 2 (in
+                // registers since stage q - 1) goes to buffer (q + 2) % 3,
+                // last read in stage q - 1, and stage q + 3 (wrapping into the
+                // next group) is fetched to registers; halo loads after the
+                // matrix ops of stages 1 and 3; then the first k-step of stage
+                // q + 1, whose buffer the previous barrier published, unless
+                // the pass ends here.  The barrier publishes stage q + 2 and
+                // frees stage q's buffer.
+                stage_mma<CIN, COUT, G::MP, G::NBW>(acc, f0, halos, wbuf + (kpos % 3) * G::WST, kpos, wm, half, lane,
+                                                    [&] {
+                    store_stage<CIN, COUT>(wbuf + ((kpos + 2) % 3) * G::WST, wreg, tid);
+                    fetch_stage<CIN, COUT>(wg, (q + 3) % NQ, wreg, tid);
+                });
+                if constexpr (kpos == 1) fetch_halos<CIN, COUT, 0, G::HPT / 2>(a, hitems, hvalid, hpass, hreg, hok, tid);
+                if constexpr (kpos == 3)
+                    fetch_halos<CIN, COUT, G::HPT / 2, G::HPT>(a, hitems, hvalid, hpass, hreg, hok, tid);
+                if constexpr (kpos < 8)
+                    load_kstep<CIN, COUT>(f0, halos, wbuf + ((kpos + 1) % 3) * G::WST, kpos + 1, 0, wm, half, lane);
+                lds_barrier();
+            };
+            [&]<int... K>(std::integer_sequence<int, K...>) {
+                (stage(std::integral_constant<int, K>{}), ...);
+            }(std::make_integer_sequence<int, 9>{});
+            if (!last_pass) {
+                store_halos<CIN, COUT>(halos, hreg, hok, tid);    // every wave is past the pass's last read
+                lds_barrier();
+                load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
             }
-            store_stage<CIN, COUT>(wbuf + (buf ^ 1) * G::WST, wreg, tid);
-            buf ^= 1;
-            __syncthreads();
         }
+        __builtin_amdgcn_sched_barrier(0);
+        // Items of group it + 2 to LDS (its slot last served group it - 1),
+        // then the load of group it + 3's items.
+        if (tid < G::T) s_items[(it + 2) % 3][tid] = ireg;
+        ireg = items_of(it + 3);
 
-        // Epilogue: bias, ReLU, zero outside the image, round to bf16, stage the
-        // group's outputs in the (now free) halo area, then coalesced stores.
-        uint16_t *stage = halos;
-        const int m = lane & 15, kq = lane >> 4;
+        // The next group's first halo chunk goes to LDS now (every wave is
+        // past the last read of this group's halos), then the epilogue: bias,
+        // ReLU, zero outside the image, round to bf16 and store straight to
+        // the cache.  Lanes l and l + 32 hold the two halves of each 8-channel
+        // group of a pixel; one v_permlane32_swap per word gives the lower
+        // lane the whole of groups 0 and 2 and the upper lane groups 1 and 3,
+        // so every lane stores 16 contiguous bytes.
+        if (nvalid_of(it + 1) > 0) store_halos<CIN, COUT>(halos, hreg, hok, tid);
+        const int col = lane & 31, h = lane >> 5, m = col & 15;
+        const int py = m & 3, px = m >> 2;
 #pragma unroll
-        for (int mt = 0; mt < G::MT; ++mt) {
-            const int t = wm * G::MT + mt;
+        for (int p = 0; p < G::MP; ++p) {
+            const int t = wm * 2 * G::MP + 2 * p + (col >> 4);
             const TileRef r = item_ref(a, s_items[cur][t]);
-            const bool col_in = r.tx * kTile + kq < a.W;
+            const bool inside = (r.ty * kTile + py < a.H) & (r.tx * kTile + px < a.W);
+            uint16_t *dst = outp + (size_t)r.slot * a.out_stride + ((size_t)r.tile * kTilePx + py * 4 + px) * COUT;
 #pragma unroll
             for (int nb = 0; nb < G::NBW; ++nb) {
-                const int n = (half * G::NBW + nb) * 16 + m;
-                const float b = s_bias[n];
+                const int nbase = (half * G::NBW + nb) * 32;
+                uint32_t wd[4][2];                         // [channel group][word]
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float v = acc[mt][nb][i] + b;
-                    v = v > 0.0f ? v : 0.0f;
-                    const bool inside = col_in & (r.ty * kTile + i < a.H);
-                    v = inside ? v : 0.0f;
-                    stage[(t * 16 + i * 4 + kq) * G::SR + n] = f2bf(v);
+                for (int gq = 0; gq < 4; ++gq) {
+                    const int n0 = nbase + 8 * gq + 4 * h;
+                    const float4 b = *reinterpret_cast<const float4 *>(s_bias + n0);
+                    float x[4] = {acc[p][nb][4 * gq] + b.x, acc[p][nb][4 * gq + 1] + b.y,
+                                  acc[p][nb][4 * gq + 2] + b.z, acc[p][nb][4 * gq + 3] + b.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) x[i] = inside && x[i] > 0.0f ? x[i] : 0.0f;
+                    const bf16x2 lo = {(__bf16)x[0], (__bf16)x[1]}, hi = {(__bf16)x[2], (__bf16)x[3]};
+                    wd[gq][0] = __builtin_bit_cast(uint32_t, lo);
+                    wd[gq][1] = __builtin_bit_cast(uint32_t, hi);
+                }
+#pragma unroll
+                for (int g0 = 0; g0 < 4; g0 += 2) {
+                    const auto s0 = __builtin_amdgcn_permlane32_swap(wd[g0][0], wd[g0 + 1][0], false, false);
+                    const auto s1 = __builtin_amdgcn_permlane32_swap(wd[g0][1], wd[g0 + 1][1], false, false);
+                    const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
+                    if (t < nvalid) *reinterpret_cast<u32x4 *>(dst + nbase + 8 * (g0 + h)) = v;
                 }
             }
         }
-        __syncthreads();
-        constexpr int V8 = 16 * COUT / 8;                  // 16-byte vectors per tile
-        for (int e = tid; e < G::T * V8; e += G::THREADS) {
-            const int t = e / V8, o8 = e - t * V8;
-            if (t < nvalid) {
-                const TileRef r = item_ref(a, s_items[cur][t]);
-                const int px = (8 * o8) / COUT, n = 8 * o8 - px * COUT;
-                reinterpret_cast<u32x4 *>(outp + (size_t)r.slot * a.out_stride +
-                                          (size_t)r.tile * kTilePx * COUT)[o8] =
-                    *reinterpret_cast<const u32x4 *>(stage + (t * 16 + px) * G::SR + n);
-            }
-        }
-        __syncthreads();
-        if (has_next) store_group_halos<CIN, COUT>(halos, hreg, tid);
-        __syncthreads();
+        lds_barrier();
+        load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
     }
 }
 
@@ -446,18 +529,18 @@ float round_bf16_host(float v) {
 }
 
 void pack_conv_mfma_bf16(const float *oihw, int cin, int cout, void *dst) {
-    // [kpos][block][nb][lane][j]: block b covers channels [32 b, 32 b + 32);
-    // element j of lane l is B[channel][n], n = nb * 16 + l % 16,
-    // channel = 32 b + 8 (l / 16) + j.
+    // [kpos][step][n-block][lane][j]: step s covers channels [16 s, 16 s + 16);
+    // element j of lane l is W[n][c] with n = 32 n-block + l % 32 and
+    // c = 16 s + 8 (l / 32) + j.
     uint16_t *d = static_cast<uint16_t *>(dst);
-    const int nb_n = cout / 16, nblk = cin / 32;
+    const int nbn = cout / 32, ns = cin / 16;
     size_t o = 0;
     for (int kpos = 0; kpos < 9; ++kpos)
-        for (int b = 0; b < nblk; ++b)
-            for (int nb = 0; nb < nb_n; ++nb)
+        for (int st = 0; st < ns; ++st)
+            for (int nb = 0; nb < nbn; ++nb)
                 for (int l = 0; l < 64; ++l)
                     for (int j = 0; j < 8; ++j) {
-                        const int ci = 32 * b + 8 * (l / 16) + j, n = nb * 16 + l % 16;
+                        const int ci = 16 * st + 8 * (l / 32) + j, n = nb * 32 + l % 32;
                         d[o++] = host_bf16(oihw[((size_t)n * cin + ci) * 9 + kpos]);
                     }
 }

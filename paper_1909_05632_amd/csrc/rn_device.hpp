@@ -17,6 +17,13 @@ __device__ inline void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Block barrier for data exchanged through LDS only: waits for this wave's
+// LDS (and scalar) operations, then s_barrier.  Unlike __syncthreads it does
+// not wait for the wave's outstanding global loads and stores, so prefetches
+// stay in flight across it.  Use only where no global-memory data passes
+// between the waves of the block.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 struct TileRef {
     int slot, tile, ty, tx;
 };
