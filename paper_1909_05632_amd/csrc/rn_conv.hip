@@ -471,58 +471,174 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
 }
 
 // Weights too large for LDS: a block works on a group of 4 tiles (one per
-// wave) and streams the weights through LDS in stages of KPS kernel positions.
-template <int CIN, int COUT, int KPS>
+// wave, one wave per SIMD: the float32 matrix op issues at full rate from a
+// single wave) and streams the weights through LDS in stages of one kernel
+// position x SC input channels, double-buffered.  The weights of stage q + 2
+// are fetched into registers at the start of stage q and written to the free
+// buffer at the start of stage q + 1, so each load has a whole stage (4096
+// matrix cycles at 128 outputs and 64 channels) to arrive and the block
+// barrier that ends a stage only orders LDS.  Each wave fetches the halo of
+// its tile of the next group into registers halfway through the group (every
+// load issued, out-of-image and absent ones from a fixed valid address and
+// dropped when stored) and writes it to its own halo area after its epilogue.
+template <int CIN, int COUT>
 struct Staged {
-    static constexpr int NST = (9 + KPS - 1) / KPS;
-    static constexpr int WST = KPS * CIN * COUT;
-    static constexpr size_t lds_bytes = (size_t)(WST + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
+    static constexpr int SC = (CIN > 64 && CIN % 64 == 0) ? 64 : CIN;   // channels per stage
+    static constexpr int NCH = CIN / SC;             // stages per kernel position
+    static constexpr int NQ = 9 * NCH;               // stages per group
+    static constexpr int SB = SC / 16;               // 16-channel blocks per stage
+    static constexpr int WST = SC * COUT;            // floats per stage
+    static constexpr int WPT = (WST / 4 + 255) / 256;   // 16-byte weight loads per thread and stage
+    static constexpr size_t lds_bytes = (size_t)(2 * WST + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
+    static_assert(SC % 16 == 0, "whole 16-channel blocks per stage");
 };
 
-template <int CIN, int COUT, int KPS, bool DENSE>
+template <int CIN, int COUT>
+__device__ inline void fetch_wstage(const float *wg, int q, floatx4 *regs, int tid) {
+    using S = Staged<CIN, COUT>;
+    const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
+    const floatx4 *src = reinterpret_cast<const floatx4 *>(wg + (size_t)kpos * CIN * COUT + (size_t)ch * S::WST);
+#pragma unroll
+    for (int j = 0; j < S::WPT; ++j) {
+        const int e = tid + 256 * j;
+        if ((S::WST / 4) % 256 == 0 || e < S::WST / 4) regs[j] = src[e];
+    }
+}
+
+template <int CIN, int COUT>
+__device__ inline void store_wstage(float *dst, const floatx4 *regs, int tid) {
+    using S = Staged<CIN, COUT>;
+#pragma unroll
+    for (int j = 0; j < S::WPT; ++j) {
+        const int e = tid + 256 * j;
+        if ((S::WST / 4) % 256 == 0 || e < S::WST / 4) reinterpret_cast<floatx4 *>(dst)[e] = regs[j];
+    }
+}
+
+// Halo of tile r into registers with every load issued; bit j of `ok` says
+// whether element j counts (inside the image and `valid`).
+template <int CIN, int COUT>
+__device__ inline void fetch_halo_all(const ConvArgs &a, const TileRef &r, bool valid, floatx4 *regs, uint32_t &ok,
+                                      int lane) {
+    using M = Mfma<CIN, COUT>;
+    static_assert(M::HV <= 32, "halo mask width");
+    const float *base = static_cast<const float *>(a.in);
+    ok = 0;
+#pragma unroll
+    for (int j = 0; j < M::HV; ++j) {
+        const int h = lane + 64 * j;
+        const int pos = h / M::C4, c4 = h - pos * M::C4;
+        const int hy = pos / 6, hx = pos - hy * 6;
+        const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+        const bool in = valid && h < 36 * M::C4 && y >= 0 && y < a.H && x >= 0 && x < a.W;
+        const size_t e = in ? (size_t)r.slot * a.in_stride +
+                                  ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
+                                  c4 * 4
+                            : 0;
+        regs[j] = *reinterpret_cast<const floatx4 *>(base + e);
+        ok |= (uint32_t)in << j;
+    }
+}
+
+template <int CIN, int COUT>
+__device__ inline void store_halo_masked(float *halo, const floatx4 *regs, uint32_t ok, int lane) {
+    using M = Mfma<CIN, COUT>;
+#pragma unroll
+    for (int j = 0; j < M::HV; ++j) {
+        const int h = lane + 64 * j;
+        if (h < 36 * M::C4) {
+            const int pos = h / M::C4, c4 = h - pos * M::C4;
+            *reinterpret_cast<floatx4 *>(halo + chunk_off<CIN, COUT>(pos, c4)) =
+                (ok >> j) & 1 ? regs[j] : floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+}
+
+// acc += the stage's channels (blocks ch * SB .. + SB) at kernel position kpos;
+// s_w holds the stage's weights, [block][nb][lane][4].
+template <int CIN, int COUT>
+__device__ inline void mfma_stage(floatx4 *acc, const float *halo, const float *s_w, int kpos, int ch, int lane) {
+    using M = Mfma<CIN, COUT>;
+    using S = Staged<CIN, COUT>;
+    const int mrow = lane & 15, kq = lane >> 4;
+    const int pix = (mrow & 3) * 6 + (mrow >> 2);   // column-major pixel rows
+    const int ky = kpos / 3, kx = kpos - ky * 3;
+    const int p = pix + ky * 6 + kx;
+    BlockOps<M::NB> cur, nxt;
+    auto load = [&](BlockOps<M::NB> &o, int b) {
+        o.a = *reinterpret_cast<const float4 *>(halo + chunk_off<CIN, COUT>(p, 4 * (ch * S::SB + b) + kq));
+        const float *wb = s_w + (size_t)b * 16 * COUT;
+#pragma unroll
+        for (int nb = 0; nb < M::NB; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + (nb * 64 + lane) * 4);
+    };
+    load(cur, 0);
+#pragma unroll
+    for (int b = 0; b < S::SB; ++b) {
+        if (b + 1 < S::SB) load(nxt, b + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_block<CIN, COUT>(acc, cur, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        cur = nxt;
+    }
+}
+
+template <int CIN, int COUT, bool DENSE>
 __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
-    using S = Staged<CIN, COUT, KPS>;
+    using S = Staged<CIN, COUT>;
+    static_assert(M::TAIL == 0, "staged layers take whole 16-channel blocks");
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cnt = work_count<DENSE>(a);
     const XcdRange xr = xcd_range(cnt, 4);
     if (xr.first >= xr.end) return;                       // uniform per block
-    float *s_w = smem;
-    float *halo = smem + S::WST + wave * M::HALO;
+    float *wbuf = smem;                                   // two stages
+    float *halo = smem + 2 * S::WST + wave * M::HALO;
     const float *wg = static_cast<const float *>(a.w);
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
 
+    // Prologue: this wave's halo of group 0; stage 0 in LDS, stage 1 in flight.
+    int t = xr.first + wave;
+    uint32_t e_cur = t < xr.end ? item_word<DENSE>(a, t) : 0u;
+    floatx4 wreg[S::WPT];           // ext-vector arrays stay in registers
+    fetch_wstage<CIN, COUT>(wg, 0, wreg, tid);
+    floatx4 hreg[M::HV];
+    uint32_t hok;
+    fetch_halo_all<CIN, COUT>(a, item_ref(a, e_cur), t < xr.end, hreg, hok, lane);
+    store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);
+    store_wstage<CIN, COUT>(wbuf, wreg, tid);
+    fetch_wstage<CIN, COUT>(wg, 1 % S::NQ, wreg, tid);
+    lds_barrier();
+
+    int buf = 0;
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        const int t = g + wave;
+        t = g + wave;
         const bool valid = t < xr.end;
-        TileRef r{0, 0, 0, 0};
-        if (valid) {
-            r = decode<DENSE>(a, t);
-            float4 regs[M::HV];
-            fetch_halo<CIN, COUT>(a, r, regs, lane);
-            store_halo<CIN, COUT>(halo, regs, lane);
-        }
+        const int tn = t + xr.stride;
+        const uint32_t e_nxt = tn < xr.end ? item_word<DENSE>(a, tn) : 0u;
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int st = 0; st < S::NST; ++st) {
-            __syncthreads();                               // previous stage fully consumed
-            const int n0 = st * S::WST;
-            const int nf = min(S::WST, M::WTOT - n0);
-            for (int j = tid; j < nf / 4; j += blockDim.x)
-                reinterpret_cast<float4 *>(s_w)[j] = reinterpret_cast<const float4 *>(wg + n0)[j];
-            __syncthreads();
-            if (valid) {
-                if (st * KPS + KPS <= 9) mfma_positions<CIN, COUT, KPS>(acc, halo, s_w, st * KPS, lane);
-                else mfma_positions<CIN, COUT, 9 % KPS>(acc, halo, s_w, st * KPS, lane);
-            }
+        for (int q = 0; q < S::NQ; ++q) {
+            // Stage q + 1 to the free buffer (its last reader finished before the
+            // previous barrier), stage q + 2 (wrapping into the next group) to
+            // registers, the next halo at mid-group, then the matrix work.
+            store_wstage<CIN, COUT>(wbuf + (buf ^ 1) * S::WST, wreg, tid);
+            fetch_wstage<CIN, COUT>(wg, (q + 2) % S::NQ, wreg, tid);
+            if (q == S::NQ / 2) fetch_halo_all<CIN, COUT>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
+            const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
+            if (valid) mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane);
+            buf ^= 1;
+            lds_barrier();
         }
         if (valid) {
             wave_sync();
-            epilogue<CIN, COUT>(a, r, acc, s_bias, halo, lane);
+            epilogue<CIN, COUT>(a, item_ref(a, e_cur), acc, s_bias, halo, lane);
         }
+        store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);      // this wave's own area
+        wave_sync();
+        e_cur = e_nxt;
     }
 }
 
@@ -538,12 +654,6 @@ template <int CIN, int COUT>
 constexpr bool fused_fits() {
     return Resident<CIN, COUT, 8>::lds_bytes + (COUT + 10 * CIN) * sizeof(float) <= 160 * 1024;
 }
-
-template <int CIN, int COUT>
-constexpr int pick_kps() {
-    return Staged<CIN, COUT, 3>::lds_bytes <= kLdsBudget ? 3 : 1;
-}
-
 
 template <int CIN, int COUT, bool DENSE, bool FUSE>
 hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {
@@ -563,9 +673,9 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         return run_resident<CIN, COUT, DENSE, false>(a, cus, s);
     } else {
         if (a.fuse_first) return hipErrorInvalidValue;
-        constexpr int KPS = pick_kps<CIN, COUT>();
-        constexpr size_t lds = Staged<CIN, COUT, KPS>::lds_bytes;
-        auto kern = k_conv_mfma_staged<CIN, COUT, KPS, DENSE>;
+        constexpr size_t lds = Staged<CIN, COUT>::lds_bytes;
+        static_assert(lds <= kLdsBudget, "staged layer exceeds LDS");
+        auto kern = k_conv_mfma_staged<CIN, COUT, DENSE>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
         const int grid = persistent_grid(cus, (a.max_tiles + 3) / 4);
