@@ -194,14 +194,22 @@ __device__ inline float fetch_patch(const ConvArgs &a, const TileRef &r, int lan
     return (y >= 0 && y < a.H && x >= 0 && x < a.W) ? plane[(size_t)y * a.W + x] : 0.f;
 }
 
+// The 8x8 input patch sits in the last 64 floats of the wave's halo area
+// (written there by the caller, after the previous tile's epilogue, whose
+// output staging ends below it).
 template <int CIN, int COUT>
-__device__ inline void build_halo_fused(float *halo, float pin, const ConvArgs &a, const TileRef &r,
-                                        const float *s_w1, const float *s_b1, int lane) {
+__device__ inline float *patch_area(float *halo) {
+    return halo + Mfma<CIN, COUT>::HALO - 64;
+}
+
+template <int CIN, int COUT>
+__device__ inline void build_halo_fused(float *halo, const ConvArgs &a, const TileRef &r, const float *s_w1,
+                                        const float *s_b1, int lane) {
     using M = Mfma<CIN, COUT>;
     constexpr int NU = 36 * M::C4;            // 4-channel units of the halo
     constexpr int UV = (NU + 63) / 64;
-    float *patch = halo + M::HALO - 64;       // scratch: tail of this wave's halo area
-    patch[lane] = pin;
+    static_assert(16 * M::SR <= M::HALO - 64, "output staging must end below the patch");
+    const float *patch = patch_area<CIN, COUT>(halo);
     wave_sync();
     float4 v[UV];
 #pragma unroll
@@ -316,7 +324,11 @@ __device__ inline void mfma_positions(floatx4 *acc, const float *halo, const flo
 
 // Bias, ReLU, zero outside the image, coalesced store of the 16 x COUT tile
 // through LDS (the halo area is free by now), and the tile's head partials.
-template <int CIN, int COUT>
+// NO is the number of logits when known at compile time (0: this layer feeds
+// no head partials), else -1 (a.n_out at run time).  A fixed count keeps the
+// number of memory operations per tile fixed, so the next tile's waits can
+// name exactly the loads they need instead of draining this tile's stores.
+template <int CIN, int COUT, int NO>
 __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *acc, const float *s_bias,
                                 float *stage, int lane) {
     using M = Mfma<CIN, COUT>;
@@ -327,34 +339,26 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
         const float b = s_bias[nb * 16 + mrow];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            float v = acc[nb][i] + b;
-            v = v > 0.0f ? v : 0.0f;
-            if (!col_in || r.ty * kTile + i >= a.H) v = 0.0f;
-            acc[nb][i] = v;
-            stage[(i * 4 + kq) * M::SR + nb * 16 + mrow] = v;
+            const float v = acc[nb][i] + b;
+            const bool keep = col_in & (r.ty * kTile + i < a.H) & (v > 0.0f);
+            acc[nb][i] = keep ? v : 0.0f;
+            stage[(i * 4 + kq) * M::SR + nb * 16 + mrow] = acc[nb][i];
         }
     }
     wave_sync();
-    float4 *d4 = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
-                                            (size_t)r.tile * kTilePx * COUT);
-#pragma unroll
-    for (int j = 0; j < M::NB; ++j) {              // 16 * COUT / 4 float4 = 64 * NB
-        const int o4 = lane + 64 * j;
-        const int e = 4 * o4, m = e / COUT, n = e - m * COUT;
-        d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
-    }
-    if (a.n_out > 0) {
+    const int n_out = NO >= 0 ? NO : a.n_out;
+    if (NO != 0 && n_out > 0) {
         // Tile contribution to each logit: per-lane partial dot products, then
         // the lane sums, 8 logits at a time so the butterfly steps of
         // different logits overlap.
         const int ntiles = a.TH * a.TW;
-        for (int o0 = 0; o0 < a.n_out; o0 += 8) {
+        for (int o0 = 0; o0 < n_out; o0 += 8) {
             float p[8];
 #pragma unroll
             for (int q = 0; q < 8; q += 2) {
                 // Two logits per batch: their 2 x NB weight loads are issued
                 // together (indices clamped, results of absent logits dropped).
-                const int oa = min(o0 + q, a.n_out - 1), ob = min(o0 + q + 1, a.n_out - 1);
+                const int oa = min(o0 + q, n_out - 1), ob = min(o0 + q + 1, n_out - 1);
                 const float4 *wa = reinterpret_cast<const float4 *>(
                                        a.hw + ((size_t)oa * ntiles + r.tile) * kTilePx * COUT) + lane;
                 const float4 *wb = reinterpret_cast<const float4 *>(
@@ -379,7 +383,7 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
                 }
                 p[q] = pa;
                 p[q + 1] = pb;
-                if (o0 + q + 2 >= a.n_out) {
+                if (o0 + q + 2 >= n_out) {
                     for (int z = q + 2; z < 8; ++z) p[z] = 0.f;
                     break;
                 }
@@ -388,13 +392,23 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
             for (int off = 32; off > 0; off >>= 1)
 #pragma unroll
                 for (int q = 0; q < 8; ++q) p[q] += __shfl_xor(p[q], off, 64);
-            if (lane < 8 && o0 + lane < a.n_out) {
+            if (lane < 8 && o0 + lane < n_out) {
                 float v = p[0];
 #pragma unroll
                 for (int q = 1; q < 8; ++q) v = lane == q ? p[q] : v;
-                a.hpart[((size_t)r.slot * ntiles + r.tile) * a.n_out + o0 + lane] = v;
+                a.hpart[((size_t)r.slot * ntiles + r.tile) * n_out + o0 + lane] = v;
             }
         }
+    }
+    // The tile's stores go last: the next tile's waits on its own loads then
+    // never have to drain them.
+    float4 *d4 = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
+                                            (size_t)r.tile * kTilePx * COUT);
+#pragma unroll
+    for (int j = 0; j < M::NB; ++j) {              // 16 * COUT / 4 float4 = 64 * NB
+        const int o4 = lane + 64 * j;
+        const int e = 4 * o4, m = e / COUT, n = e - m * COUT;
+        d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
     }
     wave_sync();
 }
@@ -408,7 +422,7 @@ struct Resident {
         (size_t)(Mfma<CIN, COUT>::WTOT + WAVES * Mfma<CIN, COUT>::HALO) * sizeof(float);
 };
 
-template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE>
+template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE, int NO>
 __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
     extern __shared__ float smem[];
@@ -442,18 +456,17 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     float pin = 0.f;
     uint32_t e_cur = item_word<DENSE>(a, t);
     uint32_t e_nxt = t + stride < xr.end ? item_word<DENSE>(a, t + stride) : 0u;
-    if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_cur), lane);
+    if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = fetch_patch(a, item_ref(a, e_cur), lane);
     else fetch_halo<CIN, COUT>(a, item_ref(a, e_cur), pre, lane);
     for (; t < xr.end; t += stride) {
         const TileRef cur = item_ref(a, e_cur);
-        if constexpr (FUSE) build_halo_fused<CIN, COUT>(halo, pin, a, cur, s_w1, s_b1, lane);
+        if constexpr (FUSE) build_halo_fused<CIN, COUT>(halo, a, cur, s_w1, s_b1, lane);
         else store_halo<CIN, COUT>(halo, pre, lane);
         wave_sync();
         const uint32_t e_nn = t + 2 * stride < xr.end ? item_word<DENSE>(a, t + 2 * stride) : 0u;
-        if (t + stride < xr.end) {
-            if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_nxt), lane);
-            else fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
-        }
+        // The next tile's input (past the end: item 0's, never used).
+        if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_nxt), lane);
+        else if (t + stride < xr.end) fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -464,7 +477,11 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
         __builtin_amdgcn_s_setprio(0);
         wave_sync();
-        epilogue<CIN, COUT>(a, cur, acc, s_bias, halo, lane);
+        epilogue<CIN, COUT, NO>(a, cur, acc, s_bias, halo, lane);
+        // The next patch goes to LDS here rather than at the top of the loop:
+        // the wait for its load then counts exactly this tile's later memory
+        // operations, where at the loop top it would have to drain them all.
+        if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = pin;
         e_cur = e_nxt;
         e_nxt = e_nn;
     }
@@ -634,7 +651,7 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         }
         if (valid) {
             wave_sync();
-            epilogue<CIN, COUT>(a, item_ref(a, e_cur), acc, s_bias, halo, lane);
+            epilogue<CIN, COUT, -1>(a, item_ref(a, e_cur), acc, s_bias, halo, lane);
         }
         store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);      // this wave's own area
         wave_sync();
@@ -655,15 +672,23 @@ constexpr bool fused_fits() {
     return Resident<CIN, COUT, 8>::lds_bytes + (COUT + 10 * CIN) * sizeof(float) <= 160 * 1024;
 }
 
-template <int CIN, int COUT, bool DENSE, bool FUSE>
-hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {
+template <int CIN, int COUT, bool DENSE, bool FUSE, int NO>
+hipError_t run_resident_no(const ConvArgs &a, int cus, hipStream_t s) {
     constexpr size_t lds = Resident<CIN, COUT, 8>::lds_bytes;
-    auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE, FUSE>;
+    auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE, FUSE, NO>;
     static hipError_t attr = set_lds(kern, lds);
     if (attr != hipSuccess) return attr;
     const int grid = persistent_grid(cus, (a.max_tiles + 7) / 8);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, a);
     return hipGetLastError();
+}
+
+// Logit count as a template argument where it is a common one.
+template <int CIN, int COUT, bool DENSE, bool FUSE>
+hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {
+    if (a.n_out == 0) return run_resident_no<CIN, COUT, DENSE, FUSE, 0>(a, cus, s);
+    if (a.n_out == 6) return run_resident_no<CIN, COUT, DENSE, FUSE, 6>(a, cus, s);
+    return run_resident_no<CIN, COUT, DENSE, FUSE, -1>(a, cus, s);
 }
 
 template <int CIN, int COUT, bool DENSE>
