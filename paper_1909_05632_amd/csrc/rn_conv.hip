@@ -114,20 +114,21 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
 // values for the block's 4 (2) k-steps are contiguous channels of one halo
 // pixel: one 16-byte (8-byte) LDS read.  The weights are packed to match,
 // [kpos][block][nb][lane][j], so the B values are one 16-byte read per nb.
-// Bank layout of the halo: the 16-byte A reads of one 8-lane phase touch 8
-// pixels.  With a pixel stride of CIN + 4 floats they fall in distinct banks.
-// When CIN = 8 (mod 32) the halo is stored unpadded (pixel stride CIN, which
-// lets 8 waves' halos fit in LDS next to the 40->80 weights) and the 16-byte
-// chunk index of pixel p is XOR-ed with (p / 12) & 1, which again puts every
-// phase in distinct banks for all 9 kernel positions (checked exhaustively on
-// the host for CIN = 40, 72, 104, 136).  Blocks are double-buffered: the
-// operands of the next block are read while the matrix cores work on the
+// Bank layout of the halo: the LDS serves 16 lanes of a 16-byte read per
+// clock (64 banks), and the A reads of such a group touch 16 pixels of the
+// 6x6 halo, one chunk each.  The halo is stored unpadded (pixel stride CIN,
+// which lets 8 waves' halos fit in LDS next to the 40->80 weights) with the
+// 16-byte chunk index of halo pixel (hy, hx) XOR-ed with g(hy, hx): hy % 2
+// for 10 chunks per pixel, hy % 4 for 20, (hy % 4) + 4 (hx % 4) for 16 or
+// 32; every group then falls in 16 distinct bank groups for all 9 kernel
+// positions, and the 8-byte reads of the 8-channel tail block in distinct
+// banks too (checked exhaustively on the host).  Blocks are double-buffered:
+// the operands of the next block are read while the matrix cores work on the
 // current one.
 template <int CIN, int COUT>
 struct Mfma {
     static constexpr int NB = COUT / 16;
-    static constexpr bool SWZ = (CIN % 32) == 8;
-    static constexpr int CS = SWZ ? CIN : CIN + 4;   // halo pixel stride in LDS (floats)
+    static constexpr int CS = CIN;            // halo pixel stride in LDS (floats)
     static constexpr int NF = CIN / 16;       // full channel blocks per kernel position
     static constexpr int TAIL = (CIN % 16) ? 1 : 0;
     static constexpr int NBLK = NF + TAIL;
@@ -138,6 +139,7 @@ struct Mfma {
     static constexpr int WTOT = 9 * CIN * COUT;
     static_assert(16 * SR <= HALO, "output staging must fit in the halo area");
     static_assert(COUT % 16 == 0 && CIN % 8 == 0, "MFMA tiling");
+    static_assert(C4 == 10 || C4 == 20 || C4 == 16 || C4 == 32, "halo swizzle defined for 40, 64, 80, 128 channels");
 };
 
 // Global -> registers: the halo of one tile, 16 bytes per lane per load.
@@ -166,8 +168,9 @@ __device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *r
 template <int CIN, int COUT>
 __device__ inline int chunk_off(int p, int c) {
     using M = Mfma<CIN, COUT>;
-    if constexpr (M::SWZ) return p * M::CS + 4 * (c ^ ((p / 12) & 1));
-    else return p * M::CS + 4 * c;
+    const int hy = p / 6, hx = p - 6 * hy;
+    const int g = M::C4 == 10 ? (hy & 1) : M::C4 == 20 ? (hy & 3) : (hy & 3) | ((hx & 3) << 2);
+    return p * M::CS + 4 * (c ^ g);
 }
 
 template <int CIN, int COUT>
