@@ -219,85 +219,90 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
 //   hpart[tile][o] = sum_k act_tile[k] * hw[P][k][o],  k = pixel * C + channel,
 // on v_mfma_f32_16x16x32_bf16 (A: the tile's cache slice read straight from
 // memory, 16 bytes per lane per k-step; products of two bf16 values are exact
-// in float32).  The work list is position-major, so a block of 16 consecutive
-// items mostly shares one position and the position's weights are read once
-// for all of them; a block with several positions makes one pass per
-// position, each row kept only in its own pass.  The four waves split K into
-// fixed quarters and add them in wave order, so a row's result does not
-// depend on which rows share its block: list and dense passes agree bit for
-// bit.
+// in float32).  A block takes 64 consecutive work items, one 16-row block per
+// wave; the work list is position-major, so the 64 items mostly share one or
+// two positions and each position's weights are read once for all of them
+// (the four waves read the same addresses, served by L1/L2).  A block makes
+// one pass per distinct position; a wave computes in a pass only if one of
+// its rows has that position, and keeps only those rows.  Each row's sum runs
+// over the full K in one wave in a fixed order, so the result does not depend
+// on which rows share the block: list and dense passes agree bit for bit.
 template <int C, int NBO, bool DENSE>
 __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     constexpr int KS = 16 * C / 32;           // k-steps
-    constexpr int KW = KS / 4;                // per wave
-    __shared__ floatx4 red[4][NBO][64];
-    __shared__ uint32_t s_item[16];
-    __shared__ int s_pos[16];
+    constexpr int KB = 8;                     // k-steps per batch of loads
+    static_assert(KS % KB == 0, "whole batches");
+    __shared__ int s_pos[64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, 16);
+    const XcdRange xr = xcd_range(cnt, 64);
     const uint16_t *act = static_cast<const uint16_t *>(a.in);
     const uint16_t *hw = reinterpret_cast<const uint16_t *>(a.hw);
     const int ntiles = a.TH * a.TW;
     const int row = lane & 15, kq = lane >> 4;
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        if (tid < 16) {
-            const bool valid = g + tid < xr.end;
-            const uint32_t e = valid ? item_word<DENSE>(a, g + tid) : 0u;
-            s_item[tid] = e;
-            s_pos[tid] = valid ? item_ref(a, e).tile : -1;
+        const int it = g + wave * 16 + row;                 // this lane's A row
+        const bool valid = it < xr.end;
+        const uint32_t e = valid ? item_word<DENSE>(a, it) : 0u;
+        const TileRef r = item_ref(a, e);
+        const int my_pos = valid ? r.tile : -1;
+        if (tid < 64) {
+            const int t2 = g + tid;
+            s_pos[tid] = t2 < xr.end ? item_ref(a, item_word<DENSE>(a, t2)).tile : -1;
         }
         __syncthreads();
-        const TileRef r = item_ref(a, s_item[row]);
-        const int my_pos = s_pos[row];
+        // Positions of the wave's 16 rows, for the per-pass "any row of mine" test.
+        uint64_t mine_mask = 0;
         const uint16_t *arow = act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C + 8 * kq;
-        uint32_t done = 0;                     // rows handled (same value in every thread)
+        uint64_t done = 0;                                   // rows of the block handled
         for (;;) {
             int P = -1;
-            for (int q = 0; q < 16; ++q)
+            for (int q = 0; q < 64; ++q)
                 if (P < 0 && !((done >> q) & 1) && s_pos[q] >= 0) P = s_pos[q];
             if (P < 0) break;
+            uint64_t pmask = 0;
+            for (int q = 0; q < 64; ++q) pmask |= (uint64_t)(s_pos[q] == P) << q;
+            done |= pmask;
+            mine_mask = (pmask >> (16 * wave)) & 0xFFFFu;
+            if (mine_mask == 0) continue;                    // uniform per wave
             const bool mine = my_pos == P;
             floatx4 acc[NBO];
 #pragma unroll
             for (int nb = 0; nb < NBO; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-            const uint16_t *wp = hw + (((size_t)P * KS + wave * KW) * NBO * 64 + lane) * 8;
-#pragma unroll 4
-            for (int s = 0; s < KW; ++s) {
-                u32x4 av = {0u, 0u, 0u, 0u};
-                if (mine) av = *reinterpret_cast<const u32x4 *>(arow + 32 * (wave * KW + s));
-                const bf16x8 a8 = __builtin_bit_cast(bf16x8, av);
+            const uint16_t *wp = hw + ((size_t)P * KS * NBO * 64 + lane) * 8;
+            for (int s0 = 0; s0 < KS; s0 += KB) {
+                u32x4 av[KB], bv[KB][NBO];
 #pragma unroll
-                for (int nb = 0; nb < NBO; ++nb) {
-                    const bf16x8 b8 = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const u32x4 *>(wp + ((size_t)s * NBO + nb) * 64 * 8));
-                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8, b8, acc[nb], 0, 0, 0);
+                for (int s = 0; s < KB; ++s) {
+                    av[s] = mine ? *reinterpret_cast<const u32x4 *>(arow + 32 * (s0 + s)) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb)
+                        bv[s][nb] = *reinterpret_cast<const u32x4 *>(wp + ((size_t)(s0 + s) * NBO + nb) * 64 * 8);
                 }
+#pragma unroll
+                for (int s = 0; s < KB; ++s)
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb)
+                        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[s]),
+                                                                          __builtin_bit_cast(bf16x8, bv[s][nb]),
+                                                                          acc[nb], 0, 0, 0);
             }
+            // D: rows 4 kq + i, column lane % 16 = logit nb * 16 + row.
 #pragma unroll
-            for (int nb = 0; nb < NBO; ++nb) red[wave][nb][lane] = acc[nb];
-            __syncthreads();
-            if (wave == 0) {
+            for (int nb = 0; nb < NBO; ++nb) {
+                const int o = nb * 16 + row;
 #pragma unroll
-                for (int nb = 0; nb < NBO; ++nb) {
-                    floatx4 v = red[0][nb][lane];
-#pragma unroll
-                    for (int w = 1; w < 4; ++w) v += red[w][nb][lane];
-                    const int o = nb * 16 + row;      // D: rows 4 kq + i, column lane % 16
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int q = 4 * kq + i;
-                        if (o < a.n_out && s_pos[q] == P) {
-                            const TileRef rq = item_ref(a, s_item[q]);
-                            a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = v[i];
-                        }
+                for (int i = 0; i < 4; ++i) {
+                    const int q = 4 * kq + i;                // row of the wave's block
+                    const uint32_t eq = __shfl(e, q, 64);   // lane q holds row q's item
+                    if (o < a.n_out && ((mine_mask >> q) & 1)) {
+                        const TileRef rq = item_ref(a, eq);
+                        a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = acc[nb][i];
                     }
                 }
             }
-            for (int q = 0; q < 16; ++q)
-                if (s_pos[q] == P) done |= 1u << q;
-            __syncthreads();                   // red is reused by the next pass
         }
+        __syncthreads();                                     // s_pos is rewritten next round
     }
 }
 
@@ -358,7 +363,7 @@ void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, i
 
 template <int C, bool DENSE>
 hipError_t run_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
-    const int grid = dev::persistent_grid(cus * 4, (a.max_tiles + 15) / 16);
+    const int grid = dev::persistent_grid(cus * 4, (a.max_tiles + 63) / 64);
     if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_bf16<C, 1, DENSE>), dim3(grid), dim3(256), 0, s, a);
     else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_bf16<C, 2, DENSE>), dim3(grid), dim3(256), 0, s, a);
     else hipLaunchKernelGGL((k_tile_part_bf16<C, 4, DENSE>), dim3(grid), dim3(256), 0, s, a);
