@@ -11,7 +11,8 @@ Workloads (synth.WORKLOADS):
   atari-ds2-256x64 (default)  256 streams x 64 frames, 105x80, 1->40->80, dense->6
   atari-ds4-1x16              1 stream x 16 frames, 53x40
   stack4-512x64               512 streams, the last 4 frames stacked as input channels
-  occlusion-105x80-4096       4096 occlusion variants as 64 streams x 64 boxed steps
+  occlusion-105x80-4096       4096 occlusion variants of one base image, one
+                              reuse_net_variants call (copy-on-write overlays) per step
   fullres-1024x32             1024 streams x 32 frames, 210x160, 1->64->128->128, dense->18
                               (--change-frac picks the sprite preset of the sweep)
 The frame order runs 1..F-1 and then back and forth, so every transition is
@@ -81,19 +82,20 @@ class SpriteDriver:
         from synth import frames as synth
         self.wl = wl
         self.S = wl.streams
+        self.max_streams = wl.streams
         self.preset = preset or {}
         self.u8 = synth.sprite_batch(wl, **self.preset)            # [F][S][H][W]
         self.frames = torch.from_numpy(synth.to_f32(self.u8)).cuda().unsqueeze(2).contiguous()
         self.seq = schedule(wl.frames, length)
 
-    def prime_frames(self):
-        return self.frames[0]
+    def prime(self, net, out):
+        net.full(self.frames[0], out=out)
 
-    def step(self, k):
-        return self.frames[self.seq[k]], None, None
+    def reuse_step(self, net, k, out):
+        net.step(self.frames[self.seq[k]], out=out)
 
-    def dense_frames(self, k):
-        return self.frames[self.seq[k]]
+    def dense_step(self, net, k, out):
+        net.full(self.frames[self.seq[k]], out=out)
 
     def cpu_sample(self, oracle, weights, budget_s):
         from synth import frames as synth
@@ -123,60 +125,61 @@ class SpriteDriver:
 
 
 class OcclusionDriver:
-    """4096 occlusion variants of one base image: stream y moves an 8x8 zero
-    patch along row y, one column per step, with explicit change boxes."""
+    """Occlusion map of one base image: 4096 variants, each the base with an
+    8x8 zero patch at one corner of a 64x64 grid.  A step evaluates all of them
+    in one reuse_net_variants call against the primed base slot (no per-variant
+    caches; at most 16 dirty tiles per variant and layer).  The dense path runs
+    the same 4096 variant frames through reuse_net_full, 512 at a time."""
 
     unit = "variants/s"
     metric = "occlusion variants/sec"
+    DENSE_BATCH = 512
+    MAX_TILES = 16
 
     def __init__(self, torch, wl, length):
         from synth import frames as synth
         self.wl = wl
         P, G = wl.extra["patch"], wl.extra["grid"]
-        self.S = G
+        self.S = G * G
+        self.max_streams = self.DENSE_BATCH
         self.base = synth.to_f32(synth.occlusion_base(wl))
-        var = np.stack([np.stack([synth.occlusion_variant_frame(self.base, y, x, P)[None]
-                                  for y in range(G)]) for x in range(G)])  # [x][y][1][H][W]
+        self.base_dev = torch.from_numpy(self.base[None, None]).cuda().contiguous()
+        var = np.stack([synth.occlusion_variant_frame(self.base, i // G, i % G, P)[None]
+                        for i in range(self.S)])                   # [4096][1][H][W]
         self.frames = torch.from_numpy(var).cuda().contiguous()
-        boxes = np.zeros((G, 2 * G, 4), np.int32)
-        for x in range(G):
-            px = (x - 1) % G
-            for y in range(G):
-                boxes[x, 2 * y] = (y, px, y + P, px + P)          # previous patch: restore
-                boxes[x, 2 * y + 1] = (y, x, y + P, x + P)        # new patch
+        boxes = np.asarray([(y, x, y + P, x + P) for y in range(G) for x in range(G)], np.int32)
         self.boxes = torch.from_numpy(boxes).cuda()
-        self.box_off = torch.arange(0, 2 * G + 1, 2, dtype=torch.int32).cuda()
-        self.base_dev = torch.from_numpy(np.stack([self.base[None]] * G)).cuda().contiguous()
-        self.G = G
+        self.box_off = torch.arange(0, self.S + 1, dtype=torch.int32).cuda()
+        self.zero = torch.zeros((1, 1, wl.h, wl.w), dtype=torch.float32).cuda()
+        self.P, self.G = P, G
 
-    def prime_frames(self):
-        return self.base_dev
+    def prime(self, net, out):
+        net.full(self.base_dev, out=out[:1])
 
-    def step(self, k):
-        # Step k places the patch at column k % G (the first step after priming
-        # also "restores" column G-1, which is unchanged: a harmless extra box).
-        x = k % self.G
-        return self.frames[x], self.boxes[x], self.box_off
+    def reuse_step(self, net, k, out):
+        net.variants(0, self.boxes, self.box_off, self.zero, max_tiles=self.MAX_TILES, out=out)
 
-    def dense_frames(self, k):
-        return self.frames[k % self.G]
+    def dense_step(self, net, k, out):
+        B = self.DENSE_BATCH
+        for j in range(0, self.S, B):
+            net.full(self.frames[j:j + B], out=out[j:j + B])
 
     def cpu_sample(self, oracle, weights, budget_s):
         from synth import frames as synth
         wl = self.wl
         onet = oracle.Net(1, wl.h, wl.w, wl.conv_specs(), wl.n_out)
-        P, n = wl.extra["patch"], 16
-        done, t0, x = 0, time.perf_counter(), 0
+        P, G, n = self.P, self.G, 16
+        done, t0, i0 = 0, time.perf_counter(), 0
         while True:
-            var = np.stack([synth.occlusion_variant_frame(self.base, y, x, P)[None] for y in range(n)])
-            px = (x - 1) % self.G
-            d0 = np.stack([oracle.box_mask(wl.h, wl.w, [(y, px, y + P, px + P), (y, x, y + P, x + P)])
-                           for y in range(n)])
+            idx = [(i0 + j) % self.S for j in range(n)]
+            var = np.stack([synth.occlusion_variant_frame(self.base, i // G, i % G, P)[None] for i in idx])
+            d0 = np.stack([oracle.box_mask(wl.h, wl.w, [(i // G, i % G, i // G + P, i % G + P)])
+                           for i in idx])
             _, m = oracle.masks(onet, d0, want_pixels=False)
             oracle.worklists(m)
             oracle.forward(onet, *weights, var)
             done += n
-            x = (x + 1) % self.G
+            i0 = (i0 + n) % self.S
             el = time.perf_counter() - t0
             if el >= budget_s:
                 break
@@ -235,17 +238,16 @@ def main():
         drv = SpriteDriver(torch, wl, length, preset)
     S = drv.S
     weights = synth.net_weights(wl)
-    net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, S, weights, act_dtype=args.dtype,
+    net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, drv.max_streams, weights, act_dtype=args.dtype,
                    stack=wl.stack, head=args.head, fuse_first=not args.separate_first)
     out = torch.empty((S, wl.n_out), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
     def do_step(k):
-        f, b, bo = drv.step(k)
-        net.step(f, boxes=b, box_off=bo, out=out)
+        drv.reuse_step(net, k, out)
 
     # Stats pass: dirty tiles of exactly the steps the timed pass will run.
-    net.full(drv.prime_frames(), out=out)
+    drv.prime(net, out)
     stats = []
     for k in range(length):
         do_step(k)
@@ -253,7 +255,7 @@ def main():
     timed_stats = stats[args.warmup:]
 
     def run_reuse(profile: bool):
-        net.full(drv.prime_frames(), out=out)
+        drv.prime(net, out)
         for k in range(args.warmup):
             do_step(k)
         torch.cuda.synchronize()
@@ -275,12 +277,12 @@ def main():
     # Dense recompute path of the same library on the same frames.
     dsteps = args.dense_steps or max(10, args.steps // 2)
     for k in range(args.warmup):
-        net.full(drv.dense_frames(k), out=out)
+        drv.dense_step(net, k, out)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for k in range(args.warmup, args.warmup + dsteps):
-        net.full(drv.dense_frames(k), out=out)
+        drv.dense_step(net, k, out)
     e1.record(stream)
     torch.cuda.synchronize()
     ms_dense = e0.elapsed_time(e1) / dsteps

@@ -153,6 +153,43 @@ rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *dev_stream_id
  * everything.  Synchronises the last step's stream. */
 rn_status reuse_net_reset(reuse_net *net, int32_t stream_id);
 
+/* ---- variants of one slot: copy-on-write overlays (Sec. 1, known change) ---- */
+
+/* Device scratch bytes reuse_net_variants needs for n variants when no variant
+ * has more than max_tiles dirty tiles in any layer 1..n_conv (max_tiles <= 0:
+ * no limit, room for every tile).  0 if n is outside 1..65535 or the net
+ * cannot run variants (head_mode RN_HEAD_FULL, fewer than 2 layers, stack = 4). */
+size_t reuse_net_variant_scratch_bytes(const reuse_net *net, int32_t n, int32_t max_tiles);
+
+/* Evaluate n variants of one primed slot in a single pass, as used for
+ * occlusion maps (Sec. 1): variant i is the slot's cached input with the
+ * pixels of its boxes [box_off[i], box_off[i+1]) replaced by the same pixels
+ * of frame i (frame_count = n) or of frame 0 (frame_count = 1: e.g. one
+ * all-zero frame for zero patches).  Boxes are (y0, x0, y1, x1) int32,
+ * half-open, clipped; box_off has n+1 entries, box_off[0] = 0.
+ * The result is what a step with those boxes would give on a copy of the slot,
+ * to float32 rounding (the same tiles are recomputed).  Nothing of the slot
+ * changes: each variant recomputes only the tiles its change reaches, writes
+ * them to per-layer overlays in dev_scratch (row = position in the layer's
+ * work list) and reads every other activation and per-tile head contribution
+ * from the base slot.  Logits go to dev_logits [n][n_out].
+ *   dev_frames:   [frame_count][in_c][in_h][in_w], RN_F32 or RN_U8 (k / 255);
+ *                 only pixels inside the variant's boxes are read.
+ *   max_tiles:    per-variant limit that sizes the scratch (see above).  A
+ *                 variant over the limit is left out and its logits are NaN;
+ *                 all logits are NaN if the base slot was never primed.
+ *   dev_scratch:  caller-owned device memory, 256-byte aligned, at least
+ *                 reuse_net_variant_scratch_bytes(net, n, max_tiles) bytes.
+ * Needs head_mode RN_HEAD_TILES, n_conv >= 2 and stack = 1 (RN_EUNSUPPORTED
+ * otherwise).  Enqueues on hip_stream only.  Until the next step, full or
+ * variants call, the introspection functions below describe the variants
+ * (stream_id = variant index i; work-list entries i << 16 | ty << 8 | tx) and
+ * read them from dev_scratch, which must then still hold them. */
+rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, const void *dev_frames,
+                             rn_dtype frame_dtype, int32_t frame_count, const int32_t *dev_boxes,
+                             const int32_t *dev_box_off, int32_t max_tiles, void *dev_scratch,
+                             size_t scratch_bytes, float *dev_logits, void *hip_stream);
+
 /* ---- introspection (synchronous; for parity checks and statistics) ---- */
 
 /* Pixel change mask of a slot after its last step, layer 0 (input) .. n_conv.
@@ -166,9 +203,9 @@ rn_status reuse_net_get_pixel_mask(reuse_net *net, int32_t layer, int32_t stream
 rn_status reuse_net_get_tile_mask(reuse_net *net, int32_t layer, int32_t stream_id,
                                   uint64_t *out, size_t words);
 
-/* Work list of layer 1..n_conv from the last step or full: the dirty tiles in
- * ascending (batch index i, ty, tx) order, encoded i << 16 | ty << 8 | tx, where
- * i indexes that call's stream batch.  *count receives the length; at most
+/* Work list of layer 1..n_conv from the last step: the dirty tiles in
+ * ascending (ty, tx, batch index i) order, encoded i << 16 | ty << 8 | tx, where
+ * i indexes that call's stream batch (RN_ESTATE after a full).  *count receives the length; at most
  * cap entries are copied (RN_ENOSPACE if cap < count, with *count still set). */
 rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, size_t cap,
                                  int32_t *count);

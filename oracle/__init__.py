@@ -133,6 +133,17 @@ def box_mask(h: int, w: int, boxes) -> np.ndarray:
     return d0
 
 
+def variant_input(base: np.ndarray, frame: np.ndarray, boxes) -> np.ndarray:
+    """Input [C][H][W] of a known-change variant (Sec. 1, occlusion use): the
+    base input with the pixels inside the boxes (half-open, clipped, union)
+    taken from `frame`; every other pixel keeps the base value."""
+    base = _f32(base)
+    inside = box_mask(base.shape[1], base.shape[2], boxes).astype(bool)
+    x = base.copy()
+    x[:, inside] = _f32(frame)[:, inside]
+    return x
+
+
 def dilate(d: np.ndarray, k: int, s: int, p: int) -> np.ndarray:
     d = _u8(d)
     h, w = d.shape

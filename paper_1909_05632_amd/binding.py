@@ -32,7 +32,7 @@ EXPORTS = (
     "reuse_net_reset", "reuse_net_get_pixel_mask", "reuse_net_get_tile_mask",
     "reuse_net_get_worklist", "reuse_net_read_activation", "reuse_net_get_stats",
     "reuse_net_set_profiling", "reuse_net_get_profile", "reuse_net_last_error",
-    "reuse_net_destroy",
+    "reuse_net_destroy", "reuse_net_variant_scratch_bytes", "reuse_net_variants",
 )
 
 
@@ -91,6 +91,10 @@ def load_library(path: str = LIB_PATH):
     L.reuse_net_full.argtypes = [P, I32, P, P, ctypes.c_int, P, P]
     L.reuse_net_reset.restype = st
     L.reuse_net_reset.argtypes = [P, I32]
+    L.reuse_net_variant_scratch_bytes.restype = SZ
+    L.reuse_net_variant_scratch_bytes.argtypes = [P, I32, I32]
+    L.reuse_net_variants.restype = st
+    L.reuse_net_variants.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, SZ, P, P]
     for name in ("reuse_net_get_pixel_mask", "reuse_net_get_tile_mask"):
         getattr(L, name).restype = st
         getattr(L, name).argtypes = [P, I32, I32, P, SZ]
@@ -152,6 +156,18 @@ def reuse_net_full(net: int, n: int, dev_stream_ids: int, dev_frames: int, frame
 
 def reuse_net_reset(net: int, stream_id: int) -> None:
     _check(load_library().reuse_net_reset(net, stream_id), net)
+
+
+def reuse_net_variant_scratch_bytes(net: int, n: int, max_tiles: int) -> int:
+    return load_library().reuse_net_variant_scratch_bytes(net, n, max_tiles)
+
+
+def reuse_net_variants(net: int, base_stream: int, n: int, dev_frames: int, frame_dtype: int,
+                       frame_count: int, dev_boxes: int, dev_box_off: int, max_tiles: int,
+                       dev_scratch: int, scratch_bytes: int, dev_logits: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_variants(net, base_stream, n, dev_frames, frame_dtype, frame_count,
+                                             dev_boxes, dev_box_off, max_tiles, dev_scratch,
+                                             scratch_bytes, dev_logits, hip_stream), net)
 
 
 def reuse_net_get_pixel_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
@@ -297,6 +313,31 @@ class ReuseNet:
     def reset(self, stream_id: int = -1):
         reuse_net_reset(self.handle, stream_id)
 
+    def variants(self, base_stream: int, boxes, box_off, frames, max_tiles: int = 0, out=None,
+                 stream=None):
+        """Logits of n variants of slot base_stream (reuse_net_variants): variant i
+        takes the pixels of its boxes [box_off[i], box_off[i+1]) from frames[i]
+        (frames of length n) or frames[0] (length 1).  The scratch is a torch
+        tensor kept on this object and grown as needed."""
+        t = self.torch
+        frames, code = self._frames(frames)
+        n = box_off.shape[0] - 1
+        need = reuse_net_variant_scratch_bytes(self.handle, n, max_tiles)
+        if need == 0:
+            _check(load_library().reuse_net_variants(self.handle, base_stream, n, None, 0, 0, None,
+                                                     None, max_tiles, None, 0, None, None),
+                   self.handle)
+        if getattr(self, "_scratch", None) is None or self._scratch.numel() < need:
+            self._scratch = t.empty(need, dtype=t.uint8, device=self.device)
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_variants(self.handle, base_stream, n, frames.data_ptr(), code, frames.shape[0],
+                           boxes.data_ptr(), box_off.data_ptr(), max_tiles, self._scratch.data_ptr(),
+                           self._scratch.numel(), out.data_ptr(), s)
+        self._last_batch = n
+        return out
+
     # -- introspection
     def pixel_mask(self, layer: int, stream_id: int) -> np.ndarray:
         """uint64 [H][words_per_row] bit rows."""
@@ -317,7 +358,8 @@ class ReuseNet:
         return bits[:th * tw].reshape(th, tw)
 
     def worklist(self, layer: int, cap: Optional[int] = None) -> np.ndarray:
-        cap = cap if cap is not None else self.max_streams * self.tiles[0] * self.tiles[1]
+        batch = max(self.max_streams, getattr(self, "_last_batch", 0))
+        cap = cap if cap is not None else batch * self.tiles[0] * self.tiles[1]
         return reuse_net_get_worklist(self.handle, layer, cap)
 
     def activation(self, stream_id: int, layer: int) -> np.ndarray:

@@ -34,8 +34,10 @@ using namespace dev;
 
 // Direct conv for a few input channels (1, or 4 stacked frames): 9 * CIN FMAs
 // per output, too few for a matrix core to pay off; the layer is HBM-bound on
-// its output writes.  One wave per tile; weights and bias in LDS.
-template <int CIN, int COUT, bool DENSE>
+// its output writes.  One wave per tile; weights and bias in LDS.  VAR: the
+// tiles of variants (input from the base slot and the variant's frame, output
+// to the overlay row of the work item).
+template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     __shared__ float s_w[CIN * 9 * COUT];
     __shared__ float s_b[COUT];
@@ -57,28 +59,33 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
         const TileRef r = decode<DENSE>(a, t);
         int head = 0;
-        if (a.stack != 1) head = a.ring_head[r.slot];
+        if (!VAR && a.stack != 1) head = a.ring_head[r.slot];
         for (int h = lane; h < CIN * 36; h += 64) {
             const int c = h / 36, pos = h - c * 36;
             const int hy = pos / 6, hx = pos - hy * 6;
             const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
             float v = 0.0f;
             if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
-                const float *plane;
-                if (a.stack == 1) {
-                    plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                if constexpr (VAR) {
+                    v = var_input(a, r.slot, c, y, x);
                 } else {
-                    // Channel c = frame j (oldest first) of the ring, channel c1 of it.
-                    const int j = c / cin1, c1 = c - j * cin1;
-                    const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
-                    plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                    const float *plane;
+                    if (a.stack == 1) {
+                        plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                    } else {
+                        // Channel c = frame j (oldest first) of the ring, channel c1 of it.
+                        const int j = c / cin1, c1 = c - j * cin1;
+                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                        plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                    }
+                    v = plane[(size_t)y * a.W + x];
                 }
-                v = plane[(size_t)y * a.W + x];
             }
             halo[h] = v;
         }
         wave_sync();
-        float *dst = outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
+        float *dst = VAR ? static_cast<float *>(a.vov_out) + (size_t)t * kTilePx * COUT
+                         : outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
         for (int o = lane; o < kTilePx * COUT; o += 64) {
             const int m = o / COUT, co = o - m * COUT;
             const int py = m >> 2, px = m & 3;
@@ -143,10 +150,10 @@ struct Mfma {
 };
 
 // Global -> registers: the halo of one tile, 16 bytes per lane per load.
-template <int CIN, int COUT>
+template <int CIN, int COUT, bool VAR>
 __device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *regs, int lane) {
     using M = Mfma<CIN, COUT>;
-    const float *src = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
+    const float *src = static_cast<const float *>(a.in) + (VAR ? 0 : (size_t)r.slot * a.in_stride);
 #pragma unroll
     for (int j = 0; j < M::HV; ++j) {
         const int h = lane + 64 * j;
@@ -157,7 +164,8 @@ __device__ inline void fetch_halo(const ConvArgs &a, const TileRef &r, float4 *r
             const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
             if (y >= 0 && y < a.H && x >= 0 && x < a.W)
                 v = *reinterpret_cast<const float4 *>(
-                    src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
+                    (VAR ? var_src<float>(a, r.slot, y, x, CIN)
+                         : src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN) +
                     c4 * 4);
         }
         regs[j] = v;
@@ -191,10 +199,13 @@ __device__ inline void store_halo(float *halo, const float4 *regs, int lane) {
 // around it, in the same FMA order as k_conv_first_f32 (so the values are the
 // bits that kernel would have cached).  Halo pixels outside the image are the
 // layer-2 zero padding.
+template <bool VAR>
 __device__ inline float fetch_patch(const ConvArgs &a, const TileRef &r, int lane) {
     const int y = r.ty * kTile - 2 + (lane >> 3), x = r.tx * kTile - 2 + (lane & 7);
+    const bool in = y >= 0 && y < a.H && x >= 0 && x < a.W;
+    if constexpr (VAR) return in ? var_input(a, r.slot, 0, y, x) : 0.f;
     const float *plane = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
-    return (y >= 0 && y < a.H && x >= 0 && x < a.W) ? plane[(size_t)y * a.W + x] : 0.f;
+    return in ? plane[(size_t)y * a.W + x] : 0.f;
 }
 
 // The 8x8 input patch sits in the last 64 floats of the wave's halo area
@@ -331,9 +342,12 @@ __device__ inline void mfma_positions(floatx4 *acc, const float *halo, const flo
 // no head partials), else -1 (a.n_out at run time).  A fixed count keeps the
 // number of memory operations per tile fixed, so the next tile's waits can
 // name exactly the loads they need instead of draining this tile's stores.
-template <int CIN, int COUT, int NO>
+// VAR: work item widx of a variant list; the outputs go to overlay row widx
+// (none for a last layer, which only feeds the head), the partials to row
+// widx of the variant partials.
+template <int CIN, int COUT, int NO, bool VAR>
 __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *acc, const float *s_bias,
-                                float *stage, int lane) {
+                                float *stage, int lane, int widx) {
     using M = Mfma<CIN, COUT>;
     const int mrow = lane & 15, kq = lane >> 4;       // D holds pixels (py = i, px = kq)
     const bool col_in = r.tx * kTile + kq < a.W;
@@ -399,19 +413,24 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
                 float v = p[0];
 #pragma unroll
                 for (int q = 1; q < 8; ++q) v = lane == q ? p[q] : v;
-                a.hpart[((size_t)r.slot * ntiles + r.tile) * n_out + o0 + lane] = v;
+                float *hp = VAR ? a.vhpart + (size_t)widx * n_out
+                                : a.hpart + ((size_t)r.slot * ntiles + r.tile) * n_out;
+                hp[o0 + lane] = v;
             }
         }
     }
     // The tile's stores go last: the next tile's waits on its own loads then
     // never have to drain them.
-    float4 *d4 = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
-                                            (size_t)r.tile * kTilePx * COUT);
+    if (!VAR || n_out == 0) {
+        float4 *d4 = reinterpret_cast<float4 *>(
+            VAR ? static_cast<float *>(a.vov_out) + (size_t)widx * kTilePx * COUT
+                : static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT);
 #pragma unroll
-    for (int j = 0; j < M::NB; ++j) {              // 16 * COUT / 4 float4 = 64 * NB
-        const int o4 = lane + 64 * j;
-        const int e = 4 * o4, m = e / COUT, n = e - m * COUT;
-        d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
+        for (int j = 0; j < M::NB; ++j) {              // 16 * COUT / 4 float4 = 64 * NB
+            const int o4 = lane + 64 * j;
+            const int e = 4 * o4, m = e / COUT, n = e - m * COUT;
+            d4[o4] = *reinterpret_cast<const float4 *>(stage + m * M::SR + n);
+        }
     }
     wave_sync();
 }
@@ -425,7 +444,7 @@ struct Resident {
         (size_t)(Mfma<CIN, COUT>::WTOT + WAVES * Mfma<CIN, COUT>::HALO) * sizeof(float);
 };
 
-template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE, int NO>
+template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE, int NO, bool VAR>
 __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
     extern __shared__ float smem[];
@@ -459,8 +478,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     float pin = 0.f;
     uint32_t e_cur = item_word<DENSE>(a, t);
     uint32_t e_nxt = t + stride < xr.end ? item_word<DENSE>(a, t + stride) : 0u;
-    if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = fetch_patch(a, item_ref(a, e_cur), lane);
-    else fetch_halo<CIN, COUT>(a, item_ref(a, e_cur), pre, lane);
+    if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = fetch_patch<VAR>(a, item_ref(a, e_cur), lane);
+    else fetch_halo<CIN, COUT, VAR>(a, item_ref(a, e_cur), pre, lane);
     for (; t < xr.end; t += stride) {
         const TileRef cur = item_ref(a, e_cur);
         if constexpr (FUSE) build_halo_fused<CIN, COUT>(halo, a, cur, s_w1, s_b1, lane);
@@ -468,8 +487,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         wave_sync();
         const uint32_t e_nn = t + 2 * stride < xr.end ? item_word<DENSE>(a, t + 2 * stride) : 0u;
         // The next tile's input (past the end: item 0's, never used).
-        if constexpr (FUSE) pin = fetch_patch(a, item_ref(a, e_nxt), lane);
-        else if (t + stride < xr.end) fetch_halo<CIN, COUT>(a, item_ref(a, e_nxt), pre, lane);
+        if constexpr (FUSE) pin = fetch_patch<VAR>(a, item_ref(a, e_nxt), lane);
+        else if (t + stride < xr.end) fetch_halo<CIN, COUT, VAR>(a, item_ref(a, e_nxt), pre, lane);
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -480,7 +499,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
         __builtin_amdgcn_s_setprio(0);
         wave_sync();
-        epilogue<CIN, COUT, NO>(a, cur, acc, s_bias, halo, lane);
+        epilogue<CIN, COUT, NO, VAR>(a, cur, acc, s_bias, halo, lane, t);
         // The next patch goes to LDS here rather than at the top of the loop:
         // the wait for its load then counts exactly this tile's later memory
         // operations, where at the loop top it would have to drain them all.
@@ -537,7 +556,7 @@ __device__ inline void store_wstage(float *dst, const floatx4 *regs, int tid) {
 
 // Halo of tile r into registers with every load issued; bit j of `ok` says
 // whether element j counts (inside the image and `valid`).
-template <int CIN, int COUT>
+template <int CIN, int COUT, bool VAR>
 __device__ inline void fetch_halo_all(const ConvArgs &a, const TileRef &r, bool valid, floatx4 *regs, uint32_t &ok,
                                       int lane) {
     using M = Mfma<CIN, COUT>;
@@ -551,11 +570,16 @@ __device__ inline void fetch_halo_all(const ConvArgs &a, const TileRef &r, bool 
         const int hy = pos / 6, hx = pos - hy * 6;
         const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
         const bool in = valid && h < 36 * M::C4 && y >= 0 && y < a.H && x >= 0 && x < a.W;
-        const size_t e = in ? (size_t)r.slot * a.in_stride +
-                                  ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
-                                  c4 * 4
-                            : 0;
-        regs[j] = *reinterpret_cast<const floatx4 *>(base + e);
+        const float *src;
+        if constexpr (VAR) {
+            src = in ? var_src<float>(a, r.slot, y, x, CIN) + c4 * 4 : base;
+        } else {
+            src = base + (in ? (size_t)r.slot * a.in_stride +
+                                   ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN +
+                                   c4 * 4
+                             : 0);
+        }
+        regs[j] = *reinterpret_cast<const floatx4 *>(src);
         ok |= (uint32_t)in << j;
     }
 }
@@ -602,7 +626,7 @@ __device__ inline void mfma_stage(floatx4 *acc, const float *halo, const float *
     }
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
@@ -625,7 +649,7 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     fetch_wstage<CIN, COUT>(wg, 0, wreg, tid);
     floatx4 hreg[M::HV];
     uint32_t hok;
-    fetch_halo_all<CIN, COUT>(a, item_ref(a, e_cur), t < xr.end, hreg, hok, lane);
+    fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_cur), t < xr.end, hreg, hok, lane);
     store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);
     store_wstage<CIN, COUT>(wbuf, wreg, tid);
     fetch_wstage<CIN, COUT>(wg, 1 % S::NQ, wreg, tid);
@@ -646,7 +670,7 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
             // registers, the next halo at mid-group, then the matrix work.
             store_wstage<CIN, COUT>(wbuf + (buf ^ 1) * S::WST, wreg, tid);
             fetch_wstage<CIN, COUT>(wg, (q + 2) % S::NQ, wreg, tid);
-            if (q == S::NQ / 2) fetch_halo_all<CIN, COUT>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
+            if (q == S::NQ / 2) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
             const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
             if (valid) mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane);
             buf ^= 1;
@@ -654,7 +678,7 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         }
         if (valid) {
             wave_sync();
-            epilogue<CIN, COUT, -1>(a, item_ref(a, e_cur), acc, s_bias, halo, lane);
+            epilogue<CIN, COUT, -1, VAR>(a, item_ref(a, e_cur), acc, s_bias, halo, lane, t);
         }
         store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);      // this wave's own area
         wave_sync();
@@ -675,10 +699,10 @@ constexpr bool fused_fits() {
     return Resident<CIN, COUT, 8>::lds_bytes + (COUT + 10 * CIN) * sizeof(float) <= 160 * 1024;
 }
 
-template <int CIN, int COUT, bool DENSE, bool FUSE, int NO>
+template <int CIN, int COUT, bool DENSE, bool FUSE, int NO, bool VAR>
 hipError_t run_resident_no(const ConvArgs &a, int cus, hipStream_t s) {
     constexpr size_t lds = Resident<CIN, COUT, 8>::lds_bytes;
-    auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE, FUSE, NO>;
+    auto kern = k_conv_mfma_res<CIN, COUT, 8, DENSE, FUSE, NO, VAR>;
     static hipError_t attr = set_lds(kern, lds);
     if (attr != hipSuccess) return attr;
     const int grid = persistent_grid(cus, (a.max_tiles + 7) / 8);
@@ -687,23 +711,23 @@ hipError_t run_resident_no(const ConvArgs &a, int cus, hipStream_t s) {
 }
 
 // Logit count as a template argument where it is a common one.
-template <int CIN, int COUT, bool DENSE, bool FUSE>
+template <int CIN, int COUT, bool DENSE, bool FUSE, bool VAR>
 hipError_t run_resident(const ConvArgs &a, int cus, hipStream_t s) {
-    if (a.n_out == 0) return run_resident_no<CIN, COUT, DENSE, FUSE, 0>(a, cus, s);
-    if (a.n_out == 6) return run_resident_no<CIN, COUT, DENSE, FUSE, 6>(a, cus, s);
-    return run_resident_no<CIN, COUT, DENSE, FUSE, -1>(a, cus, s);
+    if (a.n_out == 0) return run_resident_no<CIN, COUT, DENSE, FUSE, 0, VAR>(a, cus, s);
+    if (a.n_out == 6) return run_resident_no<CIN, COUT, DENSE, FUSE, 6, VAR>(a, cus, s);
+    return run_resident_no<CIN, COUT, DENSE, FUSE, -1, VAR>(a, cus, s);
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
     if constexpr (use_resident<CIN, COUT>()) {
-        if (a.fuse_first) return run_resident<CIN, COUT, DENSE, true>(a, cus, s);
-        return run_resident<CIN, COUT, DENSE, false>(a, cus, s);
+        if (a.fuse_first) return run_resident<CIN, COUT, DENSE, true, VAR>(a, cus, s);
+        return run_resident<CIN, COUT, DENSE, false, VAR>(a, cus, s);
     } else {
         if (a.fuse_first) return hipErrorInvalidValue;
         constexpr size_t lds = Staged<CIN, COUT>::lds_bytes;
         static_assert(lds <= kLdsBudget, "staged layer exceeds LDS");
-        auto kern = k_conv_mfma_staged<CIN, COUT, DENSE>;
+        auto kern = k_conv_mfma_staged<CIN, COUT, DENSE, VAR>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
         const int grid = persistent_grid(cus, (a.max_tiles + 3) / 4);
@@ -712,11 +736,11 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
     const int total_max = a.max_tiles;
     const int grid = persistent_grid(cus * 8, (total_max + 3) / 4);
-    hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -751,23 +775,27 @@ bool conv_first_supported(int cin, int cout, rn_dtype dt) {
 
 // cus: compute units of the device; the persistent grid is at most one block
 // (resident or staged MFMA kernel) or eight blocks (first layer) per CU.
-hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s) {
+hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s, bool var) {
     (void)dt;
     const bool dense = a.wl == nullptr;
+    if (var && dense) return hipErrorInvalidValue;
 #define X(ci, co)                                                                          \
     if (a.cin == ci && a.cout == co)                                                       \
-        return dense ? run_mfma<ci, co, true>(a, cus, s) : run_mfma<ci, co, false>(a, cus, s);
+        return var ? run_mfma<ci, co, false, true>(a, cus, s)                              \
+                   : dense ? run_mfma<ci, co, true, false>(a, cus, s) : run_mfma<ci, co, false, false>(a, cus, s);
     RN_MFMA_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s) {
+hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int cus, hipStream_t s, bool var) {
     (void)dt;
     const bool dense = a.wl == nullptr;
+    if (var && dense) return hipErrorInvalidValue;
 #define X(ci, co)                                                                          \
     if (a.cin == ci && a.cout == co)                                                       \
-        return dense ? run_first<ci, co, true>(a, cus, s) : run_first<ci, co, false>(a, cus, s);
+        return var ? run_first<ci, co, false, true>(a, cus, s)                             \
+                   : dense ? run_first<ci, co, true, false>(a, cus, s) : run_first<ci, co, false, false>(a, cus, s);
     RN_FIRST_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;

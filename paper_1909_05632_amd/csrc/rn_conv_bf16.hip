@@ -32,7 +32,9 @@ __device__ inline float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h <<
 
 // Direct conv for a few input channels; the input is rounded to bf16 as it is
 // staged, the weights arrive rounded, the output is rounded and stored as bf16.
-template <int CIN, int COUT, bool DENSE>
+// VAR: variant tiles (input from the base slot and the variant's frame, output
+// to the work item's overlay row).
+template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
     __shared__ float s_w[CIN * 9 * COUT];
     __shared__ float s_b[COUT];
@@ -54,27 +56,32 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
     for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
         const TileRef r = decode<DENSE>(a, t);
         int head = 0;
-        if (a.stack != 1) head = a.ring_head[r.slot];
+        if (!VAR && a.stack != 1) head = a.ring_head[r.slot];
         for (int h = lane; h < CIN * 36; h += 64) {
             const int c = h / 36, pos = h - c * 36;
             const int hy = pos / 6, hx = pos - hy * 6;
             const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
             float v = 0.0f;
             if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
-                const float *plane;
-                if (a.stack == 1) {
-                    plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                if constexpr (VAR) {
+                    v = bf2f(f2bf(var_input(a, r.slot, c, y, x)));
                 } else {
-                    const int j = c / cin1, c1 = c - j * cin1;
-                    const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
-                    plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                    const float *plane;
+                    if (a.stack == 1) {
+                        plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                    } else {
+                        const int j = c / cin1, c1 = c - j * cin1;
+                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                        plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                    }
+                    v = bf2f(f2bf(plane[(size_t)y * a.W + x]));
                 }
-                v = bf2f(f2bf(plane[(size_t)y * a.W + x]));
             }
             halo[h] = v;
         }
         wave_sync();
-        uint16_t *dst = outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
+        uint16_t *dst = VAR ? static_cast<uint16_t *>(a.vov_out) + (size_t)t * kTilePx * COUT
+                            : outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
         for (int o = lane; o < kTilePx * COUT; o += 64) {
             const int m = o / COUT, co = o - m * COUT;
             const int py = m >> 2, px = m & 3;
@@ -176,7 +183,7 @@ __device__ inline int halo_chunk(int hy, int hx, int c) {
 // PSTEP j, p0 = (tid % (THREADS / T)) / C8.  The load is always issued (from
 // the cache's first element when the pixel is outside the image, past 36 or
 // of an absent tile) and bit j of `ok` says whether it counts.
-template <int CIN, int COUT, int J>
+template <int CIN, int COUT, bool VAR, int J>
 __device__ inline void fetch_halo_chunk(const ConvArgs &a, const uint32_t *items, int nvalid, int pass, u32x4 *regs,
                                         uint32_t &ok, int tid) {
     using G = GrpBf<CIN, COUT>;
@@ -188,18 +195,23 @@ __device__ inline void fetch_halo_chunk(const ConvArgs &a, const uint32_t *items
     const int hy = pos / 6, hx = pos - hy * 6;
     const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
     const bool in = t < nvalid && pos < 36 && y >= 0 && y < a.H && x >= 0 && x < a.W;
-    const size_t e = in ? (size_t)r.slot * a.in_stride + pass * G::HC + c * 8 +
+    const uint16_t *src;
+    if constexpr (VAR) {
+        src = in ? var_src<uint16_t>(a, r.slot, y, x, CIN) + pass * G::HC + c * 8 : inp;
+    } else {
+        src = inp + (in ? (size_t)r.slot * a.in_stride + pass * G::HC + c * 8 +
                               ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN
-                        : 0;
-    regs[J] = *reinterpret_cast<const u32x4 *>(inp + e);
+                        : 0);
+    }
+    regs[J] = *reinterpret_cast<const u32x4 *>(src);
     ok = in ? ok | (1u << J) : ok & ~(1u << J);
 }
 
-template <int CIN, int COUT, int J0, int J1>
+template <int CIN, int COUT, bool VAR, int J0, int J1>
 __device__ inline void fetch_halos(const ConvArgs &a, const uint32_t *items, int nvalid, int pass, u32x4 *regs,
                                    uint32_t &ok, int tid) {
     [&]<int... J>(std::integer_sequence<int, J...>) {
-        (fetch_halo_chunk<CIN, COUT, J0 + J>(a, items, nvalid, pass, regs, ok, tid), ...);
+        (fetch_halo_chunk<CIN, COUT, VAR, J0 + J>(a, items, nvalid, pass, regs, ok, tid), ...);
     }(std::make_integer_sequence<int, J1 - J0>{});
 }
 
@@ -297,7 +309,7 @@ __device__ inline void stage_mma(floatx16 (&acc)[MP][NBW], const FragsBf<MP, NBW
     }
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     using G = GrpBf<CIN, COUT>;
     constexpr int NQ = 9 * G::NPASS;                      // stages per group
@@ -335,7 +347,7 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     lds_barrier();
     u32x4 hreg[G::HPT];
     uint32_t hok = 0;
-    fetch_halos<CIN, COUT, 0, G::HPT>(a, s_items[0], nvalid_of(0), 0, hreg, hok, tid);
+    fetch_halos<CIN, COUT, VAR, 0, G::HPT>(a, s_items[0], nvalid_of(0), 0, hreg, hok, tid);
     store_halos<CIN, COUT>(halos, hreg, hok, tid);
     store_stage<CIN, COUT>(wbuf, wreg, tid);
     fetch_stage<CIN, COUT>(wg, 1, wreg, tid);
@@ -384,9 +396,10 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
                     store_stage<CIN, COUT>(wbuf + ((kpos + 2) % 3) * G::WST, wreg, tid);
                     fetch_stage<CIN, COUT>(wg, (q + 3) % NQ, wreg, tid);
                 });
-                if constexpr (kpos == 1) fetch_halos<CIN, COUT, 0, G::HPT / 2>(a, hitems, hvalid, hpass, hreg, hok, tid);
+                if constexpr (kpos == 1)
+                    fetch_halos<CIN, COUT, VAR, 0, G::HPT / 2>(a, hitems, hvalid, hpass, hreg, hok, tid);
                 if constexpr (kpos == 3)
-                    fetch_halos<CIN, COUT, G::HPT / 2, G::HPT>(a, hitems, hvalid, hpass, hreg, hok, tid);
+                    fetch_halos<CIN, COUT, VAR, G::HPT / 2, G::HPT>(a, hitems, hvalid, hpass, hreg, hok, tid);
                 if constexpr (kpos < 8)
                     load_kstep<CIN, COUT>(f0, halos, wbuf + ((kpos + 1) % 3) * G::WST, kpos + 1, 0, wm, half, lane);
                 lds_barrier();
@@ -421,7 +434,9 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
             const int t = wm * 2 * G::MP + 2 * p + (col >> 4);
             const TileRef r = item_ref(a, s_items[cur][t]);
             const bool inside = (r.ty * kTile + py < a.H) & (r.tx * kTile + px < a.W);
-            uint16_t *dst = outp + (size_t)r.slot * a.out_stride + ((size_t)r.tile * kTilePx + py * 4 + px) * COUT;
+            // VAR: the work item's index is g + t, its overlay row.
+            uint16_t *dst = VAR ? static_cast<uint16_t *>(a.vov_out) + ((size_t)(g + t) * kTilePx + py * 4 + px) * COUT
+                                : outp + (size_t)r.slot * a.out_stride + ((size_t)r.tile * kTilePx + py * 4 + px) * COUT;
 #pragma unroll
             for (int nb = 0; nb < G::NBW; ++nb) {
                 const int nbase = (half * G::NBW + nb) * 32;
@@ -452,12 +467,12 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     }
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 hipError_t run_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s) {
     using G = GrpBf<CIN, COUT>;
     if (a.n_out > 0) return hipErrorInvalidValue;          // head partials come from their own kernel
     constexpr size_t lds = G::lds_bytes;
-    auto kern = k_conv_bf16_grp<CIN, COUT, DENSE>;
+    auto kern = k_conv_bf16_grp<CIN, COUT, DENSE, VAR>;
     static hipError_t attr = set_lds(kern, lds);
     if (attr != hipSuccess) return attr;
     const int grid = persistent_grid(cus, (a.max_tiles + G::T - 1) / G::T);
@@ -465,10 +480,10 @@ hipError_t run_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int CIN, int COUT, bool DENSE>
+template <int CIN, int COUT, bool DENSE, bool VAR>
 hipError_t run_first_bf16(const ConvArgs &a, int cus, hipStream_t s) {
     const int grid = persistent_grid(cus * 8, (a.max_tiles + 3) / 4);
-    hipLaunchKernelGGL((k_conv_first_bf16<CIN, COUT, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_conv_first_bf16<CIN, COUT, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -499,21 +514,25 @@ bool conv_first_bf16_supported(int cin, int cout) {
     return false;
 }
 
-hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s) {
+hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var) {
     const bool dense = a.wl == nullptr;
+    if (var && dense) return hipErrorInvalidValue;
 #define X(ci, co)                                                                                \
     if (a.cin == ci && a.cout == co)                                                             \
-        return dense ? run_mfma_bf16<ci, co, true>(a, cus, s) : run_mfma_bf16<ci, co, false>(a, cus, s);
+        return var ? run_mfma_bf16<ci, co, false, true>(a, cus, s)                               \
+                   : dense ? run_mfma_bf16<ci, co, true, false>(a, cus, s) : run_mfma_bf16<ci, co, false, false>(a, cus, s);
     RN_BF16_MFMA_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s) {
+hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var) {
     const bool dense = a.wl == nullptr;
+    if (var && dense) return hipErrorInvalidValue;
 #define X(ci, co)                                                                                \
     if (a.cin == ci && a.cout == co)                                                             \
-        return dense ? run_first_bf16<ci, co, true>(a, cus, s) : run_first_bf16<ci, co, false>(a, cus, s);
+        return var ? run_first_bf16<ci, co, false, true>(a, cus, s)                              \
+                   : dense ? run_first_bf16<ci, co, true, false>(a, cus, s) : run_first_bf16<ci, co, false, false>(a, cus, s);
     RN_BF16_FIRST_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;

@@ -72,6 +72,39 @@ __device__ inline int work_count(const ConvArgs &a) {
     else return *a.cnt;
 }
 
+// ---- variant mode: copy-on-write overlays of one base slot
+//
+// A variant is the base slot's input with the pixels of its change boxes
+// taken from its own frame.  It owns no caches: the tiles it recomputes in a
+// layer go to that layer's overlay, row = their index in the layer's work
+// list, and everything else is read from the base slot.
+
+// Input value (float32, channel c, pixel (y, x) inside the image) of variant i.
+__device__ inline float var_input(const ConvArgs &a, int i, int c, int y, int x) {
+    const size_t HW = (size_t)a.H * a.W, px = (size_t)y * a.W + x;
+    const uint64_t w = a.vpm0[((size_t)i * a.H + y) * a.WW + (x >> 6)];
+    if ((w >> (x & 63)) & 1ull) {
+        const size_t f = (a.vframe_shared ? 0 : (size_t)i * a.vcin) * HW + (size_t)c * HW + px;
+        return a.vframe_u8 ? a.lut[static_cast<const uint8_t *>(a.vframes)[f]]
+                           : static_cast<const float *>(a.vframes)[f];
+    }
+    return static_cast<const float *>(a.in)[(size_t)a.vbase * a.in_stride + (size_t)c * HW + px];
+}
+
+// Address of channel 0 of pixel (y, x) (inside the image) of layer l-1 as
+// variant i sees it: its overlay row where it recomputed the tile, else the
+// base slot's cache.
+template <typename T>
+__device__ inline const T *var_src(const ConvArgs &a, int i, int y, int x, int cin) {
+    const int ntiles = a.TH * a.TW, TMW = (ntiles + 63) >> 6;
+    const int t = (y >> 2) * a.TW + (x >> 2);
+    const int m = ((y & 3) * 4 + (x & 3)) * cin;
+    const uint64_t w = a.vtm_in[(size_t)i * TMW + (t >> 6)];
+    if ((w >> (t & 63)) & 1ull)
+        return static_cast<const T *>(a.vov_in) + (size_t)a.vmap_in[(size_t)i * ntiles + t] * kTilePx * cin + m;
+    return static_cast<const T *>(a.in) + (size_t)a.vbase * a.in_stride + (size_t)t * kTilePx * cin + m;
+}
+
 // XCD-aware split of the work items [0, cnt): workgroups are dispatched round
 // robin over the chip's 8 XCDs (block b runs on XCD b % 8), each with its own
 // L2.  Item range [cnt x / 8, cnt (x + 1) / 8) goes to the blocks of XCD x, so

@@ -149,6 +149,73 @@ __global__ __launch_bounds__(kThreads) void k_tile_head(TileHeadArgs a) {
     }
 }
 
+// Variant mode: a variant that was left out of the work lists (more than vmax
+// dirty tiles in some layer), or whose base slot holds no state yet, gets NaN.
+__device__ inline bool var_bad(const TileHeadArgs &a, int i) {
+    if (!a.primed[a.vbase]) return true;
+    if (a.vmax <= 0) return false;
+    for (int l = 1; l <= a.L; ++l)
+        if (a.ntile[(size_t)i * (a.L + 1) + l] > a.vmax) return true;
+    return false;
+}
+
+// Partials of tile t as variant i sees them: its own row where it recomputed
+// the tile, else the base slot's.  Only for variants that passed var_bad: a
+// variant left out of the lists has tile-mask bits but no list rows.
+__device__ inline const float *var_part(const TileHeadArgs &a, int i, int t, int no) {
+    const uint64_t w = a.vtm[(size_t)i * a.TMW + (t >> 6)];
+    if ((w >> (t & 63)) & 1ull) return a.vhpart + (size_t)a.vmap[(size_t)i * a.ntiles + t] * no;
+    return a.hpart + ((size_t)a.vbase * a.ntiles + t) * no;
+}
+
+// k_tile_head for variants: the same fixed order of tiles and of the sums, so
+// a variant whose boxes are empty gets the base slot's logits bit for bit.
+template <int NO>
+__global__ __launch_bounds__(kThreads) void k_tile_head_var(TileHeadArgs a) {
+    __shared__ float red[kThreads / 64][NO];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = blockIdx.x;
+    if (var_bad(a, i)) {                                   // uniform per block
+        if (threadIdx.x < NO) a.logits[(size_t)i * NO + threadIdx.x] = __builtin_nanf("");
+        return;
+    }
+    float acc[NO];
+#pragma unroll
+    for (int o = 0; o < NO; ++o) acc[o] = 0.f;
+    for (int t = threadIdx.x; t < a.ntiles; t += kThreads) {
+        const float *P = var_part(a, i, t, NO);
+#pragma unroll
+        for (int o = 0; o < NO; ++o) acc[o] += P[o];
+    }
+#pragma unroll
+    for (int o = 0; o < NO; ++o) {
+        float v = acc[o];
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0) red[wave][o] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < NO) {
+        float v = red[0][threadIdx.x];
+        for (int w = 1; w < kThreads / 64; ++w) v += red[w][threadIdx.x];
+        a.logits[(size_t)i * NO + threadIdx.x] = v + a.bias[threadIdx.x];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_tile_head_var_generic(TileHeadArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = blockIdx.x;
+    if (var_bad(a, i)) {                                   // uniform per block
+        for (int o = threadIdx.x; o < a.n_out; o += kThreads) a.logits[(size_t)i * a.n_out + o] = __builtin_nanf("");
+        return;
+    }
+    for (int o = wave; o < a.n_out; o += kThreads / 64) {
+        float v = 0.f;
+        for (int t = lane; t < a.ntiles; t += 64) v += var_part(a, i, t, a.n_out)[o];
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0) a.logits[(size_t)i * a.n_out + o] = v + a.bias[o];
+    }
+}
+
 // Any n_out: wave w of the block handles logits o = w, w + 4, ...
 __global__ __launch_bounds__(kThreads) void k_tile_head_generic(TileHeadArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -227,7 +294,10 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
 // its rows has that position, and keeps only those rows.  Each row's sum runs
 // over the full K in one wave in a fixed order, so the result does not depend
 // on which rows share the block: list and dense passes agree bit for bit.
-template <int C, int NBO, bool DENSE>
+// VAR: variant work items; the tile's activations are its overlay row (the
+// item's list index) and its partials go to the same row of the variant
+// partials.
+template <int C, int NBO, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     constexpr int KS = 16 * C / 32;           // k-steps
     constexpr int KB = 8;                     // k-steps per batch of loads
@@ -253,7 +323,9 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
         __syncthreads();
         // Positions of the wave's 16 rows, for the per-pass "any row of mine" test.
         uint64_t mine_mask = 0;
-        const uint16_t *arow = act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C + 8 * kq;
+        const uint16_t *arow = (VAR ? static_cast<const uint16_t *>(a.vov_in) + (size_t)it * kTilePx * C
+                                    : act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C) +
+                               8 * kq;
         uint64_t done = 0;                                   // rows of the block handled
         for (;;) {
             int P = -1;
@@ -297,7 +369,9 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
                     const uint32_t eq = __shfl(e, q, 64);   // lane q holds row q's item
                     if (o < a.n_out && ((mine_mask >> q) & 1)) {
                         const TileRef rq = item_ref(a, eq);
-                        a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = acc[nb][i];
+                        float *hp = VAR ? a.vhpart + (size_t)(g + wave * 16 + q) * a.n_out
+                                        : a.hpart + ((size_t)rq.slot * ntiles + rq.tile) * a.n_out;
+                        hp[o] = acc[nb][i];
                     }
                 }
             }
@@ -361,26 +435,40 @@ void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, i
     }
 }
 
-template <int C, bool DENSE>
+template <int C, bool DENSE, bool VAR>
 hipError_t run_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
     const int grid = dev::persistent_grid(cus * 4, (a.max_tiles + 63) / 64);
-    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_bf16<C, 1, DENSE>), dim3(grid), dim3(256), 0, s, a);
-    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_bf16<C, 2, DENSE>), dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_tile_part_bf16<C, 4, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_bf16<C, 1, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_bf16<C, 2, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_tile_part_bf16<C, 4, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 bool tile_part_bf16_supported(int C) { return C == 64 || C == 128; }
 
-hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
+hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var) {
     const bool dense = a.wl == nullptr;
-    if (a.cout == 64) return dense ? run_tile_part_bf16<64, true>(a, cus, s) : run_tile_part_bf16<64, false>(a, cus, s);
+    if (var && dense) return hipErrorInvalidValue;
+    if (a.cout == 64)
+        return var ? run_tile_part_bf16<64, false, true>(a, cus, s)
+                   : dense ? run_tile_part_bf16<64, true, false>(a, cus, s) : run_tile_part_bf16<64, false, false>(a, cus, s);
     if (a.cout == 128)
-        return dense ? run_tile_part_bf16<128, true>(a, cus, s) : run_tile_part_bf16<128, false>(a, cus, s);
+        return var ? run_tile_part_bf16<128, false, true>(a, cus, s)
+                   : dense ? run_tile_part_bf16<128, true, false>(a, cus, s)
+                           : run_tile_part_bf16<128, false, false>(a, cus, s);
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s) {
+    if (a.var) {
+        if (a.n_out == 6)
+            hipLaunchKernelGGL(k_tile_head_var<6>, dim3(a.n), dim3(kThreads), 0, s, a);
+        else if (a.n_out == 18)
+            hipLaunchKernelGGL(k_tile_head_var<18>, dim3(a.n), dim3(kThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL(k_tile_head_var_generic, dim3(a.n), dim3(kThreads), 0, s, a);
+        return hipGetLastError();
+    }
     if (a.n_out == 6)
         hipLaunchKernelGGL(k_tile_head<6>, dim3(a.n), dim3(kThreads), 0, s, a);
     else if (a.n_out == 18)

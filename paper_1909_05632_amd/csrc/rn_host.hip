@@ -179,6 +179,51 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     return RN_OK;
 }
 
+// Scratch layout of a reuse_net_variants call: per-variant masks, the work
+// lists, (variant, tile) -> list index maps, the overlays of recomputed tiles
+// (row = list index) and the recomputed tiles' head partials.
+struct VarPlan {
+    int n = 0, vmax = 0;                   // vmax 0: no per-variant limit
+    size_t cap = 0;                        // list capacity per layer
+    size_t o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile, o_wl[RN_MAX_CONV + 1],
+        o_map[RN_MAX_CONV + 1], o_ov[RN_MAX_CONV + 1], o_hp, o_cnt;
+    bool has_ov[RN_MAX_CONV + 1] = {false};
+    size_t total = 0;
+};
+
+// Layer l's recomputed tiles are read back by layer l + 1 (unless layer 1 is
+// folded into layer 2) or, bf16 last layer, by the head-partial kernel; a
+// float32 last layer feeds the head from its epilogue and stores nothing.
+VarPlan plan_variants(const Plan &p, int n, int max_tiles) {
+    VarPlan v;
+    v.n = n;
+    v.vmax = (max_tiles <= 0 || max_tiles >= p.ntiles) ? 0 : max_tiles;
+    v.cap = (size_t)n * (v.vmax ? v.vmax : p.ntiles);
+    const size_t HWW = (size_t)p.H * p.WW;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + std::max<size_t>(bytes, 1));
+        return o;
+    };
+    for (int l = 0; l <= p.L; ++l) {
+        v.o_pm[l] = take((size_t)n * HWW * 8);
+        v.o_tm[l] = take((size_t)n * p.TMW * 8);
+    }
+    v.o_nchg = take((size_t)n * 4);
+    v.o_ntile = take((size_t)n * (p.L + 1) * 4);
+    for (int l = 1; l <= p.L; ++l) {
+        v.o_wl[l] = take(v.cap * 4);
+        v.o_map[l] = take((size_t)n * p.ntiles * 4);
+        v.has_ov[l] = l < p.L ? !(l == 1 && p.fuse_first) : p.dt == RN_BF16;
+        v.o_ov[l] = take(v.has_ov[l] ? v.cap * kTilePx * p.C[l] * p.esz : 0);
+    }
+    v.o_hp = take(v.cap * p.N * 4);
+    v.o_cnt = take((RN_MAX_CONV + 1) * 4);
+    v.total = off;
+    return v;
+}
+
 struct ProfRec {
     int phase;
     hipEvent_t e0, e1;
@@ -195,6 +240,9 @@ struct reuse_net {
     int last_n = 0;
     bool has_step = false;
     bool last_was_full = false;
+    bool last_was_var = false;           // the last call was reuse_net_variants
+    char *var_scratch = nullptr;         // ... with this scratch and layout
+    VarPlan var_plan;
     bool prof = false;
     std::vector<hipEvent_t> pool;
     size_t pool_used = 0;
@@ -392,6 +440,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
         ca.wls[l] = l ? net->at<uint32_t>(p.o_wls[l]) : nullptr;
     }
     ca.cnt = net->at<int32_t>(p.o_cnt);
+    ca.cap = (size_t)n * p.ntiles;
     e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
 
@@ -401,6 +450,167 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     net->last_n = n;
     net->has_step = true;
     net->last_was_full = false;
+    net->last_was_var = false;
+    net->err.clear();
+    return RN_OK;
+}
+
+const char *variants_unsupported(const Plan &p) {
+    if (p.head_mode != RN_HEAD_TILES) return "variants need the tile-partial head (head_mode RN_HEAD_TILES, >= 2 layers)";
+    if (p.stack != 1) return "variants with stacked frames are not implemented";
+    return nullptr;
+}
+
+// n variants of slot `base` in one pass: masks from the boxes, lists and maps,
+// each layer's recomputed tiles into its overlay, the head from base and
+// variant partials.
+rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *frames, rn_dtype fdt,
+                       int32_t frame_count, const int32_t *boxes, const int32_t *box_off, int32_t max_tiles,
+                       void *scratch, size_t scratch_bytes, float *logits, void *stream) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (const char *why = variants_unsupported(p)) return net->fail(RN_EUNSUPPORTED, why);
+    if (base < 0 || base >= p.S) return net->fail(RN_EINVAL, "base_stream out of range");
+    if (n < 1 || n > 65535) return net->fail(RN_EINVAL, "n must be 1..65535");
+    if (!frames) return net->fail(RN_EINVAL, "frames are NULL");
+    if (frame_count != 1 && frame_count != n) return net->fail(RN_EINVAL, "frame_count must be 1 or n");
+    if (fdt != RN_F32 && fdt != RN_U8) return net->fail(RN_EINVAL, "frame dtype must be F32 or U8");
+    if (!boxes || !box_off) return net->fail(RN_EINVAL, "variants need boxes and box offsets");
+    if (!logits) return net->fail(RN_EINVAL, "logits are NULL");
+    if (!scratch) return net->fail(RN_EINVAL, "scratch is NULL");
+    if (reinterpret_cast<uintptr_t>(scratch) % kAlign) return net->fail(RN_EINVAL, "scratch must be 256-byte aligned");
+    const VarPlan vp = plan_variants(p, n, max_tiles);
+    if (scratch_bytes < vp.total)
+        return net->fail(RN_ENOSPACE, "scratch too small: need " + std::to_string(vp.total) + " bytes");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *sc = static_cast<char *>(scratch);
+    auto at = [&](size_t off) { return static_cast<void *>(sc + off); };
+
+    MaskGeom g = make_geom(net);
+    for (int l = 0; l <= p.L; ++l) {
+        g.pmask[l] = static_cast<uint64_t *>(at(vp.o_pm[l]));
+        g.tmask[l] = static_cast<uint64_t *>(at(vp.o_tm[l]));
+    }
+    MaskArgs ma{};
+    ma.n = n;
+    ma.frames = frames;
+    ma.frame_u8 = fdt == RN_U8;
+    ma.boxes = boxes;
+    ma.box_off = box_off;
+    ma.lut = net->at<float>(p.o_lut);
+    ma.nchg = static_cast<int32_t *>(at(vp.o_nchg));
+    ma.ntile = static_cast<int32_t *>(at(vp.o_ntile));
+    ma.variant = 1;
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("mask kernel: ") + hipGetErrorString(e));
+
+    CompactArgs ca{};
+    ca.n = n;
+    ca.L = p.L;
+    ca.TW = p.TW;
+    ca.TMW = p.TMW;
+    ca.ntiles = p.ntiles;
+    ca.ntile = ma.ntile;
+    for (int l = 0; l <= p.L; ++l) {
+        ca.tmask[l] = g.tmask[l];
+        ca.wl[l] = l ? static_cast<uint32_t *>(at(vp.o_wl[l])) : nullptr;
+        ca.vmap[l] = l ? static_cast<int32_t *>(at(vp.o_map[l])) : nullptr;
+    }
+    ca.cnt = static_cast<int32_t *>(at(vp.o_cnt));
+    ca.cap = vp.cap;
+    ca.vmax = vp.vmax;
+    e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
+
+    const bool bf = p.dt == RN_BF16;
+    ConvArgs last{};
+    for (int l = 1; l <= p.L; ++l) {
+        if (l == 1 && p.fuse_first) continue;
+        ConvArgs cv{};
+        cv.wl = ca.wl[l];
+        cv.cnt = ca.cnt + l;
+        cv.in = l == 1 ? static_cast<const void *>(net->at<float>(p.o_xin)) : net->at<void>(p.o_act[l - 1]);
+        cv.w = net->at<void>(p.o_w[l - 1]);
+        cv.bias = net->at<float>(p.o_b[l - 1]);
+        cv.H = p.H;
+        cv.W = p.W;
+        cv.TH = p.TH;
+        cv.TW = p.TW;
+        cv.cin = p.C[l - 1];
+        cv.cout = p.C[l];
+        cv.stack = p.stack;
+        cv.in_stride = p.act_stride[l - 1];
+        cv.out_stride = p.act_stride[l];
+        cv.max_tiles = (int)std::min<size_t>(vp.cap, (size_t)INT32_MAX);
+        cv.vbase = base;
+        cv.vcin = p.in_c;
+        cv.WW = p.WW;
+        if (l >= 2) {
+            cv.vtm_in = g.tmask[l - 1];
+            cv.vmap_in = ca.vmap[l - 1];
+            cv.vov_in = at(vp.o_ov[l - 1]);
+        }
+        cv.vov_out = vp.has_ov[l] ? at(vp.o_ov[l]) : nullptr;
+        cv.vpm0 = g.pmask[0];
+        cv.vframes = frames;
+        cv.vframe_u8 = fdt == RN_U8;
+        cv.vframe_shared = frame_count == 1 ? 1 : 0;
+        cv.lut = net->at<float>(p.o_lut);
+        if (l == 2 && p.fuse_first) {
+            cv.fuse_first = 1;
+            cv.in = net->at<float>(p.o_xin);
+            cv.in_stride = p.act_stride[0];
+            cv.w1 = net->at<float>(p.o_w[0]);
+            cv.b1 = net->at<float>(p.o_b[0]);
+        }
+        if (l == p.L) {
+            cv.n_out = p.N;
+            cv.hw = net->at<float>(p.o_hw);
+            cv.vhpart = static_cast<float *>(at(vp.o_hp));
+            last = cv;
+            if (bf) cv.n_out = 0;
+        }
+        if (l == 1)
+            e = timed(net, RN_PHASE_CONV1, s, [&] {
+                return bf ? launch_conv_first_bf16(cv, net->cus, s, true) : launch_conv_first(cv, p.dt, net->cus, s, true);
+            });
+        else
+            e = timed(net, RN_PHASE_CONVN, s, [&] {
+                return bf ? launch_conv_mfma_bf16(cv, net->cus, s, true) : launch_conv_mfma(cv, p.dt, net->cus, s, true);
+            });
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv kernels: ") + hipGetErrorString(e));
+    }
+    if (bf) {
+        last.vov_in = at(vp.o_ov[p.L]);
+        e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_part_bf16(last, net->cus, s, true); });
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head partials: ") + hipGetErrorString(e));
+    }
+    TileHeadArgs ta{};
+    ta.n = n;
+    ta.n_out = p.N;
+    ta.ntiles = p.ntiles;
+    ta.hpart = net->at<float>(p.o_hp);
+    ta.bias = net->at<float>(p.o_bd);
+    ta.logits = logits;
+    ta.var = 1;
+    ta.vbase = base;
+    ta.L = p.L;
+    ta.TMW = p.TMW;
+    ta.vmax = vp.vmax;
+    ta.vtm = g.tmask[p.L];
+    ta.vmap = ca.vmap[p.L];
+    ta.vhpart = static_cast<float *>(at(vp.o_hp));
+    ta.ntile = ma.ntile;
+    ta.primed = net->at<int32_t>(p.o_primed);
+    e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_head(ta, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head: ") + hipGetErrorString(e));
+    net->last_stream = s;
+    net->last_n = n;
+    net->has_step = true;
+    net->last_was_full = false;
+    net->last_was_var = true;
+    net->var_scratch = sc;
+    net->var_plan = vp;
     net->err.clear();
     return RN_OK;
 }
@@ -442,6 +652,7 @@ rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     net->last_n = n;
     net->has_step = true;
     net->last_was_full = true;
+    net->last_was_var = false;
     net->err.clear();
     return RN_OK;
 }
@@ -578,6 +789,18 @@ rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *ids, const vo
     return run_full(net, n, ids, frames, fdt, logits, stream);
 }
 
+size_t reuse_net_variant_scratch_bytes(const reuse_net *net, int32_t n, int32_t max_tiles) {
+    if (!net || n < 1 || n > 65535 || variants_unsupported(net->p)) return 0;
+    return plan_variants(net->p, n, max_tiles).total;
+}
+
+rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, const void *frames, rn_dtype fdt,
+                             int32_t frame_count, const int32_t *boxes, const int32_t *box_off, int32_t max_tiles,
+                             void *scratch, size_t scratch_bytes, float *logits, void *stream) {
+    return run_variants(net, base_stream, n, frames, fdt, frame_count, boxes, box_off, max_tiles, scratch,
+                        scratch_bytes, logits, stream);
+}
+
 rn_status reuse_net_reset(reuse_net *net, int32_t sid) {
     if (!net) return RN_EINVAL;
     if (sid < -1 || sid >= net->p.S) return net->fail(RN_EINVAL, "stream_id out of range");
@@ -598,21 +821,64 @@ static rn_status copy_out(reuse_net *net, void *dst, const void *src, size_t byt
     return RN_OK;
 }
 
+// Where the masks, counts and lists of the last call live: the net's own
+// buffers (index = slot), or the scratch of the last variants call (index =
+// variant).
+struct MaskView {
+    const uint64_t *pm[RN_MAX_CONV + 1], *tm[RN_MAX_CONV + 1];
+    const int32_t *nchg, *ntile, *cnt;
+    const uint32_t *wl[RN_MAX_CONV + 1];
+    int limit;                    // valid stream / variant indices
+};
+
+static MaskView mask_view(reuse_net *net) {
+    const Plan &p = net->p;
+    MaskView v{};
+    if (net->last_was_var) {
+        const VarPlan &vp = net->var_plan;
+        char *sc = net->var_scratch;
+        for (int l = 0; l <= p.L; ++l) {
+            v.pm[l] = reinterpret_cast<const uint64_t *>(sc + vp.o_pm[l]);
+            v.tm[l] = reinterpret_cast<const uint64_t *>(sc + vp.o_tm[l]);
+            v.wl[l] = l ? reinterpret_cast<const uint32_t *>(sc + vp.o_wl[l]) : nullptr;
+        }
+        v.nchg = reinterpret_cast<const int32_t *>(sc + vp.o_nchg);
+        v.ntile = reinterpret_cast<const int32_t *>(sc + vp.o_ntile);
+        v.cnt = reinterpret_cast<const int32_t *>(sc + vp.o_cnt);
+        v.limit = vp.n;
+        return v;
+    }
+    for (int l = 0; l <= p.L; ++l) {
+        v.pm[l] = net->at<uint64_t>(p.o_pm[l]);
+        v.tm[l] = net->at<uint64_t>(p.o_tm[l]);
+        v.wl[l] = l ? net->at<uint32_t>(p.o_wl[l]) : nullptr;
+    }
+    v.nchg = net->at<int32_t>(p.o_nchg);
+    v.ntile = net->at<int32_t>(p.o_ntile);
+    v.cnt = net->at<int32_t>(p.o_cnt);
+    v.limit = p.S;
+    return v;
+}
+
 rn_status reuse_net_get_pixel_mask(reuse_net *net, int32_t layer, int32_t sid, uint64_t *out, size_t words) {
     if (!net) return RN_EINVAL;
     const Plan &p = net->p;
-    if (layer < 0 || layer > p.L || sid < 0 || sid >= p.S || !out) return net->fail(RN_EINVAL, "bad layer, stream or buffer");
+    const MaskView v = mask_view(net);
+    if (layer < 0 || layer > p.L || sid < 0 || sid >= v.limit || !out)
+        return net->fail(RN_EINVAL, "bad layer, stream or buffer");
     const size_t need = (size_t)p.H * p.WW;
     if (words < need) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(need) + " words");
-    return copy_out(net, out, net->at<uint64_t>(p.o_pm[layer]) + (size_t)sid * need, need * 8);
+    return copy_out(net, out, v.pm[layer] + (size_t)sid * need, need * 8);
 }
 
 rn_status reuse_net_get_tile_mask(reuse_net *net, int32_t layer, int32_t sid, uint64_t *out, size_t words) {
     if (!net) return RN_EINVAL;
     const Plan &p = net->p;
-    if (layer < 0 || layer > p.L || sid < 0 || sid >= p.S || !out) return net->fail(RN_EINVAL, "bad layer, stream or buffer");
+    const MaskView v = mask_view(net);
+    if (layer < 0 || layer > p.L || sid < 0 || sid >= v.limit || !out)
+        return net->fail(RN_EINVAL, "bad layer, stream or buffer");
     if (words < (size_t)p.TMW) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(p.TMW) + " words");
-    return copy_out(net, out, net->at<uint64_t>(p.o_tm[layer]) + (size_t)sid * p.TMW, (size_t)p.TMW * 8);
+    return copy_out(net, out, v.tm[layer] + (size_t)sid * p.TMW, (size_t)p.TMW * 8);
 }
 
 rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, size_t cap, int32_t *count) {
@@ -620,14 +886,15 @@ rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, s
     const Plan &p = net->p;
     if (layer < 1 || layer > p.L || !count) return net->fail(RN_EINVAL, "bad layer or count pointer");
     if (net->last_was_full) return net->fail(RN_ESTATE, "the last call was reuse_net_full: no work list");
+    const MaskView v = mask_view(net);
     int32_t c = 0;
-    rn_status st = copy_out(net, &c, net->at<int32_t>(p.o_cnt) + layer, 4);
+    rn_status st = copy_out(net, &c, v.cnt + layer, 4);
     if (st != RN_OK) return st;
     *count = c;
     if ((size_t)c > cap) return net->fail(RN_ENOSPACE, "work list has " + std::to_string(c) + " entries");
     if (c == 0) return RN_OK;
     if (!out) return net->fail(RN_EINVAL, "out is NULL");
-    return copy_out(net, out, net->at<uint32_t>(p.o_wl[layer]), (size_t)c * 4);
+    return copy_out(net, out, v.wl[layer], (size_t)c * 4);
 }
 
 rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, float *host_out) {
@@ -702,9 +969,10 @@ rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out) {
     if (!net->has_step) return RN_OK;
     const Plan &p = net->p;
     const int n = net->last_n;
+    const MaskView v = mask_view(net);
     std::vector<int32_t> nchg(n), ntile((size_t)n * (p.L + 1));
-    rn_status st = copy_out(net, nchg.data(), net->at<int32_t>(p.o_nchg), (size_t)n * 4);
-    if (st == RN_OK) st = copy_out(net, ntile.data(), net->at<int32_t>(p.o_ntile), ntile.size() * 4);
+    rn_status st = copy_out(net, nchg.data(), v.nchg, (size_t)n * 4);
+    if (st == RN_OK) st = copy_out(net, ntile.data(), v.ntile, ntile.size() * 4);
     if (st != RN_OK) return st;
     out->streams = n;
     for (int i = 0; i < n; ++i) {

@@ -47,6 +47,9 @@ struct MaskArgs {
     int32_t *primed;              // [S]
     int32_t *nchg;                // [n] changed pixels
     int32_t *ntile;               // [n][L+1] dirty tiles per layer
+    // Variant mode: item i is a variant of a base slot whose change set is its
+    // boxes; masks are written at index i and no cache or slot state changes.
+    int variant;
 };
 
 struct CompactArgs {
@@ -55,8 +58,14 @@ struct CompactArgs {
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
     uint32_t *wl[RN_MAX_CONV + 1];  // entries i << 16 | ty << 8 | tx (batch index i)
-    uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels
+    uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels (NULL: none)
     int32_t *cnt;                 // [L+1]
+    size_t cap;                   // entries each list can hold
+    // Variant mode (ids == NULL: item i's masks are at index i): vmap[l][i][t]
+    // receives the list index of tile t of variant i, and a variant with more
+    // than vmax dirty tiles in some layer is left out of every list.
+    int32_t *vmap[RN_MAX_CONV + 1];
+    int vmax;
 };
 
 struct ConvArgs {
@@ -85,6 +94,24 @@ struct ConvArgs {
     int fuse_first;
     const float *w1;              // layer-1 weights, [k][c1] (first-layer packing, one input channel)
     const float *b1;              // [c1]
+    // Variant mode (kernels instantiated with VAR): the work items are
+    // i << 16 | ty << 8 | tx for variant i of base slot vbase, and item t of
+    // the list writes its outputs to row t of this layer's overlay instead of
+    // a cache.  A variant's layer-(l-1) tile is its own overlay row where its
+    // tile mask has the tile, else the base slot's cached tile.
+    int vbase;
+    int vcin;                     // input channels of the frames (layer-1 reads)
+    int WW;                       // 64-bit words per pixel-mask row
+    const uint64_t *vtm_in;       // layer l-1 tile masks [n][TMW]
+    const int32_t *vmap_in;       // layer l-1 list index of (variant, tile) [n][TH*TW]
+    const void *vov_in;           // layer l-1 overlay [list index][16][cin]
+    void *vov_out;                // this layer's overlay [list index][16][cout] (NULL: not stored)
+    float *vhpart;                // head partials [list index][n_out]
+    const uint64_t *vpm0;         // layer-0 change masks [n][H][WW]: input pixels taken from the frame
+    const void *vframes;          // [1 or n][vcin][H][W]
+    int vframe_u8;
+    int vframe_shared;            // 1: every variant reads frame 0
+    const float *lut;             // [256] level -> float32
 };
 
 // Dense path: copy the frames into the input cache and mark the slots primed.
@@ -110,6 +137,16 @@ struct TileHeadArgs {
     const float *hpart;
     const float *bias;
     float *logits;
+    // Variant mode (var = 1): tile t of variant i takes its partials from
+    // vhpart[vmap[i][t]] where the variant recomputed it (vtm), else from the
+    // base slot; variants left out of the lists (more than vmax dirty tiles in
+    // a layer) and variants of an unprimed base get NaN logits.
+    int var, vbase, L, TMW, vmax;
+    const uint64_t *vtm;          // [n][TMW] last layer
+    const int32_t *vmap;          // [n][ntiles] last layer
+    const float *vhpart;          // [list index][n_out]
+    const int32_t *ntile;         // [n][L+1]
+    const int32_t *primed;        // [S]
 };
 
 struct HeadArgs {
@@ -132,15 +169,17 @@ hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s);
 size_t tile_head_w_elems(int ntiles, int cout, int n_out);
 void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s);
-hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
-hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s);
+// Conv launchers: list mode (a.wl set), dense mode (a.wl NULL), or variant
+// mode (var = true, a.wl set).
+hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s, bool var = false);
+hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s, bool var = false);
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt);
 bool conv_first_supported(int cin, int cout, rn_dtype dt);
 bool conv_fused_first_supported(int c1, int c2, rn_dtype dt);
 bool conv_mfma_bf16_supported(int cin, int cout);
 bool conv_first_bf16_supported(int cin, int cout);
-hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s);
-hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s);
+hipError_t launch_conv_mfma_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var = false);
+hipError_t launch_conv_first_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var = false);
 void pack_conv_mfma_bf16(const float *oihw, int cin, int cout, void *dst);
 float round_bf16_host(float v);
 uint16_t bf16_bits_host(float v);
@@ -149,7 +188,7 @@ uint16_t bf16_bits_host(float v);
 bool tile_part_bf16_supported(int C);
 size_t tile_part_bf16_elems(int ntiles, int C, int n_out);
 void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, uint16_t *dst);
-hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s);
+hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s, bool var = false);
 hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
 int head_streams_per_block(int n_out);
 

@@ -117,8 +117,10 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     float *lut = reinterpret_cast<float *>(smem + 2 * HWW);
 
     const int i = blockIdx.x;
-    const int slot = a.ids[i];
-    const int primed = a.force_all ? 0 : a.primed[slot];
+    // Variant mode: the masks of variant i go to index i; its change set is
+    // its boxes and nothing is written to any slot.
+    const int slot = a.variant ? i : a.ids[i];
+    const int primed = a.variant ? 1 : a.force_all ? 0 : a.primed[slot];
     const size_t HW = (size_t)g.H * g.W;
     const int C = g.cin;
 
@@ -128,9 +130,10 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     __syncthreads();
 
     // Cache planes: the previous newest frame, and where the new frame goes.
-    float *prev, *next;
+    float *prev = nullptr, *next = nullptr;
     int head = 0, nhead = 0;
-    if (g.stack == 1) {
+    if (a.variant) {
+    } else if (g.stack == 1) {
         prev = next = a.xin + (size_t)slot * C * HW;
     } else {
         head = a.ring_head[slot];
@@ -152,8 +155,9 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
             for (int e = threadIdx.x; e < bh * bw; e += blockDim.x) {
                 const int y = y0 + e / bw, x = x0 + e % bw;
                 const size_t px = (size_t)y * g.W + x;
-                for (int c = 0; c < C; ++c)
-                    next[c * HW + px] = load1<U8>(a.frames, fbase + c * HW + px, lut);
+                if (!a.variant)
+                    for (int c = 0; c < C; ++c)
+                        next[c * HW + px] = load1<U8>(a.frames, fbase + c * HW + px, lut);
                 atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
                          1ull << (x & 63));
             }
@@ -249,8 +253,10 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     if (threadIdx.x == 0) {
         a.nchg[i] = nchg;
         for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_tiles[l];
-        a.primed[slot] = 1;
-        if (g.stack != 1) a.ring_head[slot] = nhead;
+        if (!a.variant) {
+            a.primed[slot] = 1;
+            if (g.stack != 1) a.ring_head[slot] = nhead;
+        }
     }
 }
 
@@ -300,12 +306,23 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 // Every entry has exactly one writer; no global atomics.
 constexpr int kChunksPerPass = 16;          // 1024 streams per pass
 
+// Index of item i's masks (its slot; variant mode: i), or -1 when the item is
+// absent or is a variant left out of the lists (more than vmax dirty tiles in
+// some layer 1..L).
+__device__ inline int mask_index(const CompactArgs &a, int i) {
+    if (i >= a.n) return -1;
+    if (a.ids) return a.ids[i];
+    if (a.vmax > 0)
+        for (int l = 1; l <= a.L; ++l)
+            if (a.ntile[(size_t)i * (a.L + 1) + l] > a.vmax) return -1;
+    return i;
+}
+
 // Stage the slots and this word's tile bits of streams [64 c0, 64 (c0 + nc)) in LDS.
 __device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, int nc, int32_t *s_slot,
                                   uint64_t *s_word) {
     for (int j = threadIdx.x; j < nc * 64; j += blockDim.x) {
-        const int i = 64 * c0 + j;
-        const int slot = i < a.n ? a.ids[i] : -1;
+        const int slot = mask_index(a, 64 * c0 + j);
         s_slot[j] = slot;
         s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMW + wd] : 0ull;
     }
@@ -328,7 +345,9 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // per stream; the words of a stream are independent loads).
     int pre = 0;
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * a.TMW;
+        const int mi = mask_index(a, i);
+        if (mi < 0) continue;
+        const uint64_t *tm = a.tmask[l] + (size_t)mi * a.TMW;
         for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
     }
     pre = block_sum(pre, red);
@@ -360,11 +379,11 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             s_run[j] = r;
             r += s_cnt[j];
         }
-        if (wd == a.TMW - 1) a.cnt[l] = r;       // the last word closes the list
+        if (wd == a.TMW - 1) a.cnt[l] = (int)min((size_t)r, a.cap);   // the last word closes the list
     }
     __syncthreads();
 
-    const int cap = a.n * a.ntiles;
+    const size_t cap = a.cap;
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
         if (nch > kChunksPerPass) {
@@ -404,9 +423,10 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
                 const int k = __ffsll((long long)b) - 1;  // next stream of this position
                 b &= b - 1;
                 const int i = 64 * (c0 + cc) + k;
-                if (idx < cap) {
+                if ((size_t)idx < cap) {
                     a.wl[l][idx] = ((uint32_t)i << 16) | pos;
-                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
+                    if (a.wls[l]) a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
+                    if (a.vmap[l]) a.vmap[l][(size_t)i * a.ntiles + t] = idx;
                 }
                 ++idx;
             }

@@ -446,3 +446,40 @@ def test_reset_makes_next_step_all_dirty(orc):
     got = rs.step(x)                                      # unchanged input, but reset
     ref = orc.forward(net, cw, cb, dw, db, x[None])[0][0]
     assert np.array_equal(got, ref)
+
+
+def test_variant_input_pins(orc):
+    # Closed forms: no boxes -> the base; a box over the whole frame (or past
+    # it, clipped) -> the frame; and brute force over every pixel with the
+    # half-open box rule written out, for overlapping, clipped and empty boxes.
+    rng = np.random.default_rng(31)
+    base = rng.random((2, 7, 9), dtype=np.float32)
+    frame = -rng.random((2, 7, 9), dtype=np.float32)
+    assert np.array_equal(orc.variant_input(base, frame, np.zeros((0, 4), np.int32)), base)
+    assert np.array_equal(orc.variant_input(base, frame, [(-3, -1, 20, 30)]), frame)
+    boxes = [(1, 2, 4, 5), (3, 4, 6, 9), (-2, 7, 2, 12), (5, 5, 5, 8), (6, 0, 9, 1)]
+    got = orc.variant_input(base, frame, boxes)
+    for y in range(7):
+        for x in range(9):
+            inside = any(y0 <= y < y1 and x0 <= x < x1 for (y0, x0, y1, x1) in boxes)
+            want = frame[:, y, x] if inside else base[:, y, x]
+            assert np.array_equal(got[:, y, x], want), (y, x)
+
+
+def test_variant_equals_reuse_step_from_base(orc):
+    # A variant is what one known-change step from the base state computes:
+    # reuse on the boxes' dirty tiles from the base caches gives the full
+    # recompute of the variant input bit for bit, and the base is untouched
+    # when each variant starts from a fresh copy of the base state.
+    net = _small_net(orc, h=15, w=13)
+    cw, cb, dw, db = _rand_weights(net, 32)
+    rng = np.random.default_rng(33)
+    base = rng.random((1, 15, 13), dtype=np.float32)
+    for boxes in ([(2, 3, 6, 9)], [(0, 0, 1, 1), (10, 9, 20, 20)], [(4, 4, 4, 9)]):
+        frame = np.zeros_like(base)
+        x = orc.variant_input(base, frame, boxes)
+        rs = orc.ReuseStream(net, cw, cb, dw, db)
+        rs.step(base)
+        got = rs.step(x, d0=orc.box_mask(15, 13, boxes))
+        ref = orc.forward(net, cw, cb, dw, db, x[None])[0][0]
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), boxes
