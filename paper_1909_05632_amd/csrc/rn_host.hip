@@ -186,7 +186,7 @@ struct VarPlan {
     int n = 0, vmax = 0;                   // vmax 0: no per-variant limit
     size_t cap = 0;                        // list capacity per layer
     size_t o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile, o_wl[RN_MAX_CONV + 1],
-        o_map[RN_MAX_CONV + 1], o_ov[RN_MAX_CONV + 1], o_hp, o_cnt;
+        o_map[RN_MAX_CONV + 1], o_ov[RN_MAX_CONV + 1], o_bits[RN_MAX_CONV + 1], o_pcnt, o_hp, o_cnt;
     bool has_ov[RN_MAX_CONV + 1] = {false};
     size_t total = 0;
 };
@@ -212,12 +212,15 @@ VarPlan plan_variants(const Plan &p, int n, int max_tiles) {
     }
     v.o_nchg = take((size_t)n * 4);
     v.o_ntile = take((size_t)n * (p.L + 1) * 4);
+    const size_t nch = ((size_t)n + 63) / 64;
     for (int l = 1; l <= p.L; ++l) {
         v.o_wl[l] = take(v.cap * 4);
         v.o_map[l] = take((size_t)n * p.ntiles * 4);
+        v.o_bits[l] = take((size_t)p.ntiles * nch * 8);
         v.has_ov[l] = l < p.L ? !(l == 1 && p.fuse_first) : p.dt == RN_BF16;
         v.o_ov[l] = take(v.has_ov[l] ? v.cap * kTilePx * p.C[l] * p.esz : 0);
     }
+    v.o_pcnt = take((size_t)p.L * p.ntiles * 4);
     v.o_hp = take(v.cap * p.N * 4);
     v.o_cnt = take((RN_MAX_CONV + 1) * 4);
     v.total = off;
@@ -480,55 +483,54 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
     if (!scratch) return net->fail(RN_EINVAL, "scratch is NULL");
     if (reinterpret_cast<uintptr_t>(scratch) % kAlign) return net->fail(RN_EINVAL, "scratch must be 256-byte aligned");
     const VarPlan vp = plan_variants(p, n, max_tiles);
+    if (vp.cap > (size_t)INT32_MAX) return net->fail(RN_EINVAL, "n x max_tiles exceeds 2^31 work-list entries");
     if (scratch_bytes < vp.total)
         return net->fail(RN_ENOSPACE, "scratch too small: need " + std::to_string(vp.total) + " bytes");
     hipStream_t s = static_cast<hipStream_t>(stream);
     char *sc = static_cast<char *>(scratch);
     auto at = [&](size_t off) { return static_cast<void *>(sc + off); };
 
-    MaskGeom g = make_geom(net);
+    VarMaskArgs va{};
+    va.n = n;
+    va.L = p.L;
+    va.H = p.H;
+    va.W = p.W;
+    va.WW = p.WW;
+    va.TH = p.TH;
+    va.TW = p.TW;
+    va.TMW = p.TMW;
+    va.ntiles = p.ntiles;
+    va.nch = (n + 63) / 64;
+    va.vmax = vp.vmax;
+    for (int l = 1; l <= p.L; ++l) va.R[l] = va.R[l - 1] + p.radius[l - 1];
+    va.boxes = boxes;
+    va.box_off = box_off;
     for (int l = 0; l <= p.L; ++l) {
-        g.pmask[l] = static_cast<uint64_t *>(at(vp.o_pm[l]));
-        g.tmask[l] = static_cast<uint64_t *>(at(vp.o_tm[l]));
+        va.pmask[l] = static_cast<uint64_t *>(at(vp.o_pm[l]));
+        va.tmask[l] = static_cast<uint64_t *>(at(vp.o_tm[l]));
+        if (l) {
+            va.bits[l] = static_cast<uint64_t *>(at(vp.o_bits[l]));
+            va.wl[l] = static_cast<uint32_t *>(at(vp.o_wl[l]));
+            va.vmap[l] = static_cast<int32_t *>(at(vp.o_map[l]));
+        }
     }
-    MaskArgs ma{};
-    ma.n = n;
-    ma.frames = frames;
-    ma.frame_u8 = fdt == RN_U8;
-    ma.boxes = boxes;
-    ma.box_off = box_off;
-    ma.lut = net->at<float>(p.o_lut);
-    ma.nchg = static_cast<int32_t *>(at(vp.o_nchg));
-    ma.ntile = static_cast<int32_t *>(at(vp.o_ntile));
-    ma.variant = 1;
-    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, s); });
+    va.nchg = static_cast<int32_t *>(at(vp.o_nchg));
+    va.ntile = static_cast<int32_t *>(at(vp.o_ntile));
+    va.cnt = static_cast<int32_t *>(at(vp.o_cnt));
+    va.pos_cnt = static_cast<int32_t *>(at(vp.o_pcnt));
+    va.cap = vp.cap;
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_var_masks(va, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("mask kernel: ") + hipGetErrorString(e));
-
-    CompactArgs ca{};
-    ca.n = n;
-    ca.L = p.L;
-    ca.TW = p.TW;
-    ca.TMW = p.TMW;
-    ca.ntiles = p.ntiles;
-    ca.ntile = ma.ntile;
-    for (int l = 0; l <= p.L; ++l) {
-        ca.tmask[l] = g.tmask[l];
-        ca.wl[l] = l ? static_cast<uint32_t *>(at(vp.o_wl[l])) : nullptr;
-        ca.vmap[l] = l ? static_cast<int32_t *>(at(vp.o_map[l])) : nullptr;
-    }
-    ca.cnt = static_cast<int32_t *>(at(vp.o_cnt));
-    ca.cap = vp.cap;
-    ca.vmax = vp.vmax;
-    e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
-    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
+    e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_var_lists(va, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("work-list kernel: ") + hipGetErrorString(e));
 
     const bool bf = p.dt == RN_BF16;
     ConvArgs last{};
     for (int l = 1; l <= p.L; ++l) {
         if (l == 1 && p.fuse_first) continue;
         ConvArgs cv{};
-        cv.wl = ca.wl[l];
-        cv.cnt = ca.cnt + l;
+        cv.wl = va.wl[l];
+        cv.cnt = va.cnt + l;
         cv.in = l == 1 ? static_cast<const void *>(net->at<float>(p.o_xin)) : net->at<void>(p.o_act[l - 1]);
         cv.w = net->at<void>(p.o_w[l - 1]);
         cv.bias = net->at<float>(p.o_b[l - 1]);
@@ -546,12 +548,12 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
         cv.vcin = p.in_c;
         cv.WW = p.WW;
         if (l >= 2) {
-            cv.vtm_in = g.tmask[l - 1];
-            cv.vmap_in = ca.vmap[l - 1];
+            cv.vtm_in = va.tmask[l - 1];
+            cv.vmap_in = va.vmap[l - 1];
             cv.vov_in = at(vp.o_ov[l - 1]);
         }
         cv.vov_out = vp.has_ov[l] ? at(vp.o_ov[l]) : nullptr;
-        cv.vpm0 = g.pmask[0];
+        cv.vpm0 = va.pmask[0];
         cv.vframes = frames;
         cv.vframe_u8 = fdt == RN_U8;
         cv.vframe_shared = frame_count == 1 ? 1 : 0;
@@ -597,10 +599,10 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
     ta.L = p.L;
     ta.TMW = p.TMW;
     ta.vmax = vp.vmax;
-    ta.vtm = g.tmask[p.L];
-    ta.vmap = ca.vmap[p.L];
+    ta.vtm = va.tmask[p.L];
+    ta.vmap = va.vmap[p.L];
     ta.vhpart = static_cast<float *>(at(vp.o_hp));
-    ta.ntile = ma.ntile;
+    ta.ntile = va.ntile;
     ta.primed = net->at<int32_t>(p.o_primed);
     e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_head(ta, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head: ") + hipGetErrorString(e));
@@ -791,7 +793,8 @@ rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *ids, const vo
 
 size_t reuse_net_variant_scratch_bytes(const reuse_net *net, int32_t n, int32_t max_tiles) {
     if (!net || n < 1 || n > 65535 || variants_unsupported(net->p)) return 0;
-    return plan_variants(net->p, n, max_tiles).total;
+    const VarPlan vp = plan_variants(net->p, n, max_tiles);
+    return vp.cap > (size_t)INT32_MAX ? 0 : vp.total;
 }
 
 rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, const void *frames, rn_dtype fdt,

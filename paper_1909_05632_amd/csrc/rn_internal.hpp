@@ -47,9 +47,6 @@ struct MaskArgs {
     int32_t *primed;              // [S]
     int32_t *nchg;                // [n] changed pixels
     int32_t *ntile;               // [n][L+1] dirty tiles per layer
-    // Variant mode: item i is a variant of a base slot whose change set is its
-    // boxes; masks are written at index i and no cache or slot state changes.
-    int variant;
 };
 
 struct CompactArgs {
@@ -58,14 +55,30 @@ struct CompactArgs {
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
     uint32_t *wl[RN_MAX_CONV + 1];  // entries i << 16 | ty << 8 | tx (batch index i)
-    uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels (NULL: none)
+    uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels
     int32_t *cnt;                 // [L+1]
     size_t cap;                   // entries each list can hold
-    // Variant mode (ids == NULL: item i's masks are at index i): vmap[l][i][t]
-    // receives the list index of tile t of variant i, and a variant with more
-    // than vmax dirty tiles in some layer is left out of every list.
-    int32_t *vmap[RN_MAX_CONV + 1];
-    int vmax;
+};
+
+// Masks and work lists of n variants straight from their boxes (variant i's
+// change set is the union of boxes [box_off[i], box_off[i+1])).  Masks are
+// indexed by variant.  A variant with more than vmax (> 0) dirty tiles in a
+// layer 1..L is left out of every list; vmap[l][i][t] receives the list index
+// of tile t of variant i (written for listed tiles only).
+struct VarMaskArgs {
+    int n, L, H, W, WW, TH, TW, TMW, ntiles, nch, vmax;
+    int R[RN_MAX_CONV + 1];       // growth radius of layer l's change set (R[0] = 0)
+    const int32_t *boxes, *box_off;
+    uint64_t *pmask[RN_MAX_CONV + 1];   // [n][H][WW]
+    uint64_t *tmask[RN_MAX_CONV + 1];   // [n][TMW]
+    int32_t *nchg;                // [n]
+    int32_t *ntile;               // [n][L+1]
+    uint64_t *bits[RN_MAX_CONV + 1];    // layers 1..L: [ntiles][nch] listed variants per position
+    int32_t *pos_cnt;             // [L][ntiles] listed entries per position
+    uint32_t *wl[RN_MAX_CONV + 1];
+    int32_t *vmap[RN_MAX_CONV + 1];     // [n][ntiles]
+    int32_t *cnt;
+    size_t cap;
 };
 
 struct ConvArgs {
@@ -169,6 +182,8 @@ hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s);
 size_t tile_head_w_elems(int ntiles, int cout, int n_out);
 void pack_tile_head(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s);
+hipError_t launch_var_masks(const VarMaskArgs &a, hipStream_t s);
+hipError_t launch_var_lists(const VarMaskArgs &a, hipStream_t s);
 // Conv launchers: list mode (a.wl set), dense mode (a.wl NULL), or variant
 // mode (var = true, a.wl set).
 hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s, bool var = false);

@@ -117,10 +117,8 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     float *lut = reinterpret_cast<float *>(smem + 2 * HWW);
 
     const int i = blockIdx.x;
-    // Variant mode: the masks of variant i go to index i; its change set is
-    // its boxes and nothing is written to any slot.
-    const int slot = a.variant ? i : a.ids[i];
-    const int primed = a.variant ? 1 : a.force_all ? 0 : a.primed[slot];
+    const int slot = a.ids[i];
+    const int primed = a.force_all ? 0 : a.primed[slot];
     const size_t HW = (size_t)g.H * g.W;
     const int C = g.cin;
 
@@ -130,10 +128,9 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     __syncthreads();
 
     // Cache planes: the previous newest frame, and where the new frame goes.
-    float *prev = nullptr, *next = nullptr;
+    float *prev, *next;
     int head = 0, nhead = 0;
-    if (a.variant) {
-    } else if (g.stack == 1) {
+    if (g.stack == 1) {
         prev = next = a.xin + (size_t)slot * C * HW;
     } else {
         head = a.ring_head[slot];
@@ -155,9 +152,8 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
             for (int e = threadIdx.x; e < bh * bw; e += blockDim.x) {
                 const int y = y0 + e / bw, x = x0 + e % bw;
                 const size_t px = (size_t)y * g.W + x;
-                if (!a.variant)
-                    for (int c = 0; c < C; ++c)
-                        next[c * HW + px] = load1<U8>(a.frames, fbase + c * HW + px, lut);
+                for (int c = 0; c < C; ++c)
+                    next[c * HW + px] = load1<U8>(a.frames, fbase + c * HW + px, lut);
                 atomicOr(reinterpret_cast<unsigned long long *>(&A[y * g.WW + (x >> 6)]),
                          1ull << (x & 63));
             }
@@ -253,10 +249,8 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     if (threadIdx.x == 0) {
         a.nchg[i] = nchg;
         for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_tiles[l];
-        if (!a.variant) {
-            a.primed[slot] = 1;
-            if (g.stack != 1) a.ring_head[slot] = nhead;
-        }
+        a.primed[slot] = 1;
+        if (g.stack != 1) a.ring_head[slot] = nhead;
     }
 }
 
@@ -306,23 +300,12 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 // Every entry has exactly one writer; no global atomics.
 constexpr int kChunksPerPass = 16;          // 1024 streams per pass
 
-// Index of item i's masks (its slot; variant mode: i), or -1 when the item is
-// absent or is a variant left out of the lists (more than vmax dirty tiles in
-// some layer 1..L).
-__device__ inline int mask_index(const CompactArgs &a, int i) {
-    if (i >= a.n) return -1;
-    if (a.ids) return a.ids[i];
-    if (a.vmax > 0)
-        for (int l = 1; l <= a.L; ++l)
-            if (a.ntile[(size_t)i * (a.L + 1) + l] > a.vmax) return -1;
-    return i;
-}
-
 // Stage the slots and this word's tile bits of streams [64 c0, 64 (c0 + nc)) in LDS.
 __device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, int nc, int32_t *s_slot,
                                   uint64_t *s_word) {
     for (int j = threadIdx.x; j < nc * 64; j += blockDim.x) {
-        const int slot = mask_index(a, 64 * c0 + j);
+        const int i = 64 * c0 + j;
+        const int slot = i < a.n ? a.ids[i] : -1;
         s_slot[j] = slot;
         s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMW + wd] : 0ull;
     }
@@ -345,9 +328,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // per stream; the words of a stream are independent loads).
     int pre = 0;
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const int mi = mask_index(a, i);
-        if (mi < 0) continue;
-        const uint64_t *tm = a.tmask[l] + (size_t)mi * a.TMW;
+        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * a.TMW;
         for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
     }
     pre = block_sum(pre, red);
@@ -425,8 +406,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
                 const int i = 64 * (c0 + cc) + k;
                 if ((size_t)idx < cap) {
                     a.wl[l][idx] = ((uint32_t)i << 16) | pos;
-                    if (a.wls[l]) a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
-                    if (a.vmap[l]) a.vmap[l][(size_t)i * a.ntiles + t] = idx;
+                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
                 }
                 ++idx;
             }
@@ -434,7 +414,195 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ variants
+//
+// The change set of a variant is a union of boxes, and growing a union grows
+// each member: the layer-l set is every box clipped to the frame, widened by
+// R_l (the summed growth radii of layers 1..l) on each side and clipped again
+// (Fig. 1's one-pixel growth per 3x3 layer, composed; exact for rectangles).
+// Every mask word is therefore a direct test against the boxes, with no
+// layer-to-layer dependence, and the tiles a box touches form a rectangle of
+// the tile grid.
+//
+// k_var_pix: one wave per (variant, layer); lanes own pixel rows and 64-tile
+// words; per-variant counts by wave reduction.
+// k_var_bits: one wave per (64-variant chunk, layer 1..L, tile word): the
+// chunk's words transposed by 64 ballots into one 64-variant bitmap per tile
+// position, bits[l][t][chunk], with variants over the per-variant limit
+// cleared, and each position's entry count summed (integer atomics: the sum
+// does not depend on their order).
+// k_var_lists: block (b, l) owns positions [b P, b P + P); its entries start
+// after those of every earlier position, and a block scan over its
+// (position, chunk) bitmaps places each entry: position-major, variants
+// ascending within a position, as for streams.
+
+constexpr int kVarThreads = 1024;
+
+// Bits of the index range [x0, x1) that fall in 64-bit word wx.
+__device__ inline uint64_t range_bits(int x0, int x1, int wx) {
+    const int lo = max(x0 - 64 * wx, 0), hi = min(x1 - 64 * wx, 64);
+    if (hi <= lo) return 0ull;
+    const uint64_t upto = hi == 64 ? ~0ull : ((1ull << hi) - 1ull);
+    return upto & ~((1ull << lo) - 1ull);
+}
+
+__device__ inline int wave_sum(int v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Box k grown by R and clipped, (y0, x0, y1, x1); empty (y1 <= y0 or x1 <= x0)
+// when the box is empty after clipping to the frame.
+__device__ inline int4 grown_box(const VarMaskArgs &a, int k, int R) {
+    const int32_t *b = a.boxes + 4 * (size_t)k;
+    const int y0 = max(b[0], 0), x0 = max(b[1], 0), y1 = min(b[2], a.H), x1 = min(b[3], a.W);
+    if (y1 <= y0 || x1 <= x0) return make_int4(0, 0, 0, 0);
+    return make_int4(max(y0 - R, 0), max(x0 - R, 0), min(y1 + R, a.H), min(x1 + R, a.W));
+}
+
+__global__ __launch_bounds__(256) void k_var_pix(VarMaskArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int task = blockIdx.x * 4 + (threadIdx.x >> 6);
+    // Block 0 also clears the per-position entry counts that k_var_bits adds to.
+    if (blockIdx.x == 0)
+        for (int j = threadIdx.x; j < a.L * a.ntiles; j += blockDim.x) a.pos_cnt[j] = 0;
+    if (task >= a.n * (a.L + 1)) return;
+    const int i = task / (a.L + 1), l = task - i * (a.L + 1);
+    const int R = a.R[l];
+    const int k0 = a.box_off[i], k1 = a.box_off[i + 1];
+    int px = 0, tl = 0;
+    for (int y = lane; y < a.H; y += 64) {
+        uint64_t *dst = a.pmask[l] + ((size_t)i * a.H + y) * a.WW;
+        for (int wx = 0; wx < a.WW; ++wx) {
+            uint64_t word = 0;
+            for (int k = k0; k < k1; ++k) {
+                const int4 g = grown_box(a, k, R);
+                if (y >= g.x && y < g.z) word |= range_bits(g.y, g.w, wx);
+            }
+            dst[wx] = word;
+            px += __popcll(word);
+        }
+    }
+    for (int wd = lane; wd < a.TMW; wd += 64) {
+        uint64_t word = 0;
+        const int t0 = 64 * wd, t1 = t0 + 64;
+        for (int k = k0; k < k1; ++k) {
+            const int4 g = grown_box(a, k, R);
+            if (g.z <= g.x) continue;
+            const int ty0 = g.x / kTile, ty1 = (g.z + kTile - 1) / kTile;
+            const int tx0 = g.y / kTile, tx1 = (g.w + kTile - 1) / kTile;
+            // tile rows whose index range [ty TW + tx0, ty TW + tx1) can meet [t0, t1)
+            const int r0 = max(ty0, (t0 - tx1) / a.TW), r1 = min(ty1, t1 / a.TW + 1);
+            for (int ty = r0; ty < r1; ++ty) word |= range_bits(ty * a.TW + tx0, ty * a.TW + tx1, wd);
+        }
+        a.tmask[l][(size_t)i * a.TMW + wd] = word;
+        tl += __popcll(word);
+    }
+    px = wave_sum(px);
+    tl = wave_sum(tl);
+    if (lane == 0) {
+        a.ntile[(size_t)i * (a.L + 1) + l] = tl;
+        if (l == 0) a.nchg[i] = px;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_var_bits(VarMaskArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int task = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (task >= a.nch * a.L * a.TMW) return;
+    const int wd = task % a.TMW, r = task / a.TMW;
+    const int l = 1 + r % a.L, c = r / a.L;
+    const int i = 64 * c + lane;
+    bool ok = i < a.n;
+    if (ok && a.vmax > 0)
+        for (int q = 1; q <= a.L; ++q) ok = ok && a.ntile[(size_t)i * (a.L + 1) + q] <= a.vmax;
+    const uint64_t w = ok ? a.tmask[l][(size_t)i * a.TMW + wd] : 0ull;
+    uint64_t mine = 0;
+    for (int j = 0; j < 64; ++j) {
+        const uint64_t b = __ballot((w >> j) & 1ull);
+        if (lane == j) mine = b;
+    }
+    const int t = 64 * wd + lane;
+    if (t < a.ntiles) {
+        a.bits[l][(size_t)t * a.nch + c] = mine;
+        if (mine) atomicAdd(&a.pos_cnt[(size_t)(l - 1) * a.ntiles + t], __popcll(mine));
+    }
+}
+
+// Exclusive block-wide prefix sum of v; *total receives the block's sum.
+__device__ inline int block_excl_scan(int v, int *s_w, int *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = (int)(blockDim.x >> 6);
+    int x = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    __syncthreads();                      // s_w of the previous call has been read
+    if (lane == 63) s_w[wave] = x;
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < nw; ++w) {
+        const int s = s_w[w];
+        off += w < wave ? s : 0;
+        tot += s;
+    }
+    *total = tot;
+    return off + x - v;
+}
+
+__global__ __launch_bounds__(kVarThreads) void k_var_lists(VarMaskArgs a) {
+    __shared__ int red[kVarThreads / 64];
+    __shared__ int s_w[kVarThreads / 64];
+    const int l = blockIdx.y + 1;
+    const int P = max(1, (int)blockDim.x / a.nch);
+    const int t0 = blockIdx.x * P, t1 = min(t0 + P, a.ntiles);
+    const uint64_t *B = a.bits[l];
+    int pre = 0;
+    for (int t = threadIdx.x; t < t0; t += blockDim.x) pre += a.pos_cnt[(size_t)(l - 1) * a.ntiles + t];
+    int run = block_sum(pre, red);
+    const size_t k0 = (size_t)t0 * a.nch, k1 = (size_t)t1 * a.nch;
+    for (size_t base = k0; base < k1; base += blockDim.x) {
+        const size_t k = base + threadIdx.x;
+        const uint64_t w = k < k1 ? B[k] : 0ull;
+        int total;
+        int idx = run + block_excl_scan(__popcll(w), s_w, &total);
+        if (w) {
+            const int t = (int)(k / a.nch), cc = (int)(k - (size_t)t * a.nch);
+            const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
+            uint64_t b = w;
+            while (b) {
+                const int j = __ffsll((long long)b) - 1;
+                b &= b - 1;
+                const int i = 64 * cc + j;
+                if ((size_t)idx < a.cap) {
+                    a.wl[l][idx] = ((uint32_t)i << 16) | pos;
+                    a.vmap[l][(size_t)i * a.ntiles + t] = idx;
+                }
+                ++idx;
+            }
+        }
+        run += total;
+    }
+    if (t1 == a.ntiles && threadIdx.x == 0) a.cnt[l] = (int)min((size_t)run, a.cap);
+}
+
 }  // namespace
+
+hipError_t launch_var_masks(const VarMaskArgs &a, hipStream_t s) {
+    const int waves = a.n * (a.L + 1);
+    hipLaunchKernelGGL(k_var_pix, dim3((waves + 3) / 4), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int tw = a.nch * a.L * a.TMW;
+    hipLaunchKernelGGL(k_var_bits, dim3((tw + 3) / 4), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_var_lists(const VarMaskArgs &a, hipStream_t s) {
+    const int P = std::max(1, kVarThreads / a.nch);
+    hipLaunchKernelGGL(k_var_lists, dim3((a.ntiles + P - 1) / P, a.L), dim3(kVarThreads), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s) {
     const size_t shm = (size_t)2 * g.H * g.WW * sizeof(uint64_t) + 256 * sizeof(float);
