@@ -97,6 +97,11 @@ class SpriteDriver:
     def dense_step(self, net, k, out):
         net.full(self.frames[self.seq[k]], out=out)
 
+    def mask_bytes(self):
+        # frame + cached input, read once per step
+        wl = self.wl
+        return 2 * self.S * wl.h * wl.w * 4 * wl.in_c
+
     def cpu_sample(self, oracle, weights, budget_s):
         from synth import frames as synth
         wl = self.wl
@@ -163,6 +168,12 @@ class OcclusionDriver:
         B = self.DENSE_BATCH
         for j in range(0, self.S, B):
             net.full(self.frames[j:j + B], out=out[j:j + B])
+
+    def mask_bytes(self):
+        # pixel and tile masks of every layer written per variant (no frame is read)
+        wl = self.wl
+        L, th, tw = len(wl.convs), -(-wl.h // 4), -(-wl.w // 4)
+        return self.S * (L + 1) * (wl.h * -(-wl.w // 64) + -(-th * tw // 64)) * 8
 
     def cpu_sample(self, oracle, weights, budget_s):
         from synth import frames as synth
@@ -314,7 +325,7 @@ def main():
     else:
         head_bytes = S * tiles * wl.n_out * 4 * K               # per-tile partials
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
-    mask_bytes = 2 * S * wl.h * wl.w * 4 * wl.in_c * K         # frame + cached input
+    mask_bytes = drv.mask_bytes() * K
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
     if prof["conv1"]["ms"] > 0:
         conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + 36 * chans[0] * 4)

@@ -77,7 +77,7 @@ WORKLOADS = {
         cid=3, streams=64, frames=64, h=105, w=80, convs=(40, 80), n_out=6,
         n_sprites=6, smin=4, smax=8, vmin=1, vmax=3,
         description="4096 occlusion variants (8x8 zero patch, 64x64 top-left grid) "
-                    "of one 105x80 base, as 64 streams x 64 steps of change boxes",
+                    "of one 105x80 base, evaluated together against the base's caches",
         extra={"patch": 8, "grid": 64}),
     "stack4-512x64": Workload(
         cid=4, streams=512, frames=64, h=105, w=80, convs=(40, 80), n_out=6,
