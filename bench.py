@@ -11,6 +11,8 @@ Workloads (synth.WORKLOADS):
   atari-ds2-256x64 (default)  256 streams x 64 frames, 105x80, 1->40->80, dense->6
   atari-ds4-1x16              1 stream x 16 frames, 53x40
   stack4-512x64               512 streams, the last 4 frames stacked as input channels
+  dqn-84x84-256x64            256 streams x 64 frames, 84x84, 4 stacked frames, DQN-style trunk
+                              (8x8/4 4->32, 4x4/2 32->64, 3x3/1 64->64, no padding), dense->6
   occlusion-105x80-4096       4096 occlusion variants of one base image, one
                               reuse_net_variants call (copy-on-write overlays) per step
   fullres-1024x32             1024 streams x 32 frames, 210x160, 1->64->128->128, dense->18
@@ -303,8 +305,12 @@ def main():
     fps = S / (ms_step / 1e3)
     fps_dense = S / (ms_dense / 1e3)
     L = len(wl.convs)
-    chans = [wl.in_c * wl.stack] + list(wl.convs)
-    tiles = -(-wl.h // 4) * -(-wl.w // 4)
+    specs = wl.conv_specs()
+    chans = wl.channels()
+    ltiles = [-(-gh // 4) * -(-gw // 4) for gh, gw in wl.grids()]   # 4x4 tiles per layer grid
+    general = [not (k == 3 and st == 1 and pd == 1) for (_ci, _co, k, st, pd) in specs]
+    # algorithmic flops per dirty tile of layer l: 16 px x cout x k k cin x 2
+    fpt = [0] + [16 * co * k * k * ci * 2 for (ci, co, k, _st, _pd) in specs]
     dirty = np.array([[s["dirty_tiles"][l] for l in range(L + 1)] for s in timed_stats], float)
     changed = np.mean([s["changed_px"] for s in timed_stats]) / (S * wl.h * wl.w)
     useful = np.mean([s["useful_mac"] for s in timed_stats])
@@ -314,26 +320,35 @@ def main():
     kern = {}
     for name, rec in prof.items():
         kern[name] = {"ms_per_step": rec["ms"] / K, "launches": rec["launches"]}
-    # MFMA conv layers 2..L: algorithmic flops = dirty tiles x 16 px x cout x 9 cin x 2
-    flops_convn = sum(dirty[:, l].sum() * 16 * chans[l] * 9 * chans[l - 1] * 2 for l in range(2, L + 1))
+    # MFMA conv layers 2..L (and a general first layer): flops of the dirty tiles
+    flops_convn = sum(dirty[:, l].sum() * fpt[l] for l in range(2, L + 1))
     if prof["convN"]["ms"] > 0:
         kern["convN"]["tflops"] = flops_convn / (prof["convN"]["ms"] / 1e3) / 1e12
-    K_el = tiles * 16 * chans[L]
+    if general[0] and prof["conv1"]["ms"] > 0:
+        kern["conv1"]["tflops"] = dirty[:, 1].sum() * fpt[1] / (prof["conv1"]["ms"] / 1e3) / 1e12
+    K_el = ltiles[L] * 16 * chans[L]
     esz = 2 if args.dtype == "bf16" else 4
     if args.head == "full":
         head_bytes = (S * K_el * esz + wl.n_out * K_el * 4) * K  # whole last-layer caches + weights
     else:
-        head_bytes = S * tiles * wl.n_out * 4 * K               # per-tile partials
+        head_bytes = S * ltiles[L] * wl.n_out * 4 * K           # per-tile partials
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
     mask_bytes = drv.mask_bytes() * K
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
     if prof["conv1"]["ms"] > 0:
-        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + 36 * chans[0] * 4)
+        k1, s1 = specs[0][2], specs[0][3]
+        patch = (3 * s1 + k1) ** 2                              # input pixels read per output tile
+        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + patch * chans[0] * 4)
         kern["conv1"]["gbs"] = conv1_bytes / (prof["conv1"]["ms"] / 1e3) / 1e9
 
-    folded = (not args.separate_first) and chans[0] == 1 and L >= 2 and chans[1] == 40
+    folded = (not args.separate_first) and chans[0] == 1 and L >= 2 and chans[1] == 40 and not any(general[:2])
     dominant = max(("convN", "head", "masks", "conv1", "compact"), key=lambda k: prof[k]["ms"])
-    if dominant == "convN":
+    if dominant == "conv1" and general[0]:
+        ach = kern["conv1"]["tflops"]
+        roof = {"bound": "mfma", "kernel": "MFMA dirty-tile conv, general first layer", "achieved": ach,
+                "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_MFMA_F32_TFLOPS,
+                "traffic": None}
+    elif dominant == "convN":
         ach = kern["convN"]["tflops"]
         peak = PEAK_MFMA_BF16_TFLOPS if args.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
         roof = {"bound": "mfma",
@@ -378,7 +393,7 @@ def main():
         "dense_path": {"value": fps_dense, "unit": drv.unit, "ms_per_step": ms_dense},
         "speedup_vs_dense": fps / fps_dense,
         "changed_px_frac": changed,
-        "dirty_tile_frac": [float(dirty[:, l].mean() / (S * tiles)) for l in range(L + 1)],
+        "dirty_tile_frac": [float(dirty[:, l].mean() / (S * ltiles[l])) for l in range(L + 1)],
         "effective_gmacs": dense_mac * fps / 1e9,
         "useful_gmacs": useful / (ms_step / 1e3) / 1e9,
         "ms_per_step_profiled": ms_prof / K,

@@ -230,7 +230,8 @@ def _dtype_code(name: str) -> int:
 class ReuseNet:
     """One reuse net on a CUDA (HIP) device, workspace held in a torch tensor.
 
-    convs: sequence of output channels (3x3, stride 1, pad 1 each).
+    convs: per layer either an output channel count (3x3, stride 1, pad 1) or a
+    tuple (cout, k, stride, pad).
     weights: (conv_w list of OIHW float32, conv_b list, dense_w [n_out][C_L*H*W], dense_b).
     """
 
@@ -245,10 +246,15 @@ class ReuseNet:
         self.n_out, self.max_streams = n_out, max_streams
         specs = []
         c = in_c * stack
+        self.grids = [(h, w)]                     # output grid of each layer (0: the input)
         for co in self.convs:
-            specs.append((c, co, 3, 1, 1))
-            c = co
+            cout, k, st, pd = (tuple(co) if isinstance(co, (tuple, list)) else (co, 3, 1, 1))
+            specs.append((c, cout, k, st, pd))
+            gh, gw = self.grids[-1]
+            self.grids.append((max(0, (gh + 2 * pd - k) // st + 1), max(0, (gw + 2 * pd - k) // st + 1)))
+            c = cout
         self.specs = specs
+        self.channels = [in_c] + [sp[1] for sp in specs]
         self._spec_arr = (rn_conv_spec * len(specs))(*[rn_conv_spec(*s) for s in specs])
         self.cfg = rn_config(in_c, h, w, stack, len(specs), self._spec_arr, n_out, tile, tile,
                              max_streams, _dtype_code(act_dtype),
@@ -272,6 +278,7 @@ class ReuseNet:
         self.words_per_row = -(-w // 64)
         self.tiles = (-(-h // tile), -(-w // tile))
         self.tile_words = -(-(self.tiles[0] * self.tiles[1]) // 64)
+        self.layer_tiles = [(-(-gh // tile), -(-gw // tile)) for gh, gw in self.grids]
 
     # -- hot path
     def _frames(self, frames):
@@ -340,31 +347,33 @@ class ReuseNet:
 
     # -- introspection
     def pixel_mask(self, layer: int, stream_id: int) -> np.ndarray:
-        """uint64 [H][words_per_row] bit rows."""
-        words = self.h * self.words_per_row
-        return reuse_net_get_pixel_mask(self.handle, layer, stream_id, words).reshape(
-            self.h, self.words_per_row)
+        """uint64 [H_l][words_per_row_l] bit rows of layer l's grid."""
+        gh, gw = self.grids[layer]
+        wpr = -(-gw // 64)
+        return reuse_net_get_pixel_mask(self.handle, layer, stream_id, gh * wpr).reshape(gh, wpr)
 
     def pixel_mask_u8(self, layer: int, stream_id: int) -> np.ndarray:
-        """uint8 [H][W], 1 = dirty (unpacked from the bit rows)."""
+        """uint8 [H_l][W_l], 1 = dirty (unpacked from the bit rows)."""
+        gh, gw = self.grids[layer]
         m = self.pixel_mask(layer, stream_id)
-        bits = np.unpackbits(m.view(np.uint8).reshape(self.h, -1), axis=1, bitorder="little")
-        return bits[:, :self.w]
+        bits = np.unpackbits(m.view(np.uint8).reshape(gh, -1), axis=1, bitorder="little")
+        return bits[:, :gw]
 
     def tile_mask_u8(self, layer: int, stream_id: int) -> np.ndarray:
-        m = reuse_net_get_tile_mask(self.handle, layer, stream_id, self.tile_words)
+        th, tw = self.layer_tiles[layer]
+        m = reuse_net_get_tile_mask(self.handle, layer, stream_id, -(-(th * tw) // 64))
         bits = np.unpackbits(m.view(np.uint8), bitorder="little")
-        th, tw = self.tiles
         return bits[:th * tw].reshape(th, tw)
 
     def worklist(self, layer: int, cap: Optional[int] = None) -> np.ndarray:
         batch = max(self.max_streams, getattr(self, "_last_batch", 0))
-        cap = cap if cap is not None else batch * self.tiles[0] * self.tiles[1]
+        th, tw = self.layer_tiles[layer]
+        cap = cap if cap is not None else batch * th * tw
         return reuse_net_get_worklist(self.handle, layer, cap)
 
     def activation(self, stream_id: int, layer: int) -> np.ndarray:
-        c = self.in_c if layer == 0 else self.convs[layer - 1]
-        return reuse_net_read_activation(self.handle, stream_id, layer, (c, self.h, self.w))
+        gh, gw = self.grids[layer]
+        return reuse_net_read_activation(self.handle, stream_id, layer, (self.channels[layer], gh, gw))
 
     def stats(self) -> dict:
         return reuse_net_get_stats(self.handle)

@@ -345,10 +345,16 @@ __device__ inline void mfma_positions(floatx4 *acc, const float *halo, const flo
 // VAR: work item widx of a variant list; the outputs go to overlay row widx
 // (none for a last layer, which only feeds the head), the partials to row
 // widx of the variant partials.
-template <int CIN, int COUT, int NO, bool VAR>
+template <int COUT>
+struct Epi {
+    static constexpr int NB = COUT / 16;      // 16-column blocks of the 16x16x4 product
+    static constexpr int SR = COUT + 4;       // row stride of the output staging area
+};
+
+template <int COUT, int NO, bool VAR>
 __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *acc, const float *s_bias,
                                 float *stage, int lane, int widx) {
-    using M = Mfma<CIN, COUT>;
+    using M = Epi<COUT>;
     const int mrow = lane & 15, kq = lane >> 4;       // D holds pixels (py = i, px = kq)
     const bool col_in = r.tx * kTile + kq < a.W;
 #pragma unroll
@@ -499,7 +505,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
         __builtin_amdgcn_s_setprio(0);
         wave_sync();
-        epilogue<CIN, COUT, NO, VAR>(a, cur, acc, s_bias, halo, lane, t);
+        epilogue<COUT, NO, VAR>(a, cur, acc, s_bias, halo, lane, t);
         // The next patch goes to LDS here rather than at the top of the loop:
         // the wait for its load then counts exactly this tile's later memory
         // operations, where at the loop top it would have to drain them all.
@@ -678,11 +684,158 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         }
         if (valid) {
             wave_sync();
-            epilogue<CIN, COUT, -1, VAR>(a, item_ref(a, e_cur), acc, s_bias, halo, lane, t);
+            epilogue<COUT, -1, VAR>(a, item_ref(a, e_cur), acc, s_bias, halo, lane, t);
         }
         store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);      // this wave's own area
         wave_sync();
         e_cur = e_nxt;
+    }
+}
+
+// ------------------------------------------------------------------ general layers
+
+// Any k x k kernel with stride s and zero padding p <= (k - 1) / 2 (the growth
+// rule of Fig. 1 for general k and s; DQN-style trunks: 8x8/4, 4x4/2, 3x3/1
+// without padding).  A 4x4 output tile reads an E x E input patch, E = 3 s + k,
+// whose corner is input pixel (4 s ty - p, 4 s tx - p); out-of-grid pixels are
+// zero.  Implicit GEMM on v_mfma_f32_16x16x4_f32 (operand layout as in Mfma):
+// M = 16 tile pixels (column-major rows), N = COUT, K = k k CIN in (ky, kx, c)
+// order, walked in blocks of 16 K values: in block b, k-step j gives lane group
+// kq the K index 16 b + 4 kq + j, so a lane's four k-steps are consecutive K
+// values (four consecutive channels of one input pixel when CIN % 4 = 0: one
+// 16-byte LDS read).  K is padded to a multiple of 16 with zero weights and
+// zero A values.  The patch sits in LDS channel-innermost; the weights,
+// packed [block][n-block][lane][j], stream from global memory (the same few
+// hundred KB for every wave, served by L1/L2), one 16-byte load per lane and
+// n-block, a block ahead of their use.  One wave per tile, four waves per block;
+// the epilogue is the one of the 3x3 kernels (bias, ReLU, zero outside the
+// output grid, tile head partials on the last layer, cache store).
+// FIRST: the input is the float32 input cache (planar, a ring of 4 frames when
+// stacking) instead of a tiled layer cache.
+template <int KS, int ST, int CIN, int COUT>
+struct Gen {
+    static constexpr int E = 3 * ST + KS;
+    static constexpr int KT = KS * KS * CIN;
+    static constexpr int NBLK = (KT + 15) / 16;
+    static constexpr int NB = COUT / 16;
+    static constexpr int HALO = E * E * CIN;
+    static constexpr int STAGE = 16 * Epi<COUT>::SR;
+    static constexpr int AREA = HALO > STAGE ? HALO : STAGE;   // floats per wave
+    static constexpr size_t lds_bytes = (size_t)4 * AREA * sizeof(float);
+    static_assert(COUT % 16 == 0, "16-column blocks");
+};
+
+template <int KS, int ST, int CIN, int COUT, bool FIRST>
+__device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float *halo, int lane) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    const int y0 = 4 * ST * r.ty - a.pad, x0 = 4 * ST * r.tx - a.pad;
+    if constexpr (FIRST) {
+        const float *xin = static_cast<const float *>(a.in);
+        const size_t HW = (size_t)a.Hin * a.Win;
+        const int cin1 = CIN / a.stack;
+        const int head = a.stack != 1 ? a.ring_head[r.slot] : 0;
+        for (int h = lane; h < G::HALO; h += 64) {
+            const int c = h / (G::E * G::E), pos = h - c * (G::E * G::E);
+            const int hy = pos / G::E, hx = pos - hy * G::E;
+            const int y = y0 + hy, x = x0 + hx;
+            float v = 0.0f;
+            if (y >= 0 && y < a.Hin && x >= 0 && x < a.Win) {
+                const float *plane;
+                if (a.stack == 1) {
+                    plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                } else {
+                    const int j = c / cin1, c1 = c - j * cin1;
+                    const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                    plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                }
+                v = plane[(size_t)y * a.Win + x];
+            }
+            halo[pos * CIN + c] = v;
+        }
+    } else {
+        static_assert(CIN % 4 == 0, "cache layers carry whole 16-byte channel groups");
+        constexpr int C4 = CIN / 4;
+        const float *src = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
+        for (int h = lane; h < G::E * G::E * C4; h += 64) {
+            const int pos = h / C4, c4 = h - pos * C4;
+            const int hy = pos / G::E, hx = pos - hy * G::E;
+            const int y = y0 + hy, x = x0 + hx;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
+                v = *reinterpret_cast<const float4 *>(
+                    src + ((size_t)((y >> 2) * a.TWin + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN + 4 * c4);
+            *reinterpret_cast<float4 *>(halo + pos * CIN + 4 * c4) = v;
+        }
+    }
+}
+
+// A values of block b for this lane: K = 16 b + 4 kq + j, j = 0..3, of tile
+// pixel (py, px).
+template <int KS, int ST, int CIN, int COUT>
+__device__ inline float4 gen_a(const float *halo, int b, int kq, int py, int px) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    const int K0 = 16 * b + 4 * kq;
+    if constexpr (CIN % 4 == 0) {
+        if (K0 >= G::KT) return make_float4(0.f, 0.f, 0.f, 0.f);
+        const int kpos = K0 / CIN, c = K0 - kpos * CIN;
+        const int ky = kpos / KS, kx = kpos - ky * KS;
+        return *reinterpret_cast<const float4 *>(halo + ((py * ST + ky) * G::E + px * ST + kx) * CIN + c);
+    } else {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int K = K0 + j < G::KT ? K0 + j : G::KT - 1;   // padded K: an in-patch address, value 0
+            const int kpos = K / CIN, c = K - kpos * CIN;
+            const int ky = kpos / KS, kx = kpos - ky * KS;
+            const float hv = halo[((py * ST + ky) * G::E + px * ST + kx) * CIN + c];
+            v[j] = K0 + j < G::KT ? hv : 0.f;
+        }
+        return make_float4(v[0], v[1], v[2], v[3]);
+    }
+}
+
+template <int KS, int ST, int CIN, int COUT, bool DENSE, bool FIRST>
+__global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    extern __shared__ float smem[];
+    __shared__ float s_bias[COUT];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+    __syncthreads();
+    float *halo = smem + wave * G::AREA;
+    const floatx4 *wg = static_cast<const floatx4 *>(a.w);
+    const int cnt = work_count<DENSE>(a);
+    const XcdRange xr = xcd_range(cnt, 4);
+    const int m = lane & 15, kq = lane >> 4;
+    const int py = m & 3, px = m >> 2;
+    for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
+        const TileRef r = decode<DENSE>(a, t);
+        gen_load_patch<KS, ST, CIN, COUT, FIRST>(a, r, halo, lane);
+        wave_sync();
+        floatx4 acc[G::NB];
+#pragma unroll
+        for (int nb = 0; nb < G::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        floatx4 bc[G::NB], bn[G::NB];           // ext-vector arrays stay in registers
+#pragma unroll
+        for (int nb = 0; nb < G::NB; ++nb) bc[nb] = wg[nb * 64 + lane];
+        for (int b = 0; b < G::NBLK; ++b) {
+            if (b + 1 < G::NBLK) {
+#pragma unroll
+                for (int nb = 0; nb < G::NB; ++nb) bn[nb] = wg[((b + 1) * G::NB + nb) * 64 + lane];
+            }
+            const float4 av = gen_a<KS, ST, CIN, COUT>(halo, b, kq, py, px);
+            const float al[4] = {av.x, av.y, av.z, av.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int nb = 0; nb < G::NB; ++nb) {
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], bc[nb][j], acc[nb], 0, 0, 0);
+                }
+#pragma unroll
+            for (int nb = 0; nb < G::NB; ++nb) bc[nb] = bn[nb];
+        }
+        wave_sync();
+        epilogue<COUT, -1, false>(a, r, acc, s_bias, halo, lane, t);
     }
 }
 
@@ -745,9 +898,77 @@ hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
 }
 
 #define RN_MFMA_SHAPES(X) X(40, 80) X(80, 160) X(64, 128) X(128, 128)
+// General layers: (k, stride, cin, cout); first layers read the input frames.
+#define RN_GEN_FIRST_SHAPES(X) X(8, 4, 4, 32) X(8, 4, 1, 32) X(5, 1, 1, 32) X(7, 2, 1, 32) X(5, 2, 4, 32)
+#define RN_GEN_SHAPES(X) X(4, 2, 32, 64) X(3, 1, 64, 64) X(3, 1, 32, 64) X(3, 2, 32, 64) X(5, 2, 32, 64) X(5, 1, 32, 32)
+
+template <int KS, int ST, int CIN, int COUT, bool FIRST>
+hipError_t run_gen(const ConvArgs &a, int cus, hipStream_t s) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    const bool dense = a.wl == nullptr;
+    auto kern = dense ? k_conv_gen<KS, ST, CIN, COUT, true, FIRST> : k_conv_gen<KS, ST, CIN, COUT, false, FIRST>;
+    static hipError_t attr = set_lds(k_conv_gen<KS, ST, CIN, COUT, true, FIRST>, G::lds_bytes);
+    static hipError_t attr2 = set_lds(k_conv_gen<KS, ST, CIN, COUT, false, FIRST>, G::lds_bytes);
+    if (attr != hipSuccess) return attr;
+    if (attr2 != hipSuccess) return attr2;
+    const int grid = persistent_grid(cus * 4, (a.max_tiles + 3) / 4);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), G::lds_bytes, s, a);
+    return hipGetLastError();
+}
 #define RN_FIRST_SHAPES(X) X(1, 20) X(1, 40) X(1, 64) X(1, 80) X(4, 20) X(4, 40) X(4, 64) X(4, 80)
 
 }  // namespace
+
+bool conv_gen_supported(int k, int s, int cin, int cout, bool first) {
+#define X(kk, ss, ci, co) if (k == kk && s == ss && cin == ci && cout == co) return true;
+    if (first) {
+        RN_GEN_FIRST_SHAPES(X)
+    } else {
+        RN_GEN_SHAPES(X)
+    }
+#undef X
+    return false;
+}
+
+hipError_t launch_conv_gen(const ConvArgs &a, int k, int s, bool first, int cus, hipStream_t st) {
+#define X(kk, ss, ci, co) \
+    if (k == kk && s == ss && a.cin == ci && a.cout == co) return run_gen<kk, ss, ci, co, FIRSTV>(a, cus, st);
+    if (first) {
+#define FIRSTV true
+        RN_GEN_FIRST_SHAPES(X)
+#undef FIRSTV
+    } else {
+#define FIRSTV false
+        RN_GEN_SHAPES(X)
+#undef FIRSTV
+    }
+#undef X
+    return hipErrorInvalidValue;
+}
+
+size_t conv_gen_packed_elems(int k, int cin, int cout) {
+    const int kt = k * k * cin;
+    return (size_t)((kt + 15) / 16) * 16 * cout;
+}
+
+void pack_conv_gen(const float *oihw, int k, int cin, int cout, float *dst) {
+    // [block][n-block][lane][j]: K = 16 block + 4 (lane / 16) + j in (ky, kx, c)
+    // order, n = 16 n-block + lane % 16; zero past K = k k cin.
+    const int kt = k * k * cin, nblk = (kt + 15) / 16, nbn = cout / 16;
+    size_t o = 0;
+    for (int b = 0; b < nblk; ++b)
+        for (int nb = 0; nb < nbn; ++nb)
+            for (int l = 0; l < 64; ++l)
+                for (int j = 0; j < 4; ++j) {
+                    const int K = 16 * b + 4 * (l / 16) + j, n = nb * 16 + l % 16;
+                    float v = 0.f;
+                    if (K < kt) {
+                        const int kpos = K / cin, c = K % cin, ky = kpos / k, kx = kpos % k;
+                        v = oihw[(((size_t)n * cin + c) * k + ky) * k + kx];
+                    }
+                    dst[o++] = v;
+                }
+}
 
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt) {
     if (dt != RN_F32) return false;

@@ -24,7 +24,14 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 struct Plan {
-    int L = 0, H = 0, W = 0, WW = 0, TH = 0, TW = 0, TMW = 0, ntiles = 0;
+    int L = 0, H = 0, W = 0, WW = 0, TH = 0, TW = 0, TMW = 0, ntiles = 0;   // input grid
+    // Layer l's output grid (l = 0: the input) and its tiles.
+    int Hl[RN_MAX_CONV + 1] = {0}, Wl[RN_MAX_CONV + 1] = {0}, WWl[RN_MAX_CONV + 1] = {0};
+    int THl[RN_MAX_CONV + 1] = {0}, TWl[RN_MAX_CONV + 1] = {0}, TMWl[RN_MAX_CONV + 1] = {0};
+    int ntl[RN_MAX_CONV + 1] = {0};
+    int ks[RN_MAX_CONV] = {0}, st[RN_MAX_CONV] = {0}, pd[RN_MAX_CONV] = {0};   // of layer l + 1
+    bool gen[RN_MAX_CONV] = {false};       // layer l + 1 is not 3x3 stride 1 pad 1 (general kernel)
+    bool any_gen = false;
     int in_c = 0, stack = 1, S = 0, N = 0;
     rn_dtype dt = RN_F32;
     size_t esz = 4;
@@ -74,8 +81,9 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
         const rn_conv_spec &s = cfg->conv[l];
         if (s.cin != c) return fail(RN_EINVAL, "conv channel chain is inconsistent at layer " + std::to_string(l + 1));
         if (s.cout < 1 || s.k < 1 || s.stride < 1 || s.pad < 0) return fail(RN_EINVAL, "bad conv spec");
-        if (s.k % 2 == 0 || s.pad != (s.k - 1) / 2) return fail(RN_EINVAL, "conv needs odd k and pad = (k-1)/2");
-        if (s.k != 3 || s.stride != 1) return fail(RN_EUNSUPPORTED, "only 3x3 stride-1 conv layers are implemented");
+        if (s.pad > (s.k - 1) / 2) return fail(RN_EINVAL, "conv pad must be at most (k-1)/2");
+        if (s.k > 8 || (s.stride != 1 && s.stride != 2 && s.stride != 4))
+            return fail(RN_EUNSUPPORTED, "conv layers need k <= 8 and stride 1, 2 or 4");
         c = s.cout;
     }
     if (cfg->tile_h != kTile || cfg->tile_w != kTile) return fail(RN_EUNSUPPORTED, "only 4x4 tiles are implemented");
@@ -92,6 +100,27 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     if (p->TH > 256 || p->TW > 256) return fail(RN_EUNSUPPORTED, "frames above 1024 x 1024 are not implemented");
     p->ntiles = p->TH * p->TW;
     p->TMW = ceil_div(p->ntiles, 64);
+    p->Hl[0] = p->H;
+    p->Wl[0] = p->W;
+    for (int l = 0; l < cfg->n_conv; ++l) {
+        const rn_conv_spec &cs = cfg->conv[l];
+        p->ks[l] = cs.k;
+        p->st[l] = cs.stride;
+        p->pd[l] = cs.pad;
+        p->gen[l] = !(cs.k == 3 && cs.stride == 1 && cs.pad == 1);
+        p->any_gen = p->any_gen || p->gen[l];
+        const int nh = p->Hl[l] + 2 * cs.pad - cs.k, nw = p->Wl[l] + 2 * cs.pad - cs.k;
+        if (nh < 0 || nw < 0) return fail(RN_EINVAL, "layer " + std::to_string(l + 1) + " leaves no output pixels");
+        p->Hl[l + 1] = nh / cs.stride + 1;
+        p->Wl[l + 1] = nw / cs.stride + 1;
+    }
+    for (int l = 0; l <= cfg->n_conv; ++l) {
+        p->WWl[l] = ceil_div(p->Wl[l], 64);
+        p->THl[l] = ceil_div(p->Hl[l], kTile);
+        p->TWl[l] = ceil_div(p->Wl[l], kTile);
+        p->ntl[l] = p->THl[l] * p->TWl[l];
+        p->TMWl[l] = ceil_div(p->ntl[l], 64);
+    }
     p->in_c = cfg->in_c;
     p->stack = cfg->stack;
     p->S = cfg->max_streams;
@@ -105,19 +134,29 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     }
     const bool bf = p->dt == RN_BF16;
     const char *dts = bf ? " (bf16)" : " (float32)";
-    if (!(bf ? conv_first_bf16_supported(p->C[0], p->C[1]) : conv_first_supported(p->C[0], p->C[1], p->dt)))
-        return fail(RN_EUNSUPPORTED, "no first-layer kernel for " + std::to_string(p->C[0]) + "->" +
-                                         std::to_string(p->C[1]) + dts);
+    if (bf && p->any_gen) return fail(RN_EUNSUPPORTED, "bf16 needs 3x3 stride-1 pad-1 layers");
+    auto shape = [&](int l) {
+        return std::to_string(p->C[l - 1]) + "->" + std::to_string(p->C[l]) +
+               (p->gen[l - 1] ? " (" + std::to_string(p->ks[l - 1]) + "x" + std::to_string(p->ks[l - 1]) + " stride " +
+                                    std::to_string(p->st[l - 1]) + ")"
+                              : "") +
+               dts;
+    };
+    if (p->gen[0] ? !conv_gen_supported(p->ks[0], p->st[0], p->C[0], p->C[1], true)
+                  : !(bf ? conv_first_bf16_supported(p->C[0], p->C[1]) : conv_first_supported(p->C[0], p->C[1], p->dt)))
+        return fail(RN_EUNSUPPORTED, "no first-layer kernel for " + shape(1));
     for (int l = 2; l <= p->L; ++l)
-        if (!(bf ? conv_mfma_bf16_supported(p->C[l - 1], p->C[l]) : conv_mfma_supported(p->C[l - 1], p->C[l], p->dt)))
-            return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + std::to_string(p->C[l - 1]) + "->" +
-                                             std::to_string(p->C[l]) + dts);
-    p->K = (size_t)p->ntiles * kTilePx * p->C[p->L];
+        if (p->gen[l - 1] ? !conv_gen_supported(p->ks[l - 1], p->st[l - 1], p->C[l - 1], p->C[l], false)
+                          : !(bf ? conv_mfma_bf16_supported(p->C[l - 1], p->C[l])
+                                 : conv_mfma_supported(p->C[l - 1], p->C[l], p->dt)))
+            return fail(RN_EUNSUPPORTED, "no MFMA conv kernel for " + shape(l));
+    p->K = (size_t)p->ntl[p->L] * kTilePx * p->C[p->L];
     p->fuse_first = !(cfg->options & RN_OPT_SEPARATE_FIRST) && p->L >= 2 && p->C[0] == 1 && p->stack == 1 &&
-                    conv_fused_first_supported(p->C[1], p->C[2], p->dt);
+                    !p->gen[0] && !p->gen[1] && conv_fused_first_supported(p->C[1], p->C[2], p->dt);
     // The tile-partial head lives in the epilogue of an MFMA layer (float32) or
     // in its own matrix kernel after the last layer (bf16).
-    p->head_mode = (cfg->head_mode == RN_HEAD_TILES && p->L >= 2 && (!bf || tile_part_bf16_supported(p->C[p->L])))
+    p->head_mode = (cfg->head_mode == RN_HEAD_TILES && (p->L >= 2 || p->gen[p->L - 1]) &&
+                    (!bf || tile_part_bf16_supported(p->C[p->L])))
                        ? RN_HEAD_TILES
                        : RN_HEAD_FULL;
     p->head_sg = head_streams_per_block(p->N);
@@ -130,7 +169,7 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     }
     p->part_elems = part * p->N;
 
-    const size_t S = p->S, HW = (size_t)p->H * p->W, HWW = (size_t)p->H * p->WW;
+    const size_t S = p->S, HW = (size_t)p->H * p->W, HWW = (size_t)p->H * p->WW;   // input grid
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -145,12 +184,13 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_ids = take(S * 4);
     p->act_stride[0] = (size_t)p->stack * p->in_c * HW;
     for (int l = 1; l <= p->L; ++l) {
-        p->act_stride[l] = (size_t)p->ntiles * kTilePx * p->C[l];
+        p->act_stride[l] = (size_t)p->ntl[l] * kTilePx * p->C[l];
         p->o_act[l] = take(S * p->act_stride[l] * p->esz);
     }
     for (int l = 0; l < p->L; ++l) {
-        p->w_elems[l] = l == 0 ? conv_first_packed_elems(p->C[0], p->C[1])
-                               : conv_mfma_packed_elems(p->C[l], p->C[l + 1], p->dt);
+        p->w_elems[l] = p->gen[l] ? conv_gen_packed_elems(p->ks[l], p->C[l], p->C[l + 1])
+                        : l == 0  ? conv_first_packed_elems(p->C[0], p->C[1])
+                                  : conv_mfma_packed_elems(p->C[l], p->C[l + 1], p->dt);
         // layer 1 keeps float32 weights (bf16-rounded values in bf16 mode); MFMA layers store bf16.
         p->w_bytes[l] = p->w_elems[l] * ((l > 0 && p->dt == RN_BF16) ? 2 : 4);
         p->o_w[l] = take(p->w_bytes[l]);
@@ -159,22 +199,22 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_wd = take((size_t)p->N * p->K * 4);
     p->o_bd = take((size_t)p->N * 4);
     for (int l = 0; l <= p->L; ++l) {
-        p->o_pm[l] = take(S * HWW * 8);
-        p->o_tm[l] = take(S * p->TMW * 8);
+        p->o_pm[l] = take(S * p->Hl[l] * p->WWl[l] * 8);
+        p->o_tm[l] = take(S * p->TMWl[l] * 8);
     }
     p->o_nchg = take(S * 4);
     p->o_ntile = take(S * (p->L + 1) * 4);
     for (int l = 1; l <= p->L; ++l) {
-        p->o_wl[l] = take(S * p->ntiles * 4);
-        p->o_wls[l] = take(S * p->ntiles * 4);
+        p->o_wl[l] = take(S * p->ntl[l] * 4);
+        p->o_wls[l] = take(S * p->ntl[l] * 4);
     }
     p->o_cnt = take((RN_MAX_CONV + 1) * 4);
     const bool tiles_head = p->head_mode == RN_HEAD_TILES;
     p->o_part = take(tiles_head ? 0 : p->part_elems * 4);
     p->o_hw = take(!tiles_head ? 0
-                   : p->dt == RN_BF16 ? tile_part_bf16_elems(p->ntiles, p->C[p->L], p->N) * 2
-                                      : tile_head_w_elems(p->ntiles, p->C[p->L], p->N) * 4);
-    p->o_hp = take(tiles_head ? S * p->ntiles * p->N * 4 : 0);
+                   : p->dt == RN_BF16 ? tile_part_bf16_elems(p->ntl[p->L], p->C[p->L], p->N) * 2
+                                      : tile_head_w_elems(p->ntl[p->L], p->C[p->L], p->N) * 4);
+    p->o_hp = take(tiles_head ? S * p->ntl[p->L] * p->N * 4 : 0);
     p->total = off;
     return RN_OK;
 }
@@ -302,7 +342,19 @@ MaskGeom make_geom(reuse_net *net) {
     g.TMW = p.TMW;
     g.cin = p.in_c;
     g.stack = p.stack;
-    for (int l = 0; l < p.L; ++l) g.radius[l] = p.radius[l];
+    for (int l = 0; l <= p.L; ++l) {
+        g.Hl[l] = p.Hl[l];
+        g.Wl[l] = p.Wl[l];
+        g.WWl[l] = p.WWl[l];
+        g.THl[l] = p.THl[l];
+        g.TWl[l] = p.TWl[l];
+        g.TMWl[l] = p.TMWl[l];
+    }
+    for (int l = 0; l < p.L; ++l) {
+        g.ks[l] = p.ks[l];
+        g.st[l] = p.st[l];
+        g.pd[l] = p.pd[l];
+    }
     for (int l = 0; l <= p.L; ++l) {
         g.pmask[l] = net->at<uint64_t>(p.o_pm[l]);
         g.tmask[l] = net->at<uint64_t>(p.o_tm[l]);
@@ -328,17 +380,21 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
         cv.w = net->at<void>(p.o_w[l - 1]);
         cv.bias = net->at<float>(p.o_b[l - 1]);
         cv.ring_head = net->at<int32_t>(p.o_ring);
-        cv.H = p.H;
-        cv.W = p.W;
-        cv.TH = p.TH;
-        cv.TW = p.TW;
+        cv.H = p.Hl[l];
+        cv.W = p.Wl[l];
+        cv.TH = p.THl[l];
+        cv.TW = p.TWl[l];
+        cv.Hin = p.Hl[l - 1];
+        cv.Win = p.Wl[l - 1];
+        cv.TWin = p.TWl[l - 1];
+        cv.pad = p.pd[l - 1];
         cv.cin = p.C[l - 1];
         cv.cout = p.C[l];
         cv.stack = p.stack;
         cv.in_stride = p.act_stride[l - 1];
         cv.out_stride = p.act_stride[l];
         cv.dense_n = dense ? n : 0;
-        cv.max_tiles = n * p.ntiles;
+        cv.max_tiles = n * p.ntl[l];
         if (l == 2 && p.fuse_first) {
             cv.fuse_first = 1;
             cv.in = net->at<float>(p.o_xin);
@@ -354,7 +410,11 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
             last = cv;
             if (bf) cv.n_out = 0;                         // partials from their own kernel below
         }
-        if (l == 1)
+        if (p.gen[l - 1])
+            e = timed(net, l == 1 ? RN_PHASE_CONV1 : RN_PHASE_CONVN, s, [&] {
+                return launch_conv_gen(cv, p.ks[l - 1], p.st[l - 1], l == 1, net->cus, s);
+            });
+        else if (l == 1)
             e = timed(net, RN_PHASE_CONV1, s, [&] {
                 return bf ? launch_conv_first_bf16(cv, net->cus, s) : launch_conv_first(cv, p.dt, net->cus, s);
             });
@@ -376,7 +436,7 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
         TileHeadArgs ta{};
         ta.n = n;
         ta.n_out = p.N;
-        ta.ntiles = p.ntiles;
+        ta.ntiles = p.ntl[p.L];
         ta.ids = ids;
         ta.hpart = net->at<float>(p.o_hp);
         ta.bias = net->at<float>(p.o_bd);
@@ -432,9 +492,12 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     CompactArgs ca{};
     ca.n = n;
     ca.L = p.L;
-    ca.TW = p.TW;
-    ca.TMW = p.TMW;
-    ca.ntiles = p.ntiles;
+    for (int l = 0; l <= p.L; ++l) {
+        ca.TWl[l] = p.TWl[l];
+        ca.TMWl[l] = p.TMWl[l];
+        ca.ntl[l] = p.ntl[l];
+        ca.cap[l] = (size_t)n * p.ntl[l];
+    }
     ca.ids = ids;
     ca.ntile = ma.ntile;
     for (int l = 0; l <= p.L; ++l) {
@@ -443,7 +506,6 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
         ca.wls[l] = l ? net->at<uint32_t>(p.o_wls[l]) : nullptr;
     }
     ca.cnt = net->at<int32_t>(p.o_cnt);
-    ca.cap = (size_t)n * p.ntiles;
     e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
 
@@ -459,6 +521,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
 }
 
 const char *variants_unsupported(const Plan &p) {
+    if (p.any_gen) return "variants need 3x3 stride-1 pad-1 layers";
     if (p.head_mode != RN_HEAD_TILES) return "variants need the tile-partial head (head_mode RN_HEAD_TILES, >= 2 layers)";
     if (p.stack != 1) return "variants with stacked frames are not implemented";
     return nullptr;
@@ -544,6 +607,10 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
         cv.in_stride = p.act_stride[l - 1];
         cv.out_stride = p.act_stride[l];
         cv.max_tiles = (int)std::min<size_t>(vp.cap, (size_t)INT32_MAX);
+        cv.Hin = p.H;
+        cv.Win = p.W;
+        cv.TWin = p.TW;
+        cv.pad = 1;
         cv.vbase = base;
         cv.vcin = p.in_c;
         cv.WW = p.WW;
@@ -634,7 +701,7 @@ rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     pa.stack = p.stack;
     pa.H = p.H;
     pa.W = p.W;
-    pa.ntiles = p.ntiles;
+    for (int l = 0; l <= p.L; ++l) pa.ntl[l] = p.ntl[l];
     pa.ids = ids;
     pa.frames = frames;
     pa.frame_u8 = fdt == RN_U8;
@@ -723,7 +790,9 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     std::vector<std::vector<unsigned char>> wpack(p.L);
     for (int l = 0; l < p.L; ++l) {
         wpack[l].assign(p.w_bytes[l], 0);
-        if (l == 0) {
+        if (p.gen[l]) {
+            pack_conv_gen(w->conv_w[l], p.ks[l], p.C[l], p.C[l + 1], reinterpret_cast<float *>(wpack[l].data()));
+        } else if (l == 0) {
             float *d = reinterpret_cast<float *>(wpack[l].data());
             pack_conv_first(w->conv_w[0], p.C[0], p.C[1], p.dt, d);
             for (size_t j = 0; j < p.w_elems[0]; ++j) d[j] = rnd(d[j]);
@@ -734,17 +803,17 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
         }
     }
     // Dense weights from (c, y, x) order to the tiled cache order, 0 at padded pixels.
-    const int CL = p.C[p.L];
+    const int CL = p.C[p.L], HL = p.Hl[p.L], WL = p.Wl[p.L], THL = p.THl[p.L], TWL = p.TWl[p.L];
     std::vector<float> wd((size_t)p.N * p.K, 0.f);
     for (int o = 0; o < p.N; ++o)
-        for (int ty = 0; ty < p.TH; ++ty)
-            for (int tx = 0; tx < p.TW; ++tx)
+        for (int ty = 0; ty < THL; ++ty)
+            for (int tx = 0; tx < TWL; ++tx)
                 for (int m = 0; m < kTilePx; ++m) {
                     const int y = ty * kTile + m / kTile, x = tx * kTile + m % kTile;
-                    if (y >= p.H || x >= p.W) continue;
-                    const size_t dst = (size_t)o * p.K + ((size_t)(ty * p.TW + tx) * kTilePx + m) * CL;
+                    if (y >= HL || x >= WL) continue;
+                    const size_t dst = (size_t)o * p.K + ((size_t)(ty * TWL + tx) * kTilePx + m) * CL;
                     for (int c = 0; c < CL; ++c)
-                        wd[dst + c] = rnd(w->dense_w[(size_t)o * CL * p.H * p.W + ((size_t)c * p.H + y) * p.W + x]);
+                        wd[dst + c] = rnd(w->dense_w[(size_t)o * CL * HL * WL + ((size_t)c * HL + y) * WL + x]);
                 }
 
     hipError_t e = hipMemsetAsync(dev_workspace, 0, p.total, s);
@@ -761,12 +830,12 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     std::vector<float> hw;
     std::vector<uint16_t> hwb;
     if (p.head_mode == RN_HEAD_TILES && bf) {
-        hwb.assign(tile_part_bf16_elems(p.ntiles, CL, p.N), 0);
-        pack_tile_part_bf16(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hwb.data());
+        hwb.assign(tile_part_bf16_elems(p.ntl[p.L], CL, p.N), 0);
+        pack_tile_part_bf16(w->dense_w, p.N, CL, HL, WL, THL, TWL, hwb.data());
         up(p.o_hw, hwb.data(), hwb.size() * 2);
     } else if (p.head_mode == RN_HEAD_TILES) {
-        hw.assign(tile_head_w_elems(p.ntiles, CL, p.N), 0.f);
-        pack_tile_head(w->dense_w, p.N, CL, p.H, p.W, p.TH, p.TW, hw.data());
+        hw.assign(tile_head_w_elems(p.ntl[p.L], CL, p.N), 0.f);
+        pack_tile_head(w->dense_w, p.N, CL, HL, WL, THL, TWL, hw.data());
         for (float &v : hw) v = rnd(v);
         up(p.o_hw, hw.data(), hw.size() * 4);
     }
@@ -869,7 +938,7 @@ rn_status reuse_net_get_pixel_mask(reuse_net *net, int32_t layer, int32_t sid, u
     const MaskView v = mask_view(net);
     if (layer < 0 || layer > p.L || sid < 0 || sid >= v.limit || !out)
         return net->fail(RN_EINVAL, "bad layer, stream or buffer");
-    const size_t need = (size_t)p.H * p.WW;
+    const size_t need = (size_t)p.Hl[layer] * p.WWl[layer];
     if (words < need) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(need) + " words");
     return copy_out(net, out, v.pm[layer] + (size_t)sid * need, need * 8);
 }
@@ -880,8 +949,9 @@ rn_status reuse_net_get_tile_mask(reuse_net *net, int32_t layer, int32_t sid, ui
     const MaskView v = mask_view(net);
     if (layer < 0 || layer > p.L || sid < 0 || sid >= v.limit || !out)
         return net->fail(RN_EINVAL, "bad layer, stream or buffer");
-    if (words < (size_t)p.TMW) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(p.TMW) + " words");
-    return copy_out(net, out, v.tm[layer] + (size_t)sid * p.TMW, (size_t)p.TMW * 8);
+    const int tmw = p.TMWl[layer];
+    if (words < (size_t)tmw) return net->fail(RN_ENOSPACE, "buffer needs " + std::to_string(tmw) + " words");
+    return copy_out(net, out, v.tm[layer] + (size_t)sid * tmw, (size_t)tmw * 8);
 }
 
 rn_status reuse_net_get_worklist(reuse_net *net, int32_t layer, uint32_t *out, size_t cap, int32_t *count) {
@@ -926,10 +996,11 @@ rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, 
         cv.w = net->at<void>(p.o_w[0]);
         cv.bias = net->at<float>(p.o_b[0]);
         cv.ring_head = net->at<int32_t>(p.o_ring);
-        cv.H = p.H;
-        cv.W = p.W;
+        cv.H = cv.Hin = p.H;
+        cv.W = cv.Win = p.W;
         cv.TH = p.TH;
-        cv.TW = p.TW;
+        cv.TW = cv.TWin = p.TW;
+        cv.pad = 1;
         cv.cin = p.C[0];
         cv.cout = p.C[1];
         cv.stack = p.stack;
@@ -957,10 +1028,12 @@ rn_status reuse_net_read_activation(reuse_net *net, int32_t sid, int32_t layer, 
                       p.act_stride[layer] * 4);
     }
     if (st != RN_OK) return st;
-    for (int y = 0; y < p.H; ++y)
-        for (int x = 0; x < p.W; ++x) {
-            const size_t src = ((size_t)((y / kTile) * p.TW + x / kTile) * kTilePx + (y % kTile) * kTile + x % kTile) * C;
-            for (int c = 0; c < C; ++c) host_out[(size_t)c * HW + (size_t)y * p.W + x] = buf[src + c];
+    const int Hl = p.Hl[layer], Wl = p.Wl[layer], TWl = p.TWl[layer];
+    const size_t HWl = (size_t)Hl * Wl;
+    for (int y = 0; y < Hl; ++y)
+        for (int x = 0; x < Wl; ++x) {
+            const size_t src = ((size_t)((y / kTile) * TWl + x / kTile) * kTilePx + (y % kTile) * kTile + x % kTile) * C;
+            for (int c = 0; c < C; ++c) host_out[(size_t)c * HWl + (size_t)y * Wl + x] = buf[src + c];
         }
     return RN_OK;
 }
@@ -982,23 +1055,24 @@ rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out) {
         out->changed_px += nchg[i];
         for (int l = 0; l <= p.L; ++l) out->dirty_tiles[l] += ntile[(size_t)i * (p.L + 1) + l];
     }
-    const int64_t head_mac = (int64_t)n * p.N * p.C[p.L] * p.H * p.W;
+    const int64_t head_mac = (int64_t)n * p.N * p.C[p.L] * p.Hl[p.L] * p.Wl[p.L];
     int64_t useful = head_mac, issued = (int64_t)n * p.N * (int64_t)p.K, dense = head_mac;
     for (int l = 1; l <= p.L; ++l) {
-        const int64_t per_px = (int64_t)9 * p.C[l - 1] * p.C[l];
-        dense += (int64_t)n * p.H * p.W * per_px;
+        const int64_t per_px = (int64_t)p.ks[l - 1] * p.ks[l - 1] * p.C[l - 1] * p.C[l];
+        const int Hl = p.Hl[l], Wl = p.Wl[l];
+        dense += (int64_t)n * Hl * Wl * per_px;
         issued += out->dirty_tiles[l] * kTilePx * per_px;
         if (net->last_was_full) {
-            useful += (int64_t)n * p.H * p.W * per_px;
+            useful += (int64_t)n * Hl * Wl * per_px;
             continue;
         }
         int32_t c = 0;
-        std::vector<uint32_t> wl((size_t)n * p.ntiles);
+        std::vector<uint32_t> wl((size_t)n * p.ntl[l]);
         st = reuse_net_get_worklist(net, l, wl.data(), wl.size(), &c);
         if (st != RN_OK) return st;
         for (int j = 0; j < c; ++j) {
             const int ty = (wl[j] >> 8) & 255, tx = wl[j] & 255;
-            const int hy = std::min(kTile, p.H - ty * kTile), wx = std::min(kTile, p.W - tx * kTile);
+            const int hy = std::min(kTile, Hl - ty * kTile), wx = std::min(kTile, Wl - tx * kTile);
             useful += (int64_t)hy * wx * per_px;
         }
     }

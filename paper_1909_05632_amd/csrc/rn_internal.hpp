@@ -18,17 +18,20 @@ constexpr int kTile = 4;          // dirty-tile edge on every layer
 constexpr int kTilePx = kTile * kTile;
 constexpr int kHeadMaxOut = 64;
 
-// Geometry shared by the mask kernels.  Every supported layer is 3x3, stride 1,
-// pad 1, so every layer's output grid equals the input grid.
+// Geometry shared by the mask kernels.  Layer l's grid is Hl[l] x Wl[l]
+// (layer 0: the input); a 3x3 stride-1 pad-1 layer keeps its input grid, other
+// layers shrink it (pad <= (k - 1) / 2).
 struct MaskGeom {
     int L;                        // conv layers
-    int H, W, WW;                 // rows, columns, 64-bit words per mask row
-    int TH, TW, TMW;              // tile rows, tile columns, 64-bit words per tile mask
+    int H, W, WW;                 // input rows, columns, 64-bit words per mask row
+    int TH, TW, TMW;              // input tile rows, tile columns, 64-bit words per tile mask
     int cin;                      // channels per frame
     int stack;                    // 1, or 4 (ring of the last 4 frames)
-    int radius[RN_MAX_CONV];      // (k - 1) / 2 per layer
-    uint64_t *pmask[RN_MAX_CONV + 1];   // [S][H][WW] per layer
-    uint64_t *tmask[RN_MAX_CONV + 1];   // [S][TMW] per layer
+    int Hl[RN_MAX_CONV + 1], Wl[RN_MAX_CONV + 1], WWl[RN_MAX_CONV + 1];
+    int THl[RN_MAX_CONV + 1], TWl[RN_MAX_CONV + 1], TMWl[RN_MAX_CONV + 1];
+    int ks[RN_MAX_CONV], st[RN_MAX_CONV], pd[RN_MAX_CONV];   // kernel, stride, pad of layer l + 1
+    uint64_t *pmask[RN_MAX_CONV + 1];   // [S][Hl][WWl] per layer
+    uint64_t *tmask[RN_MAX_CONV + 1];   // [S][TMWl] per layer
 };
 
 // Per-step inputs of the mask kernel.
@@ -50,14 +53,15 @@ struct MaskArgs {
 };
 
 struct CompactArgs {
-    int n, L, TW, TMW, ntiles;
+    int n, L;
+    int TWl[RN_MAX_CONV + 1], TMWl[RN_MAX_CONV + 1], ntl[RN_MAX_CONV + 1];   // per layer
     const int32_t *ids;
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
     uint32_t *wl[RN_MAX_CONV + 1];  // entries i << 16 | ty << 8 | tx (batch index i)
     uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels
     int32_t *cnt;                 // [L+1]
-    size_t cap;                   // entries each list can hold
+    size_t cap[RN_MAX_CONV + 1];  // entries each layer's list can hold
 };
 
 // Masks and work lists of n variants straight from their boxes (variant i's
@@ -90,9 +94,11 @@ struct ConvArgs {
     const void *w;                // packed weights
     const float *bias;            // [cout]
     const int32_t *ring_head;     // stack=4 only
-    int H, W, TH, TW;
+    int H, W, TH, TW;             // this layer's output grid and its tile grid
     int cin, cout;
     int stack;
+    int Hin, Win, TWin;           // input grid (layers other than 3x3 stride 1 pad 1)
+    int pad;
     size_t in_stride, out_stride; // elements per slot
     int dense_n;                  // dense mode (wl == NULL): every tile of streams 0..dense_n-1
     int max_tiles;                // host bound on the tiles of this launch (sizes the grid)
@@ -129,7 +135,8 @@ struct ConvArgs {
 
 // Dense path: copy the frames into the input cache and mark the slots primed.
 struct PrimeArgs {
-    int n, L, cin, stack, H, W, ntiles;
+    int n, L, cin, stack, H, W;
+    int ntl[RN_MAX_CONV + 1];     // tiles per layer
     const int32_t *ids;
     const void *frames;
     int frame_u8;
@@ -190,6 +197,12 @@ hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int grid, hipStream
 hipError_t launch_conv_mfma(const ConvArgs &a, rn_dtype dt, int grid, hipStream_t s, bool var = false);
 bool conv_mfma_supported(int cin, int cout, rn_dtype dt);
 bool conv_first_supported(int cin, int cout, rn_dtype dt);
+// General layers (any k <= 8, stride 1, 2 or 4, pad <= (k - 1) / 2; float32):
+// first = the layer reads the input frames.
+bool conv_gen_supported(int k, int s, int cin, int cout, bool first);
+size_t conv_gen_packed_elems(int k, int cin, int cout);
+void pack_conv_gen(const float *oihw, int k, int cin, int cout, float *dst);
+hipError_t launch_conv_gen(const ConvArgs &a, int k, int s, bool first, int cus, hipStream_t st);
 bool conv_fused_first_supported(int c1, int c2, rn_dtype dt);
 bool conv_mfma_bf16_supported(int cin, int cout);
 bool conv_first_bf16_supported(int cin, int cout);

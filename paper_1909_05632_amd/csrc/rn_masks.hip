@@ -2,7 +2,10 @@
 //
 // Change detection (Abstract; Sec. 1): a pixel changed iff the float32 bits of
 // one of its channels differ from the cached input.  Growth (Fig. 1 caption):
-// a 3x3 stride-1 layer spreads a change by one pixel on each side.  Dirty
+// a 3x3 stride-1 layer spreads a change by one pixel on each side; in general
+// an output pixel of a k x k layer with stride s and pad p changed iff its
+// window (rows s y - p .. s y - p + k - 1, the same for columns) holds a
+// changed input pixel.  Dirty
 // tiles (Sec. 3, local areas instead of one rectangle): a 4x4 cell of a
 // layer's grid is dirty iff it holds a dirty pixel.  The work list of a layer
 // is its dirty tiles in (tile row, tile column, batch index) order.
@@ -60,22 +63,23 @@ __device__ inline float load1(const void *frames, size_t off, const float *lut) 
 
 // Write layer l's pixel mask and tile mask of one slot; returns the dirty tiles.
 __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red) {
-    const int HWW = g.H * g.WW;
+    const int H = g.Hl[l], WW = g.WWl[l], TW = g.TWl[l];
+    const int HWW = H * WW;
     uint64_t *pm = g.pmask[l] + (size_t)slot * HWW;
     for (int w = threadIdx.x; w < HWW; w += blockDim.x) pm[w] = A[w];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ntiles = g.TH * g.TW;
-    uint64_t *tm = g.tmask[l] + (size_t)slot * g.TMW;
+    const int ntiles = g.THl[l] * TW;
+    uint64_t *tm = g.tmask[l] + (size_t)slot * g.TMWl[l];
     int cnt = 0;
     for (int base = wave * 64; base < ntiles; base += (int)blockDim.x) {
         const int t = base + lane;
         bool dirty = false;
         if (t < ntiles) {
-            const int ty = t / g.TW, tx = t - ty * g.TW;
+            const int ty = t / TW, tx = t - ty * TW;
             const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
-            const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+            const int y0 = ty * kTile, y1 = min(y0 + kTile, H);
             uint64_t bits = 0;
-            for (int y = y0; y < y1; ++y) bits |= A[y * g.WW + wx] >> sh;
+            for (int y = y0; y < y1; ++y) bits |= A[y * WW + wx] >> sh;
             dirty = (bits & ((1ull << kTile) - 1ull)) != 0;
         }
         const uint64_t m = __ballot(dirty);
@@ -87,23 +91,69 @@ __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot,
     return block_sum(lane == 0 ? cnt : 0, red);
 }
 
-// Grow a change set by one pixel on every side (3x3 window), clipped to the grid.
-__device__ void grow1(const MaskGeom &g, const uint64_t *src, uint64_t *dst) {
-    const int HWW = g.H * g.WW;
+// Grow a change set by one pixel on every side (3x3 window), clipped to the
+// H x W grid (3x3 stride-1 pad-1 layer: the output grid is the input grid).
+__device__ void grow1(int H, int W, int WW, const uint64_t *src, uint64_t *dst) {
+    const int HWW = H * WW;
     for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
-        const int y = w / g.WW, wx = w - y * g.WW;
+        const int y = w / WW, wx = w - y * WW;
         uint64_t acc = 0;
         for (int dy = -1; dy <= 1; ++dy) {
             const int yy = y + dy;
-            if (yy < 0 || yy >= g.H) continue;
-            const uint64_t *row = src + yy * g.WW;
+            if (yy < 0 || yy >= H) continue;
+            const uint64_t *row = src + yy * WW;
             const uint64_t c = row[wx];
             const uint64_t lft = wx > 0 ? row[wx - 1] : 0ull;
-            const uint64_t rgt = wx + 1 < g.WW ? row[wx + 1] : 0ull;
+            const uint64_t rgt = wx + 1 < WW ? row[wx + 1] : 0ull;
             acc |= c | (c << 1) | (lft >> 63) | (c >> 1) | (rgt << 63);
         }
-        dst[w] = acc & row_valid_bits(g.W, wx);
+        dst[w] = acc & row_valid_bits(W, wx);
     }
+}
+
+// Bits of the index range [x0, x1) that fall in 64-bit word wx.
+__device__ inline uint64_t range_bits(int x0, int x1, int wx) {
+    const int lo = max(x0 - 64 * wx, 0), hi = min(x1 - 64 * wx, 64);
+    if (hi <= lo) return 0ull;
+    const uint64_t upto = hi == 64 ? ~0ull : ((1ull << hi) - 1ull);
+    return upto & ~((1ull << lo) - 1ull);
+}
+
+// Growth through a general layer l (k x k, stride s, pad p), separably: rows
+// first (V row y = OR of the input rows s y - p .. s y - p + k - 1 inside the
+// grid, on the input columns), then columns (output bit x = any bit of V row y
+// in s x - p .. s x - p + k - 1).  src: layer l - 1's rows; mid: scratch of
+// Hl[l] x WWl[l - 1] words; the result goes back to src.
+__device__ void grow_general(const MaskGeom &g, int l, uint64_t *src, uint64_t *mid) {
+    const int Hi = g.Hl[l - 1], Wi = g.Wl[l - 1], WWi = g.WWl[l - 1];
+    const int Ho = g.Hl[l], Wo = g.Wl[l], WWo = g.WWl[l];
+    const int k = g.ks[l - 1], s = g.st[l - 1], p = g.pd[l - 1];
+    for (int w = threadIdx.x; w < Ho * WWi; w += blockDim.x) {
+        const int y = w / WWi, wx = w - y * WWi;
+        const int r0 = max(s * y - p, 0), r1 = min(s * y - p + k, Hi);
+        uint64_t acc = 0;
+        for (int r = r0; r < r1; ++r) acc |= src[r * WWi + wx];
+        mid[w] = acc;
+    }
+    __syncthreads();
+    for (int w = threadIdx.x; w < Ho * WWo; w += blockDim.x) {
+        const int y = w / WWo, wx = w - y * WWo;
+        const uint64_t *row = mid + y * WWi;
+        uint64_t word = 0;
+        for (int j = 0; j < 64; ++j) {
+            const int x = 64 * wx + j;
+            if (x >= Wo) break;
+            const int c0 = max(s * x - p, 0), c1 = min(s * x - p + k, Wi);
+            bool any = false;
+            for (int cw = c0 >> 6; cw <= (c1 - 1) >> 6 && c0 < c1; ++cw) any |= (row[cw] & range_bits(c0, c1, cw)) != 0;
+            word |= (uint64_t)any << j;
+        }
+        src[w] = word;
+    }
+}
+
+__device__ inline bool standard_layer(const MaskGeom &g, int l) {
+    return g.ks[l - 1] == 3 && g.st[l - 1] == 1 && g.pd[l - 1] == 1;
 }
 
 template <bool U8>
@@ -235,13 +285,16 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     int t0 = emit_layer(g, A, 0, slot, red);
     if (threadIdx.x == 0) s_tiles[0] = t0;
     for (int l = 1; l <= g.L; ++l) {
-        for (int r = 0; r < g.radius[l - 1]; ++r) {
-            __syncthreads();
-            grow1(g, A, B);
+        __syncthreads();
+        if (standard_layer(g, l)) {
+            grow1(g.Hl[l], g.Wl[l], g.WWl[l], A, B);
             __syncthreads();
             uint64_t *t = A;
             A = B;
             B = t;
+        } else {
+            grow_general(g, l, A, B);
+            __syncthreads();
         }
         const int tl = emit_layer(g, A, l, slot, red);
         if (threadIdx.x == 0) s_tiles[l] = tl;
@@ -286,7 +339,7 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
         a.primed[slot] = 1;
         if (a.stack != 1) a.ring_head[slot] = 0;
         a.nchg[i] = (int)HW;
-        for (int l = 0; l <= a.L; ++l) a.ntile[(size_t)i * (a.L + 1) + l] = a.ntiles;
+        for (int l = 0; l <= a.L; ++l) a.ntile[(size_t)i * (a.L + 1) + l] = a.ntl[l];
     }
 }
 
@@ -307,7 +360,7 @@ __device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, i
         const int i = 64 * c0 + j;
         const int slot = i < a.n ? a.ids[i] : -1;
         s_slot[j] = slot;
-        s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMW + wd] : 0ull;
+        s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMWl[l] + wd] : 0ull;
     }
 }
 
@@ -320,6 +373,8 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     __shared__ int32_t s_slot[kChunksPerPass * 64];
     __shared__ uint64_t s_word[kChunksPerPass * 64];
     const int wd = blockIdx.x, l = blockIdx.y + 1;
+    const int TMW = a.TMWl[l], TW = a.TWl[l], ntiles = a.ntl[l];
+    if (wd >= TMW) return;                       // the grid covers the widest layer; uniform per block
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int nwaves = (int)(blockDim.x >> 6);
     const int nch = (a.n + 63) / 64;
@@ -328,7 +383,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // per stream; the words of a stream are independent loads).
     int pre = 0;
     for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * a.TMW;
+        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * TMW;
         for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
     }
     pre = block_sum(pre, red);
@@ -360,11 +415,11 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             s_run[j] = r;
             r += s_cnt[j];
         }
-        if (wd == a.TMW - 1) a.cnt[l] = (int)min((size_t)r, a.cap);   // the last word closes the list
+        if (wd == TMW - 1) a.cnt[l] = (int)min((size_t)r, a.cap[l]);   // the last word closes the list
     }
     __syncthreads();
 
-    const size_t cap = a.cap;
+    const size_t cap = a.cap[l];
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
         if (nch > kChunksPerPass) {
@@ -397,8 +452,8 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             const int cc = pi >> 6, j = pi & 63;
             const int t = 64 * wd + j;
             uint64_t b = s_bal[cc][j];
-            if (t >= a.ntiles) continue;
-            const uint32_t pos = ((uint32_t)(t / a.TW) << 8) | (uint32_t)(t % a.TW);
+            if (t >= ntiles) continue;
+            const uint32_t pos = ((uint32_t)(t / TW) << 8) | (uint32_t)(t % TW);
             int idx = s_base[cc][j];
             while (b) {
                 const int k = __ffsll((long long)b) - 1;  // next stream of this position
@@ -437,14 +492,6 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
 // ascending within a position, as for streams.
 
 constexpr int kVarThreads = 1024;
-
-// Bits of the index range [x0, x1) that fall in 64-bit word wx.
-__device__ inline uint64_t range_bits(int x0, int x1, int wx) {
-    const int lo = max(x0 - 64 * wx, 0), hi = min(x1 - 64 * wx, 64);
-    if (hi <= lo) return 0ull;
-    const uint64_t upto = hi == 64 ? ~0ull : ((1ull << hi) - 1ull);
-    return upto & ~((1ull << lo) - 1ull);
-}
 
 __device__ inline int wave_sum(int v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -623,7 +670,9 @@ hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_compact(const CompactArgs &a, hipStream_t s) {
-    dim3 grid(a.TMW, a.L);
+    int tmw = 1;
+    for (int l = 1; l <= a.L; ++l) tmw = std::max(tmw, a.TMWl[l]);
+    dim3 grid(tmw, a.L);
     hipLaunchKernelGGL(k_compact_pos, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }

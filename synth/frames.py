@@ -28,7 +28,8 @@ class Workload:
     frames: int
     h: int
     w: int
-    convs: tuple                  # output channels of each 3x3 s1 p1 conv layer
+    convs: tuple                  # per conv layer: output channels (3x3, stride 1, pad 1)
+                                  # or (cout, k, stride, pad)
     n_out: int                    # logits
     n_sprites: int = 3
     smin: int = 4
@@ -47,20 +48,31 @@ class Workload:
         """(cin, cout, k, stride, pad) per conv layer."""
         specs = []
         cin = self.in_c
-        for cout in self.convs:
-            specs.append((cin, cout, 3, 1, 1))
+        for c in self.convs:
+            cout, k, s, p = tuple(c) if isinstance(c, (tuple, list)) else (c, 3, 1, 1)
+            specs.append((cin, cout, k, s, p))
             cin = cout
         return specs
 
+    def grids(self):
+        """(h, w) of the input and of each conv layer's output."""
+        g = [(self.h, self.w)]
+        for (_ci, _co, k, s, p) in self.conv_specs():
+            gh, gw = g[-1]
+            g.append(((gh + 2 * p - k) // s + 1, (gw + 2 * p - k) // s + 1))
+        return g
+
+    def channels(self):
+        return [self.in_c] + [sp[1] for sp in self.conv_specs()]
+
     def dense_in(self) -> int:
-        return self.convs[-1] * self.h * self.w
+        gh, gw = self.grids()[-1]
+        return self.conv_specs()[-1][1] * gh * gw
 
     def dense_macs_per_frame(self) -> int:
         m = 0
-        cin = self.in_c
-        for cout in self.convs:
-            m += self.h * self.w * cout * cin * 9
-            cin = cout
+        for (ci, co, k, _s, _p), (gh, gw) in zip(self.conv_specs(), self.grids()[1:]):
+            m += gh * gw * co * ci * k * k
         return m + self.n_out * self.dense_in()
 
 
@@ -79,6 +91,12 @@ WORKLOADS = {
         description="4096 occlusion variants (8x8 zero patch, 64x64 top-left grid) "
                     "of one 105x80 base, evaluated together against the base's caches",
         extra={"patch": 8, "grid": 64}),
+    "dqn-84x84-256x64": Workload(
+        cid=6, streams=256, frames=64, h=84, w=84,
+        convs=((32, 8, 4, 0), (64, 4, 2, 0), (64, 3, 1, 0)), n_out=6,
+        n_sprites=5, smin=3, smax=6, vmin=1, vmax=2, stack=4,
+        description="256 streams x 64 frames, 84x84, the last 4 frames stacked, conv 8x8/4 4->32, "
+                    "4x4/2 32->64, 3x3/1 64->64 (no padding), dense->6"),
     "stack4-512x64": Workload(
         cid=4, streams=512, frames=64, h=105, w=80, convs=(40, 80), n_out=6,
         n_sprites=6, smin=4, smax=8, vmin=1, vmax=3, stack=4,

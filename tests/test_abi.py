@@ -74,9 +74,28 @@ def test_workspace_bytes_valid_configs():
         _cfg(((1, 64), (64, 128), (128, 128)), h=210, w=160, n_out=18)) > 0
 
 
+def test_general_layer_configs():
+    # DQN-style trunk: 8x8 stride 4, 4x4 stride 2, 3x3 stride 1, no padding, 4 stacked frames.
+    specs = (B.rn_conv_spec * 3)(B.rn_conv_spec(4, 32, 8, 4, 0), B.rn_conv_spec(32, 64, 4, 2, 0),
+                                 B.rn_conv_spec(64, 64, 3, 1, 0))
+    def cfg(dtype=B.RN_F32, spec=specs, h=84, w=84):
+        c = B.rn_config(1, h, w, 4, 3, spec, 6, 4, 4, 8, dtype, B.RN_HEAD_TILES, 0)
+        c._keep = spec
+        return c
+    n = B.reuse_net_workspace_bytes(cfg())
+    # the caches follow the shrinking grids: 20x20x32 + 9x9x64 + 7x7x64 (tiled) per stream
+    assert n > 8 * (25 * 16 * 32 + 9 * 16 * 64 + 4 * 16 * 64) * 4
+    assert B.reuse_net_workspace_bytes(cfg(B.RN_BF16)) == 0             # general layers: float32 only
+    bad = (B.rn_conv_spec * 3)(B.rn_conv_spec(4, 32, 8, 3, 0), B.rn_conv_spec(32, 64, 4, 2, 0),
+                               B.rn_conv_spec(64, 64, 3, 1, 0))
+    assert B.reuse_net_workspace_bytes(cfg(spec=bad)) == 0              # stride 3
+    assert B.reuse_net_workspace_bytes(cfg(h=12, w=12)) == 0            # no output pixels left
+
+
 @pytest.mark.parametrize("bad", [
-    dict(k=2, p=0),                   # even kernel
-    dict(p=0),                        # pad != (k-1)/2
+    dict(k=2, p=0),                   # 2x2 kernel: no kernel for these shapes
+    dict(p=0),                        # 3x3 without padding: no kernel for 1->40
+    dict(p=2),                        # pad > (k-1)/2
     dict(s=0),                        # stride 0
     dict(convs=((1, 40), (32, 80))),  # broken channel chain
     dict(convs=()),                   # no layers
@@ -114,8 +133,10 @@ def _create(cfg, weights=True, ptr=256, nbytes=None):
 
 
 def test_create_reports_argument_errors_without_touching_the_gpu():
+    st, h, msg = _create(_cfg(p=2))
+    assert st == B.RN_EINVAL and h is None and "pad" in msg
     st, h, msg = _create(_cfg(k=2, p=0))
-    assert st == B.RN_EINVAL and h is None and "odd" in msg
+    assert st == B.RN_EUNSUPPORTED and h is None and "kernel" in msg
     st, h, msg = _create(_cfg(tile=8))
     assert st == B.RN_EUNSUPPORTED and "tile" in msg
     st, h, msg = _create(_cfg(), weights=False)
