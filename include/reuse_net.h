@@ -10,10 +10,13 @@
  * Sec. 3), and many independent streams (environments, cameras, occlusion
  * variants) are processed per launch.
  *
- * Network: n_conv 3x3 stride-1 pad-1 conv layers, each followed by bias and
- * ReLU, then a dense layer to n_out logits (Sec. 2: two conv layers and a
- * dense layer).  The dense input is the last conv output flattened in
- * (channel, row, column) order, as torch's NCHW .flatten(1).
+ * Network: n_conv conv layers, each followed by bias and ReLU, then a dense
+ * layer to n_out logits (Sec. 2: two conv layers and a dense layer).  The
+ * dense input is the last conv output flattened in (channel, row, column)
+ * order, as torch's NCHW .flatten(1).  A change spreads through a layer by its
+ * window (Fig. 1): output pixel (y, x) of a k x k layer with stride s and zero
+ * pad p changed iff an input pixel in rows s y - p .. s y - p + k - 1 and the
+ * same columns changed.
  *
  * Conventions
  *   - Every function returns an rn_status (0 = RN_OK, negative = error) unless
@@ -61,10 +64,15 @@ typedef enum { RN_F32 = 0, RN_BF16 = 1, RN_U8 = 2 } rn_dtype;
  *     every tile it recomputes, and the head adds the cached contributions in
  *     a fixed tile order.  Needs n_conv >= 2.
  *   RN_HEAD_FULL: the head reads the whole last-layer cache of every stream
- *     every step (split-K GEMV over C_L*H*W). */
+ *     every step (split-K GEMV over C_L*H_L*W_L). */
 typedef enum { RN_HEAD_TILES = 0, RN_HEAD_FULL = 1 } rn_head_mode;
 
-/* One conv layer (OIHW weights).  Supported: k = 3, stride = 1, pad = 1. */
+/* One conv layer (OIHW weights), output grid ((H + 2 pad - k) / stride + 1) per
+ * side.  Valid: k >= 1, stride >= 1, 0 <= pad <= (k - 1) / 2.  Kernels exist for
+ * 3x3 stride 1 pad 1 (float32 and bf16, the channel pairs listed in the design
+ * notes), and, float32 only, for k <= 8 with stride 1, 2 or 4 at the
+ * (k, stride, cin, cout) shapes of the general-layer kernel; other layers make
+ * reuse_net_create return RN_EUNSUPPORTED naming the shape. */
 typedef struct {
     int32_t cin, cout, k, stride, pad;
 } rn_conv_spec;

@@ -1,11 +1,14 @@
 // Dirty-tile convolution kernels (Sec. 1: recompute only where the change can
 // reach and reuse the cached activations elsewhere).
 //
-// Every conv layer is 3x3, stride 1, zero pad 1, then bias and ReLU:
-//   out[y][x][co] = ReLU(b[co] + sum_{ky,kx,ci} w[co][ci][ky][kx] * in[y-1+ky][x-1+kx][ci]).
-// Each work-list entry names one 4x4 output tile of one stream; the kernels
-// compute its 16 pixels x cout outputs from the 6x6 input halo and write them
-// in place into the stream's cache (scatter fused with bias and ReLU).
+// A conv layer is bias and ReLU after a k x k cross-correlation with stride s
+// and zero padding p:
+//   out[y][x][co] = ReLU(b[co] + sum_{ky,kx,ci} w[co][ci][ky][kx] * in[s y-p+ky][s x-p+kx][ci]).
+// Most kernels here are for 3x3, stride 1, pad 1 (6x6 input halo per tile); the
+// general-layer kernel k_conv_gen takes other k and s.  Each work-list entry
+// names one 4x4 output tile of one stream; the kernels compute its 16 pixels x
+// cout outputs and write them in place into the stream's cache (scatter fused
+// with bias and ReLU).
 // Pixels of a ragged edge tile that fall outside the image are written as 0:
 // they are the next layer's zero padding and carry zero dense weights.
 //
@@ -707,7 +710,10 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
 // zero A values.  The patch sits in LDS channel-innermost; the weights,
 // packed [block][n-block][lane][j], stream from global memory (the same few
 // hundred KB for every wave, served by L1/L2), one 16-byte load per lane and
-// n-block, a block ahead of their use.  One wave per tile, four waves per block;
+// n-block, three blocks ahead of their use (a ring of three register sets
+// with fixed roles, the loop unrolled by three).  One wave per tile, eight
+// waves per block (two per SIMD, so one wave's patch loads overlap the other's
+// matrix work);
 // the epilogue is the one of the 3x3 kernels (bias, ReLU, zero outside the
 // output grid, tile head partials on the last layer, cache store).
 // FIRST: the input is the float32 input cache (planar, a ring of 4 frames when
@@ -716,12 +722,13 @@ template <int KS, int ST, int CIN, int COUT>
 struct Gen {
     static constexpr int E = 3 * ST + KS;
     static constexpr int KT = KS * KS * CIN;
-    static constexpr int NBLK = (KT + 15) / 16;
+    static constexpr int NBLK = ((KT + 15) / 16 + 2) / 3 * 3;   // 16-K blocks, padded to whole triples
     static constexpr int NB = COUT / 16;
     static constexpr int HALO = E * E * CIN;
     static constexpr int STAGE = 16 * Epi<COUT>::SR;
     static constexpr int AREA = HALO > STAGE ? HALO : STAGE;   // floats per wave
-    static constexpr size_t lds_bytes = (size_t)4 * AREA * sizeof(float);
+    static constexpr int WAVES = 8;
+    static constexpr size_t lds_bytes = (size_t)WAVES * AREA * sizeof(float);
     static_assert(COUT % 16 == 0, "16-column blocks");
 };
 
@@ -795,7 +802,7 @@ __device__ inline float4 gen_a(const float *halo, int b, int kq, int py, int px)
 }
 
 template <int KS, int ST, int CIN, int COUT, bool DENSE, bool FIRST>
-__global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
+__global__ __launch_bounds__(512) void k_conv_gen(ConvArgs a) {
     using G = Gen<KS, ST, CIN, COUT>;
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
@@ -805,7 +812,7 @@ __global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
     float *halo = smem + wave * G::AREA;
     const floatx4 *wg = static_cast<const floatx4 *>(a.w);
     const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, 4);
+    const XcdRange xr = xcd_range(cnt, G::WAVES);
     const int m = lane & 15, kq = lane >> 4;
     const int py = m & 3, px = m >> 2;
     for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
@@ -815,24 +822,35 @@ __global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
         floatx4 acc[G::NB];
 #pragma unroll
         for (int nb = 0; nb < G::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        floatx4 bc[G::NB], bn[G::NB];           // ext-vector arrays stay in registers
+        // Weight ring: block b's fragments live in set b % 3 (ext-vector arrays stay in registers).
+        floatx4 w0[G::NB], w1[G::NB], w2[G::NB];
+        // Every fetch is issued (past the end: the last block again, never used),
+        // so each wait names exactly the loads it needs.
+        auto fetch = [&](floatx4 *dst, int b) __attribute__((always_inline)) {
+            const int bb = b < G::NBLK ? b : G::NBLK - 1;
 #pragma unroll
-        for (int nb = 0; nb < G::NB; ++nb) bc[nb] = wg[nb * 64 + lane];
-        for (int b = 0; b < G::NBLK; ++b) {
-            if (b + 1 < G::NBLK) {
-#pragma unroll
-                for (int nb = 0; nb < G::NB; ++nb) bn[nb] = wg[((b + 1) * G::NB + nb) * 64 + lane];
-            }
+            for (int nb = 0; nb < G::NB; ++nb) dst[nb] = wg[(bb * G::NB + nb) * 64 + lane];
+        };
+        auto block = [&](floatx4 *w, int b) __attribute__((always_inline)) {
             const float4 av = gen_a<KS, ST, CIN, COUT>(halo, b, kq, py, px);
             const float al[4] = {av.x, av.y, av.z, av.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int nb = 0; nb < G::NB; ++nb) {
-                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], bc[nb][j], acc[nb], 0, 0, 0);
-                }
-#pragma unroll
-            for (int nb = 0; nb < G::NB; ++nb) bc[nb] = bn[nb];
+                for (int nb = 0; nb < G::NB; ++nb)
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], w[nb][j], acc[nb], 0, 0, 0);
+        };
+        fetch(w0, 0);
+        fetch(w1, 1);
+        fetch(w2, 2);
+#pragma unroll 1
+        for (int b = 0; b < G::NBLK; b += 3) {
+            block(w0, b);
+            fetch(w0, b + 3);
+            block(w1, b + 1);
+            fetch(w1, b + 4);
+            block(w2, b + 2);
+            fetch(w2, b + 5);
         }
         wave_sync();
         epilogue<COUT, -1, false>(a, r, acc, s_bias, halo, lane, t);
@@ -911,8 +929,8 @@ hipError_t run_gen(const ConvArgs &a, int cus, hipStream_t s) {
     static hipError_t attr2 = set_lds(k_conv_gen<KS, ST, CIN, COUT, false, FIRST>, G::lds_bytes);
     if (attr != hipSuccess) return attr;
     if (attr2 != hipSuccess) return attr2;
-    const int grid = persistent_grid(cus * 4, (a.max_tiles + 3) / 4);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), G::lds_bytes, s, a);
+    const int grid = persistent_grid(cus * 2, (a.max_tiles + G::WAVES - 1) / G::WAVES);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * G::WAVES), G::lds_bytes, s, a);
     return hipGetLastError();
 }
 #define RN_FIRST_SHAPES(X) X(1, 20) X(1, 40) X(1, 64) X(1, 80) X(4, 20) X(4, 40) X(4, 64) X(4, 80)
@@ -946,15 +964,15 @@ hipError_t launch_conv_gen(const ConvArgs &a, int k, int s, bool first, int cus,
     return hipErrorInvalidValue;
 }
 
-size_t conv_gen_packed_elems(int k, int cin, int cout) {
-    const int kt = k * k * cin;
-    return (size_t)((kt + 15) / 16) * 16 * cout;
-}
+// 16-K blocks of a general layer, padded to whole triples (the kernel's ring).
+static int gen_blocks(int k, int cin) { return ((k * k * cin + 15) / 16 + 2) / 3 * 3; }
+
+size_t conv_gen_packed_elems(int k, int cin, int cout) { return (size_t)gen_blocks(k, cin) * 16 * cout; }
 
 void pack_conv_gen(const float *oihw, int k, int cin, int cout, float *dst) {
     // [block][n-block][lane][j]: K = 16 block + 4 (lane / 16) + j in (ky, kx, c)
     // order, n = 16 n-block + lane % 16; zero past K = k k cin.
-    const int kt = k * k * cin, nblk = (kt + 15) / 16, nbn = cout / 16;
+    const int kt = k * k * cin, nblk = gen_blocks(k, cin), nbn = cout / 16;
     size_t o = 0;
     for (int b = 0; b < nblk; ++b)
         for (int nb = 0; nb < nbn; ++nb)
