@@ -212,6 +212,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=None)
     ap.add_argument("--head", default="tiles", choices=["tiles", "full"])
+    ap.add_argument("--update-every", type=int, default=0,
+                    help="training rollouts: replace the weights every N steps (inside the timed "
+                         "region; every slot then recomputes everything on its next step)")
     ap.add_argument("--separate-first", action="store_true",
                     help="run layer 1 as its own kernel instead of inside layer 2")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -256,11 +259,21 @@ def main():
     out = torch.empty((S, wl.n_out), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
+    alt_weights = [weights, synth.net_weights(wl, seed_extra=1)] if args.update_every else None
+
     def do_step(k):
+        if args.update_every and k % args.update_every == 0 and k > 0:
+            net.set_weights(alt_weights[(k // args.update_every) % 2])
         drv.reuse_step(net, k, out)
 
+    def restart():
+        # every pass starts from the first weight set, primed on the first frames
+        if args.update_every:
+            net.set_weights(weights)
+        drv.prime(net, out)
+
     # Stats pass: dirty tiles of exactly the steps the timed pass will run.
-    drv.prime(net, out)
+    restart()
     stats = []
     for k in range(length):
         do_step(k)
@@ -268,7 +281,7 @@ def main():
     timed_stats = stats[args.warmup:]
 
     def run_reuse(profile: bool):
-        drv.prime(net, out)
+        restart()
         for k in range(args.warmup):
             do_step(k)
         torch.cuda.synchronize()
@@ -376,6 +389,8 @@ def main():
            "stack": wl.stack, "description": wl.description}
     if args.change_frac is not None:
         cfg["change_preset"] = args.change_frac
+    if args.update_every:
+        cfg["weight_update_every"] = args.update_every
     line = {
         "metric": drv.metric,
         "value": fps,

@@ -161,6 +161,16 @@ rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *dev_stream_id
  * everything.  Synchronises the last step's stream. */
 rn_status reuse_net_reset(reuse_net *net, int32_t stream_id);
 
+/* Replace the weights (training between rollouts: activations are reused
+ * within a rollout whose weights are fixed, Sec. 1 and Sec. 2).  Same layout,
+ * packing and host pointers as reuse_net_create.  Waits for the last step's
+ * stream, uploads on hip_stream, marks every slot unprimed (the caches hold
+ * activations of the old weights, so each slot's next step recomputes
+ * everything; with stacked frames the frame ring restarts as at an episode
+ * start, the next frame standing for the older ones) and synchronises
+ * hip_stream.  On an argument error nothing changes. */
+rn_status reuse_net_set_weights(reuse_net *net, const rn_weights *w, void *hip_stream);
+
 /* ---- variants of one slot: copy-on-write overlays (Sec. 1, known change) ---- */
 
 /* Device scratch bytes reuse_net_variants needs for n variants when no variant

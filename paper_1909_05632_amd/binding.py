@@ -33,6 +33,7 @@ EXPORTS = (
     "reuse_net_get_worklist", "reuse_net_read_activation", "reuse_net_get_stats",
     "reuse_net_set_profiling", "reuse_net_get_profile", "reuse_net_last_error",
     "reuse_net_destroy", "reuse_net_variant_scratch_bytes", "reuse_net_variants",
+    "reuse_net_set_weights",
 )
 
 
@@ -91,6 +92,8 @@ def load_library(path: str = LIB_PATH):
     L.reuse_net_full.argtypes = [P, I32, P, P, ctypes.c_int, P, P]
     L.reuse_net_reset.restype = st
     L.reuse_net_reset.argtypes = [P, I32]
+    L.reuse_net_set_weights.restype = st
+    L.reuse_net_set_weights.argtypes = [P, ctypes.POINTER(rn_weights), P]
     L.reuse_net_variant_scratch_bytes.restype = SZ
     L.reuse_net_variant_scratch_bytes.argtypes = [P, I32, I32]
     L.reuse_net_variants.restype = st
@@ -156,6 +159,10 @@ def reuse_net_full(net: int, n: int, dev_stream_ids: int, dev_frames: int, frame
 
 def reuse_net_reset(net: int, stream_id: int) -> None:
     _check(load_library().reuse_net_reset(net, stream_id), net)
+
+
+def reuse_net_set_weights(net: int, weights: rn_weights, hip_stream: int) -> None:
+    _check(load_library().reuse_net_set_weights(net, ctypes.byref(weights), hip_stream), net)
 
 
 def reuse_net_variant_scratch_bytes(net: int, n: int, max_tiles: int) -> int:
@@ -266,19 +273,30 @@ class ReuseNet:
             _check(load_library().reuse_net_create(ctypes.byref(self.cfg), None, None, 0, None,
                                                    ctypes.byref(ctypes.c_void_p())))
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
-        conv_w, conv_b, dense_w, dense_b = weights
-        self._host = [np.ascontiguousarray(a, dtype=np.float32) for a in (*conv_w, *conv_b, dense_w, dense_b)]
-        L = len(specs)
-        cw = (ctypes.c_void_p * L)(*[a.ctypes.data for a in self._host[:L]])
-        cb = (ctypes.c_void_p * L)(*[a.ctypes.data for a in self._host[L:2 * L]])
-        wts = rn_weights(cw, cb, self._host[2 * L].ctypes.data, self._host[2 * L + 1].ctypes.data)
+        keep, wts = self._weights(weights)
         stream = torch.cuda.current_stream(self.device).cuda_stream
         self.handle = reuse_net_create(self.cfg, wts, self.workspace.data_ptr(), nbytes, stream)
-        self._host = None
+        del keep
         self.words_per_row = -(-w // 64)
         self.tiles = (-(-h // tile), -(-w // tile))
         self.tile_words = -(-(self.tiles[0] * self.tiles[1]) // 64)
         self.layer_tiles = [(-(-gh // tile), -(-gw // tile)) for gh, gw in self.grids]
+
+    def _weights(self, weights):
+        """rn_weights over contiguous float32 host copies (kept alive by the returned list)."""
+        conv_w, conv_b, dense_w, dense_b = weights
+        host = [np.ascontiguousarray(a, dtype=np.float32) for a in (*conv_w, *conv_b, dense_w, dense_b)]
+        L = len(self.specs)
+        cw = (ctypes.c_void_p * L)(*[a.ctypes.data for a in host[:L]])
+        cb = (ctypes.c_void_p * L)(*[a.ctypes.data for a in host[L:2 * L]])
+        return [host, cw, cb], rn_weights(cw, cb, host[2 * L].ctypes.data, host[2 * L + 1].ctypes.data)
+
+    def set_weights(self, weights, stream=None):
+        """New weights (same shapes); every slot recomputes everything on its next step."""
+        keep, wts = self._weights(weights)
+        s = (stream or self.torch.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_set_weights(self.handle, wts, s)
+        del keep
 
     # -- hot path
     def _frames(self, frames):

@@ -726,65 +726,10 @@ rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     return RN_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t reuse_net_workspace_bytes(const rn_config *cfg) {
-    Plan p;
-    std::string err;
-    if (plan_config(cfg, &p, &err) != RN_OK) return 0;
-    return p.total;
-}
-
-rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_workspace, size_t bytes,
-                           void *hip_stream, reuse_net **out) {
-    g_create_error.clear();
-    if (!out) {
-        g_create_error = "out is NULL";
-        return RN_EINVAL;
-    }
-    *out = nullptr;
-    Plan p;
-    rn_status st = plan_config(cfg, &p, &g_create_error);
-    if (st != RN_OK) return st;
-    if (!w || !w->conv_w || !w->conv_b || !w->dense_w || !w->dense_b) {
-        g_create_error = "weights are NULL";
-        return RN_EINVAL;
-    }
-    for (int l = 0; l < p.L; ++l)
-        if (!w->conv_w[l] || !w->conv_b[l]) {
-            g_create_error = "conv weights of layer " + std::to_string(l + 1) + " are NULL";
-            return RN_EINVAL;
-        }
-    if (!dev_workspace) {
-        g_create_error = "workspace is NULL";
-        return RN_EINVAL;
-    }
-    if (reinterpret_cast<uintptr_t>(dev_workspace) % kAlign) {
-        g_create_error = "workspace must be 256-byte aligned";
-        return RN_EINVAL;
-    }
-    if (bytes < p.total) {
-        g_create_error = "workspace too small: need " + std::to_string(p.total) + " bytes";
-        return RN_ENOSPACE;
-    }
-    reuse_net *net = new reuse_net();
-    net->p = p;
-    net->cfg = *cfg;
-    net->cfg.conv = nullptr;
-    net->ws = static_cast<char *>(dev_workspace);
-    int dev = 0;
-    hipDeviceProp_t prop;
-    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
-        net->cus = std::max(1, prop.multiProcessorCount);
-    hipStream_t s = static_cast<hipStream_t>(hip_stream);
-
-    // Host-side images of the constant parts.
-    std::vector<float> lut(256);
-    for (int k = 0; k < 256; ++k) lut[k] = (float)k / 255.0f;   // IEEE division: correctly rounded
-    std::vector<int32_t> ids(p.S);
-    for (int i = 0; i < p.S; ++i) ids[i] = i;
+// Pack the weights into the kernels' layouts on the host and enqueue their
+// upload on s (weights, biases, dense weights, tile-head weights).
+hipError_t upload_weights(reuse_net *net, const rn_weights *w, hipStream_t s) {
+    const Plan &p = net->p;
     const bool bf = p.dt == RN_BF16;
     auto rnd = [&](float v) { return bf ? round_bf16_host(v) : v; };
     std::vector<std::vector<unsigned char>> wpack(p.L);
@@ -815,13 +760,10 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
                     for (int c = 0; c < CL; ++c)
                         wd[dst + c] = rnd(w->dense_w[(size_t)o * CL * HL * WL + ((size_t)c * HL + y) * WL + x]);
                 }
-
-    hipError_t e = hipMemsetAsync(dev_workspace, 0, p.total, s);
+    hipError_t e = hipSuccess;
     auto up = [&](size_t off, const void *src, size_t n) {
         if (e == hipSuccess) e = hipMemcpyAsync(net->ws + off, src, n, hipMemcpyHostToDevice, s);
     };
-    up(p.o_lut, lut.data(), 256 * 4);
-    up(p.o_ids, ids.data(), (size_t)p.S * 4);
     for (int l = 0; l < p.L; ++l) {
         up(p.o_w[l], wpack[l].data(), p.w_bytes[l]);
         up(p.o_b[l], w->conv_b[l], (size_t)p.C[l + 1] * 4);
@@ -840,6 +782,81 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
         up(p.o_hw, hw.data(), hw.size() * 4);
     }
     up(p.o_bd, w->dense_b, (size_t)p.N * 4);
+    // pageable host buffers: the copies are done with the vectors before they go
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    return e;
+}
+
+// NULL checks of a weight set (message in *err).
+rn_status check_weights(const Plan &p, const rn_weights *w, std::string *err) {
+    if (!w || !w->conv_w || !w->conv_b || !w->dense_w || !w->dense_b) {
+        *err = "weights are NULL";
+        return RN_EINVAL;
+    }
+    for (int l = 0; l < p.L; ++l)
+        if (!w->conv_w[l] || !w->conv_b[l]) {
+            *err = "conv weights of layer " + std::to_string(l + 1) + " are NULL";
+            return RN_EINVAL;
+        }
+    return RN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t reuse_net_workspace_bytes(const rn_config *cfg) {
+    Plan p;
+    std::string err;
+    if (plan_config(cfg, &p, &err) != RN_OK) return 0;
+    return p.total;
+}
+
+rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_workspace, size_t bytes,
+                           void *hip_stream, reuse_net **out) {
+    g_create_error.clear();
+    if (!out) {
+        g_create_error = "out is NULL";
+        return RN_EINVAL;
+    }
+    *out = nullptr;
+    Plan p;
+    rn_status st = plan_config(cfg, &p, &g_create_error);
+    if (st != RN_OK) return st;
+    st = check_weights(p, w, &g_create_error);
+    if (st != RN_OK) return st;
+    if (!dev_workspace) {
+        g_create_error = "workspace is NULL";
+        return RN_EINVAL;
+    }
+    if (reinterpret_cast<uintptr_t>(dev_workspace) % kAlign) {
+        g_create_error = "workspace must be 256-byte aligned";
+        return RN_EINVAL;
+    }
+    if (bytes < p.total) {
+        g_create_error = "workspace too small: need " + std::to_string(p.total) + " bytes";
+        return RN_ENOSPACE;
+    }
+    reuse_net *net = new reuse_net();
+    net->p = p;
+    net->cfg = *cfg;
+    net->cfg.conv = nullptr;
+    net->ws = static_cast<char *>(dev_workspace);
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
+        net->cus = std::max(1, prop.multiProcessorCount);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+    // Host-side images of the constant parts.
+    std::vector<float> lut(256);
+    for (int k = 0; k < 256; ++k) lut[k] = (float)k / 255.0f;   // IEEE division: correctly rounded
+    std::vector<int32_t> ids(p.S);
+    for (int i = 0; i < p.S; ++i) ids[i] = i;
+    hipError_t e = hipMemsetAsync(dev_workspace, 0, p.total, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(net->ws + p.o_lut, lut.data(), 256 * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(net->ws + p.o_ids, ids.data(), (size_t)p.S * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = upload_weights(net, w, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         g_create_error = std::string("upload: ") + hipGetErrorString(e);
@@ -871,6 +888,22 @@ rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, con
                              void *scratch, size_t scratch_bytes, float *logits, void *stream) {
     return run_variants(net, base_stream, n, frames, fdt, frame_count, boxes, box_off, max_tiles, scratch,
                         scratch_bytes, logits, stream);
+}
+
+rn_status reuse_net_set_weights(reuse_net *net, const rn_weights *w, void *hip_stream) {
+    if (!net) return RN_EINVAL;
+    rn_status st = check_weights(net->p, w, &net->err);
+    if (st != RN_OK) return st;
+    st = sync_last(net);                     // no step may still read the old weights
+    if (st != RN_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    hipError_t e = upload_weights(net, w, s);
+    // Every cache now holds activations of the old weights: all slots unprimed.
+    if (e == hipSuccess) e = hipMemsetAsync(net->at<int32_t>(net->p.o_primed), 0, (size_t)net->p.S * 4, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("weight upload: ") + hipGetErrorString(e));
+    net->err.clear();
+    return RN_OK;
 }
 
 rn_status reuse_net_reset(reuse_net *net, int32_t sid) {
