@@ -32,19 +32,26 @@ __device__ inline float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h <<
 
 // Direct conv for a few input channels; the input is rounded to bf16 as it is
 // staged, the weights arrive rounded, the output is rounded and stored as bf16.
-// VAR: variant tiles (input from the base slot and the variant's frame, output
-// to the work item's overlay row).
+// Lane l owns output channels l, l + 64 (weights in registers); the halo is
+// read once from LDS into every lane's registers (the layout of the float32
+// first-layer kernel).  VAR: variant tiles (input from the base slot and the
+// variant's frame, output to the work item's overlay row).
 template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
-    __shared__ float s_w[CIN * 9 * COUT];
-    __shared__ float s_b[COUT];
-    __shared__ float s_halo[4][CIN * 36];
-    const float *wg = static_cast<const float *>(a.w);
-    for (int j = threadIdx.x; j < CIN * 9 * COUT; j += blockDim.x) s_w[j] = wg[j];
-    for (int j = threadIdx.x; j < COUT; j += blockDim.x) s_b[j] = a.bias[j];
-    __syncthreads();
-
+    constexpr int CPL = (COUT + 63) / 64;
+    constexpr int HN = 36 * CIN;
+    __shared__ float s_halo[4][HN];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float *wg = static_cast<const float *>(a.w);
+    float wr[CPL][CIN * 9], br[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        const int co = min(lane + 64 * j, COUT - 1);
+#pragma unroll
+        for (int k = 0; k < CIN * 9; ++k) wr[j][k] = wg[k * COUT + co];
+        br[j] = a.bias[co];
+    }
+
     const int cnt = work_count<DENSE>(a);
     const size_t HW = (size_t)a.H * a.W;
     const int cin1 = CIN / a.stack;
@@ -52,17 +59,23 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
     const float *xin = static_cast<const float *>(a.in);
     uint16_t *outp = static_cast<uint16_t *>(a.out);
 
+    // The halo values of the next tile (past the end: the last tile again,
+    // never used) are loaded into registers, HPL per lane, before this tile's
+    // FMAs, so their latency overlaps the arithmetic.
+    constexpr int HPL = (HN + 63) / 64;
     const XcdRange xr = xcd_range(cnt, 4);
-    for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
+    auto load_tile = [&](int t, float *pv) __attribute__((always_inline)) {
         const TileRef r = decode<DENSE>(a, t);
         int head = 0;
         if (!VAR && a.stack != 1) head = a.ring_head[r.slot];
-        for (int h = lane; h < CIN * 36; h += 64) {
+#pragma unroll
+        for (int k = 0; k < HPL; ++k) {
+            const int h = lane + 64 * k;
             const int c = h / 36, pos = h - c * 36;
             const int hy = pos / 6, hx = pos - hy * 6;
             const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
             float v = 0.0f;
-            if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
+            if (h < HN && y >= 0 && y < a.H && x >= 0 && x < a.W) {
                 if constexpr (VAR) {
                     v = bf2f(f2bf(var_input(a, r.slot, c, y, x)));
                 } else {
@@ -70,6 +83,7 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
                     if (a.stack == 1) {
                         plane = xin + ((size_t)r.slot * CIN + c) * HW;
                     } else {
+                        // Channel c = frame j (oldest first) of the ring, channel c1 of it.
                         const int j = c / cin1, c1 = c - j * cin1;
                         const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
                         plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
@@ -77,29 +91,68 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
                     v = bf2f(f2bf(plane[(size_t)y * a.W + x]));
                 }
             }
-            halo[h] = v;
+            pv[k] = v;
+        }
+    };
+    int t = xr.first + wave;
+    if (t >= xr.end) return;
+    float pv[HPL];
+    load_tile(t, pv);
+    for (; t < xr.end; t += xr.stride) {
+        const TileRef r = decode<DENSE>(a, t);
+#pragma unroll
+        for (int k = 0; k < HPL; ++k) {
+            const int h = lane + 64 * k;
+            if (h < HN) {
+                const int c = h / 36, pos = h - c * 36;
+                halo[pos * CIN + c] = pv[k];
+            }
         }
         wave_sync();
+        // One output row at a time: its three halo rows (18 pixels x CIN,
+        // contiguous in LDS) go to registers by broadcast reads.
+        float hr[18 * CIN];
+        load_tile(min(t + xr.stride, xr.end - 1), pv);
         uint16_t *dst = VAR ? static_cast<uint16_t *>(a.vov_out) + (size_t)t * kTilePx * COUT
                             : outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
-        for (int o = lane; o < kTilePx * COUT; o += 64) {
-            const int m = o / COUT, co = o - m * COUT;
-            const int py = m >> 2, px = m & 3;
-            float acc = 0.0f;
 #pragma unroll
-            for (int c = 0; c < CIN; ++c)
+        for (int py = 0; py < kTile; ++py) {
+            if constexpr (CIN % 4 == 0) {
 #pragma unroll
-                for (int ky = 0; ky < 3; ++ky)
+                for (int q = 0; q < 18 * CIN / 4; ++q) {
+                    const float4 v4 = reinterpret_cast<const float4 *>(halo + py * 6 * CIN)[q];
+                    hr[4 * q] = v4.x;
+                    hr[4 * q + 1] = v4.y;
+                    hr[4 * q + 2] = v4.z;
+                    hr[4 * q + 3] = v4.w;
+                }
+            } else {
 #pragma unroll
-                    for (int kx = 0; kx < 3; ++kx)
-                        acc = fmaf(s_w[(c * 9 + ky * 3 + kx) * COUT + co],
-                                   halo[c * 36 + (py + ky) * 6 + px + kx], acc);
-            float v = acc + s_b[co];
-            v = v > 0.0f ? v : 0.0f;
-            if (r.ty * kTile + py >= a.H || r.tx * kTile + px >= a.W) v = 0.0f;
-            dst[o] = f2bf(v);
+                for (int q = 0; q < 18 * CIN; ++q) hr[q] = halo[py * 6 * CIN + q];
+            }
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                const int co = lane + 64 * j;
+                if (co >= COUT) continue;
+#pragma unroll
+                for (int px = 0; px < kTile; ++px) {
+                    const int m = py * kTile + px;
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < CIN; ++c)
+#pragma unroll
+                        for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+                            for (int kx = 0; kx < 3; ++kx)
+                                acc = fmaf(wr[j][c * 9 + ky * 3 + kx], hr[(ky * 6 + px + kx) * CIN + c], acc);
+                    float v = acc + br[j];
+                    v = v > 0.0f ? v : 0.0f;
+                    if (r.ty * kTile + py >= a.H || r.tx * kTile + px >= a.W) v = 0.0f;
+                    dst[m * COUT + co] = f2bf(v);
+                }
+            }
         }
-        wave_sync();
+        wave_sync();                                   // halo reads done before the next tile's writes
     }
 }
 
