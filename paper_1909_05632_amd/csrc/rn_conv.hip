@@ -767,9 +767,11 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
 // packed [block][n-block][lane][j], stream from global memory (the same few
 // hundred KB for every wave, served by L1/L2), one 16-byte load per lane and
 // n-block, three blocks ahead of their use (a ring of three register sets
-// with fixed roles, the loop unrolled by three).  One wave per tile, eight
-// waves per block (two per SIMD, so one wave's patch loads overlap the other's
-// matrix work);
+// with fixed roles, the loop unrolled by three).  A block of four waves works
+// on one tile at a time and splits its K blocks four ways (these layers have
+// few tiles on their small grids, so a launch lasts about one tile's latency);
+// the four partial products are added in LDS in wave order and wave 0 runs
+// the epilogue;
 // the epilogue is the one of the 3x3 kernels (bias, ReLU, zero outside the
 // output grid, tile head partials on the last layer, cache store).
 // FIRST: the input is the float32 input cache (planar, a ring of 4 frames when
@@ -778,18 +780,21 @@ template <int KS, int ST, int CIN, int COUT>
 struct Gen {
     static constexpr int E = 3 * ST + KS;
     static constexpr int KT = KS * KS * CIN;
-    static constexpr int NBLK = ((KT + 15) / 16 + 2) / 3 * 3;   // 16-K blocks, padded to whole triples
+    static constexpr int KSPLIT = 4;                             // waves per tile, each a quarter of K
+    static constexpr int NBLK = ((KT + 15) / 16 + 11) / 12 * 12;  // 16-K blocks, padded to 4 x whole triples
+    static constexpr int NBW = NBLK / KSPLIT;                    // blocks per wave
     static constexpr int NB = COUT / 16;
     static constexpr int HALO = E * E * CIN;
     static constexpr int STAGE = 16 * Epi<COUT>::SR;
     static constexpr int AREA = HALO > STAGE ? HALO : STAGE;   // floats per wave
-    static constexpr int WAVES = 8;
-    static constexpr size_t lds_bytes = (size_t)WAVES * AREA * sizeof(float);
+    static constexpr int PART = (KSPLIT - 1) * NB * 64 * 4;     // partial products of waves 1..3
+    static constexpr size_t lds_bytes = (size_t)(AREA + PART) * sizeof(float);
     static_assert(COUT % 16 == 0, "16-column blocks");
 };
 
+// Threads idx, idx + nt, ... of the block load the patch of tile r.
 template <int KS, int ST, int CIN, int COUT, bool FIRST>
-__device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float *halo, int lane) {
+__device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float *halo, int idx, int nt) {
     using G = Gen<KS, ST, CIN, COUT>;
     const int y0 = 4 * ST * r.ty - a.pad, x0 = 4 * ST * r.tx - a.pad;
     if constexpr (FIRST) {
@@ -797,7 +802,7 @@ __device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float
         const size_t HW = (size_t)a.Hin * a.Win;
         const int cin1 = CIN / a.stack;
         const int head = a.stack != 1 ? a.ring_head[r.slot] : 0;
-        for (int h = lane; h < G::HALO; h += 64) {
+        for (int h = idx; h < G::HALO; h += nt) {
             const int c = h / (G::E * G::E), pos = h - c * (G::E * G::E);
             const int hy = pos / G::E, hx = pos - hy * G::E;
             const int y = y0 + hy, x = x0 + hx;
@@ -819,7 +824,7 @@ __device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float
         static_assert(CIN % 4 == 0, "cache layers carry whole 16-byte channel groups");
         constexpr int C4 = CIN / 4;
         const float *src = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
-        for (int h = lane; h < G::E * G::E * C4; h += 64) {
+        for (int h = idx; h < G::E * G::E * C4; h += nt) {
             const int pos = h / C4, c4 = h - pos * C4;
             const int hy = pos / G::E, hx = pos - hy * G::E;
             const int y = y0 + hy, x = x0 + hx;
@@ -858,32 +863,32 @@ __device__ inline float4 gen_a(const float *halo, int b, int kq, int py, int px)
 }
 
 template <int KS, int ST, int CIN, int COUT, bool DENSE, bool FIRST>
-__global__ __launch_bounds__(512) void k_conv_gen(ConvArgs a) {
+__global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
     using G = Gen<KS, ST, CIN, COUT>;
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
-    __syncthreads();
-    float *halo = smem + wave * G::AREA;
+    float *halo = smem;                                   // patch, then the epilogue's staging
+    floatx4 *part = reinterpret_cast<floatx4 *>(smem + G::AREA);
     const floatx4 *wg = static_cast<const floatx4 *>(a.w);
     const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, G::WAVES);
+    const XcdRange xr = xcd_range(cnt, 1);
     const int m = lane & 15, kq = lane >> 4;
     const int py = m & 3, px = m >> 2;
-    for (int t = xr.first + wave; t < xr.end; t += xr.stride) {
+    const int b0 = wave * G::NBW;                         // this wave's K blocks [b0, b0 + NBW)
+    for (int t = xr.first; t < xr.end; t += xr.stride) {  // uniform per block
         const TileRef r = decode<DENSE>(a, t);
-        gen_load_patch<KS, ST, CIN, COUT, FIRST>(a, r, halo, lane);
-        wave_sync();
+        __syncthreads();                                  // the previous tile's epilogue is done with the area
+        gen_load_patch<KS, ST, CIN, COUT, FIRST>(a, r, halo, tid, (int)blockDim.x);
+        __syncthreads();
         floatx4 acc[G::NB];
 #pragma unroll
         for (int nb = 0; nb < G::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        // Weight ring: block b's fragments live in set b % 3 (ext-vector arrays stay in registers).
+        // Weight ring: block b's fragments live in set (b - b0) % 3 (ext-vector arrays stay in registers).
         floatx4 w0[G::NB], w1[G::NB], w2[G::NB];
-        // Every fetch is issued (past the end: the last block again, never used),
-        // so each wait names exactly the loads it needs.
         auto fetch = [&](floatx4 *dst, int b) __attribute__((always_inline)) {
-            const int bb = b < G::NBLK ? b : G::NBLK - 1;
+            const int bb = b < b0 + G::NBW ? b : b0 + G::NBW - 1;   // past this wave's range: unused
 #pragma unroll
             for (int nb = 0; nb < G::NB; ++nb) dst[nb] = wg[(bb * G::NB + nb) * 64 + lane];
         };
@@ -896,11 +901,11 @@ __global__ __launch_bounds__(512) void k_conv_gen(ConvArgs a) {
                 for (int nb = 0; nb < G::NB; ++nb)
                     acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], w[nb][j], acc[nb], 0, 0, 0);
         };
-        fetch(w0, 0);
-        fetch(w1, 1);
-        fetch(w2, 2);
+        fetch(w0, b0);
+        fetch(w1, b0 + 1);
+        fetch(w2, b0 + 2);
 #pragma unroll 1
-        for (int b = 0; b < G::NBLK; b += 3) {
+        for (int b = b0; b < b0 + G::NBW; b += 3) {
             block(w0, b);
             fetch(w0, b + 3);
             block(w1, b + 1);
@@ -908,8 +913,18 @@ __global__ __launch_bounds__(512) void k_conv_gen(ConvArgs a) {
             block(w2, b + 2);
             fetch(w2, b + 5);
         }
-        wave_sync();
-        epilogue<COUT, -1, false>(a, r, acc, s_bias, halo, lane, t);
+        if (wave > 0) {
+#pragma unroll
+            for (int nb = 0; nb < G::NB; ++nb) part[((wave - 1) * G::NB + nb) * 64 + lane] = acc[nb];
+        }
+        __syncthreads();
+        if (wave == 0) {
+#pragma unroll
+            for (int w = 0; w < G::KSPLIT - 1; ++w)
+#pragma unroll
+                for (int nb = 0; nb < G::NB; ++nb) acc[nb] += part[(w * G::NB + nb) * 64 + lane];
+            epilogue<COUT, -1, false>(a, r, acc, s_bias, halo, lane, t);
+        }
     }
 }
 
@@ -985,8 +1000,8 @@ hipError_t run_gen(const ConvArgs &a, int cus, hipStream_t s) {
     static hipError_t attr2 = set_lds(k_conv_gen<KS, ST, CIN, COUT, false, FIRST>, G::lds_bytes);
     if (attr != hipSuccess) return attr;
     if (attr2 != hipSuccess) return attr2;
-    const int grid = persistent_grid(cus * 2, (a.max_tiles + G::WAVES - 1) / G::WAVES);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * G::WAVES), G::lds_bytes, s, a);
+    const int grid = persistent_grid(cus * 4, a.max_tiles);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * G::KSPLIT), G::lds_bytes, s, a);
     return hipGetLastError();
 }
 #define RN_FIRST_SHAPES(X) X(1, 20) X(1, 40) X(1, 64) X(1, 80) X(4, 20) X(4, 40) X(4, 64) X(4, 80)
@@ -1020,10 +1035,15 @@ hipError_t launch_conv_gen(const ConvArgs &a, int k, int s, bool first, int cus,
     return hipErrorInvalidValue;
 }
 
-// 16-K blocks of a general layer, padded to whole triples (the kernel's ring).
-static int gen_blocks(int k, int cin) { return ((k * k * cin + 15) / 16 + 2) / 3 * 3; }
+// 16-K blocks of a general layer, padded like Gen::NBLK (four waves x whole
+// triples of the kernel's weight ring).
+static int gen_blocks(int k, int cin) { return ((k * k * cin + 15) / 16 + 11) / 12 * 12; }
 
 size_t conv_gen_packed_elems(int k, int cin, int cout) { return (size_t)gen_blocks(k, cin) * 16 * cout; }
+#define X(kk, ss, ci, co) static_assert(Gen<kk, ss, ci, co>::NBLK == ((kk * kk * ci + 15) / 16 + 11) / 12 * 12, "padding");
+RN_GEN_FIRST_SHAPES(X)
+RN_GEN_SHAPES(X)
+#undef X
 
 void pack_conv_gen(const float *oihw, int k, int cin, int cout, float *dst) {
     // [block][n-block][lane][j]: K = 16 block + 4 (lane / 16) + j in (ky, kx, c)
