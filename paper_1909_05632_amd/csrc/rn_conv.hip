@@ -431,8 +431,7 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
     const int n_out = NO >= 0 ? NO : a.n_out;
     if (NO != 0 && n_out > 0) {
         // Tile contribution to each logit: per-lane partial dot products, then
-        // the lane sums, 8 logits at a time so the butterfly steps of
-        // different logits overlap.
+        // the lane sums, 8 logits at a time (lane_sums8).
         const int ntiles = a.TH * a.TW;
         for (int o0 = 0; o0 < n_out; o0 += 8) {
             float p[8];
@@ -470,17 +469,12 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
                     break;
                 }
             }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1)
-#pragma unroll
-                for (int q = 0; q < 8; ++q) p[q] += __shfl_xor(p[q], off, 64);
-            if (lane < 8 && o0 + lane < n_out) {
-                float v = p[0];
-#pragma unroll
-                for (int q = 1; q < 8; ++q) v = lane == q ? p[q] : v;
+            const float v = lane_sums8(p, lane);
+            const int q = (lane >> 5) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+            if ((lane & 7) == 0 && o0 + q < n_out) {
                 float *hp = VAR ? a.vhpart + (size_t)widx * n_out
                                 : a.hpart + ((size_t)r.slot * ntiles + r.tile) * n_out;
-                hp[o0 + lane] = v;
+                hp[o0 + q] = v;
             }
         }
     }
@@ -517,9 +511,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     __shared__ float s_w1[FUSE ? 9 * CIN : 1];
     __shared__ float s_b1[FUSE ? CIN : 1];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    static_assert(WAVES == 8, "item mapping for two waves per SIMD");
     const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, WAVES);
-    if (xr.first >= xr.end) return;                       // uniform per block
+    const XcdRangeW xr = xcd_range_simd2(cnt, wave);
+    if (xr.block_first >= xr.end) return;                 // uniform per block
     float *s_w = smem;
     float *halo = smem + M::WTOT + wave * M::HALO;
     const float4 *wg = static_cast<const float4 *>(a.w);
@@ -532,7 +527,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     __syncthreads();
 
     const int stride = xr.stride;
-    int t = xr.first + wave;
+    int t = xr.first;
     if (t >= xr.end) return;                              // no block barrier after this point
     // Pipeline: the halo (or, fused, the input patch) of the next tile is
     // fetched into registers during this tile's matrix work, and the work item

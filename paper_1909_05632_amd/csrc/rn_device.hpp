@@ -24,6 +24,47 @@ __device__ inline void wave_sync() {
 // between the waves of the block.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// Sums over the 64 lanes of a wave of eight per-lane values p[0..7], by
+// halving: at each step (partner lane l ^ 32, 16, 8, 4, 2, 1) a lane keeps
+// half of the values it still holds and adds the partner's copy of them, so
+// 8 + 4 + ... values cross lanes in 10 moves instead of 48.  Each sum is
+// formed by the same pairings as the full xor butterfly (p += its value at
+// lane l ^ off, off = 32 .. 1), so the results are the butterfly's bits.  The
+// moves are the gfx950 permlane swaps for 32 and 16 (rows of 16 lanes) and
+// DPP row moves for the rest.  Lane l returns the sum of p[4 b5 + 2 b4 + b3]
+// (b_i: bit i of l).
+__device__ inline float lane_sums8(const float *p, int lane) {
+    float h[4], g[2];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        // Lanes 0-31 keep p[k], lanes 32-63 p[4 + k]; each half receives the
+        // other half's copy of the value it keeps.
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(p[k]), __float_as_uint(p[4 + k]), false,
+                                                        false);
+        h[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        // Even rows keep h[k], odd rows h[2 + k].
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(h[k]), __float_as_uint(h[2 + k]), false,
+                                                        false);
+        g[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    const bool b3 = (lane >> 3) & 1;
+    const float keep = b3 ? g[1] : g[0], send = b3 ? g[0] : g[1];
+    // row_ror:8 reads lane l ^ 8 within a row.
+    float v = keep + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(send), 0x128, 0xf, 0xf, false));
+    // Lane l ^ 4: row_shl:4 into lanes 0-3 and 8-11 of each row (banks 0, 2),
+    // row_shr:4 into lanes 4-7 and 12-15 (banks 1, 3).
+    int x = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x104, 0xf, 0x5, false);
+    x = __builtin_amdgcn_update_dpp(x, __float_as_int(v), 0x114, 0xf, 0xa, false);
+    v += __int_as_float(x);
+    // Lane l ^ 2 and l ^ 1: quad permutations [2, 3, 0, 1] and [1, 0, 3, 2].
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4e, 0xf, 0xf, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false));
+    return v;
+}
+
 struct TileRef {
     int slot, tile, ty, tx;
 };
@@ -122,6 +163,31 @@ __device__ inline XcdRange xcd_range(int cnt, int units) {
     r.first = (int)((long long)cnt * x / kXcd) + k * units;
     r.end = (int)((long long)cnt * (x + 1) / kXcd);
     r.stride = blocks_x * units;
+    return r;
+}
+
+// The same segments for blocks of 8 waves, two per SIMD (waves w and w + 4 of
+// a block share one), returning wave `wave`'s own first item.  A round of the
+// segment holds 8 B items (B blocks on the XCD): its first 4 B go to waves 0-3,
+// four consecutive items per block (neighbouring tiles stay on one CU), the
+// next 4 B to waves 4-7.  The partial last round then gives every SIMD of the
+// XCD one extra item before any SIMD gets a second, where a block-major split
+// would give both waves of a SIMD one.  `block_first` is the block's smallest
+// item (wave 0's), for a block-uniform early exit.
+struct XcdRangeW {
+    int first, block_first, end, stride;
+};
+
+__device__ inline XcdRangeW xcd_range_simd2(int cnt, int wave) {
+    constexpr int kXcd = 8;
+    const int x = blockIdx.x % kXcd, k = blockIdx.x / kXcd;
+    const int blocks_x = ((int)gridDim.x - x + kXcd - 1) / kXcd;
+    const int seg = (int)((long long)cnt * x / kXcd);
+    XcdRangeW r;
+    r.block_first = seg + 4 * k;
+    r.first = r.block_first + (wave & 3) + (wave >> 2) * 4 * blocks_x;
+    r.end = (int)((long long)cnt * (x + 1) / kXcd);
+    r.stride = blocks_x * 8;
     return r;
 }
 
