@@ -268,7 +268,7 @@ __device__ inline float fetch_patch(const ConvArgs &a, const TileRef &r, int lan
 }
 
 // The 8x8 input patch sits in the last 64 floats of the wave's halo area
-// (written there by the caller, after the previous tile's epilogue, whose
+// (written there by the caller before the previous tile's epilogue, whose
 // output staging ends below it).
 template <int CIN, int COUT>
 __device__ inline float *patch_area(float *halo) {
@@ -415,15 +415,21 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
                                 float *stage, int lane, int widx) {
     using M = Epi<COUT>;
     const int mrow = lane & 15, kq = lane >> 4;       // D holds pixels (py = i, px = kq)
-    const bool col_in = r.tx * kTile + kq < a.W;
+    // Bias, then ReLU and the zero outside the image on the bit patterns, with
+    // no per-value compare into a lane mask: a float above zero has a positive
+    // int pattern (zeros, negatives go to +0 under the int max), and pixels
+    // outside the image are masked to +0 (all-ones / all-zero row masks; the
+    // row bound is the same for the whole wave).
+    const int col_keep = ~((a.W - 1 - (r.tx * kTile + kq)) >> 31);
+    int keep[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) keep[i] = col_keep & ~((a.H - 1 - (r.ty * kTile + i)) >> 31);
 #pragma unroll
     for (int nb = 0; nb < M::NB; ++nb) {
         const float b = s_bias[nb * 16 + mrow];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float v = acc[nb][i] + b;
-            const bool keep = col_in & (r.ty * kTile + i < a.H) & (v > 0.0f);
-            acc[nb][i] = keep ? v : 0.0f;
+            acc[nb][i] = __int_as_float(max(__float_as_int(acc[nb][i] + b), 0) & keep[i]);
             stage[(i * 4 + kq) * M::SR + nb * 16 + mrow] = acc[nb][i];
         }
     }
@@ -494,29 +500,81 @@ __device__ inline void epilogue(const ConvArgs &a, const TileRef &r, floatx4 *ac
     wave_sync();
 }
 
-// Weights resident in LDS for the whole persistent kernel; every wave walks its
-// own tiles independently and prefetches the next tile's halo into registers
-// while the matrix cores work on the current one.
+// Weights resident in LDS for the whole persistent kernel, 8 waves per block
+// (two per SIMD: waves w and w + 4 share one); every wave walks its own tiles
+// independently.  A tile's input (the next halo, or fused, the next 8x8 input
+// patch) is fetched into registers a whole tile ahead.  Measured on gfx950: a
+// wave's VALU work makes no progress while the other wave of its SIMD issues
+// float32 matrix ops, so the two add up and the per-tile VALU work is what
+// this kernel keeps small (item words 64 at a time, one per lane, read with
+// readlane; the epilogue masks on bit patterns).
 template <int CIN, int COUT, int WAVES>
 struct Resident {
     static constexpr size_t lds_bytes =
         (size_t)(Mfma<CIN, COUT>::WTOT + WAVES * Mfma<CIN, COUT>::HALO) * sizeof(float);
 };
 
+// Item words of a wave's items, 64 at a time: lane j of chunk c holds the
+// word of the wave's item 64 c + j (items past the last repeat the range's
+// last word, so every load reads a valid entry).  The words of a whole chunk
+// arrive in one load, long before they are read with readlane, so no per-tile
+// word load is waited for.
+template <bool DENSE>
+__device__ inline uint32_t word_chunk(const ConvArgs &a, int first, int stride, int end, int c, int lane) {
+    return item_word<DENSE>(a, (int)min((long long)first + (long long)(64 * c + lane) * stride, (long long)end - 1));
+}
+
+// Word of item j, held in chunk c0 (w0) or c0 + 1 (w1); j is wave-uniform.
+__device__ inline TileRef item_of(const ConvArgs &a, uint32_t w0, uint32_t w1, int c0, int j) {
+    const uint32_t src = (j >> 6) == c0 ? w0 : w1;
+    return item_ref(a, (uint32_t)__builtin_amdgcn_readlane((int)src, j & 63));
+}
+
+// Halo of tile r into LDS, then the input loads of tile rn (when there is
+// one) into the registers just freed (fused: the patch was written to its
+// area, above the output staging, before the previous tile's epilogue).
+template <int CIN, int COUT, bool FUSE, bool VAR>
+__device__ inline void res_build(const ConvArgs &a, float *halo, const float *s_w1, const float *s_b1, float4 *pre,
+                                 float &pin, const TileRef &r, const TileRef &rn, bool next, int lane) {
+    if constexpr (FUSE) {
+        if (next) pin = fetch_patch<VAR>(a, rn, lane);
+        build_halo_fused<CIN, COUT>(halo, a, r, s_w1, s_b1, lane);
+    } else {
+        store_halo<CIN, COUT>(halo, pre, lane);
+        if (next) fetch_halo<CIN, COUT, VAR>(a, rn, pre, lane);
+    }
+}
+
 template <int CIN, int COUT, int WAVES, bool DENSE, bool FUSE, int NO, bool VAR>
 __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
+    static_assert(WAVES == 8, "item mapping for two waves per SIMD");
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
     __shared__ float s_w1[FUSE ? 9 * CIN : 1];
     __shared__ float s_b1[FUSE ? CIN : 1];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    static_assert(WAVES == 8, "item mapping for two waves per SIMD");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int cnt = work_count<DENSE>(a);
     const XcdRangeW xr = xcd_range_simd2(cnt, wave);
     if (xr.block_first >= xr.end) return;                 // uniform per block
+    const int stride = xr.stride;
+    const int n_me = xr.first < xr.end ? (xr.end - xr.first + stride - 1) / stride : 0;
     float *s_w = smem;
     float *halo = smem + M::WTOT + wave * M::HALO;
+
+    // Item words in two chunks of 64 (w0: chunk c0, w1: chunk c0 + 1); the
+    // first tile's input is fetched before the weights are staged.
+    int c0 = 0;
+    uint32_t w0 = word_chunk<DENSE>(a, xr.first, stride, xr.end, 0, lane);
+    uint32_t w1 = word_chunk<DENSE>(a, xr.first, stride, xr.end, 1, lane);
+    constexpr int HVR = FUSE ? 1 : M::HV;
+    float4 pre[HVR];
+    float pin = 0.f;
+    if (n_me > 0) {
+        if constexpr (FUSE) pin = fetch_patch<VAR>(a, item_of(a, w0, w1, c0, 0), lane);
+        else fetch_halo<CIN, COUT, VAR>(a, item_of(a, w0, w1, c0, 0), pre, lane);
+    }
     const float4 *wg = static_cast<const float4 *>(a.w);
     for (int j = tid; j < M::WTOT / 4; j += blockDim.x) reinterpret_cast<float4 *>(s_w)[j] = wg[j];
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
@@ -526,46 +584,33 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     }
     __syncthreads();
 
-    const int stride = xr.stride;
-    int t = xr.first;
-    if (t >= xr.end) return;                              // no block barrier after this point
-    // Pipeline: the halo (or, fused, the input patch) of the next tile is
-    // fetched into registers during this tile's matrix work, and the work item
-    // after that is read one more iteration ahead, so neither load is waited
-    // for before the matrix ops.
-    constexpr int HVR = FUSE ? 1 : M::HV;
-    float4 pre[HVR];
-    float pin = 0.f;
-    uint32_t e_cur = item_word<DENSE>(a, t);
-    uint32_t e_nxt = t + stride < xr.end ? item_word<DENSE>(a, t + stride) : 0u;
-    if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = fetch_patch<VAR>(a, item_ref(a, e_cur), lane);
-    else fetch_halo<CIN, COUT, VAR>(a, item_ref(a, e_cur), pre, lane);
-    for (; t < xr.end; t += stride) {
-        const TileRef cur = item_ref(a, e_cur);
-        if constexpr (FUSE) build_halo_fused<CIN, COUT>(halo, a, cur, s_w1, s_b1, lane);
-        else store_halo<CIN, COUT>(halo, pre, lane);
+    if (n_me == 0) return;                                // no block barrier after this point
+
+    // Per tile: halo (issuing the next tile's input loads first), matrix
+    // work, epilogue; fused, the next patch goes to its area after the
+    // epilogue, its load having had the whole tile to arrive.
+    if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = pin;
+    for (int k = 0; k < n_me; ++k) {
+        if (k >= 64 * (c0 + 1)) {                         // tile k starts the next chunk of words
+            w0 = w1;
+            ++c0;
+            w1 = word_chunk<DENSE>(a, xr.first, stride, xr.end, c0 + 1, lane);
+        }
+        res_build<CIN, COUT, FUSE, VAR>(a, halo, s_w1, s_b1, pre, pin, item_of(a, w0, w1, c0, k),
+                                        item_of(a, w0, w1, c0, k + 1), k + 1 < n_me, lane);
         wave_sync();
-        const uint32_t e_nn = t + 2 * stride < xr.end ? item_word<DENSE>(a, t + 2 * stride) : 0u;
-        // The next tile's input (past the end: item 0's, never used).
-        if constexpr (FUSE) pin = fetch_patch<VAR>(a, item_ref(a, e_nxt), lane);
-        else if (t + stride < xr.end) fetch_halo<CIN, COUT, VAR>(a, item_ref(a, e_nxt), pre, lane);
         floatx4 acc[M::NB];
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        // A wave in its matrix phase issues ahead of the other wave of its SIMD
-        // (which is then staging or storing), so the two drift out of phase
-        // and the matrix pipe is not left idle while both do memory work.
+        // A wave in its matrix phase issues ahead of the other wave of its SIMD.
         __builtin_amdgcn_s_setprio(2);
         mfma_positions<CIN, COUT, 9>(acc, halo, s_w, 0, lane);
         __builtin_amdgcn_s_setprio(0);
         wave_sync();
-        epilogue<COUT, NO, VAR>(a, cur, acc, s_bias, halo, lane, t);
-        // The next patch goes to LDS here rather than at the top of the loop:
-        // the wait for its load then counts exactly this tile's later memory
-        // operations, where at the loop top it would have to drain them all.
-        if constexpr (FUSE) patch_area<CIN, COUT>(halo)[lane] = pin;
-        e_cur = e_nxt;
-        e_nxt = e_nn;
+        epilogue<COUT, NO, VAR>(a, item_of(a, w0, w1, c0, k), acc, s_bias, halo, lane, xr.first + k * stride);
+        if constexpr (FUSE) {
+            if (k + 1 < n_me) patch_area<CIN, COUT>(halo)[lane] = pin;
+        }
     }
 }
 
