@@ -582,7 +582,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         for (int j = tid; j < 9 * CIN; j += blockDim.x) s_w1[j] = a.w1[j];
         for (int j = tid; j < CIN; j += blockDim.x) s_b1[j] = a.b1[j];
     }
-    __syncthreads();
+    lds_barrier();                                        // the first input loads stay in flight
 
     if (n_me == 0) return;                                // no block barrier after this point
 
@@ -919,9 +919,9 @@ __global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
     const int b0 = wave * G::NBW;                         // this wave's K blocks [b0, b0 + NBW)
     for (int t = xr.first; t < xr.end; t += xr.stride) {  // uniform per block
         const TileRef r = decode<DENSE>(a, t);
-        __syncthreads();                                  // the previous tile's epilogue is done with the area
+        lds_barrier();                                    // the previous tile's epilogue is done with the area
         gen_load_patch<KS, ST, CIN, COUT, FIRST>(a, r, halo, tid, (int)blockDim.x);
-        __syncthreads();
+        lds_barrier();
         floatx4 acc[G::NB];
 #pragma unroll
         for (int nb = 0; nb < G::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -957,7 +957,7 @@ __global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
 #pragma unroll
             for (int nb = 0; nb < G::NB; ++nb) part[((wave - 1) * G::NB + nb) * 64 + lane] = acc[nb];
         }
-        __syncthreads();
+        lds_barrier();
         if (wave == 0) {
 #pragma unroll
             for (int w = 0; w < G::KSPLIT - 1; ++w)

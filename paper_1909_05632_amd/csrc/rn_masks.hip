@@ -28,6 +28,12 @@ constexpr int kMaskThreads = 1024;         // one block per stream
 
 __device__ inline uint32_t f32_bits(float v) { return __float_as_uint(v); }
 
+// Block barrier for data exchanged through LDS only (waits for this wave's LDS
+// operations, then s_barrier).  __syncthreads would also drain every global
+// store in flight (its release fence), a full memory round trip per barrier;
+// no kernel here reads global data that another wave of its block wrote.
+__device__ inline void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ inline uint64_t row_valid_bits(int W, int wx) {
     int nb = W - 64 * wx;
     return nb >= 64 ? ~0ull : ((1ull << nb) - 1ull);
@@ -36,9 +42,9 @@ __device__ inline uint64_t row_valid_bits(int W, int wx) {
 __device__ inline int block_sum(int v, int *red) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();
+    lds_sync();
     if (lane == 0) red[wave] = v;
-    __syncthreads();
+    lds_sync();
     int s = 0;
     for (int w = 0; w < (int)(blockDim.x >> 6); ++w) s += red[w];
     return s;
@@ -135,7 +141,7 @@ __device__ void grow_general(const MaskGeom &g, int l, uint64_t *src, uint64_t *
         for (int r = r0; r < r1; ++r) acc |= src[r * WWi + wx];
         mid[w] = acc;
     }
-    __syncthreads();
+    lds_sync();
     for (int w = threadIdx.x; w < Ho * WWo; w += blockDim.x) {
         const int y = w / WWo, wx = w - y * WWo;
         const uint64_t *row = mid + y * WWi;
@@ -175,7 +181,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     for (int w = threadIdx.x; w < HWW; w += blockDim.x) A[w] = 0ull;
     if (U8)
         for (int j = threadIdx.x; j < 256; j += blockDim.x) lut[j] = a.lut[j];
-    __syncthreads();
+    lds_sync();
 
     // Cache planes: the previous newest frame, and where the new frame goes.
     float *prev, *next;
@@ -258,7 +264,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
             }
         }
     }
-    __syncthreads();
+    lds_sync();
 
     if (g.stack != 1) {
         // Stacked input: channel j of step t is frame t-3+j, so the stack
@@ -275,7 +281,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
                        ring[((nhead + 3) & 3) * HWW + w];
             }
         }
-        __syncthreads();
+        lds_sync();
     }
 
     int nchg = 0;
@@ -285,16 +291,16 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     int t0 = emit_layer(g, A, 0, slot, red);
     if (threadIdx.x == 0) s_tiles[0] = t0;
     for (int l = 1; l <= g.L; ++l) {
-        __syncthreads();
+        lds_sync();
         if (standard_layer(g, l)) {
             grow1(g.Hl[l], g.Wl[l], g.WWl[l], A, B);
-            __syncthreads();
+            lds_sync();
             uint64_t *t = A;
             A = B;
             B = t;
         } else {
             grow_general(g, l, A, B);
-            __syncthreads();
+            lds_sync();
         }
         const int tl = emit_layer(g, A, l, slot, red);
         if (threadIdx.x == 0) s_tiles[l] = tl;
@@ -392,9 +398,9 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // Per-position counts of this word over all streams.
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
-        __syncthreads();
+        lds_sync();
         stage_pass(a, l, wd, c0, nc, s_slot, s_word);
-        __syncthreads();
+        lds_sync();
         for (int cc = wave; cc < nc; cc += nwaves) {
             const uint64_t word = s_word[cc * 64 + lane];
             int mine = 0;
@@ -408,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             atomicAdd(&s_cnt[lane], mine);       // LDS
         }
     }
-    __syncthreads();
+    lds_sync();
     if (threadIdx.x == 0) {
         int r = pre;
         for (int j = 0; j < 64; ++j) {
@@ -417,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
         }
         if (wd == TMW - 1) a.cnt[l] = (int)min((size_t)r, a.cap[l]);   // the last word closes the list
     }
-    __syncthreads();
+    lds_sync();
 
     const size_t cap = a.cap[l];
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
@@ -425,9 +431,9 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
         if (nch > kChunksPerPass) {
             // More than one pass: stage and transpose this pass again (with a
             // single pass, LDS still holds it from the counting loop).
-            __syncthreads();
+            lds_sync();
             stage_pass(a, l, wd, c0, nc, s_slot, s_word);
-            __syncthreads();
+            lds_sync();
             for (int cc = wave; cc < nc; cc += nwaves) {
                 const uint64_t word = s_word[cc * 64 + lane];
                 for (int j = 0; j < 64; ++j) {
@@ -435,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
                     if (lane == j) s_bal[cc][j] = b;
                 }
             }
-            __syncthreads();
+            lds_sync();
         }
         if (threadIdx.x < 64) {
             int r = s_run[threadIdx.x];
@@ -445,7 +451,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             }
             s_run[threadIdx.x] = r;
         }
-        __syncthreads();
+        lds_sync();
         // One thread per (chunk, position): walk the set bits of the position's
         // stream bitmap; its entries are [base, base + popcount) in stream order.
         for (int pi = threadIdx.x; pi < nc * 64; pi += blockDim.x) {
@@ -584,9 +590,9 @@ __device__ inline int block_excl_scan(int v, int *s_w, int *total) {
         const int y = __shfl_up(x, o, 64);
         if (lane >= o) x += y;
     }
-    __syncthreads();                      // s_w of the previous call has been read
+    lds_sync();                      // s_w of the previous call has been read
     if (lane == 63) s_w[wave] = x;
-    __syncthreads();
+    lds_sync();
     int off = 0, tot = 0;
     for (int w = 0; w < nw; ++w) {
         const int s = s_w[w];
