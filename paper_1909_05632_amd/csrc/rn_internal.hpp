@@ -27,6 +27,7 @@ struct MaskGeom {
     int TH, TW, TMW;              // input tile rows, tile columns, 64-bit words per tile mask
     int cin;                      // channels per frame
     int stack;                    // 1, or 4 (ring of the last 4 frames)
+    int dil;                      // every layer 3x3/1/1: layer l's mask is the change set dilated by l (set by the launcher)
     int Hl[RN_MAX_CONV + 1], Wl[RN_MAX_CONV + 1], WWl[RN_MAX_CONV + 1];
     int THl[RN_MAX_CONV + 1], TWl[RN_MAX_CONV + 1], TMWl[RN_MAX_CONV + 1];
     int ks[RN_MAX_CONV], st[RN_MAX_CONV], pd[RN_MAX_CONV];   // kernel, stride, pad of layer l + 1

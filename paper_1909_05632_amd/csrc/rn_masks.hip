@@ -117,6 +117,24 @@ __device__ void grow1(int H, int W, int WW, const uint64_t *src, uint64_t *dst) 
     }
 }
 
+// Word wx of row y of the change set src dilated by R pixels (every pixel
+// within Chebyshev distance R of a changed one), clipped to the H x W grid.
+// Growing by one pixel per 3x3 stride-1 layer, clipped each time, gives the
+// same set after R layers: inside a rectangle, a point within distance R of a
+// changed pixel is reached by R one-pixel steps that stay in the rectangle.
+__device__ inline uint64_t dilate_word(const uint64_t *src, int H, int W, int WW, int y, int wx, int R) {
+    uint64_t lft = 0, mid = 0, rgt = 0;
+    for (int yy = max(y - R, 0); yy <= min(y + R, H - 1); ++yy) {
+        const uint64_t *row = src + yy * WW;
+        mid |= row[wx];
+        if (wx > 0) lft |= row[wx - 1];
+        if (wx + 1 < WW) rgt |= row[wx + 1];
+    }
+    uint64_t out = mid;
+    for (int d = 1; d <= R; ++d) out |= (mid << d) | (lft >> (64 - d)) | (mid >> d) | (rgt << (64 - d));
+    return out & row_valid_bits(W, wx);
+}
+
 // Bits of the index range [x0, x1) that fall in 64-bit word wx.
 __device__ inline uint64_t range_bits(int x0, int x1, int wx) {
     const int lo = max(x0 - 64 * wx, 0), hi = min(x1 - 64 * wx, 64);
@@ -170,7 +188,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
     const int HWW = g.H * g.WW;
     uint64_t *A = smem;
     uint64_t *B = smem + HWW;
-    float *lut = reinterpret_cast<float *>(smem + 2 * HWW);
+    float *lut = reinterpret_cast<float *>(smem + (g.dil ? max(2, g.L + 1) : 2) * HWW);
 
     const int i = blockIdx.x;
     const int slot = a.ids[i];
@@ -282,6 +300,59 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
             }
         }
         lds_sync();
+    }
+
+    if (g.dil) {
+        // Every layer 3x3 stride 1 pad 1 (one grid): all layers' masks at once
+        // (layer l: the change set dilated by l), then all layers' tile words;
+        // two barriers instead of four per layer.
+        __shared__ int s_cnt[RN_MAX_CONV + 2];
+        if (threadIdx.x < RN_MAX_CONV + 2) s_cnt[threadIdx.x] = 0;
+        int nc = 0;
+        for (int e = threadIdx.x; e < (g.L + 1) * HWW; e += blockDim.x) {
+            const int l = e / HWW, w = e - l * HWW;
+            uint64_t v;
+            if (l == 0) {
+                v = A[w];
+                nc += __popcll(v);
+            } else {
+                const int y = w / g.WW;
+                v = dilate_word(A, g.H, g.W, g.WW, y, w - y * g.WW, l);
+                smem[(size_t)l * HWW + w] = v;
+            }
+            g.pmask[l][(size_t)slot * HWW + w] = v;
+        }
+        lds_sync();
+        if (nc) atomicAdd(&s_cnt[RN_MAX_CONV + 1], nc);
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        const int TMW = g.TMW, ntiles = g.TH * g.TW;
+        for (int e = wave; e < (g.L + 1) * TMW; e += (int)(blockDim.x >> 6)) {
+            const int l = e / TMW, wd = e - l * TMW;
+            const uint64_t *M = smem + (size_t)l * HWW;
+            const int t = 64 * wd + lane;
+            bool dirty = false;
+            if (t < ntiles) {
+                const int ty = t / g.TW, tx = t - ty * g.TW;
+                const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
+                const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+                uint64_t bits = 0;
+                for (int y = y0; y < y1; ++y) bits |= M[y * g.WW + wx] >> sh;
+                dirty = (bits & ((1ull << kTile) - 1ull)) != 0;
+            }
+            const uint64_t m = __ballot(dirty);
+            if (lane == 0) {
+                g.tmask[l][(size_t)slot * TMW + wd] = m;
+                if (m) atomicAdd(&s_cnt[l], __popcll(m));
+            }
+        }
+        lds_sync();
+        if (threadIdx.x == 0) {
+            a.nchg[i] = s_cnt[RN_MAX_CONV + 1];
+            for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_cnt[l];
+            a.primed[slot] = 1;
+            if (g.stack != 1) a.ring_head[slot] = nhead;
+        }
+        return;
     }
 
     int nchg = 0;
@@ -657,8 +728,14 @@ hipError_t launch_var_lists(const VarMaskArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, hipStream_t s) {
-    const size_t shm = (size_t)2 * g.H * g.WW * sizeof(uint64_t) + 256 * sizeof(float);
+hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, hipStream_t s) {
+    MaskGeom g = geom;
+    const size_t hww = (size_t)g.H * g.WW;
+    bool all_std = true;
+    for (int l = 0; l < g.L; ++l) all_std = all_std && g.ks[l] == 3 && g.st[l] == 1 && g.pd[l] == 1;
+    const size_t dil_bytes = (size_t)std::max(2, g.L + 1) * hww * sizeof(uint64_t) + 256 * sizeof(float);
+    g.dil = all_std && dil_bytes <= 48 * 1024 ? 1 : 0;
+    const size_t shm = g.dil ? dil_bytes : 2 * hww * sizeof(uint64_t) + 256 * sizeof(float);
     if (a.frame_u8)
         hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kMaskThreads), shm, s, g, a);
     else
