@@ -424,11 +424,29 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 // (ty, tx, batch index) order.  One block per (64-position word wd, layer):
 //   - its offset is the number of dirty tiles at earlier positions, i.e. the
 //     popcount of tile-mask words 0..wd-1 of every stream;
-//   - 64 ballots per chunk of 64 streams transpose the chunk's words into one
-//     stream bitmap per position, giving per-position counts and, by
-//     popcount below the lane, each stream's rank within its position.
+//   - a 64 x 64 bit transpose per chunk of 64 streams (lane r holds stream
+//     r's word; six exchange stages leave lane j with position j's stream
+//     bitmap) gives per-position counts and the streams of each position.
 // Every entry has exactly one writer; no global atomics.
 constexpr int kChunksPerPass = 16;          // 1024 streams per pass
+
+// 64 x 64 bit-matrix transpose across a wave: on entry lane r holds row r
+// (bit c = element (r, c)); on return lane c holds column c (bit r = element
+// (r, c)).  Stage s (32, 16, .., 1) swaps the off-diagonal s x s blocks of
+// every 2s x 2s block between lanes r and r ^ s.
+__device__ inline uint64_t transpose64(uint64_t x, int lane) {
+    const uint64_t masks[6] = {0x00000000FFFFFFFFull, 0x0000FFFF0000FFFFull, 0x00FF00FF00FF00FFull,
+                               0x0F0F0F0F0F0F0F0Full, 0x3333333333333333ull, 0x5555555555555555ull};
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+        const int sh = 32 >> k;
+        const uint64_t m = masks[k];
+        const uint32_t lo = __shfl_xor((uint32_t)x, sh, 64), hi = __shfl_xor((uint32_t)(x >> 32), sh, 64);
+        const uint64_t y = ((uint64_t)hi << 32) | lo;
+        x = (lane & sh) ? (x & ~m) | ((y & ~m) >> sh) : (x & m) | ((y & m) << sh);
+    }
+    return x;
+}
 
 // Stage the slots and this word's tile bits of streams [64 c0, 64 (c0 + nc)) in LDS.
 __device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, int nc, int32_t *s_slot,
@@ -455,44 +473,51 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int nwaves = (int)(blockDim.x >> 6);
     const int nch = (a.n + 63) / 64;
+    const int nc0 = min(kChunksPerPass, nch);
 
-    // Dirty tiles at positions before this word, over all streams (one thread
-    // per stream; the words of a stream are independent loads).
+    // One pass over the streams (thread per stream, one slot load then
+    // independent word loads): dirty tiles at positions before this word, and
+    // the first pass's slots and words of this word staged in LDS.
     int pre = 0;
-    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const uint64_t *tm = a.tmask[l] + (size_t)a.ids[i] * TMW;
-        for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
+    for (int i = threadIdx.x; i < 64 * nc0 || i < a.n; i += blockDim.x) {
+        const int slot = i < a.n ? a.ids[i] : -1;
+        if (slot >= 0) {
+            const uint64_t *tm = a.tmask[l] + (size_t)slot * TMW;
+            for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
+        }
+        if (i < 64 * nc0) {
+            s_slot[i] = slot;
+            s_word[i] = slot >= 0 ? a.tmask[l][(size_t)slot * TMW + wd] : 0ull;
+        }
     }
-    pre = block_sum(pre, red);
+    pre = block_sum(pre, red);                   // its barriers also publish the staging
     if (threadIdx.x < 64) s_cnt[threadIdx.x] = 0;
 
     // Per-position counts of this word over all streams.
     for (int c0 = 0; c0 < nch; c0 += kChunksPerPass) {
         const int nc = min(kChunksPerPass, nch - c0);
-        lds_sync();
-        stage_pass(a, l, wd, c0, nc, s_slot, s_word);
+        if (c0 > 0) {
+            lds_sync();
+            stage_pass(a, l, wd, c0, nc, s_slot, s_word);
+        }
         lds_sync();
         for (int cc = wave; cc < nc; cc += nwaves) {
-            const uint64_t word = s_word[cc * 64 + lane];
-            int mine = 0;
-            for (int j = 0; j < 64; ++j) {
-                const uint64_t b = __ballot((word >> j) & 1ull);
-                if (lane == j) {
-                    mine = __popcll(b);
-                    s_bal[cc][j] = b;
-                }
-            }
-            atomicAdd(&s_cnt[lane], mine);       // LDS
+            const uint64_t b = transpose64(s_word[cc * 64 + lane], lane);
+            s_bal[cc][lane] = b;
+            atomicAdd(&s_cnt[lane], __popcll(b));   // LDS
         }
     }
     lds_sync();
-    if (threadIdx.x == 0) {
-        int r = pre;
-        for (int j = 0; j < 64; ++j) {
-            s_run[j] = r;
-            r += s_cnt[j];
+    if (threadIdx.x < 64) {
+        // Exclusive scan of the position counts, after the earlier words' total.
+        const int c = s_cnt[lane];
+        int x = c;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
         }
-        if (wd == TMW - 1) a.cnt[l] = (int)min((size_t)r, a.cap[l]);   // the last word closes the list
+        s_run[lane] = pre + x - c;
+        if (lane == 63 && wd == TMW - 1) a.cnt[l] = (int)min((size_t)(pre + x), a.cap[l]);   // the last word closes the list
     }
     lds_sync();
 
@@ -505,13 +530,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             lds_sync();
             stage_pass(a, l, wd, c0, nc, s_slot, s_word);
             lds_sync();
-            for (int cc = wave; cc < nc; cc += nwaves) {
-                const uint64_t word = s_word[cc * 64 + lane];
-                for (int j = 0; j < 64; ++j) {
-                    const uint64_t b = __ballot((word >> j) & 1ull);
-                    if (lane == j) s_bal[cc][j] = b;
-                }
-            }
+            for (int cc = wave; cc < nc; cc += nwaves) s_bal[cc][lane] = transpose64(s_word[cc * 64 + lane], lane);
             lds_sync();
         }
         if (threadIdx.x < 64) {
