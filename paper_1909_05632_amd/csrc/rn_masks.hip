@@ -578,8 +578,8 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
 // k_var_pix: one wave per (variant, layer); lanes own pixel rows and 64-tile
 // words; per-variant counts by wave reduction.
 // k_var_bits: one wave per (64-variant chunk, layer 1..L, tile word): the
-// chunk's words transposed by 64 ballots into one 64-variant bitmap per tile
-// position, bits[l][t][chunk], with variants over the per-variant limit
+// chunk's words transposed across the lanes (transpose64) into one
+// 64-variant bitmap per tile position, bits[l][t][chunk], with variants over the per-variant limit
 // cleared, and each position's entry count summed (integer atomics: the sum
 // does not depend on their order).
 // k_var_lists: block (b, l) owns positions [b P, b P + P); its entries start
@@ -660,11 +660,7 @@ __global__ __launch_bounds__(256) void k_var_bits(VarMaskArgs a) {
     if (ok && a.vmax > 0)
         for (int q = 1; q <= a.L; ++q) ok = ok && a.ntile[(size_t)i * (a.L + 1) + q] <= a.vmax;
     const uint64_t w = ok ? a.tmask[l][(size_t)i * a.TMW + wd] : 0ull;
-    uint64_t mine = 0;
-    for (int j = 0; j < 64; ++j) {
-        const uint64_t b = __ballot((w >> j) & 1ull);
-        if (lane == j) mine = b;
-    }
+    const uint64_t mine = transpose64(w, lane);         // position 64 wd + lane's variant bitmap
     const int t = 64 * wd + lane;
     if (t < a.ntiles) {
         a.bits[l][(size_t)t * a.nch + c] = mine;
