@@ -24,6 +24,7 @@ using dev::xcd_range;
 using dev::item_ref;
 using dev::item_word;
 using dev::work_count;
+using dev::lds_barrier;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -286,24 +287,29 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
 //   hpart[tile][o] = sum_k act_tile[k] * hw[P][k][o],  k = pixel * C + channel,
 // on v_mfma_f32_16x16x32_bf16 (A: the tile's cache slice read straight from
 // memory, 16 bytes per lane per k-step; products of two bf16 values are exact
-// in float32).  A block takes 64 consecutive work items, one 16-row block per
-// wave; the work list is position-major, so the 64 items mostly share one or
-// two positions and each position's weights are read once for all of them
-// (the four waves read the same addresses, served by L1/L2).  A block makes
-// one pass per distinct position; a wave computes in a pass only if one of
-// its rows has that position, and keeps only those rows.  Each row's sum runs
-// over the full K in one wave in a fixed order, so the result does not depend
-// on which rows share the block: list and dense passes agree bit for bit.
-// VAR: variant work items; the tile's activations are its overlay row (the
-// item's list index) and its partials go to the same row of the variant
-// partials.
+// in float32).  A block takes 64 consecutive work items (four 16-row groups);
+// the work list is position-major, so the 64 items mostly share one or two
+// positions, and the block makes one pass per distinct position.  In a pass
+// the four waves split K: wave w runs k-steps [w KS/4, (w + 1) KS/4) for all
+// four row groups, so each weight fragment of P is read once per block (the
+// weights of the positions in flight do not fit in L2; reading them once per
+// wave cost more than the activations), rows not at P contributing zeros.
+// The four K-quarter partials go through LDS and wave g adds those of row
+// group g in wave order.  A row's sum therefore has a fixed order that does
+// not depend on which rows share the block: list and dense passes agree bit
+// for bit.  VAR: variant work items; the tile's activations are its overlay
+// row (the item's list index) and its partials go to the same row of the
+// variant partials.
 template <int C, int NBO, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     constexpr int KS = 16 * C / 32;           // k-steps
-    constexpr int KB = 8;                     // k-steps per batch of loads
-    static_assert(KS % KB == 0, "whole batches");
+    constexpr int KW = KS / 4;                // k-steps per wave
+    constexpr int KB = 4;                     // k-steps per batch of loads
+    static_assert(KW % KB == 0, "whole batches");
     __shared__ int s_pos[64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ floatx4 s_acc[4][4][NBO][64];  // [wave][row group][n-block][lane]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int cnt = work_count<DENSE>(a);
     const XcdRange xr = xcd_range(cnt, 64);
     const uint16_t *act = static_cast<const uint16_t *>(a.in);
@@ -311,72 +317,92 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     const int ntiles = a.TH * a.TW;
     const int row = lane & 15, kq = lane >> 4;
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        const int it = g + wave * 16 + row;                 // this lane's A row
-        const bool valid = it < xr.end;
-        const uint32_t e = valid ? item_word<DENSE>(a, it) : 0u;
-        const TileRef r = item_ref(a, e);
-        const int my_pos = valid ? r.tile : -1;
+        // This lane's A rows: row `row` of each group (items g + 16 rg + row).
+        uint32_t e[4];
+        int pos[4];
+        const uint16_t *arow[4];
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+            const int it = g + 16 * rg + row;
+            const bool valid = it < xr.end;
+            e[rg] = valid ? item_word<DENSE>(a, it) : 0u;
+            const TileRef r = item_ref(a, e[rg]);
+            pos[rg] = valid ? r.tile : -1;
+            arow[rg] = (VAR ? static_cast<const uint16_t *>(a.vov_in) + (size_t)it * kTilePx * C
+                            : act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C) +
+                       8 * kq + 32 * KW * wave;
+        }
         if (tid < 64) {
             const int t2 = g + tid;
             s_pos[tid] = t2 < xr.end ? item_ref(a, item_word<DENSE>(a, t2)).tile : -1;
         }
-        __syncthreads();
-        // Positions of the wave's 16 rows, for the per-pass "any row of mine" test.
-        uint64_t mine_mask = 0;
-        const uint16_t *arow = (VAR ? static_cast<const uint16_t *>(a.vov_in) + (size_t)it * kTilePx * C
-                                    : act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C) +
-                               8 * kq;
-        uint64_t done = 0;                                   // rows of the block handled
-        for (;;) {
-            int P = -1;
-            for (int q = 0; q < 64; ++q)
-                if (P < 0 && !((done >> q) & 1) && s_pos[q] >= 0) P = s_pos[q];
-            if (P < 0) break;
-            uint64_t pmask = 0;
-            for (int q = 0; q < 64; ++q) pmask |= (uint64_t)(s_pos[q] == P) << q;
-            done |= pmask;
-            mine_mask = (pmask >> (16 * wave)) & 0xFFFFu;
-            if (mine_mask == 0) continue;                    // uniform per wave
-            const bool mine = my_pos == P;
-            floatx4 acc[NBO];
+        lds_barrier();
+        // Lane q of every wave holds row q's position; the passes take the
+        // positions in order of first appearance, found by ballots.
+        const int my_sp = s_pos[lane];
+        uint64_t left = __ballot(my_sp >= 0);                // rows of the block not yet handled
+        while (left) {                                       // uniform per block
+            const int P = __builtin_amdgcn_readlane(my_sp, __ffsll((long long)left) - 1);
+            const uint64_t pmask = __ballot(my_sp == P);
+            left &= ~pmask;
+            floatx4 acc[4][NBO];
 #pragma unroll
-            for (int nb = 0; nb < NBO; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-            const uint16_t *wp = hw + ((size_t)P * KS * NBO * 64 + lane) * 8;
-            for (int s0 = 0; s0 < KS; s0 += KB) {
-                u32x4 av[KB], bv[KB][NBO];
+            for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) acc[rg][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            const uint16_t *wp = hw + (((size_t)P * KS + KW * wave) * NBO * 64 + lane) * 8;
+            for (int s0 = 0; s0 < KW; s0 += KB) {
+                u32x4 av[KB][4], bv[KB][NBO];
 #pragma unroll
                 for (int s = 0; s < KB; ++s) {
-                    av[s] = mine ? *reinterpret_cast<const u32x4 *>(arow + 32 * (s0 + s)) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
                     for (int nb = 0; nb < NBO; ++nb)
                         bv[s][nb] = *reinterpret_cast<const u32x4 *>(wp + ((size_t)(s0 + s) * NBO + nb) * 64 * 8);
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg)
+                        av[s][rg] = pos[rg] == P ? *reinterpret_cast<const u32x4 *>(arow[rg] + 32 * (s0 + s))
+                                                 : u32x4{0u, 0u, 0u, 0u};
                 }
 #pragma unroll
                 for (int s = 0; s < KB; ++s)
 #pragma unroll
-                    for (int nb = 0; nb < NBO; ++nb)
-                        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[s]),
-                                                                          __builtin_bit_cast(bf16x8, bv[s][nb]),
-                                                                          acc[nb], 0, 0, 0);
+                    for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+                        for (int nb = 0; nb < NBO; ++nb)
+                            acc[rg][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8, av[s][rg]), __builtin_bit_cast(bf16x8, bv[s][nb]), acc[rg][nb],
+                                0, 0, 0);
             }
-            // D: rows 4 kq + i, column lane % 16 = logit nb * 16 + row.
 #pragma unroll
-            for (int nb = 0; nb < NBO; ++nb) {
-                const int o = nb * 16 + row;
+            for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int q = 4 * kq + i;                // row of the wave's block
-                    const uint32_t eq = __shfl(e, q, 64);   // lane q holds row q's item
-                    if (o < a.n_out && ((mine_mask >> q) & 1)) {
-                        const TileRef rq = item_ref(a, eq);
-                        float *hp = VAR ? a.vhpart + (size_t)(g + wave * 16 + q) * a.n_out
-                                        : a.hpart + ((size_t)rq.slot * ntiles + rq.tile) * a.n_out;
-                        hp[o] = acc[nb][i];
+                for (int nb = 0; nb < NBO; ++nb) s_acc[wave][rg][nb][lane] = acc[rg][nb];
+            lds_barrier();
+            // Wave `wave` finishes row group `wave`: the K quarters in wave order.
+            const uint64_t gmask = (pmask >> (16 * wave)) & 0xFFFFu;
+            if (gmask) {                                     // uniform per wave
+                const uint32_t ew = wave == 0 ? e[0] : wave == 1 ? e[1] : wave == 2 ? e[2] : e[3];
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) {
+                    const floatx4 v = s_acc[0][wave][nb][lane] + s_acc[1][wave][nb][lane] +
+                                      s_acc[2][wave][nb][lane] + s_acc[3][wave][nb][lane];
+                    // D: rows 4 kq + i of the group, column lane % 16 = logit nb * 16 + row.
+                    const int o = nb * 16 + row;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = 4 * kq + i;
+                        const uint32_t eq = __shfl(ew, q, 64);   // lane q holds row q's item
+                        if (o < a.n_out && ((gmask >> q) & 1)) {
+                            const TileRef rq = item_ref(a, eq);
+                            float *hp = VAR ? a.vhpart + (size_t)(g + 16 * wave + q) * a.n_out
+                                            : a.hpart + ((size_t)rq.slot * ntiles + rq.tile) * a.n_out;
+                            hp[o] = v[i];
+                        }
                     }
                 }
             }
+            lds_barrier();                                   // s_acc is rewritten by the next pass
         }
-        __syncthreads();                                     // s_pos is rewritten next round
     }
 }
 
@@ -437,7 +463,9 @@ void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, i
 
 template <int C, bool DENSE, bool VAR>
 hipError_t run_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s) {
-    const int grid = dev::persistent_grid(cus * 4, (a.max_tiles + 63) / 64);
+    // Two blocks per CU are resident (registers), so a larger grid would only
+    // run in a second generation.
+    const int grid = dev::persistent_grid(cus * (a.n_out <= 32 ? 2 : 1), (a.max_tiles + 63) / 64);
     if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_bf16<C, 1, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_bf16<C, 2, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     else hipLaunchKernelGGL((k_tile_part_bf16<C, 4, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
