@@ -486,7 +486,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     ma.primed = net->at<int32_t>(p.o_primed);
     ma.nchg = net->at<int32_t>(p.o_nchg);
     ma.ntile = net->at<int32_t>(p.o_ntile);
-    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, s); });
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, net->cus, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("mask kernel: ") + hipGetErrorString(e));
 
     CompactArgs ca{};

@@ -24,7 +24,9 @@ namespace rn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaskThreads = 1024;         // one block per stream
+// k_masks: one block per stream, of 1024 threads when the streams fit one
+// block per CU, else smaller blocks so that several streams share a CU and
+// their serial phases overlap.
 
 __device__ inline uint32_t f32_bits(float v) { return __float_as_uint(v); }
 
@@ -117,19 +119,15 @@ __device__ void grow1(int H, int W, int WW, const uint64_t *src, uint64_t *dst) 
     }
 }
 
-// Word wx of row y of the change set src dilated by R pixels (every pixel
-// within Chebyshev distance R of a changed one), clipped to the H x W grid.
+// Dilation of a change set by R pixels (every pixel within Chebyshev
+// distance R of a changed one), clipped to the H x W grid, in two separable
+// passes: the OR of rows y - R .. y + R (k_masks), then the OR of bits
+// x - R .. x + R of that row (hdilate_word, word wx).
 // Growing by one pixel per 3x3 stride-1 layer, clipped each time, gives the
 // same set after R layers: inside a rectangle, a point within distance R of a
 // changed pixel is reached by R one-pixel steps that stay in the rectangle.
-__device__ inline uint64_t dilate_word(const uint64_t *src, int H, int W, int WW, int y, int wx, int R) {
-    uint64_t lft = 0, mid = 0, rgt = 0;
-    for (int yy = max(y - R, 0); yy <= min(y + R, H - 1); ++yy) {
-        const uint64_t *row = src + yy * WW;
-        mid |= row[wx];
-        if (wx > 0) lft |= row[wx - 1];
-        if (wx + 1 < WW) rgt |= row[wx + 1];
-    }
+__device__ inline uint64_t hdilate_word(const uint64_t *row, int W, int WW, int wx, int R) {
+    const uint64_t mid = row[wx], lft = wx > 0 ? row[wx - 1] : 0ull, rgt = wx + 1 < WW ? row[wx + 1] : 0ull;
     uint64_t out = mid;
     for (int d = 1; d <= R; ++d) out |= (mid << d) | (lft >> (64 - d)) | (mid >> d) | (rgt << (64 - d));
     return out & row_valid_bits(W, wx);
@@ -180,15 +178,15 @@ __device__ inline bool standard_layer(const MaskGeom &g, int l) {
     return g.ks[l - 1] == 3 && g.st[l - 1] == 1 && g.pd[l - 1] == 1;
 }
 
-template <bool U8>
-__global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) {
+template <bool U8, int NT>
+__global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     extern __shared__ uint64_t smem[];
-    __shared__ int red[kMaskThreads / 64];
+    __shared__ int red[NT / 64];
     __shared__ int s_tiles[RN_MAX_CONV + 1];
     const int HWW = g.H * g.WW;
     uint64_t *A = smem;
     uint64_t *B = smem + HWW;
-    float *lut = reinterpret_cast<float *>(smem + (g.dil ? max(2, g.L + 1) : 2) * HWW);
+    float *lut = reinterpret_cast<float *>(smem + (g.dil ? 2 * g.L + 1 : 2) * HWW);
 
     const int i = blockIdx.x;
     const int slot = a.ids[i];
@@ -304,45 +302,54 @@ __global__ __launch_bounds__(kMaskThreads) void k_masks(MaskGeom g, MaskArgs a) 
 
     if (g.dil) {
         // Every layer 3x3 stride 1 pad 1 (one grid): all layers' masks at once
-        // (layer l: the change set dilated by l), then all layers' tile words;
-        // two barriers instead of four per layer.
+        // (layer l: the change set dilated by l, rows then columns), then all
+        // layers' tile words; three barriers instead of four per layer.
+        // LDS: the change set, then the vertical ORs V_l (l = 1..L), then the
+        // masks M_l.  Each thread keeps its words' coordinates for all layers
+        // (V_l = V_{l-1} | the rows y - l and y + l; M_l from V_l's row).
         __shared__ int s_cnt[RN_MAX_CONV + 2];
         if (threadIdx.x < RN_MAX_CONV + 2) s_cnt[threadIdx.x] = 0;
         int nc = 0;
-        for (int e = threadIdx.x; e < (g.L + 1) * HWW; e += blockDim.x) {
-            const int l = e / HWW, w = e - l * HWW;
-            uint64_t v;
-            if (l == 0) {
-                v = A[w];
-                nc += __popcll(v);
-            } else {
-                const int y = w / g.WW;
-                v = dilate_word(A, g.H, g.W, g.WW, y, w - y * g.WW, l);
+        for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
+            const int y = w / g.WW, wx = w - y * g.WW;
+            uint64_t v = A[w];
+            nc += __popcll(v);
+            g.pmask[0][(size_t)slot * HWW + w] = v;
+            for (int l = 1; l <= g.L; ++l) {
+                if (y - l >= 0) v |= A[w - l * g.WW];
+                if (y + l < g.H) v |= A[w + l * g.WW];
                 smem[(size_t)l * HWW + w] = v;
             }
-            g.pmask[l][(size_t)slot * HWW + w] = v;
+        }
+        lds_sync();
+        for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
+            const int y = w / g.WW, wx = w - y * g.WW;
+            for (int l = 1; l <= g.L; ++l) {
+                const uint64_t v = hdilate_word(smem + (size_t)l * HWW + y * g.WW, g.W, g.WW, wx, l);
+                smem[(size_t)(g.L + l) * HWW + w] = v;
+                g.pmask[l][(size_t)slot * HWW + w] = v;
+            }
         }
         lds_sync();
         if (nc) atomicAdd(&s_cnt[RN_MAX_CONV + 1], nc);
         const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
         const int TMW = g.TMW, ntiles = g.TH * g.TW;
-        for (int e = wave; e < (g.L + 1) * TMW; e += (int)(blockDim.x >> 6)) {
-            const int l = e / TMW, wd = e - l * TMW;
-            const uint64_t *M = smem + (size_t)l * HWW;
+        for (int wd = wave; wd < TMW; wd += (int)(blockDim.x >> 6)) {
             const int t = 64 * wd + lane;
-            bool dirty = false;
-            if (t < ntiles) {
-                const int ty = t / g.TW, tx = t - ty * g.TW;
-                const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
-                const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+            const bool in = t < ntiles;
+            const int ty = in ? t / g.TW : 0, tx = in ? t - ty * g.TW : 0;
+            const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
+            const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+            for (int l = 0; l <= g.L; ++l) {
+                const uint64_t *M = smem + (size_t)(l == 0 ? 0 : g.L + l) * HWW;
                 uint64_t bits = 0;
-                for (int y = y0; y < y1; ++y) bits |= M[y * g.WW + wx] >> sh;
-                dirty = (bits & ((1ull << kTile) - 1ull)) != 0;
-            }
-            const uint64_t m = __ballot(dirty);
-            if (lane == 0) {
-                g.tmask[l][(size_t)slot * TMW + wd] = m;
-                if (m) atomicAdd(&s_cnt[l], __popcll(m));
+                if (in)
+                    for (int y = y0; y < y1; ++y) bits |= M[y * g.WW + wx] >> sh;
+                const uint64_t m = __ballot((bits & ((1ull << kTile) - 1ull)) != 0);
+                if (lane == 0) {
+                    g.tmask[l][(size_t)slot * TMW + wd] = m;
+                    if (m) atomicAdd(&s_cnt[l], __popcll(m));
+                }
             }
         }
         lds_sync();
@@ -743,18 +750,25 @@ hipError_t launch_var_lists(const VarMaskArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, hipStream_t s) {
+hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStream_t s) {
     MaskGeom g = geom;
     const size_t hww = (size_t)g.H * g.WW;
     bool all_std = true;
     for (int l = 0; l < g.L; ++l) all_std = all_std && g.ks[l] == 3 && g.st[l] == 1 && g.pd[l] == 1;
-    const size_t dil_bytes = (size_t)std::max(2, g.L + 1) * hww * sizeof(uint64_t) + 256 * sizeof(float);
+    const size_t dil_bytes = (size_t)(2 * g.L + 1) * hww * sizeof(uint64_t) + 256 * sizeof(float);
     g.dil = all_std && dil_bytes <= 48 * 1024 ? 1 : 0;
     const size_t shm = g.dil ? dil_bytes : 2 * hww * sizeof(uint64_t) + 256 * sizeof(float);
-    if (a.frame_u8)
-        hipLaunchKernelGGL(k_masks<true>, dim3(a.n), dim3(kMaskThreads), shm, s, g, a);
-    else
-        hipLaunchKernelGGL(k_masks<false>, dim3(a.n), dim3(kMaskThreads), shm, s, g, a);
+    const int nt = a.n <= cus ? 1024 : a.n <= 2 * cus ? 512 : 256;
+    auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(a.n), dim3(nt), shm, s, g, a); };
+    if (a.frame_u8) {
+        if (nt == 1024) go(k_masks<true, 1024>);
+        else if (nt == 512) go(k_masks<true, 512>);
+        else go(k_masks<true, 256>);
+    } else {
+        if (nt == 1024) go(k_masks<false, 1024>);
+        else if (nt == 512) go(k_masks<false, 512>);
+        else go(k_masks<false, 256>);
+    }
     return hipGetLastError();
 }
 
