@@ -44,7 +44,7 @@ struct Plan {
     size_t part_elems = 0;
     // byte offsets into the workspace
     size_t o_lut, o_xin, o_ring, o_dring, o_primed, o_ids, o_act[RN_MAX_CONV + 1], o_w[RN_MAX_CONV],
-        o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_nchg, o_ntile,
+        o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_tpfx[RN_MAX_CONV + 1], o_nchg, o_ntile,
         o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
     size_t w_bytes[RN_MAX_CONV] = {0};
@@ -201,6 +201,7 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     for (int l = 0; l <= p->L; ++l) {
         p->o_pm[l] = take(S * p->Hl[l] * p->WWl[l] * 8);
         p->o_tm[l] = take(S * p->TMWl[l] * 8);
+        p->o_tpfx[l] = take(l ? S * p->TMWl[l] * 4 : 0);
     }
     p->o_nchg = take(S * 4);
     p->o_ntile = take(S * (p->L + 1) * 4);
@@ -358,6 +359,8 @@ MaskGeom make_geom(reuse_net *net) {
     for (int l = 0; l <= p.L; ++l) {
         g.pmask[l] = net->at<uint64_t>(p.o_pm[l]);
         g.tmask[l] = net->at<uint64_t>(p.o_tm[l]);
+        // Per-slot word prefixes only pay for grids of many tile words.
+        g.tpfx[l] = l && p.TMW > 16 ? net->at<int32_t>(p.o_tpfx[l]) : nullptr;
     }
     return g;
 }
@@ -502,6 +505,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     ca.ntile = ma.ntile;
     for (int l = 0; l <= p.L; ++l) {
         ca.tmask[l] = g.tmask[l];
+        ca.tpfx[l] = g.tpfx[l];
         ca.wl[l] = l ? net->at<uint32_t>(p.o_wl[l]) : nullptr;
         ca.wls[l] = l ? net->at<uint32_t>(p.o_wls[l]) : nullptr;
     }

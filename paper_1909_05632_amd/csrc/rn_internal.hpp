@@ -33,6 +33,7 @@ struct MaskGeom {
     int ks[RN_MAX_CONV], st[RN_MAX_CONV], pd[RN_MAX_CONV];   // kernel, stride, pad of layer l + 1
     uint64_t *pmask[RN_MAX_CONV + 1];   // [S][Hl][WWl] per layer
     uint64_t *tmask[RN_MAX_CONV + 1];   // [S][TMWl] per layer
+    int32_t *tpfx[RN_MAX_CONV + 1];     // [S][TMWl] per layer 1..L: dirty tiles in the slot's earlier tile words (NULL: not kept)
 };
 
 // Per-step inputs of the mask kernel.
@@ -59,6 +60,7 @@ struct CompactArgs {
     const int32_t *ids;
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
+    const int32_t *tpfx[RN_MAX_CONV + 1];   // per-slot word prefixes written by k_masks
     uint32_t *wl[RN_MAX_CONV + 1];  // entries i << 16 | ty << 8 | tx (batch index i)
     uint32_t *wls[RN_MAX_CONV + 1]; // the same list as slot << 16 | ty << 8 | tx, for the kernels
     int32_t *cnt;                 // [L+1]

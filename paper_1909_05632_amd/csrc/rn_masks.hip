@@ -70,7 +70,7 @@ __device__ inline float load1(const void *frames, size_t off, const float *lut) 
 }
 
 // Write layer l's pixel mask and tile mask of one slot; returns the dirty tiles.
-__device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red) {
+__device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red, int *s_wc) {
     const int H = g.Hl[l], WW = g.WWl[l], TW = g.TWl[l];
     const int HWW = H * WW;
     uint64_t *pm = g.pmask[l] + (size_t)slot * HWW;
@@ -93,10 +93,34 @@ __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot,
         const uint64_t m = __ballot(dirty);
         if (lane == 0) {
             tm[base >> 6] = m;
+            if (l) s_wc[(l - 1) * g.TMW + (base >> 6)] = __popcll(m);
             cnt += __popcll(m);
         }
     }
     return block_sum(lane == 0 ? cnt : 0, red);
+}
+
+// tpfx[l][slot][w] = dirty tiles in tile words 0 .. w - 1 of layer l (1..L),
+// from the per-word counts in s_wc ([l - 1][w], row stride TMW); one wave per
+// layer, a wave scan per 64 words.
+__device__ void write_tpfx(const MaskGeom &g, const int *s_wc, int slot) {
+    if (g.tpfx[1] == nullptr) return;            // few words per layer: the list build sums them itself
+    const int lane = threadIdx.x & 63, nw = (int)(blockDim.x >> 6);
+    for (int l = 1 + (int)(threadIdx.x >> 6); l <= g.L; l += nw) {
+        const int TMWl = g.TMWl[l];
+        int run = 0;
+        for (int b = 0; b < TMWl; b += 64) {
+            const int w = b + lane;
+            const int c = w < TMWl ? s_wc[(l - 1) * g.TMW + w] : 0;
+            int x = c;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int y = __shfl_up(x, o, 64);
+                if (lane >= o) x += y;
+            }
+            if (w < TMWl) g.tpfx[l][(size_t)slot * TMWl + w] = run + x - c;
+            run += __shfl(x, 63, 64);
+        }
+    }
 }
 
 // Grow a change set by one pixel on every side (3x3 window), clipped to the
@@ -187,6 +211,7 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     uint64_t *A = smem;
     uint64_t *B = smem + HWW;
     float *lut = reinterpret_cast<float *>(smem + (g.dil ? 2 * g.L + 1 : 2) * HWW);
+    int *s_wc = reinterpret_cast<int *>(lut + 256);            // [L][TMW] dirty tiles per tile word
 
     const int i = blockIdx.x;
     const int slot = a.ids[i];
@@ -348,11 +373,13 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
                 const uint64_t m = __ballot((bits & ((1ull << kTile) - 1ull)) != 0);
                 if (lane == 0) {
                     g.tmask[l][(size_t)slot * TMW + wd] = m;
+                    if (l) s_wc[(l - 1) * TMW + wd] = __popcll(m);
                     if (m) atomicAdd(&s_cnt[l], __popcll(m));
                 }
             }
         }
         lds_sync();
+        write_tpfx(g, s_wc, slot);
         if (threadIdx.x == 0) {
             a.nchg[i] = s_cnt[RN_MAX_CONV + 1];
             for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_cnt[l];
@@ -366,7 +393,7 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     for (int w = threadIdx.x; w < HWW; w += blockDim.x) nchg += __popcll(A[w]);
     nchg = block_sum(nchg, red);
 
-    int t0 = emit_layer(g, A, 0, slot, red);
+    int t0 = emit_layer(g, A, 0, slot, red, s_wc);
     if (threadIdx.x == 0) s_tiles[0] = t0;
     for (int l = 1; l <= g.L; ++l) {
         lds_sync();
@@ -380,9 +407,10 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
             grow_general(g, l, A, B);
             lds_sync();
         }
-        const int tl = emit_layer(g, A, l, slot, red);
+        const int tl = emit_layer(g, A, l, slot, red, s_wc);
         if (threadIdx.x == 0) s_tiles[l] = tl;
     }
+    write_tpfx(g, s_wc, slot);                   // the last block_sum published every count
     if (threadIdx.x == 0) {
         a.nchg[i] = nchg;
         for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_tiles[l];
@@ -429,8 +457,9 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
 
 // Work lists, position-major: the entries of layer l are its dirty tiles in
 // (ty, tx, batch index) order.  One block per (64-position word wd, layer):
-//   - its offset is the number of dirty tiles at earlier positions, i.e. the
-//     popcount of tile-mask words 0..wd-1 of every stream;
+//   - its offset is the number of dirty tiles at earlier positions: over
+//     the streams, the popcount of tile-mask words 0..wd-1 (for grids of
+//     more than 16 words, the per-slot word prefix that k_masks wrote);
 //   - a 64 x 64 bit transpose per chunk of 64 streams (lane r holds stream
 //     r's word; six exchange stages leave lane j with position j's stream
 //     bitmap) gives per-position counts and the streams of each position.
@@ -482,15 +511,19 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     const int nch = (a.n + 63) / 64;
     const int nc0 = min(kChunksPerPass, nch);
 
-    // One pass over the streams (thread per stream, one slot load then
-    // independent word loads): dirty tiles at positions before this word, and
-    // the first pass's slots and words of this word staged in LDS.
+    // One pass over the streams (thread per stream): dirty tiles at positions
+    // before this word (the per-slot word prefix k_masks wrote), and the first
+    // pass's slots and words of this word staged in LDS.
     int pre = 0;
     for (int i = threadIdx.x; i < 64 * nc0 || i < a.n; i += blockDim.x) {
         const int slot = i < a.n ? a.ids[i] : -1;
-        if (slot >= 0) {
-            const uint64_t *tm = a.tmask[l] + (size_t)slot * TMW;
-            for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
+        if (slot >= 0 && wd > 0) {
+            if (a.tpfx[l] != nullptr) {
+                pre += a.tpfx[l][(size_t)slot * TMW + wd];
+            } else {
+                const uint64_t *tm = a.tmask[l] + (size_t)slot * TMW;
+                for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
+            }
         }
         if (i < 64 * nc0) {
             s_slot[i] = slot;
@@ -755,9 +788,10 @@ hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStr
     const size_t hww = (size_t)g.H * g.WW;
     bool all_std = true;
     for (int l = 0; l < g.L; ++l) all_std = all_std && g.ks[l] == 3 && g.st[l] == 1 && g.pd[l] == 1;
-    const size_t dil_bytes = (size_t)(2 * g.L + 1) * hww * sizeof(uint64_t) + 256 * sizeof(float);
+    const size_t tail = 256 * sizeof(float) + (size_t)g.L * g.TMW * sizeof(int);   // LUT, per-word tile counts
+    const size_t dil_bytes = (size_t)(2 * g.L + 1) * hww * sizeof(uint64_t) + tail;
     g.dil = all_std && dil_bytes <= 48 * 1024 ? 1 : 0;
-    const size_t shm = g.dil ? dil_bytes : 2 * hww * sizeof(uint64_t) + 256 * sizeof(float);
+    const size_t shm = g.dil ? dil_bytes : 2 * hww * sizeof(uint64_t) + tail;
     const int nt = a.n <= cus ? 1024 : a.n <= 2 * cus ? 512 : 256;
     auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(a.n), dim3(nt), shm, s, g, a); };
     if (a.frame_u8) {

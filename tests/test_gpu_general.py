@@ -69,6 +69,16 @@ def test_general_layers_single_channel_same_and_strided(torch):
         _run(torch, wl, 4, 6, weights, label=f"{convs}").close()
 
 
+def test_general_layers_wide_grid(torch):
+    # A 160x168 frame: 1680 tiles (27 tile words) on the 5x5/1 layer's grid, so
+    # the list build takes its per-word offsets from the mask kernel's per-slot
+    # prefixes; then 3x3/2 pad 1 to 80x84.
+    wl = synth.Workload(cid=115, streams=3, frames=4, h=160, w=168, convs=((32, 5, 1, 2), (64, 3, 2, 1)), n_out=6,
+                        n_sprites=5, smin=3, smax=8, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.1)
+    _run(torch, wl, 3, 4, weights, sample=[0, 2], label="wide general").close()
+
+
 def test_standard_layers_around_a_general_one(torch):
     # 3x3/1 pad 1 (standard first-layer kernel) -> 3x3/1 pad 0 (general: the grid
     # shrinks by 2) -> 3x3/1 pad 1 64->128 (standard staged MFMA kernel on the
