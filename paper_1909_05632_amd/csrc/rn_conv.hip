@@ -166,6 +166,122 @@ __global__ __launch_bounds__(256) void k_conv_first_f32(ConvArgs a) {
     }
 }
 
+// Layer 1 with four input channels (stacked frames, or a 4-channel input) on
+// the matrix cores: for every output channel count a lane-per-channel kernel
+// leaves lanes idle (40 channels use 40 of 64 lanes) and runs its FMAs at the
+// VALU rate.  Per tile an implicit GEMM on v_mfma_f32_16x16x4_f32: M = 16
+// pixels (row m = pixel (m / 4, m % 4)), N = COUT in blocks of 16 (padded with
+// zero weights), K = 36 in (c, ky, kx) order, nine k-steps; step s gives lane
+// group kq the K index 4 s + kq, a halo value gathered from LDS (offsets fixed
+// per lane), and the B fragments stay in registers for the kernel's life.
+// D: lane (n, kq) holds pixels 4 kq + i (row kq, column i) of channel
+// 16 nb + n.  The halo prefetch and the VAR handling are those of
+// k_conv_first_f32.
+template <int COUT, bool DENSE, bool VAR>
+__global__ __launch_bounds__(256) void k_conv_first4_mfma(ConvArgs a) {
+    constexpr int CIN = 4, KS = 9, NB = (COUT + 15) / 16;
+    constexpr int HN = 36 * CIN;                  // halo values
+    constexpr int HPL = (HN + 63) / 64;
+    __shared__ float s_halo[4][HN];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int mrow = lane & 15, kq = lane >> 4;
+    const float *wg = static_cast<const float *>(a.w);
+    float bw[KS][NB], bias[NB];
+    int aoff[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const int k = 4 * s + kq, c = k / 9, r = k - 9 * c, ky = r / 3, kx = r - 3 * ky;
+        aoff[s] = (((mrow >> 2) + ky) * 6 + (mrow & 3) + kx) * CIN + c;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int n = 16 * nb + mrow;
+            bw[s][nb] = n < COUT ? wg[k * COUT + n] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) bias[nb] = 16 * nb + mrow < COUT ? a.bias[16 * nb + mrow] : 0.f;
+
+    const int cnt = work_count<DENSE>(a);
+    const size_t HW = (size_t)a.H * a.W;
+    const int cin1 = CIN / a.stack;               // channels per frame
+    float *halo = s_halo[wave];
+    const float *xin = static_cast<const float *>(a.in);
+    float *outp = static_cast<float *>(a.out);
+    const XcdRange xr = xcd_range(cnt, 4);
+    auto load_tile = [&](int t, float *pv) __attribute__((always_inline)) {
+        const TileRef r = decode<DENSE>(a, t);
+        int head = 0;
+        if (!VAR && a.stack != 1) head = a.ring_head[r.slot];
+#pragma unroll
+        for (int k = 0; k < HPL; ++k) {
+            const int h = lane + 64 * k;
+            const int c = h / 36, pos = h - c * 36;
+            const int hy = pos / 6, hx = pos - hy * 6;
+            const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+            float v = 0.0f;
+            if (h < HN && y >= 0 && y < a.H && x >= 0 && x < a.W) {
+                if constexpr (VAR) {
+                    v = var_input(a, r.slot, c, y, x);
+                } else {
+                    const float *plane;
+                    if (a.stack == 1) {
+                        plane = xin + ((size_t)r.slot * CIN + c) * HW;
+                    } else {
+                        const int j = c / cin1, c1 = c - j * cin1;
+                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                        plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
+                    }
+                    v = plane[(size_t)y * a.W + x];
+                }
+            }
+            pv[k] = v;
+        }
+    };
+    int t = xr.first + wave;
+    if (t >= xr.end) return;
+    float pv[HPL];
+    load_tile(t, pv);
+    for (; t < xr.end; t += xr.stride) {
+        const TileRef r = decode<DENSE>(a, t);
+#pragma unroll
+        for (int k = 0; k < HPL; ++k) {
+            const int h = lane + 64 * k;
+            if (h < HN) {
+                const int c = h / 36, pos = h - c * 36;
+                halo[pos * CIN + c] = pv[k];
+            }
+        }
+        wave_sync();
+        float av[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) av[s] = halo[aoff[s]];
+        load_tile(min(t + xr.stride, xr.end - 1), pv);
+        floatx4 acc[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s], bw[s][nb], acc[nb], 0, 0, 0);
+        float *dst = VAR ? static_cast<float *>(a.vov_out) + (size_t)t * kTilePx * COUT
+                         : outp + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
+        const bool row_in = r.ty * kTile + kq < a.H;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int n = 16 * nb + mrow;
+            if (n >= COUT) continue;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float v = acc[nb][i] + bias[nb];
+                v = v > 0.0f ? v : 0.0f;
+                if (!row_in || r.tx * kTile + i >= a.W) v = 0.0f;
+                dst[(4 * kq + i) * COUT + n] = v;
+            }
+        }
+        wave_sync();                                   // halo reads done before the next tile's writes
+    }
+}
+
 // ------------------------------------------------------------------ MFMA layers
 
 // Implicit GEMM per tile: M = 16 pixels, N = COUT, K = 9 * CIN.
@@ -1021,8 +1137,14 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
 template <int CIN, int COUT, bool DENSE, bool VAR>
 hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
     const int total_max = a.max_tiles;
-    const int grid = persistent_grid(cus * 8, (total_max + 3) / 4);
-    hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    if constexpr (CIN == 4) {
+        // about 100-150 registers: four blocks of four waves are resident per CU
+        const int grid = persistent_grid(cus * 4, (total_max + 3) / 4);
+        hipLaunchKernelGGL((k_conv_first4_mfma<COUT, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    } else {
+        const int grid = persistent_grid(cus * 8, (total_max + 3) / 4);
+        hipLaunchKernelGGL((k_conv_first_f32<CIN, COUT, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 
