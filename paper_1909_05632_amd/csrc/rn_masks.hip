@@ -182,19 +182,23 @@ __device__ void grow_general(const MaskGeom &g, int l, uint64_t *src, uint64_t *
         mid[w] = acc;
     }
     lds_sync();
-    for (int w = threadIdx.x; w < Ho * WWo; w += blockDim.x) {
+    // One wave per output word, one lane per output bit (the window spans at
+    // most two input words: k <= 8), the word by ballot.
+    const int lane = threadIdx.x & 63;
+    for (int w = (int)(threadIdx.x >> 6); w < Ho * WWo; w += (int)(blockDim.x >> 6)) {
         const int y = w / WWo, wx = w - y * WWo;
         const uint64_t *row = mid + y * WWi;
-        uint64_t word = 0;
-        for (int j = 0; j < 64; ++j) {
-            const int x = 64 * wx + j;
-            if (x >= Wo) break;
-            const int c0 = max(s * x - p, 0), c1 = min(s * x - p + k, Wi);
-            bool any = false;
-            for (int cw = c0 >> 6; cw <= (c1 - 1) >> 6 && c0 < c1; ++cw) any |= (row[cw] & range_bits(c0, c1, cw)) != 0;
-            word |= (uint64_t)any << j;
+        const int x = 64 * wx + lane;
+        const int c0 = max(s * x - p, 0), c1 = min(s * x - p + k, Wi);
+        bool any = false;
+        if (x < Wo && c0 < c1) {
+            const int w0 = c0 >> 6, w1 = (c1 - 1) >> 6, sh = c0 & 63;
+            uint64_t bits = row[w0] >> sh;
+            if (w1 != w0) bits |= row[w1] << (64 - sh);     // sh > 0 here: the window crosses a word edge
+            any = (bits & ((1ull << (c1 - c0)) - 1ull)) != 0;
         }
-        src[w] = word;
+        const uint64_t word = __ballot(any);
+        if (lane == 0) src[w] = word;
     }
 }
 
