@@ -927,7 +927,8 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
 // on one tile at a time and splits its K blocks four ways (these layers have
 // few tiles on their small grids, so a launch lasts about one tile's latency);
 // the four partial products are added in LDS in wave order and wave 0 runs
-// the epilogue;
+// the epilogue; the next tile's patch is fetched into registers during this
+// tile's matrix work;
 // the epilogue is the one of the 3x3 kernels (bias, ReLU, zero outside the
 // output grid, tile head partials on the last layer, cache store).
 // FIRST: the input is the float32 input cache (planar, a ring of 4 frames when
@@ -948,22 +949,37 @@ struct Gen {
     static_assert(COUT % 16 == 0, "16-column blocks");
 };
 
-// Threads idx, idx + nt, ... of the block load the patch of tile r.
+// The patch of tile r, thread idx's share (elements idx, idx + 256, ...), in
+// registers: PF values per thread (scalars from the input frames, FIRST), or
+// PF 16-byte channel groups (cache layers).  Every load is issued before any
+// is used; out-of-image elements are zero.
 template <int KS, int ST, int CIN, int COUT, bool FIRST>
-__device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float *halo, int idx, int nt) {
+struct GenPatch {
     using G = Gen<KS, ST, CIN, COUT>;
+    static constexpr int N = FIRST ? G::HALO : G::E * G::E * (CIN / 4);   // elements
+    static constexpr int PF = (N + 255) / 256;                            // per thread
+    using T = typename std::conditional<FIRST, float, float4>::type;
+};
+
+template <int KS, int ST, int CIN, int COUT, bool FIRST>
+__device__ inline void gen_fetch_patch(const ConvArgs &a, const TileRef &r,
+                                       typename GenPatch<KS, ST, CIN, COUT, FIRST>::T *v, int idx) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    using P = GenPatch<KS, ST, CIN, COUT, FIRST>;
     const int y0 = 4 * ST * r.ty - a.pad, x0 = 4 * ST * r.tx - a.pad;
     if constexpr (FIRST) {
         const float *xin = static_cast<const float *>(a.in);
         const size_t HW = (size_t)a.Hin * a.Win;
         const int cin1 = CIN / a.stack;
         const int head = a.stack != 1 ? a.ring_head[r.slot] : 0;
-        for (int h = idx; h < G::HALO; h += nt) {
+#pragma unroll
+        for (int k = 0; k < P::PF; ++k) {
+            const int h = idx + 256 * k;
             const int c = h / (G::E * G::E), pos = h - c * (G::E * G::E);
             const int hy = pos / G::E, hx = pos - hy * G::E;
             const int y = y0 + hy, x = x0 + hx;
-            float v = 0.0f;
-            if (y >= 0 && y < a.Hin && x >= 0 && x < a.Win) {
+            float val = 0.0f;
+            if (h < P::N && y >= 0 && y < a.Hin && x >= 0 && x < a.Win) {
                 const float *plane;
                 if (a.stack == 1) {
                     plane = xin + ((size_t)r.slot * CIN + c) * HW;
@@ -972,26 +988,49 @@ __device__ inline void gen_load_patch(const ConvArgs &a, const TileRef &r, float
                     const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
                     plane = xin + (((size_t)r.slot * 4 + rp) * cin1 + c1) * HW;
                 }
-                v = plane[(size_t)y * a.Win + x];
+                val = plane[(size_t)y * a.Win + x];
             }
-            halo[pos * CIN + c] = v;
+            v[k] = val;
         }
     } else {
         static_assert(CIN % 4 == 0, "cache layers carry whole 16-byte channel groups");
         constexpr int C4 = CIN / 4;
         const float *src = static_cast<const float *>(a.in) + (size_t)r.slot * a.in_stride;
-        for (int h = idx; h < G::E * G::E * C4; h += nt) {
+#pragma unroll
+        for (int k = 0; k < P::PF; ++k) {
+            const int h = idx + 256 * k;
             const int pos = h / C4, c4 = h - pos * C4;
             const int hy = pos / G::E, hx = pos - hy * G::E;
             const int y = y0 + hy, x = x0 + hx;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
-                v = *reinterpret_cast<const float4 *>(
+            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (h < P::N && y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
+                val = *reinterpret_cast<const float4 *>(
                     src + ((size_t)((y >> 2) * a.TWin + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN + 4 * c4);
-            *reinterpret_cast<float4 *>(halo + pos * CIN + 4 * c4) = v;
+            v[k] = val;
         }
     }
 }
+
+// The fetched patch into LDS, channel-innermost.
+template <int KS, int ST, int CIN, int COUT, bool FIRST>
+__device__ inline void gen_store_patch(float *halo, const typename GenPatch<KS, ST, CIN, COUT, FIRST>::T *v, int idx) {
+    using G = Gen<KS, ST, CIN, COUT>;
+    using P = GenPatch<KS, ST, CIN, COUT, FIRST>;
+#pragma unroll
+    for (int k = 0; k < P::PF; ++k) {
+        const int h = idx + 256 * k;
+        if (h >= P::N) break;
+        if constexpr (FIRST) {
+            const int c = h / (G::E * G::E), pos = h - c * (G::E * G::E);
+            halo[pos * CIN + c] = v[k];
+        } else {
+            constexpr int C4 = CIN / 4;
+            const int pos = h / C4, c4 = h - pos * C4;
+            *reinterpret_cast<float4 *>(halo + pos * CIN + 4 * c4) = v[k];
+        }
+    }
+}
+
 
 // A values of block b for this lane: K = 16 b + 4 kq + j, j = 0..3, of tile
 // pixel (py, px).
@@ -1033,10 +1072,16 @@ __global__ __launch_bounds__(256) void k_conv_gen(ConvArgs a) {
     const int m = lane & 15, kq = lane >> 4;
     const int py = m & 3, px = m >> 2;
     const int b0 = wave * G::NBW;                         // this wave's K blocks [b0, b0 + NBW)
+    // The next tile's patch is fetched into registers while this tile's
+    // matrix work runs (past the end: the last tile again, never used).
+    using P = GenPatch<KS, ST, CIN, COUT, FIRST>;
+    typename P::T pv[P::PF];
+    if (xr.first < xr.end) gen_fetch_patch<KS, ST, CIN, COUT, FIRST>(a, decode<DENSE>(a, xr.first), pv, tid);
     for (int t = xr.first; t < xr.end; t += xr.stride) {  // uniform per block
         const TileRef r = decode<DENSE>(a, t);
         lds_barrier();                                    // the previous tile's epilogue is done with the area
-        gen_load_patch<KS, ST, CIN, COUT, FIRST>(a, r, halo, tid, (int)blockDim.x);
+        gen_store_patch<KS, ST, CIN, COUT, FIRST>(halo, pv, tid);
+        gen_fetch_patch<KS, ST, CIN, COUT, FIRST>(a, decode<DENSE>(a, min(t + xr.stride, xr.end - 1)), pv, tid);
         lds_barrier();
         floatx4 acc[G::NB];
 #pragma unroll
