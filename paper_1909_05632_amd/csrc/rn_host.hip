@@ -100,6 +100,9 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     if (p->TH > 256 || p->TW > 256) return fail(RN_EUNSUPPORTED, "frames above 1024 x 1024 are not implemented");
     p->ntiles = p->TH * p->TW;
     p->TMW = ceil_div(p->ntiles, 64);
+    if (masks_lds_bytes(p->H, p->WW, cfg->n_conv, p->TMW) > kMasksLdsMax)
+        return fail(RN_EUNSUPPORTED, "frame too large: the mask kernel keeps two bit planes of it in LDS "
+                                     "(in_h x ceil(in_w / 64) must stay under about 10000 words)");
     p->Hl[0] = p->H;
     p->Wl[0] = p->W;
     for (int l = 0; l < cfg->n_conv; ++l) {

@@ -187,6 +187,8 @@ struct HeadArgs {
 
 // Launchers (each returns the hipGetLastError of its launch).
 hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, int cus, hipStream_t s);
+size_t masks_lds_bytes(int H, int WW, int L, int TMW);   // dynamic LDS of the layer-by-layer mask kernel
+constexpr size_t kMasksLdsMax = 160 * 1024 - 1024;       // per block, less the static arrays
 hipError_t launch_prime(const PrimeArgs &a, hipStream_t s);
 hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s);
 size_t tile_head_w_elems(int ntiles, int cout, int n_out);

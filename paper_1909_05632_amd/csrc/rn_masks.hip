@@ -787,6 +787,12 @@ hipError_t launch_var_lists(const VarMaskArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Dynamic LDS of k_masks growing layer by layer: two bit planes of the input
+// grid, the LUT and the per-word tile counts.
+size_t masks_lds_bytes(int H, int WW, int L, int TMW) {
+    return (size_t)2 * H * WW * sizeof(uint64_t) + 256 * sizeof(float) + (size_t)L * TMW * sizeof(int);
+}
+
 hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStream_t s) {
     MaskGeom g = geom;
     const size_t hww = (size_t)g.H * g.WW;
@@ -795,9 +801,17 @@ hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStr
     const size_t tail = 256 * sizeof(float) + (size_t)g.L * g.TMW * sizeof(int);   // LUT, per-word tile counts
     const size_t dil_bytes = (size_t)(2 * g.L + 1) * hww * sizeof(uint64_t) + tail;
     g.dil = all_std && dil_bytes <= 48 * 1024 ? 1 : 0;
-    const size_t shm = g.dil ? dil_bytes : 2 * hww * sizeof(uint64_t) + tail;
+    const size_t shm = g.dil ? dil_bytes : masks_lds_bytes(g.H, g.WW, g.L, g.TMW);
     const int nt = a.n <= cus ? 1024 : a.n <= 2 * cus ? 512 : 256;
-    auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(a.n), dim3(nt), shm, s, g, a); };
+    hipError_t attr = hipSuccess;
+    auto go = [&](auto kern) {
+        // Above the default 64 KiB of dynamic LDS (frames of more than ~4 K
+        // mask words) the kernel has to be allowed more; create checks the limit.
+        if (shm > 64 * 1024)
+            attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)shm);
+        if (attr == hipSuccess) hipLaunchKernelGGL(kern, dim3(a.n), dim3(nt), shm, s, g, a);
+    };
     if (a.frame_u8) {
         if (nt == 1024) go(k_masks<true, 1024>);
         else if (nt == 512) go(k_masks<true, 512>);
@@ -807,7 +821,7 @@ hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStr
         else if (nt == 512) go(k_masks<false, 512>);
         else go(k_masks<false, 256>);
     }
-    return hipGetLastError();
+    return attr != hipSuccess ? attr : hipGetLastError();
 }
 
 hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {

@@ -92,6 +92,13 @@ def test_general_layer_configs():
     assert B.reuse_net_workspace_bytes(cfg(h=12, w=12)) == 0            # no output pixels left
 
 
+def test_frame_size_limit_of_the_mask_kernel():
+    # Two bit planes of the frame in LDS: 640 x 448 (4480 words, more than the
+    # default 64 KiB of dynamic LDS) is accepted, 1024 x 1024 is not.
+    assert B.reuse_net_workspace_bytes(_cfg(h=640, w=448, streams=1)) > 0
+    assert B.reuse_net_workspace_bytes(_cfg(h=1024, w=1024, streams=1)) == 0
+
+
 @pytest.mark.parametrize("bad", [
     dict(k=2, p=0),                   # 2x2 kernel: no kernel for these shapes
     dict(p=0),                        # 3x3 without padding: no kernel for 1->40
@@ -139,6 +146,8 @@ def test_create_reports_argument_errors_without_touching_the_gpu():
     assert st == B.RN_EUNSUPPORTED and h is None and "kernel" in msg
     st, h, msg = _create(_cfg(tile=8))
     assert st == B.RN_EUNSUPPORTED and "tile" in msg
+    st, h, msg = _create(_cfg(h=1024, w=1024))
+    assert st == B.RN_EUNSUPPORTED and "frame too large" in msg
     st, h, msg = _create(_cfg(), weights=False)
     assert st == B.RN_EINVAL and "weights" in msg
     st, h, msg = _create(_cfg(), nbytes=1024)

@@ -334,3 +334,30 @@ def test_bf16_fullres_210x160(torch):
     weights = synth.net_weights(wl)
     _run_sequence(torch, wl, 2, 3, weights, sample=[0], value_every=10, label="bf16 210x160",
                   act_dtype="bf16").close()
+
+
+def test_large_frame_masks_beyond_64k_lds(torch):
+    # 640 x 448 frames: the mask kernel's two bit planes take ~72 KB of LDS
+    # (above the default dynamic limit).  Masks and work lists of every step
+    # bit-exact against the oracle; the logits of every reuse step are the bits
+    # of a full recompute of the same frame (the oracle's own full forward at
+    # this size takes ~20 s on the host, so the values are pinned by the smaller
+    # tests).
+    wl = synth.Workload(cid=140, streams=2, frames=3, h=640, w=448, convs=(40, 80), n_out=6,
+                        n_sprites=8, smin=4, smax=10, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    u8x, x = sprite_inputs(wl, range(2), 3)
+    a, b = make_net(wl, 2, weights), make_net(wl, 2, weights)
+    onet = oracle_net(wl)
+    dev = torch.from_numpy(x).cuda()
+    prev = None
+    for t in range(3):
+        cur = dev[t][:, None].contiguous()
+        la = a.step(cur).cpu().numpy()
+        lb = b.full(cur).cpu().numpy()
+        assert np.array_equal(la.view(np.uint32), lb.view(np.uint32)), f"t={t}"
+        xs = x[t][:, None]
+        check_masks(a, onet, oracle_d0(prev, xs, primed=t > 0), np.arange(2), label=f"640x448 t={t}")
+        prev = xs
+    a.close()
+    b.close()
