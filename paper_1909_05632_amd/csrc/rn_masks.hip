@@ -503,6 +503,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     __shared__ int red[kThreads / 64];
     __shared__ int s_cnt[64];
     __shared__ int s_run[64];
+    __shared__ int s_most;
     __shared__ int s_base[kChunksPerPass][64];
     __shared__ uint64_t s_bal[kChunksPerPass][64];
     __shared__ int32_t s_slot[kChunksPerPass * 64];
@@ -577,33 +578,59 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
             for (int cc = wave; cc < nc; cc += nwaves) s_bal[cc][lane] = transpose64(s_word[cc * 64 + lane], lane);
             lds_sync();
         }
+        const int npos = min(64, ntiles - 64 * wd);       // positions of this word inside the grid
         if (threadIdx.x < 64) {
-            int r = s_run[threadIdx.x];
+            int r = s_run[threadIdx.x], most = 0;
             for (int cc = 0; cc < nc; ++cc) {
                 s_base[cc][threadIdx.x] = r;
-                r += __popcll(s_bal[cc][threadIdx.x]);
+                const int c = __popcll(s_bal[cc][threadIdx.x]);
+                r += c;
+                most = max(most, c);
             }
             s_run[threadIdx.x] = r;
+            for (int o = 32; o > 0; o >>= 1) most = max(most, __shfl_xor(most, o, 64));
+            if (threadIdx.x == 0) s_most = most;
         }
         lds_sync();
-        // One thread per (chunk, position): walk the set bits of the position's
-        // stream bitmap; its entries are [base, base + popcount) in stream order.
-        for (int pi = threadIdx.x; pi < nc * 64; pi += blockDim.x) {
-            const int cc = pi >> 6, j = pi & 63;
-            const int t = 64 * wd + j;
-            uint64_t b = s_bal[cc][j];
-            if (t >= ntiles) continue;
-            const uint32_t pos = ((uint32_t)(t / TW) << 8) | (uint32_t)(t % TW);
-            int idx = s_base[cc][j];
-            while (b) {
-                const int k = __ffsll((long long)b) - 1;  // next stream of this position
-                b &= b - 1;
-                const int i = 64 * (c0 + cc) + k;
-                if ((size_t)idx < cap) {
-                    a.wl[l][idx] = ((uint32_t)i << 16) | pos;
-                    a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
+        // Entries of (chunk cc, position j) are [base, base + popcount) in
+        // stream order.  Either one thread per (chunk, position) walks the set
+        // bits of its stream bitmap, or, when the busiest bitmap has more bits
+        // than a wave has bitmaps to visit (few positions, dense bitmaps: small
+        // grids of strided layers), one wave per bitmap with a lane per stream
+        // (rank among the set bits by mbcnt).  Both write the same entries.
+        if (s_most > (nc * npos + nwaves - 1) / nwaves) {
+            for (int q = wave; q < nc * npos; q += nwaves) {
+                const int cc = q / npos, j = q - cc * npos;
+                const uint64_t b = s_bal[cc][j];
+                if ((b >> lane) & 1ull) {
+                    const int t = 64 * wd + j;
+                    const uint32_t pos = ((uint32_t)(t / TW) << 8) | (uint32_t)(t % TW);
+                    const int idx = s_base[cc][j] + (int)__builtin_amdgcn_mbcnt_hi(
+                                        (uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+                    if ((size_t)idx < cap) {
+                        a.wl[l][idx] = ((uint32_t)(64 * (c0 + cc) + lane) << 16) | pos;
+                        a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + lane] << 16) | pos;
+                    }
                 }
-                ++idx;
+            }
+        } else {
+            for (int pi = threadIdx.x; pi < nc * 64; pi += blockDim.x) {
+                const int cc = pi >> 6, j = pi & 63;
+                const int t = 64 * wd + j;
+                uint64_t b = s_bal[cc][j];
+                if (j >= npos) continue;
+                const uint32_t pos = ((uint32_t)(t / TW) << 8) | (uint32_t)(t % TW);
+                int idx = s_base[cc][j];
+                while (b) {
+                    const int k = __ffsll((long long)b) - 1;  // next stream of this position
+                    b &= b - 1;
+                    const int i = 64 * (c0 + cc) + k;
+                    if ((size_t)idx < cap) {
+                        a.wl[l][idx] = ((uint32_t)i << 16) | pos;
+                        a.wls[l][idx] = ((uint32_t)s_slot[cc * 64 + k] << 16) | pos;
+                    }
+                    ++idx;
+                }
             }
         }
     }
