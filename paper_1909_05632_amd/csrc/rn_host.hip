@@ -492,7 +492,13 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     ma.primed = net->at<int32_t>(p.o_primed);
     ma.nchg = net->at<int32_t>(p.o_nchg);
     ma.ntile = net->at<int32_t>(p.o_ntile);
-    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, net->cus, s); });
+    for (int l = 1; l <= p.L; ++l) {
+        ma.wl[l] = net->at<uint32_t>(p.o_wl[l]);
+        ma.wls[l] = net->at<uint32_t>(p.o_wls[l]);
+    }
+    ma.cnt = net->at<int32_t>(p.o_cnt);
+    bool fused = false;
+    hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_masks(g, ma, net->cus, s, &fused); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("mask kernel: ") + hipGetErrorString(e));
 
     CompactArgs ca{};
@@ -513,8 +519,10 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
         ca.wls[l] = l ? net->at<uint32_t>(p.o_wls[l]) : nullptr;
     }
     ca.cnt = net->at<int32_t>(p.o_cnt);
-    e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
-    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
+    if (!fused) {
+        e = timed(net, RN_PHASE_COMPACT, s, [&] { return launch_compact(ca, s); });
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
+    }
 
     e = run_layers(net, n, ids, ca.wls, ca.cnt, logits, s, false);
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));

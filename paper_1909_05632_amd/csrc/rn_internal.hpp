@@ -52,6 +52,13 @@ struct MaskArgs {
     int32_t *primed;              // [S]
     int32_t *nchg;                // [n] changed pixels
     int32_t *ntile;               // [n][L+1] dirty tiles per layer
+    // Work lists of layers 1..L (as CompactArgs); with one stream the mask
+    // kernel writes them itself (fuse_lists, set by launch_masks) and no
+    // compaction launch follows.
+    uint32_t *wl[RN_MAX_CONV + 1];
+    uint32_t *wls[RN_MAX_CONV + 1];
+    int32_t *cnt;
+    int fuse_lists;
 };
 
 struct CompactArgs {
@@ -186,7 +193,9 @@ struct HeadArgs {
 };
 
 // Launchers (each returns the hipGetLastError of its launch).
-hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, int cus, hipStream_t s);
+// Sets *fused when the kernel also wrote the work lists (one stream, lists
+// given in a.wl / a.wls / a.cnt): the caller then skips launch_compact.
+hipError_t launch_masks(const MaskGeom &g, const MaskArgs &a, int cus, hipStream_t s, bool *fused);
 size_t masks_lds_bytes(int H, int WW, int L, int TMW);   // dynamic LDS of the layer-by-layer mask kernel
 constexpr size_t kMasksLdsMax = 160 * 1024 - 1024;       // per block, less the static arrays
 hipError_t launch_prime(const PrimeArgs &a, hipStream_t s);

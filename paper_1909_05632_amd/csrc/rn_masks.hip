@@ -70,7 +70,8 @@ __device__ inline float load1(const void *frames, size_t off, const float *lut) 
 }
 
 // Write layer l's pixel mask and tile mask of one slot; returns the dirty tiles.
-__device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red, int *s_wc) {
+__device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red, int *s_wc,
+                          uint64_t *s_tw) {
     const int H = g.Hl[l], WW = g.WWl[l], TW = g.TWl[l];
     const int HWW = H * WW;
     uint64_t *pm = g.pmask[l] + (size_t)slot * HWW;
@@ -94,6 +95,7 @@ __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot,
         if (lane == 0) {
             tm[base >> 6] = m;
             if (l) s_wc[(l - 1) * g.TMW + (base >> 6)] = __popcll(m);
+            if (l && s_tw) s_tw[(l - 1) * g.TMW + (base >> 6)] = m;
             cnt += __popcll(m);
         }
     }
@@ -120,6 +122,44 @@ __device__ void write_tpfx(const MaskGeom &g, const int *s_wc, int slot) {
             if (w < TMWl) g.tpfx[l][(size_t)slot * TMWl + w] = run + x - c;
             run += __shfl(x, 63, 64);
         }
+    }
+}
+
+// Work lists of a batch of one stream (batch index 0), from the tile words
+// and per-word counts in LDS: layer l's entries are its dirty tiles in
+// position order, as the compaction kernel writes them.  One wave per layer:
+// a wave scan of the word counts gives each word's offset, then a lane per
+// tile bit writes the entry at offset + the set bits below it (mbcnt).
+__device__ void write_lists(const MaskGeom &g, const MaskArgs &a, const int *s_wc, const uint64_t *s_tw, int slot) {
+    const int lane = threadIdx.x & 63, nw = (int)(blockDim.x >> 6);
+    for (int l = 1 + (int)(threadIdx.x >> 6); l <= g.L; l += nw) {
+        const int TMWl = g.TMWl[l], TWl = g.TWl[l];
+        int run = 0;
+        for (int b = 0; b < TMWl; b += 64) {
+            const int w = b + lane;
+            const int c = w < TMWl ? s_wc[(l - 1) * g.TMW + w] : 0;
+            int x = c;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int y = __shfl_up(x, o, 64);
+                if (lane >= o) x += y;
+            }
+            const int pre = run + x - c;
+            const int nwc = min(64, TMWl - b);
+            for (int j = 0; j < nwc; ++j) {
+                const uint64_t m = s_tw[(l - 1) * g.TMW + b + j];
+                const int base = __shfl(pre, j, 64);
+                if ((m >> lane) & 1ull) {
+                    const int t = 64 * (b + j) + lane;
+                    const uint32_t pos = ((uint32_t)(t / TWl) << 8) | (uint32_t)(t % TWl);
+                    const int idx = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                    a.wl[l][idx] = pos;                           // batch index 0
+                    a.wls[l][idx] = ((uint32_t)slot << 16) | pos;
+                }
+            }
+            run += __shfl(x, 63, 64);
+        }
+        if (lane == 0) a.cnt[l] = run;                            // at most the layer's tiles: the list's capacity
     }
 }
 
@@ -214,7 +254,11 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     const int HWW = g.H * g.WW;
     uint64_t *A = smem;
     uint64_t *B = smem + HWW;
-    float *lut = reinterpret_cast<float *>(smem + (g.dil ? 2 * g.L + 1 : 2) * HWW);
+    // After the bit planes: the tile words of layers 1..L when this kernel
+    // writes the lists ([L][TMW]), the level LUT, the per-word tile counts.
+    uint64_t *s_tw = a.fuse_lists ? smem + (g.dil ? 2 * g.L + 1 : 2) * HWW : nullptr;
+    float *lut = reinterpret_cast<float *>(smem + (g.dil ? 2 * g.L + 1 : 2) * HWW +
+                                           (a.fuse_lists ? g.L * g.TMW : 0));
     int *s_wc = reinterpret_cast<int *>(lut + 256);            // [L][TMW] dirty tiles per tile word
 
     const int i = blockIdx.x;
@@ -378,12 +422,14 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
                 if (lane == 0) {
                     g.tmask[l][(size_t)slot * TMW + wd] = m;
                     if (l) s_wc[(l - 1) * TMW + wd] = __popcll(m);
+                    if (l && s_tw) s_tw[(l - 1) * TMW + wd] = m;
                     if (m) atomicAdd(&s_cnt[l], __popcll(m));
                 }
             }
         }
         lds_sync();
         write_tpfx(g, s_wc, slot);
+        if (a.fuse_lists) write_lists(g, a, s_wc, s_tw, slot);
         if (threadIdx.x == 0) {
             a.nchg[i] = s_cnt[RN_MAX_CONV + 1];
             for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_cnt[l];
@@ -397,7 +443,7 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     for (int w = threadIdx.x; w < HWW; w += blockDim.x) nchg += __popcll(A[w]);
     nchg = block_sum(nchg, red);
 
-    int t0 = emit_layer(g, A, 0, slot, red, s_wc);
+    int t0 = emit_layer(g, A, 0, slot, red, s_wc, s_tw);
     if (threadIdx.x == 0) s_tiles[0] = t0;
     for (int l = 1; l <= g.L; ++l) {
         lds_sync();
@@ -411,10 +457,11 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
             grow_general(g, l, A, B);
             lds_sync();
         }
-        const int tl = emit_layer(g, A, l, slot, red, s_wc);
+        const int tl = emit_layer(g, A, l, slot, red, s_wc, s_tw);
         if (threadIdx.x == 0) s_tiles[l] = tl;
     }
     write_tpfx(g, s_wc, slot);                   // the last block_sum published every count
+    if (a.fuse_lists) write_lists(g, a, s_wc, s_tw, slot);
     if (threadIdx.x == 0) {
         a.nchg[i] = nchg;
         for (int l = 0; l <= g.L; ++l) a.ntile[(size_t)i * (g.L + 1) + l] = s_tiles[l];
@@ -820,15 +867,22 @@ size_t masks_lds_bytes(int H, int WW, int L, int TMW) {
     return (size_t)2 * H * WW * sizeof(uint64_t) + 256 * sizeof(float) + (size_t)L * TMW * sizeof(int);
 }
 
-hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &a, int cus, hipStream_t s) {
+hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &args, int cus, hipStream_t s, bool *fused) {
     MaskGeom g = geom;
+    MaskArgs a = args;
     const size_t hww = (size_t)g.H * g.WW;
     bool all_std = true;
     for (int l = 0; l < g.L; ++l) all_std = all_std && g.ks[l] == 3 && g.st[l] == 1 && g.pd[l] == 1;
     const size_t tail = 256 * sizeof(float) + (size_t)g.L * g.TMW * sizeof(int);   // LUT, per-word tile counts
     const size_t dil_bytes = (size_t)(2 * g.L + 1) * hww * sizeof(uint64_t) + tail;
     g.dil = all_std && dil_bytes <= 48 * 1024 ? 1 : 0;
-    const size_t shm = g.dil ? dil_bytes : masks_lds_bytes(g.H, g.WW, g.L, g.TMW);
+    size_t shm = g.dil ? dil_bytes : masks_lds_bytes(g.H, g.WW, g.L, g.TMW);
+    // One stream: the block that has its tile words also writes the lists
+    // (saving the compaction launch), when their words fit the default LDS.
+    const size_t tw_bytes = (size_t)g.L * g.TMW * sizeof(uint64_t);
+    a.fuse_lists = a.n == 1 && a.wl[1] != nullptr && shm + tw_bytes <= 64 * 1024 ? 1 : 0;
+    if (a.fuse_lists) shm += tw_bytes;
+    *fused = a.fuse_lists != 0;
     const int nt = a.n <= cus ? 1024 : a.n <= 2 * cus ? 512 : 256;
     hipError_t attr = hipSuccess;
     auto go = [&](auto kern) {

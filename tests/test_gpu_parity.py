@@ -187,6 +187,39 @@ def test_reset_recomputes_everything(torch):
     net.close()
 
 
+def test_batches_of_one_stream_between_larger_ones(torch):
+    # A batch of one stream gets its work lists from the mask kernel itself
+    # (no compaction launch).  Batches of one and of several streams alternate
+    # on one net, over cache slots other than 0 and slots seen for the first
+    # time (all changed) next to primed ones, for a net of 3x3 layers (every
+    # layer's mask at once) and one of strided general layers (growth layer by
+    # layer); every step's masks, lists, logits and activations match the oracle.
+    batches = [[3], [0, 3, 4], [3], [1], [4, 1], [1], [3], [2]]
+    F = len(batches)
+    for cid, convs in [(140, (40, 80)), (141, ((32, 7, 2, 3), (64, 3, 2, 1)))]:
+        wl = synth.Workload(cid=cid, streams=5, frames=F, h=37, w=68, convs=convs, n_out=6,
+                            n_sprites=3, smin=2, smax=6, vmin=1, vmax=3)
+        weights = synth.net_weights(wl, bias_std=0.1)
+        _, x = sprite_inputs(wl, range(5), F)                 # [F][5][H][W]
+        net = make_net(wl, 5, weights)
+        onet = oracle_net(wl)
+        dev = torch.from_numpy(x).cuda()
+        seen = {}
+        for t, b in enumerate(batches):
+            slots = np.asarray(b)
+            ids = torch.from_numpy(slots.astype(np.int32)).cuda()
+            logits = net.step(dev[t][ids.long()][:, None].contiguous(), stream_ids=ids).cpu().numpy()
+            cur = x[t][slots][:, None]
+            d0 = np.stack([oracle.diff(seen[s], cur[j]) if s in seen else np.ones((wl.h, wl.w), np.uint8)
+                           for j, s in enumerate(b)])
+            label = f"convs={convs} t={t} batch={b}"
+            check_masks(net, onet, d0, slots, label=label)
+            check_values(net, onet, weights, cur, slots, list(range(len(b))), logits, label=label)
+            for j, s in enumerate(b):
+                seen[s] = cur[j]
+        net.close()
+
+
 def test_change_boxes_occlusion(torch):
     # Known-change mode: prime every stream on the base image with the dense
     # path, then move an 8x8 zero patch along a row with explicit boxes: each
