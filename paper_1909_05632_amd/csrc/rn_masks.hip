@@ -69,6 +69,16 @@ __device__ inline float load1(const void *frames, size_t off, const float *lut) 
     else return static_cast<const float *>(frames)[off];
 }
 
+// OR of mask word wx of the tile rows y0 .. y0 + 3 that lie inside the H rows
+// (the four LDS reads issued together, not one round trip per row).
+__device__ inline uint64_t tile_rows(const uint64_t *M, int y0, int H, int WW, int wx) {
+    static_assert(kTile == 4, "four rows per tile");
+    uint64_t r[kTile];
+#pragma unroll
+    for (int k = 0; k < kTile; ++k) r[k] = y0 + k < H ? M[(y0 + k) * WW + wx] : 0ull;
+    return (r[0] | r[1]) | (r[2] | r[3]);
+}
+
 // Write layer l's pixel mask and tile mask of one slot; returns the dirty tiles.
 __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot, int *red, int *s_wc,
                           uint64_t *s_tw) {
@@ -86,9 +96,7 @@ __device__ int emit_layer(const MaskGeom &g, const uint64_t *A, int l, int slot,
         if (t < ntiles) {
             const int ty = t / TW, tx = t - ty * TW;
             const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
-            const int y0 = ty * kTile, y1 = min(y0 + kTile, H);
-            uint64_t bits = 0;
-            for (int y = y0; y < y1; ++y) bits |= A[y * WW + wx] >> sh;
+            const uint64_t bits = tile_rows(A, ty * kTile, H, WW, wx) >> sh;
             dirty = (bits & ((1ull << kTile) - 1ull)) != 0;
         }
         const uint64_t m = __ballot(dirty);
@@ -412,12 +420,10 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
             const bool in = t < ntiles;
             const int ty = in ? t / g.TW : 0, tx = in ? t - ty * g.TW : 0;
             const int x0 = tx * kTile, wx = x0 >> 6, sh = x0 & 63;
-            const int y0 = ty * kTile, y1 = min(y0 + kTile, g.H);
+            const int y0 = ty * kTile;
             for (int l = 0; l <= g.L; ++l) {
                 const uint64_t *M = smem + (size_t)(l == 0 ? 0 : g.L + l) * HWW;
-                uint64_t bits = 0;
-                if (in)
-                    for (int y = y0; y < y1; ++y) bits |= M[y * g.WW + wx] >> sh;
+                const uint64_t bits = in ? tile_rows(M, y0, g.H, g.WW, wx) >> sh : 0ull;
                 const uint64_t m = __ballot((bits & ((1ull << kTile) - 1ull)) != 0);
                 if (lane == 0) {
                     g.tmask[l][(size_t)slot * TMW + wd] = m;
