@@ -283,7 +283,9 @@ __global__ __launch_bounds__(kThreads) void k_head_partial_generic(HeadArgs a, i
 
 // Tile contributions to the logits for a bf16 last layer, as a matrix product
 // per tile position: for the tiles of one position P (rows), with the head
-// weights of P (bf16, packed [P][k-step][n-block][lane][8]),
+// weights of P (bf16, packed [P][k-step][n-block][k-quarter][column][8] with
+// only the n_out real columns stored: a last n-block of w < 16 logits holds w
+// columns and its other lanes take zeros without a load),
 //   hpart[tile][o] = sum_k act_tile[k] * hw[P][k][o],  k = pixel * C + channel,
 // on v_mfma_f32_16x16x32_bf16 (A: the tile's cache slice read straight from
 // memory, 16 bytes per lane per k-step; products of two bf16 values are exact
@@ -316,6 +318,17 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     const uint16_t *hw = reinterpret_cast<const uint16_t *>(a.hw);
     const int ntiles = a.TH * a.TW;
     const int row = lane & 15, kq = lane >> 4;
+    // This lane's B fragment of n-block nb within a k-step's n_out x 32 weights
+    // (column `row`, k-quarter kq), or none past the last real column.
+    const int kstep_elems = a.n_out * 32;
+    int boff[NBO];
+    bool bval[NBO];
+#pragma unroll
+    for (int nb = 0; nb < NBO; ++nb) {
+        const int wb = min(16, a.n_out - 16 * nb);
+        bval[nb] = row < wb;
+        boff[nb] = nb * 16 * 32 + (kq * wb + row) * 8;
+    }
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
         // This lane's A rows: row `row` of each group (items g + 16 rg + row).
         uint32_t e[4];
@@ -350,14 +363,15 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
             for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
                 for (int nb = 0; nb < NBO; ++nb) acc[rg][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-            const uint16_t *wp = hw + (((size_t)P * KS + KW * wave) * NBO * 64 + lane) * 8;
+            const uint16_t *wp = hw + ((size_t)P * KS + KW * wave) * kstep_elems;
             for (int s0 = 0; s0 < KW; s0 += KB) {
                 u32x4 av[KB][4], bv[KB][NBO];
 #pragma unroll
                 for (int s = 0; s < KB; ++s) {
 #pragma unroll
                     for (int nb = 0; nb < NBO; ++nb)
-                        bv[s][nb] = *reinterpret_cast<const u32x4 *>(wp + ((size_t)(s0 + s) * NBO + nb) * 64 * 8);
+                        bv[s][nb] = bval[nb] ? *reinterpret_cast<const u32x4 *>(wp + (size_t)(s0 + s) * kstep_elems + boff[nb])
+                                             : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
                     for (int rg = 0; rg < 4; ++rg)
                         av[s][rg] = pos[rg] == P ? *reinterpret_cast<const u32x4 *>(arow[rg] + 32 * (s0 + s))
@@ -434,30 +448,33 @@ hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s) {
 }
 
 size_t tile_part_bf16_elems(int ntiles, int C, int n_out) {
-    const int nbo = n_out <= 16 ? 1 : n_out <= 32 ? 2 : 4;
-    return (size_t)ntiles * kTilePx * C * 16 * nbo;
+    return (size_t)ntiles * kTilePx * C * n_out;
 }
 
 void pack_tile_part_bf16(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, uint16_t *dst) {
-    // [tile][k-step][n-block][lane][j]: k = 32 step + 8 (lane / 16) + j is
-    // pixel k / C (row-major in the tile) and channel k % C; column
-    // o = 16 n-block + lane % 16.  Zero for o >= n_out and outside the image.
-    const int nbo = n_out <= 16 ? 1 : n_out <= 32 ? 2 : 4;
+    // [tile][k-step][n-block][kq][column][j] with the n-block of width
+    // wb = min(16, n_out - 16 n-block): k = 32 step + 8 kq + j is pixel k / C
+    // (row-major in the tile) and channel k % C; logit o = 16 n-block + column.
+    // Zero outside the image.
+    const int nbo = (n_out + 15) / 16;
     const int ntiles = TH * TW, KS = kTilePx * C / 32;
     size_t d = 0;
     for (int t = 0; t < ntiles; ++t) {
         const int ty = t / TW, tx = t % TW;
         for (int s = 0; s < KS; ++s)
-            for (int nb = 0; nb < nbo; ++nb)
-                for (int l = 0; l < 64; ++l)
-                    for (int j = 0; j < 8; ++j) {
-                        const int k = 32 * s + 8 * (l / 16) + j, m = k / C, c = k % C;
-                        const int o = nb * 16 + l % 16, y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
-                        const float v = (o < n_out && y < H && x < W)
-                                            ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x]
-                                            : 0.f;
-                        dst[d++] = bf16_bits_host(v);
-                    }
+            for (int nb = 0; nb < nbo; ++nb) {
+                const int wb = std::min(16, n_out - 16 * nb);
+                for (int kq = 0; kq < 4; ++kq)
+                    for (int col = 0; col < wb; ++col)
+                        for (int j = 0; j < 8; ++j) {
+                            const int k = 32 * s + 8 * kq + j, m = k / C, c = k % C;
+                            const int o = nb * 16 + col, y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
+                            const float v = (y < H && x < W)
+                                                ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x]
+                                                : 0.f;
+                            dst[d++] = bf16_bits_host(v);
+                        }
+            }
     }
 }
 
