@@ -217,6 +217,9 @@ def main():
                          "region; every slot then recomputes everything on its next step)")
     ap.add_argument("--separate-first", action="store_true",
                     help="run layer 1 as its own kernel instead of inside layer 2")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each reuse step from a HIP graph captured once per frame buffer "
+                         "(one launch per step instead of one per kernel; the profiled pass stays eager)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy, 3 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -261,10 +264,29 @@ def main():
 
     alt_weights = [weights, synth.net_weights(wl, seed_extra=1)] if args.update_every else None
 
-    def do_step(k):
+    graphs = {}
+    if args.graph:
+        if not isinstance(drv, SpriteDriver) or args.update_every:
+            print("bench.py: --graph applies to the sprite workloads without weight updates", file=sys.stderr)
+            sys.exit(2)
+        # One eager step first, so one-time set-up happens outside the capture.
+        drv.prime(net, out)
+        drv.reuse_step(net, 0, out)
+        torch.cuda.synchronize()
+        for t in sorted(set(drv.seq)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                net.step(drv.frames[t], out=out)
+            graphs[t] = g
+        torch.cuda.synchronize()
+
+    def do_step(k, eager=False):
         if args.update_every and k % args.update_every == 0 and k > 0:
             net.set_weights(alt_weights[(k // args.update_every) % 2])
-        drv.reuse_step(net, k, out)
+        if graphs and not eager:
+            graphs[drv.seq[k]].replay()
+        else:
+            drv.reuse_step(net, k, out)
 
     def restart():
         # every pass starts from the first weight set, primed on the first frames
@@ -277,19 +299,21 @@ def main():
     stats = []
     for k in range(length):
         do_step(k)
+        if graphs:
+            torch.cuda.synchronize()                            # the replay's stream, not the capture's
         stats.append(net.stats())
     timed_stats = stats[args.warmup:]
 
     def run_reuse(profile: bool):
         restart()
         for k in range(args.warmup):
-            do_step(k)
+            do_step(k, eager=profile)
         torch.cuda.synchronize()
         net.set_profiling(profile)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for k in range(args.warmup, length):
-            do_step(k)
+            do_step(k, eager=profile)
         e1.record(stream)
         torch.cuda.synchronize()
         prof = net.profile() if profile else None
@@ -391,6 +415,8 @@ def main():
         cfg["change_preset"] = args.change_frac
     if args.update_every:
         cfg["weight_update_every"] = args.update_every
+    if graphs:
+        cfg["launch"] = "graph replay per step"
     line = {
         "metric": drv.metric,
         "value": fps,
