@@ -358,12 +358,45 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
             const int P = __builtin_amdgcn_readlane(my_sp, __ffsll((long long)left) - 1);
             const uint64_t pmask = __ballot(my_sp == P);
             left &= ~pmask;
+            const uint16_t *wp = hw + ((size_t)P * KS + KW * wave) * kstep_elems;
+            if constexpr (KW * NBO <= 32) {
+                // The wave's whole K quarter of P's weights is loaded at once,
+                // then per row group holding rows at P its activations: one
+                // memory round trip for the weights and one per such group.
+                // Products in k-step order, as in the batched loop below.
+                u32x4 bq[KW][NBO];
+#pragma unroll
+                for (int s = 0; s < KW; ++s)
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb)
+                        bq[s][nb] = bval[nb] ? *reinterpret_cast<const u32x4 *>(wp + (size_t)s * kstep_elems + boff[nb])
+                                             : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int rg = 0; rg < 4; ++rg) {
+                    if (((pmask >> (16 * rg)) & 0xFFFFu) == 0) continue;   // uniform: no row of this group at P
+                    u32x4 aq[KW];
+                    const bool mine = pos[rg] == P;
+#pragma unroll
+                    for (int s = 0; s < KW; ++s)
+                        aq[s] = mine ? *reinterpret_cast<const u32x4 *>(arow[rg] + 32 * s) : u32x4{0u, 0u, 0u, 0u};
+                    floatx4 acc[NBO];
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int s = 0; s < KW; ++s)
+#pragma unroll
+                        for (int nb = 0; nb < NBO; ++nb)
+                            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8, aq[s]), __builtin_bit_cast(bf16x8, bq[s][nb]), acc[nb], 0, 0, 0);
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb) s_acc[wave][rg][nb][lane] = acc[nb];
+                }
+            } else {
             floatx4 acc[4][NBO];
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
                 for (int nb = 0; nb < NBO; ++nb) acc[rg][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-            const uint16_t *wp = hw + ((size_t)P * KS + KW * wave) * kstep_elems;
             for (int s0 = 0; s0 < KW; s0 += KB) {
                 u32x4 av[KB][4], bv[KB][NBO];
 #pragma unroll
@@ -391,6 +424,7 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
             for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
                 for (int nb = 0; nb < NBO; ++nb) s_acc[wave][rg][nb][lane] = acc[rg][nb];
+            }
             lds_barrier();
             // Wave `wave` finishes row group `wave`: the K quarters in wave order.
             const uint64_t gmask = (pmask >> (16 * wave)) & 0xFFFFu;
