@@ -479,7 +479,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     MaskGeom g = make_geom(net);
     MaskArgs ma{};
     ma.n = n;
-    ma.ids = ids;
+    ma.ids = ids_in;                          // NULL: the identity batch, no table load
     ma.frames = frames;
     ma.frame_u8 = fdt == RN_U8;
     ma.boxes = boxes;
@@ -510,7 +510,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
         ca.ntl[l] = p.ntl[l];
         ca.cap[l] = (size_t)n * p.ntl[l];
     }
-    ca.ids = ids;
+    ca.ids = ids_in;
     ca.ntile = ma.ntile;
     for (int l = 0; l <= p.L; ++l) {
         ca.tmask[l] = g.tmask[l];

@@ -39,7 +39,7 @@ struct MaskGeom {
 // Per-step inputs of the mask kernel.
 struct MaskArgs {
     int n;
-    const int32_t *ids;           // [n] slots (never NULL: identity table otherwise)
+    const int32_t *ids;           // [n] slots, or NULL: slot i for batch index i
     const void *frames;           // [n][cin][H][W]
     int frame_u8;                 // 1: uint8 levels, 0: float32
     const int32_t *boxes;         // NULL: diff
@@ -64,7 +64,7 @@ struct MaskArgs {
 struct CompactArgs {
     int n, L;
     int TWl[RN_MAX_CONV + 1], TMWl[RN_MAX_CONV + 1], ntl[RN_MAX_CONV + 1];   // per layer
-    const int32_t *ids;
+    const int32_t *ids;           // [n] slots, or NULL: slot i for batch index i
     const int32_t *ntile;         // [n][L+1]
     uint64_t *tmask[RN_MAX_CONV + 1];
     const int32_t *tpfx[RN_MAX_CONV + 1];   // per-slot word prefixes written by k_masks

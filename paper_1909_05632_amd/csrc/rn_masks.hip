@@ -270,7 +270,7 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     int *s_wc = reinterpret_cast<int *>(lut + 256);            // [L][TMW] dirty tiles per tile word
 
     const int i = blockIdx.x;
-    const int slot = a.ids[i];
+    const int slot = a.ids ? a.ids[i] : i;
     const int primed = a.force_all ? 0 : a.primed[slot];
     const size_t HW = (size_t)g.H * g.W;
     const int C = g.cin;
@@ -546,7 +546,7 @@ __device__ inline void stage_pass(const CompactArgs &a, int l, int wd, int c0, i
                                   uint64_t *s_word) {
     for (int j = threadIdx.x; j < nc * 64; j += blockDim.x) {
         const int i = 64 * c0 + j;
-        const int slot = i < a.n ? a.ids[i] : -1;
+        const int slot = i >= a.n ? -1 : a.ids ? a.ids[i] : i;
         s_slot[j] = slot;
         s_word[j] = slot >= 0 ? a.tmask[l][(size_t)slot * a.TMWl[l] + wd] : 0ull;
     }
@@ -574,7 +574,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // pass's slots and words of this word staged in LDS.
     int pre = 0;
     for (int i = threadIdx.x; i < 64 * nc0 || i < a.n; i += blockDim.x) {
-        const int slot = i < a.n ? a.ids[i] : -1;
+        const int slot = i >= a.n ? -1 : a.ids ? a.ids[i] : i;
         if (slot >= 0 && wd > 0) {
             if (a.tpfx[l] != nullptr) {
                 pre += a.tpfx[l][(size_t)slot * TMW + wd];
