@@ -892,8 +892,11 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
             store_wstage<CIN, COUT>(wbuf + (buf ^ 1) * S::WST, wreg, tid);
             fetch_wstage<CIN, COUT>(wg, (q + 2) % S::NQ, wreg, tid);
             if (q == S::NQ / 2) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
+            // Unconditional: a wave without a tile has an all-zero halo and
+            // skips only the epilogue (a guarded call would make the compiler
+            // copy every accumulator between register files each stage).
             const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-            if (valid) mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane);
+            mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane);
             buf ^= 1;
             lds_barrier();
         }
