@@ -225,8 +225,8 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(streams shard across GPUs with no exchange; see the design notes)", file=sys.stderr)
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(streams would shard across GPUs, one process each, with no exchange between them)", file=sys.stderr)
         sys.exit(2)
 
     import torch

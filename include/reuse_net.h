@@ -48,7 +48,7 @@ extern "C" {
 typedef enum {
     RN_OK = 0,
     RN_EINVAL = -1,        /* bad argument or null pointer */
-    RN_EUNSUPPORTED = -2,  /* valid request this build does not implement */
+    RN_EUNSUPPORTED = -2,  /* valid request the library does not implement */
     RN_ENOSPACE = -3,      /* workspace or caller buffer too small */
     RN_EHIP = -4,          /* a HIP runtime call failed */
     RN_ESTATE = -5         /* call not valid in the net's current state */

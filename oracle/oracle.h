@@ -14,8 +14,7 @@
  * each side), dirty-tile masks and the work list depend only on the change
  * set and are written out from their definitions.
  *
- * Conventions (the paper is silent on them; the readings are listed with the
- * design notes):
+ * Conventions (readings where the paper is silent):
  *   - tensors are C-contiguous float32, channel-major [C][H][W];
  *   - convolution is cross-correlation with OIHW weights, zero padding,
  *     output size floor((n + 2p - k) / s) + 1, then bias, then ReLU;
