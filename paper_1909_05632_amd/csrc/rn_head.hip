@@ -128,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void k_tile_head(TileHeadArgs a) {
     __shared__ float red[kThreads / 64][NO];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int i = blockIdx.x;
-    const float *P = a.hpart + (size_t)a.ids[i] * a.ntiles * NO;
+    const float *P = a.hpart + (size_t)(a.ids ? a.ids[i] : i) * a.ntiles * NO;
     float acc[NO];
 #pragma unroll
     for (int o = 0; o < NO; ++o) acc[o] = 0.f;
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void k_tile_head_var_generic(TileHeadArgs
 __global__ __launch_bounds__(kThreads) void k_tile_head_generic(TileHeadArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int i = blockIdx.x;
-    const float *P = a.hpart + (size_t)a.ids[i] * a.ntiles * a.n_out;
+    const float *P = a.hpart + (size_t)(a.ids ? a.ids[i] : i) * a.ntiles * a.n_out;
     for (int o = wave; o < a.n_out; o += kThreads / 64) {
         float v = 0.f;
         for (int t = lane; t < a.ntiles; t += 64) v += P[(size_t)t * a.n_out + o];

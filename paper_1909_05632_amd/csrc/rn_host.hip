@@ -369,8 +369,10 @@ MaskGeom make_geom(reuse_net *net) {
 }
 
 // Conv layers 1..L (list mode: the work lists; dense mode: every tile), then the head.
-hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const *wl, const int32_t *cnt,
-                      float *logits, hipStream_t s, bool dense) {
+// identity: the batch is slots 0..n-1 in order (ids is then the identity table;
+// kernels that only need a stream's slot skip loading it).
+hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, bool identity, uint32_t *const *wl,
+                      const int32_t *cnt, float *logits, hipStream_t s, bool dense) {
     const Plan &p = net->p;
     const bool tiles_head = p.head_mode == RN_HEAD_TILES;
     hipError_t e = hipSuccess;
@@ -443,7 +445,7 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, uint32_t *const
         ta.n = n;
         ta.n_out = p.N;
         ta.ntiles = p.ntl[p.L];
-        ta.ids = ids;
+        ta.ids = identity ? nullptr : ids;
         ta.hpart = net->at<float>(p.o_hp);
         ta.bias = net->at<float>(p.o_bd);
         ta.logits = logits;
@@ -524,7 +526,7 @@ rn_status run_step(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("compaction kernel: ") + hipGetErrorString(e));
     }
 
-    e = run_layers(net, n, ids, ca.wls, ca.cnt, logits, s, false);
+    e = run_layers(net, n, ids, ids_in == nullptr, ca.wls, ca.cnt, logits, s, false);
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));
     net->last_stream = s;
     net->last_n = n;
@@ -730,7 +732,7 @@ rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     pa.dring_words = p.stack == 4 ? (size_t)4 * p.H * p.WW : 0;
     hipError_t e = timed(net, RN_PHASE_MASKS, s, [&] { return launch_prime(pa, s); });
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("prime kernel: ") + hipGetErrorString(e));
-    e = run_layers(net, n, ids, nullptr, nullptr, logits, s, true);
+    e = run_layers(net, n, ids, ids_in == nullptr, nullptr, nullptr, logits, s, true);
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv/head kernels: ") + hipGetErrorString(e));
     net->last_stream = s;
     net->last_n = n;

@@ -163,7 +163,7 @@ struct PrimeArgs {
 // Sum of the per-tile head partials: logits[i][o] = bd[o] + sum_t hpart[ids[i]][t][o].
 struct TileHeadArgs {
     int n, n_out, ntiles;
-    const int32_t *ids;
+    const int32_t *ids;           // [n] slots, or NULL: slot i for batch index i
     const float *hpart;
     const float *bias;
     float *logits;
