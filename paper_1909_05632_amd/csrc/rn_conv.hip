@@ -1210,7 +1210,16 @@ hipError_t run_gen(const ConvArgs &a, int cus, hipStream_t s) {
     static hipError_t attr2 = set_lds(k_conv_gen<KS, ST, CIN, COUT, false, FIRST>, G::lds_bytes);
     if (attr != hipSuccess) return attr;
     if (attr2 != hipSuccess) return attr2;
-    const int grid = persistent_grid(cus * 4, a.max_tiles);
+    // As many blocks as the CUs hold at once (registers and LDS decide), so
+    // every block starts in the first generation and walks several tiles.
+    static int occ = [] {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k_conv_gen<KS, ST, CIN, COUT, false, FIRST>,
+                                                         64 * G::KSPLIT, G::lds_bytes) != hipSuccess || b < 1)
+            b = 2;
+        return b;
+    }();
+    const int grid = persistent_grid(cus * occ, a.max_tiles);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * G::KSPLIT), G::lds_bytes, s, a);
     return hipGetLastError();
 }
