@@ -691,8 +691,24 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
         if constexpr (FUSE) pin = fetch_patch<VAR>(a, item_of(a, w0, w1, c0, 0), lane);
         else fetch_halo<CIN, COUT, VAR>(a, item_of(a, w0, w1, c0, 0), pre, lane);
     }
+    // Weights into LDS in batches of 8 loads per thread, each batch issued
+    // before any of it is written (indices past the end read the last
+    // element and are not stored): a few memory round trips, not one per
+    // 16 bytes.
     const float4 *wg = static_cast<const float4 *>(a.w);
-    for (int j = tid; j < M::WTOT / 4; j += blockDim.x) reinterpret_cast<float4 *>(s_w)[j] = wg[j];
+    constexpr int NW4 = M::WTOT / 4, WPER = (NW4 + WAVES * 64 - 1) / (WAVES * 64), WB = 8;
+#pragma unroll
+    for (int k0 = 0; k0 < WPER; k0 += WB) {
+        float4 wv[WB];
+#pragma unroll
+        for (int k = 0; k < WB; ++k)
+            if (k0 + k < WPER) wv[k] = wg[min(tid + (k0 + k) * WAVES * 64, NW4 - 1)];
+#pragma unroll
+        for (int k = 0; k < WB; ++k) {
+            const int j = tid + (k0 + k) * WAVES * 64;
+            if (k0 + k < WPER && j < NW4) reinterpret_cast<float4 *>(s_w)[j] = wv[k];
+        }
+    }
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
     if constexpr (FUSE) {
         for (int j = tid; j < 9 * CIN; j += blockDim.x) s_w1[j] = a.w1[j];
