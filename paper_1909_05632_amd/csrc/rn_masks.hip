@@ -572,20 +572,36 @@ __global__ __launch_bounds__(kThreads) void k_compact_pos(CompactArgs a) {
     // One pass over the streams (thread per stream): dirty tiles at positions
     // before this word (the per-slot word prefix k_masks wrote), and the first
     // pass's slots and words of this word staged in LDS.
+    // Four streams per thread at a time, their loads issued together.
+    constexpr int UB = 4;
     int pre = 0;
-    for (int i = threadIdx.x; i < 64 * nc0 || i < a.n; i += blockDim.x) {
-        const int slot = i >= a.n ? -1 : a.ids ? a.ids[i] : i;
-        if (slot >= 0 && wd > 0) {
-            if (a.tpfx[l] != nullptr) {
-                pre += a.tpfx[l][(size_t)slot * TMW + wd];
-            } else {
-                const uint64_t *tm = a.tmask[l] + (size_t)slot * TMW;
+    for (int i0 = threadIdx.x; i0 < 64 * nc0 || i0 < a.n; i0 += UB * (int)blockDim.x) {
+        int slot[UB];
+#pragma unroll
+        for (int u = 0; u < UB; ++u) {
+            const int i = i0 + u * (int)blockDim.x;
+            slot[u] = i >= a.n ? -1 : a.ids ? a.ids[i] : i;
+        }
+        int pf[UB];
+        uint64_t word[UB];
+#pragma unroll
+        for (int u = 0; u < UB; ++u) {
+            const int i = i0 + u * (int)blockDim.x;
+            pf[u] = slot[u] >= 0 && wd > 0 && a.tpfx[l] != nullptr ? a.tpfx[l][(size_t)slot[u] * TMW + wd] : 0;
+            word[u] = i < 64 * nc0 && slot[u] >= 0 ? a.tmask[l][(size_t)slot[u] * TMW + wd] : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < UB; ++u) {
+            const int i = i0 + u * (int)blockDim.x;
+            pre += pf[u];
+            if (slot[u] >= 0 && wd > 0 && a.tpfx[l] == nullptr) {
+                const uint64_t *tm = a.tmask[l] + (size_t)slot[u] * TMW;
                 for (int w = 0; w < wd; ++w) pre += __popcll(tm[w]);
             }
-        }
-        if (i < 64 * nc0) {
-            s_slot[i] = slot;
-            s_word[i] = slot >= 0 ? a.tmask[l][(size_t)slot * TMW + wd] : 0ull;
+            if (i < 64 * nc0) {
+                s_slot[i] = slot[u];
+                s_word[i] = word[u];
+            }
         }
     }
     pre = block_sum(pre, red);                   // its barriers also publish the staging
