@@ -695,6 +695,15 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     // before any of it is written (indices past the end read the last
     // element and are not stored): a few memory round trips, not one per
     // 16 bytes.
+    // The biases and the folded layer's weights (at most one value of each
+    // per thread) are loaded up front, in flight with the weights below.
+    static_assert(COUT <= WAVES * 64 && 9 * CIN <= WAVES * 64, "one small value per thread");
+    const float bias_v = tid < COUT ? a.bias[tid] : 0.f;
+    float w1_v = 0.f, b1_v = 0.f;
+    if constexpr (FUSE) {
+        if (tid < 9 * CIN) w1_v = a.w1[tid];
+        if (tid < CIN) b1_v = a.b1[tid];
+    }
     const float4 *wg = static_cast<const float4 *>(a.w);
     constexpr int NW4 = M::WTOT / 4, WPER = (NW4 + WAVES * 64 - 1) / (WAVES * 64), WB = 8;
 #pragma unroll
@@ -709,10 +718,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
             if (k0 + k < WPER && j < NW4) reinterpret_cast<float4 *>(s_w)[j] = wv[k];
         }
     }
-    for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+    if (tid < COUT) s_bias[tid] = bias_v;
     if constexpr (FUSE) {
-        for (int j = tid; j < 9 * CIN; j += blockDim.x) s_w1[j] = a.w1[j];
-        for (int j = tid; j < CIN; j += blockDim.x) s_b1[j] = a.b1[j];
+        if (tid < 9 * CIN) s_w1[tid] = w1_v;
+        if (tid < CIN) s_b1[tid] = b1_v;
     }
     lds_barrier();                                        // the first input loads stay in flight
 
