@@ -55,6 +55,15 @@ def test_dqn_trunk_84x84_stacked(torch):
         _run(torch, wl, 6, 8, weights, head=head, sample=[0, 5], label=f"dqn head={head}").close()
 
 
+def test_dqn_trunk_one_stream(torch):
+    # A batch of one stream (the mask kernel writes the work lists itself) on
+    # the stacked DQN-style trunk: growth layer by layer through strided
+    # layers, the single-frame change ring, every step checked.
+    wl = synth.WORKLOADS["dqn-84x84-256x64"]
+    weights = synth.net_weights(wl, bias_std=0.05)
+    _run(torch, wl, 1, 7, weights, label="dqn one stream").close()
+
+
 def test_general_layers_single_channel_same_and_strided(torch):
     # One input channel: 5x5/1 pad 2 (same grid), 5x5/1 pad 2, 3x3/2 pad 1 on a
     # ragged 44x36 frame, and 7x7/2 pad 3 first.
