@@ -8,15 +8,15 @@ dense recompute path of the same library (`reuse_net_full`) and the CPU
 oracle are timed in the same run.
 
 Workloads (synth.WORKLOADS):
-  atari-ds2-256x64 (default)  256 streams x 64 frames, 105x80, 1->40->80, dense->6
+  fullres-1024x32 (default)   1024 streams x 32 frames, 210x160, 1->64->128->128, dense->18
+                              (--change-frac picks the sprite preset of the sweep; default 0.01)
+  atari-ds2-256x64            256 streams x 64 frames, 105x80, 1->40->80, dense->6
   atari-ds4-1x16              1 stream x 16 frames, 53x40
   stack4-512x64               512 streams, the last 4 frames stacked as input channels
   dqn-84x84-256x64            256 streams x 64 frames, 84x84, 4 stacked frames, DQN-style trunk
                               (8x8/4 4->32, 4x4/2 32->64, 3x3/1 64->64, no padding), dense->6
   occlusion-105x80-4096       4096 occlusion variants of one base image, one
                               reuse_net_variants call (copy-on-write overlays) per step
-  fullres-1024x32             1024 streams x 32 frames, 210x160, 1->64->128->128, dense->18
-                              (--change-frac picks the sprite preset of the sweep)
 The frame order runs 1..F-1 and then back and forth, so every transition is
 an ordinary sprite move.
 
@@ -39,25 +39,51 @@ if ROOT not in sys.path:
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_F32_TFLOPS = 157.3
 PEAK_MFMA_BF16_TFLOPS = 2500.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_conv_mfma_atari-ds2-256x64.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_1909_05632_amd", "csrc", "rn_conv.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_1909_05632_amd", "csrc")
+DEFAULT_WORKLOAD = "fullres-1024x32"
+DEFAULT_CHANGE_FRAC = 0.01          # the full-resolution workload's 1% change preset
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(source: str) -> str:
+    """Hash of a kernel source file together with the device headers it includes."""
     import hashlib
-    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in (source, "rn_device.hpp", "rn_internal.hpp"):
+        h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the committed counter runs, or None
-    when they are missing or were taken on a different kernel source."""
-    try:
-        rec = json.load(open(TRAFFIC_FILE))
-    except (OSError, ValueError):
-        return None
-    if rec.get("source_sha256_16") != kernel_source_hash() or rec.get("kernel") != kernel:
-        return None
-    return rec.get("bytes_per_launch")
+def measured_traffic(key: dict):
+    """HBM bytes per launch of one conv layer's kernel from the committed counter
+    runs (profiles/traffic_*.json) whose workload key equals `key`, or None when
+    there is none or it was taken on a different kernel source."""
+    import glob
+    for path in sorted(glob.glob(os.path.join(PROFILES, "traffic_*.json"))):
+        try:
+            rec = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        if rec.get("key") != key:
+            continue
+        if rec.get("source_sha256_16") != kernel_source_hash(rec.get("source", "")):
+            return None
+        return rec.get("bytes_per_launch")
+    return None
+
+
+def layer_kernel(specs, l, dtype, folded):
+    """Name of the kernel that computes conv layer l (1-based) in the library."""
+    ci, co, k, st, pd = specs[l - 1]
+    if not (k == 3 and st == 1 and pd == 1):
+        return f"k_conv_gen<{k}, {st}, {ci}, {co}>"
+    if dtype == "bf16":
+        return f"k_conv_first_bf16<{ci}, {co}>" if l == 1 else f"k_conv_bf16_grp<{ci}, {co}>"
+    if l == 1:
+        return f"k_conv_first4_mfma<{co}>" if ci == 4 else f"k_conv_first_f32<{ci}, {co}>"
+    if (ci, co) == (40, 80):                                     # weights resident in LDS
+        return "k_conv_mfma_res<40, 80>" + (" (layer 1 folded in)" if folded else "")
+    return f"k_conv_mfma_staged<{ci}, {co}>"
 
 
 def schedule(frames: int, length: int):
@@ -204,9 +230,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=120)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="atari-ds2-256x64")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--change-frac", type=float, default=None,
-                    help="full-resolution sweep preset: 0.001, 0.01, 0.05, 0.2 or 1.0")
+                    help="full-resolution sweep preset: 0.001, 0.01, 0.05, 0.2 or 1.0 "
+                         f"(default {DEFAULT_CHANGE_FRAC} for {DEFAULT_WORKLOAD})")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
@@ -245,6 +272,8 @@ def main():
     from paper_1909_05632_amd import ReuseNet
     from synth import frames as synth
 
+    if args.change_frac is None and args.workload == DEFAULT_WORKLOAD:
+        args.change_frac = DEFAULT_CHANGE_FRAC
     wl = synth.WORKLOADS[args.workload]
     length = args.warmup + args.steps
     if args.workload.startswith("occlusion"):
@@ -355,8 +384,8 @@ def main():
 
     # Per-kernel figures from the HIP events of the profiled pass.
     kern = {}
-    for name, rec in prof.items():
-        kern[name] = {"ms_per_step": rec["ms"] / K, "launches": rec["launches"]}
+    for name in ("masks", "compact", "conv1", "convN", "head"):
+        kern[name] = {"ms_per_step": prof[name]["ms"] / K, "launches": prof[name]["launches"]}
     # MFMA conv layers 2..L (and a general first layer): flops of the dirty tiles
     flops_convn = sum(dirty[:, l].sum() * fpt[l] for l in range(2, L + 1))
     if prof["convN"]["ms"] > 0:
@@ -372,32 +401,57 @@ def main():
     kern["head"]["gbs"] = head_bytes / (prof["head"]["ms"] / 1e3) / 1e9
     mask_bytes = drv.mask_bytes() * K
     kern["masks"]["gbs"] = mask_bytes / (prof["masks"]["ms"] / 1e3) / 1e9
+    k1, s1 = specs[0][2], specs[0][3]
+    conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + (3 * s1 + k1) ** 2 * chans[0] * 4)
     if prof["conv1"]["ms"] > 0:
-        k1, s1 = specs[0][2], specs[0][3]
-        patch = (3 * s1 + k1) ** 2                              # input pixels read per output tile
-        conv1_bytes = dirty[:, 1].sum() * (16 * chans[1] * esz + patch * chans[0] * 4)
         kern["conv1"]["gbs"] = conv1_bytes / (prof["conv1"]["ms"] / 1e3) / 1e9
 
+    # Per conv layer: one kernel per layer and step, so its average launch is
+    # the layer's summed event time over its launches.
     folded = (not args.separate_first) and chans[0] == 1 and L >= 2 and chans[1] == 40 and not any(general[:2])
-    dominant = max(("convN", "head", "masks", "conv1", "compact"), key=lambda k: prof[k]["ms"])
-    if dominant == "conv1" and general[0]:
-        ach = kern["conv1"]["tflops"]
-        roof = {"bound": "mfma", "kernel": "MFMA dirty-tile conv, general first layer", "achieved": ach,
-                "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_MFMA_F32_TFLOPS,
-                "traffic": None}
-    elif dominant == "convN":
-        ach = kern["convN"]["tflops"]
-        peak = PEAK_MFMA_BF16_TFLOPS if args.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
-        roof = {"bound": "mfma",
-                "kernel": "MFMA dirty-tile conv, layers 2..L" + (" (layer 1 folded into layer 2)"
-                                                                  if folded else ""),
-                "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak,
-                "traffic": measured_traffic("conv_mfma_res_40_80_reuse")
-                if args.workload == "atari-ds2-256x64" and folded and args.head == "tiles" else None}
+    mfma_layer = [False] + [l >= 2 or general[0] or chans[0] == 4 for l in range(1, L + 1)]
+    layers = {}
+    for l in range(1, L + 1):
+        rec = prof["layers"][l]
+        if rec["launches"] == 0:
+            continue                                            # layer 1 folded into layer 2
+        ent = {"kernel": layer_kernel(specs, l, args.dtype, folded and l == 2), "launches": rec["launches"],
+               "ms_per_step": rec["ms"] / K, "us_per_launch": 1e3 * rec["ms"] / rec["launches"],
+               "dirty_tiles_per_launch": float(dirty[:, l].sum() / rec["launches"])}
+        if mfma_layer[l]:
+            ent["tflops"] = dirty[:, l].sum() * fpt[l] / (rec["ms"] / 1e3) / 1e12
+        else:
+            ent["gbs"] = conv1_bytes / (rec["ms"] / 1e3) / 1e9
+        layers[str(l)] = ent
+    kern["layers"] = layers
+
+    # The roofline object reports the single kernel with the most time.
+    cands = {("layer", l): layers[str(l)]["ms_per_step"] for l in range(1, L + 1) if str(l) in layers}
+    for name in ("masks", "compact", "head"):
+        cands[("phase", name)] = kern[name]["ms_per_step"]
+    dom = max(cands, key=cands.get)
+    if dom[0] == "layer":
+        l = dom[1]
+        ent = layers[str(l)]
+        desc = f"{ent['kernel']}: dirty-tile conv layer {l} ({chans[l - 1]}->{chans[l]})"
+        key = {"workload": args.workload, "change_preset": args.change_frac, "dtype": args.dtype,
+               "head": args.head, "layer": l, "folded": bool(folded and l == 2)}
+        traffic = measured_traffic(key)
+        if mfma_layer[l]:
+            peak = PEAK_MFMA_BF16_TFLOPS if args.dtype == "bf16" else PEAK_MFMA_F32_TFLOPS
+            roof = {"bound": "mfma", "kernel": desc, "achieved": ent["tflops"], "peak": peak, "unit": "TFLOP/s",
+                    "frac": ent["tflops"] / peak, "traffic": traffic}
+        else:
+            roof = {"bound": "hbm", "kernel": desc, "achieved": ent["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": ent["gbs"] / PEAK_HBM_GBS, "traffic": traffic}
+        roof["us_per_launch"] = ent["us_per_launch"]
+        roof["work_per_launch"] = (f"{ent['dirty_tiles_per_launch']:.0f} dirty tiles x "
+                                   f"{fpt[l] / 1e6:.4f} MFLOP (2 x 16 px x {chans[l]} x "
+                                   f"{specs[l - 1][2] ** 2 * chans[l - 1]})")
     else:
-        ach = kern[dominant].get("gbs", 0.0)
-        roof = {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": PEAK_HBM_GBS,
+        name = dom[1]
+        ach = kern[name].get("gbs", 0.0)
+        roof = {"bound": "hbm", "kernel": name, "achieved": ach, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None}
 
     cpu = None

@@ -133,8 +133,10 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
  *                   caller states the change (Sec. 1, known-change use such as
  *                   occlusion): boxes [nb][4] int32 (y0, x0, y1, x1), half-open, clipped
  *                   to the frame; stream i owns boxes [box_off[i], box_off[i+1]);
- *                   box_off has n+1 entries and box_off[0] = 0.  Only pixels inside
- *                   the boxes are read from dev_frames.
+ *                   box_off has n+1 entries and box_off[0] = 0.  On a primed slot only
+ *                   pixels inside the boxes are read from dev_frames; a slot that was
+ *                   never primed (or was reset) ignores its boxes and reads and caches
+ *                   the whole frame, so its frame must be complete.
  *   dev_logits:     [n][n_out] float32 output.
  * Change rule: a pixel changed iff the float32 bits of some channel differ from
  * the cached input (so -0 vs +0 is a change and an identical NaN is not).  A
@@ -149,9 +151,13 @@ rn_status reuse_net_step(reuse_net *net, int32_t n, const int32_t *dev_stream_id
 
 /* Dense recompute of every layer for n streams (the comparison path): the
  * frames are copied into the input caches and every tile of every layer is
- * recomputed, without change detection or work lists.  Gives the same bits as
- * a step on which every pixel changed, and leaves the slots primed.  The
- * change masks of the slots are left as they were; reuse_net_get_worklist
+ * recomputed, without work lists.  Gives the same bits as a step on which
+ * every pixel changed, and leaves the slots primed.  With stack = 4 the frame
+ * enters the slot's frame ring as a step's frame does (a never-primed slot
+ * takes it as all four frames), and its change against the previous newest
+ * frame is kept for the steps that follow, so a full call in the middle of a
+ * stream leaves the same state as a step on the same frame.  The pixel and
+ * tile masks of the slots are left as they were; reuse_net_get_worklist
  * reports RN_ESTATE until the next step. */
 rn_status reuse_net_full(reuse_net *net, int32_t n, const int32_t *dev_stream_ids,
                          const void *dev_frames, rn_dtype frame_dtype, float *dev_logits,
@@ -259,6 +265,9 @@ typedef enum {
 typedef struct {
     double ms[RN_PHASES];         /* summed event time per phase */
     int64_t launches[RN_PHASES];  /* kernel launches per phase */
+    double layer_ms[RN_MAX_CONV + 1];          /* conv kernels of layer l = 1..n_conv
+                                                  (index 0: every other kernel) */
+    int64_t layer_launches[RN_MAX_CONV + 1];
 } rn_profile;
 
 /* enable != 0: bracket every later kernel launch with HIP events on the

@@ -65,7 +65,9 @@ class rn_stats(ctypes.Structure):
 
 
 class rn_profile(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * RN_PHASES), ("launches", ctypes.c_int64 * RN_PHASES)]
+    _fields_ = [("ms", ctypes.c_double * RN_PHASES), ("launches", ctypes.c_int64 * RN_PHASES),
+                ("layer_ms", ctypes.c_double * (RN_MAX_CONV + 1)),
+                ("layer_launches", ctypes.c_int64 * (RN_MAX_CONV + 1))]
 
 
 _lib = None
@@ -216,7 +218,9 @@ def reuse_net_set_profiling(net: int, enable: bool) -> None:
 def reuse_net_get_profile(net: int) -> dict:
     p = rn_profile()
     _check(load_library().reuse_net_get_profile(net, ctypes.byref(p)), net)
-    return {name: {"ms": p.ms[i], "launches": p.launches[i]} for i, name in enumerate(PHASES)}
+    out = {name: {"ms": p.ms[i], "launches": p.launches[i]} for i, name in enumerate(PHASES)}
+    out["layers"] = [{"ms": p.layer_ms[l], "launches": p.layer_launches[l]} for l in range(RN_MAX_CONV + 1)]
+    return out
 
 
 def reuse_net_last_error(net: Optional[int]) -> str:
@@ -247,7 +251,10 @@ class ReuseNet:
                  device="cuda", tile: int = 4, head: str = "tiles", fuse_first: bool = True):
         import torch
         self.torch = torch
-        self.device = torch.device(device)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev                         # with its index: tensors are compared against it
         self.in_c, self.h, self.w, self.stack = in_c, h, w, stack
         self.convs = list(convs)
         self.n_out, self.max_streams = n_out, max_streams
@@ -299,39 +306,83 @@ class ReuseNet:
         del keep
 
     # -- hot path
-    def _frames(self, frames):
+    # Every tensor handed to the library is checked here, before any launch:
+    # the C ABI takes raw pointers and sizes, so a wrong dtype, device, layout
+    # or length would otherwise be read or written out of bounds on the GPU.
+    def _check_dev(self, x, what: str, dtype, shape):
         t = self.torch
+        if not isinstance(x, t.Tensor):
+            raise TypeError(f"{what} must be a torch tensor")
+        if x.dtype != dtype:
+            raise TypeError(f"{what} must be {dtype}, got {x.dtype}")
+        if x.device != self.device:
+            raise ValueError(f"{what} must be on {self.device}, got {x.device}")
+        if not x.is_contiguous():
+            raise ValueError(f"{what} must be contiguous")
+        if tuple(x.shape) != tuple(shape):
+            raise ValueError(f"{what} must have shape {tuple(shape)}, got {tuple(x.shape)}")
+        return x
+
+    def _frames(self, frames):
+        """(frames, dtype code); frames [n][in_c][h][w] uint8 or float32 on the net's device."""
+        t = self.torch
+        if not isinstance(frames, t.Tensor):
+            raise TypeError("frames must be a torch tensor")
         if frames.dtype == t.uint8:
             code = RN_U8
         elif frames.dtype == t.float32:
             code = RN_F32
         else:
             raise TypeError("frames must be uint8 or float32")
-        if not frames.is_cuda or not frames.is_contiguous():
-            raise ValueError("frames must be a contiguous device tensor")
+        if frames.dim() != 4 or tuple(frames.shape[1:]) != (self.in_c, self.h, self.w):
+            raise ValueError(f"frames must have shape (n, {self.in_c}, {self.h}, {self.w}), "
+                             f"got {tuple(frames.shape)}")
+        self._check_dev(frames, "frames", frames.dtype, (frames.shape[0], self.in_c, self.h, self.w))
         return frames, code
 
-    def step(self, frames, stream_ids=None, boxes=None, box_off=None, out=None, stream=None):
+    def _batch(self, frames, stream_ids, out):
+        """Checked batch size, id pointer and logits tensor of a step or full call."""
         t = self.torch
         frames, code = self._frames(frames)
         n = frames.shape[0]
+        if not 1 <= n <= self.max_streams:
+            raise ValueError(f"batch of {n} streams: must be 1..{self.max_streams}")
+        ids = None
+        if stream_ids is not None:
+            ids = self._check_dev(stream_ids, "stream_ids", t.int32, (n,)).data_ptr()
         if out is None:
             out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        self._check_dev(out, "out", t.float32, (n, self.n_out))
+        return frames, code, n, ids, out
+
+    def _boxes(self, boxes, box_off, n):
+        t = self.torch
+        if boxes is None or box_off is None:
+            raise ValueError("boxes and box_off go together")
+        if boxes.dim() != 2:
+            raise ValueError("boxes must have shape (nb, 4)")
+        self._check_dev(boxes, "boxes", t.int32, (boxes.shape[0], 4))
+        self._check_dev(box_off, "box_off", t.int32, (n + 1,))
+        if boxes.shape[0] == 0:
+            # No boxes at all (no change): still a valid pointer, never read.
+            boxes = t.zeros((1, 4), dtype=t.int32, device=self.device)
+            self._empty_boxes = boxes
+        return boxes.data_ptr(), box_off.data_ptr()
+
+    def step(self, frames, stream_ids=None, boxes=None, box_off=None, out=None, stream=None):
+        t = self.torch
+        frames, code, n, ids, out = self._batch(frames, stream_ids, out)
+        bx = bo = None
+        if boxes is not None or box_off is not None:
+            bx, bo = self._boxes(boxes, box_off, n)
         s = (stream or t.cuda.current_stream(self.device)).cuda_stream
-        ids = stream_ids.data_ptr() if stream_ids is not None else None
-        bx = boxes.data_ptr() if boxes is not None else None
-        bo = box_off.data_ptr() if box_off is not None else None
         reuse_net_step(self.handle, n, ids, frames.data_ptr(), code, bx, bo, out.data_ptr(), s)
         return out
 
     def full(self, frames, stream_ids=None, out=None, stream=None):
         t = self.torch
-        frames, code = self._frames(frames)
-        n = frames.shape[0]
-        if out is None:
-            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        frames, code, n, ids, out = self._batch(frames, stream_ids, out)
         s = (stream or t.cuda.current_stream(self.device)).cuda_stream
-        ids = stream_ids.data_ptr() if stream_ids is not None else None
         reuse_net_full(self.handle, n, ids, frames.data_ptr(), code, out.data_ptr(), s)
         return out
 
@@ -346,7 +397,15 @@ class ReuseNet:
         tensor kept on this object and grown as needed."""
         t = self.torch
         frames, code = self._frames(frames)
+        if not isinstance(box_off, t.Tensor) or box_off.dim() != 1 or box_off.shape[0] < 2:
+            raise ValueError("box_off must be a 1-D int32 tensor of n + 1 entries")
         n = box_off.shape[0] - 1
+        if frames.shape[0] not in (1, n):
+            raise ValueError(f"frames must hold 1 or n = {n} frames, got {frames.shape[0]}")
+        bx, bo = self._boxes(boxes, box_off, n)
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        self._check_dev(out, "out", t.float32, (n, self.n_out))
         need = reuse_net_variant_scratch_bytes(self.handle, n, max_tiles)
         if need == 0:
             _check(load_library().reuse_net_variants(self.handle, base_stream, n, None, 0, 0, None,
@@ -354,11 +413,9 @@ class ReuseNet:
                    self.handle)
         if getattr(self, "_scratch", None) is None or self._scratch.numel() < need:
             self._scratch = t.empty(need, dtype=t.uint8, device=self.device)
-        if out is None:
-            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
         s = (stream or t.cuda.current_stream(self.device)).cuda_stream
         reuse_net_variants(self.handle, base_stream, n, frames.data_ptr(), code, frames.shape[0],
-                           boxes.data_ptr(), box_off.data_ptr(), max_tiles, self._scratch.data_ptr(),
+                           bx, bo, max_tiles, self._scratch.data_ptr(),
                            self._scratch.numel(), out.data_ptr(), s)
         self._last_batch = n
         return out

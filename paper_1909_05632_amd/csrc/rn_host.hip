@@ -273,6 +273,7 @@ VarPlan plan_variants(const Plan &p, int n, int max_tiles) {
 
 struct ProfRec {
     int phase;
+    int layer;                            // conv layer 1..L of the launch, 0 for other kernels
     hipEvent_t e0, e1;
 };
 
@@ -316,14 +317,14 @@ struct reuse_net {
 namespace {
 
 template <typename F>
-hipError_t timed(reuse_net *net, int phase, hipStream_t s, F &&fn) {
+hipError_t timed(reuse_net *net, int phase, hipStream_t s, F &&fn, int layer = 0) {
     if (!net->prof) return fn();
     hipEvent_t e0 = net->next_event(), e1 = net->next_event();
     if (!e0 || !e1) return hipErrorOutOfMemory;
     (void)hipEventRecord(e0, s);
     hipError_t e = fn();
     (void)hipEventRecord(e1, s);
-    net->recs.push_back({phase, e0, e1});
+    net->recs.push_back({phase, layer, e0, e1});
     return e;
 }
 
@@ -421,15 +422,15 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, bool identity, 
         if (p.gen[l - 1])
             e = timed(net, l == 1 ? RN_PHASE_CONV1 : RN_PHASE_CONVN, s, [&] {
                 return launch_conv_gen(cv, p.ks[l - 1], p.st[l - 1], l == 1, net->cus, s);
-            });
+            }, l);
         else if (l == 1)
             e = timed(net, RN_PHASE_CONV1, s, [&] {
                 return bf ? launch_conv_first_bf16(cv, net->cus, s) : launch_conv_first(cv, p.dt, net->cus, s);
-            });
+            }, l);
         else
             e = timed(net, RN_PHASE_CONVN, s, [&] {
                 return bf ? launch_conv_mfma_bf16(cv, net->cus, s) : launch_conv_mfma(cv, p.dt, net->cus, s);
-            });
+            }, l);
         if (e != hipSuccess) return e;
     }
     if (tiles_head && p.dt == RN_BF16) {
@@ -659,11 +660,11 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
         if (l == 1)
             e = timed(net, RN_PHASE_CONV1, s, [&] {
                 return bf ? launch_conv_first_bf16(cv, net->cus, s, true) : launch_conv_first(cv, p.dt, net->cus, s, true);
-            });
+            }, l);
         else
             e = timed(net, RN_PHASE_CONVN, s, [&] {
                 return bf ? launch_conv_mfma_bf16(cv, net->cus, s, true) : launch_conv_mfma(cv, p.dt, net->cus, s, true);
-            });
+            }, l);
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv kernels: ") + hipGetErrorString(e));
     }
     if (bf) {
@@ -718,6 +719,7 @@ rn_status run_full(reuse_net *net, int32_t n, const int32_t *ids_in, const void 
     pa.stack = p.stack;
     pa.H = p.H;
     pa.W = p.W;
+    pa.WW = p.WW;
     for (int l = 0; l <= p.L; ++l) pa.ntl[l] = p.ntl[l];
     pa.ids = ids;
     pa.frames = frames;
@@ -1154,6 +1156,8 @@ rn_status reuse_net_get_profile(reuse_net *net, rn_profile *out) {
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("event time: ") + hipGetErrorString(e));
         out->ms[r.phase] += ms;
         out->launches[r.phase] += 1;
+        out->layer_ms[r.layer] += ms;
+        out->layer_launches[r.layer] += 1;
     }
     return RN_OK;
 }

@@ -145,7 +145,7 @@ struct ConvArgs {
 
 // Dense path: copy the frames into the input cache and mark the slots primed.
 struct PrimeArgs {
-    int n, L, cin, stack, H, W;
+    int n, L, cin, stack, H, W, WW;
     int ntl[RN_MAX_CONV + 1];     // tiles per layer
     const int32_t *ids;
     const void *frames;

@@ -476,9 +476,15 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
     }
 }
 
-// Dense path: copy every pixel of the frames into the input cache (all four
-// ring positions when stacking: before 4 frames exist, frame 0 repeats), mark
-// the slots primed and report every pixel and tile as recomputed.
+// Dense path: copy every pixel of the frames into the input cache, mark the
+// slots primed and report every pixel and tile as recomputed.
+// Stacked input (one block per slot: the block reads the slot's primed flag
+// and ring head before its thread 0 updates them): an unprimed slot takes the
+// frame at all four ring positions (before 4 frames exist, frame 0 repeats)
+// and an empty change ring, as a first step does; a primed slot pushes the
+// frame into its ring as a step does, with the frame's own change against
+// the newest cached frame in the change ring, so the steps that follow see
+// the stack's change exactly as after a step on this frame.
 template <bool U8>
 __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
     const int i = blockIdx.x;
@@ -486,27 +492,53 @@ __global__ __launch_bounds__(kThreads) void k_prime(PrimeArgs a) {
     const size_t HW = (size_t)a.H * a.W;
     const int C = a.cin;
     const size_t fbase = (size_t)i * C * HW;
-    const int n4 = (int)(HW / 4);
-    for (int q = blockIdx.y * blockDim.x + threadIdx.x; q < n4; q += gridDim.y * blockDim.x) {
-        for (int c = 0; c < C; ++c) {
-            const float4 v = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, a.lut);
-            if (a.stack == 1) {
+    if (a.stack == 1) {
+        const int n4 = (int)(HW / 4);
+        for (int q = blockIdx.y * blockDim.x + threadIdx.x; q < n4; q += gridDim.y * blockDim.x)
+            for (int c = 0; c < C; ++c) {
+                const float4 v = load4<U8>(a.frames, fbase + c * HW + 4 * (size_t)q, a.lut);
                 *reinterpret_cast<float4 *>(a.xin + (size_t)slot * C * HW + c * HW + 4 * (size_t)q) = v;
+            }
+    } else {
+        const int primed = a.primed[slot];
+        const int head = a.ring_head[slot];
+        const int nhead = primed ? (head + 1) & 3 : 0;
+        float *planes = a.xin + (size_t)slot * 4 * C * HW;        // ring position r: planes + r C HW
+        const float *prev = planes + (size_t)head * C * HW;
+        uint64_t *ring = a.dring + (size_t)slot * a.dring_words;  // [4][H][WW]
+        const size_t HWW = (size_t)a.H * a.WW;
+        for (size_t w = threadIdx.x; w < HWW; w += blockDim.x) {
+            const int y = (int)(w / a.WW), x0 = (int)(w - (size_t)y * a.WW) * 64;
+            const int x1 = min(x0 + 64, a.W);
+            uint64_t bits = 0ull;
+            for (int c = 0; c < C; ++c)
+                for (int x = x0; x < x1; x += 4) {
+                    const size_t px = c * HW + (size_t)y * a.W + x;
+                    const float4 v = load4<U8>(a.frames, fbase + px, a.lut);
+                    if (primed) {
+                        const float4 o = *reinterpret_cast<const float4 *>(prev + px);
+                        const uint64_t d = (f32_bits(v.x) != f32_bits(o.x) ? 1u : 0u) |
+                                           (f32_bits(v.y) != f32_bits(o.y) ? 2u : 0u) |
+                                           (f32_bits(v.z) != f32_bits(o.z) ? 4u : 0u) |
+                                           (f32_bits(v.w) != f32_bits(o.w) ? 8u : 0u);
+                        bits |= d << (x - x0);
+                        *reinterpret_cast<float4 *>(planes + (size_t)nhead * C * HW + px) = v;
+                    } else {
+                        for (int r = 0; r < 4; ++r)
+                            *reinterpret_cast<float4 *>(planes + (size_t)r * C * HW + px) = v;
+                    }
+                }
+            if (primed) {
+                ring[(size_t)nhead * HWW + w] = bits;
             } else {
-                for (int r = 0; r < 4; ++r)
-                    *reinterpret_cast<float4 *>(a.xin + ((size_t)slot * 4 + r) * C * HW + c * HW +
-                                                4 * (size_t)q) = v;
+                for (int r = 0; r < 4; ++r) ring[(size_t)r * HWW + w] = 0ull;
             }
         }
-    }
-    if (a.stack != 1) {
-        uint64_t *ring = a.dring + (size_t)slot * a.dring_words;
-        for (size_t w = blockIdx.y * blockDim.x + threadIdx.x; w < a.dring_words; w += gridDim.y * blockDim.x)
-            ring[w] = 0ull;
+        __syncthreads();                      // every thread has read the flags
+        if (threadIdx.x == 0) a.ring_head[slot] = nhead;
     }
     if (blockIdx.y == 0 && threadIdx.x == 0) {
         a.primed[slot] = 1;
-        if (a.stack != 1) a.ring_head[slot] = 0;
         a.nchg[i] = (int)HW;
         for (int l = 0; l <= a.L; ++l) a.ntile[(size_t)i * (a.L + 1) + l] = a.ntl[l];
     }
@@ -928,7 +960,7 @@ hipError_t launch_masks(const MaskGeom &geom, const MaskArgs &args, int cus, hip
 }
 
 hipError_t launch_prime(const PrimeArgs &a, hipStream_t s) {
-    dim3 grid(a.n, 4);
+    dim3 grid(a.n, a.stack == 1 ? 4 : 1);     // stacked: one block per slot (see k_prime)
     if (a.frame_u8)
         hipLaunchKernelGGL(k_prime<true>, grid, dim3(kThreads), 0, s, a);
     else

@@ -171,3 +171,61 @@ def test_null_net_calls_return_einval():
     assert lib.reuse_net_variant_scratch_bytes(None, 4, 0) == 0
     assert lib.reuse_net_variants(None, 0, 4, None, 0, 1, None, None, 0, None, 0, None, None) == B.RN_EINVAL
     lib.reuse_net_destroy(None)
+
+
+def _bare_net(in_c=1, h=16, w=12, n_out=6, max_streams=8):
+    """A ReuseNet shell with the fields the binding's argument checks read, on
+    the CPU device (no library handle: every case below must fail before a
+    call reaches the library)."""
+    import torch
+    net = B.ReuseNet.__new__(B.ReuseNet)
+    net.torch = torch
+    net.device = torch.device("cpu")
+    net.in_c, net.h, net.w, net.n_out, net.max_streams = in_c, h, w, n_out, max_streams
+    net.handle = None
+    return net
+
+
+def test_binding_rejects_bad_tensors_before_any_launch():
+    import torch
+    net = _bare_net()
+    f = torch.zeros((3, 1, 16, 12), dtype=torch.float32)
+    ok_ids = torch.arange(3, dtype=torch.int32)
+    ok_out = torch.zeros((3, 6), dtype=torch.float32)
+    bad = [
+        # int64 ids (torch's default integer) would be read as int32 pairs
+        dict(stream_ids=torch.arange(3)),
+        dict(stream_ids=torch.arange(4, dtype=torch.int32)),                 # wrong length
+        dict(stream_ids=torch.arange(6, dtype=torch.int32)[::2]),            # not contiguous
+        dict(out=torch.zeros((3, 5), dtype=torch.float32)),                  # undersized logits
+        dict(out=torch.zeros((3, 6), dtype=torch.float64)),
+        dict(out=torch.zeros((6, 3), dtype=torch.float32).t()),              # not contiguous
+        dict(boxes=torch.zeros((2, 4), dtype=torch.int64), box_off=torch.tensor([0, 1, 2, 2], dtype=torch.int32)),
+        dict(boxes=torch.zeros((2, 4), dtype=torch.int32), box_off=torch.tensor([0, 1, 2], dtype=torch.int32)),
+        dict(boxes=torch.zeros((2, 3), dtype=torch.int32), box_off=torch.tensor([0, 1, 2, 2], dtype=torch.int32)),
+        dict(boxes=torch.zeros((2, 4), dtype=torch.int32)),                  # boxes without offsets
+    ]
+    for kw in bad:
+        args = dict(stream_ids=ok_ids, out=ok_out)
+        args.update(kw)
+        with pytest.raises((TypeError, ValueError)):
+            net.step(f, **args)
+    for frames in (torch.zeros((3, 1, 16, 8)),                                # wrong frame shape
+                   torch.zeros((3, 2, 16, 12)),                               # wrong channel count
+                   torch.zeros((3, 16, 12)),                                  # missing channel axis
+                   torch.zeros((3, 1, 16, 12), dtype=torch.float16),          # unsupported dtype
+                   torch.zeros((9, 1, 16, 12)),                               # more streams than slots
+                   torch.zeros((3, 1, 12, 16)).transpose(2, 3)):              # not contiguous
+        with pytest.raises((TypeError, ValueError)):
+            net.step(frames)
+        with pytest.raises((TypeError, ValueError)):
+            net.full(frames)
+    # variants: 1 or n frames, int32 boxes and n + 1 offsets
+    boxes = torch.zeros((2, 4), dtype=torch.int32)
+    off = torch.tensor([0, 1, 2], dtype=torch.int32)
+    with pytest.raises(ValueError):
+        net.variants(0, boxes, off, torch.zeros((3, 1, 16, 12)))
+    with pytest.raises((TypeError, ValueError)):
+        net.variants(0, boxes, off.long(), torch.zeros((1, 1, 16, 12)))
+    with pytest.raises((TypeError, ValueError)):
+        net.variants(0, boxes, off, torch.zeros((2, 1, 16, 12)), out=torch.zeros((2, 5)))
