@@ -77,6 +77,9 @@ def lib():
         L.orc_forward.argtypes = [ctypes.POINTER(_Net), P, P, P, P, I, P, P, P]
         L.orc_masks.argtypes = [ctypes.POINTER(_Net), I, P, P, P]
         L.orc_reuse_step.argtypes = [ctypes.POINTER(_Net), P, P, P, P, P, P, I, P, P]
+        L.orc_reinforce_dlogits.argtypes = [I, I, P, P, P, P]
+        L.orc_forward_preact.argtypes = [ctypes.POINTER(_Net), P, P, P, P]
+        L.orc_backward.argtypes = [ctypes.POINTER(_Net), P, P, P, P, I, P, P, P, P, P, P]
         _lib = L
     return _lib
 
@@ -310,3 +313,48 @@ class ReuseStream:
             raise ValueError("oracle: bad net description")
         self.primed = True
         return logits
+
+
+# ------------------------------------------------------------ training
+
+def reinforce_dlogits(logits: np.ndarray, actions: np.ndarray, returns: np.ndarray) -> np.ndarray:
+    """dJ/dlogits [n][n_out] of the REINFORCE loss (Sec. 2) J = sum_i -G_i log softmax(z_i)[a_i]."""
+    z = _f32(logits)
+    n, n_out = z.shape
+    a = np.ascontiguousarray(actions, dtype=np.int32)
+    g = _f32(returns)
+    out = np.empty((n, n_out), np.float32)
+    lib().orc_reinforce_dlogits(n, n_out, _p(z), _p(a), _p(g), _p(out))
+    return out
+
+
+def forward_preact(net: Net, conv_w, conv_b, x: np.ndarray) -> list:
+    """Pre-activations (before the ReLU) of every layer for one input x [in_c][h][w]."""
+    x = _f32(x)
+    cw = [_f32(w) for w in conv_w]
+    cb = [_f32(b) for b in conv_b]
+    z = [np.empty(net.layer_shape(l + 1), np.float32) for l in range(len(net.convs))]
+    rc = lib().orc_forward_preact(ctypes.byref(net.c_struct()), _ptr_array(cw), _ptr_array(cb), _p(x),
+                                  _ptr_array(z))
+    if rc != 0:
+        raise ValueError("oracle: bad net description (float32 nets only)")
+    return z
+
+
+def backward(net: Net, conv_w, conv_b, dense_w, dense_b, x: np.ndarray, g: np.ndarray):
+    """Gradients of sum_i sum_o g[i][o] logits[i][o] over n inputs x [n][in_c][h][w]
+    -> (dconv_w list OIHW, dconv_b list, ddense_w [n_out][C_L H_L W_L], ddense_b)."""
+    x, g = _f32(x), _f32(g)
+    n = x.shape[0]
+    assert g.shape == (n, net.n_out)
+    cw = [_f32(w) for w in conv_w]
+    cb = [_f32(b) for b in conv_b]
+    dw, db = _f32(dense_w), _f32(dense_b)
+    gw = [np.empty_like(w) for w in cw]
+    gb = [np.empty_like(b) for b in cb]
+    gdw, gdb = np.empty_like(dw), np.empty_like(db)
+    rc = lib().orc_backward(ctypes.byref(net.c_struct()), _ptr_array(cw), _ptr_array(cb), _p(dw), _p(db),
+                            n, _p(x), _p(g), _ptr_array(gw), _ptr_array(gb), _p(gdw), _p(gdb))
+    if rc != 0:
+        raise ValueError("oracle: bad net description (float32 nets only)")
+    return gw, gb, gdw, gdb

@@ -357,3 +357,192 @@ int orc_reuse_step(const orc_net *net, const float *const *conv_w, const float *
     orc_dense((int)layer_elems(net, L), cache[L], net->n_out, dense_w, dense_b, logits);
     return 0;
 }
+
+/* ------------------------------------------------------------- training */
+
+/* Sec. 2: the policy is trained with REINFORCE.  For input i with logits z,
+ * sampled action a and return G, the loss is -G log softmax(z)[a]; its
+ * derivative with respect to z[o] is G (softmax(z)[o] - [o == a]). */
+void orc_reinforce_dlogits(int n, int n_out, const float *logits, const int32_t *actions,
+                           const float *returns, float *g) {
+    for (int i = 0; i < n; ++i) {
+        const float *z = logits + (size_t)i * n_out;
+        double zmax = z[0];
+        for (int o = 1; o < n_out; ++o)
+            if (z[o] > zmax) zmax = z[o];
+        double den = 0.0;
+        for (int o = 0; o < n_out; ++o) den += exp((double)z[o] - zmax);
+        for (int o = 0; o < n_out; ++o) {
+            double p = exp((double)z[o] - zmax) / den;
+            double onehot = (o == actions[i]) ? 1.0 : 0.0;
+            g[(size_t)i * n_out + o] = (float)((double)returns[i] * (p - onehot));
+        }
+    }
+}
+
+static double conv_sum(int cin, int h, int w, const float *x, int k, int s, int p,
+                       const float *wt, const float *b, int co, int yo, int xo) {
+    /* b[co] + sum_{ci,ky,kx} w[co][ci][ky][kx] * x[ci][s*yo-p+ky][s*xo-p+kx] */
+    double acc = (double)b[co];
+    for (int ci = 0; ci < cin; ++ci)
+        for (int ky = 0; ky < k; ++ky)
+            for (int kx = 0; kx < k; ++kx) {
+                int y = s * yo - p + ky, xx = s * xo - p + kx;
+                if (y < 0 || y >= h || xx < 0 || xx >= w) continue;
+                acc += (double)wt[(((size_t)co * cin + ci) * k + ky) * k + kx] *
+                       (double)x[((size_t)ci * h + y) * w + xx];
+            }
+    return acc;
+}
+
+int orc_forward_preact(const orc_net *net, const float *const *conv_w, const float *const *conv_b,
+                       const float *x, float *const *z) {
+    /* One input: each layer's pre-activation fl32(b + sum w a) (before the
+     * ReLU), with the layer inputs a the float32 activations of orc_forward. */
+    if (!net_ok(net) || net->bf16) return -1;
+    int L = net->n_conv;
+    float *a = (float *)malloc(layer_elems(net, 0) * sizeof(float));
+    memcpy(a, x, layer_elems(net, 0) * sizeof(float));
+    for (int l = 0; l < L; ++l) {
+        int c, h, w, co, ho, wo;
+        orc_layer_shape(net, l, &c, &h, &w);
+        orc_layer_shape(net, l + 1, &co, &ho, &wo);
+        float *an = (float *)malloc((size_t)co * ho * wo * sizeof(float));
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int o = 0; o < co; ++o)
+            for (int yo = 0; yo < ho; ++yo)
+                for (int xo = 0; xo < wo; ++xo) {
+                    float v = (float)conv_sum(c, h, w, a, net->k[l], net->s[l], net->p[l], conv_w[l],
+                                              conv_b[l], o, yo, xo);
+                    z[l][((size_t)o * ho + yo) * wo + xo] = v;
+                    an[((size_t)o * ho + yo) * wo + xo] = v > 0.0f ? v : 0.0f;
+                }
+        free(a);
+        a = an;
+    }
+    free(a);
+    return 0;
+}
+
+int orc_backward(const orc_net *net, const float *const *conv_w, const float *const *conv_b,
+                 const float *dense_w, const float *dense_b, int n, const float *x, const float *g,
+                 float *const *dconv_w, float *const *dconv_b, float *ddense_w, float *ddense_b) {
+    /* Backpropagation of J = sum_i sum_o g[i][o] logits[i][o] through the
+     * network of orc_forward (float32 activations a_l = ReLU(fl32(z_l))),
+     * summed over the n inputs x [n][in_c][h][w].  Chain rule, all in double:
+     *   dbd[o]      = sum_i g[i][o]
+     *   dWd[o][j]   = sum_i g[i][o] a_L[i][j]
+     *   da_L[i][j]  = sum_o Wd[o][j] g[i][o]
+     *   dz_l        = da_l where a_l > 0, else 0   (ReLU derivative, 0 at the kink)
+     *   dW_l[co][ci][ky][kx] = sum_i sum_{yo,xo} dz_l[co][yo][xo] a_{l-1}[ci][s yo-p+ky][s xo-p+kx]
+     *   db_l[co]    = sum_i sum_{yo,xo} dz_l[co][yo][xo]
+     *   da_{l-1}[ci][y][x] = sum over (co, ky, kx, yo, xo) with s yo-p+ky = y and
+     *                        s xo-p+kx = x of W_l[co][ci][ky][kx] dz_l[co][yo][xo]
+     * Each gradient is rounded once to float32.  Float32 weights only. */
+    if (!net_ok(net) || net->bf16) return -1;
+    int L = net->n_conv;
+    size_t kdim = layer_elems(net, L);
+    size_t nw[ORC_MAX_LAYERS];
+    double *gw[ORC_MAX_LAYERS], *gb[ORC_MAX_LAYERS];
+    for (int l = 0; l < L; ++l) {
+        nw[l] = (size_t)net->cout[l] * net->cin[l] * net->k[l] * net->k[l];
+        gw[l] = (double *)calloc(nw[l], sizeof(double));
+        gb[l] = (double *)calloc((size_t)net->cout[l], sizeof(double));
+    }
+    double *gwd = (double *)calloc((size_t)net->n_out * kdim, sizeof(double));
+    double *gbd = (double *)calloc((size_t)net->n_out, sizeof(double));
+    float *act[ORC_MAX_LAYERS + 1];
+    for (int l = 0; l <= L; ++l) act[l] = (float *)malloc(layer_elems(net, l) * sizeof(float));
+    double *da = (double *)malloc(kdim * sizeof(double));
+    for (int i = 0; i < n; ++i) {
+        const float *gi = g + (size_t)i * net->n_out;
+        /* forward: the float32 activations of every layer */
+        memcpy(act[0], x + (size_t)i * layer_elems(net, 0), layer_elems(net, 0) * sizeof(float));
+        for (int l = 0; l < L; ++l) {
+            int c, h, w, co, ho, wo;
+            orc_layer_shape(net, l, &c, &h, &w);
+            orc_layer_shape(net, l + 1, &co, &ho, &wo);
+#pragma omp parallel for schedule(dynamic, 1)
+            for (int o = 0; o < co; ++o)
+                for (int yo = 0; yo < ho; ++yo)
+                    for (int xo = 0; xo < wo; ++xo)
+                        act[l + 1][((size_t)o * ho + yo) * wo + xo] =
+                            conv_pixel(c, h, w, act[l], net->k[l], net->s[l], net->p[l], conv_w[l],
+                                       conv_b[l], 0, o, yo, xo);
+        }
+        /* dense layer */
+        for (int o = 0; o < net->n_out; ++o) gbd[o] += (double)gi[o];
+#pragma omp parallel for schedule(static)
+        for (size_t j = 0; j < kdim; ++j) {
+            double s = 0.0;
+            for (int o = 0; o < net->n_out; ++o) {
+                gwd[(size_t)o * kdim + j] += (double)gi[o] * (double)act[L][j];
+                s += (double)dense_w[(size_t)o * kdim + j] * (double)gi[o];
+            }
+            da[j] = s;
+        }
+        /* conv layers, last to first; da holds dJ/da_l on entry */
+        double *da_cur = da;
+        for (int l = L - 1; l >= 0; --l) {
+            int c, h, w, co, ho, wo;
+            orc_layer_shape(net, l, &c, &h, &w);
+            orc_layer_shape(net, l + 1, &co, &ho, &wo);
+            int k = net->k[l], s = net->s[l], p = net->p[l];
+            size_t nout = (size_t)co * ho * wo;
+            double *dz = (double *)malloc(nout * sizeof(double));
+            for (size_t e = 0; e < nout; ++e) dz[e] = act[l + 1][e] > 0.0f ? da_cur[e] : 0.0;
+#pragma omp parallel for schedule(dynamic, 1)
+            for (int o = 0; o < co; ++o)
+                for (int yo = 0; yo < ho; ++yo)
+                    for (int xo = 0; xo < wo; ++xo) {
+                        double d = dz[((size_t)o * ho + yo) * wo + xo];
+                        gb[l][o] += d;
+                        for (int ci = 0; ci < c; ++ci)
+                            for (int ky = 0; ky < k; ++ky)
+                                for (int kx = 0; kx < k; ++kx) {
+                                    int y = s * yo - p + ky, xx = s * xo - p + kx;
+                                    if (y < 0 || y >= h || xx < 0 || xx >= w) continue;
+                                    gw[l][(((size_t)o * c + ci) * k + ky) * k + kx] +=
+                                        d * (double)act[l][((size_t)ci * h + y) * w + xx];
+                                }
+                    }
+            double *da_prev = NULL;
+            if (l > 0) {
+                da_prev = (double *)malloc((size_t)c * h * w * sizeof(double));
+#pragma omp parallel for schedule(dynamic, 1)
+                for (int ci = 0; ci < c; ++ci)
+                    for (int y = 0; y < h; ++y)
+                        for (int xx = 0; xx < w; ++xx) {
+                            double acc = 0.0;
+                            for (int o = 0; o < co; ++o)
+                                for (int ky = 0; ky < k; ++ky)
+                                    for (int kx = 0; kx < k; ++kx) {
+                                        int ny = y + p - ky, nx = xx + p - kx;
+                                        if (ny < 0 || nx < 0 || ny % s || nx % s) continue;
+                                        int yo = ny / s, xo = nx / s;
+                                        if (yo >= ho || xo >= wo) continue;
+                                        acc += (double)conv_w[l][(((size_t)o * c + ci) * k + ky) * k + kx] *
+                                               dz[((size_t)o * ho + yo) * wo + xo];
+                                    }
+                            da_prev[((size_t)ci * h + y) * w + xx] = acc;
+                        }
+            }
+            free(dz);
+            if (da_cur != da) free(da_cur);
+            da_cur = da_prev;
+        }
+    }
+    for (int l = 0; l < L; ++l) {
+        for (size_t e = 0; e < nw[l]; ++e) dconv_w[l][e] = (float)gw[l][e];
+        for (int o = 0; o < net->cout[l]; ++o) dconv_b[l][o] = (float)gb[l][o];
+        free(gw[l]);
+        free(gb[l]);
+    }
+    for (size_t e = 0; e < (size_t)net->n_out * kdim; ++e) ddense_w[e] = (float)gwd[e];
+    for (int o = 0; o < net->n_out; ++o) ddense_b[o] = (float)gbd[o];
+    free(gwd);
+    free(gbd);
+    free(da);
+    for (int l = 0; l <= L; ++l) free(act[l]);
+    return 0;
+}

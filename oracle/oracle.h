@@ -123,6 +123,29 @@ int orc_reuse_step(const orc_net *net, const float *const *conv_w, const float *
                    const float *dense_w, const float *dense_b, const float *x,
                    const uint8_t *d0_given, int primed, float *const *cache, float *logits);
 
+/* ---- training (Sec. 2: the policy is trained with REINFORCE) ---- */
+
+/* dJ/dlogits of the REINFORCE loss J = sum_i -returns[i] log softmax(logits_i)[actions[i]]:
+ * g[i][o] = returns[i] (softmax(logits_i)[o] - [o == actions[i]]).  Double inside. */
+void orc_reinforce_dlogits(int n, int n_out, const float *logits, const int32_t *actions,
+                           const float *returns, float *g);
+
+/* Pre-activations of one input: z[l] = fl32(b + sum w a_{l-1}) of layer l + 1,
+ * [C][H][W], before the ReLU (a = the float32 activations of orc_forward).
+ * Float32 nets only.  Returns 0 or -1. */
+int orc_forward_preact(const orc_net *net, const float *const *conv_w, const float *const *conv_b,
+                       const float *x, float *const *z);
+
+/* Gradients of J = sum_i sum_o g[i][o] logits[i][o] with respect to every
+ * weight and bias, summed over the n inputs x [n][in_c][h][w] (backpropagation
+ * through orc_forward, double accumulation, ReLU derivative 0 at the kink).
+ * Outputs in the layouts of the weights: dconv_w[l] OIHW, dconv_b[l] [cout],
+ * ddense_w [n_out][C_L H_L W_L] in (c, y, x) order, ddense_b [n_out].
+ * Float32 nets only.  Returns 0 or -1. */
+int orc_backward(const orc_net *net, const float *const *conv_w, const float *const *conv_b,
+                 const float *dense_w, const float *dense_b, int n, const float *x, const float *g,
+                 float *const *dconv_w, float *const *dconv_b, float *ddense_w, float *ddense_b);
+
 #ifdef __cplusplus
 }
 #endif

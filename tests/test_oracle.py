@@ -483,3 +483,102 @@ def test_variant_equals_reuse_step_from_base(orc):
         got = rs.step(x, d0=orc.box_mask(15, 13, boxes))
         ref = orc.forward(net, cw, cb, dw, db, x[None])[0][0]
         assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), boxes
+
+
+# ------------------------------------------------------------------ training (Sec. 2: REINFORCE)
+
+def _torch_grads(net, cw, cb, dw, db, x, g):
+    """Gradients of sum(g * logits) by torch float64 autograd through the same
+    function the oracle evaluates: float32 activations (the rounding passes
+    the gradient through unchanged), double arithmetic otherwise."""
+    T = lambda a: torch.tensor(a, dtype=torch.float64, requires_grad=True)
+    tw, tb, tdw, tdb = [T(w) for w in cw], [T(b) for b in cb], T(dw), T(db)
+    a = torch.tensor(x, dtype=torch.float64)
+    for (ci, co, k, s, p), w_, b_ in zip(net.convs, tw, tb):
+        a = torch.relu(F.conv2d(a, w_, b_, stride=s, padding=p)).float().double()
+    logits = a.flatten(1) @ tdw.T + tdb
+    (logits * torch.tensor(g, dtype=torch.float64)).sum().backward()
+    return [w.grad.numpy() for w in tw], [b.grad.numpy() for b in tb], tdw.grad.numpy(), tdb.grad.numpy()
+
+
+def _rand_net(orc, rng, convs, h, w, n_out, in_c=1):
+    net = orc.Net(in_c, h, w, convs, n_out)
+    cw = [rng.normal(0, 0.3, (co, ci, k, k)).astype(np.float32) for (ci, co, k, s, p) in convs]
+    cb = [rng.normal(0, 0.1, co).astype(np.float32) for (ci, co, k, s, p) in convs]
+    c, hl, wl = net.layer_shape(len(convs))
+    dw = rng.normal(0, 0.1, (n_out, c * hl * wl)).astype(np.float32)
+    db = rng.normal(0, 0.1, n_out).astype(np.float32)
+    return net, cw, cb, dw, db
+
+
+@pytest.mark.parametrize("convs,h,w,in_c", [
+    ([(1, 5, 3, 1, 1), (5, 7, 3, 1, 1)], 12, 16, 1),                      # the paper's 2 conv + dense
+    ([(4, 6, 3, 1, 1), (6, 8, 3, 1, 1), (8, 8, 3, 1, 1)], 9, 13, 4),     # ragged, stacked input
+    ([(1, 4, 5, 2, 2), (4, 6, 3, 1, 0)], 17, 15, 1),                      # strided, unpadded
+])
+def test_backward_matches_torch_autograd(orc, convs, h, w, in_c):
+    rng = np.random.default_rng(len(convs) * 100 + h)
+    net, cw, cb, dw, db = _rand_net(orc, rng, convs, h, w, 5, in_c)
+    x = rng.random((3, in_c, h, w)).astype(np.float32)
+    g = rng.normal(0, 1, (3, 5)).astype(np.float32)
+    got = orc.backward(net, cw, cb, dw, db, x, g)
+    want = _torch_grads(net, cw, cb, dw, db, x, g)
+    for gs, ws in zip(got, want):
+        for a, b in zip(gs if isinstance(gs, list) else [gs], ws if isinstance(ws, list) else [ws]):
+            assert a.shape == b.shape
+            assert np.abs(a - b).max() <= 1e-6 * max(1.0, np.abs(b).max())
+
+
+def test_backward_dense_closed_form_and_linearity(orc):
+    # The dense layer's gradients are the outer products g^T a_L and g summed
+    # over the batch; every gradient is linear in g and additive over inputs.
+    rng = np.random.default_rng(5)
+    net, cw, cb, dw, db = _rand_net(orc, rng, [(1, 4, 3, 1, 1), (4, 6, 3, 1, 1)], 10, 12, 3)
+    x = rng.random((4, 1, 10, 12)).astype(np.float32)
+    g = rng.normal(0, 1, (4, 3)).astype(np.float32)
+    _, acts = orc.forward(net, cw, cb, dw, db, x, want_acts=True)
+    gw, gb, gdw, gdb = orc.backward(net, cw, cb, dw, db, x, g)
+    aL = acts[-1].reshape(4, -1).astype(np.float64)
+    assert np.allclose(gdw, g.astype(np.float64).T @ aL, rtol=0, atol=1e-6)
+    assert np.allclose(gdb, g.sum(0), rtol=0, atol=1e-6)
+    g2 = orc.backward(net, cw, cb, dw, db, x, 2 * g)
+    for a, b in zip(gw + gb + [gdw, gdb], g2[0] + g2[1] + [g2[2], g2[3]]):
+        assert np.array_equal(2 * a, b)                # scaling by 2 is exact
+    parts = [orc.backward(net, cw, cb, dw, db, x[i:i + 1], g[i:i + 1]) for i in range(4)]
+    for k, tot in enumerate(gw):
+        assert np.allclose(sum(p[0][k] for p in parts), tot, rtol=0, atol=1e-5)
+    # an input whose activations are all zero passes no gradient to the conv weights
+    z = orc.backward(net, cw, [np.full_like(b, -50.0) for b in cb], dw, db, x[:1], g[:1])
+    assert all(np.count_nonzero(a) == 0 for a in z[0] + z[1])
+
+
+def test_reinforce_dlogits(orc):
+    # g = G (softmax(z) - onehot(a)): rows sum to 0, G = 0 gives 0, and it is
+    # torch's float64 gradient of -G log_softmax(z)[a].
+    rng = np.random.default_rng(9)
+    z = rng.normal(0, 3, (7, 6)).astype(np.float32)
+    a = rng.integers(0, 6, 7).astype(np.int32)
+    G = rng.normal(0, 2, 7).astype(np.float32)
+    G[3] = 0.0
+    g = orc.reinforce_dlogits(z, a, G)
+    assert np.abs(g.sum(1)).max() <= 1e-6
+    assert np.count_nonzero(g[3]) == 0
+    tz = torch.tensor(z, dtype=torch.float64, requires_grad=True)
+    loss = -(torch.tensor(G, dtype=torch.float64) *
+             torch.log_softmax(tz, 1)[torch.arange(7), torch.tensor(a, dtype=torch.long)]).sum()
+    loss.backward()
+    assert np.abs(g - tz.grad.numpy()).max() <= 1e-6
+    # large logits do not overflow (the maximum is taken out before exp)
+    big = orc.reinforce_dlogits(np.array([[1000.0, 0.0]], np.float32), np.array([0], np.int32),
+                                np.array([1.0], np.float32))
+    assert np.all(np.isfinite(big)) and abs(big[0, 0]) < 1e-6
+
+
+def test_forward_preact_relu_gives_forward(orc):
+    rng = np.random.default_rng(11)
+    net, cw, cb, dw, db = _rand_net(orc, rng, [(1, 4, 3, 1, 1), (4, 6, 3, 1, 1)], 10, 12, 3)
+    x = rng.random((1, 1, 10, 12)).astype(np.float32)
+    z = orc.forward_preact(net, cw, cb, x[0])
+    _, acts = orc.forward(net, cw, cb, dw, db, x, want_acts=True)
+    for zl, al in zip(z, acts):
+        assert np.array_equal(np.where(zl > 0, zl, np.float32(0)), al[0])
