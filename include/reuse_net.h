@@ -214,6 +214,26 @@ rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, con
                              const int32_t *dev_box_off, int32_t max_tiles, void *dev_scratch,
                              size_t scratch_bytes, float *dev_logits, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * reuse_net_variants with the library's own scratch instead of dev_scratch.
+ * That scratch is a static device array of RN_STATIC_SCRATCH_BYTES per GPU
+ * (64 MiB; 4096 variants of a 105x80 frame with max_tiles = 16 need about
+ * 44 MB), held by each GPU the library runs on until the process ends.  The
+ * call allocates nothing; a request whose scratch
+ * (reuse_net_variant_scratch_bytes) exceeds the limit returns RN_ENOSPACE and
+ * launches nothing.  Every call on one GPU, from any net, shares that GPU's
+ * array and leaves its contents there: calls that overlap on one GPU (on
+ * different streams or from different threads) race, and the introspection
+ * functions describe a static call's variants only until the next one on
+ * that GPU.  The net must be used with the device that was current at
+ * reuse_net_create.  Arguments and results as reuse_net_variants. */
+#define RN_STATIC_SCRATCH_BYTES (64u << 20)
+rn_status reuse_net_variants_static(reuse_net *net, int32_t base_stream, int32_t n, const void *dev_frames,
+                                    rn_dtype frame_dtype, int32_t frame_count, const int32_t *dev_boxes,
+                                    const int32_t *dev_box_off, int32_t max_tiles, float *dev_logits,
+                                    void *hip_stream);
+
 /* ---- introspection (synchronous; for parity checks and statistics) ---- */
 
 /* Pixel change mask of a slot after its last step, layer 0 (input) .. n_conv.

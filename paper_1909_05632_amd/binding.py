@@ -33,8 +33,9 @@ EXPORTS = (
     "reuse_net_get_worklist", "reuse_net_read_activation", "reuse_net_get_stats",
     "reuse_net_set_profiling", "reuse_net_get_profile", "reuse_net_last_error",
     "reuse_net_destroy", "reuse_net_variant_scratch_bytes", "reuse_net_variants",
-    "reuse_net_set_weights",
+    "reuse_net_set_weights", "reuse_net_variants_static",
 )
+RN_STATIC_SCRATCH_BYTES = 64 << 20
 
 
 class rn_conv_spec(ctypes.Structure):
@@ -100,6 +101,8 @@ def load_library(path: str = LIB_PATH):
     L.reuse_net_variant_scratch_bytes.argtypes = [P, I32, I32]
     L.reuse_net_variants.restype = st
     L.reuse_net_variants.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, SZ, P, P]
+    L.reuse_net_variants_static.restype = st
+    L.reuse_net_variants_static.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, P]
     for name in ("reuse_net_get_pixel_mask", "reuse_net_get_tile_mask"):
         getattr(L, name).restype = st
         getattr(L, name).argtypes = [P, I32, I32, P, SZ]
@@ -177,6 +180,14 @@ def reuse_net_variants(net: int, base_stream: int, n: int, dev_frames: int, fram
     _check(load_library().reuse_net_variants(net, base_stream, n, dev_frames, frame_dtype, frame_count,
                                              dev_boxes, dev_box_off, max_tiles, dev_scratch,
                                              scratch_bytes, dev_logits, hip_stream), net)
+
+
+def reuse_net_variants_static(net: int, base_stream: int, n: int, dev_frames: int, frame_dtype: int,
+                              frame_count: int, dev_boxes: int, dev_box_off: int, max_tiles: int,
+                              dev_logits: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_variants_static(net, base_stream, n, dev_frames, frame_dtype, frame_count,
+                                                    dev_boxes, dev_box_off, max_tiles, dev_logits, hip_stream),
+           net)
 
 
 def reuse_net_get_pixel_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
@@ -417,6 +428,28 @@ class ReuseNet:
         reuse_net_variants(self.handle, base_stream, n, frames.data_ptr(), code, frames.shape[0],
                            bx, bo, max_tiles, self._scratch.data_ptr(),
                            self._scratch.numel(), out.data_ptr(), s)
+        self._last_batch = n
+        return out
+
+    def variants_static(self, base_stream: int, boxes, box_off, frames, max_tiles: int = 0, out=None,
+                        stream=None):
+        """As variants(), through reuse_net_variants_static: the library's static
+        per-GPU scratch, no allocation by the library (out is allocated here
+        only when not given)."""
+        t = self.torch
+        frames, code = self._frames(frames)
+        if not isinstance(box_off, t.Tensor) or box_off.dim() != 1 or box_off.shape[0] < 2:
+            raise ValueError("box_off must be a 1-D int32 tensor of n + 1 entries")
+        n = box_off.shape[0] - 1
+        if frames.shape[0] not in (1, n):
+            raise ValueError(f"frames must hold 1 or n = {n} frames, got {frames.shape[0]}")
+        bx, bo = self._boxes(boxes, box_off, n)
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        self._check_dev(out, "out", t.float32, (n, self.n_out))
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_variants_static(self.handle, base_stream, n, frames.data_ptr(), code, frames.shape[0],
+                                  bx, bo, max_tiles, out.data_ptr(), s)
         self._last_batch = n
         return out
 

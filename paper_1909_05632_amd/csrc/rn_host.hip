@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -277,12 +278,47 @@ struct ProfRec {
     hipEvent_t e0, e1;
 };
 
+// Scratch of reuse_net_variants_static: a file-scope device array, so the
+// call needs no allocation.  Each GPU the library runs on holds its own copy
+// until the process ends; host code must use the per-device address from
+// hipGetSymbolAddress, never the array's name (a host-side stand-in).
+static __device__ __align__(256) unsigned char scratch[RN_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {nullptr};
+
+// Device address of `scratch` on device dev (looked up once per device, with
+// dev current).  NULL and a message in *err on failure.
+void *static_scratch(int dev, std::string *err) {
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = "device index beyond the static scratch table";
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int cur = -1;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+        void *p = nullptr;
+        if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+        if (e != hipSuccess || !p) {
+            *err = std::string("static scratch address: ") + hipGetErrorString(e);
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 struct reuse_net {
     Plan p;
     rn_config cfg;
     char *ws = nullptr;
+    int dev = 0;                         // the device current at create
     int cus = 256;
     hipStream_t last_stream = nullptr;
     int last_n = 0;
@@ -865,6 +901,13 @@ rn_status reuse_net_create(const rn_config *cfg, const rn_weights *w, void *dev_
     hipDeviceProp_t prop;
     if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
         net->cus = std::max(1, prop.multiProcessorCount);
+    net->dev = dev;
+    {
+        // Set-up of the static scratch on this device (reuse_net_variants_static);
+        // a failure here is reported by that call, which looks it up again.
+        std::string ignored;
+        (void)static_scratch(dev, &ignored);
+    }
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
 
     // Host-side images of the constant parts.
@@ -907,6 +950,24 @@ rn_status reuse_net_variants(reuse_net *net, int32_t base_stream, int32_t n, con
                              void *scratch, size_t scratch_bytes, float *logits, void *stream) {
     return run_variants(net, base_stream, n, frames, fdt, frame_count, boxes, box_off, max_tiles, scratch,
                         scratch_bytes, logits, stream);
+}
+
+rn_status reuse_net_variants_static(reuse_net *net, int32_t base_stream, int32_t n, const void *frames,
+                                    rn_dtype fdt, int32_t frame_count, const int32_t *boxes, const int32_t *box_off,
+                                    int32_t max_tiles, float *logits, void *stream) {
+    if (!net) return RN_EINVAL;
+    if (const char *why = variants_unsupported(net->p)) return net->fail(RN_EUNSUPPORTED, why);
+    if (n < 1 || n > 65535) return net->fail(RN_EINVAL, "n must be 1..65535");
+    const VarPlan vp = plan_variants(net->p, n, max_tiles);
+    if (vp.total > (size_t)RN_STATIC_SCRATCH_BYTES)
+        return net->fail(RN_ENOSPACE, "variants need " + std::to_string(vp.total) + " bytes of scratch, above the " +
+                                          std::to_string((size_t)RN_STATIC_SCRATCH_BYTES) +
+                                          "-byte static scratch: use fewer variants or a smaller max_tiles");
+    std::string err;
+    void *sc = static_scratch(net->dev, &err);
+    if (!sc) return net->fail(RN_EHIP, err);
+    return run_variants(net, base_stream, n, frames, fdt, frame_count, boxes, box_off, max_tiles, sc,
+                        (size_t)RN_STATIC_SCRATCH_BYTES, logits, stream);
 }
 
 rn_status reuse_net_set_weights(reuse_net *net, const rn_weights *w, void *hip_stream) {
