@@ -225,6 +225,127 @@ class OcclusionDriver:
         return done / el, f"{done} variants (16 per batch) of {wl.h}x{wl.w}"
 
 
+def train_bench(args, torch):
+    """REINFORCE training with activation reuse (Sec. 2: the policy is trained
+    with REINFORCE; the weights stay fixed within an episode).  One episode of
+    T frames for every stream: a rollout of T reuse steps, then a replay of the
+    same frames as reuse steps, each followed by the REINFORCE logit gradient
+    (synthetic seeded actions and discounted returns) and a backward pass
+    accumulating the episode's gradient, then one SGD step on the device (which
+    unprimes every slot).  The dense comparison runs the same loop with
+    reuse_net_full for every forward pass.  Frames/s = streams x T per episode
+    time."""
+    from paper_1909_05632_amd import ReuseNet
+    from synth import frames as synth
+
+    wl = synth.WORKLOADS[args.workload]
+    T, S, F = args.episode, wl.streams, wl.frames
+    preset = {}
+    if args.change_frac is not None:
+        preset = ({"full_change": True} if args.change_frac >= 1.0 else dict(synth.FRACTION_PRESETS[args.change_frac]))
+    u8 = synth.sprite_batch(wl, **preset)
+    frames = torch.from_numpy(synth.to_f32(u8)).cuda().unsqueeze(2).contiguous()
+    weights = synth.net_weights(wl)
+    net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, S, weights, stack=wl.stack, head=args.head,
+                   fuse_first=not args.separate_first)
+    grads = net.new_grads()
+    rng = np.random.default_rng([wl.cid, 7])
+    actions = torch.from_numpy(rng.integers(0, wl.n_out, (T, S)).astype(np.int32)).cuda()
+    rewards = rng.uniform(-1.0, 1.0, (T, S))
+    G = np.zeros_like(rewards)
+    acc = np.zeros(S)
+    for t in range(T - 1, -1, -1):                          # discounted returns, gamma 0.99
+        acc = rewards[t] + 0.99 * acc
+        G[t] = acc
+    returns = torch.from_numpy(G.astype(np.float32)).cuda()
+    out = torch.empty((T, S, wl.n_out), dtype=torch.float32, device="cuda")
+    dl = torch.empty((S, wl.n_out), dtype=torch.float32, device="cuda")
+    lr = 1e-3
+    stream = torch.cuda.current_stream()
+
+    def episode(e, dense):
+        f0 = (e * T) % max(1, F - T)
+        fwd = net.full if dense else net.step
+        for t in range(T):                                  # rollout
+            fwd(frames[f0 + t], out=out[t])
+        for t in range(T):                                  # replay with the episode's returns
+            fwd(frames[f0 + t], out=out[t])
+            net.reinforce_dlogits(out[t], actions[t], returns[t], out=dl)
+            net.backward(dl, grads, accumulate=t > 0)
+        net.sgd_step(grads, lr)
+
+    def timed(dense, episodes, profile=False):
+        for e in range(args.warmup):
+            episode(e, dense)
+        torch.cuda.synchronize()
+        net.set_profiling(profile)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for e in range(episodes):
+            episode(args.warmup + e, dense)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        prof = net.profile() if profile else None
+        net.set_profiling(False)
+        return e0.elapsed_time(e1) / episodes, prof
+
+    K = args.steps
+    ms_ep, _ = timed(False, K)
+    _, prof = timed(False, 1, profile=True)
+    ms_dense, _ = timed(True, max(1, K // 2))
+    fps = S * T / (ms_ep / 1e3)
+    fps_dense = S * T / (ms_dense / 1e3)
+
+    specs = wl.conv_specs()
+    grids = wl.grids()
+    tiles = [-(-gh // 4) * -(-gw // 4) for gh, gw in grids]
+    # algorithmic flops of one backward call over S streams (padded tile pixels included)
+    f_dw = sum(2 * S * tiles[l + 1] * 16 * co * (k * k * ci + 1) for l, (ci, co, k, _s, _p) in enumerate(specs))
+    f_dx = sum(2 * S * tiles[l + 1] * 16 * ci * k * k * co for l, (ci, co, k, _s, _p) in enumerate(specs) if l > 0)
+    kern = {name: {"ms_per_episode": prof[name]["ms"], "launches": prof[name]["launches"]}
+            for name in ("masks", "compact", "conv1", "convN", "head", "bwd_head", "bwd_dw", "bwd_dx", "sgd")}
+    kern["bwd_dw"]["tflops"] = f_dw * T / (prof["bwd_dw"]["ms"] / 1e3) / 1e12
+    if f_dx:
+        kern["bwd_dx"]["tflops"] = f_dx * T / (prof["bwd_dx"]["ms"] / 1e3) / 1e12
+    dom = max(("bwd_dw", "bwd_dx"), key=lambda k: prof[k]["ms"])
+    ach = kern[dom]["tflops"]
+    roof = {"bound": "mfma", "kernel": {"bwd_dw": "k_bwd_dw (weight gradients, split-K MFMA)",
+                                        "bwd_dx": "k_bwd_dx (input gradients, transposed conv on MFMA)"}[dom],
+            "achieved": ach, "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_MFMA_F32_TFLOPS,
+            "traffic": None}
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        onet = oracle.Net(wl.in_c, wl.h, wl.w, specs, wl.n_out)
+        x = synth.to_f32(u8[:T, :2])
+        done, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_budget:
+            t = done % T
+            cur = x[t][:, None] if wl.stack == 1 else np.stack([synth.stacked_view(x[:, i], t) for i in range(2)])
+            z, _ = oracle.forward(onet, *weights, cur)
+            g = oracle.reinforce_dlogits(z, actions[t, :2].cpu().numpy(), returns[t, :2].cpu().numpy())
+            oracle.backward(onet, *weights, cur, g)
+            done += 1
+        el = time.perf_counter() - t0
+        cpu = {"value": 2 * done / el, "unit": "frames/s", "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+               "sample": f"2 streams x {done} frames: full forward, REINFORCE logit gradient and backpropagation "
+                         "in double (one forward pass per frame, no rollout/replay split)"}
+    line = {
+        "metric": "training frames/sec (REINFORCE: reuse rollout + replay with backward + SGD step, all streams)",
+        "value": fps, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_ep, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "streams": S, "episode_frames": T, "h": wl.h, "w": wl.w,
+                   "convs": list(wl.convs), "n_out": wl.n_out, "head": args.head, "lr": lr,
+                   "step": "one episode: T rollout steps, T replay steps with backward, one SGD step"},
+        "dense_path": {"value": fps_dense, "unit": "frames/s", "ms_per_step": ms_dense},
+        "speedup_vs_dense": fps / fps_dense,
+        "kernels": kern, "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+    net.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -247,6 +368,10 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="replay each reuse step from a HIP graph captured once per frame buffer "
                          "(one launch per step instead of one per kernel; the profiled pass stays eager)")
+    ap.add_argument("--train", action="store_true",
+                    help="time REINFORCE training episodes (rollout, replay with backward, SGD step) "
+                         "instead of inference steps; --steps counts episodes")
+    ap.add_argument("--episode", type=int, default=16, help="frames per training episode (--train)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy, 3 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -272,6 +397,12 @@ def main():
     from paper_1909_05632_amd import ReuseNet
     from synth import frames as synth
 
+    if args.train:
+        if args.workload == DEFAULT_WORKLOAD and "--workload" not in sys.argv:
+            args.workload = "atari-ds2-256x64"              # the paper's training net (2 conv + dense)
+        if args.steps == 120 and "--steps" not in sys.argv:
+            args.steps = 4
+        return train_bench(args, torch)
     if args.change_frac is None and args.workload == DEFAULT_WORKLOAD:
         args.change_frac = DEFAULT_CHANGE_FRAC
     wl = synth.WORKLOADS[args.workload]

@@ -177,6 +177,65 @@ rn_status reuse_net_reset(reuse_net *net, int32_t stream_id);
  * hip_stream.  On an argument error nothing changes. */
 rn_status reuse_net_set_weights(reuse_net *net, const rn_weights *w, void *hip_stream);
 
+/* ---- training (Sec. 2: the policy is trained with REINFORCE) ----
+ *
+ * Within a rollout the weights are fixed, so every forward step reuses
+ * activations as in inference; a step's gradient is taken from the
+ * activations the slots' caches hold after it.  A REINFORCE update over an
+ * episode replays its frames through reuse steps and, after each, adds that
+ * step's gradient (reuse_net_backward with accumulate = 1), then applies one
+ * SGD step.  Supported for float32 nets of 3x3 stride-1 pad-1 layers at the
+ * channel pairs of the backward kernels (first layer 1 or 4 -> 20, 40, 64 or
+ * 80 channels; later layers 40->80, 64->128, 128->128); other nets return
+ * RN_EUNSUPPORTED from the calls below.
+ *
+ * Gradient buffer (float32, device, caller-owned): the weights of rn_weights
+ * in that order and layout, conv layer l's OIHW weights [cout][cin][3][3]
+ * then its bias [cout] for l = 1..n_conv, then the dense weights
+ * [n_out][C_L * H_L * W_L] in (c, y, x) order and the dense bias [n_out];
+ * reuse_net_grad_elems floats in all. */
+
+/* Floats of a gradient buffer (0 if the net does not support training). */
+size_t reuse_net_grad_elems(const reuse_net *net);
+
+/* Device scratch bytes reuse_net_backward needs for a batch of n streams
+ * (0 if n is outside 1..max_streams or the net does not support training). */
+size_t reuse_net_backward_scratch_bytes(const reuse_net *net, int32_t n);
+
+/* REINFORCE's logit gradient (Sec. 2): for n streams with logits z [n][n_out],
+ * sampled actions a [n] (0..n_out-1) and returns G [n],
+ *   dlogits[i][o] = G_i (softmax(z_i)[o] - [o == a_i]),
+ * the derivative of -G_i log softmax(z_i)[a_i].  Device pointers, enqueued on
+ * hip_stream; RN_EINVAL for NULL pointers or n_out outside 1..64. */
+rn_status reuse_net_reinforce_dlogits(int32_t n, int32_t n_out, const float *dev_logits,
+                                      const int32_t *dev_actions, const float *dev_returns,
+                                      float *dev_dlogits, void *hip_stream);
+
+/* Gradient of J = sum_i sum_o dlogits[i][o] logits[i][o] with respect to
+ * every weight and bias, for the n streams dev_stream_ids (NULL: 0..n-1) at the
+ * inputs their slots' caches hold (the last step or full call on them; the
+ * ReLU derivative is taken as 0 where an activation is 0).
+ *   dev_dlogits: [n][n_out] float32.
+ *   dev_grads:   reuse_net_grad_elems floats; accumulate = 0 overwrites it,
+ *                accumulate != 0 adds this gradient to it.
+ *   dev_scratch: caller-owned, 256-byte aligned, at least
+ *                reuse_net_backward_scratch_bytes(net, n) bytes.
+ * Deterministic (fixed summation order).  Enqueued on hip_stream; with layer
+ * 1 folded into layer 2 (the default for one-channel frames) it first
+ * recomputes the slots' layer-1 activations into the layer-1 cache. */
+rn_status reuse_net_backward(reuse_net *net, int32_t n, const int32_t *dev_stream_ids,
+                             const float *dev_dlogits, float *dev_grads, int32_t accumulate,
+                             void *dev_scratch, size_t scratch_bytes, void *hip_stream);
+
+/* One SGD step on the device: every weight w becomes fl(w - fl(lr * g)) with g
+ * its entry of dev_grads (layout above), in every packed copy the kernels
+ * read, so the net computes exactly as one created with the updated weights.
+ * Marks every slot unprimed (the caches hold activations of the old weights;
+ * the next step of each slot recomputes everything, and with stacked frames
+ * the frame ring restarts as at an episode start).  Enqueued on hip_stream,
+ * no host synchronisation. */
+rn_status reuse_net_sgd_step(reuse_net *net, const float *dev_grads, float lr, void *hip_stream);
+
 /* ---- variants of one slot: copy-on-write overlays (Sec. 1, known change) ---- */
 
 /* Device scratch bytes reuse_net_variants needs for n variants when no variant
@@ -273,13 +332,17 @@ rn_status reuse_net_get_stats(reuse_net *net, rn_stats *out);
 
 /* ---- kernel timing with HIP events (measurement support) ---- */
 
-#define RN_PHASES 5
+#define RN_PHASES 9
 typedef enum {
     RN_PHASE_MASKS = 0,   /* diff or boxes, dilation, tile masks */
     RN_PHASE_COMPACT = 1, /* work-list compaction */
     RN_PHASE_CONV1 = 2,   /* first conv layer on dirty tiles */
     RN_PHASE_CONVN = 3,   /* conv layers 2..n_conv on dirty tiles (MFMA) */
-    RN_PHASE_HEAD = 4     /* dense head */
+    RN_PHASE_HEAD = 4,    /* dense head */
+    RN_PHASE_BWD_HEAD = 5,/* backward: dense head and the last layer's gradient (and a layer-1 recompute) */
+    RN_PHASE_BWD_DW = 6,  /* backward: weight and bias gradients of the conv layers (MFMA) */
+    RN_PHASE_BWD_DX = 7,  /* backward: gradients at the conv layers' inputs (MFMA) */
+    RN_PHASE_SGD = 8      /* SGD step on the packed weights */
 } rn_phase;
 
 typedef struct {

@@ -17,12 +17,12 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libreuse_net.so")
 
 RN_MAX_CONV = 8
-RN_PHASES = 5
+RN_PHASES = 9
 RN_OK, RN_EINVAL, RN_EUNSUPPORTED, RN_ENOSPACE, RN_EHIP, RN_ESTATE = 0, -1, -2, -3, -4, -5
 RN_F32, RN_BF16, RN_U8 = 0, 1, 2
 RN_HEAD_TILES, RN_HEAD_FULL = 0, 1
 RN_OPT_SEPARATE_FIRST = 1
-PHASES = ("masks", "compact", "conv1", "convN", "head")
+PHASES = ("masks", "compact", "conv1", "convN", "head", "bwd_head", "bwd_dw", "bwd_dx", "sgd")
 STATUS_NAMES = {0: "RN_OK", -1: "RN_EINVAL", -2: "RN_EUNSUPPORTED", -3: "RN_ENOSPACE",
                 -4: "RN_EHIP", -5: "RN_ESTATE"}
 
@@ -33,7 +33,9 @@ EXPORTS = (
     "reuse_net_get_worklist", "reuse_net_read_activation", "reuse_net_get_stats",
     "reuse_net_set_profiling", "reuse_net_get_profile", "reuse_net_last_error",
     "reuse_net_destroy", "reuse_net_variant_scratch_bytes", "reuse_net_variants",
-    "reuse_net_set_weights", "reuse_net_variants_static",
+    "reuse_net_set_weights", "reuse_net_variants_static", "reuse_net_grad_elems",
+    "reuse_net_backward_scratch_bytes", "reuse_net_reinforce_dlogits", "reuse_net_backward",
+    "reuse_net_sgd_step",
 )
 RN_STATIC_SCRATCH_BYTES = 64 << 20
 
@@ -101,6 +103,16 @@ def load_library(path: str = LIB_PATH):
     L.reuse_net_variant_scratch_bytes.argtypes = [P, I32, I32]
     L.reuse_net_variants.restype = st
     L.reuse_net_variants.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, SZ, P, P]
+    L.reuse_net_grad_elems.restype = SZ
+    L.reuse_net_grad_elems.argtypes = [P]
+    L.reuse_net_backward_scratch_bytes.restype = SZ
+    L.reuse_net_backward_scratch_bytes.argtypes = [P, I32]
+    L.reuse_net_reinforce_dlogits.restype = st
+    L.reuse_net_reinforce_dlogits.argtypes = [I32, I32, P, P, P, P, P]
+    L.reuse_net_backward.restype = st
+    L.reuse_net_backward.argtypes = [P, I32, P, P, P, I32, P, SZ, P]
+    L.reuse_net_sgd_step.restype = st
+    L.reuse_net_sgd_step.argtypes = [P, P, ctypes.c_float, P]
     L.reuse_net_variants_static.restype = st
     L.reuse_net_variants_static.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, P]
     for name in ("reuse_net_get_pixel_mask", "reuse_net_get_tile_mask"):
@@ -188,6 +200,30 @@ def reuse_net_variants_static(net: int, base_stream: int, n: int, dev_frames: in
     _check(load_library().reuse_net_variants_static(net, base_stream, n, dev_frames, frame_dtype, frame_count,
                                                     dev_boxes, dev_box_off, max_tiles, dev_logits, hip_stream),
            net)
+
+
+def reuse_net_grad_elems(net: int) -> int:
+    return load_library().reuse_net_grad_elems(net)
+
+
+def reuse_net_backward_scratch_bytes(net: int, n: int) -> int:
+    return load_library().reuse_net_backward_scratch_bytes(net, n)
+
+
+def reuse_net_reinforce_dlogits(n: int, n_out: int, dev_logits: int, dev_actions: int, dev_returns: int,
+                                dev_dlogits: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_reinforce_dlogits(n, n_out, dev_logits, dev_actions, dev_returns,
+                                                      dev_dlogits, hip_stream))
+
+
+def reuse_net_backward(net: int, n: int, dev_stream_ids: int, dev_dlogits: int, dev_grads: int,
+                       accumulate: bool, dev_scratch: int, scratch_bytes: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_backward(net, n, dev_stream_ids, dev_dlogits, dev_grads, int(accumulate),
+                                             dev_scratch, scratch_bytes, hip_stream), net)
+
+
+def reuse_net_sgd_step(net: int, dev_grads: int, lr: float, hip_stream: int) -> None:
+    _check(load_library().reuse_net_sgd_step(net, dev_grads, lr, hip_stream), net)
 
 
 def reuse_net_get_pixel_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
@@ -452,6 +488,72 @@ class ReuseNet:
                                   bx, bo, max_tiles, out.data_ptr(), s)
         self._last_batch = n
         return out
+
+    # -- training
+    def grad_elems(self) -> int:
+        return reuse_net_grad_elems(self.handle)
+
+    def new_grads(self):
+        """A zeroed float32 gradient buffer (layout of reuse_net_backward)."""
+        n = self.grad_elems()
+        if n == 0:
+            _check(load_library().reuse_net_sgd_step(self.handle, None, 0.0, None), self.handle)
+        return self.torch.zeros(n, dtype=self.torch.float32, device=self.device)
+
+    def split_grads(self, grads):
+        """Views of a gradient buffer: (conv_w list OIHW, conv_b list, dense_w, dense_b)."""
+        off, cw, cb = 0, [], []
+        for (ci, co, k, _s, _p) in self.specs:
+            cw.append(grads[off:off + co * ci * k * k].view(co, ci, k, k))
+            off += co * ci * k * k
+            cb.append(grads[off:off + co])
+            off += co
+        gh, gw = self.grids[-1]
+        nd = self.n_out * self.channels[-1] * gh * gw
+        return cw, cb, grads[off:off + nd].view(self.n_out, -1), grads[off + nd:off + nd + self.n_out]
+
+    def reinforce_dlogits(self, logits, actions, returns, out=None, stream=None):
+        """dJ/dlogits of REINFORCE (reuse_net_reinforce_dlogits) for [n][n_out] logits."""
+        t = self.torch
+        n = logits.shape[0] if logits.dim() == 2 else -1
+        self._check_dev(logits, "logits", t.float32, (n, self.n_out))
+        self._check_dev(actions, "actions", t.int32, (n,))
+        self._check_dev(returns, "returns", t.float32, (n,))
+        if out is None:
+            out = t.empty((n, self.n_out), dtype=t.float32, device=self.device)
+        self._check_dev(out, "out", t.float32, (n, self.n_out))
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_reinforce_dlogits(n, self.n_out, logits.data_ptr(), actions.data_ptr(), returns.data_ptr(),
+                                    out.data_ptr(), s)
+        return out
+
+    def backward(self, dlogits, grads, stream_ids=None, accumulate=False, stream=None):
+        """Add (accumulate) or write the gradient of sum(dlogits * logits) for the
+        streams' cached inputs into grads (reuse_net_backward)."""
+        t = self.torch
+        n = dlogits.shape[0] if dlogits.dim() == 2 else -1
+        self._check_dev(dlogits, "dlogits", t.float32, (n, self.n_out))
+        self._check_dev(grads, "grads", t.float32, (self.grad_elems(),))
+        ids = None
+        if stream_ids is not None:
+            ids = self._check_dev(stream_ids, "stream_ids", t.int32, (n,)).data_ptr()
+        need = reuse_net_backward_scratch_bytes(self.handle, n)
+        if need == 0:
+            _check(load_library().reuse_net_backward(self.handle, n, None, None, None, 0, None, 0, None),
+                   self.handle)
+        if getattr(self, "_bwd_scratch", None) is None or self._bwd_scratch.numel() < need:
+            self._bwd_scratch = t.empty(need, dtype=t.uint8, device=self.device)
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_backward(self.handle, n, ids, dlogits.data_ptr(), grads.data_ptr(), accumulate,
+                           self._bwd_scratch.data_ptr(), self._bwd_scratch.numel(), s)
+        return grads
+
+    def sgd_step(self, grads, lr: float, stream=None):
+        """W <- W - lr * grads on the device; every slot recomputes on its next step."""
+        t = self.torch
+        self._check_dev(grads, "grads", t.float32, (self.grad_elems(),))
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_sgd_step(self.handle, grads.data_ptr(), lr, s)
 
     # -- introspection
     def pixel_mask(self, layer: int, stream_id: int) -> np.ndarray:

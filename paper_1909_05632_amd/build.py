@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libreuse_net.so")
-SOURCES = ["rn_host.hip", "rn_masks.hip", "rn_conv.hip", "rn_conv_bf16.hip", "rn_head.hip"]
+SOURCES = ["rn_host.hip", "rn_masks.hip", "rn_conv.hip", "rn_conv_bf16.hip", "rn_head.hip", "rn_train.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",

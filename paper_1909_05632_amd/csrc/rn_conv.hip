@@ -763,7 +763,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
 // buffer at the start of stage q + 1, so each load has a whole stage (4096
 // matrix cycles at 128 outputs and 64 channels) to arrive and the block
 // barrier that ends a stage only orders LDS.  Each wave fetches the halo of
-// its tile of the next group into registers halfway through the group (every
+// its tile of the next group into registers in the group's last stage (every
 // load issued, out-of-image and absent ones from a fixed valid address and
 // dropped when stored) and writes it to its own halo area after its epilogue.
 template <int CIN, int COUT>
@@ -844,27 +844,36 @@ __device__ inline void store_halo_masked(float *halo, const floatx4 *regs, uint3
     }
 }
 
-// acc += the stage's channels (blocks ch * SB .. + SB) at kernel position kpos;
-// s_w holds the stage's weights, [block][nb][lane][4].
+// Operands of block b of a stage: A from the wave's halo (channels of block
+// ch * SB + b at kernel position kpos), B from the stage's weights in LDS,
+// [block][nb][lane][4].
 template <int CIN, int COUT>
-__device__ inline void mfma_stage(floatx4 *acc, const float *halo, const float *s_w, int kpos, int ch, int lane) {
+__device__ inline void stage_block(BlockOps<Mfma<CIN, COUT>::NB> &o, const float *halo, const float *s_w, int kpos,
+                                   int ch, int b, int lane) {
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
     const int mrow = lane & 15, kq = lane >> 4;
     const int pix = (mrow & 3) * 6 + (mrow >> 2);   // column-major pixel rows
     const int ky = kpos / 3, kx = kpos - ky * 3;
-    const int p = pix + ky * 6 + kx;
-    BlockOps<M::NB> cur, nxt;
-    auto load = [&](BlockOps<M::NB> &o, int b) {
-        o.a = *reinterpret_cast<const float4 *>(halo + chunk_off<CIN, COUT>(p, 4 * (ch * S::SB + b) + kq));
-        const float *wb = s_w + (size_t)b * 16 * COUT;
+    o.a = *reinterpret_cast<const float4 *>(halo + chunk_off<CIN, COUT>(pix + ky * 6 + kx, 4 * (ch * S::SB + b) + kq));
+    const float *wb = s_w + (size_t)b * 16 * COUT;
 #pragma unroll
-        for (int nb = 0; nb < M::NB; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + (nb * 64 + lane) * 4);
-    };
-    load(cur, 0);
+    for (int nb = 0; nb < M::NB; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + (nb * 64 + lane) * 4);
+}
+
+// acc += the stage's channels (blocks ch * SB .. + SB) at kernel position
+// kpos; `cur` holds block 0's operands on entry (the caller reads them
+// before its other LDS work of the stage), each later block's are read
+// during the previous block's matrix ops.
+template <int CIN, int COUT>
+__device__ inline void mfma_stage(floatx4 *acc, const float *halo, const float *s_w, int kpos, int ch, int lane,
+                                  BlockOps<Mfma<CIN, COUT>::NB> &cur) {
+    using M = Mfma<CIN, COUT>;
+    using S = Staged<CIN, COUT>;
+    BlockOps<M::NB> nxt;
 #pragma unroll
     for (int b = 0; b < S::SB; ++b) {
-        if (b + 1 < S::SB) load(nxt, b + 1);
+        if (b + 1 < S::SB) stage_block<CIN, COUT>(nxt, halo, s_w, kpos, ch, b + 1, lane);
         __builtin_amdgcn_sched_barrier(0);
         mma_block<CIN, COUT>(acc, cur, 0);
         __builtin_amdgcn_sched_barrier(0);
@@ -911,17 +920,24 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
 #pragma unroll
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int q = 0; q < S::NQ; ++q) {
-            // Stage q + 1 to the free buffer (its last reader finished before the
-            // previous barrier), stage q + 2 (wrapping into the next group) to
-            // registers, the next halo at mid-group, then the matrix work.
+            // The stage's first operands (its weights are visible since the
+            // last barrier), then, while they arrive: stage q + 1 to the free
+            // buffer (its last reader finished before that barrier), stage
+            // q + 2 (wrapping into the next group) to registers and, in the
+            // last stage, the next group's halo; then the matrix work.  The
+            // halo loads are issued last in the group so that no weight wait
+            // of a later stage in this group has to drain them (the waits are
+            // counted in issue order); the epilogue runs before they are used.
+            const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
+            BlockOps<M::NB> first;
+            stage_block<CIN, COUT>(first, halo, wbuf + buf * S::WST, kpos, ch, 0, lane);
             store_wstage<CIN, COUT>(wbuf + (buf ^ 1) * S::WST, wreg, tid);
             fetch_wstage<CIN, COUT>(wg, (q + 2) % S::NQ, wreg, tid);
-            if (q == S::NQ / 2) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
+            if (q == S::NQ - 1) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
             // Unconditional: a wave without a tile has an all-zero halo and
             // skips only the epilogue (a guarded call would make the compiler
             // copy every accumulator between register files each stage).
-            const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-            mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane);
+            mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane, first);
             buf ^= 1;
             lds_barrier();
         }

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "rn_internal.hpp"
+#include "rn_train.hpp"
 
 using namespace rn;
 
@@ -49,6 +50,13 @@ struct Plan {
         o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
     size_t w_bytes[RN_MAX_CONV] = {0};
+    // Training (backward and SGD step): float32 nets of 3x3 stride-1 pad-1
+    // layers at the kernels' shapes; o_wt[l] holds layer l's weights
+    // transposed and flipped for the input-gradient product (l >= 1, i.e.
+    // conv layers 2..L).
+    const char *train_why = nullptr;        // NULL: training supported
+    size_t o_wt[RN_MAX_CONV] = {0};
+    size_t wt_elems[RN_MAX_CONV] = {0};
     size_t act_stride[RN_MAX_CONV + 1] = {0};   // elements per slot
     size_t total = 0;
 };
@@ -199,6 +207,16 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
         p->w_bytes[l] = p->w_elems[l] * ((l > 0 && p->dt == RN_BF16) ? 2 : 4);
         p->o_w[l] = take(p->w_bytes[l]);
         p->o_b[l] = take((size_t)p->C[l + 1] * 4);
+    }
+    if (p->dt != RN_F32) p->train_why = "training needs a float32 net";
+    else if (p->any_gen) p->train_why = "training needs 3x3 stride-1 pad-1 layers";
+    else if (!train_shapes_supported(p->C[0], p->C[1], true)) p->train_why = "no backward kernel for the first layer's channels";
+    for (int l = 1; l < p->L && !p->train_why; ++l)
+        if (!train_shapes_supported(p->C[l], p->C[l + 1], false) || !train_dx_supported(p->C[l + 1], p->C[l]))
+            p->train_why = "no backward kernels for a layer's channel pair";
+    for (int l = 1; l < p->L; ++l) {
+        p->wt_elems[l] = p->train_why ? 0 : dx_weights_elems(p->C[l + 1], p->C[l]);
+        p->o_wt[l] = take(p->wt_elems[l] * 4);
     }
     p->o_wd = take((size_t)p->N * p->K * 4);
     p->o_bd = take((size_t)p->N * 4);
@@ -802,6 +820,12 @@ hipError_t upload_weights(reuse_net *net, const rn_weights *w, hipStream_t s) {
             pack_conv_mfma(w->conv_w[l], p.C[l], p.C[l + 1], p.dt, wpack[l].data());
         }
     }
+    std::vector<std::vector<float>> wtpack(p.L);
+    for (int l = 1; l < p.L; ++l)
+        if (p.wt_elems[l]) {
+            wtpack[l].assign(p.wt_elems[l], 0.f);
+            pack_dx_weights(w->conv_w[l], p.C[l], p.C[l + 1], wtpack[l].data());
+        }
     // Dense weights from (c, y, x) order to the tiled cache order, 0 at padded pixels.
     const int CL = p.C[p.L], HL = p.Hl[p.L], WL = p.Wl[p.L], THL = p.THl[p.L], TWL = p.TWl[p.L];
     std::vector<float> wd((size_t)p.N * p.K, 0.f);
@@ -822,6 +846,7 @@ hipError_t upload_weights(reuse_net *net, const rn_weights *w, hipStream_t s) {
     for (int l = 0; l < p.L; ++l) {
         up(p.o_w[l], wpack[l].data(), p.w_bytes[l]);
         up(p.o_b[l], w->conv_b[l], (size_t)p.C[l + 1] * 4);
+        if (p.wt_elems[l]) up(p.o_wt[l], wtpack[l].data(), p.wt_elems[l] * 4);
     }
     up(p.o_wd, wd.data(), wd.size() * 4);
     std::vector<float> hw;
@@ -854,6 +879,60 @@ rn_status check_weights(const Plan &p, const rn_weights *w, std::string *err) {
             return RN_EINVAL;
         }
     return RN_OK;
+}
+
+
+// Offsets (floats) of each weight's gradient in a gradient buffer: the
+// rn_weights order, conv layer l's OIHW weights then its bias, then the
+// dense weights [n_out][C_L][H_L][W_L] and the dense bias.
+struct GradLayout {
+    size_t w[RN_MAX_CONV], b[RN_MAX_CONV], dw, db, total;
+};
+
+GradLayout grad_layout(const Plan &p) {
+    GradLayout g{};
+    size_t off = 0;
+    for (int l = 0; l < p.L; ++l) {
+        g.w[l] = off;
+        off += (size_t)p.C[l + 1] * p.C[l] * 9;
+        g.b[l] = off;
+        off += (size_t)p.C[l + 1];
+    }
+    g.dw = off;
+    off += (size_t)p.N * p.C[p.L] * p.Hl[p.L] * p.Wl[p.L];
+    g.db = off;
+    off += (size_t)p.N;
+    g.total = off;
+    return g;
+}
+
+// Scratch of a backward call for n streams: two gradient buffers of the
+// largest layer (dJ/dz of layer l and of layer l - 1) and the dW partial sums
+// of the largest layer.
+struct BwdPlan {
+    size_t o_dz0, o_dz1, o_part, total;
+    int teams[RN_MAX_CONV];
+};
+
+BwdPlan plan_backward(const Plan &p, int n, int cus) {
+    BwdPlan b{};
+    size_t dzmax = 0, pmax = 0;
+    for (int l = 0; l < p.L; ++l) {
+        dzmax = std::max(dzmax, (size_t)n * p.act_stride[l + 1]);
+        b.teams[l] = bwd_dw_teams(p.C[l], p.C[l + 1], l == 0, n, p.ntl[l + 1], cus);
+        pmax = std::max(pmax, bwd_dw_part_elems(p.C[l], p.C[l + 1], b.teams[l]));
+    }
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + std::max<size_t>(bytes, 1));
+        return o;
+    };
+    b.o_dz0 = take(dzmax * 4);
+    b.o_dz1 = take(dzmax * 4);
+    b.o_part = take(pmax * 4);
+    b.total = off;
+    return b;
 }
 
 }  // namespace
@@ -982,6 +1061,174 @@ rn_status reuse_net_set_weights(reuse_net *net, const rn_weights *w, void *hip_s
     if (e == hipSuccess) e = hipMemsetAsync(net->at<int32_t>(net->p.o_primed), 0, (size_t)net->p.S * 4, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return net->fail(RN_EHIP, std::string("weight upload: ") + hipGetErrorString(e));
+    net->err.clear();
+    return RN_OK;
+}
+
+/* ---- training ---- */
+
+size_t reuse_net_grad_elems(const reuse_net *net) {
+    if (!net || net->p.train_why) return 0;
+    return grad_layout(net->p).total;
+}
+
+size_t reuse_net_backward_scratch_bytes(const reuse_net *net, int32_t n) {
+    if (!net || net->p.train_why || n < 1 || n > net->p.S) return 0;
+    return plan_backward(net->p, n, net->cus).total;
+}
+
+rn_status reuse_net_reinforce_dlogits(int32_t n, int32_t n_out, const float *logits, const int32_t *actions,
+                                      const float *returns, float *dlogits, void *stream) {
+    if (n < 1 || n_out < 1 || n_out > kHeadMaxOut || !logits || !actions || !returns || !dlogits) return RN_EINVAL;
+    return launch_reinforce(n, n_out, logits, actions, returns, dlogits, static_cast<hipStream_t>(stream)) ==
+                   hipSuccess
+               ? RN_OK
+               : RN_EHIP;
+}
+
+rn_status reuse_net_backward(reuse_net *net, int32_t n, const int32_t *ids_in, const float *dlogits, float *grads,
+                             int32_t accumulate, void *scratch, size_t scratch_bytes, void *stream) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (p.train_why) return net->fail(RN_EUNSUPPORTED, p.train_why);
+    if (n < 1 || n > p.S) return net->fail(RN_EINVAL, "n must be 1..max_streams");
+    if (!dlogits || !grads) return net->fail(RN_EINVAL, "dlogits and grads must not be NULL");
+    if (!scratch) return net->fail(RN_EINVAL, "scratch is NULL");
+    if (reinterpret_cast<uintptr_t>(scratch) % kAlign) return net->fail(RN_EINVAL, "scratch must be 256-byte aligned");
+    const BwdPlan bp = plan_backward(p, n, net->cus);
+    if (scratch_bytes < bp.total)
+        return net->fail(RN_ENOSPACE, "scratch too small: need " + std::to_string(bp.total) + " bytes");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int32_t *ids = ids_in ? ids_in : net->at<int32_t>(p.o_ids);
+    char *sc = static_cast<char *>(scratch);
+    float *dz[2] = {reinterpret_cast<float *>(sc + bp.o_dz0), reinterpret_cast<float *>(sc + bp.o_dz1)};
+    const GradLayout gl = grad_layout(p);
+    hipError_t e = hipSuccess;
+    if (p.fuse_first) {
+        // Layer 1 is computed inside layer 2's kernel and has no cache of its
+        // own: recompute it for these slots (same arithmetic, same bits).
+        ConvArgs cv{};
+        cv.ids = ids;
+        cv.in = net->at<float>(p.o_xin);
+        cv.out = net->at<void>(p.o_act[1]);
+        cv.w = net->at<void>(p.o_w[0]);
+        cv.bias = net->at<float>(p.o_b[0]);
+        cv.ring_head = net->at<int32_t>(p.o_ring);
+        cv.H = cv.Hin = p.H;
+        cv.W = cv.Win = p.W;
+        cv.TH = p.TH;
+        cv.TW = cv.TWin = p.TW;
+        cv.pad = 1;
+        cv.cin = p.C[0];
+        cv.cout = p.C[1];
+        cv.stack = p.stack;
+        cv.in_stride = p.act_stride[0];
+        cv.out_stride = p.act_stride[1];
+        cv.dense_n = n;
+        cv.max_tiles = n * p.ntiles;
+        e = timed(net, RN_PHASE_BWD_HEAD, s, [&] { return launch_conv_first(cv, p.dt, net->cus, s); });
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("layer-1 recompute: ") + hipGetErrorString(e));
+    }
+    const int L = p.L;
+    HeadBwdArgs ha{};
+    ha.n = n;
+    ha.n_out = p.N;
+    ha.C = p.C[L];
+    ha.ntiles = p.ntl[L];
+    ha.TW = p.TWl[L];
+    ha.H = p.Hl[L];
+    ha.W = p.Wl[L];
+    ha.K = p.K;
+    ha.ids = ids;
+    ha.act = net->at<float>(p.o_act[L]);
+    ha.act_stride = p.act_stride[L];
+    ha.wd = net->at<float>(p.o_wd);
+    ha.g = dlogits;
+    ha.dz = dz[0];
+    ha.gwd = grads + gl.dw;
+    ha.gbd = grads + gl.db;
+    ha.accumulate = accumulate != 0;
+    e = timed(net, RN_PHASE_BWD_HEAD, s, [&] { return launch_bwd_head(ha, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head backward: ") + hipGetErrorString(e));
+    int cur = 0;
+    for (int l = L - 1; l >= 0; --l) {                  // conv layer l + 1
+        BwdArgs ba{};
+        ba.n = n;
+        ba.H = p.Hl[l + 1];
+        ba.W = p.Wl[l + 1];
+        ba.TH = p.THl[l + 1];
+        ba.TW = p.TWl[l + 1];
+        ba.ntiles = p.ntl[l + 1];
+        ba.ca = p.C[l];
+        ba.cz = p.C[l + 1];
+        ba.ids = ids;
+        ba.dz_in = dz[cur];
+        ba.first = l == 0;
+        ba.act_prev = l == 0 ? net->at<float>(p.o_xin) : net->at<float>(p.o_act[l]);
+        ba.prev_stride = p.act_stride[l];
+        ba.stack = p.stack;
+        ba.cin0 = p.in_c;
+        ba.ring_head = net->at<int32_t>(p.o_ring);
+        ba.dz_out = dz[cur ^ 1];
+        ba.wt = l > 0 ? net->at<float>(p.o_wt[l]) : nullptr;
+        ba.part = reinterpret_cast<float *>(sc + bp.o_part);
+        ba.teams = bp.teams[l];
+        ba.gw = grads + gl.w[l];
+        ba.gb = grads + gl.b[l];
+        ba.accumulate = accumulate != 0;
+        e = timed(net, RN_PHASE_BWD_DW, s, [&] { return launch_bwd_dw(ba, net->cus, s); });
+        if (e != hipSuccess) return net->fail(RN_EHIP, std::string("weight gradient: ") + hipGetErrorString(e));
+        if (l > 0) {
+            e = timed(net, RN_PHASE_BWD_DX, s, [&] { return launch_bwd_dx(ba, s); });
+            if (e != hipSuccess) return net->fail(RN_EHIP, std::string("input gradient: ") + hipGetErrorString(e));
+            cur ^= 1;
+        }
+    }
+    net->last_stream = s;
+    net->has_step = true;
+    net->err.clear();
+    return RN_OK;
+}
+
+rn_status reuse_net_sgd_step(reuse_net *net, const float *grads, float lr, void *stream) {
+    if (!net) return RN_EINVAL;
+    const Plan &p = net->p;
+    if (p.train_why) return net->fail(RN_EUNSUPPORTED, p.train_why);
+    if (!grads) return net->fail(RN_EINVAL, "grads are NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const GradLayout gl = grad_layout(p);
+    hipError_t e = hipSuccess;
+    auto upd = [&](size_t off, size_t count, int kind, const float *g, int cin, int cout) {
+        if (e != hipSuccess || count == 0) return;
+        SgdArgs a{};
+        a.dst = net->at<float>(off);
+        a.count = count;
+        a.kind = kind;
+        a.g = g;
+        a.lr = lr;
+        a.cin = cin;
+        a.cout = cout;
+        a.C = p.C[p.L];
+        a.H = p.Hl[p.L];
+        a.W = p.Wl[p.L];
+        a.TW = p.TWl[p.L];
+        a.ntiles = p.ntl[p.L];
+        a.K = p.K;
+        e = timed(net, RN_PHASE_SGD, s, [&] { return launch_sgd(a, s); });
+    };
+    for (int l = 0; l < p.L; ++l) {
+        upd(p.o_w[l], p.w_elems[l], l == 0 ? SGD_FIRST : SGD_MFMA, grads + gl.w[l], p.C[l], p.C[l + 1]);
+        upd(p.o_b[l], p.C[l + 1], SGD_PLAIN, grads + gl.b[l], 0, 0);
+        if (l > 0) upd(p.o_wt[l], p.wt_elems[l], SGD_DX, grads + gl.w[l], p.C[l], p.C[l + 1]);
+    }
+    upd(p.o_wd, (size_t)p.N * p.K, SGD_DENSE, grads + gl.dw, 0, 0);
+    if (p.head_mode == RN_HEAD_TILES) upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, grads + gl.dw, 0, 0);
+    upd(p.o_bd, p.N, SGD_PLAIN, grads + gl.db, 0, 0);
+    // Every cache now holds activations of the old weights: all slots unprimed.
+    if (e == hipSuccess) e = timed(net, RN_PHASE_SGD, s, [&] { return launch_unprime(net->at<int32_t>(p.o_primed), p.S, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("sgd step: ") + hipGetErrorString(e));
+    net->last_stream = s;
+    net->has_step = true;
     net->err.clear();
     return RN_OK;
 }

@@ -1,0 +1,575 @@
+// Training kernels (Sec. 2: the policy is trained with REINFORCE; within a
+// rollout the weights are fixed, so the forward steps reuse activations as in
+// inference, and the gradient of a step is taken from the activations the
+// caches then hold).
+//
+// For a batch of streams and given dJ/dlogits g, backpropagation through
+// logits = Wd a_L + bd and a_l = ReLU(conv(a_{l-1}, W_l) + b_l):
+//   head:   dWd (+)= sum_i g_i a_L,i^T,  dbd (+)= sum_i g_i,
+//           dz_L = (Wd^T g_i) where a_L > 0 (the ReLU derivative, 0 at the kink);
+//   layer l: dW_l (+)= sum over pixels of dz_l x im2col(a_{l-1}), db_l (+)= sum dz_l,
+//           dz_{l-1} = (transposed conv of dz_l with W_l) where a_{l-1} > 0.
+// Both conv products run on the float32 matrix cores (v_mfma_f32_16x16x4_f32):
+//   dx: per 4x4 tile of layer l-1 an implicit GEMM, M = 16 pixels, N = C_{l-1},
+//       K = 9 C_l, i.e. a forward 3x3 conv of dz_l with the weights transposed
+//       (input <-> output channels) and flipped (kernel position 8 - k);
+//   dW: M = C_l, N = 9 C_{l-1} + 1 (the last column, all ones, gives the bias
+//       gradient), K = every pixel of every stream, split over teams of blocks
+//       whose partial sums are added in team order (no atomics, so the result
+//       is deterministic).
+// The SGD step updates every packed copy of a weight in place.
+#include "rn_device.hpp"
+#include "rn_train.hpp"
+
+namespace rn {
+namespace {
+
+using dev::floatx4;
+
+// ------------------------------------------------------------------ REINFORCE
+
+// g[i][o] = G_i (softmax(z_i)[o] - [o == a_i]): the derivative of
+// -G_i log softmax(z_i)[a_i] with respect to z_i (one thread per stream).
+__global__ __launch_bounds__(256) void k_reinforce(int n, int n_out, const float *z, const int32_t *act,
+                                                   const float *ret, float *g) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float *zi = z + (size_t)i * n_out;
+    float m = zi[0];
+    for (int o = 1; o < n_out; ++o) m = fmaxf(m, zi[o]);
+    float den = 0.f;
+    for (int o = 0; o < n_out; ++o) den += expf(zi[o] - m);
+    const float G = ret[i];
+    const int a = act[i];
+    for (int o = 0; o < n_out; ++o) {
+        const float p = expf(zi[o] - m) / den;
+        g[(size_t)i * n_out + o] = G * (p - (o == a ? 1.f : 0.f));
+    }
+}
+
+// ------------------------------------------------------------------ dense head
+
+// One block per tile position t of the last layer; a thread owns one of the
+// tile's 16 C head inputs j at a time, keeps its NO weights and NO gradient
+// sums in registers and walks the streams (their g rows staged in LDS).
+template <int NO>
+__global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
+    constexpr int kHeadStreams = NO <= 32 ? 256 : 128;    // streams per LDS stage of g (32 KB at most)
+    __shared__ float s_g[kHeadStreams * NO];
+    __shared__ int32_t s_slot[kHeadStreams];
+    const int t = blockIdx.x;
+    const int E = kTilePx * a.C;
+    const int ty = t / a.TW, tx = t - ty * a.TW;
+    for (int e0 = 0; e0 < E; e0 += blockDim.x) {
+        const int j = e0 + threadIdx.x;
+        const bool ok = j < E;
+        float w[NO], acc[NO];
+#pragma unroll
+        for (int o = 0; o < NO; ++o) {
+            w[o] = ok && o < a.n_out ? a.wd[(size_t)o * a.K + (size_t)t * E + j] : 0.f;
+            acc[o] = 0.f;
+        }
+        for (int i0 = 0; i0 < a.n; i0 += kHeadStreams) {
+            const int nc = min(kHeadStreams, a.n - i0);
+            __syncthreads();                      // the previous stage's readers are done
+            for (int k = threadIdx.x; k < nc * NO; k += blockDim.x) {
+                const int ii = k / NO, o = k - ii * NO;
+                s_g[k] = o < a.n_out ? a.g[(size_t)(i0 + ii) * a.n_out + o] : 0.f;
+            }
+            for (int k = threadIdx.x; k < nc; k += blockDim.x) s_slot[k] = a.ids[i0 + k];
+            __syncthreads();
+            if (ok) {
+#pragma unroll 4
+                for (int ii = 0; ii < nc; ++ii) {
+                    const float v = a.act[(size_t)s_slot[ii] * a.act_stride + (size_t)t * E + j];
+                    float da = 0.f;
+#pragma unroll
+                    for (int o = 0; o < NO; ++o) {
+                        const float gv = s_g[ii * NO + o];
+                        da = fmaf(w[o], gv, da);
+                        acc[o] = fmaf(gv, v, acc[o]);
+                    }
+                    a.dz[((size_t)(i0 + ii) * a.ntiles + t) * E + j] = v > 0.f ? da : 0.f;
+                }
+            }
+        }
+        if (ok) {
+            const int m = j / a.C, c = j - m * a.C;
+            const int y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
+            if (y < a.H && x < a.W) {
+#pragma unroll
+                for (int o = 0; o < NO; ++o) {
+                    if (o >= a.n_out) break;
+                    float *d = a.gwd + (size_t)o * a.C * a.H * a.W + ((size_t)c * a.H + y) * a.W + x;
+                    *d = a.accumulate ? *d + acc[o] : acc[o];
+                }
+            }
+        }
+    }
+    if (t == 0 && (int)threadIdx.x < a.n_out) {
+        float s = 0.f;
+        for (int i = 0; i < a.n; ++i) s += a.g[(size_t)i * a.n_out + threadIdx.x];
+        a.gbd[threadIdx.x] = a.accumulate ? a.gbd[threadIdx.x] + s : s;
+    }
+}
+
+// ------------------------------------------------------------------ dx
+
+// Offset (floats) of 16-byte channel chunk c4 of halo pixel p (6x6 halo,
+// pixel stride CZ): the chunk index XOR-ed with a function of the pixel, so
+// the 16 pixels one 16-lane group reads at a kernel position fall in distinct
+// bank groups (the scheme of the forward MFMA kernels).
+template <int CZ>
+__device__ inline int hoff(int p, int c4) {
+    constexpr int C4 = CZ / 4;
+    static_assert(C4 == 10 || C4 == 20 || C4 == 16 || C4 == 32, "halo swizzle defined for 40, 64, 80, 128 channels");
+    const int hy = p / 6, hx = p - 6 * hy;
+    const int g = C4 == 10 ? (hy & 1) : C4 == 20 ? (hy & 3) : (hy & 3) | ((hx & 3) << 2);
+    return p * CZ + 4 * (c4 ^ g);
+}
+
+template <int CZ, int CA>
+struct Dx {
+    static constexpr int NB = (CA + 15) / 16;   // 16-column output blocks (CA padded with zero weights)
+    static constexpr int KB = 9 * CZ / 16;      // 16-deep K blocks: kernel position (CZ / 16 blocks each)
+    static constexpr int HALO = 36 * CZ;        // floats of one wave's halo
+    static constexpr size_t lds_bytes = (size_t)4 * HALO * sizeof(float);
+    static_assert(CZ % 16 == 0, "whole 16-channel K blocks per kernel position");
+};
+
+// One wave per 4x4 tile of layer l-1 (tile id = 4 block + wave over the
+// batch's tiles); the wave stages the 6x6 x CZ halo of dz_l in its own LDS
+// area, walks K with the operands of the next block loaded during the
+// current block's matrix ops, and writes dz_{l-1} = acc where a_{l-1} > 0.
+// Operand layout of v_mfma_f32_16x16x4_f32 as in the forward kernels: A row
+// m = tile pixel (m % 4, m / 4), lane group kq takes K = 16 b + 4 kq + j;
+// D lane (n, kq) holds pixels (i, kq), i = 0..3, of output channel 16 nb + n.
+template <int CZ, int CA>
+__global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
+    using D = Dx<CZ, CA>;
+    extern __shared__ float smem[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const long long tid = (long long)blockIdx.x * 4 + wave;
+    if (tid >= (long long)a.n * a.ntiles) return;                 // wave-uniform; no block barriers below
+    const int i = (int)(tid / a.ntiles), t = (int)(tid - (long long)i * a.ntiles);
+    const int ty = t / a.TW, tx = t - ty * a.TW;
+    float *halo = smem + wave * D::HALO;
+    const float *src = a.dz_in + (size_t)i * a.ntiles * kTilePx * CZ;
+    constexpr int C4 = CZ / 4;
+    for (int h = lane; h < 36 * C4; h += 64) {
+        const int pos = h / C4, c4 = h - pos * C4;
+        const int hy = pos / 6, hx = pos - hy * 6;
+        const int y = ty * kTile - 1 + hy, x = tx * kTile - 1 + hx;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+            v = *reinterpret_cast<const float4 *>(
+                src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CZ + 4 * c4);
+        *reinterpret_cast<float4 *>(halo + hoff<CZ>(pos, c4)) = v;
+    }
+    dev::wave_sync();
+    const int mrow = lane & 15, kq = lane >> 4;
+    const int pix = (mrow & 3) * 6 + (mrow >> 2);
+    const floatx4 *wt = reinterpret_cast<const floatx4 *>(a.wt);
+    floatx4 acc[D::NB];
+#pragma unroll
+    for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    floatx4 bcur[D::NB], bnxt[D::NB];
+#pragma unroll
+    for (int nb = 0; nb < D::NB; ++nb) bcur[nb] = wt[nb * 64 + lane];
+    for (int b = 0; b < D::KB; ++b) {
+        if (b + 1 < D::KB) {
+#pragma unroll
+            for (int nb = 0; nb < D::NB; ++nb) bnxt[nb] = wt[((b + 1) * D::NB + nb) * 64 + lane];
+        }
+        const int K0 = 16 * b, kpos = K0 / CZ, c16 = (K0 - kpos * CZ) >> 4;
+        const int ky = kpos / 3, kx = kpos - ky * 3;
+        const float4 av = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * c16 + kq));
+        const float al[4] = {av.x, av.y, av.z, av.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int nb = 0; nb < D::NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], bcur[nb][j], acc[nb], 0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < D::NB; ++nb) bcur[nb] = bnxt[nb];
+    }
+    const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + (size_t)t * kTilePx * CA;
+    float *dst = a.dz_out + ((size_t)i * a.ntiles + t) * kTilePx * CA;
+#pragma unroll
+    for (int nb = 0; nb < D::NB; ++nb) {
+        const int c = nb * 16 + mrow;
+        if (c >= CA) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = r * 4 + kq;                          // pixel (row r, column kq)
+            dst[m * CA + c] = ap[m * CA + c] > 0.f ? acc[nb][r] : 0.f;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ dW
+
+// Row stride (floats) that puts the four lane groups of a 32-bit LDS read of
+// consecutive rows in distinct bank groups: stride % 64 in {16, 48}.
+constexpr int bank_stride(int c) {
+    int s = c;
+    while (s % 64 != 16 && s % 64 != 48) ++s;
+    return s;
+}
+
+template <int CA, int CZ, bool FIRST>
+struct Dw {
+    static constexpr int NQ = 9 * CA + 1;                 // columns: (kernel position, input channel), bias
+    static constexpr int NBQ = (NQ + 15) / 16;            // 16-column blocks
+    static constexpr int NCH = (NBQ + 23) / 24;           // column chunks (at most 24 blocks per wave)
+    static constexpr int QW = (NBQ + NCH - 1) / NCH;      // column blocks per wave
+    static constexpr int MB = (CZ + 15) / 16;             // 16-row blocks (output channels)
+    static constexpr int U = MB * NCH;                    // waves per team
+    static constexpr int BPT = (U + 3) / 4;               // blocks per team
+    static constexpr int SZ = bank_stride(CZ);            // dz tile row stride in LDS
+    static constexpr int SA = FIRST ? CA : bank_stride(CA);   // halo pixel stride in LDS
+};
+
+// Block = 4 waves of one team; wave w of block b of the team owns row block
+// mb and QW column blocks (unit 4 b + w) and accumulates them over the team's
+// share of the batch's tiles.  Per tile the block stages dz_l's tile and
+// a_{l-1}'s 6x6 halo in LDS; per 4-pixel k-step a lane reads one A value
+// (dz at pixel 4 s + kq, channel 16 mb + n) and one B value per column block
+// (a_{l-1} at that pixel shifted by the column's kernel position, or 1 for
+// the bias column).  D lane (n, kq) holds rows 4 kq + r (output channels) of
+// column n.
+template <int CA, int CZ, bool FIRST>
+__global__ __launch_bounds__(256) void k_bwd_dw(BwdArgs a) {
+    using D = Dw<CA, CZ, FIRST>;
+    __shared__ float s_dz[16 * D::SZ];
+    __shared__ float s_h[36 * D::SA];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int team = blockIdx.x / D::BPT, u = (blockIdx.x - team * D::BPT) * 4 + wave;
+    const bool active = u < D::U;
+    const int mb = active ? u / D::NCH : 0, qb0 = active ? (u - mb * D::NCH) * D::QW : 0;
+    const int kq = lane >> 4, col = lane & 15;
+    for (int e = threadIdx.x; e < 16 * D::SZ; e += blockDim.x) s_dz[e] = 0.f;   // row padding stays 0
+    // This lane's B offset per column block: (kernel position, channel) ->
+    // halo offset relative to the pixel's own position; -1 bias, -2 zero.
+    int boff[D::QW];
+#pragma unroll
+    for (int k = 0; k < D::QW; ++k) {
+        const int q = (qb0 + k) * 16 + col;
+        if (q < 9 * CA) {
+            const int kpos = q / CA, ci = q - kpos * CA;
+            boff[k] = ((kpos / 3) * 6 + kpos % 3) * D::SA + ci;
+        } else {
+            boff[k] = q == 9 * CA ? -1 : -2;
+        }
+    }
+    floatx4 acc[D::QW];
+#pragma unroll
+    for (int k = 0; k < D::QW; ++k) acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const long long NT = (long long)a.n * a.ntiles;
+    const long long t0 = NT * team / a.teams, t1 = NT * (team + 1) / a.teams;
+    const size_t HW = (size_t)a.H * a.W;
+    for (long long tt = t0; tt < t1; ++tt) {
+        const int i = (int)(tt / a.ntiles), t = (int)(tt - (long long)i * a.ntiles);
+        const int ty = t / a.TW, tx = t - ty * a.TW;
+        const int slot = a.ids[i];
+        __syncthreads();                                   // the previous tile's LDS readers are done
+        const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
+        for (int e = threadIdx.x; e < 4 * CZ; e += blockDim.x) {   // 16 pixels x CZ / 4 chunks
+            const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);
+            *reinterpret_cast<float4 *>(s_dz + m * D::SZ + 4 * c4) = dzp[e];
+        }
+        if constexpr (FIRST) {
+            // 6x6 x CA input halo from the float32 input planes (a ring of four
+            // frames, oldest first as channels, when stacking).
+            const int head = a.stack != 1 ? a.ring_head[slot] : 0;
+            for (int e = threadIdx.x; e < 36 * CA; e += blockDim.x) {
+                const int c = e / 36, pos = e - c * 36;
+                const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
+                float v = 0.f;
+                if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
+                    const float *plane;
+                    if (a.stack == 1) {
+                        plane = a.act_prev + ((size_t)slot * CA + c) * HW;
+                    } else {
+                        const int j = c / a.cin0, c1 = c - j * a.cin0;
+                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
+                        plane = a.act_prev + (((size_t)slot * 4 + rp) * a.cin0 + c1) * HW;
+                    }
+                    v = plane[(size_t)y * a.W + x];
+                }
+                s_h[pos * D::SA + c] = v;
+            }
+        } else {
+            const float *ap = a.act_prev + (size_t)slot * a.prev_stride;
+            for (int e = threadIdx.x; e < 9 * CA; e += blockDim.x) {   // 36 pixels x CA / 4 chunks
+                const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+                const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
+                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+                    v = *reinterpret_cast<const float4 *>(
+                        ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
+                *reinterpret_cast<float4 *>(s_h + pos * D::SA + 4 * c4) = v;
+            }
+        }
+        __syncthreads();
+        if (active) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const float av = s_dz[(4 * s + kq) * D::SZ + mb * 16 + col];
+                const int hb = (s * 6 + kq) * D::SA;        // pixel (row s, column kq)
+#pragma unroll
+                for (int k = 0; k < D::QW; ++k) {
+                    const float bv = boff[k] >= 0 ? s_h[hb + boff[k]] : (boff[k] == -1 ? 1.f : 0.f);
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[k], 0, 0, 0);
+                }
+            }
+        }
+    }
+    if (!active) return;
+#pragma unroll
+    for (int k = 0; k < D::QW; ++k) {
+        const int q = (qb0 + k) * 16 + col;
+        if (q >= D::NQ) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = mb * 16 + 4 * kq + r;
+            if (co < CZ) a.part[((size_t)team * CZ + co) * D::NQ + q] = acc[k][r];
+        }
+    }
+}
+
+// dW_l and db_l from the teams' partial sums, added in team order.
+__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a) {
+    const int NQ = 9 * a.ca + 1;
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= a.cz * NQ) return;
+    const int co = e / NQ, q = e - co * NQ;
+    float s = 0.f;
+    for (int team = 0; team < a.teams; ++team) s += a.part[((size_t)team * a.cz + co) * NQ + q];
+    float *d;
+    if (q < 9 * a.ca) {
+        const int kpos = q / a.ca, ci = q - kpos * a.ca;
+        d = a.gw + ((size_t)co * a.ca + ci) * 9 + kpos;
+    } else {
+        d = a.gb + co;
+    }
+    *d = a.accumulate ? *d + s : s;
+}
+
+// ------------------------------------------------------------------ SGD
+
+// Natural-layout index of packed element d (or -1 for a padding zero).
+__device__ inline long long sgd_src(const SgdArgs &a, size_t d) {
+    switch (a.kind) {
+    case SGD_FIRST: {                                         // [ci * 9 + k][co]
+        const int co = (int)(d % a.cout);
+        const size_t r = d / a.cout;
+        const int ci = (int)(r / 9), k = (int)(r % 9);
+        return ((long long)co * a.cin + ci) * 9 + k;
+    }
+    case SGD_MFMA: {                                          // [kpos][block][nb][lane][j]
+        const size_t per = (size_t)a.cin * a.cout;
+        const int kpos = (int)(d / per);
+        size_t r = d - (size_t)kpos * per;
+        const int nf = a.cin / 16;
+        const size_t full = (size_t)nf * 16 * a.cout;
+        int ci, n;
+        if (r < full) {
+            const int b = (int)(r / (16 * a.cout));
+            const int rb = (int)(r - (size_t)b * 16 * a.cout);
+            const int nb = rb / 256, l = (rb / 4) % 64, j = rb % 4;
+            ci = 16 * b + 4 * (l / 16) + j;
+            n = nb * 16 + l % 16;
+        } else {
+            const int rt = (int)(r - full);
+            const int nb = rt / 128, l = (rt / 2) % 64, j = rt % 2;
+            ci = 16 * nf + 2 * (l / 16) + j;
+            n = nb * 16 + l % 16;
+        }
+        return ((long long)n * a.cin + ci) * 9 + kpos;
+    }
+    case SGD_DENSE: {                                         // [o][tile][16][C], 0 outside the image
+        const int o = (int)(d / a.K);
+        const size_t e = d - (size_t)o * a.K;
+        const int c = (int)(e % a.C), m = (int)((e / a.C) % kTilePx), tile = (int)(e / ((size_t)kTilePx * a.C));
+        const int ty = tile / a.TW, tx = tile - ty * a.TW;
+        const int y = ty * kTile + m / 4, x = tx * kTile + m % 4;
+        if (y >= a.H || x >= a.W) return -1;
+        return (long long)o * a.C * a.H * a.W + ((long long)c * a.H + y) * a.W + x;
+    }
+    case SGD_TILE_HEAD: {                                     // [o][tile][nb][lane][i]
+        const int NB = a.C / 16;
+        const int i = (int)(d % 4), l = (int)((d / 4) % 64), nb = (int)((d / 256) % NB);
+        const size_t r = d / (256 * (size_t)NB);
+        const int tile = (int)(r % a.ntiles), o = (int)(r / a.ntiles);
+        const int ty = tile / a.TW, tx = tile - ty * a.TW;
+        const int c = nb * 16 + l % 16, y = ty * kTile + i, x = tx * kTile + l / 16;
+        if (y >= a.H || x >= a.W) return -1;
+        return (long long)o * a.C * a.H * a.W + ((long long)c * a.H + y) * a.W + x;
+    }
+    case SGD_DX: {                                            // [b][nb][lane][j], cin = ca, cout = cz
+        const int NB = (a.cin + 15) / 16;
+        const int j = (int)(d % 4), l = (int)((d / 4) % 64), nb = (int)((d / 256) % NB);
+        const int b = (int)(d / (256 * (size_t)NB));
+        const int K = 16 * b + 4 * (l / 16) + j, n = nb * 16 + l % 16;
+        if (n >= a.cin) return -1;
+        const int kpos = K / a.cout, co = K - kpos * a.cout;
+        return ((long long)co * a.cin + n) * 9 + (8 - kpos);
+    }
+    default:
+        return (long long)d;
+    }
+}
+
+// Two roundings, fl(w - fl(lr g)), as a host computing the same update in
+// float32 does: contraction into one fused multiply-add is switched off.
+__global__ __launch_bounds__(256) void k_sgd(SgdArgs a) {
+#pragma clang fp contract(off)
+    for (size_t d = (size_t)blockIdx.x * blockDim.x + threadIdx.x; d < a.count; d += (size_t)gridDim.x * blockDim.x) {
+        const long long s = sgd_src(a, d);
+        if (s >= 0) {
+            const float step = a.lr * a.g[s];
+            a.dst[d] = a.dst[d] - step;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_unprime(int32_t *primed, int S) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < S) primed[i] = 0;
+}
+
+// ------------------------------------------------------------------ launchers
+
+#define RN_DW_FIRST_SHAPES(X) X(1, 20) X(1, 40) X(1, 64) X(1, 80) X(4, 20) X(4, 40) X(4, 64) X(4, 80)
+#define RN_DW_SHAPES(X) X(40, 80) X(64, 128) X(128, 128)
+#define RN_DX_SHAPES(X) X(80, 40) X(128, 64) X(128, 128)
+
+template <int CA, int CZ, bool FIRST>
+int dw_bpt() {
+    return Dw<CA, CZ, FIRST>::BPT;
+}
+
+int dw_blocks_per_team(int ca, int cz, bool first) {
+#define X(a_, z_) \
+    if (first && ca == a_ && cz == z_) return dw_bpt<a_, z_, true>();
+    RN_DW_FIRST_SHAPES(X)
+#undef X
+#define X(a_, z_) \
+    if (!first && ca == a_ && cz == z_) return dw_bpt<a_, z_, false>();
+    RN_DW_SHAPES(X)
+#undef X
+    return 0;
+}
+
+template <int CA, int CZ, bool FIRST>
+hipError_t run_dw(const BwdArgs &a, hipStream_t s) {
+    using D = Dw<CA, CZ, FIRST>;
+    hipLaunchKernelGGL((k_bwd_dw<CA, CZ, FIRST>), dim3(D::BPT * a.teams), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int total = CZ * D::NQ;
+    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 255) / 256), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int CZ, int CA>
+hipError_t run_dx(const BwdArgs &a, hipStream_t s) {
+    using D = Dx<CZ, CA>;
+    auto kern = k_bwd_dx<CZ, CA>;
+    static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
+    if (attr != hipSuccess) return attr;
+    const long long tiles = (long long)a.n * a.ntiles;
+    hipLaunchKernelGGL(kern, dim3((unsigned)((tiles + 3) / 4)), dim3(256), D::lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool train_shapes_supported(int ca, int cz, bool first) { return dw_blocks_per_team(ca, cz, first) > 0; }
+
+bool train_dx_supported(int cz, int ca) {
+#define X(z_, a_) \
+    if (cz == z_ && ca == a_) return true;
+    RN_DX_SHAPES(X)
+#undef X
+    return false;
+}
+
+size_t dx_weights_elems(int cz, int ca) { return (size_t)9 * cz * ((ca + 15) / 16) * 16; }
+
+void pack_dx_weights(const float *oihw, int ca, int cz, float *dst) {
+    // [b][nb][lane][j]: K = 16 b + 4 (lane / 16) + j is (kernel position
+    // K / cz, channel K % cz of layer l), column n = 16 nb + lane % 16 is
+    // channel n of layer l-1; the value is W_l[K % cz][n] at the flipped
+    // position 8 - K / cz, 0 for padding columns.
+    const int NB = (ca + 15) / 16, KB = 9 * cz / 16;
+    size_t d = 0;
+    for (int b = 0; b < KB; ++b)
+        for (int nb = 0; nb < NB; ++nb)
+            for (int l = 0; l < 64; ++l)
+                for (int j = 0; j < 4; ++j) {
+                    const int K = 16 * b + 4 * (l / 16) + j, n = nb * 16 + l % 16;
+                    const int kpos = K / cz, co = K % cz;
+                    dst[d++] = n < ca ? oihw[((size_t)co * ca + n) * 9 + (8 - kpos)] : 0.f;
+                }
+}
+
+int bwd_dw_teams(int ca, int cz, bool first, int n, int ntiles, int cus) {
+    const int bpt = std::max(1, dw_blocks_per_team(ca, cz, first));
+    const long long tiles = (long long)n * ntiles;
+    const long long want = (3LL * cus + bpt - 1) / bpt;      // about three blocks per CU
+    return (int)std::max(1LL, std::min(want, (tiles + 7) / 8));
+}
+
+size_t bwd_dw_part_elems(int ca, int cz, int teams) { return (size_t)teams * cz * (9 * ca + 1); }
+
+hipError_t launch_reinforce(int n, int n_out, const float *logits, const int32_t *actions, const float *returns,
+                            float *g, hipStream_t s) {
+    hipLaunchKernelGGL(k_reinforce, dim3((n + 255) / 256), dim3(256), 0, s, n, n_out, logits, actions, returns, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_head(const HeadBwdArgs &a, hipStream_t s) {
+    const dim3 grid(a.ntiles), block(256);
+    if (a.n_out <= 8) hipLaunchKernelGGL(k_bwd_head<8>, grid, block, 0, s, a);
+    else if (a.n_out <= 32) hipLaunchKernelGGL(k_bwd_head<32>, grid, block, 0, s, a);
+    else hipLaunchKernelGGL(k_bwd_head<64>, grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dw(const BwdArgs &a, int cus, hipStream_t s) {
+    (void)cus;
+    const bool first = a.first != 0;
+#define X(a_, z_) \
+    if (first && a.ca == a_ && a.cz == z_) return run_dw<a_, z_, true>(a, s);
+    RN_DW_FIRST_SHAPES(X)
+#undef X
+#define X(a_, z_) \
+    if (!first && a.ca == a_ && a.cz == z_) return run_dw<a_, z_, false>(a, s);
+    RN_DW_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_bwd_dx(const BwdArgs &a, hipStream_t s) {
+#define X(z_, a_) \
+    if (a.cz == z_ && a.ca == a_) return run_dx<z_, a_>(a, s);
+    RN_DX_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_sgd(const SgdArgs &a, hipStream_t s) {
+    if (a.count == 0) return hipSuccess;
+    const size_t blocks = std::min<size_t>((a.count + 255) / 256, 65536);
+    hipLaunchKernelGGL(k_sgd, dim3((unsigned)blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_unprime(int32_t *primed, int S, hipStream_t s) {
+    hipLaunchKernelGGL(k_unprime, dim3((S + 255) / 256), dim3(256), 0, s, primed, S);
+    return hipGetLastError();
+}
+
+}  // namespace rn

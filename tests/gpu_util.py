@@ -66,3 +66,42 @@ def check_values(net, onet, weights, x, slots, sample, logits, atol=ATOL_F32, la
 def sprite_inputs(wl, streams, frames, **override):
     u8 = synth.sprite_batch(wl, streams=streams, frames=frames, **override)
     return u8, synth.to_f32(u8)
+
+
+def condition_biases(onet, weights, xs, rel=2.0 ** -17, tries=400):
+    """Seeded test weights whose ReLU decisions are well separated from the kink.
+
+    Backward parity compares gradients whose ReLU derivative (0 or 1) is
+    decided by each activation's sign; where a pre-activation lies within the
+    float32 evaluation error of 0, both derivatives are correct and two
+    implementations may legitimately differ.  The error of a float32 sum of
+    terms t_k scales with S = sum |t_k| (about sqrt(K) ulps of S for K terms,
+    far below 2^-17 S here), so this shifts each conv channel's bias, layer by
+    layer, by the smallest of a fixed sequence of steps that leaves every
+    pre-activation of the inputs xs [n][C][H][W] at |z| >= 2 delta_l, delta_l
+    = rel * max S_l (S_l from the oracle: the layer with |W|, |b| on the
+    non-negative activations; nothing comes from the HIP path).  Returns the
+    new weight tuple and the deltas."""
+    conv_w, conv_b, dense_w, dense_b = weights
+    conv_b = [np.array(b, np.float32, copy=True) for b in conv_b]
+    deltas = []
+    for l, (ci, co, k, s, p) in enumerate(onet.convs):
+        _, acts = oracle.forward(onet, conv_w, conv_b, dense_w, dense_b, xs, want_acts=True)
+        prev = xs if l == 0 else acts[l - 1]
+        S = max(oracle.conv2d_relu(a, np.abs(conv_w[l]), np.abs(conv_b[l]), s, p).max() for a in prev)
+        delta = rel * float(S)
+        deltas.append(delta)
+        z = np.stack([oracle.forward_preact(onet, conv_w, conv_b, x)[l] for x in xs])   # [n][co][H][W]
+        steps = [0.0] + [sgn * 3.0 * delta * j for j in range(1, tries) for sgn in (1.0, -1.0)]
+        for c in range(co):
+            v = z[:, c].astype(np.float64).ravel()
+            for eps in steps:
+                if np.abs(v + eps).min() >= 2 * delta:
+                    conv_b[l][c] = np.float32(conv_b[l][c] + eps)
+                    break
+            else:
+                raise AssertionError(f"no bias shift separates layer {l + 1} channel {c} from the kink")
+    for l in range(len(onet.convs)):
+        zmin = min(np.abs(oracle.forward_preact(onet, conv_w, conv_b, x)[l]).min() for x in xs)
+        assert zmin >= deltas[l], (l, zmin, deltas[l])
+    return (conv_w, conv_b, dense_w, dense_b), deltas
