@@ -1376,6 +1376,14 @@ hipError_t launch_conv_first(const ConvArgs &a, rn_dtype dt, int cus, hipStream_
     return hipErrorInvalidValue;
 }
 
+bool conv_mfma_is_staged(int cin, int cout) {
+#define X(ci, co) \
+    if (cin == ci && cout == co) return !use_resident<ci, co>();
+    RN_MFMA_SHAPES(X)
+#undef X
+    return false;
+}
+
 size_t conv_first_packed_elems(int cin, int cout) { return (size_t)cin * 9 * cout; }
 
 size_t conv_mfma_packed_elems(int cin, int cout, rn_dtype dt) {

@@ -454,6 +454,128 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
     }
 }
 
+
+// ------------------------------------------------------------------ float32 tile partials
+
+// The same product for a float32 last layer on the staged conv kernel, whose
+// epilogue would otherwise read the tile's whole n_out x 16 C slice of head
+// weights from L2 for every tile:
+//   hpart[tile][o] = sum_k act_tile[k] * hw[P][k][o],  k = pixel * C + channel,
+// on v_mfma_f32_16x16x4_f32 with K walked in 16-deep blocks: in block b lane
+// group kq takes k = 16 b + 4 kq + j, j = 0..3 (one 16-byte load of the
+// tile's cache slice per lane), the weights packed [P][b][kq][o][4] with only
+// the n_out real logits (lanes of padding columns take zeros without a load).
+// Rows, one pass per distinct position, K quarters per wave and their sum in
+// wave order as in k_tile_part_bf16, so list and dense passes agree bit for
+// bit.
+template <int C, int NBO, bool DENSE>
+__global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
+    constexpr int KBL = C;                    // 16-deep K blocks per tile (16 C / 16)
+    constexpr int KW = KBL / 4;               // blocks per wave
+    constexpr int KB = 4;                     // blocks per batch of loads
+    static_assert(KW % KB == 0, "whole batches");
+    __shared__ int s_pos[64];
+    __shared__ floatx4 s_acc[4][4][NBO][64];  // [wave][row group][n-block][lane]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int cnt = work_count<DENSE>(a);
+    const XcdRange xr = xcd_range(cnt, 64);
+    const float *act = static_cast<const float *>(a.in);
+    const int ntiles = a.TH * a.TW;
+    const int row = lane & 15, kq = lane >> 4;
+    const int blk_elems = a.n_out * 16;       // weights of one K block
+    int boff[NBO];
+    bool bval[NBO];
+#pragma unroll
+    for (int nb = 0; nb < NBO; ++nb) {
+        const int o = nb * 16 + row;
+        bval[nb] = o < a.n_out;
+        boff[nb] = (kq * a.n_out + o) * 4;
+    }
+    for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
+        uint32_t e[4];
+        int pos[4];
+        const float *arow[4];
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+            const int it = g + 16 * rg + row;
+            const bool valid = it < xr.end;
+            e[rg] = valid ? item_word<DENSE>(a, it) : 0u;
+            const TileRef r = item_ref(a, e[rg]);
+            pos[rg] = valid ? r.tile : -1;
+            arow[rg] = act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C + 4 * kq + 16 * KW * wave;
+        }
+        if (tid < 64) {
+            const int t2 = g + tid;
+            s_pos[tid] = t2 < xr.end ? item_ref(a, item_word<DENSE>(a, t2)).tile : -1;
+        }
+        lds_barrier();
+        const int my_sp = s_pos[lane];
+        uint64_t left = __ballot(my_sp >= 0);                // rows of the block not yet handled
+        while (left) {                                       // uniform per block
+            const int P = __builtin_amdgcn_readlane(my_sp, __ffsll((long long)left) - 1);
+            const uint64_t pmask = __ballot(my_sp == P);
+            left &= ~pmask;
+            const float *wp = a.hw + ((size_t)P * KBL + KW * wave) * blk_elems;
+            floatx4 acc[4][NBO];
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) acc[rg][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            for (int s0 = 0; s0 < KW; s0 += KB) {
+                floatx4 av[KB][4], bv[KB][NBO];
+#pragma unroll
+                for (int s = 0; s < KB; ++s) {
+#pragma unroll
+                    for (int nb = 0; nb < NBO; ++nb)
+                        bv[s][nb] = bval[nb] ? *reinterpret_cast<const floatx4 *>(wp + (size_t)(s0 + s) * blk_elems + boff[nb])
+                                             : floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg)
+                        av[s][rg] = pos[rg] == P ? *reinterpret_cast<const floatx4 *>(arow[rg] + 16 * (s0 + s))
+                                                 : floatx4{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int s = 0; s < KB; ++s)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+                            for (int nb = 0; nb < NBO; ++nb)
+                                acc[rg][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][rg][j], bv[s][nb][j],
+                                                                                   acc[rg][nb], 0, 0, 0);
+            }
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) s_acc[wave][rg][nb][lane] = acc[rg][nb];
+            lds_barrier();
+            // Wave `wave` finishes row group `wave`: the K quarters in wave order.
+            const uint64_t gmask = (pmask >> (16 * wave)) & 0xFFFFu;
+            if (gmask) {                                     // uniform per wave
+                const uint32_t ew = wave == 0 ? e[0] : wave == 1 ? e[1] : wave == 2 ? e[2] : e[3];
+#pragma unroll
+                for (int nb = 0; nb < NBO; ++nb) {
+                    const floatx4 v = s_acc[0][wave][nb][lane] + s_acc[1][wave][nb][lane] +
+                                      s_acc[2][wave][nb][lane] + s_acc[3][wave][nb][lane];
+                    const int o = nb * 16 + row;             // D: rows 4 kq + i of the group, column `row`
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = 4 * kq + i;
+                        const uint32_t eq = __shfl(ew, q, 64);   // lane q holds row q's item
+                        if (o < a.n_out && ((gmask >> q) & 1)) {
+                            const TileRef rq = item_ref(a, eq);
+                            a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = v[i];
+                        }
+                    }
+                }
+            }
+            lds_barrier();                                   // s_acc is rewritten by the next pass
+        }
+    }
+}
+
 }  // namespace
 
 int head_streams_per_block(int n_out) { return n_out == 18 ? 4 : 8; }
@@ -536,6 +658,44 @@ hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s, bool
                    : dense ? run_tile_part_bf16<128, true, false>(a, cus, s)
                            : run_tile_part_bf16<128, false, false>(a, cus, s);
     return hipErrorInvalidValue;
+}
+
+template <int C, bool DENSE>
+hipError_t run_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s) {
+    const int grid = dev::persistent_grid(cus * 2, (a.max_tiles + 63) / 64);
+    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_f32<C, 1, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_f32<C, 2, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_tile_part_f32<C, 4, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+bool tile_part_f32_supported(int C) { return C == 128 || C == 160; }
+
+hipError_t launch_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s) {
+    const bool dense = a.wl == nullptr;
+    if (a.cout == 128) return dense ? run_tile_part_f32<128, true>(a, cus, s) : run_tile_part_f32<128, false>(a, cus, s);
+    if (a.cout == 160) return dense ? run_tile_part_f32<160, true>(a, cus, s) : run_tile_part_f32<160, false>(a, cus, s);
+    return hipErrorInvalidValue;
+}
+
+size_t tile_part_f32_elems(int ntiles, int C, int n_out) { return (size_t)ntiles * kTilePx * C * n_out; }
+
+void pack_tile_part_f32(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst) {
+    // [tile][b][kq][o][j]: k = 16 b + 4 kq + j is pixel k / C (row-major in the
+    // tile) and channel k % C; zero outside the image.
+    const int ntiles = TH * TW;
+    size_t d = 0;
+    for (int t = 0; t < ntiles; ++t) {
+        const int ty = t / TW, tx = t % TW;
+        for (int b = 0; b < C; ++b)
+            for (int kq = 0; kq < 4; ++kq)
+                for (int o = 0; o < n_out; ++o)
+                    for (int j = 0; j < 4; ++j) {
+                        const int k = 16 * b + 4 * kq + j, m = k / C, c = k % C;
+                        const int y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
+                        dst[d++] = (y < H && x < W) ? dense_w[(size_t)o * C * H * W + ((size_t)c * H + y) * W + x] : 0.f;
+                    }
+    }
 }
 
 hipError_t launch_tile_head(const TileHeadArgs &a, hipStream_t s) {

@@ -41,13 +41,14 @@ struct Plan {
     int radius[RN_MAX_CONV] = {0};         // change growth per layer, (k - 1) / 2
     size_t K = 0;                          // head input elements per slot (tiled)
     int head_mode = RN_HEAD_TILES;
+    bool part_f32 = false;                 // float32 tile partials by position (own kernel) instead of in the epilogue
     bool fuse_first = false;               // layer 1 folded into layer 2's halo staging
     int head_sg = 8;
     size_t part_elems = 0;
     // byte offsets into the workspace
     size_t o_lut, o_xin, o_ring, o_dring, o_primed, o_ids, o_act[RN_MAX_CONV + 1], o_w[RN_MAX_CONV],
         o_b[RN_MAX_CONV], o_wd, o_bd, o_pm[RN_MAX_CONV + 1], o_tm[RN_MAX_CONV + 1], o_tpfx[RN_MAX_CONV + 1], o_nchg, o_ntile,
-        o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hp;
+        o_wl[RN_MAX_CONV + 1], o_wls[RN_MAX_CONV + 1], o_cnt, o_part, o_hw, o_hw2, o_hp;
     size_t w_elems[RN_MAX_CONV] = {0};
     size_t w_bytes[RN_MAX_CONV] = {0};
     // Training (backward and SGD step): float32 nets of 3x3 stride-1 pad-1
@@ -171,6 +172,8 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
                     (!bf || tile_part_bf16_supported(p->C[p->L])))
                        ? RN_HEAD_TILES
                        : RN_HEAD_FULL;
+    p->part_f32 = p->head_mode == RN_HEAD_TILES && !bf && p->L >= 2 && !p->gen[p->L - 1] &&
+                  conv_mfma_is_staged(p->C[p->L - 1], p->C[p->L]) && tile_part_f32_supported(p->C[p->L]);
     p->head_sg = head_streams_per_block(p->N);
     size_t part = 0;
     for (int n = 1; n <= p->S; ++n) {
@@ -237,6 +240,7 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_hw = take(!tiles_head ? 0
                    : p->dt == RN_BF16 ? tile_part_bf16_elems(p->ntl[p->L], p->C[p->L], p->N) * 2
                                       : tile_head_w_elems(p->ntl[p->L], p->C[p->L], p->N) * 4);
+    p->o_hw2 = take(p->part_f32 ? tile_part_f32_elems(p->ntl[p->L], p->C[p->L], p->N) * 4 : 0);
     p->o_hp = take(tiles_head ? S * p->ntl[p->L] * p->N * 4 : 0);
     p->total = off;
     return RN_OK;
@@ -471,7 +475,7 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, bool identity, 
             cv.hw = net->at<float>(p.o_hw);
             cv.hpart = net->at<float>(p.o_hp);
             last = cv;
-            if (bf) cv.n_out = 0;                         // partials from their own kernel below
+            if (bf || p.part_f32) cv.n_out = 0;           // partials from their own kernel below
         }
         if (p.gen[l - 1])
             e = timed(net, l == 1 ? RN_PHASE_CONV1 : RN_PHASE_CONVN, s, [&] {
@@ -487,12 +491,16 @@ hipError_t run_layers(reuse_net *net, int n, const int32_t *ids, bool identity, 
             }, l);
         if (e != hipSuccess) return e;
     }
-    if (tiles_head && p.dt == RN_BF16) {
-        // bf16: the tiles of the last work list (every tile in dense mode) get
-        // their partials from the matrix kernel, reading the updated cache.
+    if (tiles_head && (p.dt == RN_BF16 || p.part_f32)) {
+        // bf16, or a float32 last layer on the staged kernel: the tiles of the
+        // last work list (every tile in dense mode) get their partials from a
+        // matrix kernel by position, reading the updated cache.
         last.in = net->at<void>(p.o_act[p.L]);
         last.in_stride = p.act_stride[p.L];
-        e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_part_bf16(last, net->cus, s); });
+        if (p.part_f32) last.hw = net->at<float>(p.o_hw2);
+        e = timed(net, RN_PHASE_HEAD, s, [&] {
+            return p.part_f32 ? launch_tile_part_f32(last, net->cus, s) : launch_tile_part_bf16(last, net->cus, s);
+        });
         if (e != hipSuccess) return e;
     }
     if (tiles_head) {
@@ -861,6 +869,12 @@ hipError_t upload_weights(reuse_net *net, const rn_weights *w, hipStream_t s) {
         for (float &v : hw) v = rnd(v);
         up(p.o_hw, hw.data(), hw.size() * 4);
     }
+    std::vector<float> hw2;
+    if (p.part_f32) {
+        hw2.assign(tile_part_f32_elems(p.ntl[p.L], CL, p.N), 0.f);
+        pack_tile_part_f32(w->dense_w, p.N, CL, HL, WL, THL, TWL, hw2.data());
+        up(p.o_hw2, hw2.data(), hw2.size() * 4);
+    }
     up(p.o_bd, w->dense_b, (size_t)p.N * 4);
     // pageable host buffers: the copies are done with the vectors before they go
     if (e == hipSuccess) e = hipStreamSynchronize(s);
@@ -1213,6 +1227,7 @@ rn_status reuse_net_sgd_step(reuse_net *net, const float *grads, float lr, void 
         a.W = p.Wl[p.L];
         a.TW = p.TWl[p.L];
         a.ntiles = p.ntl[p.L];
+        a.n_out = p.N;
         a.K = p.K;
         e = timed(net, RN_PHASE_SGD, s, [&] { return launch_sgd(a, s); });
     };
@@ -1223,6 +1238,7 @@ rn_status reuse_net_sgd_step(reuse_net *net, const float *grads, float lr, void 
     }
     upd(p.o_wd, (size_t)p.N * p.K, SGD_DENSE, grads + gl.dw, 0, 0);
     if (p.head_mode == RN_HEAD_TILES) upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, grads + gl.dw, 0, 0);
+    if (p.part_f32) upd(p.o_hw2, tile_part_f32_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_PART, grads + gl.dw, 0, 0);
     upd(p.o_bd, p.N, SGD_PLAIN, grads + gl.db, 0, 0);
     // Every cache now holds activations of the old weights: all slots unprimed.
     if (e == hipSuccess) e = timed(net, RN_PHASE_SGD, s, [&] { return launch_unprime(net->at<int32_t>(p.o_primed), p.S, s); });

@@ -407,6 +407,20 @@ __device__ inline long long sgd_src(const SgdArgs &a, size_t d) {
         if (y >= a.H || x >= a.W) return -1;
         return (long long)o * a.C * a.H * a.W + ((long long)c * a.H + y) * a.W + x;
     }
+    case SGD_TILE_PART: {                                     // [tile][b][kq][o][j], b < C
+        const int j = (int)(d % 4);
+        size_t r = d / 4;
+        const int o = (int)(r % a.n_out);
+        r /= a.n_out;
+        const int kq = (int)(r % 4);
+        r /= 4;
+        const int b = (int)(r % a.C), tile = (int)(r / a.C);
+        const int k = 16 * b + 4 * kq + j, m = k / a.C, c = k - m * a.C;
+        const int ty = tile / a.TW, tx = tile - ty * a.TW;
+        const int y = ty * kTile + m / 4, x = tx * kTile + m % 4;
+        if (y >= a.H || x >= a.W) return -1;
+        return (long long)o * a.C * a.H * a.W + ((long long)c * a.H + y) * a.W + x;
+    }
     case SGD_DX: {                                            // [b][nb][lane][j], cin = ca, cout = cz
         const int NB = (a.cin + 15) / 16;
         const int j = (int)(d % 4), l = (int)((d / 4) % 64), nb = (int)((d / 256) % NB);

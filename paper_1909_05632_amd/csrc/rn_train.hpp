@@ -51,7 +51,7 @@ struct BwdArgs {
 // that holds weight v of the natural layout becomes fl(v - fl(lr * g)), with g
 // the gradient of that weight, so each packed copy stays the packing of the
 // updated weights.  kind: what layout dst has.
-enum SgdKind { SGD_PLAIN = 0, SGD_FIRST = 1, SGD_MFMA = 2, SGD_DENSE = 3, SGD_TILE_HEAD = 4, SGD_DX = 5 };
+enum SgdKind { SGD_PLAIN = 0, SGD_FIRST = 1, SGD_MFMA = 2, SGD_DENSE = 3, SGD_TILE_HEAD = 4, SGD_DX = 5, SGD_TILE_PART = 6 };
 struct SgdArgs {
     float *dst;
     size_t count;                 // elements of dst
@@ -59,7 +59,7 @@ struct SgdArgs {
     const float *g;               // gradient in the natural layout of this weight (OIHW, or [n_out][C][H][W])
     float lr;
     int cin, cout;                // conv layers
-    int C, H, W, TW, ntiles;      // dense / tile head: last layer
+    int C, H, W, TW, ntiles, n_out;   // dense / tile head / tile partials: last layer
     size_t K;
 };
 

@@ -362,6 +362,27 @@ def test_bf16_step_equals_full_bitwise(torch):
     b.close()
 
 
+def test_staged_last_layer_step_equals_full_bitwise(torch):
+    # float32 1->64->128->128: the last layer runs on the staged kernel and its
+    # tile partials come from the position-batched kernel; an all-changed step
+    # (work lists, 64-item groups mixing positions) and the dense pass give the
+    # same bits, and a later sprite step matches the oracle.
+    wl = synth.Workload(cid=81, streams=5, frames=3, h=28, w=36, convs=(64, 128, 128), n_out=18)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    u8 = synth.sprite_batch(wl, streams=range(5), frames=2, full_change=True)
+    x = synth.to_f32(u8)
+    dev = torch.from_numpy(x).cuda()
+    a, b = make_net(wl, 5, weights), make_net(wl, 5, weights)
+    a.step(dev[0][:, None].contiguous())
+    la = a.step(dev[1][:, None].contiguous()).cpu().numpy()
+    lb = b.full(dev[1][:, None].contiguous()).cpu().numpy()
+    assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
+    onet = oracle_net(wl)
+    check_values(a, onet, weights, x[1][:, None], np.arange(5), [0, 4], la, label="staged last layer")
+    a.close()
+    b.close()
+
+
 def test_bf16_fullres_210x160(torch):
     wl = synth.WORKLOADS["fullres-1024x32"]
     weights = synth.net_weights(wl)
