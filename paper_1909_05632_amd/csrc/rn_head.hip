@@ -522,6 +522,11 @@ __global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
             for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
                 for (int nb = 0; nb < NBO; ++nb) acc[rg][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            // Row groups with no row at P skip their loads and matrix ops
+            // (the flags are uniform: whole groups, from the ballot).
+            bool gact[4];
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) gact[rg] = ((pmask >> (16 * rg)) & 0xFFFFu) != 0;
             for (int s0 = 0; s0 < KW; s0 += KB) {
                 floatx4 av[KB][4], bv[KB][NBO];
 #pragma unroll
@@ -532,19 +537,21 @@ __global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
                                              : floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int rg = 0; rg < 4; ++rg)
-                        av[s][rg] = pos[rg] == P ? *reinterpret_cast<const floatx4 *>(arow[rg] + 16 * (s0 + s))
-                                                 : floatx4{0.f, 0.f, 0.f, 0.f};
+                        av[s][rg] = gact[rg] && pos[rg] == P ? *reinterpret_cast<const floatx4 *>(arow[rg] + 16 * (s0 + s))
+                                                             : floatx4{0.f, 0.f, 0.f, 0.f};
                 }
 #pragma unroll
-                for (int s = 0; s < KB; ++s)
+                for (int rg = 0; rg < 4; ++rg) {
+                    if (!gact[rg]) continue;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
+                    for (int s = 0; s < KB; ++s)
 #pragma unroll
-                        for (int rg = 0; rg < 4; ++rg)
+                        for (int j = 0; j < 4; ++j)
 #pragma unroll
                             for (int nb = 0; nb < NBO; ++nb)
                                 acc[rg][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][rg][j], bv[s][nb][j],
                                                                                    acc[rg][nb], 0, 0, 0);
+                }
             }
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg)

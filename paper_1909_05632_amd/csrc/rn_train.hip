@@ -18,6 +18,8 @@
 //       whose partial sums are added in team order (no atomics, so the result
 //       is deterministic).
 // The SGD step updates every packed copy of a weight in place.
+#include <type_traits>
+
 #include "rn_device.hpp"
 #include "rn_train.hpp"
 
@@ -49,9 +51,10 @@ __global__ __launch_bounds__(256) void k_reinforce(int n, int n_out, const float
 
 // ------------------------------------------------------------------ dense head
 
-// One block per tile position t of the last layer; a thread owns one of the
-// tile's 16 C head inputs j at a time, keeps its NO weights and NO gradient
-// sums in registers and walks the streams (their g rows staged in LDS).
+// Block (t, c) takes 256 of the 16 C head inputs of tile position t of the
+// last layer (chunk c); a thread owns one input j, keeps its NO weights and
+// NO gradient sums in registers and walks the streams (their g rows staged
+// in LDS).
 template <int NO>
 __global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
     constexpr int kHeadStreams = NO <= 32 ? 256 : 128;    // streams per LDS stage of g (32 KB at most)
@@ -60,8 +63,8 @@ __global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
     const int t = blockIdx.x;
     const int E = kTilePx * a.C;
     const int ty = t / a.TW, tx = t - ty * a.TW;
-    for (int e0 = 0; e0 < E; e0 += blockDim.x) {
-        const int j = e0 + threadIdx.x;
+    {
+        const int j = blockIdx.y * blockDim.x + threadIdx.x;
         const bool ok = j < E;
         float w[NO], acc[NO];
 #pragma unroll
@@ -106,7 +109,7 @@ __global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
             }
         }
     }
-    if (t == 0 && (int)threadIdx.x < a.n_out) {
+    if (t == 0 && blockIdx.y == 0 && (int)threadIdx.x < a.n_out) {
         float s = 0.f;
         for (int i = 0; i < a.n; ++i) s += a.g[(size_t)i * a.n_out + threadIdx.x];
         a.gbd[threadIdx.x] = a.accumulate ? a.gbd[threadIdx.x] + s : s;
@@ -217,17 +220,37 @@ constexpr int bank_stride(int c) {
     return s;
 }
 
+// Column chunks per wave for NBQ column blocks and MB row blocks: at most 24
+// blocks per wave (its accumulators), and, among those, the fewest idle
+// waves in the blocks of four (the count that leaves the fewest, then the
+// smallest such count).
+constexpr int dw_chunks(int nbq, int mb) {
+    int best = (nbq + 23) / 24, best_idle = 1 << 30;
+    for (int nch = (nbq + 23) / 24; nch <= (nbq + 23) / 24 + 3 && nch <= nbq; ++nch) {
+        const int u = mb * nch, idle = (u + 3) / 4 * 4 - u;
+        if (idle < best_idle) {
+            best = nch;
+            best_idle = idle;
+        }
+    }
+    return best;
+}
+
 template <int CA, int CZ, bool FIRST>
 struct Dw {
     static constexpr int NQ = 9 * CA + 1;                 // columns: (kernel position, input channel), bias
     static constexpr int NBQ = (NQ + 15) / 16;            // 16-column blocks
-    static constexpr int NCH = (NBQ + 23) / 24;           // column chunks (at most 24 blocks per wave)
-    static constexpr int QW = (NBQ + NCH - 1) / NCH;      // column blocks per wave
     static constexpr int MB = (CZ + 15) / 16;             // 16-row blocks (output channels)
+    static constexpr int NCH = dw_chunks(NBQ, MB);        // column chunks
+    static constexpr int QW = (NBQ + NCH - 1) / NCH;      // column blocks per wave
     static constexpr int U = MB * NCH;                    // waves per team
     static constexpr int BPT = (U + 3) / 4;               // blocks per team
     static constexpr int SZ = bank_stride(CZ);            // dz tile row stride in LDS
     static constexpr int SA = FIRST ? CA : bank_stride(CA);   // halo pixel stride in LDS
+    // Per-thread shares of a tile's operands, prefetched into registers:
+    static constexpr int DZV = (4 * CZ + 255) / 256;      // 16-byte chunks of the dz tile (16 x CZ)
+    static constexpr int HV = FIRST ? (36 * CA + 255) / 256 : (9 * CA + 255) / 256;   // halo values / chunks
+    static_assert(CZ % 4 == 0 && (FIRST || CA % 4 == 0), "16-byte channel chunks");
 };
 
 // Block = 4 waves of one team; wave w of block b of the team owns row block
@@ -268,25 +291,29 @@ __global__ __launch_bounds__(256) void k_bwd_dw(BwdArgs a) {
     const long long NT = (long long)a.n * a.ntiles;
     const long long t0 = NT * team / a.teams, t1 = NT * (team + 1) / a.teams;
     const size_t HW = (size_t)a.H * a.W;
-    for (long long tt = t0; tt < t1; ++tt) {
+    // The operands of tile tt, this thread's share, into registers (every
+    // load issued; out-of-image halo values and chunks are zero).
+    float4 rdz[D::DZV];
+    typename std::conditional<FIRST, float, float4>::type rh[D::HV];
+    auto fetch = [&](long long tt) __attribute__((always_inline)) {
         const int i = (int)(tt / a.ntiles), t = (int)(tt - (long long)i * a.ntiles);
         const int ty = t / a.TW, tx = t - ty * a.TW;
         const int slot = a.ids[i];
-        __syncthreads();                                   // the previous tile's LDS readers are done
         const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
-        for (int e = threadIdx.x; e < 4 * CZ; e += blockDim.x) {   // 16 pixels x CZ / 4 chunks
-            const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);
-            *reinterpret_cast<float4 *>(s_dz + m * D::SZ + 4 * c4) = dzp[e];
+#pragma unroll
+        for (int k = 0; k < D::DZV; ++k) {
+            const int e = threadIdx.x + 256 * k;
+            rdz[k] = e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
         if constexpr (FIRST) {
-            // 6x6 x CA input halo from the float32 input planes (a ring of four
-            // frames, oldest first as channels, when stacking).
             const int head = a.stack != 1 ? a.ring_head[slot] : 0;
-            for (int e = threadIdx.x; e < 36 * CA; e += blockDim.x) {
+#pragma unroll
+            for (int k = 0; k < D::HV; ++k) {
+                const int e = threadIdx.x + 256 * k;
                 const int c = e / 36, pos = e - c * 36;
                 const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
                 float v = 0.f;
-                if (y >= 0 && y < a.H && x >= 0 && x < a.W) {
+                if (e < 36 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W) {
                     const float *plane;
                     if (a.stack == 1) {
                         plane = a.act_prev + ((size_t)slot * CA + c) * HW;
@@ -297,21 +324,51 @@ __global__ __launch_bounds__(256) void k_bwd_dw(BwdArgs a) {
                     }
                     v = plane[(size_t)y * a.W + x];
                 }
-                s_h[pos * D::SA + c] = v;
+                rh[k] = v;
             }
         } else {
             const float *ap = a.act_prev + (size_t)slot * a.prev_stride;
-            for (int e = threadIdx.x; e < 9 * CA; e += blockDim.x) {   // 36 pixels x CA / 4 chunks
+#pragma unroll
+            for (int k = 0; k < D::HV; ++k) {
+                const int e = threadIdx.x + 256 * k;
                 const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
                 const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
                 float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (y >= 0 && y < a.H && x >= 0 && x < a.W)
+                if (e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
                     v = *reinterpret_cast<const float4 *>(
                         ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
-                *reinterpret_cast<float4 *>(s_h + pos * D::SA + 4 * c4) = v;
+                rh[k] = v;
+            }
+        }
+    };
+    if (t0 < t1) fetch(t0);
+    for (long long tt = t0; tt < t1; ++tt) {
+        __syncthreads();                                   // the previous tile's LDS readers are done
+#pragma unroll
+        for (int k = 0; k < D::DZV; ++k) {
+            const int e = threadIdx.x + 256 * k;
+            if (e < 4 * CZ) {
+                const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);
+                *reinterpret_cast<float4 *>(s_dz + m * D::SZ + 4 * c4) = rdz[k];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < D::HV; ++k) {
+            const int e = threadIdx.x + 256 * k;
+            if constexpr (FIRST) {
+                if (e < 36 * CA) {
+                    const int c = e / 36, pos = e - c * 36;
+                    s_h[pos * D::SA + c] = rh[k];
+                }
+            } else {
+                if (e < 9 * CA) {
+                    const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+                    *reinterpret_cast<float4 *>(s_h + pos * D::SA + 4 * c4) = rh[k];
+                }
             }
         }
         __syncthreads();
+        if (tt + 1 < t1) fetch(tt + 1);                    // in flight during this tile's matrix ops
         if (active) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
@@ -545,7 +602,7 @@ hipError_t launch_reinforce(int n, int n_out, const float *logits, const int32_t
 }
 
 hipError_t launch_bwd_head(const HeadBwdArgs &a, hipStream_t s) {
-    const dim3 grid(a.ntiles), block(256);
+    const dim3 grid(a.ntiles, (kTilePx * a.C + 255) / 256), block(256);
     if (a.n_out <= 8) hipLaunchKernelGGL(k_bwd_head<8>, grid, block, 0, s, a);
     else if (a.n_out <= 32) hipLaunchKernelGGL(k_bwd_head<32>, grid, block, 0, s, a);
     else hipLaunchKernelGGL(k_bwd_head<64>, grid, block, 0, s, a);
