@@ -60,9 +60,12 @@ typedef enum { RN_F32 = 0, RN_BF16 = 1, RN_U8 = 2 } rn_dtype;
  * rounding order; each is deterministic.
  *   RN_HEAD_TILES: the head is linear, so the logits are a sum over tiles of
  *     each tile's contribution (the reuse idea of Sec. 1 applied to the dense
- *     layer).  The last conv layer's epilogue recomputes the contribution of
- *     every tile it recomputes, and the head adds the cached contributions in
- *     a fixed tile order.  Needs n_conv >= 2.
+ *     layer).  The contribution of every tile the last conv layer recomputes
+ *     is recomputed with it (in that layer's epilogue, or, for bf16 and for
+ *     float32 layers too large to keep their weights in LDS, by a matrix
+ *     kernel that takes the recomputed tiles position by position), and the
+ *     head adds the cached contributions in a fixed tile order.  Needs
+ *     n_conv >= 2.
  *   RN_HEAD_FULL: the head reads the whole last-layer cache of every stream
  *     every step (split-K GEMV over C_L*H_L*W_L). */
 typedef enum { RN_HEAD_TILES = 0, RN_HEAD_FULL = 1 } rn_head_mode;
