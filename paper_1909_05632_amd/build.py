@@ -17,7 +17,7 @@ LIB = os.path.join(PKG, "libreuse_net.so")
 SOURCES = ["rn_host.hip", "rn_masks.hip", "rn_conv.hip", "rn_conv_bf16.hip", "rn_head.hip", "rn_train.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
+FLAGS = ["-O3", "-std=c++20", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
          # packed fp32 VALU ops stay off (the compiler would otherwise form them from float2 code)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]

@@ -183,10 +183,12 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
 // Loop nest per group: for each chunk of HC = min(CIN, 64) input channels (a
 // "pass"), the chunk's halos of the 16 tiles sit in LDS and the nine kernel
 // positions stream their weights for that chunk through LDS, one position per
-// stage, double-buffered.  Each weight byte brought to the CU serves 16 tiles
-// and each halo byte is brought once.  The weights two stages ahead are
-// fetched into registers at the start of a stage and written to the free
-// buffer at the start of the next stage; the next pass's halo chunk (the next
+// stage, in three buffers.  Each weight byte brought to the CU serves 16 tiles
+// and each halo byte is brought once.  The weights of a stage are fetched into
+// registers four stages ahead and written to the free buffer two stages ahead
+// (two stages of registers, so a weight load, and the group's output stores
+// that precede it in the memory counter, have two stages to complete before a
+// wait counts them); the next pass's halo chunk (the next
 // group's first chunk after the last pass) is fetched in two halves, after the
 // matrix ops of stages 1 and 3, and written to LDS once the pass is done.  The
 // nine stages are unrolled and every load is issued on every path (a halo
@@ -194,12 +196,17 @@ __global__ __launch_bounds__(256) void k_conv_first_bf16(ConvArgs a) {
 // stored), so each wait names exactly the loads it needs, all issued at least
 // a stage earlier.  Each stage ends with one block barrier.
 //
-// Halo layout in LDS: pixel p = 6 hy + hx at p * C8 16-byte chunks, chunk c of
-// the pixel stored at slot c ^ g(hy, hx), g = 2 (hy % 4) + (hx / 2) % 2 for 8
-// chunks per pixel and hy % 4 for 4.  The LDS serves 16 lanes of a 16-byte
-// read per clock (256 bytes); the 16 pixels such a group reads (one tile, one
-// chunk) then fall in 16 distinct bank groups for every kernel position
-// (checked exhaustively on the host).
+// Halo layout in LDS: chunk c of halo pixel (hy, hx) at 16-byte chunk
+// hy RS + hx CS + c, padded strides with CS = 9, RS = 60 for 8 chunks per
+// pixel (CS = 4, RS = 25 for 4).  The LDS serves 16 lanes of a 16-byte read
+// per clock (256 bytes, 16 bank groups); the 16 pixels such a group reads (one
+// tile, one chunk: rows a = 0..3, columns b = 0..3 shifted by the kernel
+// position) sit at a RS + b CS + const, and a RS + b CS mod 16 takes all 16
+// values, so every read is conflict-free.  Unlike an XOR swizzle, the layout
+// makes every read of a stage a per-lane base plus a constant, which the
+// instruction's offset field holds (no per-position address registers).
+// Within a stage the fragments of the next k-step are read before the matrix
+// ops of the current one.
 template <int CIN, int COUT>
 struct GrpBf {
     static constexpr int THREADS = 512;              // eight waves, 4 (M) x 2 (N)
@@ -211,7 +218,11 @@ struct GrpBf {
     static constexpr int HC = CIN < 64 ? CIN : 64;   // channels per pass
     static constexpr int NPASS = CIN / HC;
     static constexpr int C8 = HC / 8;                // 16-byte chunks per pixel and pass
-    static constexpr int HALO = 36 * C8 * 8;         // bf16 elements per tile halo chunk
+    // Halo pixel (hy, hx) of a pass at chunk hy RS + hx CS (16-byte chunks):
+    // a padded layout whose every read offset is a lane base plus a constant.
+    static constexpr int CS = C8 == 8 ? 9 : 4;
+    static constexpr int RS = C8 == 8 ? 60 : 25;
+    static constexpr int HALO = (5 * RS + 6 * CS) * 8;   // bf16 elements per tile halo chunk
     static constexpr int KS = HC / 16;               // k-steps per stage
     static constexpr int WST = HC * COUT;            // bf16 elements per weight stage
     static constexpr int WPT = (WST / 8 + THREADS - 1) / THREADS;   // 16-byte weight loads per thread and stage
@@ -227,8 +238,7 @@ struct GrpBf {
 template <int CIN, int COUT>
 __device__ inline int halo_chunk(int hy, int hx, int c) {
     using G = GrpBf<CIN, COUT>;
-    const int g = G::C8 == 8 ? 2 * (hy & 3) + ((hx >> 1) & 1) : (hy & 3);
-    return ((hy * 6 + hx) * G::C8 + (c ^ g)) * 8;
+    return (hy * G::RS + hx * G::CS + c) * 8;
 }
 
 // Halo chunk j of pass `pass` of a group: the THREADS / T threads tid / (THREADS
@@ -315,51 +325,72 @@ struct FragsBf {
     bf16x8 wa[NBW];
 };
 
+// Lane bases of the k-step reads: this lane's halo chunk (tile pair 0 of the
+// wave, pixel m of column l % 32, chunk half h) and its weight fragment in
+// stage buffer 0.  Every read of a stage is then base + a constant.
 template <int CIN, int COUT>
-__device__ inline void load_kstep(FragsBf<GrpBf<CIN, COUT>::MP, GrpBf<CIN, COUT>::NBW> &f, const uint16_t *halos,
-                                  const uint16_t *wst, int kpos, int s, int wm, int half, int lane) {
+__device__ inline const uint16_t *halo_lane(const uint16_t *halos, int wm, int lane) {
     using G = GrpBf<CIN, COUT>;
-    const int ky = kpos / 3, kx = kpos - ky * 3;
     const int col = lane & 31, h = lane >> 5, m = col & 15;
-    const int off = halo_chunk<CIN, COUT>((m & 3) + ky, (m >> 2) + kx, 2 * s + h);
-    const uint16_t *hb = halos + (wm * 2 * G::MP + (col >> 4)) * G::HALO + off;
-    const uint16_t *wb = wst + (((size_t)s * G::NB + half * G::NBW) * 64 + lane) * 8;
-#pragma unroll
-    for (int p = 0; p < G::MP; ++p)
-        f.xb[p] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(hb + 2 * p * G::HALO));
-#pragma unroll
-    for (int nb = 0; nb < G::NBW; ++nb)
-        f.wa[nb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wb + nb * 512));
+    return halos + (wm * 2 * G::MP + (col >> 4)) * G::HALO + halo_chunk<CIN, COUT>(m & 3, m >> 2, h);
 }
 
-// The matrix work of one stage (kernel position kpos) on the wave's MP tile
-// pairs x NBW 32-output blocks.  The first k-step's fragments arrive in f0
-// (read before the previous stage's barrier); each later k-step is read just
-// before its matrix ops (the other wave of the SIMD runs meanwhile).
-template <int CIN, int COUT, int MP, int NBW, typename Mid>
-__device__ inline void stage_mma(floatx16 (&acc)[MP][NBW], const FragsBf<MP, NBW> &f0, const uint16_t *halos,
-                                 const uint16_t *wst, int kpos, int wm, int half, int lane, Mid &&mid) {
+template <int CIN, int COUT>
+__device__ inline const uint16_t *weight_lane(const uint16_t *wbuf, int half, int lane) {
+    using G = GrpBf<CIN, COUT>;
+    return wbuf + ((size_t)half * G::NBW * 64 + lane) * 8;
+}
+
+// Fragments of k-step S of kernel position KPOS (weights in stage buffer
+// KPOS % 3).
+template <int CIN, int COUT, int KPOS, int S>
+__device__ inline void load_kstep(FragsBf<GrpBf<CIN, COUT>::MP, GrpBf<CIN, COUT>::NBW> &f, const uint16_t *hl,
+                                  const uint16_t *wl) {
+    using G = GrpBf<CIN, COUT>;
+    constexpr int ky = KPOS / 3, kx = KPOS % 3;
+    constexpr int hoff = (ky * G::RS + kx * G::CS + 2 * S) * 8;
+    constexpr int woff = (KPOS % 3) * G::WST + S * G::NB * 512;
+#pragma unroll
+    for (int p = 0; p < G::MP; ++p)
+        f.xb[p] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(hl + hoff + 2 * p * G::HALO));
+#pragma unroll
+    for (int nb = 0; nb < G::NBW; ++nb)
+        f.wa[nb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(wl + woff + nb * 512));
+}
+
+// The matrix work of one stage (kernel position KPOS) on the wave's MP tile
+// pairs x NBW 32-output blocks, from k-step S on.  The fragments of k-step S
+// arrive in f; those of the next k-step (past the stage's last: the first of
+// stage KPOS + 1, whose weight buffer the previous barrier published) are
+// read before the matrix ops of this one, so each read has a k-step of matrix
+// work to arrive.  On return f holds the next stage's first k-step.
+template <int CIN, int COUT, int KPOS, int S, int MP, int NBW, typename Mid>
+__device__ inline void stage_mma(floatx16 (&acc)[MP][NBW], FragsBf<MP, NBW> &f, const uint16_t *hl, const uint16_t *wl,
+                                 Mid &&mid) {
     using G = GrpBf<CIN, COUT>;
     static_assert(MP == G::MP && NBW == G::NBW, "accumulator shape");
+    FragsBf<MP, NBW> nxt;
+    if constexpr (S + 1 < G::KS) load_kstep<CIN, COUT, KPOS, S + 1>(nxt, hl, wl);
+    else if constexpr (KPOS < 8) load_kstep<CIN, COUT, KPOS + 1, 0>(nxt, hl, wl);
 #pragma unroll
-    for (int s = 0; s < G::KS; ++s) {
-        FragsBf<MP, NBW> f;
-        if (s == 0) f = f0;
-        else load_kstep<CIN, COUT>(f, halos, wst, kpos, s, wm, half, lane);
+    for (int p = 0; p < G::MP; ++p)
 #pragma unroll
-        for (int p = 0; p < MP; ++p)
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                acc[p][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.wa[nb], f.xb[p], acc[p][nb], 0, 0, 0);
-        // The stage's memory work goes out while the first k-step's matrix
-        // ops run (pinned there: the scheduler would sink the loads to the
-        // end of the stage, leaving them a barrier's distance to arrive).
-        __builtin_amdgcn_sched_barrier(0);
-        if (s == 0) {
-            mid();
-            __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int nb = 0; nb < G::NBW; ++nb)
+            acc[p][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.wa[nb], f.xb[p], acc[p][nb], 0, 0, 0);
+    if constexpr (S + 1 < G::KS || KPOS < 8) {
+        __builtin_amdgcn_sched_group_barrier(0x100, MP + NBW, 0);   // the next reads first,
+        __builtin_amdgcn_sched_group_barrier(0x008, MP * NBW, 0);   // then the matrix ops
     }
+    // The stage's memory work goes out while the first k-step's matrix ops
+    // run (pinned there: the scheduler would sink the loads to the end of the
+    // stage, leaving them a barrier's distance to arrive).
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (S == 0) {
+        mid();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (S + 1 < G::KS || KPOS < 8) f = nxt;
+    if constexpr (S + 1 < G::KS) stage_mma<CIN, COUT, KPOS, S + 1, MP, NBW>(acc, f, hl, wl, mid);
 }
 
 template <int CIN, int COUT, bool DENSE, bool VAR>
@@ -376,6 +407,8 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     if (xr.first >= xr.end) return;                       // uniform per block
     uint16_t *halos = smem16;
     uint16_t *wbuf = smem16 + G::T * G::HALO;             // three stages; stage q of a group in q % 3
+    const uint16_t *hl = halo_lane<CIN, COUT>(halos, wm, lane);
+    const uint16_t *wl = weight_lane<CIN, COUT>(wbuf, half, lane);
     const uint16_t *wg = static_cast<const uint16_t *>(a.w);
     uint16_t *outp = static_cast<uint16_t *>(a.out);
     for (int j = tid; j < COUT; j += G::THREADS) s_bias[j] = a.bias[j];
@@ -389,13 +422,13 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     // Prologue: items of groups 0 and 1 in LDS, of group 2 in flight (items are
     // written to LDS a group before the halo fetch that reads them and loaded
     // a group before that); pass 0 halos and weight stages 0 and 1 in LDS,
-    // stage 2 in flight to registers.
+    // stages 2 and 3 in flight to registers.
     if (tid < G::T) {
         s_items[0][tid] = items_of(0);
         s_items[1][tid] = items_of(1);
     }
     uint32_t ireg = items_of(2);
-    u32x4 wreg[G::WPT];
+    u32x4 wreg[G::WPT], wnext[G::WPT];
     fetch_stage<CIN, COUT>(wg, 0, wreg, tid);
     lds_barrier();
     u32x4 hreg[G::HPT];
@@ -406,9 +439,10 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
     fetch_stage<CIN, COUT>(wg, 1, wreg, tid);
     store_stage<CIN, COUT>(wbuf + G::WST, wreg, tid);
     fetch_stage<CIN, COUT>(wg, 2, wreg, tid);
+    fetch_stage<CIN, COUT>(wg, 3 % NQ, wnext, tid);
     lds_barrier();
     FragsBf<G::MP, G::NBW> f0;                            // first k-step of the next stage
-    load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
+    load_kstep<CIN, COUT, 0, 0>(f0, hl, wl);
     for (int it = 0;; ++it) {                             // groups, uniform per block
         const int g = xr.first + it * xr.stride;
         if (g >= xr.end) break;
@@ -436,25 +470,27 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
                 const int q = pass * 9 + kpos;
                 __builtin_amdgcn_sched_barrier(0);            // keep each stage's work in its stage
                 // The matrix work on stage q (buffer q % 3 = kpos % 3, as 9
-                // divides the stages of a group); during it, stage q + 2 (in
-                // registers since stage q - 1) goes to buffer (q + 2) % 3,
-                // last read in stage q - 1, and stage q + 3 (wrapping into the
-                // next group) is fetched to registers; halo loads after the
-                // matrix ops of stages 1 and 3; then the first k-step of stage
-                // q + 1, whose buffer the previous barrier published, unless
-                // the pass ends here.  The barrier publishes stage q + 2 and
-                // frees stage q's buffer.
-                stage_mma<CIN, COUT, G::MP, G::NBW>(acc, f0, halos, wbuf + (kpos % 3) * G::WST, kpos, wm, half, lane,
-                                                    [&] {
+                // divides the stages of a group), which also reads the first
+                // k-step of stage q + 1 unless the pass ends here; during it,
+                // stage q + 2 (in registers since stage q - 2) goes to buffer
+                // (q + 2) % 3, last read in stage q - 1, and stage q + 4
+                // (wrapping into the next group) is fetched to registers;
+                // halo loads after the matrix ops of stages 1 and 3.  The
+                // barrier publishes stage q + 2 and frees stage q's buffer.
+                stage_mma<CIN, COUT, kpos, 0, G::MP, G::NBW>(acc, f0, hl, wl, [&] {
                     store_stage<CIN, COUT>(wbuf + ((kpos + 2) % 3) * G::WST, wreg, tid);
-                    fetch_stage<CIN, COUT>(wg, (q + 3) % NQ, wreg, tid);
+                    fetch_stage<CIN, COUT>(wg, (q + 4) % NQ, wreg, tid);
+#pragma unroll
+                    for (int j = 0; j < G::WPT; ++j) {                // wreg: stage q + 3, wnext: q + 4
+                        const u32x4 t = wreg[j];
+                        wreg[j] = wnext[j];
+                        wnext[j] = t;
+                    }
                 });
                 if constexpr (kpos == 1)
                     fetch_halos<CIN, COUT, VAR, 0, G::HPT / 2>(a, hitems, hvalid, hpass, hreg, hok, tid);
                 if constexpr (kpos == 3)
                     fetch_halos<CIN, COUT, VAR, G::HPT / 2, G::HPT>(a, hitems, hvalid, hpass, hreg, hok, tid);
-                if constexpr (kpos < 8)
-                    load_kstep<CIN, COUT>(f0, halos, wbuf + ((kpos + 1) % 3) * G::WST, kpos + 1, 0, wm, half, lane);
                 lds_barrier();
             };
             [&]<int... K>(std::integer_sequence<int, K...>) {
@@ -463,7 +499,7 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
             if (!last_pass) {
                 store_halos<CIN, COUT>(halos, hreg, hok, tid);    // every wave is past the pass's last read
                 lds_barrier();
-                load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
+                load_kstep<CIN, COUT, 0, 0>(f0, hl, wl);
             }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -516,7 +552,7 @@ __global__ __launch_bounds__(512) void k_conv_bf16_grp(ConvArgs a) {
             }
         }
         lds_barrier();
-        load_kstep<CIN, COUT>(f0, halos, wbuf, 0, 0, wm, half, lane);
+        load_kstep<CIN, COUT, 0, 0>(f0, hl, wl);
     }
 }
 

@@ -392,7 +392,7 @@ __global__ __launch_bounds__(NT) void k_masks(MaskGeom g, MaskArgs a) {
         if (threadIdx.x < RN_MAX_CONV + 2) s_cnt[threadIdx.x] = 0;
         int nc = 0;
         for (int w = threadIdx.x; w < HWW; w += blockDim.x) {
-            const int y = w / g.WW, wx = w - y * g.WW;
+            const int y = w / g.WW;
             uint64_t v = A[w];
             nc += __popcll(v);
             g.pmask[0][(size_t)slot * HWW + w] = v;
