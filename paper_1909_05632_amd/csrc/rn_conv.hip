@@ -758,14 +758,15 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
 // Weights too large for LDS: a block works on a group of 4 tiles (one per
 // wave, one wave per SIMD: the float32 matrix op issues at full rate from a
 // single wave) and streams the weights through LDS in stages of one kernel
-// position x SC input channels, double-buffered.  The weights of stage q + 2
-// are fetched into registers at the start of stage q and written to the free
-// buffer at the start of stage q + 1, so each load has a whole stage (4096
-// matrix cycles at 128 outputs and 64 channels) to arrive and the block
-// barrier that ends a stage only orders LDS.  Each wave fetches the halo of
-// its tile of the next group into registers in the group's last stage (every
-// load issued, out-of-image and absent ones from a fixed valid address and
-// dropped when stored) and writes it to its own halo area after its epilogue.
+// position x SC input channels, double-buffered.  The weights of stage q + 1
+// go straight from global memory into the free buffer at the start of stage q
+// (global_load_lds_dwordx4: no registers, no LDS store instructions), so each
+// load has a whole stage (4096 matrix cycles at 128 outputs and 64 channels)
+// to arrive; each wave waits for its own before the barrier that ends the
+// stage.  Each wave fetches the halo of its tile of the next group into
+// registers in the group's last stage (every load issued, out-of-image and
+// absent ones from a fixed valid address and dropped when stored) and writes
+// it to its own halo area after its epilogue.
 template <int CIN, int COUT>
 struct Staged {
     static constexpr int SC = (CIN > 64 && CIN % 64 == 0) ? 64 : CIN;   // channels per stage
@@ -778,26 +779,32 @@ struct Staged {
     static_assert(SC % 16 == 0, "whole 16-channel blocks per stage");
 };
 
+// Stage q's weights straight from global memory into the LDS buffer dst
+// (global_load_lds_dwordx4: lane i of a wave writes the 16 bytes at the
+// wave-uniform base + 16 i), the WPT loads of this thread in flight on return.
 template <int CIN, int COUT>
-__device__ inline void fetch_wstage(const float *wg, int q, floatx4 *regs, int tid) {
+__device__ inline void dma_wstage(const float *wg, int q, float *dst, int tid) {
     using S = Staged<CIN, COUT>;
+    static_assert((S::WST / 4) % 64 == 0, "whole waves of 16-byte loads");
     const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-    const floatx4 *src = reinterpret_cast<const floatx4 *>(wg + (size_t)kpos * CIN * COUT + (size_t)ch * S::WST);
+    const float *src = wg + (size_t)kpos * CIN * COUT + (size_t)ch * S::WST;
+    const int wbase = tid & ~63;
+    // LDS byte address of this wave's first destination (the low half of a
+    // generic pointer into LDS is its LDS offset), wave-uniform.
+    const uint32_t l0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(dst + 4 * wbase));
 #pragma unroll
-    for (int j = 0; j < S::WPT; ++j) {
-        const int e = tid + 256 * j;
-        if ((S::WST / 4) % 256 == 0 || e < S::WST / 4) regs[j] = src[e];
-    }
-}
-
-template <int CIN, int COUT>
-__device__ inline void store_wstage(float *dst, const floatx4 *regs, int tid) {
-    using S = Staged<CIN, COUT>;
-#pragma unroll
-    for (int j = 0; j < S::WPT; ++j) {
-        const int e = tid + 256 * j;
-        if ((S::WST / 4) % 256 == 0 || e < S::WST / 4) reinterpret_cast<floatx4 *>(dst)[e] = regs[j];
-    }
+    for (int j = 0; j < S::WPT; ++j)
+        if ((S::WST / 4) % 256 == 0 || wbase + 256 * j < S::WST / 4)    // uniform per wave
+        {
+            // Issued in assembly: the compiler would otherwise wait for these
+            // loads before every later LDS read; the caller waits for them.
+            // M0 (the LDS base of the instruction) is restored afterwards.
+            uint32_t saved;
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                         : "=&s"(saved)
+                         : "v"(src + 4 * (tid + 256 * j)), "s"(l0 + 4096u * j)
+                         : "memory");
+        }
 }
 
 // Halo of tile r into registers with every load issued; bit j of `ok` says
@@ -897,17 +904,15 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     const float *wg = static_cast<const float *>(a.w);
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
 
-    // Prologue: this wave's halo of group 0; stage 0 in LDS, stage 1 in flight.
+    // Prologue: this wave's halo of group 0; stage 0 in LDS.
     int t = xr.first + wave;
     uint32_t e_cur = t < xr.end ? item_word<DENSE>(a, t) : 0u;
-    floatx4 wreg[S::WPT];           // ext-vector arrays stay in registers
-    fetch_wstage<CIN, COUT>(wg, 0, wreg, tid);
+    dma_wstage<CIN, COUT>(wg, 0, wbuf, tid);
     floatx4 hreg[M::HV];
     uint32_t hok;
     fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_cur), t < xr.end, hreg, hok, lane);
     store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);
-    store_wstage<CIN, COUT>(wbuf, wreg, tid);
-    fetch_wstage<CIN, COUT>(wg, 1 % S::NQ, wreg, tid);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
 
     int buf = 0;
@@ -921,24 +926,26 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int q = 0; q < S::NQ; ++q) {
             // The stage's first operands (its weights are visible since the
-            // last barrier), then, while they arrive: stage q + 1 to the free
-            // buffer (its last reader finished before that barrier), stage
-            // q + 2 (wrapping into the next group) to registers and, in the
-            // last stage, the next group's halo; then the matrix work.  The
-            // halo loads are issued last in the group so that no weight wait
-            // of a later stage in this group has to drain them (the waits are
-            // counted in issue order); the epilogue runs before they are used.
+            // last barrier), then stage q + 1 (wrapping into the next group)
+            // straight into the free buffer (its last reader finished before
+            // that barrier) and, in the last stage, the next group's halo
+            // into registers; then the matrix work, and a wait for this
+            // wave's weight loads before the barrier publishes them (the
+            // halo loads, issued after them, stay in flight: the waits count
+            // in issue order).
             const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
             BlockOps<M::NB> first;
             stage_block<CIN, COUT>(first, halo, wbuf + buf * S::WST, kpos, ch, 0, lane);
-            store_wstage<CIN, COUT>(wbuf + (buf ^ 1) * S::WST, wreg, tid);
-            fetch_wstage<CIN, COUT>(wg, (q + 2) % S::NQ, wreg, tid);
-            if (q == S::NQ - 1) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
+            dma_wstage<CIN, COUT>(wg, (q + 1) % S::NQ, wbuf + (buf ^ 1) * S::WST, tid);
+            const bool last = q == S::NQ - 1;
+            if (last) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
             // Unconditional: a wave without a tile has an all-zero halo and
             // skips only the epilogue (a guarded call would make the compiler
             // copy every accumulator between register files each stage).
             mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane, first);
             buf ^= 1;
+            if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(M::HV) : "memory");
+            else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             lds_barrier();
         }
         if (valid) {
