@@ -755,56 +755,64 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     }
 }
 
-// Weights too large for LDS: a block works on a group of 4 tiles (one per
-// wave, one wave per SIMD: the float32 matrix op issues at full rate from a
-// single wave) and streams the weights through LDS in stages of one kernel
-// position x SC input channels, double-buffered.  The weights of stage q + 1
-// go straight from global memory into the free buffer at the start of stage q
-// (global_load_lds_dwordx4: no registers, no LDS store instructions), so each
-// load has a whole stage (4096 matrix cycles at 128 outputs and 64 channels)
-// to arrive; each wave waits for its own before the barrier that ends the
-// stage.  Each wave fetches the halo of its tile of the next group into
+// Weights too large for LDS: a block works on a group of 4 tiles and splits
+// the outputs, not the tiles, across its waves (one per SIMD: the float32
+// matrix op issues at full rate from a single wave): wave w computes output
+// channels [w COUT / 4, (w + 1) COUT / 4) of all 4 tiles.  The halos of the 4
+// tiles sit in LDS for the whole group (wave w fetches and stores tile w's);
+// each wave streams only its quarter of the weights through its own pair of
+// LDS buffers, in stages of one kernel position x SC input channels: stage
+// q + 1 goes straight from global memory into the free buffer at the start of
+// stage q (global_load_lds_dwordx4: no registers, no LDS store instructions)
+// and the wave waits for its own loads at the end of the stage.  No wave reads
+// another's weights, so the stages need no block barrier: two per group remain
+// (halos read by all waves before the epilogue reuses the LDS, halos of the
+// next group stored before its first stage).  Per 16-channel block a wave
+// reads 4 halo fragments and COUT / 64 weight fragments for 4 x COUT / 64 x 4
+// matrix ops.  Each wave fetches the halo of tile w of the next group into
 // registers in the group's last stage (every load issued, out-of-image and
-// absent ones from a fixed valid address and dropped when stored) and writes
-// it to its own halo area after its epilogue.
+// absent ones from a fixed valid address and dropped when stored).
 template <int CIN, int COUT>
 struct Staged {
     static constexpr int SC = (CIN > 64 && CIN % 64 == 0) ? 64 : CIN;   // channels per stage
     static constexpr int NCH = CIN / SC;             // stages per kernel position
     static constexpr int NQ = 9 * NCH;               // stages per group
     static constexpr int SB = SC / 16;               // 16-channel blocks per stage
-    static constexpr int WST = SC * COUT;            // floats per stage
-    static constexpr int WPT = (WST / 4 + 255) / 256;   // 16-byte weight loads per thread and stage
-    static constexpr size_t lds_bytes = (size_t)(2 * WST + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
-    static_assert(SC % 16 == 0, "whole 16-channel blocks per stage");
+    static constexpr int NBW = COUT / 64;            // 16-output blocks per wave
+    static constexpr int CW = 16 * NBW;              // output channels per wave
+    static constexpr int WSW = SC * CW;              // floats per stage and wave
+    static constexpr int WPW = WSW / 256;            // 1 KB wave loads per stage (16 bytes a lane)
+    static constexpr int SR = CW + 4;                // row stride of a tile's output staging (floats)
+    static constexpr size_t lds_bytes = (size_t)(4 * 2 * WSW + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
+    static_assert(COUT % 64 == 0 && SC % 16 == 0 && WSW % 256 == 0, "whole 16-output blocks and 1 KB loads per wave");
+    static_assert(4 * 16 * SR <= Mfma<CIN, COUT>::HALO, "a wave's output staging fits its halo area");
 };
 
-// Stage q's weights straight from global memory into the LDS buffer dst
-// (global_load_lds_dwordx4: lane i of a wave writes the 16 bytes at the
-// wave-uniform base + 16 i), the WPT loads of this thread in flight on return.
+// Stage q's weights for wave w (its CW output channels) straight from global
+// memory into the wave's LDS buffer dst, [block][n-block][lane][4]
+// (global_load_lds_dwordx4: lane i writes the 16 bytes at the wave-uniform
+// base + 16 i); the WPW loads are in flight on return.
 template <int CIN, int COUT>
-__device__ inline void dma_wstage(const float *wg, int q, float *dst, int tid) {
+__device__ inline void dma_wstage(const float *wg, int q, float *dst, int w, int lane) {
+    using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
-    static_assert((S::WST / 4) % 64 == 0, "whole waves of 16-byte loads");
     const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-    const float *src = wg + (size_t)kpos * CIN * COUT + (size_t)ch * S::WST;
-    const int wbase = tid & ~63;
-    // LDS byte address of this wave's first destination (the low half of a
-    // generic pointer into LDS is its LDS offset), wave-uniform.
-    const uint32_t l0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(dst + 4 * wbase));
+    // LDS byte address of dst (the low half of a generic pointer into LDS is
+    // its LDS offset), wave-uniform.
+    const uint32_t l0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
 #pragma unroll
-    for (int j = 0; j < S::WPT; ++j)
-        if ((S::WST / 4) % 256 == 0 || wbase + 256 * j < S::WST / 4)    // uniform per wave
-        {
-            // Issued in assembly: the compiler would otherwise wait for these
-            // loads before every later LDS read; the caller waits for them.
-            // M0 (the LDS base of the instruction) is restored afterwards.
-            uint32_t saved;
-            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-                         : "=&s"(saved)
-                         : "v"(src + 4 * (tid + 256 * j)), "s"(l0 + 4096u * j)
-                         : "memory");
-        }
+    for (int j = 0; j < S::WPW; ++j) {
+        const int b = j / S::NBW, nbw = j - b * S::NBW;
+        const float *src = wg + ((size_t)(kpos * M::NBLK + ch * S::SB + b) * M::NB + w * S::NBW + nbw) * 256 + 4 * lane;
+        // Issued in assembly: the compiler would otherwise wait for these
+        // loads before every later LDS read; the caller waits for them.  M0
+        // (the LDS base of the instruction) is restored afterwards.
+        uint32_t saved;
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                     : "=&s"(saved)
+                     : "v"(src), "s"(l0 + 1024u * j)
+                     : "memory");
+    }
 }
 
 // Halo of tile r into registers with every load issued; bit j of `ok` says
@@ -851,38 +859,63 @@ __device__ inline void store_halo_masked(float *halo, const floatx4 *regs, uint3
     }
 }
 
-// Operands of block b of a stage: A from the wave's halo (channels of block
-// ch * SB + b at kernel position kpos), B from the stage's weights in LDS,
-// [block][nb][lane][4].
-template <int CIN, int COUT>
-__device__ inline void stage_block(BlockOps<Mfma<CIN, COUT>::NB> &o, const float *halo, const float *s_w, int kpos,
-                                   int ch, int b, int lane) {
+// Operands of one 16-channel block: the A fragments of the 4 tiles and the B
+// fragments of the wave's NBW output blocks.
+template <int NBW>
+struct SplitOps {
+    float4 a[4];
+    float4 b[NBW];
+};
+
+// Block b of stage (kpos, ch): A from the 4 halos (channels of block
+// ch * SB + b at kernel position kpos), B from the wave's stage buffer.
+template <int CIN, int COUT, int NBW>
+__device__ inline void split_block(SplitOps<NBW> &o, const float *halos, const float *wst, int kpos, int ch, int b,
+                                   int lane) {
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
+    static_assert(NBW == S::NBW, "operand shape");
     const int mrow = lane & 15, kq = lane >> 4;
     const int pix = (mrow & 3) * 6 + (mrow >> 2);   // column-major pixel rows
     const int ky = kpos / 3, kx = kpos - ky * 3;
-    o.a = *reinterpret_cast<const float4 *>(halo + chunk_off<CIN, COUT>(pix + ky * 6 + kx, 4 * (ch * S::SB + b) + kq));
-    const float *wb = s_w + (size_t)b * 16 * COUT;
+    const int off = chunk_off<CIN, COUT>(pix + ky * 6 + kx, 4 * (ch * S::SB + b) + kq);
 #pragma unroll
-    for (int nb = 0; nb < M::NB; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + (nb * 64 + lane) * 4);
+    for (int t = 0; t < 4; ++t) o.a[t] = *reinterpret_cast<const float4 *>(halos + t * M::HALO + off);
+#pragma unroll
+    for (int nb = 0; nb < S::NBW; ++nb)
+        o.b[nb] = *reinterpret_cast<const float4 *>(wst + ((b * S::NBW + nb) * 64 + lane) * 4);
+}
+
+template <int NBW>
+__device__ inline void split_mma(floatx4 (&acc)[4][NBW], const SplitOps<NBW> &o) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const float av = j == 0 ? o.a[t].x : j == 1 ? o.a[t].y : j == 2 ? o.a[t].z : o.a[t].w;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                const float bv = j == 0 ? o.b[nb].x : j == 1 ? o.b[nb].y : j == 2 ? o.b[nb].z : o.b[nb].w;
+                acc[t][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t][nb], 0, 0, 0);
+            }
+        }
+    }
 }
 
 // acc += the stage's channels (blocks ch * SB .. + SB) at kernel position
-// kpos; `cur` holds block 0's operands on entry (the caller reads them
-// before its other LDS work of the stage), each later block's are read
+// kpos; `cur` holds block 0's operands on entry, each later block's are read
 // during the previous block's matrix ops.
-template <int CIN, int COUT>
-__device__ inline void mfma_stage(floatx4 *acc, const float *halo, const float *s_w, int kpos, int ch, int lane,
-                                  BlockOps<Mfma<CIN, COUT>::NB> &cur) {
-    using M = Mfma<CIN, COUT>;
+template <int CIN, int COUT, int NBW>
+__device__ inline void split_stage(floatx4 (&acc)[4][NBW], const float *halos, const float *wst, int kpos, int ch,
+                                   int lane, SplitOps<NBW> &cur) {
     using S = Staged<CIN, COUT>;
-    BlockOps<M::NB> nxt;
+    static_assert(NBW == S::NBW, "accumulator shape");
+    SplitOps<S::NBW> nxt;
 #pragma unroll
     for (int b = 0; b < S::SB; ++b) {
-        if (b + 1 < S::SB) stage_block<CIN, COUT>(nxt, halo, s_w, kpos, ch, b + 1, lane);
+        if (b + 1 < S::SB) split_block<CIN, COUT, S::NBW>(nxt, halos, wst, kpos, ch, b + 1, lane);
         __builtin_amdgcn_sched_barrier(0);
-        mma_block<CIN, COUT>(acc, cur, 0);
+        split_mma<S::NBW>(acc, cur);
         __builtin_amdgcn_sched_barrier(0);
         cur = nxt;
     }
@@ -895,66 +928,99 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     static_assert(M::TAIL == 0, "staged layers take whole 16-channel blocks");
     extern __shared__ float smem[];
     __shared__ float s_bias[COUT];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int cnt = work_count<DENSE>(a);
     const XcdRange xr = xcd_range(cnt, 4);
     if (xr.first >= xr.end) return;                       // uniform per block
-    float *wbuf = smem;                                   // two stages
-    float *halo = smem + 2 * S::WST + wave * M::HALO;
+    float *halos = smem;                                  // tile t's halo at t * HALO
+    float *wbuf = smem + 4 * M::HALO + wave * 2 * S::WSW; // this wave's two stage buffers
+    float *myhalo = halos + wave * M::HALO;               // tile `wave`'s halo; the wave's output staging
     const float *wg = static_cast<const float *>(a.w);
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
+    const int mrow = lane & 15, kq = lane >> 4;
 
-    // Prologue: this wave's halo of group 0; stage 0 in LDS.
+    // Prologue: tile `wave`'s halo of group 0; the wave's stage 0 in LDS.
     int t = xr.first + wave;
-    uint32_t e_cur = t < xr.end ? item_word<DENSE>(a, t) : 0u;
-    dma_wstage<CIN, COUT>(wg, 0, wbuf, tid);
+    uint32_t e_mine = t < xr.end ? item_word<DENSE>(a, t) : 0u;
+    dma_wstage<CIN, COUT>(wg, 0, wbuf, wave, lane);
     floatx4 hreg[M::HV];
     uint32_t hok;
-    fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_cur), t < xr.end, hreg, hok, lane);
-    store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);
+    fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_mine), t < xr.end, hreg, hok, lane);
+    store_halo_masked<CIN, COUT>(myhalo, hreg, hok, lane);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
 
     int buf = 0;
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        t = g + wave;
-        const bool valid = t < xr.end;
-        const int tn = t + xr.stride;
+        const int tn = g + xr.stride + wave;
         const uint32_t e_nxt = tn < xr.end ? item_word<DENSE>(a, tn) : 0u;
-        floatx4 acc[M::NB];
+        uint32_t e_grp[4];                                // the group's items, for the epilogue
 #pragma unroll
-        for (int nb = 0; nb < M::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int tt = 0; tt < 4; ++tt) e_grp[tt] = g + tt < xr.end ? item_word<DENSE>(a, g + tt) : 0u;
+        floatx4 acc[4][S::NBW];
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int nb = 0; nb < S::NBW; ++nb) acc[tt][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int q = 0; q < S::NQ; ++q) {
-            // The stage's first operands (its weights are visible since the
-            // last barrier), then stage q + 1 (wrapping into the next group)
-            // straight into the free buffer (its last reader finished before
-            // that barrier) and, in the last stage, the next group's halo
-            // into registers; then the matrix work, and a wait for this
-            // wave's weight loads before the barrier publishes them (the
-            // halo loads, issued after them, stay in flight: the waits count
-            // in issue order).
+            // The stage's first operands, then stage q + 1 (wrapping into the
+            // next group) straight into the wave's other buffer (its last
+            // reads, of stage q - 1, fed matrix ops that have issued) and,
+            // in the last stage, the next group's halo of tile `wave` into
+            // registers; then the matrix work and the wait for the weight
+            // loads (the halo loads, issued after them, stay in flight: the
+            // waits count in issue order).
             const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-            BlockOps<M::NB> first;
-            stage_block<CIN, COUT>(first, halo, wbuf + buf * S::WST, kpos, ch, 0, lane);
-            dma_wstage<CIN, COUT>(wg, (q + 1) % S::NQ, wbuf + (buf ^ 1) * S::WST, tid);
+            const float *wst = wbuf + buf * S::WSW;
+            SplitOps<S::NBW> first;
+            split_block<CIN, COUT, S::NBW>(first, halos, wst, kpos, ch, 0, lane);
+            dma_wstage<CIN, COUT>(wg, (q + 1) % S::NQ, wbuf + (buf ^ 1) * S::WSW, wave, lane);
             const bool last = q == S::NQ - 1;
             if (last) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
-            // Unconditional: a wave without a tile has an all-zero halo and
-            // skips only the epilogue (a guarded call would make the compiler
-            // copy every accumulator between register files each stage).
-            mfma_stage<CIN, COUT>(acc, halo, wbuf + buf * S::WST, kpos, ch, lane, first);
+            split_stage<CIN, COUT, S::NBW>(acc, halos, wst, kpos, ch, lane, first);
             buf ^= 1;
             if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(M::HV) : "memory");
             else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            lds_barrier();
         }
-        if (valid) {
+        lds_barrier();                                    // every wave is past its last halo read
+        // Epilogue, tile by tile: bias, ReLU and the zero outside the image on
+        // the bit patterns (a float above zero has a positive int pattern),
+        // staged through LDS rows of the wave's CW channels, then stored 16
+        // bytes a lane.
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            const int it = g + tt;
+            if (it >= xr.end) break;                      // uniform
+            const TileRef r = item_ref(a, e_grp[tt]);
+            const int col_keep = ~((a.W - 1 - (r.tx * kTile + kq)) >> 31);
+            float *stg = myhalo + tt * 16 * S::SR;
+#pragma unroll
+            for (int nb = 0; nb < S::NBW; ++nb) {
+                const float bb = s_bias[(wave * S::NBW + nb) * 16 + mrow];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int keep = col_keep & ~((a.H - 1 - (r.ty * kTile + i)) >> 31);
+                    stg[(i * 4 + kq) * S::SR + nb * 16 + mrow] =
+                        __int_as_float(max(__float_as_int(acc[tt][nb][i] + bb), 0) & keep);
+                }
+            }
             wave_sync();
-            epilogue<COUT, -1, VAR>(a, item_ref(a, e_cur), acc, s_bias, halo, lane, t);
+            float *dst = VAR ? static_cast<float *>(a.vov_out) + (size_t)it * kTilePx * COUT
+                             : static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride + (size_t)r.tile * kTilePx * COUT;
+            if (!VAR || a.vov_out != nullptr) {
+#pragma unroll
+                for (int j = 0; j < S::CW / 16; ++j) {    // 16 x CW / 4 float4 = 64 x CW / 16
+                    const int o4 = lane + 64 * j;
+                    const int m = (4 * o4) / S::CW, n = 4 * o4 - m * S::CW;
+                    *reinterpret_cast<float4 *>(dst + m * COUT + wave * S::CW + n) =
+                        *reinterpret_cast<const float4 *>(stg + m * S::SR + n);
+                }
+            }
         }
-        store_halo_masked<CIN, COUT>(halo, hreg, hok, lane);      // this wave's own area
-        wave_sync();
-        e_cur = e_nxt;
+        wave_sync();                                      // staging reads done before the halo store
+        store_halo_masked<CIN, COUT>(myhalo, hreg, hok, lane);
+        lds_barrier();                                    // the next group's halos visible to every wave
     }
 }
 
@@ -1218,7 +1284,7 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         if (a.fuse_first) return run_resident<CIN, COUT, DENSE, true, VAR>(a, cus, s);
         return run_resident<CIN, COUT, DENSE, false, VAR>(a, cus, s);
     } else {
-        if (a.fuse_first) return hipErrorInvalidValue;
+        if (a.fuse_first || a.n_out > 0) return hipErrorInvalidValue;   // head partials come from their own kernel
         constexpr size_t lds = Staged<CIN, COUT>::lds_bytes;
         static_assert(lds <= kLdsBudget, "staged layer exceeds LDS");
         auto kern = k_conv_mfma_staged<CIN, COUT, DENSE, VAR>;
@@ -1244,7 +1310,7 @@ hipError_t run_first(const ConvArgs &a, int cus, hipStream_t s) {
     return hipGetLastError();
 }
 
-#define RN_MFMA_SHAPES(X) X(40, 80) X(80, 160) X(64, 128) X(128, 128)
+#define RN_MFMA_SHAPES(X) X(40, 80) X(64, 128) X(128, 128)
 // General layers: (k, stride, cin, cout); first layers read the input frames.
 #define RN_GEN_FIRST_SHAPES(X) X(8, 4, 4, 32) X(8, 4, 1, 32) X(5, 1, 1, 32) X(7, 2, 1, 32) X(5, 2, 4, 32)
 #define RN_GEN_SHAPES(X) X(4, 2, 32, 64) X(3, 1, 64, 64) X(3, 1, 32, 64) X(3, 2, 32, 64) X(5, 2, 32, 64) X(5, 1, 32, 32)

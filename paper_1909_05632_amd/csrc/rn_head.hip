@@ -467,8 +467,9 @@ __global__ __launch_bounds__(256) void k_tile_part_bf16(ConvArgs a) {
 // the n_out real logits (lanes of padding columns take zeros without a load).
 // Rows, one pass per distinct position, K quarters per wave and their sum in
 // wave order as in k_tile_part_bf16, so list and dense passes agree bit for
-// bit.
-template <int C, int NBO, bool DENSE>
+// bit.  VAR: variant work items, as in k_tile_part_bf16 (activations from the
+// item's overlay row, partials to the same row of the variant partials).
+template <int C, int NBO, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
     constexpr int KBL = C;                    // 16-deep K blocks per tile (16 C / 16)
     constexpr int KW = KBL / 4;               // blocks per wave
@@ -503,7 +504,9 @@ __global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
             e[rg] = valid ? item_word<DENSE>(a, it) : 0u;
             const TileRef r = item_ref(a, e[rg]);
             pos[rg] = valid ? r.tile : -1;
-            arow[rg] = act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C + 4 * kq + 16 * KW * wave;
+            arow[rg] = (VAR ? static_cast<const float *>(a.vov_in) + (size_t)it * kTilePx * C
+                            : act + (size_t)r.slot * a.in_stride + (size_t)r.tile * kTilePx * C) +
+                       4 * kq + 16 * KW * wave;
         }
         if (tid < 64) {
             const int t2 = g + tid;
@@ -573,7 +576,9 @@ __global__ __launch_bounds__(256) void k_tile_part_f32(ConvArgs a) {
                         const uint32_t eq = __shfl(ew, q, 64);   // lane q holds row q's item
                         if (o < a.n_out && ((gmask >> q) & 1)) {
                             const TileRef rq = item_ref(a, eq);
-                            a.hpart[((size_t)rq.slot * ntiles + rq.tile) * a.n_out + o] = v[i];
+                            float *hp = VAR ? a.vhpart + (size_t)(g + 16 * wave + q) * a.n_out
+                                            : a.hpart + ((size_t)rq.slot * ntiles + rq.tile) * a.n_out;
+                            hp[o] = v[i];
                         }
                     }
                 }
@@ -667,21 +672,23 @@ hipError_t launch_tile_part_bf16(const ConvArgs &a, int cus, hipStream_t s, bool
     return hipErrorInvalidValue;
 }
 
-template <int C, bool DENSE>
+template <int C, bool DENSE, bool VAR>
 hipError_t run_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s) {
     const int grid = dev::persistent_grid(cus * 2, (a.max_tiles + 63) / 64);
-    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_f32<C, 1, DENSE>), dim3(grid), dim3(256), 0, s, a);
-    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_f32<C, 2, DENSE>), dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_tile_part_f32<C, 4, DENSE>), dim3(grid), dim3(256), 0, s, a);
+    if (a.n_out <= 16) hipLaunchKernelGGL((k_tile_part_f32<C, 1, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    else if (a.n_out <= 32) hipLaunchKernelGGL((k_tile_part_f32<C, 2, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_tile_part_f32<C, 4, DENSE, VAR>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-bool tile_part_f32_supported(int C) { return C == 128 || C == 160; }
+bool tile_part_f32_supported(int C) { return C == 128; }
 
-hipError_t launch_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s) {
+hipError_t launch_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s, bool var) {
     const bool dense = a.wl == nullptr;
-    if (a.cout == 128) return dense ? run_tile_part_f32<128, true>(a, cus, s) : run_tile_part_f32<128, false>(a, cus, s);
-    if (a.cout == 160) return dense ? run_tile_part_f32<160, true>(a, cus, s) : run_tile_part_f32<160, false>(a, cus, s);
+    if (var && dense) return hipErrorInvalidValue;
+    if (a.cout == 128)
+        return var ? run_tile_part_f32<128, false, true>(a, cus, s)
+                   : dense ? run_tile_part_f32<128, true, false>(a, cus, s) : run_tile_part_f32<128, false, false>(a, cus, s);
     return hipErrorInvalidValue;
 }
 

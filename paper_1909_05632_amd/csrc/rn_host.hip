@@ -237,7 +237,9 @@ rn_status plan_config(const rn_config *cfg, Plan *p, std::string *err) {
     p->o_cnt = take((RN_MAX_CONV + 1) * 4);
     const bool tiles_head = p->head_mode == RN_HEAD_TILES;
     p->o_part = take(tiles_head ? 0 : p->part_elems * 4);
-    p->o_hw = take(!tiles_head ? 0
+    // Epilogue head weights: float32 last layers whose conv kernel forms the
+    // tile partials (a staged last layer leaves them to k_tile_part_f32, o_hw2).
+    p->o_hw = take(!tiles_head || p->part_f32 ? 0
                    : p->dt == RN_BF16 ? tile_part_bf16_elems(p->ntl[p->L], p->C[p->L], p->N) * 2
                                       : tile_head_w_elems(p->ntl[p->L], p->C[p->L], p->N) * 4);
     p->o_hw2 = take(p->part_f32 ? tile_part_f32_elems(p->ntl[p->L], p->C[p->L], p->N) * 4 : 0);
@@ -259,8 +261,9 @@ struct VarPlan {
 };
 
 // Layer l's recomputed tiles are read back by layer l + 1 (unless layer 1 is
-// folded into layer 2) or, bf16 last layer, by the head-partial kernel; a
-// float32 last layer feeds the head from its epilogue and stores nothing.
+// folded into layer 2) or, bf16 or staged float32 last layer, by the
+// head-partial kernel; another float32 last layer feeds the head from its
+// epilogue and stores nothing.
 VarPlan plan_variants(const Plan &p, int n, int max_tiles) {
     VarPlan v;
     v.n = n;
@@ -284,7 +287,7 @@ VarPlan plan_variants(const Plan &p, int n, int max_tiles) {
         v.o_wl[l] = take(v.cap * 4);
         v.o_map[l] = take((size_t)n * p.ntiles * 4);
         v.o_bits[l] = take((size_t)p.ntiles * nch * 8);
-        v.has_ov[l] = l < p.L ? !(l == 1 && p.fuse_first) : p.dt == RN_BF16;
+        v.has_ov[l] = l < p.L ? !(l == 1 && p.fuse_first) : p.dt == RN_BF16 || p.part_f32;
         v.o_ov[l] = take(v.has_ov[l] ? v.cap * kTilePx * p.C[l] * p.esz : 0);
     }
     v.o_pcnt = take((size_t)p.L * p.ntiles * 4);
@@ -717,7 +720,7 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
             cv.hw = net->at<float>(p.o_hw);
             cv.vhpart = static_cast<float *>(at(vp.o_hp));
             last = cv;
-            if (bf) cv.n_out = 0;
+            if (bf || p.part_f32) cv.n_out = 0;
         }
         if (l == 1)
             e = timed(net, RN_PHASE_CONV1, s, [&] {
@@ -729,9 +732,12 @@ rn_status run_variants(reuse_net *net, int32_t base, int32_t n, const void *fram
             }, l);
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("conv kernels: ") + hipGetErrorString(e));
     }
-    if (bf) {
+    if (bf || p.part_f32) {
         last.vov_in = at(vp.o_ov[p.L]);
-        e = timed(net, RN_PHASE_HEAD, s, [&] { return launch_tile_part_bf16(last, net->cus, s, true); });
+        if (p.part_f32) last.hw = net->at<float>(p.o_hw2);
+        e = timed(net, RN_PHASE_HEAD, s, [&] {
+            return p.part_f32 ? launch_tile_part_f32(last, net->cus, s, true) : launch_tile_part_bf16(last, net->cus, s, true);
+        });
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("head partials: ") + hipGetErrorString(e));
     }
     TileHeadArgs ta{};
@@ -863,7 +869,7 @@ hipError_t upload_weights(reuse_net *net, const rn_weights *w, hipStream_t s) {
         hwb.assign(tile_part_bf16_elems(p.ntl[p.L], CL, p.N), 0);
         pack_tile_part_bf16(w->dense_w, p.N, CL, HL, WL, THL, TWL, hwb.data());
         up(p.o_hw, hwb.data(), hwb.size() * 2);
-    } else if (p.head_mode == RN_HEAD_TILES) {
+    } else if (p.head_mode == RN_HEAD_TILES && !p.part_f32) {
         hw.assign(tile_head_w_elems(p.ntl[p.L], CL, p.N), 0.f);
         pack_tile_head(w->dense_w, p.N, CL, HL, WL, THL, TWL, hw.data());
         for (float &v : hw) v = rnd(v);
@@ -1237,7 +1243,8 @@ rn_status reuse_net_sgd_step(reuse_net *net, const float *grads, float lr, void 
         if (l > 0) upd(p.o_wt[l], p.wt_elems[l], SGD_DX, grads + gl.w[l], p.C[l], p.C[l + 1]);
     }
     upd(p.o_wd, (size_t)p.N * p.K, SGD_DENSE, grads + gl.dw, 0, 0);
-    if (p.head_mode == RN_HEAD_TILES) upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, grads + gl.dw, 0, 0);
+    if (p.head_mode == RN_HEAD_TILES && !p.part_f32)
+        upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, grads + gl.dw, 0, 0);
     if (p.part_f32) upd(p.o_hw2, tile_part_f32_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_PART, grads + gl.dw, 0, 0);
     upd(p.o_bd, p.N, SGD_PLAIN, grads + gl.db, 0, 0);
     // Every cache now holds activations of the old weights: all slots unprimed.

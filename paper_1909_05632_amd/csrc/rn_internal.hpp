@@ -238,7 +238,7 @@ bool conv_mfma_is_staged(int cin, int cout);
 bool tile_part_f32_supported(int C);
 size_t tile_part_f32_elems(int ntiles, int C, int n_out);
 void pack_tile_part_f32(const float *dense_w, int n_out, int C, int H, int W, int TH, int TW, float *dst);
-hipError_t launch_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s);
+hipError_t launch_tile_part_f32(const ConvArgs &a, int cus, hipStream_t s, bool var = false);
 hipError_t launch_head(const HeadArgs &a, rn_dtype dt, hipStream_t s);
 int head_streams_per_block(int n_out);
 
