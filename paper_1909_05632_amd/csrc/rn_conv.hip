@@ -963,6 +963,10 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
             for (int nb = 0; nb < S::NBW; ++nb) acc[tt][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // Three stages per loop iteration where the group has 18: rolled one
+        // stage at a time the compiler permutes the accumulator registers
+        // within an iteration and moves them back at its end.
+#pragma unroll(S::NQ == 18 ? 3 : 1)
         for (int q = 0; q < S::NQ; ++q) {
             // The stage's first operands, then stage q + 1 (wrapping into the
             // next group) straight into the wave's other buffer (its last
