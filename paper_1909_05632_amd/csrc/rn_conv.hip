@@ -755,11 +755,13 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
     }
 }
 
-// Weights too large for LDS: a block works on a group of 4 tiles and splits
-// the outputs, not the tiles, across its waves (one per SIMD: the float32
-// matrix op issues at full rate from a single wave): wave w computes output
-// channels [w COUT / 4, (w + 1) COUT / 4) of all 4 tiles.  The halos of the 4
-// tiles sit in LDS for the whole group (wave w fetches and stores tile w's);
+// Weights too large for LDS: a block works on a group of T tiles (8 for 64
+// input channels, 4 for 128: the halos that fit next to the weights) and
+// splits the outputs, not the tiles, across its waves (one per SIMD: the
+// float32 matrix op issues at full rate from a single wave): wave w computes
+// output channels [w COUT / 4, (w + 1) COUT / 4) of all T tiles.  The halos of
+// the T tiles sit in LDS for the whole group (wave w fetches and stores those
+// of tiles w, w + 4, ...);
 // each wave streams only its quarter of the weights through its own pair of
 // LDS buffers, in stages of one kernel position x SC input channels: stage
 // q + 1 goes straight from global memory into the free buffer at the start of
@@ -768,10 +770,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_conv_mfma_res(ConvArgs a) {
 // another's weights, so the stages need no block barrier: two per group remain
 // (halos read by all waves before the epilogue reuses the LDS, halos of the
 // next group stored before its first stage).  Per 16-channel block a wave
-// reads 4 halo fragments and COUT / 64 weight fragments for 4 x COUT / 64 x 4
-// matrix ops.  Each wave fetches the halo of tile w of the next group into
-// registers in the group's last stage (every load issued, out-of-image and
-// absent ones from a fixed valid address and dropped when stored).
+// reads T halo fragments and COUT / 64 weight fragments for T x COUT / 64 x 4
+// matrix ops.  Each wave fetches its halos of the next group into registers
+// in the group's last stage (every load issued, out-of-image and absent ones
+// from a fixed valid address and dropped when stored).
 template <int CIN, int COUT>
 struct Staged {
     static constexpr int SC = (CIN > 64 && CIN % 64 == 0) ? 64 : CIN;   // channels per stage
@@ -783,9 +785,11 @@ struct Staged {
     static constexpr int WSW = SC * CW;              // floats per stage and wave
     static constexpr int WPW = WSW / 256;            // 1 KB wave loads per stage (16 bytes a lane)
     static constexpr int SR = CW + 4;                // row stride of a tile's output staging (floats)
-    static constexpr size_t lds_bytes = (size_t)(4 * 2 * WSW + 4 * Mfma<CIN, COUT>::HALO) * sizeof(float);
+    static constexpr int T = CIN <= 64 ? 8 : 4;      // tiles per group
+    static constexpr int TW = T / 4;                 // halos fetched per wave
+    static constexpr size_t lds_bytes = (size_t)(4 * 2 * WSW + T * Mfma<CIN, COUT>::HALO) * sizeof(float);
     static_assert(COUT % 64 == 0 && SC % 16 == 0 && WSW % 256 == 0, "whole 16-output blocks and 1 KB loads per wave");
-    static_assert(4 * 16 * SR <= Mfma<CIN, COUT>::HALO, "a wave's output staging fits its halo area");
+    static_assert(4 * 16 * SR <= Mfma<CIN, COUT>::HALO, "four tiles' output staging fit one halo area");
 };
 
 // Stage q's weights for wave w (its CW output channels) straight from global
@@ -859,39 +863,39 @@ __device__ inline void store_halo_masked(float *halo, const floatx4 *regs, uint3
     }
 }
 
-// Operands of one 16-channel block: the A fragments of the 4 tiles and the B
+// Operands of one 16-channel block: the A fragments of the T tiles and the B
 // fragments of the wave's NBW output blocks.
-template <int NBW>
+template <int T, int NBW>
 struct SplitOps {
-    float4 a[4];
+    float4 a[T];
     float4 b[NBW];
 };
 
-// Block b of stage (kpos, ch): A from the 4 halos (channels of block
+// Block b of stage (kpos, ch): A from the T halos (channels of block
 // ch * SB + b at kernel position kpos), B from the wave's stage buffer.
-template <int CIN, int COUT, int NBW>
-__device__ inline void split_block(SplitOps<NBW> &o, const float *halos, const float *wst, int kpos, int ch, int b,
+template <int CIN, int COUT, int T, int NBW>
+__device__ inline void split_block(SplitOps<T, NBW> &o, const float *halos, const float *wst, int kpos, int ch, int b,
                                    int lane) {
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
-    static_assert(NBW == S::NBW, "operand shape");
+    static_assert(T == S::T && NBW == S::NBW, "operand shape");
     const int mrow = lane & 15, kq = lane >> 4;
     const int pix = (mrow & 3) * 6 + (mrow >> 2);   // column-major pixel rows
     const int ky = kpos / 3, kx = kpos - ky * 3;
     const int off = chunk_off<CIN, COUT>(pix + ky * 6 + kx, 4 * (ch * S::SB + b) + kq);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) o.a[t] = *reinterpret_cast<const float4 *>(halos + t * M::HALO + off);
+    for (int t = 0; t < T; ++t) o.a[t] = *reinterpret_cast<const float4 *>(halos + t * M::HALO + off);
 #pragma unroll
     for (int nb = 0; nb < S::NBW; ++nb)
         o.b[nb] = *reinterpret_cast<const float4 *>(wst + ((b * S::NBW + nb) * 64 + lane) * 4);
 }
 
-template <int NBW>
-__device__ inline void split_mma(floatx4 (&acc)[4][NBW], const SplitOps<NBW> &o) {
+template <int T, int NBW>
+__device__ inline void split_mma(floatx4 (&acc)[T][NBW], const SplitOps<T, NBW> &o) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < T; ++t) {
             const float av = j == 0 ? o.a[t].x : j == 1 ? o.a[t].y : j == 2 ? o.a[t].z : o.a[t].w;
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) {
@@ -905,17 +909,17 @@ __device__ inline void split_mma(floatx4 (&acc)[4][NBW], const SplitOps<NBW> &o)
 // acc += the stage's channels (blocks ch * SB .. + SB) at kernel position
 // kpos; `cur` holds block 0's operands on entry, each later block's are read
 // during the previous block's matrix ops.
-template <int CIN, int COUT, int NBW>
-__device__ inline void split_stage(floatx4 (&acc)[4][NBW], const float *halos, const float *wst, int kpos, int ch,
-                                   int lane, SplitOps<NBW> &cur) {
+template <int CIN, int COUT, int T, int NBW>
+__device__ inline void split_stage(floatx4 (&acc)[T][NBW], const float *halos, const float *wst, int kpos, int ch,
+                                   int lane, SplitOps<T, NBW> &cur) {
     using S = Staged<CIN, COUT>;
-    static_assert(NBW == S::NBW, "accumulator shape");
-    SplitOps<S::NBW> nxt;
+    static_assert(T == S::T && NBW == S::NBW, "accumulator shape");
+    SplitOps<T, NBW> nxt;
 #pragma unroll
     for (int b = 0; b < S::SB; ++b) {
-        if (b + 1 < S::SB) split_block<CIN, COUT, S::NBW>(nxt, halos, wst, kpos, ch, b + 1, lane);
+        if (b + 1 < S::SB) split_block<CIN, COUT, T, NBW>(nxt, halos, wst, kpos, ch, b + 1, lane);
         __builtin_amdgcn_sched_barrier(0);
-        split_mma<S::NBW>(acc, cur);
+        split_mma<T, NBW>(acc, cur);
         __builtin_amdgcn_sched_barrier(0);
         cur = nxt;
     }
@@ -931,60 +935,75 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int cnt = work_count<DENSE>(a);
-    const XcdRange xr = xcd_range(cnt, 4);
+    constexpr int T = S::T;
+    const XcdRange xr = xcd_range(cnt, T);
     if (xr.first >= xr.end) return;                       // uniform per block
     float *halos = smem;                                  // tile t's halo at t * HALO
-    float *wbuf = smem + 4 * M::HALO + wave * 2 * S::WSW; // this wave's two stage buffers
-    float *myhalo = halos + wave * M::HALO;               // tile `wave`'s halo; the wave's output staging
+    float *wbuf = smem + T * M::HALO + wave * 2 * S::WSW; // this wave's two stage buffers
     const float *wg = static_cast<const float *>(a.w);
     for (int j = tid; j < COUT; j += blockDim.x) s_bias[j] = a.bias[j];
     const int mrow = lane & 15, kq = lane >> 4;
 
-    // Prologue: tile `wave`'s halo of group 0; the wave's stage 0 in LDS.
-    int t = xr.first + wave;
-    uint32_t e_mine = t < xr.end ? item_word<DENSE>(a, t) : 0u;
+    // Prologue: the wave's halos (tiles wave + 4 h) of group 0; its stage 0 in LDS.
     dma_wstage<CIN, COUT>(wg, 0, wbuf, wave, lane);
-    floatx4 hreg[M::HV];
-    uint32_t hok;
-    fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_mine), t < xr.end, hreg, hok, lane);
-    store_halo_masked<CIN, COUT>(myhalo, hreg, hok, lane);
+    floatx4 hreg[S::TW][M::HV];
+    uint32_t hok[S::TW];
+#pragma unroll
+    for (int h = 0; h < S::TW; ++h) {
+        const int t = xr.first + wave + 4 * h;
+        const uint32_t e = t < xr.end ? item_word<DENSE>(a, t) : 0u;
+        fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e), t < xr.end, hreg[h], hok[h], lane);
+    }
+#pragma unroll
+    for (int h = 0; h < S::TW; ++h) store_halo_masked<CIN, COUT>(halos + (wave + 4 * h) * M::HALO, hreg[h], hok[h], lane);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
 
     int buf = 0;
     for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
-        const int tn = g + xr.stride + wave;
-        const uint32_t e_nxt = tn < xr.end ? item_word<DENSE>(a, tn) : 0u;
-        uint32_t e_grp[4];                                // the group's items, for the epilogue
+        uint32_t e_nxt[S::TW];                            // the wave's items of the next group
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt) e_grp[tt] = g + tt < xr.end ? item_word<DENSE>(a, g + tt) : 0u;
-        floatx4 acc[4][S::NBW];
+        for (int h = 0; h < S::TW; ++h) {
+            const int tn = g + xr.stride + wave + 4 * h;
+            e_nxt[h] = tn < xr.end ? item_word<DENSE>(a, tn) : 0u;
+        }
+        uint32_t e_grp[T];                                // the group's items, for the epilogue
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
+        for (int tt = 0; tt < T; ++tt) e_grp[tt] = g + tt < xr.end ? item_word<DENSE>(a, g + tt) : 0u;
+        floatx4 acc[T][S::NBW];
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
 #pragma unroll
             for (int nb = 0; nb < S::NBW; ++nb) acc[tt][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
         // Three stages per loop iteration where the group has 18: rolled one
         // stage at a time the compiler permutes the accumulator registers
         // within an iteration and moves them back at its end.
-#pragma unroll(S::NQ == 18 ? 3 : 1)
+        constexpr int QU = S::NQ == 18 ? 3 : 1;
+#pragma unroll QU
         for (int q = 0; q < S::NQ; ++q) {
             // The stage's first operands, then stage q + 1 (wrapping into the
             // next group) straight into the wave's other buffer (its last
             // reads, of stage q - 1, fed matrix ops that have issued) and,
-            // in the last stage, the next group's halo of tile `wave` into
+            // in the last stage, the wave's halos of the next group into
             // registers; then the matrix work and the wait for the weight
             // loads (the halo loads, issued after them, stay in flight: the
             // waits count in issue order).
             const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
             const float *wst = wbuf + buf * S::WSW;
-            SplitOps<S::NBW> first;
-            split_block<CIN, COUT, S::NBW>(first, halos, wst, kpos, ch, 0, lane);
+            SplitOps<T, S::NBW> first;
+            split_block<CIN, COUT, T, S::NBW>(first, halos, wst, kpos, ch, 0, lane);
             dma_wstage<CIN, COUT>(wg, (q + 1) % S::NQ, wbuf + (buf ^ 1) * S::WSW, wave, lane);
             const bool last = q == S::NQ - 1;
-            if (last) fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt), tn < xr.end, hreg, hok, lane);
-            split_stage<CIN, COUT, S::NBW>(acc, halos, wst, kpos, ch, lane, first);
+            if (last) {
+#pragma unroll
+                for (int h = 0; h < S::TW; ++h) {
+                    const int tn = g + xr.stride + wave + 4 * h;
+                    fetch_halo_all<CIN, COUT, VAR>(a, item_ref(a, e_nxt[h]), tn < xr.end, hreg[h], hok[h], lane);
+                }
+            }
+            split_stage<CIN, COUT, T, S::NBW>(acc, halos, wst, kpos, ch, lane, first);
             buf ^= 1;
-            if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(M::HV) : "memory");
+            if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(S::TW * M::HV) : "memory");
             else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
         lds_barrier();                                    // every wave is past its last halo read
@@ -993,12 +1012,13 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
         // staged through LDS rows of the wave's CW channels, then stored 16
         // bytes a lane.
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
+        for (int tt = 0; tt < T; ++tt) {
             const int it = g + tt;
             if (it >= xr.end) break;                      // uniform
             const TileRef r = item_ref(a, e_grp[tt]);
             const int col_keep = ~((a.W - 1 - (r.tx * kTile + kq)) >> 31);
-            float *stg = myhalo + tt * 16 * S::SR;
+            // staging: the wave's own halo areas (tiles wave + 4 h), four tiles each
+            float *stg = halos + (wave + 4 * (tt / 4)) * M::HALO + (tt % 4) * 16 * S::SR;
 #pragma unroll
             for (int nb = 0; nb < S::NBW; ++nb) {
                 const float bb = s_bias[(wave * S::NBW + nb) * 16 + mrow];
@@ -1023,7 +1043,8 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
             }
         }
         wave_sync();                                      // staging reads done before the halo store
-        store_halo_masked<CIN, COUT>(myhalo, hreg, hok, lane);
+#pragma unroll
+        for (int h = 0; h < S::TW; ++h) store_halo_masked<CIN, COUT>(halos + (wave + 4 * h) * M::HALO, hreg[h], hok[h], lane);
         lds_barrier();                                    // the next group's halos visible to every wave
     }
 }
@@ -1294,7 +1315,7 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         auto kern = k_conv_mfma_staged<CIN, COUT, DENSE, VAR>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;
-        const int grid = persistent_grid(cus, (a.max_tiles + 3) / 4);
+        const int grid = persistent_grid(cus, (a.max_tiles + Staged<CIN, COUT>::T - 1) / Staged<CIN, COUT>::T);
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, a);
     }
     return hipGetLastError();
