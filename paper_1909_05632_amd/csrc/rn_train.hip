@@ -395,6 +395,185 @@ __global__ __launch_bounds__(256) void k_bwd_dw(BwdArgs a) {
     }
 }
 
+// dW for layers 2..L (a_{l-1} a tiled cache), operands read 16 bytes at a
+// time.  The K index of the product is the tile's pixel: in 4 consecutive
+// k-steps lane group kq takes k = 4 kq + j, j = 0..3, pixel (row kq, column j),
+// so a lane's A values (dz at those pixels, output channel 16 mb + n) are
+// one 16-byte read of a transposed dz tile [channel][pixel], and its B values
+// (a_{l-1} at those pixels shifted by the column's kernel position (ky, kx),
+// channel ci) one 16-byte read of the halo copy for kx, [ci][halo row][4]
+// (halo columns kx .. kx + 3 of each row).  Wave u of a team owns all MBU
+// row blocks and QW column blocks (MBU x QW x 4 accumulators), so one staged
+// tile feeds MBU x QW x 4 matrix ops from MBU + QW reads.  P tiles are staged
+// per pair of barriers; the next P tiles' operands are fetched into registers
+// during their matrix work.  Row strides (20 and 28 floats) put the 16 lanes
+// of a read group in distinct bank groups.
+template <int CA, int CZ>
+struct Dw2 {
+    static constexpr int NQ = 9 * CA + 1;                 // columns: (kernel position, input channel), bias
+    static constexpr int NBQ = (NQ + 15) / 16;            // 16-column blocks
+    static constexpr int MB = CZ / 16;                    // 16-row blocks (output channels)
+    static constexpr int MBU = MB;                        // row blocks per wave
+    static constexpr int QW0 = 32 / MBU;                  // column blocks per wave, at most 32 blocks of accumulators
+    static constexpr int NCH = (NBQ + QW0 - 1) / QW0;     // column chunks (waves per team)
+    static constexpr int QW = (NBQ + NCH - 1) / NCH;
+    static constexpr int BPT = (NCH + 3) / 4;             // blocks per team
+    static constexpr int P = 2;                           // tiles per staging
+    static constexpr int SZ = 20;                         // dz row stride (16 pixels + pad)
+    static constexpr int HS = 28;                         // halo copy channel stride (6 rows x 4 + pad)
+    static constexpr int DZT = CZ * SZ;                   // floats of one staged dz tile
+    static constexpr int HT = 3 * CA * HS;                // floats of one staged halo (three copies)
+    static constexpr int DZV = (4 * CZ + 255) / 256;      // 16-byte dz chunks per thread and tile
+    static constexpr int HV = (9 * CA + 255) / 256;       // 16-byte halo chunks per thread and tile
+    static constexpr size_t lds_bytes = (size_t)P * (DZT + HT) * sizeof(float);
+    static_assert(CZ % 16 == 0 && CA % 4 == 0, "whole row blocks and 16-byte channel chunks");
+};
+
+template <int CA, int CZ>
+__global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
+    using D = Dw2<CA, CZ>;
+    extern __shared__ float smem[];
+    float *s_dz = smem;                                   // [P][CZ][SZ]
+    float *s_h = smem + D::P * D::DZT;                    // [P][3][CA][HS]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int team = blockIdx.x / D::BPT, u = (blockIdx.x - team * D::BPT) * 4 + wave;
+    const bool active = u < D::NCH;
+    const int qb0 = active ? u * D::QW : 0;
+    const int kq = lane >> 4, col = lane & 15;
+    // This lane's B offset per column block within a staged halo, or -1 for
+    // the bias column (all ones), -2 for a padding column (zeros).
+    int boff[D::QW];
+#pragma unroll
+    for (int k = 0; k < D::QW; ++k) {
+        const int q = (qb0 + k) * 16 + col;
+        if (q < 9 * CA) {
+            const int kpos = q / CA, ci = q - kpos * CA, ky = kpos / 3, kx = kpos - 3 * ky;
+            boff[k] = (kx * CA + ci) * D::HS + (kq + ky) * 4;
+        } else {
+            boff[k] = q == 9 * CA ? -1 : -2;
+        }
+    }
+    floatx4 acc[D::MBU][D::QW];
+#pragma unroll
+    for (int m = 0; m < D::MBU; ++m)
+#pragma unroll
+        for (int k = 0; k < D::QW; ++k) acc[m][k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const long long NT = (long long)a.n * a.ntiles;
+    const long long t0 = NT * team / a.teams, t1 = NT * (team + 1) / a.teams;
+    // Operands of tiles c .. c + P - 1 (this thread's share) into registers,
+    // every load issued; tiles past t1, out-of-image halo pixels: zero.
+    float4 rdz[D::P][D::DZV], rh[D::P][D::HV];
+    auto fetch = [&](long long c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int pp = 0; pp < D::P; ++pp) {
+            const long long tt = c + pp;
+            const bool ok = tt < t1;
+            const long long ts = ok ? tt : t0;
+            const int i = (int)(ts / a.ntiles), t = (int)(ts - (long long)i * a.ntiles);
+            const int ty = t / a.TW, tx = t - ty * a.TW;
+            const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
+#pragma unroll
+            for (int k = 0; k < D::DZV; ++k) {
+                const int e = threadIdx.x + 256 * k;
+                rdz[pp][k] = ok && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride;
+#pragma unroll
+            for (int k = 0; k < D::HV; ++k) {
+                const int e = threadIdx.x + 256 * k;
+                const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+                const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
+                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (ok && e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
+                    v = *reinterpret_cast<const float4 *>(
+                        ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
+                rh[pp][k] = v;
+            }
+        }
+    };
+    if (t0 < t1) fetch(t0);
+    for (long long c = t0; c < t1; c += D::P) {
+        __syncthreads();                                   // the previous tiles' LDS readers are done
+#pragma unroll
+        for (int pp = 0; pp < D::P; ++pp) {
+            float *dz = s_dz + pp * D::DZT;
+            float *h = s_h + pp * D::HT;
+#pragma unroll
+            for (int k = 0; k < D::DZV; ++k) {
+                const int e = threadIdx.x + 256 * k;
+                if (e < 4 * CZ) {
+                    const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);   // pixel m, channels 4 c4 ..
+                    const float4 v = rdz[pp][k];
+                    dz[(4 * c4 + 0) * D::SZ + m] = v.x;
+                    dz[(4 * c4 + 1) * D::SZ + m] = v.y;
+                    dz[(4 * c4 + 2) * D::SZ + m] = v.z;
+                    dz[(4 * c4 + 3) * D::SZ + m] = v.w;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < D::HV; ++k) {
+                const int e = threadIdx.x + 256 * k;
+                if (e < 9 * CA) {
+                    const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+                    const int hy = pos / 6, hx = pos - 6 * hy;
+                    const float4 v = rh[pp][k];
+#pragma unroll
+                    for (int kx = 0; kx < 3; ++kx) {
+                        const int j = hx - kx;
+                        if (j < 0 || j > 3) continue;
+                        float *d = h + (kx * CA + 4 * c4) * D::HS + hy * 4 + j;
+                        d[0] = v.x;
+                        d[D::HS] = v.y;
+                        d[2 * D::HS] = v.z;
+                        d[3 * D::HS] = v.w;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        if (c + D::P < t1) fetch(c + D::P);                // in flight during these tiles' matrix ops
+        if (active) {
+#pragma unroll
+            for (int pp = 0; pp < D::P; ++pp) {
+                if (c + pp >= t1) break;                   // uniform
+                const float *dz = s_dz + pp * D::DZT;
+                const float *h = s_h + pp * D::HT;
+                float4 av[D::MBU], bv[D::QW];
+#pragma unroll
+                for (int m = 0; m < D::MBU; ++m)
+                    av[m] = *reinterpret_cast<const float4 *>(dz + (16 * m + col) * D::SZ + 4 * kq);
+#pragma unroll
+                for (int k = 0; k < D::QW; ++k)
+                    bv[k] = boff[k] >= 0 ? *reinterpret_cast<const float4 *>(h + boff[k])
+                                         : (boff[k] == -1 ? make_float4(1.f, 1.f, 1.f, 1.f) : make_float4(0.f, 0.f, 0.f, 0.f));
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int m = 0; m < D::MBU; ++m)
+#pragma unroll
+                        for (int k = 0; k < D::QW; ++k) {
+                            const float x = j == 0 ? av[m].x : j == 1 ? av[m].y : j == 2 ? av[m].z : av[m].w;
+                            const float y = j == 0 ? bv[k].x : j == 1 ? bv[k].y : j == 2 ? bv[k].z : bv[k].w;
+                            acc[m][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(x, y, acc[m][k], 0, 0, 0);
+                        }
+            }
+        }
+    }
+    if (!active) return;
+#pragma unroll
+    for (int m = 0; m < D::MBU; ++m)
+#pragma unroll
+        for (int k = 0; k < D::QW; ++k) {
+            const int q = (qb0 + k) * 16 + col;
+            if (q >= D::NQ) continue;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = m * 16 + 4 * kq + r;
+                a.part[((size_t)team * CZ + co) * D::NQ + q] = acc[m][k][r];
+            }
+        }
+}
+
 // dW_l and db_l from the teams' partial sums, added in team order.
 __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a) {
     const int NQ = 9 * a.ca + 1;
@@ -527,7 +706,7 @@ int dw_blocks_per_team(int ca, int cz, bool first) {
     RN_DW_FIRST_SHAPES(X)
 #undef X
 #define X(a_, z_) \
-    if (!first && ca == a_ && cz == z_) return dw_bpt<a_, z_, false>();
+    if (!first && ca == a_ && cz == z_) return Dw2<a_, z_>::BPT;
     RN_DW_SHAPES(X)
 #undef X
     return 0;
@@ -537,6 +716,20 @@ template <int CA, int CZ, bool FIRST>
 hipError_t run_dw(const BwdArgs &a, hipStream_t s) {
     using D = Dw<CA, CZ, FIRST>;
     hipLaunchKernelGGL((k_bwd_dw<CA, CZ, FIRST>), dim3(D::BPT * a.teams), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int total = CZ * D::NQ;
+    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 255) / 256), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int CA, int CZ>
+hipError_t run_dw2(const BwdArgs &a, hipStream_t s) {
+    using D = Dw2<CA, CZ>;
+    auto kern = k_bwd_dw2<CA, CZ>;
+    static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
+    if (attr != hipSuccess) return attr;
+    hipLaunchKernelGGL(kern, dim3(D::BPT * a.teams), dim3(256), D::lds_bytes, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int total = CZ * D::NQ;
@@ -617,7 +810,7 @@ hipError_t launch_bwd_dw(const BwdArgs &a, int cus, hipStream_t s) {
     RN_DW_FIRST_SHAPES(X)
 #undef X
 #define X(a_, z_) \
-    if (!first && a.ca == a_ && a.cz == z_) return run_dw<a_, z_, false>(a, s);
+    if (!first && a.ca == a_ && a.cz == z_) return run_dw2<a_, z_>(a, s);
     RN_DW_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
