@@ -212,189 +212,6 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
 
 // ------------------------------------------------------------------ dW
 
-// Row stride (floats) that puts the four lane groups of a 32-bit LDS read of
-// consecutive rows in distinct bank groups: stride % 64 in {16, 48}.
-constexpr int bank_stride(int c) {
-    int s = c;
-    while (s % 64 != 16 && s % 64 != 48) ++s;
-    return s;
-}
-
-// Column chunks per wave for NBQ column blocks and MB row blocks: at most 24
-// blocks per wave (its accumulators), and, among those, the fewest idle
-// waves in the blocks of four (the count that leaves the fewest, then the
-// smallest such count).
-constexpr int dw_chunks(int nbq, int mb) {
-    int best = (nbq + 23) / 24, best_idle = 1 << 30;
-    for (int nch = (nbq + 23) / 24; nch <= (nbq + 23) / 24 + 3 && nch <= nbq; ++nch) {
-        const int u = mb * nch, idle = (u + 3) / 4 * 4 - u;
-        if (idle < best_idle) {
-            best = nch;
-            best_idle = idle;
-        }
-    }
-    return best;
-}
-
-template <int CA, int CZ, bool FIRST>
-struct Dw {
-    static constexpr int NQ = 9 * CA + 1;                 // columns: (kernel position, input channel), bias
-    static constexpr int NBQ = (NQ + 15) / 16;            // 16-column blocks
-    static constexpr int MB = (CZ + 15) / 16;             // 16-row blocks (output channels)
-    static constexpr int NCH = dw_chunks(NBQ, MB);        // column chunks
-    static constexpr int QW = (NBQ + NCH - 1) / NCH;      // column blocks per wave
-    static constexpr int U = MB * NCH;                    // waves per team
-    static constexpr int BPT = (U + 3) / 4;               // blocks per team
-    static constexpr int SZ = bank_stride(CZ);            // dz tile row stride in LDS
-    static constexpr int SA = FIRST ? CA : bank_stride(CA);   // halo pixel stride in LDS
-    // Per-thread shares of a tile's operands, prefetched into registers:
-    static constexpr int DZV = (4 * CZ + 255) / 256;      // 16-byte chunks of the dz tile (16 x CZ)
-    static constexpr int HV = FIRST ? (36 * CA + 255) / 256 : (9 * CA + 255) / 256;   // halo values / chunks
-    static_assert(CZ % 4 == 0 && (FIRST || CA % 4 == 0), "16-byte channel chunks");
-};
-
-// Block = 4 waves of one team; wave w of block b of the team owns row block
-// mb and QW column blocks (unit 4 b + w) and accumulates them over the team's
-// share of the batch's tiles.  Per tile the block stages dz_l's tile and
-// a_{l-1}'s 6x6 halo in LDS; per 4-pixel k-step a lane reads one A value
-// (dz at pixel 4 s + kq, channel 16 mb + n) and one B value per column block
-// (a_{l-1} at that pixel shifted by the column's kernel position, or 1 for
-// the bias column).  D lane (n, kq) holds rows 4 kq + r (output channels) of
-// column n.
-template <int CA, int CZ, bool FIRST>
-__global__ __launch_bounds__(256) void k_bwd_dw(BwdArgs a) {
-    using D = Dw<CA, CZ, FIRST>;
-    __shared__ float s_dz[16 * D::SZ];
-    __shared__ float s_h[36 * D::SA];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int team = blockIdx.x / D::BPT, u = (blockIdx.x - team * D::BPT) * 4 + wave;
-    const bool active = u < D::U;
-    const int mb = active ? u / D::NCH : 0, qb0 = active ? (u - mb * D::NCH) * D::QW : 0;
-    const int kq = lane >> 4, col = lane & 15;
-    for (int e = threadIdx.x; e < 16 * D::SZ; e += blockDim.x) s_dz[e] = 0.f;   // row padding stays 0
-    // This lane's B offset per column block: (kernel position, channel) ->
-    // halo offset relative to the pixel's own position; -1 bias, -2 zero.
-    int boff[D::QW];
-#pragma unroll
-    for (int k = 0; k < D::QW; ++k) {
-        const int q = (qb0 + k) * 16 + col;
-        if (q < 9 * CA) {
-            const int kpos = q / CA, ci = q - kpos * CA;
-            boff[k] = ((kpos / 3) * 6 + kpos % 3) * D::SA + ci;
-        } else {
-            boff[k] = q == 9 * CA ? -1 : -2;
-        }
-    }
-    floatx4 acc[D::QW];
-#pragma unroll
-    for (int k = 0; k < D::QW; ++k) acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const long long NT = (long long)a.n * a.ntiles;
-    const long long t0 = NT * team / a.teams, t1 = NT * (team + 1) / a.teams;
-    const size_t HW = (size_t)a.H * a.W;
-    // The operands of tile tt, this thread's share, into registers (every
-    // load issued; out-of-image halo values and chunks are zero).
-    float4 rdz[D::DZV];
-    typename std::conditional<FIRST, float, float4>::type rh[D::HV];
-    auto fetch = [&](long long tt) __attribute__((always_inline)) {
-        const int i = (int)(tt / a.ntiles), t = (int)(tt - (long long)i * a.ntiles);
-        const int ty = t / a.TW, tx = t - ty * a.TW;
-        const int slot = a.ids[i];
-        const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
-#pragma unroll
-        for (int k = 0; k < D::DZV; ++k) {
-            const int e = threadIdx.x + 256 * k;
-            rdz[k] = e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        if constexpr (FIRST) {
-            const int head = a.stack != 1 ? a.ring_head[slot] : 0;
-#pragma unroll
-            for (int k = 0; k < D::HV; ++k) {
-                const int e = threadIdx.x + 256 * k;
-                const int c = e / 36, pos = e - c * 36;
-                const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
-                float v = 0.f;
-                if (e < 36 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W) {
-                    const float *plane;
-                    if (a.stack == 1) {
-                        plane = a.act_prev + ((size_t)slot * CA + c) * HW;
-                    } else {
-                        const int j = c / a.cin0, c1 = c - j * a.cin0;
-                        const int rp = (head - (a.stack - 1) + j + 4 * a.stack) & 3;
-                        plane = a.act_prev + (((size_t)slot * 4 + rp) * a.cin0 + c1) * HW;
-                    }
-                    v = plane[(size_t)y * a.W + x];
-                }
-                rh[k] = v;
-            }
-        } else {
-            const float *ap = a.act_prev + (size_t)slot * a.prev_stride;
-#pragma unroll
-            for (int k = 0; k < D::HV; ++k) {
-                const int e = threadIdx.x + 256 * k;
-                const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
-                const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
-                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
-                    v = *reinterpret_cast<const float4 *>(
-                        ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
-                rh[k] = v;
-            }
-        }
-    };
-    if (t0 < t1) fetch(t0);
-    for (long long tt = t0; tt < t1; ++tt) {
-        __syncthreads();                                   // the previous tile's LDS readers are done
-#pragma unroll
-        for (int k = 0; k < D::DZV; ++k) {
-            const int e = threadIdx.x + 256 * k;
-            if (e < 4 * CZ) {
-                const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);
-                *reinterpret_cast<float4 *>(s_dz + m * D::SZ + 4 * c4) = rdz[k];
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < D::HV; ++k) {
-            const int e = threadIdx.x + 256 * k;
-            if constexpr (FIRST) {
-                if (e < 36 * CA) {
-                    const int c = e / 36, pos = e - c * 36;
-                    s_h[pos * D::SA + c] = rh[k];
-                }
-            } else {
-                if (e < 9 * CA) {
-                    const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
-                    *reinterpret_cast<float4 *>(s_h + pos * D::SA + 4 * c4) = rh[k];
-                }
-            }
-        }
-        __syncthreads();
-        if (tt + 1 < t1) fetch(tt + 1);                    // in flight during this tile's matrix ops
-        if (active) {
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const float av = s_dz[(4 * s + kq) * D::SZ + mb * 16 + col];
-                const int hb = (s * 6 + kq) * D::SA;        // pixel (row s, column kq)
-#pragma unroll
-                for (int k = 0; k < D::QW; ++k) {
-                    const float bv = boff[k] >= 0 ? s_h[hb + boff[k]] : (boff[k] == -1 ? 1.f : 0.f);
-                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[k], 0, 0, 0);
-                }
-            }
-        }
-    }
-    if (!active) return;
-#pragma unroll
-    for (int k = 0; k < D::QW; ++k) {
-        const int q = (qb0 + k) * 16 + col;
-        if (q >= D::NQ) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int co = mb * 16 + 4 * kq + r;
-            if (co < CZ) a.part[((size_t)team * CZ + co) * D::NQ + q] = acc[k][r];
-        }
-    }
-}
-
 // dW for layers 2..L (a_{l-1} a tiled cache), operands read 16 bytes at a
 // time.  The K index of the product is the tile's pixel: in 4 consecutive
 // k-steps lane group kq takes k = 4 kq + j, j = 0..3, pixel (row kq, column j),
@@ -458,18 +275,23 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
     for (int m = 0; m < D::MBU; ++m)
 #pragma unroll
         for (int k = 0; k < D::QW; ++k) acc[m][k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // The team's tiles [t0, t1) of the batch (batch index i, tile t), walked
+    // in order: (fi, ft) is the next tile to fetch.
     const long long NT = (long long)a.n * a.ntiles;
-    const long long t0 = NT * team / a.teams, t1 = NT * (team + 1) / a.teams;
+    const int t0 = (int)(NT * team / a.teams), t1 = (int)(NT * (team + 1) / a.teams);
+    int fi = t0 / a.ntiles, ft = t0 - fi * a.ntiles;
     // Operands of tiles c .. c + P - 1 (this thread's share) into registers,
     // every load issued; tiles past t1, out-of-image halo pixels: zero.
     float4 rdz[D::P][D::DZV], rh[D::P][D::HV];
-    auto fetch = [&](long long c) __attribute__((always_inline)) {
+    auto fetch = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
         for (int pp = 0; pp < D::P; ++pp) {
-            const long long tt = c + pp;
-            const bool ok = tt < t1;
-            const long long ts = ok ? tt : t0;
-            const int i = (int)(ts / a.ntiles), t = (int)(ts - (long long)i * a.ntiles);
+            const bool ok = c + pp < t1;
+            const int i = ok ? fi : 0, t = ok ? ft : 0;
+            if (++ft == a.ntiles) {
+                ft = 0;
+                ++fi;
+            }
             const int ty = t / a.TW, tx = t - ty * a.TW;
             const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
 #pragma unroll
@@ -492,7 +314,7 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
         }
     };
     if (t0 < t1) fetch(t0);
-    for (long long c = t0; c < t1; c += D::P) {
+    for (int c = t0; c < t1; c += D::P) {
         __syncthreads();                                   // the previous tiles' LDS readers are done
 #pragma unroll
         for (int pp = 0; pp < D::P; ++pp) {
@@ -532,10 +354,13 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
         }
         __syncthreads();
         if (c + D::P < t1) fetch(c + D::P);                // in flight during these tiles' matrix ops
-        if (active) {
+        // Unconditional: a staged tile past t1 is all zeros and adds exact
+        // zeros, and an idle wave's sums are never stored (a guarded matrix
+        // phase makes the compiler copy the accumulators between register
+        // files on every pass).
+        {
 #pragma unroll
             for (int pp = 0; pp < D::P; ++pp) {
-                if (c + pp >= t1) break;                   // uniform
                 const float *dz = s_dz + pp * D::DZT;
                 const float *h = s_h + pp * D::HT;
                 float4 av[D::MBU], bv[D::QW];
@@ -569,19 +394,138 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int co = m * 16 + 4 * kq + r;
-                a.part[((size_t)team * CZ + co) * D::NQ + q] = acc[m][k][r];
+                a.part[((size_t)co * D::NQ + q) * a.teams + team] = acc[m][k][r];
             }
         }
 }
 
-// dW_l and db_l from the teams' partial sums, added in team order.
+// dW for layer 1 (a_0 the float32 input planes, 1 or 4 channels): so few
+// columns (9 cin + 1) that staging a tile through LDS for a handful of matrix
+// ops costs more than the ops.  Each wave is a team of its own and walks its
+// tiles with the operands loaded straight into the matrix layout (lane
+// (m, kq), k-step j: A = dz at pixel (row kq, column j), channel 16 mb + m;
+// B = the input at that pixel shifted by the column's kernel position, or 1
+// for the bias column), the next tile's loads issued before this tile's
+// matrix ops.  Memory-bound: each tile's dz (16 x CZ floats) is read once.
+template <int CA, int CZ>
+struct DwFirst {
+    static constexpr int NQ = 9 * CA + 1;
+    static constexpr int NBQ = (NQ + 15) / 16;            // 16-column blocks
+    static constexpr int MB = (CZ + 15) / 16;             // 16-row blocks
+};
+
+template <int CA, int CZ>
+__global__ __launch_bounds__(256) void k_bwd_dw_first(BwdArgs a) {
+    using D = DwFirst<CA, CZ>;
+    const int lane = threadIdx.x & 63;
+    const int team = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int kq = lane >> 4, col = lane & 15;
+    const long long NT = (long long)a.n * a.ntiles;
+    const int t0 = (int)(NT * team / a.teams), t1 = (int)(NT * (team + 1) / a.teams);
+    if (team >= a.teams) return;                           // uniform per wave
+    // This lane's column per block: kernel position offset (ky, kx) and input
+    // channel, or the bias / padding column.
+    int qky[D::NBQ], qkx[D::NBQ], qci[D::NBQ], qkind[D::NBQ];   // kind 0: input, 1: bias, 2: zero
+#pragma unroll
+    for (int k = 0; k < D::NBQ; ++k) {
+        const int q = 16 * k + col;
+        const int kpos = q / CA;
+        qci[k] = q - kpos * CA;
+        qky[k] = kpos / 3;
+        qkx[k] = kpos - 3 * (kpos / 3);
+        qkind[k] = q < 9 * CA ? 0 : q == 9 * CA ? 1 : 2;
+    }
+    floatx4 acc[D::MB][D::NBQ];
+#pragma unroll
+    for (int m = 0; m < D::MB; ++m)
+#pragma unroll
+        for (int k = 0; k < D::NBQ; ++k) acc[m][k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const size_t HW = (size_t)a.H * a.W;
+    float av[2][D::MB][4], bv[2][D::NBQ][4];
+    int fi = t0 / a.ntiles, ft = t0 - fi * a.ntiles;
+    auto fetch = [&](int slot_buf) __attribute__((always_inline)) {
+        const int i = fi, t = ft;
+        if (++ft == a.ntiles) {
+            ft = 0;
+            ++fi;
+        }
+        const int ty = t / a.TW, tx = t - ty * a.TW;
+        const int slot = a.ids[i];
+        const float *dz = a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ;
+#pragma unroll
+        for (int m = 0; m < D::MB; ++m) {
+            const int co = 16 * m + col;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) av[slot_buf][m][j] = co < CZ ? dz[(4 * kq + j) * CZ + co] : 0.f;
+        }
+        const int head = a.stack != 1 ? a.ring_head[slot] : 0;
+#pragma unroll
+        for (int k = 0; k < D::NBQ; ++k) {
+            const float *plane;
+            if (a.stack == 1) {
+                plane = a.act_prev + ((size_t)slot * CA + qci[k]) * HW;
+            } else {
+                const int jj = qci[k] / a.cin0, c1 = qci[k] - jj * a.cin0;
+                const int rp = (head - (a.stack - 1) + jj + 4 * a.stack) & 3;
+                plane = a.act_prev + (((size_t)slot * 4 + rp) * a.cin0 + c1) * HW;
+            }
+            const int y = ty * kTile - 1 + kq + qky[k];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int x = tx * kTile - 1 + j + qkx[k];
+                const bool in = qkind[k] == 0 && y >= 0 && y < a.H && x >= 0 && x < a.W;
+                bv[slot_buf][k][j] = in ? plane[(size_t)y * a.W + x] : (qkind[k] == 1 ? 1.f : 0.f);
+            }
+        }
+    };
+    if (t0 < t1) fetch(0);
+    for (int tt = t0; tt < t1; tt += 2) {
+        if (tt + 1 < t1) fetch(1);                         // in flight during tile tt's matrix ops
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int m = 0; m < D::MB; ++m)
+#pragma unroll
+                for (int k = 0; k < D::NBQ; ++k)
+                    acc[m][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][m][j], bv[0][k][j], acc[m][k], 0, 0, 0);
+        if (tt + 1 >= t1) break;
+        if (tt + 2 < t1) fetch(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int m = 0; m < D::MB; ++m)
+#pragma unroll
+                for (int k = 0; k < D::NBQ; ++k)
+                    acc[m][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][m][j], bv[1][k][j], acc[m][k], 0, 0, 0);
+    }
+#pragma unroll
+    for (int m = 0; m < D::MB; ++m)
+#pragma unroll
+        for (int k = 0; k < D::NBQ; ++k) {
+            const int q = 16 * k + col;
+            if (q >= D::NQ) continue;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = 16 * m + 4 * kq + r;
+                if (co < CZ) a.part[((size_t)co * D::NQ + q) * a.teams + team] = acc[m][k][r];
+            }
+        }
+}
+
+// dW_l and db_l from the teams' partial sums ([co][column][team]): one wave
+// per weight, lane j adding teams j, j + 64, ... in order, then the lanes'
+// sums by a fixed butterfly, so the order never changes.
 __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a) {
     const int NQ = 9 * a.ca + 1;
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= a.cz * NQ) return;
+    const int e = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (e >= a.cz * NQ) return;                            // uniform per wave
     const int co = e / NQ, q = e - co * NQ;
+    const float *p = a.part + (size_t)e * a.teams;
     float s = 0.f;
-    for (int team = 0; team < a.teams; ++team) s += a.part[((size_t)team * a.cz + co) * NQ + q];
+    for (int team = lane; team < a.teams; team += 64) s += p[team];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (lane != 0) return;
     float *d;
     if (q < 9 * a.ca) {
         const int kpos = q / a.ca, ci = q - kpos * a.ca;
@@ -695,14 +639,9 @@ __global__ __launch_bounds__(256) void k_unprime(int32_t *primed, int S) {
 #define RN_DW_SHAPES(X) X(40, 80) X(64, 128) X(128, 128)
 #define RN_DX_SHAPES(X) X(80, 40) X(128, 64) X(128, 128)
 
-template <int CA, int CZ, bool FIRST>
-int dw_bpt() {
-    return Dw<CA, CZ, FIRST>::BPT;
-}
-
 int dw_blocks_per_team(int ca, int cz, bool first) {
 #define X(a_, z_) \
-    if (first && ca == a_ && cz == z_) return dw_bpt<a_, z_, true>();
+    if (first && ca == a_ && cz == z_) return 1;
     RN_DW_FIRST_SHAPES(X)
 #undef X
 #define X(a_, z_) \
@@ -712,14 +651,13 @@ int dw_blocks_per_team(int ca, int cz, bool first) {
     return 0;
 }
 
-template <int CA, int CZ, bool FIRST>
-hipError_t run_dw(const BwdArgs &a, hipStream_t s) {
-    using D = Dw<CA, CZ, FIRST>;
-    hipLaunchKernelGGL((k_bwd_dw<CA, CZ, FIRST>), dim3(D::BPT * a.teams), dim3(256), 0, s, a);
+template <int CA, int CZ>
+hipError_t run_dw_first(const BwdArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL((k_bwd_dw_first<CA, CZ>), dim3((a.teams + 3) / 4), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int total = CZ * D::NQ;
-    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 255) / 256), dim3(256), 0, s, a);
+    const int total = CZ * DwFirst<CA, CZ>::NQ;
+    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 3) / 4), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -733,7 +671,7 @@ hipError_t run_dw2(const BwdArgs &a, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int total = CZ * D::NQ;
-    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 255) / 256), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_bwd_reduce, dim3((total + 3) / 4), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -780,6 +718,11 @@ void pack_dx_weights(const float *oihw, int ca, int cz, float *dst) {
 }
 
 int bwd_dw_teams(int ca, int cz, bool first, int n, int ntiles, int cus) {
+    if (first) {
+        // a team per wave, 16 waves per CU, at least 8 tiles each
+        const long long tiles = (long long)n * ntiles;
+        return (int)std::max(1LL, std::min(16LL * cus, (tiles + 7) / 8));
+    }
     const int bpt = std::max(1, dw_blocks_per_team(ca, cz, first));
     const long long tiles = (long long)n * ntiles;
     const long long want = (3LL * cus + bpt - 1) / bpt;      // about three blocks per CU
@@ -806,7 +749,7 @@ hipError_t launch_bwd_dw(const BwdArgs &a, int cus, hipStream_t s) {
     (void)cus;
     const bool first = a.first != 0;
 #define X(a_, z_) \
-    if (first && a.ca == a_ && a.cz == z_) return run_dw<a_, z_, true>(a, s);
+    if (first && a.ca == a_ && a.cz == z_) return run_dw_first<a_, z_>(a, s);
     RN_DW_FIRST_SHAPES(X)
 #undef X
 #define X(a_, z_) \

@@ -41,7 +41,7 @@ struct BwdArgs {
     const int32_t *ring_head;
     float *dz_out;                // l >= 2
     const float *wt;              // dx weights (pack_dx_weights)
-    float *part;                  // [teams][cz][9 ca + 1]
+    float *part;                  // [cz][9 ca + 1][teams]
     int teams;
     float *gw, *gb;               // OIHW [cz][ca][3][3], [cz]
     int accumulate;
