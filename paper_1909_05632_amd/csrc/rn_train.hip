@@ -142,8 +142,10 @@ struct Dx {
 
 // One wave per 4x4 tile of layer l-1 (tile id = 4 block + wave over the
 // batch's tiles); the wave stages the 6x6 x CZ halo of dz_l in its own LDS
-// area, walks K with the operands of the next block loaded during the
-// current block's matrix ops, and writes dz_{l-1} = acc where a_{l-1} > 0.
+// area, walks K with the weights of each block (from L2) loaded three blocks
+// ahead, and writes dz_{l-1} = acc where a_{l-1} > 0.  (Two tiles per wave,
+// sharing each weight load, measured slower: the doubled halo area leaves one
+// block per CU, and the halo staging is then exposed.)
 // Operand layout of v_mfma_f32_16x16x4_f32 as in the forward kernels: A row
 // m = tile pixel (m % 4, m / 4), lane group kq takes K = 16 b + 4 kq + j;
 // D lane (n, kq) holds pixels (i, kq), i = 0..3, of output channel 16 nb + n.
@@ -176,25 +178,32 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
     floatx4 acc[D::NB];
 #pragma unroll
     for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    floatx4 bcur[D::NB], bnxt[D::NB];
+    // B (weights, from L2) in a ring of three register sets, each block's
+    // loaded three blocks ahead of its matrix ops (KB is a multiple of 3).
+    static_assert(D::KB % 3 == 0, "three-block ring");
+    floatx4 br[3][D::NB];
 #pragma unroll
-    for (int nb = 0; nb < D::NB; ++nb) bcur[nb] = wt[nb * 64 + lane];
-    for (int b = 0; b < D::KB; ++b) {
-        if (b + 1 < D::KB) {
+    for (int r = 0; r < 3; ++r)
 #pragma unroll
-            for (int nb = 0; nb < D::NB; ++nb) bnxt[nb] = wt[((b + 1) * D::NB + nb) * 64 + lane];
+        for (int nb = 0; nb < D::NB; ++nb) br[r][nb] = wt[(r * D::NB + nb) * 64 + lane];
+    for (int b0 = 0; b0 < D::KB; b0 += 3) {
+#pragma unroll
+        for (int r = 0; r < 3; ++r) {
+            const int b = b0 + r;
+            const int K0 = 16 * b, kpos = K0 / CZ, c16 = (K0 - kpos * CZ) >> 4;
+            const int ky = kpos / 3, kx = kpos - ky * 3;
+            const float4 av = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * c16 + kq));
+            const float al[4] = {av.x, av.y, av.z, av.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int nb = 0; nb < D::NB; ++nb)
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], br[r][nb][j], acc[nb], 0, 0, 0);
+            if (b + 3 < D::KB) {
+#pragma unroll
+                for (int nb = 0; nb < D::NB; ++nb) br[r][nb] = wt[((b + 3) * D::NB + nb) * 64 + lane];
+            }
         }
-        const int K0 = 16 * b, kpos = K0 / CZ, c16 = (K0 - kpos * CZ) >> 4;
-        const int ky = kpos / 3, kx = kpos - ky * 3;
-        const float4 av = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * c16 + kq));
-        const float al[4] = {av.x, av.y, av.z, av.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int nb = 0; nb < D::NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], bcur[nb][j], acc[nb], 0, 0, 0);
-#pragma unroll
-        for (int nb = 0; nb < D::NB; ++nb) bcur[nb] = bnxt[nb];
     }
     const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + (size_t)t * kTilePx * CA;
     float *dst = a.dz_out + ((size_t)i * a.ntiles + t) * kTilePx * CA;
