@@ -801,21 +801,12 @@ __device__ inline void dma_wstage(const float *wg, int q, float *dst, int w, int
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
     const int kpos = q / S::NCH, ch = q - kpos * S::NCH;
-    // LDS byte address of dst (the low half of a generic pointer into LDS is
-    // its LDS offset), wave-uniform.
-    const uint32_t l0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
+    const uint32_t l0 = lds_addr(dst);
 #pragma unroll
     for (int j = 0; j < S::WPW; ++j) {
         const int b = j / S::NBW, nbw = j - b * S::NBW;
-        const float *src = wg + ((size_t)(kpos * M::NBLK + ch * S::SB + b) * M::NB + w * S::NBW + nbw) * 256 + 4 * lane;
-        // Issued in assembly: the compiler would otherwise wait for these
-        // loads before every later LDS read; the caller waits for them.  M0
-        // (the LDS base of the instruction) is restored afterwards.
-        uint32_t saved;
-        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-                     : "=&s"(saved)
-                     : "v"(src), "s"(l0 + 1024u * j)
-                     : "memory");
+        lds_dma16(wg + ((size_t)(kpos * M::NBLK + ch * S::SB + b) * M::NB + w * S::NBW + nbw) * 256 + 4 * lane,
+                  l0 + 1024u * j);
     }
 }
 

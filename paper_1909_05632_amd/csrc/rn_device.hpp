@@ -24,6 +24,25 @@ __device__ inline void wave_sync() {
 // between the waves of the block.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// 16 bytes per lane from global memory straight into LDS
+// (global_load_lds_dwordx4: lane i writes the 16 bytes at the wave-uniform LDS
+// byte address lds + 16 i).  Issued in assembly so the compiler does not make
+// every later LDS read wait for it; the caller waits (s_waitcnt vmcnt) before
+// the data is read.  M0, the instruction's LDS base, is restored afterwards.
+__device__ inline void lds_dma16(const void *src, uint32_t lds) {
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "v"(src), "s"(lds)
+                 : "memory");
+}
+
+// LDS byte address of a pointer into LDS (the low half of a generic pointer to
+// LDS is its LDS offset), made wave-uniform.
+__device__ inline uint32_t lds_addr(const void *p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+
 // Sums over the 64 lanes of a wave of eight per-lane values p[0..7], by
 // halving: at each step (partner lane l ^ 32, 16, 8, 4, 2, 1) a lane keeps
 // half of the values it still holds and adds the partner's copy of them, so

@@ -1199,7 +1199,7 @@ rn_status reuse_net_backward(reuse_net *net, int32_t n, const int32_t *ids_in, c
         e = timed(net, RN_PHASE_BWD_DW, s, [&] { return launch_bwd_dw(ba, net->cus, s); });
         if (e != hipSuccess) return net->fail(RN_EHIP, std::string("weight gradient: ") + hipGetErrorString(e));
         if (l > 0) {
-            e = timed(net, RN_PHASE_BWD_DX, s, [&] { return launch_bwd_dx(ba, s); });
+            e = timed(net, RN_PHASE_BWD_DX, s, [&] { return launch_bwd_dx(ba, net->cus, s); });
             if (e != hipSuccess) return net->fail(RN_EHIP, std::string("input gradient: ") + hipGetErrorString(e));
             cur ^= 1;
         }

@@ -131,91 +131,174 @@ __device__ inline int hoff(int p, int c4) {
     return p * CZ + 4 * (c4 ^ g);
 }
 
+// Input gradients dz_{l-1} = (W_l^T * dz_l) where a_{l-1} > 0, as a forward
+// convolution of dz_l (CZ channels) with the transposed, flipped weights
+// (pack_dx_weights) into CA channels.  A block works on a group of 4 tiles
+// of layer l-1 (one per wave, one wave per SIMD) and streams the weights
+// through LDS in stages of one kernel position x SC channels of dz_l, two
+// buffers: stage q + 1 goes straight from global memory into the free buffer
+// at the start of stage q (lds_dma16, the block's loads split over its
+// waves), each wave waits for its own loads and a block barrier ends the
+// stage.  So each weight byte brought from L2 serves 4 tiles.  Each wave
+// keeps its tile's 6x6 x CZ halo of dz_l in its own LDS area (the next
+// group's fetched into registers in the last stage, stored after the
+// epilogue).  Operand layout of v_mfma_f32_16x16x4_f32 as in the forward
+// kernels: A row m = tile pixel (m % 4, m / 4), lane group kq takes
+// K = 16 b + 4 kq + j; D lane (n, kq) holds pixels (i, kq), i = 0..3, of
+// output channel 16 nb + n.
 template <int CZ, int CA>
 struct Dx {
     static constexpr int NB = (CA + 15) / 16;   // 16-column output blocks (CA padded with zero weights)
-    static constexpr int KB = 9 * CZ / 16;      // 16-deep K blocks: kernel position (CZ / 16 blocks each)
-    static constexpr int HALO = 36 * CZ;        // floats of one wave's halo
-    static constexpr size_t lds_bytes = (size_t)4 * HALO * sizeof(float);
-    static_assert(CZ % 16 == 0, "whole 16-channel K blocks per kernel position");
+    static constexpr int SC = (CZ > 64 && CZ % 64 == 0) ? 64 : CZ;   // channels of dz_l per stage
+    static constexpr int NCH = CZ / SC;         // stages per kernel position
+    static constexpr int NQ = 9 * NCH;          // stages per group
+    static constexpr int SB = SC / 16;          // 16-deep K blocks per stage
+    static constexpr int KBP = CZ / 16;         // K blocks per kernel position
+    static constexpr int WL = SB * NB;          // 1 KB wave loads per stage
+    static constexpr int WST = WL * 256;        // floats per stage
+    static constexpr int HALO = 36 * CZ;        // floats of one tile's halo
+    static constexpr int HV = (9 * CZ + 63) / 64;   // 16-byte halo loads per lane
+    static constexpr size_t lds_bytes = (size_t)(2 * WST + 4 * HALO) * sizeof(float);
+    static_assert(CZ % 16 == 0 && SC % 16 == 0, "whole 16-channel K blocks per stage");
+    static_assert(HV <= 32, "halo mask width");
 };
 
-// One wave per 4x4 tile of layer l-1 (tile id = 4 block + wave over the
-// batch's tiles); the wave stages the 6x6 x CZ halo of dz_l in its own LDS
-// area, walks K with the weights of each block (from L2) loaded three blocks
-// ahead, and writes dz_{l-1} = acc where a_{l-1} > 0.  (Two tiles per wave,
-// sharing each weight load, measured slower: the doubled halo area leaves one
-// block per CU, and the halo staging is then exposed.)
-// Operand layout of v_mfma_f32_16x16x4_f32 as in the forward kernels: A row
-// m = tile pixel (m % 4, m / 4), lane group kq takes K = 16 b + 4 kq + j;
-// D lane (n, kq) holds pixels (i, kq), i = 0..3, of output channel 16 nb + n.
+template <int CZ, int CA>
+__device__ inline void dx_fetch_halo(const BwdArgs &a, int tid, bool valid, float4 *regs, uint32_t &ok, int lane) {
+    using D = Dx<CZ, CA>;
+    constexpr int C4 = CZ / 4;
+    const int i = valid ? tid / a.ntiles : 0, t = valid ? tid - i * a.ntiles : 0;
+    const int ty = t / a.TW, tx = t - ty * a.TW;
+    const float *src = a.dz_in + (size_t)i * a.ntiles * kTilePx * CZ;
+    ok = 0;
+#pragma unroll
+    for (int k = 0; k < D::HV; ++k) {
+        const int e = lane + 64 * k;
+        const int pos = e / C4, c4 = e - pos * C4;
+        const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
+        const bool in = valid && e < 36 * C4 && y >= 0 && y < a.H && x >= 0 && x < a.W;
+        // every load issued (an absent one reads the tile's first chunk)
+        regs[k] = *reinterpret_cast<const float4 *>(
+            src + (in ? ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CZ + 4 * c4 : 0));
+        ok |= (uint32_t)in << k;
+    }
+}
+
+template <int CZ, int CA>
+__device__ inline void dx_store_halo(float *halo, const float4 *regs, uint32_t ok, int lane) {
+    using D = Dx<CZ, CA>;
+    constexpr int C4 = CZ / 4;
+#pragma unroll
+    for (int k = 0; k < D::HV; ++k) {
+        const int e = lane + 64 * k;
+        if (e < 36 * C4) {
+            const int pos = e / C4, c4 = e - pos * C4;
+            *reinterpret_cast<float4 *>(halo + hoff<CZ>(pos, c4)) = (ok >> k) & 1 ? regs[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+}
+
+// The block's share of stage q's weights straight into LDS: wave w issues
+// the stage's wave loads w, w + 4, ...
+template <int CZ, int CA>
+__device__ inline void dx_dma_stage(const float *wt, int q, float *dst, int wave, int lane) {
+    using D = Dx<CZ, CA>;
+    const int kpos = q / D::NCH, ch = q - kpos * D::NCH;
+    const float *src = wt + (size_t)(kpos * D::KBP + ch * D::SB) * D::NB * 256;
+    const uint32_t l0 = dev::lds_addr(dst);
+#pragma unroll
+    for (int j = 0; j < (D::WL + 3) / 4; ++j) {
+        const int wl = wave + 4 * j;
+        if (wl < D::WL) dev::lds_dma16(src + wl * 256 + 4 * lane, l0 + 1024u * wl);   // uniform per wave
+    }
+}
+
 template <int CZ, int CA>
 __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
     using D = Dx<CZ, CA>;
     extern __shared__ float smem[];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const long long tid = (long long)blockIdx.x * 4 + wave;
-    if (tid >= (long long)a.n * a.ntiles) return;                 // wave-uniform; no block barriers below
-    const int i = (int)(tid / a.ntiles), t = (int)(tid - (long long)i * a.ntiles);
-    const int ty = t / a.TW, tx = t - ty * a.TW;
-    float *halo = smem + wave * D::HALO;
-    const float *src = a.dz_in + (size_t)i * a.ntiles * kTilePx * CZ;
-    constexpr int C4 = CZ / 4;
-    for (int h = lane; h < 36 * C4; h += 64) {
-        const int pos = h / C4, c4 = h - pos * C4;
-        const int hy = pos / 6, hx = pos - hy * 6;
-        const int y = ty * kTile - 1 + hy, x = tx * kTile - 1 + hx;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (y >= 0 && y < a.H && x >= 0 && x < a.W)
-            v = *reinterpret_cast<const float4 *>(
-                src + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CZ + 4 * c4);
-        *reinterpret_cast<float4 *>(halo + hoff<CZ>(pos, c4)) = v;
-    }
-    dev::wave_sync();
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int NT = a.n * a.ntiles, NG = (NT + 3) / 4;
+    if ((int)blockIdx.x >= NG) return;                             // uniform per block
+    float *wbuf = smem;                                            // two stages
+    float *halo = smem + 2 * D::WST + wave * D::HALO;              // this wave's tile
     const int mrow = lane & 15, kq = lane >> 4;
     const int pix = (mrow & 3) * 6 + (mrow >> 2);
-    const floatx4 *wt = reinterpret_cast<const floatx4 *>(a.wt);
-    floatx4 acc[D::NB];
+
+    int g = blockIdx.x;
+    dx_dma_stage<CZ, CA>(a.wt, 0, wbuf, wave, lane);
+    float4 hreg[D::HV];
+    uint32_t hok;
+    dx_fetch_halo<CZ, CA>(a, 4 * g + wave, 4 * g + wave < NT, hreg, hok, lane);
+    dx_store_halo<CZ, CA>(halo, hreg, hok, lane);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    dev::lds_barrier();
+    int buf = 0;
+    for (; g < NG; g += gridDim.x) {                               // uniform per block
+        const int tid = 4 * g + wave, tidn = 4 * (g + (int)gridDim.x) + wave;
+        floatx4 acc[D::NB];
 #pragma unroll
-    for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // B (weights, from L2) in a ring of three register sets, each block's
-    // loaded three blocks ahead of its matrix ops (KB is a multiple of 3).
-    static_assert(D::KB % 3 == 0, "three-block ring");
-    floatx4 br[3][D::NB];
-#pragma unroll
-    for (int r = 0; r < 3; ++r)
-#pragma unroll
-        for (int nb = 0; nb < D::NB; ++nb) br[r][nb] = wt[(r * D::NB + nb) * 64 + lane];
-    for (int b0 = 0; b0 < D::KB; b0 += 3) {
-#pragma unroll
-        for (int r = 0; r < 3; ++r) {
-            const int b = b0 + r;
-            const int K0 = 16 * b, kpos = K0 / CZ, c16 = (K0 - kpos * CZ) >> 4;
+        for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < D::NQ; ++q) {
+            const int kpos = q / D::NCH, ch = q - kpos * D::NCH;
             const int ky = kpos / 3, kx = kpos - ky * 3;
-            const float4 av = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * c16 + kq));
-            const float al[4] = {av.x, av.y, av.z, av.w};
+            const float *wst = wbuf + buf * D::WST;
+            float4 av = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * ch * D::SB + kq));
+            float4 bv[D::NB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int nb = 0; nb < D::NB; ++nb) bv[nb] = *reinterpret_cast<const float4 *>(wst + (nb * 64 + lane) * 4);
+            dx_dma_stage<CZ, CA>(a.wt, q + 1 < D::NQ ? q + 1 : 0, wbuf + (buf ^ 1) * D::WST, wave, lane);
+            const bool last = q == D::NQ - 1;
+            if (last) dx_fetch_halo<CZ, CA>(a, tidn, tidn < NT, hreg, hok, lane);
 #pragma unroll
-                for (int nb = 0; nb < D::NB; ++nb)
-                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], br[r][nb][j], acc[nb], 0, 0, 0);
-            if (b + 3 < D::KB) {
+            for (int b = 0; b < D::SB; ++b) {
+                float4 an = av, bn[D::NB];
 #pragma unroll
-                for (int nb = 0; nb < D::NB; ++nb) br[r][nb] = wt[((b + 3) * D::NB + nb) * 64 + lane];
+                for (int nb = 0; nb < D::NB; ++nb) bn[nb] = bv[nb];
+                if (b + 1 < D::SB) {                               // the next block's operands during this one's ops
+                    an = *reinterpret_cast<const float4 *>(halo + hoff<CZ>(pix + ky * 6 + kx, 4 * (ch * D::SB + b + 1) + kq));
+#pragma unroll
+                    for (int nb = 0; nb < D::NB; ++nb)
+                        bn[nb] = *reinterpret_cast<const float4 *>(wst + (((b + 1) * D::NB + nb) * 64 + lane) * 4);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                const float al[4] = {av.x, av.y, av.z, av.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int nb = 0; nb < D::NB; ++nb) {
+                        const float bj = j == 0 ? bv[nb].x : j == 1 ? bv[nb].y : j == 2 ? bv[nb].z : bv[nb].w;
+                        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(al[j], bj, acc[nb], 0, 0, 0);
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+                av = an;
+#pragma unroll
+                for (int nb = 0; nb < D::NB; ++nb) bv[nb] = bn[nb];
+            }
+            buf ^= 1;
+            if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(D::HV) : "memory");
+            else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            dev::lds_barrier();
+        }
+        if (tid < NT) {
+            const int i = tid / a.ntiles, t = tid - i * a.ntiles;
+            const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + (size_t)t * kTilePx * CA;
+            float *dst = a.dz_out + ((size_t)i * a.ntiles + t) * kTilePx * CA;
+#pragma unroll
+            for (int nb = 0; nb < D::NB; ++nb) {
+                const int c = nb * 16 + mrow;
+                if (c >= CA) continue;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = r * 4 + kq;                      // pixel (row r, column kq)
+                    dst[m * CA + c] = ap[m * CA + c] > 0.f ? acc[nb][r] : 0.f;
+                }
             }
         }
-    }
-    const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + (size_t)t * kTilePx * CA;
-    float *dst = a.dz_out + ((size_t)i * a.ntiles + t) * kTilePx * CA;
-#pragma unroll
-    for (int nb = 0; nb < D::NB; ++nb) {
-        const int c = nb * 16 + mrow;
-        if (c >= CA) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = r * 4 + kq;                          // pixel (row r, column kq)
-            dst[m * CA + c] = ap[m * CA + c] > 0.f ? acc[nb][r] : 0.f;
-        }
+        dev::wave_sync();                                          // this wave's halo reads are done
+        dx_store_halo<CZ, CA>(halo, hreg, hok, lane);
+        dev::wave_sync();
     }
 }
 
@@ -685,13 +768,15 @@ hipError_t run_dw2(const BwdArgs &a, hipStream_t s) {
 }
 
 template <int CZ, int CA>
-hipError_t run_dx(const BwdArgs &a, hipStream_t s) {
+hipError_t run_dx(const BwdArgs &a, int cus, hipStream_t s) {
     using D = Dx<CZ, CA>;
     auto kern = k_bwd_dx<CZ, CA>;
     static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
     if (attr != hipSuccess) return attr;
-    const long long tiles = (long long)a.n * a.ntiles;
-    hipLaunchKernelGGL(kern, dim3((unsigned)((tiles + 3) / 4)), dim3(256), D::lds_bytes, s, a);
+    const long long groups = ((long long)a.n * a.ntiles + 3) / 4;
+    const int per_cu = D::lds_bytes <= 78 * 1024 ? 2 : 1;       // blocks that fit one CU's LDS
+    const int grid = (int)std::min<long long>(groups, (long long)per_cu * cus);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), D::lds_bytes, s, a);
     return hipGetLastError();
 }
 
@@ -768,9 +853,9 @@ hipError_t launch_bwd_dw(const BwdArgs &a, int cus, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_bwd_dx(const BwdArgs &a, hipStream_t s) {
+hipError_t launch_bwd_dx(const BwdArgs &a, int cus, hipStream_t s) {
 #define X(z_, a_) \
-    if (a.cz == z_ && a.ca == a_) return run_dx<z_, a_>(a, s);
+    if (a.cz == z_ && a.ca == a_) return run_dx<z_, a_>(a, cus, s);
     RN_DX_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;

@@ -77,7 +77,7 @@ hipError_t launch_reinforce(int n, int n_out, const float *logits, const int32_t
                             float *g, hipStream_t s);
 hipError_t launch_bwd_head(const HeadBwdArgs &a, hipStream_t s);
 hipError_t launch_bwd_dw(const BwdArgs &a, int cus, hipStream_t s);   // partials, then the reduction
-hipError_t launch_bwd_dx(const BwdArgs &a, hipStream_t s);
+hipError_t launch_bwd_dx(const BwdArgs &a, int cus, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs &a, hipStream_t s);
 hipError_t launch_unprime(int32_t *primed, int S, hipStream_t s);
 
