@@ -141,8 +141,9 @@ __device__ inline int hoff(int p, int c4) {
 // waves), each wave waits for its own loads and a block barrier ends the
 // stage.  So each weight byte brought from L2 serves 4 tiles.  Each wave
 // keeps its tile's 6x6 x CZ halo of dz_l in its own LDS area (the next
-// group's fetched into registers in the last stage, stored after the
-// epilogue).  Operand layout of v_mfma_f32_16x16x4_f32 as in the forward
+// group's fetched into registers three stages before the group ends, stored
+// after the epilogue: fetched in the last stage it arrived late, 14% of the
+// time).  Operand layout of v_mfma_f32_16x16x4_f32 as in the forward
 // kernels: A row m = tile pixel (m % 4, m / 4), lane group kq takes
 // K = 16 b + 4 kq + j; D lane (n, kq) holds pixels (i, kq), i = 0..3, of
 // output channel 16 nb + n.
@@ -249,8 +250,11 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
 #pragma unroll
             for (int nb = 0; nb < D::NB; ++nb) bv[nb] = *reinterpret_cast<const float4 *>(wst + (nb * 64 + lane) * 4);
             dx_dma_stage<CZ, CA>(a.wt, q + 1 < D::NQ ? q + 1 : 0, wbuf + (buf ^ 1) * D::WST, wave, lane);
-            const bool last = q == D::NQ - 1;
-            if (last) dx_fetch_halo<CZ, CA>(a, tidn, tidn < NT, hreg, hok, lane);
+            // The next group's halo is fetched three stages before the end
+            // (issued after this stage's weight loads: the wait below leaves
+            // it in flight, the next stages' waits find it arrived).
+            const bool hstage = q == (D::NQ >= 3 ? D::NQ - 3 : 0);
+            if (hstage) dx_fetch_halo<CZ, CA>(a, tidn, tidn < NT, hreg, hok, lane);
 #pragma unroll
             for (int b = 0; b < D::SB; ++b) {
                 float4 an = av, bn[D::NB];
@@ -277,7 +281,7 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
                 for (int nb = 0; nb < D::NB; ++nb) bv[nb] = bn[nb];
             }
             buf ^= 1;
-            if (last) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(D::HV) : "memory");
+            if (hstage) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(D::HV) : "memory");
             else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             dev::lds_barrier();
         }
