@@ -363,6 +363,9 @@ def main():
     ap.add_argument("--update-every", type=int, default=0,
                     help="training rollouts: replace the weights every N steps (inside the timed "
                          "region; every slot then recomputes everything on its next step)")
+    ap.add_argument("--host-weight-update", action="store_true",
+                    help="with --update-every: replace the weights through the host repack and upload "
+                         "(reuse_net_set_weights) even where the device path applies")
     ap.add_argument("--separate-first", action="store_true",
                     help="run layer 1 as its own kernel instead of inside layer 2")
     ap.add_argument("--graph", action="store_true",
@@ -423,6 +426,17 @@ def main():
     stream = torch.cuda.current_stream()
 
     alt_weights = [weights, synth.net_weights(wl, seed_extra=1)] if args.update_every else None
+    # Weight updates come from device buffers (reuse_net_set_weights_device) on
+    # nets the training calls support, else through the host repack.
+    dev_params = None
+    if args.update_every and net.grad_elems() > 0 and not args.host_weight_update:
+        dev_params = [net.pack_params(w) for w in alt_weights]
+
+    def set_weights(i):
+        if dev_params is not None:
+            net.set_weights_device(dev_params[i])
+        else:
+            net.set_weights(alt_weights[i])
 
     graphs = {}
     if args.graph:
@@ -442,7 +456,7 @@ def main():
 
     def do_step(k, eager=False):
         if args.update_every and k % args.update_every == 0 and k > 0:
-            net.set_weights(alt_weights[(k // args.update_every) % 2])
+            set_weights((k // args.update_every) % 2)
         if graphs and not eager:
             graphs[drv.seq[k]].replay()
         else:
@@ -451,7 +465,7 @@ def main():
     def restart():
         # every pass starts from the first weight set, primed on the first frames
         if args.update_every:
-            net.set_weights(weights)
+            set_weights(0)
         drv.prime(net, out)
 
     # Stats pass: dirty tiles of exactly the steps the timed pass will run.
@@ -600,6 +614,7 @@ def main():
         cfg["change_preset"] = args.change_frac
     if args.update_every:
         cfg["weight_update_every"] = args.update_every
+        cfg["weight_update"] = "device" if dev_params is not None else "host"
     if graphs:
         cfg["launch"] = "graph replay per step"
     line = {

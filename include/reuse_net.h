@@ -239,6 +239,22 @@ rn_status reuse_net_backward(reuse_net *net, int32_t n, const int32_t *dev_strea
  * no host synchronisation. */
 rn_status reuse_net_sgd_step(reuse_net *net, const float *dev_grads, float lr, void *hip_stream);
 
+/* Replace the weights from device memory (training between rollouts, Sec. 1
+ * and Sec. 2, when the new weights are already on the GPU: a learner's
+ * parameters, or a copy kept beside the net).  dev_params: float32, device,
+ * reuse_net_grad_elems floats in the gradient-buffer layout above (each conv
+ * layer's OIHW weights then its bias, then the dense weights in (c, y, x)
+ * order and the dense bias); read only, owned by the caller, and not
+ * referenced after the call's work on hip_stream has run.  Every packed copy
+ * the kernels read is rewritten from it on the device, so the net computes
+ * exactly as one created with those weights (the same bits), and every slot
+ * is marked unprimed as by reuse_net_set_weights.  Enqueued on hip_stream, no
+ * host synchronisation and no host copy of the weights; work on other streams
+ * that still reads the old weights must be ordered before it by the caller.
+ * RN_EINVAL for a NULL net or dev_params; RN_EUNSUPPORTED (nothing changes)
+ * for nets the training calls do not support; RN_EHIP if a launch fails. */
+rn_status reuse_net_set_weights_device(reuse_net *net, const float *dev_params, void *hip_stream);
+
 /* ---- variants of one slot: copy-on-write overlays (Sec. 1, known change) ---- */
 
 /* Device scratch bytes reuse_net_variants needs for n variants when no variant

@@ -35,7 +35,7 @@ EXPORTS = (
     "reuse_net_destroy", "reuse_net_variant_scratch_bytes", "reuse_net_variants",
     "reuse_net_set_weights", "reuse_net_variants_static", "reuse_net_grad_elems",
     "reuse_net_backward_scratch_bytes", "reuse_net_reinforce_dlogits", "reuse_net_backward",
-    "reuse_net_sgd_step",
+    "reuse_net_sgd_step", "reuse_net_set_weights_device",
 )
 RN_STATIC_SCRATCH_BYTES = 64 << 20
 
@@ -113,6 +113,8 @@ def load_library(path: str = LIB_PATH):
     L.reuse_net_backward.argtypes = [P, I32, P, P, P, I32, P, SZ, P]
     L.reuse_net_sgd_step.restype = st
     L.reuse_net_sgd_step.argtypes = [P, P, ctypes.c_float, P]
+    L.reuse_net_set_weights_device.restype = st
+    L.reuse_net_set_weights_device.argtypes = [P, P, P]
     L.reuse_net_variants_static.restype = st
     L.reuse_net_variants_static.argtypes = [P, I32, I32, P, ctypes.c_int, I32, P, P, I32, P, P]
     for name in ("reuse_net_get_pixel_mask", "reuse_net_get_tile_mask"):
@@ -224,6 +226,10 @@ def reuse_net_backward(net: int, n: int, dev_stream_ids: int, dev_dlogits: int, 
 
 def reuse_net_sgd_step(net: int, dev_grads: int, lr: float, hip_stream: int) -> None:
     _check(load_library().reuse_net_sgd_step(net, dev_grads, lr, hip_stream), net)
+
+
+def reuse_net_set_weights_device(net: int, dev_params: int, hip_stream: int) -> None:
+    _check(load_library().reuse_net_set_weights_device(net, dev_params, hip_stream), net)
 
 
 def reuse_net_get_pixel_mask(net: int, layer: int, stream_id: int, words: int) -> np.ndarray:
@@ -554,6 +560,31 @@ class ReuseNet:
         self._check_dev(grads, "grads", t.float32, (self.grad_elems(),))
         s = (stream or t.cuda.current_stream(self.device)).cuda_stream
         reuse_net_sgd_step(self.handle, grads.data_ptr(), lr, s)
+
+    def set_weights_device(self, params, stream=None):
+        """New weights from a device buffer in the gradient layout (see pack_params);
+        every slot recomputes everything on its next step."""
+        t = self.torch
+        self._check_dev(params, "params", t.float32, (self.grad_elems(),))
+        s = (stream or t.cuda.current_stream(self.device)).cuda_stream
+        reuse_net_set_weights_device(self.handle, params.data_ptr(), s)
+
+    def pack_params(self, weights):
+        """(conv_w, conv_b, dense_w, dense_b) as one float32 device buffer in the
+        gradient layout: each layer's OIHW weights then its bias, then the dense
+        weights and bias (argument marshalling: a concatenation, no arithmetic)."""
+        conv_w, conv_b, dense_w, dense_b = weights
+        parts = []
+        for w, b in zip(conv_w, conv_b):
+            parts += [np.asarray(w, dtype=np.float32).ravel(), np.asarray(b, dtype=np.float32).ravel()]
+        parts += [np.asarray(dense_w, dtype=np.float32).ravel(), np.asarray(dense_b, dtype=np.float32).ravel()]
+        flat = np.concatenate(parts)
+        n = self.grad_elems()
+        if n == 0:
+            raise RuntimeError("this net has no device weight layout (training calls unsupported)")
+        if flat.size != n:
+            raise ValueError(f"weights hold {flat.size} floats, the net needs {n}")
+        return self.torch.from_numpy(flat).to(self.device)
 
     # -- introspection
     def pixel_mask(self, layer: int, stream_id: int) -> np.ndarray:

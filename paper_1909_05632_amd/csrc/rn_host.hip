@@ -955,6 +955,52 @@ BwdPlan plan_backward(const Plan &p, int n, int cus) {
     return b;
 }
 
+// Every packed weight copy the kernels read, rewritten from a buffer in the
+// gradient layout: assign = false applies fl(w - fl(lr g)) (an SGD step),
+// assign = true stores the values themselves (new weights).  Then every slot
+// is marked unprimed: the caches hold activations of the old weights.
+rn_status write_packed(reuse_net *net, const float *src, float lr, bool assign, hipStream_t s, const char *what) {
+    const Plan &p = net->p;
+    const GradLayout gl = grad_layout(p);
+    hipError_t e = hipSuccess;
+    auto upd = [&](size_t off, size_t count, int kind, const float *g, int cin, int cout) {
+        if (e != hipSuccess || count == 0) return;
+        SgdArgs a{};
+        a.dst = net->at<float>(off);
+        a.count = count;
+        a.kind = kind;
+        a.g = g;
+        a.lr = lr;
+        a.assign = assign ? 1 : 0;
+        a.cin = cin;
+        a.cout = cout;
+        a.C = p.C[p.L];
+        a.H = p.Hl[p.L];
+        a.W = p.Wl[p.L];
+        a.TW = p.TWl[p.L];
+        a.ntiles = p.ntl[p.L];
+        a.n_out = p.N;
+        a.K = p.K;
+        e = timed(net, RN_PHASE_SGD, s, [&] { return launch_sgd(a, s); });
+    };
+    for (int l = 0; l < p.L; ++l) {
+        upd(p.o_w[l], p.w_elems[l], l == 0 ? SGD_FIRST : SGD_MFMA, src + gl.w[l], p.C[l], p.C[l + 1]);
+        upd(p.o_b[l], p.C[l + 1], SGD_PLAIN, src + gl.b[l], 0, 0);
+        if (l > 0) upd(p.o_wt[l], p.wt_elems[l], SGD_DX, src + gl.w[l], p.C[l], p.C[l + 1]);
+    }
+    upd(p.o_wd, (size_t)p.N * p.K, SGD_DENSE, src + gl.dw, 0, 0);
+    if (p.head_mode == RN_HEAD_TILES && !p.part_f32)
+        upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, src + gl.dw, 0, 0);
+    if (p.part_f32) upd(p.o_hw2, tile_part_f32_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_PART, src + gl.dw, 0, 0);
+    upd(p.o_bd, p.N, SGD_PLAIN, src + gl.db, 0, 0);
+    if (e == hipSuccess) e = timed(net, RN_PHASE_SGD, s, [&] { return launch_unprime(net->at<int32_t>(p.o_primed), p.S, s); });
+    if (e != hipSuccess) return net->fail(RN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+    net->last_stream = s;
+    net->has_step = true;
+    net->err.clear();
+    return RN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1212,48 +1258,16 @@ rn_status reuse_net_backward(reuse_net *net, int32_t n, const int32_t *ids_in, c
 
 rn_status reuse_net_sgd_step(reuse_net *net, const float *grads, float lr, void *stream) {
     if (!net) return RN_EINVAL;
-    const Plan &p = net->p;
-    if (p.train_why) return net->fail(RN_EUNSUPPORTED, p.train_why);
+    if (net->p.train_why) return net->fail(RN_EUNSUPPORTED, net->p.train_why);
     if (!grads) return net->fail(RN_EINVAL, "grads are NULL");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const GradLayout gl = grad_layout(p);
-    hipError_t e = hipSuccess;
-    auto upd = [&](size_t off, size_t count, int kind, const float *g, int cin, int cout) {
-        if (e != hipSuccess || count == 0) return;
-        SgdArgs a{};
-        a.dst = net->at<float>(off);
-        a.count = count;
-        a.kind = kind;
-        a.g = g;
-        a.lr = lr;
-        a.cin = cin;
-        a.cout = cout;
-        a.C = p.C[p.L];
-        a.H = p.Hl[p.L];
-        a.W = p.Wl[p.L];
-        a.TW = p.TWl[p.L];
-        a.ntiles = p.ntl[p.L];
-        a.n_out = p.N;
-        a.K = p.K;
-        e = timed(net, RN_PHASE_SGD, s, [&] { return launch_sgd(a, s); });
-    };
-    for (int l = 0; l < p.L; ++l) {
-        upd(p.o_w[l], p.w_elems[l], l == 0 ? SGD_FIRST : SGD_MFMA, grads + gl.w[l], p.C[l], p.C[l + 1]);
-        upd(p.o_b[l], p.C[l + 1], SGD_PLAIN, grads + gl.b[l], 0, 0);
-        if (l > 0) upd(p.o_wt[l], p.wt_elems[l], SGD_DX, grads + gl.w[l], p.C[l], p.C[l + 1]);
-    }
-    upd(p.o_wd, (size_t)p.N * p.K, SGD_DENSE, grads + gl.dw, 0, 0);
-    if (p.head_mode == RN_HEAD_TILES && !p.part_f32)
-        upd(p.o_hw, tile_head_w_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_HEAD, grads + gl.dw, 0, 0);
-    if (p.part_f32) upd(p.o_hw2, tile_part_f32_elems(p.ntl[p.L], p.C[p.L], p.N), SGD_TILE_PART, grads + gl.dw, 0, 0);
-    upd(p.o_bd, p.N, SGD_PLAIN, grads + gl.db, 0, 0);
-    // Every cache now holds activations of the old weights: all slots unprimed.
-    if (e == hipSuccess) e = timed(net, RN_PHASE_SGD, s, [&] { return launch_unprime(net->at<int32_t>(p.o_primed), p.S, s); });
-    if (e != hipSuccess) return net->fail(RN_EHIP, std::string("sgd step: ") + hipGetErrorString(e));
-    net->last_stream = s;
-    net->has_step = true;
-    net->err.clear();
-    return RN_OK;
+    return write_packed(net, grads, lr, false, static_cast<hipStream_t>(stream), "sgd step");
+}
+
+rn_status reuse_net_set_weights_device(reuse_net *net, const float *params, void *stream) {
+    if (!net) return RN_EINVAL;
+    if (net->p.train_why) return net->fail(RN_EUNSUPPORTED, net->p.train_why);
+    if (!params) return net->fail(RN_EINVAL, "params are NULL");
+    return write_packed(net, params, 0.f, true, static_cast<hipStream_t>(stream), "device weight update");
 }
 
 rn_status reuse_net_reset(reuse_net *net, int32_t sid) {

@@ -713,11 +713,14 @@ __device__ inline long long sgd_src(const SgdArgs &a, size_t d) {
 
 // Two roundings, fl(w - fl(lr g)), as a host computing the same update in
 // float32 does: contraction into one fused multiply-add is switched off.
+// assign: a plain gather into the packed layout (padding elements 0).
 __global__ __launch_bounds__(256) void k_sgd(SgdArgs a) {
 #pragma clang fp contract(off)
     for (size_t d = (size_t)blockIdx.x * blockDim.x + threadIdx.x; d < a.count; d += (size_t)gridDim.x * blockDim.x) {
         const long long s = sgd_src(a, d);
-        if (s >= 0) {
+        if (a.assign) {
+            a.dst[d] = s >= 0 ? a.g[s] : 0.f;
+        } else if (s >= 0) {
             const float step = a.lr * a.g[s];
             a.dst[d] = a.dst[d] - step;
         }

@@ -50,14 +50,17 @@ struct BwdArgs {
 // Plain SGD step applied in place to one packed weight buffer: every element
 // that holds weight v of the natural layout becomes fl(v - fl(lr * g)), with g
 // the gradient of that weight, so each packed copy stays the packing of the
-// updated weights.  kind: what layout dst has.
+// updated weights.  With assign set, the element becomes g itself (and a
+// padding element 0): the packing of the weights g, written on the device.
+// kind: what layout dst has.
 enum SgdKind { SGD_PLAIN = 0, SGD_FIRST = 1, SGD_MFMA = 2, SGD_DENSE = 3, SGD_TILE_HEAD = 4, SGD_DX = 5, SGD_TILE_PART = 6 };
 struct SgdArgs {
     float *dst;
     size_t count;                 // elements of dst
     int kind;
-    const float *g;               // gradient in the natural layout of this weight (OIHW, or [n_out][C][H][W])
+    const float *g;               // gradient (or, with assign, the weights) in the natural layout (OIHW, or [n_out][C][H][W])
     float lr;
+    int assign;
     int cin, cout;                // conv layers
     int C, H, W, TW, ntiles, n_out;   // dense / tile head / tile partials: last layer
     size_t K;

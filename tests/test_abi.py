@@ -168,6 +168,8 @@ def test_null_net_calls_return_einval():
     assert lib.reuse_net_get_stats(None, None) == B.RN_EINVAL
     assert lib.reuse_net_get_profile(None, None) == B.RN_EINVAL
     assert lib.reuse_net_set_weights(None, None, None) == B.RN_EINVAL
+    assert lib.reuse_net_set_weights_device(None, None, None) == B.RN_EINVAL
+    assert lib.reuse_net_sgd_step(None, None, 0.0, None) == B.RN_EINVAL
     assert lib.reuse_net_variant_scratch_bytes(None, 4, 0) == 0
     assert lib.reuse_net_variants(None, 0, 4, None, 0, 1, None, None, 0, None, 0, None, None) == B.RN_EINVAL
     lib.reuse_net_destroy(None)

@@ -174,3 +174,67 @@ def test_sgd_step_equals_net_with_updated_weights(torch):
         assert np.array_equal(ga.cpu().numpy().view(np.uint32), gb.cpu().numpy().view(np.uint32)), base
         a.close()
         b.close()
+
+
+def test_set_weights_device_equals_created_nets(torch):
+    # reuse_net_set_weights_device rewrites every packed copy on the device from
+    # a flat parameter buffer: the net must then compute exactly as one created
+    # with those weights (logits, masks, work lists and gradients bit for bit),
+    # and exactly as one whose weights came through the host path
+    # (reuse_net_set_weights), on the epilogue tile head, the float32 tile
+    # partials of a staged last layer (128 -> 128) and the full-read head.
+    for base, h, w, n, head in (("atari-ds2-256x64", 40, 32, 3, "tiles"), ("fullres-1024x32", 42, 32, 2, "tiles"),
+                                ("fullres-1024x32", 42, 32, 2, "full")):
+        wl = _wl(base, h, w, n)
+        F = 7
+        u8, _ = _inputs(wl, n, F)
+        w0 = synth.net_weights(wl, bias_std=0.05)
+        w1 = synth.net_weights(wl, bias_std=0.05, seed_extra=3)
+        dev = torch.from_numpy(u8).cuda()
+        a = _net(wl, n, w0, head)
+        for t in range(2):
+            a.step(dev[t][:, None].contiguous())
+        a.set_weights_device(a.pack_params(w1))
+        b = _net(wl, n, w1, head)
+        L = len(wl.convs)
+        g = torch.from_numpy(np.random.default_rng(2).normal(0, 1, (n, wl.n_out)).astype(np.float32)).cuda()
+
+        def same(t0, t1, label):
+            for t in range(t0, t1):
+                la = a.step(dev[t][:, None].contiguous()).cpu().numpy()
+                lb = b.step(dev[t][:, None].contiguous()).cpu().numpy()
+                assert np.array_equal(la.view(np.uint32), lb.view(np.uint32)), (base, head, label, t)
+                if t == t0:                                    # unprimed by the update: all dirty
+                    assert all(a.tile_mask_u8(L, i).all() for i in range(n))
+                for l in range(1, L + 1):
+                    assert np.array_equal(a.worklist(l), b.worklist(l)), (base, head, label, t, l)
+            ga, gb = a.new_grads(), b.new_grads()
+            a.backward(g, ga)
+            b.backward(g, gb)
+            assert np.array_equal(ga.cpu().numpy().view(np.uint32), gb.cpu().numpy().view(np.uint32)), \
+                (base, head, label)
+
+        same(2, 5, "device vs created")
+        # Back to w0: device path on a, host path on b.
+        a.set_weights_device(a.pack_params(w0))
+        b.set_weights(w0)
+        same(5, F, "device vs host")
+        a.close()
+        b.close()
+
+
+def test_set_weights_device_unsupported_net(torch):
+    # A net the training calls do not support (general-layer DQN trunk) refuses
+    # the device update before reading the buffer, and keeps its weights.
+    from paper_1909_05632_amd import binding as B
+    wl = synth.WORKLOADS["dqn-84x84-256x64"]
+    weights = synth.net_weights(wl)
+    from paper_1909_05632_amd import ReuseNet
+    net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, 2, weights, stack=wl.stack)
+    assert net.grad_elems() == 0
+    buf = torch.zeros(16, dtype=torch.float32, device="cuda")
+    rc = B.load_library().reuse_net_set_weights_device(net.handle, buf.data_ptr(), None)
+    assert rc == B.RN_EUNSUPPORTED
+    with pytest.raises(RuntimeError):
+        net.pack_params(weights)
+    net.close()
