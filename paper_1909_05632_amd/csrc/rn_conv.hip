@@ -916,12 +916,331 @@ __device__ inline void split_stage(floatx4 (&acc)[T][NBW], const float *halos, c
     }
 }
 
+// ---- staged layers, chunk-streamed form (launches without variant overlays)
+//
+// A block of four waves computes a group of T tiles, each wave COUT / 4 output
+// channels of all of them, walking K one 16-channel chunk at a time and, within
+// a chunk, the nine kernel positions (a stage = one position of one chunk:
+// 4 k-steps x T x COUT / 64 matrix ops per wave).  Only three chunks of the
+// group's halos are in LDS at once: chunk K is read, K + 1 is ready, K + 2 is
+// in flight, each loaded straight from global memory into LDS with
+// global_load_lds_dwordx4 (lane i writes 16 bytes at base + 16 i, so the
+// lanes' source addresses lay out the buffer: tile t's 6 x 6 pixels x 4
+// channel quads at 16-byte slot 150 t + 25 hy + 4 hx + quad, the 25-slot row
+// putting the 16 pixels of a 16-lane read in 16 distinct bank groups;
+// padding slots, pixels outside the image and tiles past the end load from a
+// zero page).  The stage sequence runs on across groups: when a chunk's last
+// stage starts, the waves have read all of it, so after one block barrier it
+// is refilled with the chunk three ahead (the next group's when the group
+// runs out), 18 stages before it is read.  Weights stream per stage through a
+// ring of five LDS slots per wave (stage q + 4 loaded at the start of stage q)
+// and each stage's operands are read during the previous stage's matrix ops.
+// The memory counter the waits use retires loads and stores in issue order,
+// so every wait names how many later operations it may leave in flight;
+// loads of the compiler's own (work items, bias) are scalar or waited for
+// before any ring load is issued.  The epilogue applies bias, ReLU and the
+// zero outside the image, transposes each lane quad's 4 x 4 values with DPP
+// moves so a lane holds four channels of one pixel, and stores 16 bytes a
+// lane straight to the cache.  The order of the sums over K (chunk, then
+// position, then channel) is the same for every T, so a tile's outputs do not
+// depend on the group size a launch picks.
+template <int CIN, int COUT, int T>
+struct Chunked {
+    static constexpr int NCH = CIN / 16;             // 16-channel chunks
+    static constexpr int NQ = 9 * NCH;               // stages per group
+    static constexpr int NB = COUT / 16;             // 16-output blocks
+    static constexpr int NBW = COUT / 64;            // 16-output blocks per wave
+    static constexpr int CW = 16 * NBW;              // output channels per wave
+    static constexpr int WSW = 16 * CW;              // weight floats per stage and wave
+    static constexpr int NWB = 5;                    // weight ring slots per wave
+    static constexpr int RS = 25;                    // 16-byte slots per halo row
+    static constexpr int HT = 6 * RS;                // slots per tile of a chunk buffer
+    static constexpr int HD = (T * HT * 16 + 1023) / 1024;   // 1 KB loads per chunk buffer
+    static constexpr int HB = HD * 1024;             // bytes per chunk buffer
+    static constexpr int HDW = (HD + 3) / 4;         // most loads of one wave per chunk
+    static constexpr int HDMIN = HD / 4;             // fewest
+    static constexpr int NS = T * NBW;               // 16-byte-a-lane stores per group and wave
+    static constexpr size_t lds_bytes = 3 * (size_t)HB + (size_t)4 * NWB * WSW * sizeof(float);
+    static_assert(CIN % 16 == 0 && COUT % 64 == 0 && NCH >= 3, "whole chunks, at least three per group");
+    static_assert(WSW == 256 * NBW, "one 1 KB load per output block and stage");
+    static_assert(T <= 16 && T % 4 == 0, "group size");
+};
+
+// 16-byte zero page: the source of every halo slot that holds no input value
+// (chunk c reads 16 c floats further on).
+__device__ __align__(16) float g_zero_page[128];
+
+// Item words of tiles g .. g + T - 1 (clamped to the last item; the callers
+// mark tiles past `end` themselves), as scalar loads issued in assembly: the
+// compiler would make these vector loads, and its wait for them would also
+// wait for every ring load issued before their use.
+template <bool DENSE, int T>
+__device__ inline void load_items(const ConvArgs &a, int g, int end, uint32_t (&it)[T]) {
+    uint32_t raw[T];
+#pragma unroll
+    for (int u = 0; u < T; ++u) {
+        const int t = min(g + u, end - 1);
+        const uint32_t *p;
+        if constexpr (DENSE) {
+            constexpr int CH = 32;                        // as item_word<true>
+            const int per_chunk = CH * a.TH * a.TW;
+            const int c = t / per_chunk, rr = t - c * per_chunk;
+            const int nc = min(CH, a.dense_n - c * CH);
+            const int tile = rr / nc;
+            const int ty = tile / a.TW;
+            p = reinterpret_cast<const uint32_t *>(a.ids) + c * CH + (rr - tile * nc);
+            it[u] = ((uint32_t)ty << 8) | (uint32_t)(tile - ty * a.TW);
+        } else {
+            p = a.wl + t;
+            it[u] = 0;
+        }
+        asm volatile("s_load_dword %0, %1, 0x0" : "=s"(raw[u]) : "s"(p) : "memory");
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int u = 0; u < T; ++u) {
+        asm volatile("" : "+s"(raw[u]));                  // used only after the wait
+        it[u] |= DENSE ? raw[u] << 16 : raw[u];
+    }
+}
+
+// Source of each of this wave's halo loads for chunk 0 of the group at g.
+template <int CIN, int COUT, int T>
+__device__ inline void chunk_sources(const ConvArgs &a, int g, int end, const uint32_t (&it)[T],
+                                     const float *(&src)[Chunked<CIN, COUT, T>::HDW], int wave, int lane) {
+    using C = Chunked<CIN, COUT, T>;
+    const float *in = static_cast<const float *>(a.in);
+#pragma unroll
+    for (int k = 0; k < C::HDW; ++k) {
+        const int s = 64 * (wave + 4 * k) + lane;
+        const int t = s / C::HT, rem = s - t * C::HT;
+        const int hy = rem / C::RS, r2 = rem - hy * C::RS;
+        const int hx = r2 >> 2, kq = r2 & 3;
+        uint32_t e = it[0];
+#pragma unroll
+        for (int u = 1; u < T; ++u) e = t == u ? it[u] : e;
+        const TileRef r = item_ref(a, e);
+        const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
+        const bool ok = t < T && g + t < end && r2 < 24 && y >= 0 && y < a.H && x >= 0 && x < a.W;
+        src[k] = ok ? in + (size_t)r.slot * a.in_stride +
+                          ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CIN + 4 * kq
+                    : g_zero_page + 4 * kq;
+    }
+}
+
+// Chunk c of the halos into the chunk buffer at LDS byte address dst.
+template <int CIN, int COUT, int T>
+__device__ inline void dma_chunk(const float *const (&src)[Chunked<CIN, COUT, T>::HDW], int c, uint32_t dst,
+                                 int wave) {
+    using C = Chunked<CIN, COUT, T>;
+#pragma unroll
+    for (int k = 0; k < C::HDW; ++k) {
+        const int j = wave + 4 * k;
+        if (k + 1 < C::HDW || j < C::HD) lds_dma16(src[k] + 16 * c, dst + 1024u * j);
+    }
+}
+
+// Stage s (chunk s / 9, position s % 9) of this wave's weights into the ring
+// slot at LDS byte address dst, [output block][lane][4].
+template <int CIN, int COUT, int T>
+__device__ inline void dma_wchunk(const float *wg, int s, uint32_t dst, int wave, int lane) {
+    using C = Chunked<CIN, COUT, T>;
+    const int c = s / 9, kpos = s - 9 * c;
+#pragma unroll
+    for (int nb = 0; nb < C::NBW; ++nb)
+        lds_dma16(wg + ((size_t)(kpos * C::NCH + c) * C::NB + wave * C::NBW + nb) * 256 + 4 * lane,
+                  dst + 1024u * nb);
+}
+
+// A fragments of the T tiles at kernel position kpos from the chunk buffer
+// (hb: this lane's slot of tile 0, position 0) and the B fragments of the
+// stage's ring slot (wb: this lane's 16 bytes of output block 0).
+template <int CIN, int COUT, int T>
+__device__ inline void chunk_ops(SplitOps<T, Chunked<CIN, COUT, T>::NBW> &o, const float *hb, const float *wb,
+                                 int kpos) {
+    using C = Chunked<CIN, COUT, T>;
+    const int ky = kpos / 3, kx = kpos - 3 * ky;
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+        o.a[t] = *reinterpret_cast<const float4 *>(hb + 4 * (t * C::HT + ky * C::RS + kx * 4));
+#pragma unroll
+    for (int nb = 0; nb < C::NBW; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + 256 * nb);
+}
+
+// 4 x 4 transpose inside each lane quad: lane 4 m + b holds v[i] = X[i][b] on
+// entry and X[b][i] on return (two exchanges, over lane bit 0 with element
+// bit 0, then over lane bit 1 with element bit 1).
+__device__ inline void quad_transpose(float (&v)[4], int b) {
+    {
+        const bool hi = b & 1;
+        const float s0 = hi ? v[0] : v[1], s1 = hi ? v[2] : v[3];
+        const float r0 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s0), 0xb1, 0xf, 0xf, false));
+        const float r1 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s1), 0xb1, 0xf, 0xf, false));
+        if (hi) {
+            v[0] = r0;
+            v[2] = r1;
+        } else {
+            v[1] = r0;
+            v[3] = r1;
+        }
+    }
+    {
+        const bool hi = b & 2;
+        const float s0 = hi ? v[0] : v[2], s1 = hi ? v[1] : v[3];
+        const float r0 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s0), 0x4e, 0xf, 0xf, false));
+        const float r1 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s1), 0x4e, 0xf, 0xf, false));
+        if (hi) {
+            v[0] = r0;
+            v[1] = r1;
+        } else {
+            v[2] = r0;
+            v[3] = r1;
+        }
+    }
+}
+
+template <int CIN, int COUT, bool DENSE, int T>
+__device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
+    using C = Chunked<CIN, COUT, T>;
+    constexpr int NBW = C::NBW;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const XcdRange xr = xcd_range(cnt, T);
+    if (xr.first >= xr.end) return;                       // uniform per block
+    const int mrow = lane & 15, kq = lane >> 4;
+    unsigned char *lds = reinterpret_cast<unsigned char *>(smem);
+    float *wring = reinterpret_cast<float *>(lds + 3 * C::HB) + wave * C::NWB * C::WSW;
+    const uint32_t hlds = lds_addr(lds), wlds = lds_addr(wring);
+    const float *wg = static_cast<const float *>(a.w);
+    // this lane's A slot (halo pixel (mrow & 3, mrow >> 2), channel quad kq) and B slot
+    const float *ha = reinterpret_cast<const float *>(lds) + 4 * ((mrow & 3) * C::RS + (mrow >> 2) * 4 + kq);
+    const float *wa = wring + 4 * lane;
+
+    // Bias of the lane's output channels, waited for before any ring load.
+    float bias[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) bias[nb] = a.bias[wave * C::CW + nb * 16 + mrow];
+    asm volatile("" ::"v"(bias[0]), "v"(bias[NBW - 1]));
+
+    // Prologue: halo chunks 0-2 and weight stages 0-3 of the first group.
+    const float *src[C::HDW];
+    {
+        uint32_t it0[T];
+        load_items<DENSE, T>(a, xr.first, xr.end, it0);
+        chunk_sources<CIN, COUT, T>(a, xr.first, xr.end, it0, src, wave, lane);
+    }
+#pragma unroll
+    for (int k = 0; k < 3; ++k) dma_chunk<CIN, COUT, T>(src, k, hlds + k * C::HB, wave);
+#pragma unroll
+    for (int q = 0; q < C::NWB - 1; ++q) dma_wchunk<CIN, COUT, T>(wg, q, wlds + q * C::WSW * 4, wave, lane);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+
+    int hk = 0;                                           // chunk buffer of the current chunk
+    int qs = 0;                                           // ring slot of the current stage
+    int dc = 3;                                           // next chunk to load (of the group at g, or, once
+                                                          // past NCH, of the next group)
+    SplitOps<T, NBW> cur;
+    chunk_ops<CIN, COUT, T>(cur, ha, wa, 0);
+    for (int g = xr.first; g < xr.end; g += xr.stride) {   // uniform per block
+        const bool stores_before = g != xr.first;         // the previous group's stores are in flight
+        floatx4 acc[T][NBW];
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) acc[t][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < C::NCH; ++c) {
+#pragma unroll
+            for (int kp = 0; kp < 9; ++kp) {
+                if (kp == 8) {
+                    // This chunk's reads are done in every wave, chunk + 1 is
+                    // in LDS: its loads (issued two chunks ago) are followed
+                    // by 17 stages' weight loads and one chunk's halo loads.
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(17 * NBW + C::HDMIN) : "memory");
+                    lds_barrier();
+                }
+                // Stage q + 4 into the slot stage q - 1 used.
+                const int s4 = c * 9 + kp + 4;
+                dma_wchunk<CIN, COUT, T>(wg, s4 >= C::NQ ? s4 - C::NQ : s4,
+                                         wlds + ((qs + C::NWB - 1) % C::NWB) * C::WSW * 4, wave, lane);
+                if (kp == 8) {
+                    // Refill this chunk's buffer with the chunk three ahead.
+                    if (dc == C::NCH) {                       // on to the next group
+                        uint32_t it_next[T];
+                        load_items<DENSE, T>(a, min(g + xr.stride, xr.end - 1), xr.end, it_next);
+                        chunk_sources<CIN, COUT, T>(a, g + xr.stride, xr.end, it_next, src, wave, lane);
+                        dc = 0;
+                    }
+                    dma_chunk<CIN, COUT, T>(src, dc, hlds + hk * C::HB, wave);
+                    ++dc;
+                }
+                // Matrix ops of this stage; the next stage's operands read
+                // meanwhile, once its weights are in: they were loaded three
+                // stages ago and are followed by 3 stages' weight loads, plus
+                // a chunk's halo loads when a chunk boundary is that close,
+                // plus the previous group's stores at a group's start.
+                SplitOps<T, NBW> nxt;
+                const int qn = qs + 1 == C::NWB ? 0 : qs + 1;
+                const int hn = kp == 8 ? (hk + 1 == 3 ? 0 : hk + 1) : hk;
+                if (kp >= 3 && kp <= 7) {
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW) : "memory");
+                } else if (c == 0 && kp <= 2 && stores_before) {
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW + C::HDMIN + C::NS) : "memory");
+                } else {
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW + C::HDMIN) : "memory");
+                }
+                chunk_ops<CIN, COUT, T>(nxt, ha + hn * (C::HB / 4), wa + qn * C::WSW, kp == 8 ? 0 : kp + 1);
+                __builtin_amdgcn_sched_barrier(0);
+                split_mma<T, NBW>(acc, cur);
+                __builtin_amdgcn_sched_barrier(0);
+                cur = nxt;
+                qs = qn;
+                hk = hn;
+            }
+        }
+        // Epilogue: bias, ReLU and the zero outside the image on the bit
+        // patterns (a float above zero has a positive int pattern), the quad
+        // transpose, 16 bytes a lane: pixel (b, kq) of the tile, channels
+        // 16 nb + 4 m .. + 3 of the wave's, for lane 16 kq + 4 m + b.
+        const int qb = lane & 3, qm = (lane >> 2) & 3;
+        uint32_t it_cur[T];
+        load_items<DENSE, T>(a, g, xr.end, it_cur);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            if (g + t >= xr.end) break;                   // uniform
+            const TileRef r = item_ref(a, it_cur[t]);
+            const int col_keep = ~((a.W - 1 - (r.tx * kTile + kq)) >> 31);
+            float *dst = static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
+                         (size_t)r.tile * kTilePx * COUT + (qb * 4 + kq) * COUT + wave * C::CW + 4 * qm;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                float v[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int keep = col_keep & ~((a.H - 1 - (r.ty * kTile + i)) >> 31);
+                    v[i] = __int_as_float(max(__float_as_int(acc[t][nb][i] + bias[nb]), 0) & keep);
+                }
+                quad_transpose(v, qb);
+                *reinterpret_cast<float4 *>(dst + 16 * nb) = make_float4(v[0], v[1], v[2], v[3]);
+            }
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");      // loads issued for a group that does not come
+}
+
 template <int CIN, int COUT, bool DENSE, bool VAR>
 __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
     using M = Mfma<CIN, COUT>;
     using S = Staged<CIN, COUT>;
     static_assert(M::TAIL == 0, "staged layers take whole 16-channel blocks");
     extern __shared__ float smem[];
+    if constexpr (!VAR) {
+        // Launches without overlays stream the halos by chunk: groups of 8
+        // tiles when every block has at least 16 of them to do, else of 4.
+        const int cnt = work_count<DENSE>(a);
+        if (cnt >= 16 * 8 * (int)gridDim.x) chunk_path<CIN, COUT, DENSE, 8>(a, cnt, smem);
+        else chunk_path<CIN, COUT, DENSE, 4>(a, cnt, smem);
+    } else {
     __shared__ float s_bias[COUT];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1037,6 +1356,7 @@ __global__ __launch_bounds__(256) void k_conv_mfma_staged(ConvArgs a) {
 #pragma unroll
         for (int h = 0; h < S::TW; ++h) store_halo_masked<CIN, COUT>(halos + (wave + 4 * h) * M::HALO, hreg[h], hok[h], lane);
         lds_barrier();                                    // the next group's halos visible to every wave
+    }
     }
 }
 
@@ -1301,8 +1621,8 @@ hipError_t run_mfma(const ConvArgs &a, int cus, hipStream_t s) {
         return run_resident<CIN, COUT, DENSE, false, VAR>(a, cus, s);
     } else {
         if (a.fuse_first || a.n_out > 0) return hipErrorInvalidValue;   // head partials come from their own kernel
-        constexpr size_t lds = Staged<CIN, COUT>::lds_bytes;
-        static_assert(lds <= kLdsBudget, "staged layer exceeds LDS");
+        constexpr size_t lds = VAR ? Staged<CIN, COUT>::lds_bytes : Chunked<CIN, COUT, 8>::lds_bytes;
+        static_assert(lds <= kLdsBudget && Chunked<CIN, COUT, 4>::lds_bytes <= lds, "staged layer exceeds LDS");
         auto kern = k_conv_mfma_staged<CIN, COUT, DENSE, VAR>;
         static hipError_t attr = set_lds(kern, lds);
         if (attr != hipSuccess) return attr;

@@ -415,3 +415,33 @@ def test_large_frame_masks_beyond_64k_lds(torch):
         prev = xs
     a.close()
     b.close()
+
+
+def test_staged_group_size_does_not_change_results(torch):
+    # The staged layers (64->128, 128->128) run groups of 8 tiles when every
+    # block has at least 16 groups to do and groups of 4 otherwise; both sum
+    # over K in one order, so a tile's outputs are the same bits either way.
+    # A full pass over 400 streams (35200 tiles per layer: groups of 8) against
+    # the same frames in batches of 8 streams (704 tiles: groups of 4): logits
+    # of every stream and the staged layers' caches of sampled streams, bit
+    # for bit, and the logits against the oracle.
+    n = 400
+    wl = synth.Workload(cid=98, streams=n, frames=1, h=42, w=32, convs=(64, 128, 128), n_out=18,
+                        n_sprites=3, smin=3, smax=6, vmin=1, vmax=3)
+    weights = synth.net_weights(wl, bias_std=0.05)
+    x = synth.to_f32(synth.sprite_batch(wl, streams=range(n), frames=1))[0]      # [n][H][W]
+    dev = torch.from_numpy(x[:, None]).cuda()
+    a, b = make_net(wl, n, weights), make_net(wl, n, weights)
+    la = a.full(dev).cpu().numpy()
+    lb = np.concatenate([b.full(dev[i:i + 8].contiguous(),
+                                stream_ids=torch.arange(i, i + 8, dtype=torch.int32).cuda()).cpu().numpy()
+                         for i in range(0, n, 8)])
+    assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
+    for i in (0, 7, 8, 133, 250, 399):
+        for l in (2, 3):
+            assert np.array_equal(a.activation(i, l).view(np.uint32), b.activation(i, l).view(np.uint32)), (i, l)
+    sample = [0, 199, 399]
+    ref, _ = oracle.forward(oracle_net(wl), *weights, x[sample][:, None])
+    assert np.abs(la[sample] - ref).max() <= ATOL_F32
+    a.close()
+    b.close()
