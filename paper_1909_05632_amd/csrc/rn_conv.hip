@@ -926,10 +926,10 @@ __device__ inline void split_stage(floatx4 (&acc)[T][NBW], const float *halos, c
 // in flight, each loaded straight from global memory into LDS with
 // global_load_lds_dwordx4 (lane i writes 16 bytes at base + 16 i, so the
 // lanes' source addresses lay out the buffer: tile t's 6 x 6 pixels x 4
-// channel quads at 16-byte slot 150 t + 25 hy + 4 hx + quad, the 25-slot row
-// putting the 16 pixels of a 16-lane read in 16 distinct bank groups;
-// padding slots, pixels outside the image and tiles past the end load from a
-// zero page).  The stage sequence runs on across groups: when a chunk's last
+// channel quads at 16-byte slot 144 t + 24 hy + 4 hx + quad; pixels outside
+// the image and tiles past the end load from a zero page).  Rows padded to
+// 25 or 27 slots, which put the 16 pixels of a 16-lane read in 16 distinct
+// bank groups, measured no faster and with the same bank-conflict count.  The stage sequence runs on across groups: when a chunk's last
 // stage starts, the waves have read all of it, so after one block barrier it
 // is refilled with the chunk three ahead (the next group's when the group
 // runs out), 18 stages before it is read.  Weights stream per stage through a
@@ -953,7 +953,8 @@ struct Chunked {
     static constexpr int CW = 16 * NBW;              // output channels per wave
     static constexpr int WSW = 16 * CW;              // weight floats per stage and wave
     static constexpr int NWB = 5;                    // weight ring slots per wave
-    static constexpr int RS = 25;                    // 16-byte slots per halo row
+    static constexpr int WL = NWB - 2;               // stages between a weight load and its wait
+    static constexpr int RS = 24;                    // 16-byte slots per halo row
     static constexpr int HT = 6 * RS;                // slots per tile of a chunk buffer
     static constexpr int HD = (T * HT * 16 + 1023) / 1024;   // 1 KB loads per chunk buffer
     static constexpr int HB = HD * 1024;             // bytes per chunk buffer
@@ -964,6 +965,7 @@ struct Chunked {
     static_assert(CIN % 16 == 0 && COUT % 64 == 0 && NCH >= 3, "whole chunks, at least three per group");
     static_assert(WSW == 256 * NBW, "one 1 KB load per output block and stage");
     static_assert(T <= 16 && T % 4 == 0, "group size");
+    static_assert(WL >= 2 && WL <= 8 && WL * NBW + HDMIN + NS <= 63, "the stage waits below assume these");
 };
 
 // 16-byte zero page: the source of every halo slot that holds no input value
@@ -1122,7 +1124,7 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
     for (int nb = 0; nb < NBW; ++nb) bias[nb] = a.bias[wave * C::CW + nb * 16 + mrow];
     asm volatile("" ::"v"(bias[0]), "v"(bias[NBW - 1]));
 
-    // Prologue: halo chunks 0-2 and weight stages 0-3 of the first group.
+    // Prologue: halo chunks 0-2 and weight stages 0 .. NWB - 2 of the first group.
     const float *src[C::HDW];
     {
         uint32_t it0[T];
@@ -1159,8 +1161,8 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(17 * NBW + C::HDMIN) : "memory");
                     lds_barrier();
                 }
-                // Stage q + 4 into the slot stage q - 1 used.
-                const int s4 = c * 9 + kp + 4;
+                // Stage q + NWB - 1 into the slot stage q - 1 used.
+                const int s4 = c * 9 + kp + C::NWB - 1;
                 dma_wchunk<CIN, COUT, T>(wg, s4 >= C::NQ ? s4 - C::NQ : s4,
                                          wlds + ((qs + C::NWB - 1) % C::NWB) * C::WSW * 4, wave, lane);
                 if (kp == 8) {
@@ -1175,19 +1177,19 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                     ++dc;
                 }
                 // Matrix ops of this stage; the next stage's operands read
-                // meanwhile, once its weights are in: they were loaded three
-                // stages ago and are followed by 3 stages' weight loads, plus
+                // meanwhile, once its weights are in: they were loaded WL
+                // stages ago and are followed by WL stages' weight loads, plus
                 // a chunk's halo loads when a chunk boundary is that close,
                 // plus the previous group's stores at a group's start.
                 SplitOps<T, NBW> nxt;
                 const int qn = qs + 1 == C::NWB ? 0 : qs + 1;
                 const int hn = kp == 8 ? (hk + 1 == 3 ? 0 : hk + 1) : hk;
-                if (kp >= 3 && kp <= 7) {
-                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW) : "memory");
-                } else if (c == 0 && kp <= 2 && stores_before) {
-                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW + C::HDMIN + C::NS) : "memory");
+                if (kp >= C::WL && kp <= 7) {
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::WL * NBW) : "memory");
+                } else if (c == 0 && kp <= C::WL - 1 && stores_before) {
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::WL * NBW + C::HDMIN + C::NS) : "memory");
                 } else {
-                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * NBW + C::HDMIN) : "memory");
+                    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::WL * NBW + C::HDMIN) : "memory");
                 }
                 chunk_ops<CIN, COUT, T>(nxt, ha + hn * (C::HB / 4), wa + qn * C::WSW, kp == 8 ? 0 : kp + 1);
                 __builtin_amdgcn_sched_barrier(0);
