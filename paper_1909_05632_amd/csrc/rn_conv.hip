@@ -961,8 +961,8 @@ struct Chunked {
     static constexpr int HDW = (HD + 3) / 4;         // most loads of one wave per chunk
     static constexpr int HDMIN = HD / 4;             // fewest
     static constexpr int NS = T * NBW;               // 16-byte-a-lane stores per group and wave
-    static constexpr size_t lds_bytes = 3 * (size_t)HB + (size_t)4 * NWB * WSW * sizeof(float);
-    static_assert(CIN % 16 == 0 && COUT % 64 == 0 && NCH >= 3, "whole chunks, at least three per group");
+    static constexpr size_t lds_bytes = 3 * (size_t)HB + (size_t)4 * NWB * WSW * sizeof(float) + 4 * 256;
+    static_assert(CIN % 16 == 0 && COUT % 64 == 0 && NCH >= 4, "whole chunks, at least four per group");
     static_assert(WSW == 256 * NBW, "one 1 KB load per output block and stage");
     static_assert(T <= 16 && T % 4 == 0, "group size");
     static_assert(WL >= 2 && WL <= 8 && WL * NBW + HDMIN + NS <= 63, "the stage waits below assume these");
@@ -972,43 +972,48 @@ struct Chunked {
 // (chunk c reads 16 c floats further on).
 __device__ __align__(16) float g_zero_page[128];
 
-// Item words of tiles g .. g + T - 1 (clamped to the last item; the callers
-// mark tiles past `end` themselves), as scalar loads issued in assembly: the
-// compiler would make these vector loads, and its wait for them would also
-// wait for every ring load issued before their use.
-template <bool DENSE, int T>
-__device__ inline void load_items(const ConvArgs &a, int g, int end, uint32_t (&it)[T]) {
-    uint32_t raw[T];
-#pragma unroll
-    for (int u = 0; u < T; ++u) {
-        const int t = min(g + u, end - 1);
-        const uint32_t *p;
-        if constexpr (DENSE) {
-            constexpr int CH = 32;                        // as item_word<true>
-            const int per_chunk = CH * a.TH * a.TW;
-            const int c = t / per_chunk, rr = t - c * per_chunk;
-            const int nc = min(CH, a.dense_n - c * CH);
-            const int tile = rr / nc;
-            const int ty = tile / a.TW;
-            p = reinterpret_cast<const uint32_t *>(a.ids) + c * CH + (rr - tile * nc);
-            it[u] = ((uint32_t)ty << 8) | (uint32_t)(tile - ty * a.TW);
-        } else {
-            p = a.wl + t;
-            it[u] = 0;
-        }
-        asm volatile("s_load_dword %0, %1, 0x0" : "=s"(raw[u]) : "s"(p) : "memory");
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-    for (int u = 0; u < T; ++u) {
-        asm volatile("" : "+s"(raw[u]));                  // used only after the wait
-        it[u] |= DENSE ? raw[u] << 16 : raw[u];
+// Work items of a group, staged per wave in LDS: lane u loads the word of
+// tile g + u (clamped to the last item) straight into the wave's item slot
+// (global_load_lds_dword), so no register is written behind the compiler's
+// back and the load is counted with the ring loads; in dense mode the words
+// loaded are the stream ids and the positions are computed on reading.
+template <bool DENSE>
+__device__ inline const uint32_t *item_src(const ConvArgs &a, int t) {
+    if constexpr (DENSE) {
+        constexpr int CH = 32;                            // as item_word<true>
+        const int per_chunk = CH * a.TH * a.TW;
+        const int c = t / per_chunk, rr = t - c * per_chunk;
+        const int nc = min(CH, a.dense_n - c * CH);
+        const int tile = rr / nc;
+        return reinterpret_cast<const uint32_t *>(a.ids) + c * CH + (rr - tile * nc);
+    } else {
+        return a.wl + t;
     }
 }
 
+template <bool DENSE>
+__device__ inline uint32_t item_from(const ConvArgs &a, int t, uint32_t raw) {
+    if constexpr (DENSE) {
+        constexpr int CH = 32;
+        const int per_chunk = CH * a.TH * a.TW;
+        const int c = t / per_chunk, rr = t - c * per_chunk;
+        const int nc = min(CH, a.dense_n - c * CH);
+        const int tile = rr / nc;
+        const int ty = tile / a.TW;
+        return (raw << 16) | ((uint32_t)ty << 8) | (uint32_t)(tile - ty * a.TW);
+    } else {
+        return raw;
+    }
+}
+
+template <bool DENSE, int T>
+__device__ inline void dma_items(const ConvArgs &a, int g, int end, uint32_t dst, int lane) {
+    lds_dma4(item_src<DENSE>(a, min(g + min(lane, T - 1), end - 1)), dst);
+}
+
 // Source of each of this wave's halo loads for chunk 0 of the group at g.
-template <int CIN, int COUT, int T>
-__device__ inline void chunk_sources(const ConvArgs &a, int g, int end, const uint32_t (&it)[T],
+template <int CIN, int COUT, int T, bool DENSE>
+__device__ inline void chunk_sources(const ConvArgs &a, int g, int end, const uint32_t *items,
                                      const float *(&src)[Chunked<CIN, COUT, T>::HDW], int wave, int lane) {
     using C = Chunked<CIN, COUT, T>;
     const float *in = static_cast<const float *>(a.in);
@@ -1018,10 +1023,8 @@ __device__ inline void chunk_sources(const ConvArgs &a, int g, int end, const ui
         const int t = s / C::HT, rem = s - t * C::HT;
         const int hy = rem / C::RS, r2 = rem - hy * C::RS;
         const int hx = r2 >> 2, kq = r2 & 3;
-        uint32_t e = it[0];
-#pragma unroll
-        for (int u = 1; u < T; ++u) e = t == u ? it[u] : e;
-        const TileRef r = item_ref(a, e);
+        const int tc = min(t, T - 1);
+        const TileRef r = item_ref(a, item_from<DENSE>(a, min(g + tc, end - 1), items[tc]));
         const int y = r.ty * kTile - 1 + hy, x = r.tx * kTile - 1 + hx;
         const bool ok = t < T && g + t < end && r2 < 24 && y >= 0 && y < a.H && x >= 0 && x < a.W;
         src[k] = ok ? in + (size_t)r.slot * a.in_stride +
@@ -1112,7 +1115,8 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
     const int mrow = lane & 15, kq = lane >> 4;
     unsigned char *lds = reinterpret_cast<unsigned char *>(smem);
     float *wring = reinterpret_cast<float *>(lds + 3 * C::HB) + wave * C::NWB * C::WSW;
-    const uint32_t hlds = lds_addr(lds), wlds = lds_addr(wring);
+    const uint32_t *items = reinterpret_cast<const uint32_t *>(lds + 3 * C::HB + 4 * C::NWB * C::WSW * 4) + 64 * wave;
+    const uint32_t hlds = lds_addr(lds), wlds = lds_addr(wring), ilds = lds_addr(items);
     const float *wg = static_cast<const float *>(a.w);
     // this lane's A slot (halo pixel (mrow & 3, mrow >> 2), channel quad kq) and B slot
     const float *ha = reinterpret_cast<const float *>(lds) + 4 * ((mrow & 3) * C::RS + (mrow >> 2) * 4 + kq);
@@ -1126,11 +1130,9 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
 
     // Prologue: halo chunks 0-2 and weight stages 0 .. NWB - 2 of the first group.
     const float *src[C::HDW];
-    {
-        uint32_t it0[T];
-        load_items<DENSE, T>(a, xr.first, xr.end, it0);
-        chunk_sources<CIN, COUT, T>(a, xr.first, xr.end, it0, src, wave, lane);
-    }
+    dma_items<DENSE, T>(a, xr.first, xr.end, ilds, lane);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    chunk_sources<CIN, COUT, T, DENSE>(a, xr.first, xr.end, items, src, wave, lane);
 #pragma unroll
     for (int k = 0; k < 3; ++k) dma_chunk<CIN, COUT, T>(src, k, hlds + k * C::HB, wave);
 #pragma unroll
@@ -1166,11 +1168,17 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                 dma_wchunk<CIN, COUT, T>(wg, s4 >= C::NQ ? s4 - C::NQ : s4,
                                          wlds + ((qs + C::NWB - 1) % C::NWB) * C::WSW * 4, wave, lane);
                 if (kp == 8) {
+                    // The wave's item slot: the next group's items a chunk
+                    // before its halo sources are needed, then this group's
+                    // for the epilogue (each followed by this boundary's halo
+                    // loads and the next nine stages' weight loads).
+                    const int gn = min(g + xr.stride, xr.end - 1);
+                    if (c == C::NCH - 4) dma_items<DENSE, T>(a, gn, xr.end, ilds, lane);
+                    if (c == C::NCH - 2) dma_items<DENSE, T>(a, g, xr.end, ilds, lane);
                     // Refill this chunk's buffer with the chunk three ahead.
                     if (dc == C::NCH) {                       // on to the next group
-                        uint32_t it_next[T];
-                        load_items<DENSE, T>(a, min(g + xr.stride, xr.end - 1), xr.end, it_next);
-                        chunk_sources<CIN, COUT, T>(a, g + xr.stride, xr.end, it_next, src, wave, lane);
+                        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(9 * NBW + C::HDMIN) : "memory");
+                        chunk_sources<CIN, COUT, T, DENSE>(a, g + xr.stride, xr.end, items, src, wave, lane);
                         dc = 0;
                     }
                     dma_chunk<CIN, COUT, T>(src, dc, hlds + hk * C::HB, wave);
@@ -1205,12 +1213,11 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
         // transpose, 16 bytes a lane: pixel (b, kq) of the tile, channels
         // 16 nb + 4 m .. + 3 of the wave's, for lane 16 kq + 4 m + b.
         const int qb = lane & 3, qm = (lane >> 2) & 3;
-        uint32_t it_cur[T];
-        load_items<DENSE, T>(a, g, xr.end, it_cur);
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(9 * NBW + 2 * C::HDMIN) : "memory");
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             if (g + t >= xr.end) break;                   // uniform
-            const TileRef r = item_ref(a, it_cur[t]);
+            const TileRef r = item_ref(a, item_from<DENSE>(a, g + t, items[t]));
             const int col_keep = ~((a.W - 1 - (r.tx * kTile + kq)) >> 31);
             float *dst = static_cast<float *>(a.out) + (size_t)r.slot * a.out_stride +
                          (size_t)r.tile * kTilePx * COUT + (qb * 4 + kq) * COUT + wave * C::CW + 4 * qm;

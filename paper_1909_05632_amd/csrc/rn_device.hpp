@@ -37,6 +37,16 @@ __device__ inline void lds_dma16(const void *src, uint32_t lds) {
                  : "memory");
 }
 
+// 4 bytes per lane (global_load_lds_dword: lane i writes the 4 bytes at lds
+// + 4 i); as lds_dma16 otherwise.
+__device__ inline void lds_dma4(const void *src, uint32_t lds) {
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "v"(src), "s"(lds)
+                 : "memory");
+}
+
 // LDS byte address of a pointer into LDS (the low half of a generic pointer to
 // LDS is its LDS offset), made wave-uniform.
 __device__ inline uint32_t lds_addr(const void *p) {
