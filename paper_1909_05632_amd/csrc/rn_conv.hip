@@ -929,21 +929,22 @@ __device__ inline void split_stage(floatx4 (&acc)[T][NBW], const float *halos, c
 // channel quads at 16-byte slot 144 t + 24 hy + 4 hx + quad; pixels outside
 // the image and tiles past the end load from a zero page).  Rows padded to
 // 25 or 27 slots, which put the 16 pixels of a 16-lane read in 16 distinct
-// bank groups, measured no faster and with the same bank-conflict count.  The stage sequence runs on across groups: when a chunk's last
-// stage starts, the waves have read all of it, so after one block barrier it
-// is refilled with the chunk three ahead (the next group's when the group
-// runs out), 18 stages before it is read.  Weights stream per stage through a
-// ring of five LDS slots per wave (stage q + 4 loaded at the start of stage q)
-// and each stage's operands are read during the previous stage's matrix ops.
-// The memory counter the waits use retires loads and stores in issue order,
-// so every wait names how many later operations it may leave in flight;
-// loads of the compiler's own (work items, bias) are scalar or waited for
-// before any ring load is issued.  The epilogue applies bias, ReLU and the
-// zero outside the image, transposes each lane quad's 4 x 4 values with DPP
-// moves so a lane holds four channels of one pixel, and stores 16 bytes a
-// lane straight to the cache.  The order of the sums over K (chunk, then
-// position, then channel) is the same for every T, so a tile's outputs do not
-// depend on the group size a launch picks.
+// bank groups, measured no faster and with the same bank-conflict count.
+// The stage sequence runs on across groups: when a chunk's last stage starts,
+// the waves have read all of it, so after one block barrier it is refilled
+// with the chunk three ahead (the next group's when the group runs out), 18
+// stages before it is read.  Weights stream per stage through a ring of five
+// LDS slots per wave (stage q + 4 loaded at the start of stage q) and each
+// stage's operands are read during the previous stage's matrix ops.  The
+// memory counter the waits use retires loads and stores in issue order, so
+// every wait names how many later operations it may leave in flight; the work
+// items are loaded into LDS the same way, and the only loads the compiler
+// issues (the bias) are waited for before the first ring load.  The epilogue
+// applies bias, ReLU and the zero outside the image, transposes each lane
+// quad's 4 x 4 values with DPP moves so a lane holds four channels of one
+// pixel, and stores 16 bytes a lane straight to the cache.  The order of the
+// sums over K (chunk, then position, then channel) is the same for every T,
+// so a tile's outputs do not depend on the group size a launch picks.
 template <int CIN, int COUT, int T>
 struct Chunked {
     static constexpr int NCH = CIN / 16;             // 16-channel chunks
@@ -968,8 +969,8 @@ struct Chunked {
     static_assert(WL >= 2 && WL <= 8 && WL * NBW + HDMIN + NS <= 63, "the stage waits below assume these");
 };
 
-// 16-byte zero page: the source of every halo slot that holds no input value
-// (chunk c reads 16 c floats further on).
+// Zero page (512 bytes): the source of every halo slot that holds no input
+// value (chunk c reads 16 c floats further on).
 __device__ __align__(16) float g_zero_page[128];
 
 // Work items of a group, staged per wave in LDS: lane u loads the word of
