@@ -1073,6 +1073,37 @@ __device__ inline void chunk_ops(SplitOps<T, Chunked<CIN, COUT, T>::NBW> &o, con
     for (int nb = 0; nb < C::NBW; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + 256 * nb);
 }
 
+// Parts of a stage, issued interleaved: A fragments of tiles [t0, t1), the
+// B fragments, and the matrix ops of one k-step (the order of the matrix ops
+// over a stage is that of split_mma).
+template <int CIN, int COUT, int T, int T0, int T1>
+__device__ inline void chunk_ops_a(SplitOps<T, Chunked<CIN, COUT, T>::NBW> &o, const float *hb, int kpos) {
+    using C = Chunked<CIN, COUT, T>;
+    const int ky = kpos / 3, kx = kpos - 3 * ky;
+#pragma unroll
+    for (int t = T0; t < T1; ++t)
+        o.a[t] = *reinterpret_cast<const float4 *>(hb + 4 * (t * C::HT + ky * C::RS + kx * 4));
+}
+
+template <int CIN, int COUT, int T>
+__device__ inline void chunk_ops_b(SplitOps<T, Chunked<CIN, COUT, T>::NBW> &o, const float *wb) {
+#pragma unroll
+    for (int nb = 0; nb < Chunked<CIN, COUT, T>::NBW; ++nb) o.b[nb] = *reinterpret_cast<const float4 *>(wb + 256 * nb);
+}
+
+template <int T, int NBW, int J>
+__device__ inline void mma_kstep(floatx4 (&acc)[T][NBW], const SplitOps<T, NBW> &o) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const float av = J == 0 ? o.a[t].x : J == 1 ? o.a[t].y : J == 2 ? o.a[t].z : o.a[t].w;
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            const float bv = J == 0 ? o.b[nb].x : J == 1 ? o.b[nb].y : J == 2 ? o.b[nb].z : o.b[nb].w;
+            acc[t][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t][nb], 0, 0, 0);
+        }
+    }
+}
+
 // 4 x 4 transpose inside each lane quad: lane 4 m + b holds v[i] = X[i][b] on
 // entry and X[b][i] on return (two exchanges, over lane bit 0 with element
 // bit 0, then over lane bit 1 with element bit 1).
@@ -1164,7 +1195,22 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(17 * NBW + C::HDMIN) : "memory");
                     lds_barrier();
                 }
-                // Stage q + NWB - 1 into the slot stage q - 1 used.
+                // Matrix ops of this stage, one k-step at a time, with the
+                // rest of the stage's work in between so the matrix pipe is
+                // never left waiting on a burst of other instructions: stage
+                // q + NWB - 1's weights into the slot stage q - 1 used (its
+                // reads fed matrix ops that have issued), at a chunk boundary
+                // the item and halo loads, and the next stage's operands,
+                // its weights once they are in: they were loaded WL stages
+                // ago and are followed by WL stages' weight loads, plus a
+                // chunk's halo loads when a chunk boundary is that close,
+                // plus the previous group's stores at a group's start.
+                SplitOps<T, NBW> nxt;
+                const int qn = qs + 1 == C::NWB ? 0 : qs + 1;
+                const int hn = kp == 8 ? (hk + 1 == 3 ? 0 : hk + 1) : hk;
+                const int kn = kp == 8 ? 0 : kp + 1;
+                mma_kstep<T, NBW, 0>(acc, cur);
+                __builtin_amdgcn_sched_barrier(0);
                 const int s4 = c * 9 + kp + C::NWB - 1;
                 dma_wchunk<CIN, COUT, T>(wg, s4 >= C::NQ ? s4 - C::NQ : s4,
                                          wlds + ((qs + C::NWB - 1) % C::NWB) * C::WSW * 4, wave, lane);
@@ -1185,14 +1231,14 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                     dma_chunk<CIN, COUT, T>(src, dc, hlds + hk * C::HB, wave);
                     ++dc;
                 }
-                // Matrix ops of this stage; the next stage's operands read
-                // meanwhile, once its weights are in: they were loaded WL
-                // stages ago and are followed by WL stages' weight loads, plus
-                // a chunk's halo loads when a chunk boundary is that close,
-                // plus the previous group's stores at a group's start.
-                SplitOps<T, NBW> nxt;
-                const int qn = qs + 1 == C::NWB ? 0 : qs + 1;
-                const int hn = kp == 8 ? (hk + 1 == 3 ? 0 : hk + 1) : hk;
+                chunk_ops_a<CIN, COUT, T, 0, T / 2>(nxt, ha + hn * (C::HB / 4), kn);
+                __builtin_amdgcn_sched_barrier(0);
+                mma_kstep<T, NBW, 1>(acc, cur);
+                __builtin_amdgcn_sched_barrier(0);
+                chunk_ops_a<CIN, COUT, T, T / 2, T>(nxt, ha + hn * (C::HB / 4), kn);
+                __builtin_amdgcn_sched_barrier(0);
+                mma_kstep<T, NBW, 2>(acc, cur);
+                __builtin_amdgcn_sched_barrier(0);
                 if (kp >= C::WL && kp <= 7) {
                     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::WL * NBW) : "memory");
                 } else if (c == 0 && kp <= C::WL - 1 && stores_before) {
@@ -1200,9 +1246,9 @@ __device__ void chunk_path(const ConvArgs &a, int cnt, float *smem) {
                 } else {
                     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C::WL * NBW + C::HDMIN) : "memory");
                 }
-                chunk_ops<CIN, COUT, T>(nxt, ha + hn * (C::HB / 4), wa + qn * C::WSW, kp == 8 ? 0 : kp + 1);
+                chunk_ops_b<CIN, COUT, T>(nxt, wa + qn * C::WSW);
                 __builtin_amdgcn_sched_barrier(0);
-                split_mma<T, NBW>(acc, cur);
+                mma_kstep<T, NBW, 3>(acc, cur);
                 __builtin_amdgcn_sched_barrier(0);
                 cur = nxt;
                 qs = qn;
