@@ -51,27 +51,33 @@ __global__ __launch_bounds__(256) void k_reinforce(int n, int n_out, const float
 
 // ------------------------------------------------------------------ dense head
 
-// Block (t, c) takes 256 of the 16 C head inputs of tile position t of the
-// last layer (chunk c); a thread owns one input j, keeps its NO weights and
-// NO gradient sums in registers and walks the streams (their g rows staged
-// in LDS).
-template <int NO>
-__global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
+// Block (t, c) takes blockDim.x V of the 16 C head inputs of tile position t
+// of the last layer (chunk c); a thread owns V consecutive inputs j (one
+// 16-byte access per stream for V = 4), keeps their NO weights and NO
+// gradient sums in registers and walks the streams (their g rows staged in
+// LDS).  Each input's sums run over o and over the streams in order, whatever
+// V is.
+template <int NO, int V>
+__global__ __launch_bounds__(512) void k_bwd_head(HeadBwdArgs a) {
+    static_assert(V == 1 || V == 4, "one float or one float4 per thread");
+    using VT = typename std::conditional<V == 4, float4, float>::type;
     constexpr int kHeadStreams = NO <= 32 ? 256 : 128;    // streams per LDS stage of g (32 KB at most)
     __shared__ float s_g[kHeadStreams * NO];
     __shared__ int32_t s_slot[kHeadStreams];
     const int t = blockIdx.x;
-    const int E = kTilePx * a.C;
+    const int E = kTilePx * a.C;                          // a multiple of V
     const int ty = t / a.TW, tx = t - ty * a.TW;
     {
-        const int j = blockIdx.y * blockDim.x + threadIdx.x;
-        const bool ok = j < E;
-        float w[NO], acc[NO];
+        const int j0 = (blockIdx.y * blockDim.x + threadIdx.x) * V;
+        const bool ok = j0 < E;
+        float w[V][NO], acc[V][NO];
 #pragma unroll
-        for (int o = 0; o < NO; ++o) {
-            w[o] = ok && o < a.n_out ? a.wd[(size_t)o * a.K + (size_t)t * E + j] : 0.f;
-            acc[o] = 0.f;
-        }
+        for (int v = 0; v < V; ++v)
+#pragma unroll
+            for (int o = 0; o < NO; ++o) {
+                w[v][o] = ok && o < a.n_out ? a.wd[(size_t)o * a.K + (size_t)t * E + j0 + v] : 0.f;
+                acc[v][o] = 0.f;
+            }
         for (int i0 = 0; i0 < a.n; i0 += kHeadStreams) {
             const int nc = min(kHeadStreams, a.n - i0);
             __syncthreads();                      // the previous stage's readers are done
@@ -84,27 +90,37 @@ __global__ __launch_bounds__(256) void k_bwd_head(HeadBwdArgs a) {
             if (ok) {
 #pragma unroll 4
                 for (int ii = 0; ii < nc; ++ii) {
-                    const float v = a.act[(size_t)s_slot[ii] * a.act_stride + (size_t)t * E + j];
-                    float da = 0.f;
+                    const VT in = *reinterpret_cast<const VT *>(a.act + (size_t)s_slot[ii] * a.act_stride + (size_t)t * E + j0);
+                    const float *vin = reinterpret_cast<const float *>(&in);
+                    VT out;
+                    float *vout = reinterpret_cast<float *>(&out);
 #pragma unroll
-                    for (int o = 0; o < NO; ++o) {
-                        const float gv = s_g[ii * NO + o];
-                        da = fmaf(w[o], gv, da);
-                        acc[o] = fmaf(gv, v, acc[o]);
+                    for (int v = 0; v < V; ++v) {
+                        float da = 0.f;
+#pragma unroll
+                        for (int o = 0; o < NO; ++o) {
+                            const float gv = s_g[ii * NO + o];
+                            da = fmaf(w[v][o], gv, da);
+                            acc[v][o] = fmaf(gv, vin[v], acc[v][o]);
+                        }
+                        vout[v] = vin[v] > 0.f ? da : 0.f;
                     }
-                    a.dz[((size_t)(i0 + ii) * a.ntiles + t) * E + j] = v > 0.f ? da : 0.f;
+                    *reinterpret_cast<VT *>(a.dz + ((size_t)(i0 + ii) * a.ntiles + t) * E + j0) = out;
                 }
             }
         }
         if (ok) {
-            const int m = j / a.C, c = j - m * a.C;
-            const int y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
-            if (y < a.H && x < a.W) {
 #pragma unroll
-                for (int o = 0; o < NO; ++o) {
-                    if (o >= a.n_out) break;
-                    float *d = a.gwd + (size_t)o * a.C * a.H * a.W + ((size_t)c * a.H + y) * a.W + x;
-                    *d = a.accumulate ? *d + acc[o] : acc[o];
+            for (int v = 0; v < V; ++v) {
+                const int j = j0 + v, m = j / a.C, c = j - m * a.C;
+                const int y = ty * kTile + (m >> 2), x = tx * kTile + (m & 3);
+                if (y < a.H && x < a.W) {
+#pragma unroll
+                    for (int o = 0; o < NO; ++o) {
+                        if (o >= a.n_out) break;
+                        float *d = a.gwd + (size_t)o * a.C * a.H * a.W + ((size_t)c * a.H + y) * a.W + x;
+                        *d = a.accumulate ? *d + acc[v][o] : acc[v][o];
+                    }
                 }
             }
         }
@@ -317,10 +333,11 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
 // channel ci) one 16-byte read of the halo copy for kx, [ci][halo row][4]
 // (halo columns kx .. kx + 3 of each row).  Wave u of a team owns all MBU
 // row blocks and QW column blocks (MBU x QW x 4 accumulators), so one staged
-// tile feeds MBU x QW x 4 matrix ops from MBU + QW reads.  P tiles are staged
-// per pair of barriers; the next P tiles' operands are fetched into registers
-// during their matrix work.  Row strides (20 and 28 floats) put the 16 lanes
-// of a read group in distinct bank groups.
+// tile feeds MBU x QW x 4 matrix ops from MBU + QW reads.  Two staging
+// buffers of P tiles each alternate: the matrix ops read one while the next P
+// tiles are written to the other between their k-steps, one barrier per pass
+// (P = 2 where both buffers fit one CU's LDS, else 1).  Row strides (20
+// and 28 floats) put the 16 lanes of a read group in distinct bank groups.
 template <int CA, int CZ>
 struct Dw2 {
     static constexpr int NQ = 9 * CA + 1;                 // columns: (kernel position, input channel), bias
@@ -331,23 +348,98 @@ struct Dw2 {
     static constexpr int NCH = (NBQ + QW0 - 1) / QW0;     // column chunks (waves per team)
     static constexpr int QW = (NBQ + NCH - 1) / NCH;
     static constexpr int BPT = (NCH + 3) / 4;             // blocks per team
-    static constexpr int P = 2;                           // tiles per staging
     static constexpr int SZ = 20;                         // dz row stride (16 pixels + pad)
     static constexpr int HS = 28;                         // halo copy channel stride (6 rows x 4 + pad)
     static constexpr int DZT = CZ * SZ;                   // floats of one staged dz tile
     static constexpr int HT = 3 * CA * HS;                // floats of one staged halo (three copies)
+    static constexpr int P = 16 * (DZT + HT) <= 160 * 1024 ? 2 : 1;  // tiles per buffer
     static constexpr int DZV = (4 * CZ + 255) / 256;      // 16-byte dz chunks per thread and tile
     static constexpr int HV = (9 * CA + 255) / 256;       // 16-byte halo chunks per thread and tile
-    static constexpr size_t lds_bytes = (size_t)P * (DZT + HT) * sizeof(float);
+    static constexpr int BUF = P * (DZT + HT);            // floats of one staging buffer
+    static constexpr size_t lds_bytes = (size_t)2 * BUF * sizeof(float);   // two buffers
+    static_assert(lds_bytes <= 160 * 1024, "two buffers fit one CU");
     static_assert(CZ % 16 == 0 && CA % 4 == 0, "whole row blocks and 16-byte channel chunks");
 };
+
+// Staging of one fetched tile into an LDS buffer: dz transposed to
+// [channel][pixel] (PART 0), the halo as three column-shifted copies
+// [kx][channel][row-major 6 x 4 window] (PART 1).
+template <int CA, int CZ, int PART>
+__device__ inline void dw2_stage(float *dz, float *h, const float4 *rdz, const float4 *rh) {
+    using D = Dw2<CA, CZ>;
+    if constexpr (PART == 0) {
+#pragma unroll
+        for (int k = 0; k < D::DZV; ++k) {
+            const int e = threadIdx.x + 256 * k;
+            if (e < 4 * CZ) {
+                const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);   // pixel m, channels 4 c4 ..
+                const float4 v = rdz[k];
+                dz[(4 * c4 + 0) * D::SZ + m] = v.x;
+                dz[(4 * c4 + 1) * D::SZ + m] = v.y;
+                dz[(4 * c4 + 2) * D::SZ + m] = v.z;
+                dz[(4 * c4 + 3) * D::SZ + m] = v.w;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < D::HV; ++k) {
+            const int e = threadIdx.x + 256 * k;
+            if (e < 9 * CA) {
+                const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+                const int hy = pos / 6, hx = pos - 6 * hy;
+                const float4 v = rh[k];
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) {
+                    const int j = hx - kx;
+                    if (j < 0 || j > 3) continue;
+                    float *d = h + (kx * CA + 4 * c4) * D::HS + hy * 4 + j;
+                    d[0] = v.x;
+                    d[D::HS] = v.y;
+                    d[2 * D::HS] = v.z;
+                    d[3 * D::HS] = v.w;
+                }
+            }
+        }
+    }
+}
+
+// One tile's A (dz rows) and B (halo columns) fragments from a staged buffer.
+template <int MBU, int QW>
+struct Dw2Ops {
+    float4 av[MBU], bv[QW];
+};
+
+template <int CA, int CZ>
+__device__ inline void dw2_ops(Dw2Ops<Dw2<CA, CZ>::MBU, Dw2<CA, CZ>::QW> &o, const float *dz, const float *h,
+                               const int *boff, int col, int kq) {
+    using D = Dw2<CA, CZ>;
+#pragma unroll
+    for (int m = 0; m < D::MBU; ++m) o.av[m] = *reinterpret_cast<const float4 *>(dz + (16 * m + col) * D::SZ + 4 * kq);
+#pragma unroll
+    for (int k = 0; k < D::QW; ++k)
+        o.bv[k] = boff[k] >= 0 ? *reinterpret_cast<const float4 *>(h + boff[k])
+                               : (boff[k] == -1 ? make_float4(1.f, 1.f, 1.f, 1.f) : make_float4(0.f, 0.f, 0.f, 0.f));
+}
+
+// Matrix ops of k-steps J0 .. J1 - 1 of one tile.
+template <int MBU, int QW, int J0, int J1>
+__device__ inline void dw2_mma(floatx4 (&acc)[MBU][QW], const Dw2Ops<MBU, QW> &o) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j)
+#pragma unroll
+        for (int m = 0; m < MBU; ++m)
+#pragma unroll
+            for (int k = 0; k < QW; ++k) {
+                const float x = j == 0 ? o.av[m].x : j == 1 ? o.av[m].y : j == 2 ? o.av[m].z : o.av[m].w;
+                const float y = j == 0 ? o.bv[k].x : j == 1 ? o.bv[k].y : j == 2 ? o.bv[k].z : o.bv[k].w;
+                acc[m][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(x, y, acc[m][k], 0, 0, 0);
+            }
+}
 
 template <int CA, int CZ>
 __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
     using D = Dw2<CA, CZ>;
-    extern __shared__ float smem[];
-    float *s_dz = smem;                                   // [P][CZ][SZ]
-    float *s_h = smem + D::P * D::DZT;                    // [P][3][CA][HS]
+    extern __shared__ float smem[];                       // two buffers of [P][CZ][SZ] dz, [P][3][CA][HS] halo
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int team = blockIdx.x / D::BPT, u = (blockIdx.x - team * D::BPT) * 4 + wave;
     const bool active = u < D::NCH;
@@ -377,108 +469,88 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
     const int t0 = (int)(NT * team / a.teams), t1 = (int)(NT * (team + 1) / a.teams);
     int fi = t0 / a.ntiles, ft = t0 - fi * a.ntiles;
     // Operands of tiles c .. c + P - 1 (this thread's share) into registers,
-    // every load issued; tiles past t1, out-of-image halo pixels: zero.
+    // every load issued; tiles past t1, out-of-image halo pixels: zero.  The
+    // slot of each tile's stream is read first, as a scalar load of a
+    // wave-uniform index, so that only the halo addresses wait for it (a
+    // vector load there would make the wait drain the dz loads as well).
     float4 rdz[D::P][D::DZV], rh[D::P][D::HV];
+    const __attribute__((address_space(4))) int32_t *ids =
+        (const __attribute__((address_space(4))) int32_t *)a.ids;
     auto fetch = [&](int c) __attribute__((always_inline)) {
+        bool ok[D::P];
+        int tl[D::P], slot[D::P];
 #pragma unroll
         for (int pp = 0; pp < D::P; ++pp) {
-            const bool ok = c + pp < t1;
-            const int i = ok ? fi : 0, t = ok ? ft : 0;
+            ok[pp] = c + pp < t1;
+            const int i = __builtin_amdgcn_readfirstlane(ok[pp] ? fi : 0);
+            tl[pp] = ok[pp] ? ft : 0;
             if (++ft == a.ntiles) {
                 ft = 0;
                 ++fi;
             }
-            const int ty = t / a.TW, tx = t - ty * a.TW;
-            const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + t) * kTilePx * CZ);
+            slot[pp] = ids[i];
+            const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + tl[pp]) * kTilePx * CZ);
 #pragma unroll
             for (int k = 0; k < D::DZV; ++k) {
                 const int e = threadIdx.x + 256 * k;
-                rdz[pp][k] = ok && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+                rdz[pp][k] = ok[pp] && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride;
+        }
+#pragma unroll
+        for (int pp = 0; pp < D::P; ++pp) {
+            const int t = tl[pp], ty = t / a.TW, tx = t - ty * a.TW;
+            const float *ap = a.act_prev + (size_t)slot[pp] * a.prev_stride;
 #pragma unroll
             for (int k = 0; k < D::HV; ++k) {
                 const int e = threadIdx.x + 256 * k;
                 const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
                 const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
                 float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (ok && e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
+                if (ok[pp] && e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
                     v = *reinterpret_cast<const float4 *>(
                         ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
                 rh[pp][k] = v;
             }
         }
     };
-    if (t0 < t1) fetch(t0);
+    // Two staging buffers: while the matrix ops read the P tiles of one, the
+    // next P tiles (fetched into registers during the previous pass) are
+    // written to the other between k-steps, and the tiles after those are
+    // fetched; one block barrier per pass.  Fetching and staging run
+    // unconditionally (tiles past t1 load zeros from valid addresses): a
+    // guarded pass would make the compiler copy the accumulators between
+    // register files.
+    fetch(t0);
+#pragma unroll
+    for (int pp = 0; pp < D::P; ++pp) {
+        dw2_stage<CA, CZ, 0>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+        dw2_stage<CA, CZ, 1>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+    }
+    fetch(t0 + D::P);
+    dev::lds_barrier();
+    int b = 0;
     for (int c = t0; c < t1; c += D::P) {
-        __syncthreads();                                   // the previous tiles' LDS readers are done
+        float *cb = smem + b * D::BUF, *nb = smem + (b ^ 1) * D::BUF;
+        Dw2Ops<D::MBU, D::QW> cur;
+        dw2_ops<CA, CZ>(cur, cb, cb + D::P * D::DZT, boff, col, kq);
 #pragma unroll
         for (int pp = 0; pp < D::P; ++pp) {
-            float *dz = s_dz + pp * D::DZT;
-            float *h = s_h + pp * D::HT;
-#pragma unroll
-            for (int k = 0; k < D::DZV; ++k) {
-                const int e = threadIdx.x + 256 * k;
-                if (e < 4 * CZ) {
-                    const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);   // pixel m, channels 4 c4 ..
-                    const float4 v = rdz[pp][k];
-                    dz[(4 * c4 + 0) * D::SZ + m] = v.x;
-                    dz[(4 * c4 + 1) * D::SZ + m] = v.y;
-                    dz[(4 * c4 + 2) * D::SZ + m] = v.z;
-                    dz[(4 * c4 + 3) * D::SZ + m] = v.w;
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < D::HV; ++k) {
-                const int e = threadIdx.x + 256 * k;
-                if (e < 9 * CA) {
-                    const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
-                    const int hy = pos / 6, hx = pos - 6 * hy;
-                    const float4 v = rh[pp][k];
-#pragma unroll
-                    for (int kx = 0; kx < 3; ++kx) {
-                        const int j = hx - kx;
-                        if (j < 0 || j > 3) continue;
-                        float *d = h + (kx * CA + 4 * c4) * D::HS + hy * 4 + j;
-                        d[0] = v.x;
-                        d[D::HS] = v.y;
-                        d[2 * D::HS] = v.z;
-                        d[3 * D::HS] = v.w;
-                    }
-                }
-            }
+            Dw2Ops<D::MBU, D::QW> nxt;
+            if (pp + 1 < D::P) dw2_ops<CA, CZ>(nxt, cb + (pp + 1) * D::DZT, cb + D::P * D::DZT + (pp + 1) * D::HT, boff, col, kq);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_mma<D::MBU, D::QW, 0, 2>(acc, cur);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_mma<D::MBU, D::QW, 2, 4>(acc, cur);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (pp + 1 < D::P) cur = nxt;
         }
-        __syncthreads();
-        if (c + D::P < t1) fetch(c + D::P);                // in flight during these tiles' matrix ops
-        // Unconditional: a staged tile past t1 is all zeros and adds exact
-        // zeros, and an idle wave's sums are never stored (a guarded matrix
-        // phase makes the compiler copy the accumulators between register
-        // files on every pass).
-        {
-#pragma unroll
-            for (int pp = 0; pp < D::P; ++pp) {
-                const float *dz = s_dz + pp * D::DZT;
-                const float *h = s_h + pp * D::HT;
-                float4 av[D::MBU], bv[D::QW];
-#pragma unroll
-                for (int m = 0; m < D::MBU; ++m)
-                    av[m] = *reinterpret_cast<const float4 *>(dz + (16 * m + col) * D::SZ + 4 * kq);
-#pragma unroll
-                for (int k = 0; k < D::QW; ++k)
-                    bv[k] = boff[k] >= 0 ? *reinterpret_cast<const float4 *>(h + boff[k])
-                                         : (boff[k] == -1 ? make_float4(1.f, 1.f, 1.f, 1.f) : make_float4(0.f, 0.f, 0.f, 0.f));
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int m = 0; m < D::MBU; ++m)
-#pragma unroll
-                        for (int k = 0; k < D::QW; ++k) {
-                            const float x = j == 0 ? av[m].x : j == 1 ? av[m].y : j == 2 ? av[m].z : av[m].w;
-                            const float y = j == 0 ? bv[k].x : j == 1 ? bv[k].y : j == 2 ? bv[k].z : bv[k].w;
-                            acc[m][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(x, y, acc[m][k], 0, 0, 0);
-                        }
-            }
-        }
+        fetch(c + 2 * D::P);                               // in flight during the next pass
+        dev::lds_barrier();                                // the other buffer staged, this one read
+        b ^= 1;
     }
     if (!active) return;
 #pragma unroll
@@ -826,7 +898,11 @@ int bwd_dw_teams(int ca, int cz, bool first, int n, int ntiles, int cus) {
     }
     const int bpt = std::max(1, dw_blocks_per_team(ca, cz, first));
     const long long tiles = (long long)n * ntiles;
-    const long long want = (3LL * cus + bpt - 1) / bpt;      // about three blocks per CU
+    // One block per CU, one round: the accumulators and operands take more
+    // than half the register file, so one wave per SIMD is resident anyway,
+    // and equal tile ranges finish together (more, shorter teams measured
+    // slower, and each adds a partial to reduce).
+    const long long want = std::max(1, cus / bpt);
     return (int)std::max(1LL, std::min(want, (tiles + 7) / 8));
 }
 
@@ -839,10 +915,17 @@ hipError_t launch_reinforce(int n, int n_out, const float *logits, const int32_t
 }
 
 hipError_t launch_bwd_head(const HeadBwdArgs &a, hipStream_t s) {
-    const dim3 grid(a.ntiles, (kTilePx * a.C + 255) / 256), block(256);
-    if (a.n_out <= 8) hipLaunchKernelGGL(k_bwd_head<8>, grid, block, 0, s, a);
-    else if (a.n_out <= 32) hipLaunchKernelGGL(k_bwd_head<32>, grid, block, 0, s, a);
-    else hipLaunchKernelGGL(k_bwd_head<64>, grid, block, 0, s, a);
+    const int E = kTilePx * a.C;
+    if (a.n_out <= 8) {
+        // a float4 of inputs per thread, one block per tile up to 512 threads
+        const int q = E / 4, th = std::min(512, (q + 63) / 64 * 64);
+        hipLaunchKernelGGL((k_bwd_head<8, 4>), dim3(a.ntiles, (q + th - 1) / th), dim3(th), 0, s, a);
+    } else {
+        // 32 or 64 weights and sums per input: one input per thread
+        const dim3 grid(a.ntiles, (E + 255) / 256), block(256);
+        if (a.n_out <= 32) hipLaunchKernelGGL((k_bwd_head<32, 1>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_bwd_head<64, 1>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 
