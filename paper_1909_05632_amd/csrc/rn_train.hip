@@ -177,6 +177,7 @@ struct Dx {
     static constexpr int HV = (9 * CZ + 63) / 64;   // 16-byte halo loads per lane
     static constexpr size_t lds_bytes = (size_t)(2 * WST + 4 * HALO) * sizeof(float);
     static_assert(CZ % 16 == 0 && SC % 16 == 0, "whole 16-channel K blocks per stage");
+    static_assert(CA % 4 == 0, "whole 16-byte channel groups in the epilogue");
     static_assert(HV <= 32, "halo mask width");
 };
 
@@ -230,6 +231,34 @@ __device__ inline void dx_dma_stage(const float *wt, int q, float *dst, int wave
     }
 }
 
+// One exchange of a quad transpose: lanes that differ in lane bit BIT swap
+// the elements that differ in element bit BIT (DPP quad permutation [1,0,3,2]
+// for bit 0, [2,3,0,1] for bit 1).
+template <int BIT>
+__device__ inline void dx_quad_xchg(float (&v)[4], int b) {
+    constexpr int step = 1 << BIT, ctrl = BIT == 0 ? 0xb1 : 0x4e;
+    const bool hi = b & step;
+    float r[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int lo = BIT == 0 ? 2 * k : k;              // the pair (lo, lo + step)
+        r[k] = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(hi ? v[lo] : v[lo + step]), ctrl, 0xf, 0xf, false));
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {                         // selects on values: constant indices only
+        const int lo = BIT == 0 ? 2 * k : k;
+        v[lo] = hi ? r[k] : v[lo];
+        v[lo + step] = hi ? v[lo + step] : r[k];
+    }
+}
+
+// 4 x 4 transpose inside each lane quad: lane 4 m + b holds v[i] = X[i][b]
+// on entry and X[b][i] on return.
+__device__ inline void dx_quad_transpose(float (&v)[4], int b) {
+    dx_quad_xchg<0>(v, b);
+    dx_quad_xchg<1>(v, b);
+}
+
 template <int CZ, int CA>
 __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
     using D = Dx<CZ, CA>;
@@ -257,6 +286,23 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
         floatx4 acc[D::NB];
 #pragma unroll
         for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // The epilogue's view, after a quad transpose of the accumulators:
+        // lane (qb, qm, kq) holds pixel qb * 4 + kq of the tile, channels
+        // c0(nb) = 16 nb + 4 qm .. + 3.  Its ReLU mask (a_{l-1} at those
+        // places, 16 bytes per block) is loaded now, waited for by the end of
+        // this stage, so the epilogue waits for no load.
+        const int qb = lane & 3, qm = (lane >> 2) & 3, em = qb * 4 + kq;
+        float4 msk[D::NB];
+        {
+            const bool tv = tid < NT;
+            const int i = tv ? tid / a.ntiles : 0, t = tv ? tid - i * a.ntiles : 0;
+            const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + ((size_t)t * kTilePx + em) * CA;
+#pragma unroll
+            for (int nb = 0; nb < D::NB; ++nb) {
+                const int c0 = nb * 16 + 4 * qm;
+                msk[nb] = *reinterpret_cast<const float4 *>(ap + (c0 < CA ? c0 : 0));
+            }
+        }
         for (int q = 0; q < D::NQ; ++q) {
             const int kpos = q / D::NCH, ch = q - kpos * D::NCH;
             const int ky = kpos / 3, kx = kpos - ky * 3;
@@ -301,19 +347,18 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
             else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             dev::lds_barrier();
         }
-        if (tid < NT) {
+        if (tid < NT) {                                            // uniform per wave
             const int i = tid / a.ntiles, t = tid - i * a.ntiles;
-            const float *ap = a.act_prev + (size_t)a.ids[i] * a.prev_stride + (size_t)t * kTilePx * CA;
-            float *dst = a.dz_out + ((size_t)i * a.ntiles + t) * kTilePx * CA;
+            float *dst = a.dz_out + (((size_t)i * a.ntiles + t) * kTilePx + em) * CA;
 #pragma unroll
             for (int nb = 0; nb < D::NB; ++nb) {
-                const int c = nb * 16 + mrow;
-                if (c >= CA) continue;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = r * 4 + kq;                      // pixel (row r, column kq)
-                    dst[m * CA + c] = ap[m * CA + c] > 0.f ? acc[nb][r] : 0.f;
-                }
+                float v[4] = {acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]};   // pixels r * 4 + kq, channel 16 nb + 4 qm + qb
+                dx_quad_transpose(v, qb);
+                const int c0 = nb * 16 + 4 * qm;
+                if (c0 < CA)                                       // CA % 4 == 0: whole float4s
+                    *reinterpret_cast<float4 *>(dst + c0) =
+                        make_float4(msk[nb].x > 0.f ? v[0] : 0.f, msk[nb].y > 0.f ? v[1] : 0.f,
+                                    msk[nb].z > 0.f ? v[2] : 0.f, msk[nb].w > 0.f ? v[3] : 0.f);
             }
         }
         dev::wave_sync();                                          // this wave's halo reads are done
