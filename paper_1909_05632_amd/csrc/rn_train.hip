@@ -406,16 +406,17 @@ struct Dw2 {
     static_assert(CZ % 16 == 0 && CA % 4 == 0, "whole row blocks and 16-byte channel chunks");
 };
 
-// Staging of one fetched tile into an LDS buffer: dz transposed to
-// [channel][pixel] (PART 0), the halo as three column-shifted copies
-// [kx][channel][row-major 6 x 4 window] (PART 1).
+// Staging of one fetched tile into an LDS buffer by 256 threads (tix the
+// thread's index among them): dz transposed to [channel][pixel] (PART 0), the
+// halo as three column-shifted copies [kx][channel][row-major 6 x 4 window]
+// (PART 1).
 template <int CA, int CZ, int PART>
-__device__ inline void dw2_stage(float *dz, float *h, const float4 *rdz, const float4 *rh) {
+__device__ inline void dw2_stage(float *dz, float *h, const float4 *rdz, const float4 *rh, int tix) {
     using D = Dw2<CA, CZ>;
     if constexpr (PART == 0) {
 #pragma unroll
         for (int k = 0; k < D::DZV; ++k) {
-            const int e = threadIdx.x + 256 * k;
+            const int e = tix + 256 * k;
             if (e < 4 * CZ) {
                 const int m = e / (CZ / 4), c4 = e - m * (CZ / 4);   // pixel m, channels 4 c4 ..
                 const float4 v = rdz[k];
@@ -428,7 +429,7 @@ __device__ inline void dw2_stage(float *dz, float *h, const float4 *rdz, const f
     } else {
 #pragma unroll
         for (int k = 0; k < D::HV; ++k) {
-            const int e = threadIdx.x + 256 * k;
+            const int e = tix + 256 * k;
             if (e < 9 * CA) {
                 const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
                 const int hy = pos / 6, hx = pos - 6 * hy;
@@ -454,14 +455,14 @@ struct Dw2Ops {
     float4 av[MBU], bv[QW];
 };
 
-template <int CA, int CZ>
-__device__ inline void dw2_ops(Dw2Ops<Dw2<CA, CZ>::MBU, Dw2<CA, CZ>::QW> &o, const float *dz, const float *h,
-                               const int *boff, int col, int kq) {
+template <int CA, int CZ, int QW = Dw2<CA, CZ>::QW>
+__device__ inline void dw2_ops(Dw2Ops<Dw2<CA, CZ>::MBU, QW> &o, const float *dz, const float *h, const int *boff,
+                               int col, int kq) {
     using D = Dw2<CA, CZ>;
 #pragma unroll
     for (int m = 0; m < D::MBU; ++m) o.av[m] = *reinterpret_cast<const float4 *>(dz + (16 * m + col) * D::SZ + 4 * kq);
 #pragma unroll
-    for (int k = 0; k < D::QW; ++k)
+    for (int k = 0; k < QW; ++k)
         o.bv[k] = boff[k] >= 0 ? *reinterpret_cast<const float4 *>(h + boff[k])
                                : (boff[k] == -1 ? make_float4(1.f, 1.f, 1.f, 1.f) : make_float4(0.f, 0.f, 0.f, 0.f));
 }
@@ -568,8 +569,8 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
     fetch(t0);
 #pragma unroll
     for (int pp = 0; pp < D::P; ++pp) {
-        dw2_stage<CA, CZ, 0>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
-        dw2_stage<CA, CZ, 1>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+        dw2_stage<CA, CZ, 0>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp], threadIdx.x);
+        dw2_stage<CA, CZ, 1>(smem + pp * D::DZT, smem + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp], threadIdx.x);
     }
     fetch(t0 + D::P);
     dev::lds_barrier();
@@ -585,11 +586,11 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
             __builtin_amdgcn_sched_barrier(0);
             dw2_mma<D::MBU, D::QW, 0, 2>(acc, cur);
             __builtin_amdgcn_sched_barrier(0);
-            dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+            dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp], threadIdx.x);
             __builtin_amdgcn_sched_barrier(0);
             dw2_mma<D::MBU, D::QW, 2, 4>(acc, cur);
             __builtin_amdgcn_sched_barrier(0);
-            dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp]);
+            dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + D::P * D::DZT + pp * D::HT, rdz[pp], rh[pp], threadIdx.x);
             __builtin_amdgcn_sched_barrier(0);
             if (pp + 1 < D::P) cur = nxt;
         }
@@ -602,6 +603,129 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
     for (int m = 0; m < D::MBU; ++m)
 #pragma unroll
         for (int k = 0; k < D::QW; ++k) {
+            const int q = (qb0 + k) * 16 + col;
+            if (q >= D::NQ) continue;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = m * 16 + 4 * kq + r;
+                a.part[((size_t)co * D::NQ + q) * a.teams + team] = acc[m][k][r];
+            }
+        }
+}
+
+// The same weight gradients with a block of 8 waves per team, for layers
+// whose row blocks and a third as many column blocks as above fit 64
+// accumulators (40 -> 80: 5 x 3 blocks): two waves per SIMD.  Waves 0-3 stage
+// and fetch the first tile of each pass, waves 4-7 the second, each half
+// between the k-steps of its own tile, so that while one wave of a SIMD runs
+// its staging the other issues matrix ops.  Teams, tile ranges and the
+// k-step order of every column block are those of the 4-wave kernel: the
+// same partial sums bit for bit.
+template <int CA, int CZ>
+struct Dw8 {
+    using D = Dw2<CA, CZ>;
+    static constexpr int QW = (D::NBQ + 7) / 8;           // column blocks per wave
+    static constexpr bool FITS = D::MBU * QW * 4 <= 64 && D::P == 2;
+};
+
+template <int CA, int CZ>
+__global__ __launch_bounds__(512) void k_bwd_dw8(BwdArgs a) {
+    using D = Dw2<CA, CZ>;
+    constexpr int QW = Dw8<CA, CZ>::QW;
+    static_assert(Dw8<CA, CZ>::FITS, "8-wave layout");
+    extern __shared__ float smem[];                       // the buffers of the 4-wave kernel
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int half = wave >> 2, hix = threadIdx.x & 255;  // tile `half` of each pass is this half's to stage
+    const int team = blockIdx.x;
+    const int qb0 = wave * QW;
+    const int kq = lane >> 4, col = lane & 15;
+    int boff[QW];
+#pragma unroll
+    for (int k = 0; k < QW; ++k) {
+        const int q = (qb0 + k) * 16 + col;
+        if (q < 9 * CA) {
+            const int kpos = q / CA, ci = q - kpos * CA, ky = kpos / 3, kx = kpos - 3 * ky;
+            boff[k] = (kx * CA + ci) * D::HS + (kq + ky) * 4;
+        } else {
+            boff[k] = q == 9 * CA ? -1 : -2;
+        }
+    }
+    floatx4 acc[D::MBU][QW];
+#pragma unroll
+    for (int m = 0; m < D::MBU; ++m)
+#pragma unroll
+        for (int k = 0; k < QW; ++k) acc[m][k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const long long NT = (long long)a.n * a.ntiles;
+    const int t0 = (int)(NT * team / a.teams), t1 = (int)(NT * (team + 1) / a.teams);
+    // This half's tiles t0 + half, t0 + half + 2, ...: (fi, ft) the next one.
+    int fi = (t0 + half) / a.ntiles, ft = (t0 + half) - fi * a.ntiles;
+    float4 rdz[D::DZV], rh[D::HV];
+    const __attribute__((address_space(4))) int32_t *ids =
+        (const __attribute__((address_space(4))) int32_t *)a.ids;
+    auto fetch = [&](int c) __attribute__((always_inline)) {   // tile c, this half's share
+        const bool ok = c < t1;
+        const int i = __builtin_amdgcn_readfirstlane(ok ? fi : 0), tl = ok ? ft : 0;
+        ft += 2;
+        while (ft >= a.ntiles) {
+            ft -= a.ntiles;
+            ++fi;
+        }
+        const int slot = ids[i];
+        const float4 *dzp = reinterpret_cast<const float4 *>(a.dz_in + ((size_t)i * a.ntiles + tl) * kTilePx * CZ);
+#pragma unroll
+        for (int k = 0; k < D::DZV; ++k) {
+            const int e = hix + 256 * k;
+            rdz[k] = ok && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        const int ty = tl / a.TW, tx = tl - ty * a.TW;
+        const float *ap = a.act_prev + (size_t)slot * a.prev_stride;
+#pragma unroll
+        for (int k = 0; k < D::HV; ++k) {
+            const int e = hix + 256 * k;
+            const int pos = e / (CA / 4), c4 = e - pos * (CA / 4);
+            const int y = ty * kTile - 1 + pos / 6, x = tx * kTile - 1 + pos % 6;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (ok && e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
+                v = *reinterpret_cast<const float4 *>(
+                    ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
+            rh[k] = v;
+        }
+    };
+    fetch(t0 + half);
+    dw2_stage<CA, CZ, 0>(smem + half * D::DZT, smem + 2 * D::DZT + half * D::HT, rdz, rh, hix);
+    dw2_stage<CA, CZ, 1>(smem + half * D::DZT, smem + 2 * D::DZT + half * D::HT, rdz, rh, hix);
+    fetch(t0 + 2 + half);
+    dev::lds_barrier();
+    int b = 0;
+    for (int c = t0; c < t1; c += 2) {
+        float *cb = smem + b * D::BUF, *nb = smem + (b ^ 1) * D::BUF;
+        Dw2Ops<D::MBU, QW> cur;
+        dw2_ops<CA, CZ, QW>(cur, cb, cb + 2 * D::DZT, boff, col, kq);
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            Dw2Ops<D::MBU, QW> nxt;
+            if (pp == 0) dw2_ops<CA, CZ, QW>(nxt, cb + D::DZT, cb + 2 * D::DZT + D::HT, boff, col, kq);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_mma<D::MBU, QW, 0, 2>(acc, cur);
+            __builtin_amdgcn_sched_barrier(0);
+            if (half == pp) dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + 2 * D::DZT + pp * D::HT, rdz, rh, hix);
+            __builtin_amdgcn_sched_barrier(0);
+            dw2_mma<D::MBU, QW, 2, 4>(acc, cur);
+            __builtin_amdgcn_sched_barrier(0);
+            if (half == pp) {
+                dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + 2 * D::DZT + pp * D::HT, rdz, rh, hix);
+                fetch(c + 4 + half);                           // in flight during the next pass
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (pp == 0) cur = nxt;
+        }
+        dev::lds_barrier();                                // the other buffer staged, this one read
+        b ^= 1;
+    }
+#pragma unroll
+    for (int m = 0; m < D::MBU; ++m)
+#pragma unroll
+        for (int k = 0; k < QW; ++k) {
             const int q = (qb0 + k) * 16 + col;
             if (q >= D::NQ) continue;
 #pragma unroll
@@ -861,7 +985,7 @@ int dw_blocks_per_team(int ca, int cz, bool first) {
     RN_DW_FIRST_SHAPES(X)
 #undef X
 #define X(a_, z_) \
-    if (!first && ca == a_ && cz == z_) return Dw2<a_, z_>::BPT;
+    if (!first && ca == a_ && cz == z_) return Dw8<a_, z_>::FITS ? 1 : Dw2<a_, z_>::BPT;
     RN_DW_SHAPES(X)
 #undef X
     return 0;
@@ -880,10 +1004,17 @@ hipError_t run_dw_first(const BwdArgs &a, hipStream_t s) {
 template <int CA, int CZ>
 hipError_t run_dw2(const BwdArgs &a, hipStream_t s) {
     using D = Dw2<CA, CZ>;
-    auto kern = k_bwd_dw2<CA, CZ>;
-    static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
-    if (attr != hipSuccess) return attr;
-    hipLaunchKernelGGL(kern, dim3(D::BPT * a.teams), dim3(256), D::lds_bytes, s, a);
+    if constexpr (Dw8<CA, CZ>::FITS) {
+        auto kern = k_bwd_dw8<CA, CZ>;
+        static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
+        if (attr != hipSuccess) return attr;
+        hipLaunchKernelGGL(kern, dim3(a.teams), dim3(512), D::lds_bytes, s, a);
+    } else {
+        auto kern = k_bwd_dw2<CA, CZ>;
+        static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
+        if (attr != hipSuccess) return attr;
+        hipLaunchKernelGGL(kern, dim3(D::BPT * a.teams), dim3(256), D::lds_bytes, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int total = CZ * D::NQ;
