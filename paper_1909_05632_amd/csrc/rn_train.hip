@@ -615,17 +615,21 @@ __global__ __launch_bounds__(256) void k_bwd_dw2(BwdArgs a) {
 
 // The same weight gradients with a block of 8 waves per team, for layers
 // whose row blocks and a third as many column blocks as above fit 64
-// accumulators (40 -> 80: 5 x 3 blocks): two waves per SIMD.  Waves 0-3 stage
-// and fetch the first tile of each pass, waves 4-7 the second, each half
-// between the k-steps of its own tile, so that while one wave of a SIMD runs
-// its staging the other issues matrix ops.  Teams, tile ranges and the
-// k-step order of every column block are those of the 4-wave kernel: the
-// same partial sums bit for bit.
+// accumulators (40 -> 80: 5 x 3 blocks): two waves per SIMD.  A pass takes
+// four tiles (two buffers of four fit one CU's LDS: one barrier per four
+// tiles); waves 0-3 stage and fetch tiles 0 and 2 of each pass, waves 4-7
+// tiles 1 and 3, each half between the k-steps of its own tiles, so that
+// while one wave of a SIMD runs its staging the other issues matrix ops.
+// Teams, tile ranges and the k-step order of every column block are those of
+// the 4-wave kernel: the same partial sums bit for bit.
 template <int CA, int CZ>
 struct Dw8 {
     using D = Dw2<CA, CZ>;
     static constexpr int QW = (D::NBQ + 7) / 8;           // column blocks per wave
-    static constexpr bool FITS = D::MBU * QW * 4 <= 64 && D::P == 2;
+    static constexpr int P = 4;                            // tiles per pass: 0 and 2 of half 0, 1 and 3 of half 1
+    static constexpr int BUF = P * (D::DZT + D::HT);
+    static constexpr size_t lds_bytes = (size_t)2 * BUF * sizeof(float);
+    static constexpr bool FITS = D::MBU * QW * 4 <= 64 && lds_bytes <= 160 * 1024;
 };
 
 template <int CA, int CZ>
@@ -659,10 +663,10 @@ __global__ __launch_bounds__(512) void k_bwd_dw8(BwdArgs a) {
     const int t0 = (int)(NT * team / a.teams), t1 = (int)(NT * (team + 1) / a.teams);
     // This half's tiles t0 + half, t0 + half + 2, ...: (fi, ft) the next one.
     int fi = (t0 + half) / a.ntiles, ft = (t0 + half) - fi * a.ntiles;
-    float4 rdz[D::DZV], rh[D::HV];
+    float4 rdz[2][D::DZV], rh[2][D::HV];
     const __attribute__((address_space(4))) int32_t *ids =
         (const __attribute__((address_space(4))) int32_t *)a.ids;
-    auto fetch = [&](int c) __attribute__((always_inline)) {   // tile c, this half's share
+    auto fetch = [&](int c, int s) __attribute__((always_inline)) {   // tile c into register set s
         const bool ok = c < t1;
         const int i = __builtin_amdgcn_readfirstlane(ok ? fi : 0), tl = ok ? ft : 0;
         ft += 2;
@@ -675,7 +679,7 @@ __global__ __launch_bounds__(512) void k_bwd_dw8(BwdArgs a) {
 #pragma unroll
         for (int k = 0; k < D::DZV; ++k) {
             const int e = hix + 256 * k;
-            rdz[k] = ok && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+            rdz[s][k] = ok && e < 4 * CZ ? dzp[e] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
         const int ty = tl / a.TW, tx = tl - ty * a.TW;
         const float *ap = a.act_prev + (size_t)slot * a.prev_stride;
@@ -688,36 +692,41 @@ __global__ __launch_bounds__(512) void k_bwd_dw8(BwdArgs a) {
             if (ok && e < 9 * CA && y >= 0 && y < a.H && x >= 0 && x < a.W)
                 v = *reinterpret_cast<const float4 *>(
                     ap + ((size_t)((y >> 2) * a.TW + (x >> 2)) * kTilePx + (y & 3) * 4 + (x & 3)) * CA + 4 * c4);
-            rh[k] = v;
+            rh[s][k] = v;
         }
     };
-    fetch(t0 + half);
-    dw2_stage<CA, CZ, 0>(smem + half * D::DZT, smem + 2 * D::DZT + half * D::HT, rdz, rh, hix);
-    dw2_stage<CA, CZ, 1>(smem + half * D::DZT, smem + 2 * D::DZT + half * D::HT, rdz, rh, hix);
-    fetch(t0 + 2 + half);
+    constexpr int P = Dw8<CA, CZ>::P, BUF = Dw8<CA, CZ>::BUF;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        fetch(t0 + half + 2 * s, s);
+        dw2_stage<CA, CZ, 0>(smem + (half + 2 * s) * D::DZT, smem + P * D::DZT + (half + 2 * s) * D::HT, rdz[s], rh[s], hix);
+        dw2_stage<CA, CZ, 1>(smem + (half + 2 * s) * D::DZT, smem + P * D::DZT + (half + 2 * s) * D::HT, rdz[s], rh[s], hix);
+    }
+    fetch(t0 + P + half, 0);
+    fetch(t0 + P + half + 2, 1);
     dev::lds_barrier();
     int b = 0;
-    for (int c = t0; c < t1; c += 2) {
-        float *cb = smem + b * D::BUF, *nb = smem + (b ^ 1) * D::BUF;
+    for (int c = t0; c < t1; c += P) {
+        float *cb = smem + b * BUF, *nb = smem + (b ^ 1) * BUF;
         Dw2Ops<D::MBU, QW> cur;
-        dw2_ops<CA, CZ, QW>(cur, cb, cb + 2 * D::DZT, boff, col, kq);
+        dw2_ops<CA, CZ, QW>(cur, cb, cb + P * D::DZT, boff, col, kq);
 #pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
+        for (int pp = 0; pp < P; ++pp) {
             Dw2Ops<D::MBU, QW> nxt;
-            if (pp == 0) dw2_ops<CA, CZ, QW>(nxt, cb + D::DZT, cb + 2 * D::DZT + D::HT, boff, col, kq);
+            if (pp + 1 < P) dw2_ops<CA, CZ, QW>(nxt, cb + (pp + 1) * D::DZT, cb + P * D::DZT + (pp + 1) * D::HT, boff, col, kq);
             __builtin_amdgcn_sched_barrier(0);
             dw2_mma<D::MBU, QW, 0, 2>(acc, cur);
             __builtin_amdgcn_sched_barrier(0);
-            if (half == pp) dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + 2 * D::DZT + pp * D::HT, rdz, rh, hix);
+            if (half == (pp & 1)) dw2_stage<CA, CZ, 0>(nb + pp * D::DZT, nb + P * D::DZT + pp * D::HT, rdz[pp >> 1], rh[pp >> 1], hix);
             __builtin_amdgcn_sched_barrier(0);
             dw2_mma<D::MBU, QW, 2, 4>(acc, cur);
             __builtin_amdgcn_sched_barrier(0);
-            if (half == pp) {
-                dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + 2 * D::DZT + pp * D::HT, rdz, rh, hix);
-                fetch(c + 4 + half);                           // in flight during the next pass
+            if (half == (pp & 1)) {
+                dw2_stage<CA, CZ, 1>(nb + pp * D::DZT, nb + P * D::DZT + pp * D::HT, rdz[pp >> 1], rh[pp >> 1], hix);
+                fetch(c + 2 * P + pp, pp >> 1);                // in flight during the next pass
             }
             __builtin_amdgcn_sched_barrier(0);
-            if (pp == 0) cur = nxt;
+            if (pp + 1 < P) cur = nxt;
         }
         dev::lds_barrier();                                // the other buffer staged, this one read
         b ^= 1;
@@ -1006,9 +1015,10 @@ hipError_t run_dw2(const BwdArgs &a, hipStream_t s) {
     using D = Dw2<CA, CZ>;
     if constexpr (Dw8<CA, CZ>::FITS) {
         auto kern = k_bwd_dw8<CA, CZ>;
-        static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
+        constexpr size_t lds8 = Dw8<CA, CZ>::lds_bytes;
+        static hipError_t attr = dev::set_lds(kern, lds8);
         if (attr != hipSuccess) return attr;
-        hipLaunchKernelGGL(kern, dim3(a.teams), dim3(512), D::lds_bytes, s, a);
+        hipLaunchKernelGGL(kern, dim3(a.teams), dim3(512), lds8, s, a);
     } else {
         auto kern = k_bwd_dw2<CA, CZ>;
         static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
