@@ -309,7 +309,7 @@ def train_bench(args, torch):
         kern["bwd_dx"]["tflops"] = f_dx * T / (prof["bwd_dx"]["ms"] / 1e3) / 1e12
     dom = max(("bwd_dw", "bwd_dx"), key=lambda k: prof[k]["ms"])
     ach = kern[dom]["tflops"]
-    roof = {"bound": "mfma", "kernel": {"bwd_dw": "k_bwd_dw2 + k_bwd_dw_first (weight gradients, teams of tiles on MFMA)",
+    roof = {"bound": "mfma", "kernel": {"bwd_dw": "k_bwd_dw8 / k_bwd_dw2 + k_bwd_dw_first (weight gradients, teams of tiles on MFMA)",
                                         "bwd_dx": "k_bwd_dx (input gradients, transposed conv on MFMA)"}[dom],
             "achieved": ach, "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_MFMA_F32_TFLOPS,
             "traffic": None}

@@ -79,6 +79,9 @@ CASES = [
     ("atari-ds2-256x64", 40, 32, 3, None, "full", False),            # separate layer 1, full-read head
     ("stack4-512x64", 40, 32, 2, [1, 0], "full", True),              # 4 stacked frames -> 40 -> 80
     ("fullres-1024x32", 42, 32, 2, None, "tiles", True),             # 1->64->128->128, 18 logits
+    # 99 tiles a stream, 297 in all: weight-gradient teams of 8 and 9 tiles,
+    # passes that end past a team's last tile, tile walks across streams
+    ("atari-ds2-256x64", 44, 36, 3, [2, 0, 1], "tiles", True),
 ]
 
 
