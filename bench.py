@@ -246,8 +246,12 @@ def train_bench(args, torch):
     u8 = synth.sprite_batch(wl, **preset)
     frames = torch.from_numpy(synth.to_f32(u8)).cuda().unsqueeze(2).contiguous()
     weights = synth.net_weights(wl)
+    # Training keeps layer 1 in its own cache unless --fold-first: the backward
+    # needs layer 1's activations, which a folded net recomputes densely for
+    # every backward call (1.98 ms per 16-frame episode against 0.47 ms for
+    # layer 1's own kernel on the dirty tiles of the forward steps).
     net = ReuseNet(1, wl.h, wl.w, wl.convs, wl.n_out, S, weights, stack=wl.stack, head=args.head,
-                   fuse_first=not args.separate_first)
+                   fuse_first=args.fold_first)
     grads = net.new_grads()
     rng = np.random.default_rng([wl.cid, 7])
     actions = torch.from_numpy(rng.integers(0, wl.n_out, (T, S)).astype(np.int32)).cuda()
@@ -337,6 +341,7 @@ def train_bench(args, torch):
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": args.workload, "streams": S, "episode_frames": T, "h": wl.h, "w": wl.w,
                    "convs": list(wl.convs), "n_out": wl.n_out, "head": args.head, "lr": lr,
+                   "first_layer": "folded into layer 2 where it applies" if args.fold_first else "own kernel and cache",
                    "step": "one episode: T rollout steps, T replay steps with backward, one SGD step"},
         "dense_path": {"value": fps_dense, "unit": "frames/s", "ms_per_step": ms_dense},
         "speedup_vs_dense": fps / fps_dense,
@@ -367,7 +372,11 @@ def main():
                     help="with --update-every: replace the weights through the host repack and upload "
                          "(reuse_net_set_weights) even where the device path applies")
     ap.add_argument("--separate-first", action="store_true",
-                    help="run layer 1 as its own kernel instead of inside layer 2")
+                    help="run layer 1 as its own kernel instead of inside layer 2 (inference; "
+                         "training always does unless --fold-first)")
+    ap.add_argument("--fold-first", action="store_true",
+                    help="--train: compute layer 1 inside layer 2 (no layer-1 cache; the backward "
+                         "then recomputes layer 1)")
     ap.add_argument("--graph", action="store_true",
                     help="replay each reuse step from a HIP graph captured once per frame buffer "
                          "(one launch per step instead of one per kernel; the profiled pass stays eager)")
