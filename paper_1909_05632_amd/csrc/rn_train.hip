@@ -149,13 +149,14 @@ __device__ inline int hoff(int p, int c4) {
 
 // Input gradients dz_{l-1} = (W_l^T * dz_l) where a_{l-1} > 0, as a forward
 // convolution of dz_l (CZ channels) with the transposed, flipped weights
-// (pack_dx_weights) into CA channels.  A block works on a group of 4 tiles
-// of layer l-1 (one per wave, one wave per SIMD) and streams the weights
+// (pack_dx_weights) into CA channels.  A block works on a group of WV tiles
+// of layer l-1 (one per wave: 8 where two weight stages and eight halos fit
+// one CU's LDS, so two waves per SIMD, else 4) and streams the weights
 // through LDS in stages of one kernel position x SC channels of dz_l, two
 // buffers: stage q + 1 goes straight from global memory into the free buffer
 // at the start of stage q (lds_dma16, the block's loads split over its
 // waves), each wave waits for its own loads and a block barrier ends the
-// stage.  So each weight byte brought from L2 serves 4 tiles.  Each wave
+// stage.  So each weight byte brought from L2 serves WV tiles.  Each wave
 // keeps its tile's 6x6 x CZ halo of dz_l in its own LDS area (the next
 // group's fetched into registers three stages before the group ends, stored
 // after the epilogue: fetched in the last stage it arrived late, 14% of the
@@ -175,7 +176,9 @@ struct Dx {
     static constexpr int WST = WL * 256;        // floats per stage
     static constexpr int HALO = 36 * CZ;        // floats of one tile's halo
     static constexpr int HV = (9 * CZ + 63) / 64;   // 16-byte halo loads per lane
-    static constexpr size_t lds_bytes = (size_t)(2 * WST + 4 * HALO) * sizeof(float);
+    // waves (tiles of a group) per block: 8 where two weight stages and 8 halos fit one CU
+    static constexpr int WV = (2 * WST + 8 * HALO) * 4 <= 160 * 1024 ? 8 : 4;
+    static constexpr size_t lds_bytes = (size_t)(2 * WST + WV * HALO) * sizeof(float);
     static_assert(CZ % 16 == 0 && SC % 16 == 0, "whole 16-channel K blocks per stage");
     static_assert(CA % 4 == 0, "whole 16-byte channel groups in the epilogue");
     static_assert(HV <= 32, "halo mask width");
@@ -225,8 +228,8 @@ __device__ inline void dx_dma_stage(const float *wt, int q, float *dst, int wave
     const float *src = wt + (size_t)(kpos * D::KBP + ch * D::SB) * D::NB * 256;
     const uint32_t l0 = dev::lds_addr(dst);
 #pragma unroll
-    for (int j = 0; j < (D::WL + 3) / 4; ++j) {
-        const int wl = wave + 4 * j;
+    for (int j = 0; j < (D::WL + D::WV - 1) / D::WV; ++j) {
+        const int wl = wave + D::WV * j;
         if (wl < D::WL) dev::lds_dma16(src + wl * 256 + 4 * lane, l0 + 1024u * wl);   // uniform per wave
     }
 }
@@ -260,12 +263,12 @@ __device__ inline void dx_quad_transpose(float (&v)[4], int b) {
 }
 
 template <int CZ, int CA>
-__global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
+__global__ __launch_bounds__((64 * Dx<CZ, CA>::WV)) void k_bwd_dx(BwdArgs a) {
     using D = Dx<CZ, CA>;
     extern __shared__ float smem[];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int NT = a.n * a.ntiles, NG = (NT + 3) / 4;
+    const int NT = a.n * a.ntiles, NG = (NT + D::WV - 1) / D::WV;
     if ((int)blockIdx.x >= NG) return;                             // uniform per block
     float *wbuf = smem;                                            // two stages
     float *halo = smem + 2 * D::WST + wave * D::HALO;              // this wave's tile
@@ -276,13 +279,13 @@ __global__ __launch_bounds__(256) void k_bwd_dx(BwdArgs a) {
     dx_dma_stage<CZ, CA>(a.wt, 0, wbuf, wave, lane);
     float4 hreg[D::HV];
     uint32_t hok;
-    dx_fetch_halo<CZ, CA>(a, 4 * g + wave, 4 * g + wave < NT, hreg, hok, lane);
+    dx_fetch_halo<CZ, CA>(a, D::WV * g + wave, D::WV * g + wave < NT, hreg, hok, lane);
     dx_store_halo<CZ, CA>(halo, hreg, hok, lane);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     dev::lds_barrier();
     int buf = 0;
     for (; g < NG; g += gridDim.x) {                               // uniform per block
-        const int tid = 4 * g + wave, tidn = 4 * (g + (int)gridDim.x) + wave;
+        const int tid = D::WV * g + wave, tidn = D::WV * (g + (int)gridDim.x) + wave;
         floatx4 acc[D::NB];
 #pragma unroll
         for (int nb = 0; nb < D::NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1038,10 +1041,10 @@ hipError_t run_dx(const BwdArgs &a, int cus, hipStream_t s) {
     auto kern = k_bwd_dx<CZ, CA>;
     static hipError_t attr = dev::set_lds(kern, D::lds_bytes);
     if (attr != hipSuccess) return attr;
-    const long long groups = ((long long)a.n * a.ntiles + 3) / 4;
+    const long long groups = ((long long)a.n * a.ntiles + D::WV - 1) / D::WV;
     const int per_cu = D::lds_bytes <= 78 * 1024 ? 2 : 1;       // blocks that fit one CU's LDS
     const int grid = (int)std::min<long long>(groups, (long long)per_cu * cus);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), D::lds_bytes, s, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * D::WV), D::lds_bytes, s, a);
     return hipGetLastError();
 }
 
