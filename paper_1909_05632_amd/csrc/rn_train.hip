@@ -640,9 +640,9 @@ __global__ __launch_bounds__(512) void k_bwd_dw8(BwdArgs a) {
     using D = Dw2<CA, CZ>;
     constexpr int QW = Dw8<CA, CZ>::QW;
     static_assert(Dw8<CA, CZ>::FITS, "8-wave layout");
-    extern __shared__ float smem[];                       // the buffers of the 4-wave kernel
+    extern __shared__ float smem[];                       // two buffers of [P][CZ][SZ] dz, [P][3][CA][HS] halo
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int half = wave >> 2, hix = threadIdx.x & 255;  // tile `half` of each pass is this half's to stage
+    const int half = wave >> 2, hix = threadIdx.x & 255;  // tiles half, half + 2 of a pass are this half's to stage
     const int team = blockIdx.x;
     const int qb0 = wave * QW;
     const int kq = lane >> 4, col = lane & 15;
